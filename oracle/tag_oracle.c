@@ -218,20 +218,31 @@ static void aggregate_row(const tago_dims *d, int32_t beg, int32_t end,
     }
 }
 
-/* y[n][f] = W^h x[n][f], W^h = columns [0, f) of the f x 2f row-major W */
+/* y[n][f] = W^h x[n][f], W^h = columns [0, f) of the f x 2f row-major W.
+ * bf16 variant: both operands are rounded to bf16 first, the sum is rounded
+ * after (the operands are rounded once, before the loops, into copies). */
 static void apply_wh(int f, int32_t n, const float *W, const double *x, double *y, int bf16)
 {
-    for (int32_t v = 0; v < n; ++v)
+    double *wr = malloc(sizeof(double) * (size_t)f * f);
+    double *hr = malloc(sizeof(double) * (size_t)f);
+    if (!wr || !hr) { free(wr); free(hr); return; }
+    for (int c = 0; c < f; ++c)
+        for (int k = 0; k < f; ++k) {
+            double w = W[(size_t)c * 2 * f + k];
+            wr[(size_t)c * f + k] = bf16 ? tago_round_bf16(w) : w;
+        }
+    for (int32_t v = 0; v < n; ++v) {
+        for (int k = 0; k < f; ++k) {
+            double h = x[(size_t)v * f + k];
+            hr[k] = bf16 ? tago_round_bf16(h) : h;
+        }
         for (int c = 0; c < f; ++c) {
             double s = 0.0;
-            for (int k = 0; k < f; ++k) {
-                double w = W[(size_t)c * 2 * f + k];
-                double h = x[(size_t)v * f + k];
-                if (bf16) { w = tago_round_bf16(w); h = tago_round_bf16(h); }
-                s += w * h;
-            }
+            for (int k = 0; k < f; ++k) s += wr[(size_t)c * f + k] * hr[k];
             y[(size_t)v * f + c] = bf16 ? tago_round_bf16(s) : s;
         }
+    }
+    free(wr); free(hr);
 }
 
 /* te[n][f] = W^e enc[n][f] + b, W^e = columns [f, 2f) */

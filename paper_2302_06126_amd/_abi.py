@@ -1,0 +1,118 @@
+"""ctypes mirror of include/tag.h.
+
+Functions keep the C names; they take plain ints/pointers and the ctypes
+structures below.  Nothing here computes anything of the method: every step
+runs in libtag.so's HIP kernels.  Loading fails loudly when the library has
+not been built.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtag.so")
+
+TAG_OK, TAG_EINVAL, TAG_ERANGE, TAG_EDUP, TAG_ESHAPE, TAG_ENOSPACE, TAG_EHIP = 0, -1, -2, -3, -4, -5, -6
+TAG_F32, TAG_BF16 = 0, 1
+STATUS_NAMES = {0: "TAG_OK", -1: "TAG_EINVAL", -2: "TAG_ERANGE", -3: "TAG_EDUP", -4: "TAG_ESHAPE",
+                -5: "TAG_ENOSPACE", -6: "TAG_EHIP"}
+
+EXPORTS = ("tag_graph_plan", "tag_graph_build", "tag_graph_get_info", "tag_graph_export",
+           "tag_graph_destroy", "tag_gnn_workspace", "tag_gnn_forward", "tag_gnn_decide_workspace",
+           "tag_gnn_decide", "tag_last_error", "tag_version")
+
+_P32 = C.POINTER(C.c_int32)
+_P64 = C.POINTER(C.c_int64)
+_PF = C.c_void_p
+
+
+class tag_graph_desc(C.Structure):
+    _fields_ = [("n_graphs", C.c_int32), ("n_op", _P32), ("n_dev", _P32),
+                ("oo_off", _P64), ("dd_off", _P64), ("od_off", _P64),
+                ("oo_src", C.c_void_p), ("oo_dst", C.c_void_p),
+                ("dd_a", C.c_void_p), ("dd_b", C.c_void_p),
+                ("od_op", C.c_void_p), ("od_dev", C.c_void_p)]
+
+
+class tag_graph_info(C.Structure):
+    _fields_ = [("n_graphs", C.c_int32), ("max_dev", C.c_int32), ("n_op", C.c_int64), ("n_dev", C.c_int64),
+                ("e_oo", C.c_int64), ("e_dd", C.c_int64), ("e_od", C.c_int64),
+                ("rows", C.c_int64 * 4), ("nnz", C.c_int64 * 4), ("max_degree", C.c_int32 * 4)]
+
+
+class tag_model_dims(C.Structure):
+    _fields_ = [("f", C.c_int32), ("heads", C.c_int32), ("layers", C.c_int32), ("f_op", C.c_int32),
+                ("f_dev", C.c_int32), ("dec_hidden", C.c_int32), ("dtype", C.c_int32),
+                ("gamma_same", C.c_float), ("gamma_cross", C.c_float), ("leaky_slope", C.c_float)]
+
+
+class tag_weights(C.Structure):
+    _fields_ = [("enc_op_w", _PF), ("enc_op_b", _PF), ("enc_dev_w", _PF), ("enc_dev_b", _PF),
+                ("enc_edge_w", _PF * 3), ("enc_edge_b", _PF * 3),
+                ("layer_w", _PF), ("layer_b", _PF), ("att_src", _PF), ("att_dst", _PF),
+                ("dec_w1", _PF), ("dec_b1", _PF), ("dec_w2", _PF), ("dec_b2", _PF)]
+
+
+class tag_features(C.Structure):
+    _fields_ = [("n_replicas", C.c_int32), ("x_op", _PF), ("x_dev", _PF), ("x_oo", _PF), ("x_dd", _PF),
+                ("x_od", _PF), ("stride_oo", C.c_int64), ("stride_dd", C.c_int64), ("stride_od", C.c_int64)]
+
+
+class tag_slices(C.Structure):
+    _fields_ = [("n_slices", C.c_int32), ("mask", C.c_void_p), ("option", C.c_void_p)]
+
+
+class tag_decision(C.Structure):
+    _fields_ = [("mask", C.c_uint64), ("option", C.c_int32), ("replicas", C.c_int32),
+                ("sync", C.c_int32), ("sfb", C.c_int32)]
+
+
+_lib = None
+
+
+def load() -> C.CDLL:
+    """Load libtag.so (built in-tree by paper_2302_06126_amd/build.py)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2302_06126_amd.build` "
+                           "(the HIP library is required; there is no fallback)")
+    lib = C.CDLL(LIB_PATH)
+    S = C.c_int32
+    vp = C.c_void_p
+    szp = C.POINTER(C.c_size_t)
+    lib.tag_graph_plan.argtypes = [C.POINTER(tag_graph_desc), szp, szp]
+    lib.tag_graph_build.argtypes = [C.POINTER(tag_graph_desc), vp, C.c_size_t, vp, C.c_size_t, vp,
+                                    C.POINTER(vp)]
+    lib.tag_graph_get_info.argtypes = [vp, C.POINTER(tag_graph_info)]
+    lib.tag_graph_export.argtypes = [vp, S, vp, vp, vp]
+    lib.tag_graph_destroy.argtypes = [vp]
+    lib.tag_graph_destroy.restype = None
+    lib.tag_gnn_workspace.argtypes = [vp, C.POINTER(tag_model_dims), S, szp]
+    lib.tag_gnn_forward.argtypes = [vp, C.POINTER(tag_model_dims), C.POINTER(tag_weights),
+                                    C.POINTER(tag_features), vp, C.c_size_t, vp, vp, vp]
+    lib.tag_gnn_decide_workspace.argtypes = [vp, C.POINTER(tag_model_dims), S, S, S, szp]
+    lib.tag_gnn_decide.argtypes = [vp, C.POINTER(tag_model_dims), C.POINTER(tag_weights), S, vp, vp,
+                                   C.POINTER(tag_slices), S, vp, vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]
+    for name in ("tag_graph_plan", "tag_graph_build", "tag_graph_get_info", "tag_graph_export",
+                 "tag_gnn_workspace", "tag_gnn_forward", "tag_gnn_decide_workspace", "tag_gnn_decide"):
+        getattr(lib, name).restype = S
+    lib.tag_last_error.restype = C.c_char_p
+    lib.tag_last_error.argtypes = []
+    lib.tag_version.restype = C.c_char_p
+    lib.tag_version.argtypes = []
+    _lib = lib
+    return lib
+
+
+class TagError(RuntimeError):
+    def __init__(self, status: int, where: str, msg: str):
+        super().__init__(f"{where}: {STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+def check(status: int, where: str) -> None:
+    if status != TAG_OK:
+        raise TagError(status, where, load().tag_last_error().decode(errors="replace"))

@@ -1,0 +1,258 @@
+// Decision head (Section 4.2.1, the decoder after the GNN; Section 4.2, the
+// placement matrix P and the four replication options O).
+//
+// For query op i and slice a = (mask, option):
+//   x     = [ sum_{j in mask} E_dev[j] ; E_op[i] ; onehot(option) ]
+//   score = w2 . ReLU(W1 x + b1) + b2   (H > 0)  or  w2 . x + b2  (H = 0)
+// W1 x splits exactly into a per-slice part and a per-query part:
+//   W1 x = sum_{j in mask} (W1_dev E_dev[j]) + W1_opt[:, option] + W1_op E_op[i]
+// so the kernels compute t_j = W1_dev E_dev[j] once per device, the slice
+// part u_a once per (candidate, slice), v_i once per query, and then only
+// the ReLU readout per (query, slice).  The softmax over the slice table
+// gives the priors; the argmax (lowest index among equal maxima) is decoded
+// into placement, replica count, sync scheme and the compression (SFB) flag.
+#include <algorithm>
+
+#include "tag_internal.hpp"
+
+namespace tag {
+namespace {
+
+struct DecArgs {
+    int32_t R, G, S, Q, F, H, Hx;
+    int64_t n_op, n_dev;
+    const int32_t *op_off, *dev_off;   // [G+1]
+    const float *E_op, *E_dev;
+    const uint64_t *mask;
+    const uint8_t *option;
+    const float *P;      // projection rows [Hx][2F+4] (W1, or w2 for the linear head)
+    const float *b1, *w2, *b2;
+    const int32_t *q_rep, *q_graph, *q_op;
+    float *t;            // [R*n_dev][Hx]
+    float *u;            // [R*G][Hx][S]
+    float *v;            // [Q][Hx]
+    int32_t *argmax;
+    float *best, *prior;
+    tag_decision *dec;
+};
+
+// t[row][h] = sum_c P[h][c] E_dev[row][c]
+__global__ void dec_dev_proj(DecArgs A) {
+    const int64_t n = (int64_t)A.R * A.n_dev * A.Hx;
+    const int din = 2 * A.F + 4;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = i / A.Hx;
+        const int h = (int)(i % A.Hx);
+        const float *e = A.E_dev + row * A.F;
+        const float *p = A.P + (size_t)h * din;
+        float s = 0.f;
+        for (int c = 0; c < A.F; ++c) s = fmaf(p[c], e[c], s);
+        A.t[i] = s;
+    }
+}
+
+// u[rg][h][a] = sum_{j in mask_a} t[dev(rg, j)][h] + P[h][2F + opt_a] (+ b1[h])
+__global__ void dec_slice(DecArgs A) {
+    const int64_t n = (int64_t)A.R * A.G * A.Hx * A.S;
+    const int din = 2 * A.F + 4;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t a = (int32_t)(i % A.S);
+        const int32_t h = (int32_t)((i / A.S) % A.Hx);
+        const int64_t rg = i / ((int64_t)A.S * A.Hx);
+        const int32_t r = (int32_t)(rg / A.G), g = (int32_t)(rg % A.G);
+        const int32_t d0 = A.dev_off[g], nd = A.dev_off[g + 1] - d0;
+        const uint64_t m = A.mask[a];
+        const int opt = min((int)A.option[a], 3);
+        float s = A.P[(size_t)h * din + 2 * A.F + opt];
+        if (A.H > 0) s += A.b1[h];
+        const float *tt = A.t + ((int64_t)r * A.n_dev + d0) * A.Hx + h;
+        for (int32_t j = 0; j < nd; ++j)
+            if ((m >> j) & 1ull) s += tt[(int64_t)j * A.Hx];
+        A.u[i] = s;
+    }
+}
+
+__device__ __forceinline__ bool query_valid(const DecArgs &A, int32_t q, int32_t *r, int32_t *g, int32_t *op) {
+    *r = A.q_rep[q]; *g = A.q_graph[q]; *op = A.q_op[q];
+    if (*r < 0 || *r >= A.R || *g < 0 || *g >= A.G) return false;
+    return *op >= 0 && *op < A.op_off[*g + 1] - A.op_off[*g];
+}
+
+// v[q][h] = sum_c P[h][F + c] E_op[row(q)][c]
+__global__ void dec_query_proj(DecArgs A) {
+    const int64_t n = (int64_t)A.Q * A.Hx;
+    const int din = 2 * A.F + 4;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t q = (int32_t)(i / A.Hx);
+        const int h = (int)(i % A.Hx);
+        int32_t r, g, op;
+        float s = 0.f;
+        if (query_valid(A, q, &r, &g, &op)) {
+            const float *e = A.E_op + ((int64_t)r * A.n_op + A.op_off[g] + op) * A.F;
+            const float *p = A.P + (size_t)h * din + A.F;
+            for (int c = 0; c < A.F; ++c) s = fmaf(p[c], e[c], s);
+        }
+        A.v[i] = s;
+    }
+}
+
+constexpr int kScoreThreads = 256;
+
+__device__ __forceinline__ float slice_score(const DecArgs &A, const float *urg, const float *vq,
+                                             const float *w2s, int32_t a) {
+    if (A.H == 0) return A.b2[0] + urg[a] + vq[0];
+    float s = 0.f;
+    for (int h = 0; h < A.H; ++h) s = fmaf(w2s[h], fmaxf(urg[(int64_t)h * A.S + a] + vq[h], 0.f), s);
+    return A.b2[0] + s;
+}
+
+// one block per query: scores, softmax prior, argmax, decoded decision
+__global__ void __launch_bounds__(kScoreThreads) dec_score(DecArgs A) {
+    extern __shared__ float sh[];   // v[Hx] | w2[H]
+    __shared__ float red_m[kScoreThreads];
+    __shared__ int32_t red_i[kScoreThreads];
+    __shared__ float red_z[kScoreThreads];
+    const int32_t q = blockIdx.x;
+    int32_t r, g, op;
+    const bool ok = query_valid(A, q, &r, &g, &op);
+    if (!ok) {
+        if (threadIdx.x == 0) {
+            A.argmax[q] = -1;
+            A.best[q] = __builtin_nanf("");
+            if (A.dec) A.dec[q] = tag_decision{0, 0, 0, 0, 0};
+        }
+        if (A.prior)
+            for (int32_t a = threadIdx.x; a < A.S; a += blockDim.x) A.prior[(int64_t)q * A.S + a] = 0.f;
+        return;
+    }
+    float *vq = sh, *w2s = sh + A.Hx;
+    for (int h = threadIdx.x; h < A.Hx; h += blockDim.x) vq[h] = A.v[(int64_t)q * A.Hx + h];
+    for (int h = threadIdx.x; h < A.H; h += blockDim.x) w2s[h] = A.w2[h];
+    __syncthreads();
+    const float *urg = A.u + ((int64_t)r * A.G + g) * A.Hx * A.S;
+    // pass 1: max (lowest index on ties) and the running sum of exponentials
+    float m = -INFINITY, z = 0.f;
+    int32_t im = INT32_MAX;
+    for (int32_t a = threadIdx.x; a < A.S; a += blockDim.x) {
+        float s = slice_score(A, urg, vq, w2s, a);
+        if (A.prior) A.prior[(int64_t)q * A.S + a] = s;
+        if (s > m) { z = z * __expf(m - s) + 1.f; m = s; im = a; }
+        else z += __expf(s - m);
+    }
+    red_m[threadIdx.x] = m; red_i[threadIdx.x] = im; red_z[threadIdx.x] = z;
+    __syncthreads();
+    for (int off = kScoreThreads / 2; off > 0; off >>= 1) {
+        if (threadIdx.x < off) {
+            float m1 = red_m[threadIdx.x], m2 = red_m[threadIdx.x + off];
+            int32_t i1 = red_i[threadIdx.x], i2 = red_i[threadIdx.x + off];
+            float z1 = red_z[threadIdx.x], z2 = red_z[threadIdx.x + off];
+            float M = fmaxf(m1, m2);
+            float zz = (m1 == -INFINITY ? 0.f : z1 * __expf(m1 - M)) + (m2 == -INFINITY ? 0.f : z2 * __expf(m2 - M));
+            int32_t ii = (m2 > m1 || (m2 == m1 && i2 < i1)) ? i2 : i1;
+            red_m[threadIdx.x] = M; red_i[threadIdx.x] = ii; red_z[threadIdx.x] = zz;
+        }
+        __syncthreads();
+    }
+    const float M = red_m[0], Z = red_z[0];
+    const int32_t best = red_i[0];
+    if (A.prior) {
+        const float inv = 1.f / Z;
+        for (int32_t a = threadIdx.x; a < A.S; a += blockDim.x) {
+            float s = A.prior[(int64_t)q * A.S + a];
+            A.prior[(int64_t)q * A.S + a] = __expf(s - M) * inv;
+        }
+    }
+    if (threadIdx.x == 0) {
+        if (best < 0 || best >= A.S) {   // no comparable score (NaN inputs)
+            A.argmax[q] = -1;
+            A.best[q] = __builtin_nanf("");
+            if (A.dec) A.dec[q] = tag_decision{0, 0, 0, 0, 0};
+            return;
+        }
+        A.argmax[q] = best;
+        A.best[q] = M;
+        if (A.dec) {
+            const int32_t nd = A.dev_off[g + 1] - A.dev_off[g];
+            const uint64_t valid = nd >= 64 ? ~0ull : ((1ull << nd) - 1ull);
+            const uint64_t msk = A.mask[best] & valid;
+            const int o = min((int)A.option[best], 3);
+            const int pc = __popcll(msk);
+            A.dec[q] = tag_decision{msk, o, o == 3 ? 1 : pc, o == 0 ? 0 : (o == 1 ? 1 : 2), o == 2 ? 1 : 0};
+        }
+    }
+}
+
+struct DecLayout {
+    float *t, *u, *v;
+};
+
+size_t carve_dec(const tag_graph *g, int32_t Hx, int32_t R, int32_t S, int32_t Q, void *base, DecLayout *L) {
+    Carver c(base);
+    L->t = c.take<float>((size_t)R * g->n_dev * Hx);
+    L->u = c.take<float>((size_t)R * g->G * Hx * S);
+    L->v = c.take<float>((size_t)std::max(Q, 1) * Hx);
+    return c.used;
+}
+
+inline unsigned grid_for(int64_t n) {
+    return (unsigned)std::max<int64_t>(1, std::min<int64_t>((n + 255) / 256, 1 << 20));
+}
+
+}  // namespace
+}  // namespace tag
+
+using namespace tag;
+
+extern "C" tag_status tag_gnn_decide_workspace(const tag_graph *g, const tag_model_dims *dims, int32_t n_replicas,
+                                               int32_t n_slices, int32_t n_query, size_t *bytes) {
+    clear_error();
+    if (!g || !dims || !bytes) TAG_FAIL(TAG_EINVAL, "graph, dims and bytes must be non-NULL");
+    if (n_replicas < 1 || n_slices < 1 || n_query < 0) TAG_FAIL(TAG_EINVAL, "need n_replicas >= 1, n_slices >= 1, n_query >= 0");
+    if (dims->dec_hidden < 0 || dims->dec_hidden > 1024) TAG_FAIL(TAG_ESHAPE, "dec_hidden must be in [0, 1024]");
+    DecLayout L;
+    *bytes = carve_dec(g, std::max(dims->dec_hidden, 1), n_replicas, n_slices, n_query, nullptr, &L);
+    return TAG_OK;
+}
+
+extern "C" tag_status tag_gnn_decide(const tag_graph *g, const tag_model_dims *dims, const tag_weights *w,
+                                     int32_t n_replicas, const float *E_op, const float *E_dev,
+                                     const tag_slices *slices, int32_t n_query, const int32_t *query_rep,
+                                     const int32_t *query_graph, const int32_t *query_op, int32_t *argmax,
+                                     float *best_score, float *prior, tag_decision *decision, void *workspace,
+                                     size_t ws_bytes, void *hip_stream) {
+    clear_error();
+    if (!g || !dims || !w || !E_op || !E_dev || !slices) TAG_FAIL(TAG_EINVAL, "NULL argument");
+    if (dims->f != 64 && dims->f != 128 && dims->f != 256) TAG_FAIL(TAG_ESHAPE, "f must be 64, 128 or 256");
+    if (dims->dec_hidden < 0 || dims->dec_hidden > 1024) TAG_FAIL(TAG_ESHAPE, "dec_hidden must be in [0, 1024]");
+    if (n_replicas < 1) TAG_FAIL(TAG_EINVAL, "n_replicas must be >= 1");
+    if (slices->n_slices < 1 || !slices->mask || !slices->option) TAG_FAIL(TAG_EINVAL, "empty or NULL slice table");
+    if (n_query < 0) TAG_FAIL(TAG_EINVAL, "n_query must be >= 0");
+    if (n_query == 0) return TAG_OK;
+    if (!query_rep || !query_graph || !query_op || !argmax || !best_score)
+        TAG_FAIL(TAG_EINVAL, "query arrays, argmax and best_score must be non-NULL");
+    if (!w->dec_w2 || !w->dec_b2 || (dims->dec_hidden > 0 && (!w->dec_w1 || !w->dec_b1)))
+        TAG_FAIL(TAG_EINVAL, "decoder weights must be non-NULL");
+    if (!workspace) TAG_FAIL(TAG_EINVAL, "workspace must be non-NULL");
+    const int32_t H = dims->dec_hidden, Hx = std::max(H, 1);
+    DecLayout L;
+    if (carve_dec(g, Hx, n_replicas, slices->n_slices, n_query, nullptr, &L) > ws_bytes)
+        TAG_FAIL(TAG_ENOSPACE, "decide workspace too small (see tag_gnn_decide_workspace)");
+    carve_dec(g, Hx, n_replicas, slices->n_slices, n_query, workspace, &L);
+    hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+    DecArgs A{};
+    A.R = n_replicas; A.G = g->G; A.S = slices->n_slices; A.Q = n_query; A.F = dims->f; A.H = H; A.Hx = Hx;
+    A.n_op = g->n_op; A.n_dev = g->n_dev;
+    A.op_off = g->op_off_d; A.dev_off = g->dev_off_d;
+    A.E_op = E_op; A.E_dev = E_dev;
+    A.mask = slices->mask; A.option = slices->option;
+    A.P = H > 0 ? w->dec_w1 : w->dec_w2;
+    A.b1 = w->dec_b1; A.w2 = w->dec_w2; A.b2 = w->dec_b2;
+    A.q_rep = query_rep; A.q_graph = query_graph; A.q_op = query_op;
+    A.t = L.t; A.u = L.u; A.v = L.v;
+    A.argmax = argmax; A.best = best_score; A.prior = prior; A.dec = decision;
+    dec_dev_proj<<<grid_for((int64_t)A.R * A.n_dev * Hx), 256, 0, stream>>>(A);
+    dec_slice<<<grid_for((int64_t)A.R * A.G * Hx * A.S), 256, 0, stream>>>(A);
+    dec_query_proj<<<grid_for((int64_t)A.Q * Hx), 256, 0, stream>>>(A);
+    dec_score<<<(unsigned)A.Q, kScoreThreads, sizeof(float) * (Hx + H), stream>>>(A);
+    return launch_status("tag_gnn_decide");
+}

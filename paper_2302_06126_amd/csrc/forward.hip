@@ -1,0 +1,654 @@
+// Forward pass of the heterogeneous GNN (Section 4.2.1 of the paper).
+//
+// Layer l, link type r, destination u, neighbour v (edge feature e_uv):
+//   m_uv  = ReLU(W^h h_v + W^e e_uv + b)                W = [W^h | W^e]
+//   s_uvk = LeakyReLU(a^(k) . m_uv^(k) + adst^(k) . (W^h h_u)^(k))
+//   h'_u  = sum_r gamma_r sum_v softmax_v(s_uvk) m_uv^(k)   (heads concatenated)
+//
+// GPU formulation (exact algebra, only rounding differs from the plain
+// definition):
+//  * Edge encoders are affine and have no activation, so W^e e + b is folded
+//    once per call into U_{l,r} = W^e A_r (f x d_r) and c'_{l,r} = W^e c_r + b;
+//    the per-entry edge term is U x + c' (d_r <= 2 multiply-adds per channel).
+//  * W^h h is computed once per node (not per entry) by an MFMA GEMM per
+//    side: op rows get [W^h_oo ; W^h_od], device rows [W^h_dd ; W^h_od],
+//    written as Y [rows][2f] (first half: same-type relation, second: od).
+//  * Aggregation runs one wavefront per destination row (per candidate),
+//    lanes own f/64 consecutive channels, head scores are reduced over the
+//    64/K lanes of a head, and the softmax is an online (running-max)
+//    softmax in the exp2 domain.  Long device<-op rows are split into
+//    chunks whose (max, denominator, accumulator) partials are merged in a
+//    fixed order, so results do not depend on scheduling.
+#include <algorithm>
+
+#include "tag_internal.hpp"
+
+namespace tag {
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kWaves = 4;        // wavefronts per aggregation block
+constexpr int kChunk = 256;      // entries per device<-op partial
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+
+// ------------------------------------------------------------------ folding
+// U[l][r][c][t] = sum_k W^e[c][k] A_r[k][t];  cp[l][r][c] = b[c] + sum_k W^e[c][k] c_r[k]
+struct FoldArgs {
+    const float *layer_w, *layer_b;
+    const float *A[3], *c[3];
+    float *U, *cp;
+    int F;
+};
+
+__global__ void fold_edge_terms(FoldArgs a) {
+    const int lr = blockIdx.x;          // l*3 + r
+    const int r = lr % 3;
+    const int F = a.F;
+    const int d = (r == 2) ? 2 : 1;
+    const float *W = a.layer_w + (size_t)lr * F * 2 * F;
+    for (int c = threadIdx.x; c < F; c += blockDim.x) {
+        float u0 = 0.f, u1 = 0.f, s = a.layer_b[(size_t)lr * F + c];
+        for (int k = 0; k < F; ++k) {
+            float we = W[(size_t)c * 2 * F + F + k];
+            u0 = fmaf(we, a.A[r][(size_t)k * d + 0], u0);
+            if (d == 2) u1 = fmaf(we, a.A[r][(size_t)k * d + 1], u1);
+            s = fmaf(we, a.c[r][k], s);
+        }
+        a.U[((size_t)lr * F + c) * 2 + 0] = u0;
+        a.U[((size_t)lr * F + c) * 2 + 1] = u1;
+        a.cp[(size_t)lr * F + c] = s;
+    }
+}
+
+// W^h of every (layer, relation) to bf16: Wb[l][r][n][k] = bf16(W[l][r][n][k]), k < F
+__global__ void convert_wh_bf16(const float *layer_w, uint16_t *Wb, int F, int LR) {
+    int64_t total = (int64_t)LR * F * F;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        int64_t lr = i / ((int64_t)F * F);
+        int64_t rem = i % ((int64_t)F * F);
+        int64_t n = rem / F, k = rem % F;
+        Wb[i] = f2bf(layer_w[(lr * F + n) * 2 * F + k]);
+    }
+}
+
+// ----------------------------------------------------------------- encoders
+// out[row][c] = ReLU(b[c] + sum_t W[c][t] x[row][t]); W^T staged in LDS.
+template <bool OUT_BF16>
+__global__ void encode_rows(const float *__restrict__ x, int64_t rows, int fin,
+                            const float *__restrict__ W, const float *__restrict__ b,
+                            void *out, int F) {
+    extern __shared__ float wt[];   // [fin][F]
+    for (int i = threadIdx.x; i < fin * F; i += blockDim.x) {
+        int t = i / F, c = i % F;
+        wt[i] = W[(size_t)c * fin + t];
+    }
+    __syncthreads();
+    const int c = threadIdx.x % F;
+    const int rstep = blockDim.x / F;
+    const float bc = b[c];
+    const int64_t r0 = (int64_t)blockIdx.x * 256;
+    for (int64_t r = r0 + threadIdx.x / F; r < std::min<int64_t>(r0 + 256, rows); r += rstep) {
+        const float *xr = x + r * fin;
+        float s = bc;
+        for (int t = 0; t < fin; ++t) s = fmaf(wt[t * F + c], xr[t], s);
+        s = fmaxf(s, 0.f);
+        if (OUT_BF16) static_cast<uint16_t *>(out)[r * F + c] = f2bf(s);
+        else static_cast<float *>(out)[r * F + c] = s;
+    }
+}
+
+// --------------------------------------------------------- relation GEMM
+// Y[m][n] = sum_k H[m][k] * B[n][k], n < F from B0 (row stride ldb), n >= F
+// from B1.  64 x 64 block tile, 4 wavefronts each 32 x 32 (2 x 2 MFMA
+// 16x16 tiles).  MFMA 16x16 operand layout: lane l supplies row/column
+// l % 16 and k-slice l / 16; result register v of lane l is row
+// 4 (l / 16) + v, column l % 16.
+constexpr int TM = 64, TN = 64;
+
+__global__ void __launch_bounds__(256) gemm_f32(const float *__restrict__ H, int64_t rows, int F,
+                                                const float *__restrict__ B0, const float *__restrict__ B1,
+                                                int ldb, float *__restrict__ Y) {
+    constexpr int BK = 16;
+    __shared__ float As[TM][BK + 1];
+    __shared__ float Bs[TN][BK + 1];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int64_t m0 = (int64_t)blockIdx.x * TM;
+    const int n0 = blockIdx.y * TN;
+    f4 acc[2][2];
+    for (int i = 0; i < 2; ++i)
+        for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+    const int lrow = tid >> 2, lk = (tid & 3) * 4;
+    for (int k0 = 0; k0 < F; k0 += BK) {
+        {
+            int64_t gm = m0 + lrow;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (gm < rows) v = *reinterpret_cast<const float4 *>(H + gm * F + k0 + lk);
+            As[lrow][lk + 0] = v.x; As[lrow][lk + 1] = v.y; As[lrow][lk + 2] = v.z; As[lrow][lk + 3] = v.w;
+            int gn = n0 + lrow;
+            const float *src = gn < F ? B0 + (size_t)gn * ldb : B1 + (size_t)(gn - F) * ldb;
+            float4 w = *reinterpret_cast<const float4 *>(src + k0 + lk);
+            Bs[lrow][lk + 0] = w.x; Bs[lrow][lk + 1] = w.y; Bs[lrow][lk + 2] = w.z; Bs[lrow][lk + 3] = w.w;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 4) {
+            float a[2], bv[2];
+            for (int i = 0; i < 2; ++i) a[i] = As[wm * 32 + i * 16 + (lane & 15)][kk + (lane >> 4)];
+            for (int j = 0; j < 2; ++j) bv[j] = Bs[wn * 32 + j * 16 + (lane & 15)][kk + (lane >> 4)];
+            for (int i = 0; i < 2; ++i)
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], bv[j], acc[i][j], 0, 0, 0);
+        }
+        __syncthreads();
+    }
+    const int ldy = 2 * F;
+    for (int i = 0; i < 2; ++i)
+        for (int j = 0; j < 2; ++j)
+            for (int v = 0; v < 4; ++v) {
+                int64_t gm = m0 + wm * 32 + i * 16 + 4 * (lane >> 4) + v;
+                int gn = n0 + wn * 32 + j * 16 + (lane & 15);
+                if (gm < rows) Y[gm * ldy + gn] = acc[i][j][v];
+            }
+}
+
+__global__ void __launch_bounds__(256) gemm_bf16(const uint16_t *__restrict__ H, int64_t rows, int F,
+                                                 const uint16_t *__restrict__ B0, const uint16_t *__restrict__ B1,
+                                                 int ldb, uint16_t *__restrict__ Y) {
+    constexpr int BK = 32, PADK = BK + 8;
+    __shared__ __attribute__((aligned(16))) uint16_t As[TM][PADK];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[TN][PADK];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int64_t m0 = (int64_t)blockIdx.x * TM;
+    const int n0 = blockIdx.y * TN;
+    f4 acc[2][2];
+    for (int i = 0; i < 2; ++i)
+        for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+    const int lrow = tid >> 2, lk = (tid & 3) * 8;
+    for (int k0 = 0; k0 < F; k0 += BK) {
+        {
+            int64_t gm = m0 + lrow;
+            uint4 v = make_uint4(0, 0, 0, 0);
+            if (gm < rows) v = *reinterpret_cast<const uint4 *>(H + gm * F + k0 + lk);
+            *reinterpret_cast<uint4 *>(&As[lrow][lk]) = v;
+            int gn = n0 + lrow;
+            const uint16_t *src = gn < F ? B0 + (size_t)gn * ldb : B1 + (size_t)(gn - F) * ldb;
+            *reinterpret_cast<uint4 *>(&Bs[lrow][lk]) = *reinterpret_cast<const uint4 *>(src + k0 + lk);
+        }
+        __syncthreads();
+        bf8 a[2], bv[2];
+        for (int i = 0; i < 2; ++i)
+            a[i] = *reinterpret_cast<const bf8 *>(&As[wm * 32 + i * 16 + (lane & 15)][8 * (lane >> 4)]);
+        for (int j = 0; j < 2; ++j)
+            bv[j] = *reinterpret_cast<const bf8 *>(&Bs[wn * 32 + j * 16 + (lane & 15)][8 * (lane >> 4)]);
+        for (int i = 0; i < 2; ++i)
+            for (int j = 0; j < 2; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bv[j], acc[i][j], 0, 0, 0);
+        __syncthreads();
+    }
+    const int ldy = 2 * F;
+    for (int i = 0; i < 2; ++i)
+        for (int j = 0; j < 2; ++j)
+            for (int v = 0; v < 4; ++v) {
+                int64_t gm = m0 + wm * 32 + i * 16 + 4 * (lane >> 4) + v;
+                int gn = n0 + wn * 32 + j * 16 + (lane & 15);
+                if (gm < rows) Y[gm * ldy + gn] = f2bf(acc[i][j][v]);
+            }
+}
+
+// -------------------------------------------------------------- aggregation
+struct AggArgs {
+    int32_t R;
+    int64_t n_op, n_dev;
+    const int32_t *rp[4], *col[4], *eid[4];
+    const void *Y_op, *Y_dev;         // [R*n][2F]
+    const float *x_oo; int64_t s_oo;
+    const float *x_dd; int64_t s_dd;
+    const uint8_t *x_od; int64_t s_od;
+    const float *att_src, *att_dst;   // [3][F] of this layer
+    const float *U;                   // [3][F][2] of this layer
+    const float *cp;                  // [3][F] of this layer
+    float g_same, g_cross, slope;
+    void *H_op, *H_dev;               // outputs (bf16 hidden or fp32)
+    int out_f32;
+    float *part;                      // device<-op partials
+    int32_t maxc;                     // chunks per device row
+};
+
+template <int CPL, bool BF>
+__device__ __forceinline__ void load_ch(const void *base, int64_t off, float (&v)[CPL]) {
+    if (BF) {
+        const uint16_t *p = static_cast<const uint16_t *>(base) + off;
+        if (CPL == 4) {
+            uint2 q = *reinterpret_cast<const uint2 *>(p);
+            v[0] = bf2f(q.x & 0xffff); v[1] = bf2f(q.x >> 16);
+            v[2 % CPL] = bf2f(q.y & 0xffff); v[3 % CPL] = bf2f(q.y >> 16);
+        } else if (CPL == 2) {
+            uint32_t q = *reinterpret_cast<const uint32_t *>(p);
+            v[0] = bf2f(q & 0xffff); v[1 % CPL] = bf2f(q >> 16);
+        } else {
+            v[0] = bf2f(p[0]);
+        }
+    } else {
+        const float *p = static_cast<const float *>(base) + off;
+        if (CPL == 4) {
+            float4 q = *reinterpret_cast<const float4 *>(p);
+            v[0] = q.x; v[1] = q.y; v[2 % CPL] = q.z; v[3 % CPL] = q.w;
+        } else if (CPL == 2) {
+            float2 q = *reinterpret_cast<const float2 *>(p);
+            v[0] = q.x; v[1 % CPL] = q.y;
+        } else {
+            v[0] = p[0];
+        }
+    }
+}
+
+template <int LPH>
+__device__ __forceinline__ float head_sum(float v) {
+#pragma unroll
+    for (int o = LPH / 2; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// per-lane constants of one relation
+template <int CPL>
+struct RelConst {
+    float a[CPL], ad[CPL], u0[CPL], u1[CPL], cp[CPL];
+    __device__ void load(const AggArgs &A, int r, int F, int c0) {
+        for (int c = 0; c < CPL; ++c) {
+            a[c] = A.att_src[r * F + c0 + c];
+            ad[c] = A.att_dst[r * F + c0 + c];
+            u0[c] = A.U[((size_t)r * F + c0 + c) * 2 + 0];
+            u1[c] = A.U[((size_t)r * F + c0 + c) * 2 + 1];
+            cp[c] = A.cp[(size_t)r * F + c0 + c];
+        }
+    }
+};
+
+template <int CPL>
+struct Online {
+    float mx, den, acc[CPL];
+    __device__ void init() {
+        mx = -INFINITY; den = 0.f;
+        for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
+    }
+    // s2: score already multiplied by log2(e)
+    __device__ void push(float s2, const float (&m)[CPL]) {
+        float nm = fmaxf(mx, s2);
+        float sc = __builtin_amdgcn_exp2f(mx - nm);
+        float p = __builtin_amdgcn_exp2f(s2 - nm);
+        den = fmaf(den, sc, p);
+        for (int c = 0; c < CPL; ++c) acc[c] = fmaf(acc[c], sc, p * m[c]);
+        mx = nm;
+    }
+};
+
+// message + score of one entry; returns the log2-domain score
+template <int CPL, int LPH>
+__device__ __forceinline__ float entry_score(const float (&y)[CPL], float x0, float x1, const RelConst<CPL> &k,
+                                             float qd, float slope, float (&m)[CPL]) {
+    float part = 0.f;
+    for (int c = 0; c < CPL; ++c) {
+        float z = y[c] + fmaf(k.u0[c], x0, fmaf(k.u1[c], x1, k.cp[c]));
+        m[c] = fmaxf(z, 0.f);
+        part = fmaf(k.a[c], m[c], part);
+    }
+    float s = head_sum<LPH>(part) + qd;
+    return leaky(s, slope) * kLog2e;
+}
+
+template <int CPL, bool BF>
+__device__ __forceinline__ void store_row(void *base, int64_t off, bool f32, const float (&v)[CPL]) {
+    if (f32) {
+        float *p = static_cast<float *>(base) + off;
+        for (int c = 0; c < CPL; ++c) p[c] = v[c];
+    } else {
+        uint16_t *p = static_cast<uint16_t *>(base) + off;
+        for (int c = 0; c < CPL; ++c) p[c] = f2bf(v[c]);
+    }
+}
+
+// op destinations: B0 (op<-op) and B1 (op<-dev)
+template <int F, int K, bool BF>
+__global__ void __launch_bounds__(256) agg_op(AggArgs A) {
+    constexpr int CPL = F / 64, LPH = 64 / K;
+    const int lane = threadIdx.x & 63;
+    const int64_t w = (int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6);
+    if (w >= (int64_t)A.R * A.n_op) return;
+    const int32_t rep = (int32_t)(w / A.n_op);
+    const int32_t u = (int32_t)(w % A.n_op);
+    const int c0 = lane * CPL;
+    const int64_t yrow_u = ((int64_t)rep * A.n_op + u) * 2 * F;
+    float out[CPL];
+    for (int c = 0; c < CPL; ++c) out[c] = 0.f;
+    {   // B0: op <- op, relation oo
+        RelConst<CPL> k; k.load(A, 0, F, c0);
+        float yd[CPL]; load_ch<CPL, BF>(A.Y_op, yrow_u + c0, yd);
+        float q = 0.f;
+        for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], yd[c], q);
+        q = head_sum<LPH>(q);
+        Online<CPL> o; o.init();
+        const int32_t beg = A.rp[0][u], end = A.rp[0][u + 1];
+        const float *xo = A.x_oo + (int64_t)rep * A.s_oo;
+        for (int32_t e = beg; e < end; ++e) {
+            const int32_t v = A.col[0][e];
+            const float x0 = xo[A.eid[0][e]];
+            float y[CPL]; load_ch<CPL, BF>(A.Y_op, ((int64_t)rep * A.n_op + v) * 2 * F + c0, y);
+            float m[CPL];
+            float s2 = entry_score<CPL, LPH>(y, x0, 0.f, k, q, A.slope, m);
+            o.push(s2, m);
+        }
+        if (end > beg) {
+            float inv = A.g_same / o.den;
+            for (int c = 0; c < CPL; ++c) out[c] = o.acc[c] * inv;
+        }
+    }
+    {   // B1: op <- device, relation od
+        RelConst<CPL> k; k.load(A, 1, F, c0);
+        float yd[CPL]; load_ch<CPL, BF>(A.Y_op, yrow_u + F + c0, yd);
+        float q = 0.f;
+        for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], yd[c], q);
+        q = head_sum<LPH>(q);
+        Online<CPL> o; o.init();
+        const int32_t beg = A.rp[1][u], end = A.rp[1][u + 1];
+        const uint8_t *xb = A.x_od + (int64_t)rep * A.s_od;
+        for (int32_t e = beg; e < end; ++e) {
+            const int32_t j = A.col[1][e];
+            const float x0 = xb[A.eid[1][e]] ? 1.f : 0.f;
+            float y[CPL]; load_ch<CPL, BF>(A.Y_dev, ((int64_t)rep * A.n_dev + j) * 2 * F + F + c0, y);
+            float m[CPL];
+            float s2 = entry_score<CPL, LPH>(y, x0, 0.f, k, q, A.slope, m);
+            o.push(s2, m);
+        }
+        if (end > beg) {
+            float inv = A.g_cross / o.den;
+            for (int c = 0; c < CPL; ++c) out[c] = fmaf(o.acc[c], inv, out[c]);
+        }
+    }
+    store_row<CPL, BF>(A.H_op, ((int64_t)rep * A.n_op + u) * F + c0, A.out_f32 != 0, out);
+}
+
+// device <- op partials over chunks of kChunk entries
+template <int F, int K, bool BF>
+__global__ void __launch_bounds__(256) agg_dev_part(AggArgs A) {
+    constexpr int CPL = F / 64, LPH = 64 / K;
+    const int lane = threadIdx.x & 63;
+    const uint32_t nblk = gridDim.x;
+    const uint32_t lb = xcd_swizzle(blockIdx.x, nblk);
+    // logical wave id: (rep, chunk, device) with the device fastest
+    const int64_t w = (int64_t)lb * kWaves + (threadIdx.x >> 6);
+    const int64_t total = (int64_t)A.R * A.maxc * A.n_dev;
+    if (w >= total) return;
+    const int32_t j = (int32_t)(w % A.n_dev);
+    const int32_t c = (int32_t)((w / A.n_dev) % A.maxc);
+    const int32_t rep = (int32_t)(w / ((int64_t)A.n_dev * A.maxc));
+    const int32_t rbeg = A.rp[2][j], rend = A.rp[2][j + 1];
+    const int32_t beg = rbeg + c * kChunk;
+    if (beg >= rend) return;
+    const int32_t end = min(beg + kChunk, rend);
+    const int c0 = lane * CPL;
+    RelConst<CPL> k; k.load(A, 1, F, c0);
+    float yd[CPL]; load_ch<CPL, BF>(A.Y_dev, ((int64_t)rep * A.n_dev + j) * 2 * F + F + c0, yd);
+    float q = 0.f;
+    for (int cc = 0; cc < CPL; ++cc) q = fmaf(k.ad[cc], yd[cc], q);
+    q = head_sum<LPH>(q);
+    Online<CPL> o; o.init();
+    const uint8_t *xb = A.x_od + (int64_t)rep * A.s_od;
+    for (int32_t e = beg; e < end; ++e) {
+        const int32_t u = A.col[2][e];
+        const float x0 = xb[A.eid[2][e]] ? 1.f : 0.f;
+        float y[CPL]; load_ch<CPL, BF>(A.Y_op, ((int64_t)rep * A.n_op + u) * 2 * F + F + c0, y);
+        float m[CPL];
+        float s2 = entry_score<CPL, LPH>(y, x0, 0.f, k, q, A.slope, m);
+        o.push(s2, m);
+    }
+    // partial record: [mx per head][den per head][acc F]
+    float *p = A.part + (((int64_t)rep * A.n_dev + j) * A.maxc + c) * (F + 2 * K);
+    const int head = lane / LPH;
+    if ((lane % LPH) == 0) { p[head] = o.mx; p[K + head] = o.den; }
+    for (int cc = 0; cc < CPL; ++cc) p[2 * K + c0 + cc] = o.acc[cc];
+}
+
+// device destinations: merge B2 partials, then B3 (dev <- dev)
+template <int F, int K, bool BF>
+__global__ void __launch_bounds__(256) agg_dev_final(AggArgs A) {
+    constexpr int CPL = F / 64, LPH = 64 / K;
+    const int lane = threadIdx.x & 63;
+    const int64_t w = (int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6);
+    if (w >= (int64_t)A.R * A.n_dev) return;
+    const int32_t rep = (int32_t)(w / A.n_dev);
+    const int32_t j = (int32_t)(w % A.n_dev);
+    const int c0 = lane * CPL;
+    const int head = lane / LPH;
+    float out[CPL];
+    for (int c = 0; c < CPL; ++c) out[c] = 0.f;
+    {   // B2 merge in chunk order
+        const int32_t deg = A.rp[2][j + 1] - A.rp[2][j];
+        const int32_t nch = (deg + kChunk - 1) / kChunk;
+        if (nch > 0) {
+            const float *p0 = A.part + ((int64_t)rep * A.n_dev + j) * A.maxc * (F + 2 * K);
+            float M = -INFINITY;
+            for (int32_t c = 0; c < nch; ++c) M = fmaxf(M, p0[(int64_t)c * (F + 2 * K) + head]);
+            float den = 0.f, acc[CPL];
+            for (int cc = 0; cc < CPL; ++cc) acc[cc] = 0.f;
+            for (int32_t c = 0; c < nch; ++c) {
+                const float *p = p0 + (int64_t)c * (F + 2 * K);
+                float sc = __builtin_amdgcn_exp2f(p[head] - M);
+                den = fmaf(p[K + head], sc, den);
+                for (int cc = 0; cc < CPL; ++cc) acc[cc] = fmaf(p[2 * K + c0 + cc], sc, acc[cc]);
+            }
+            float inv = A.g_cross / den;
+            for (int cc = 0; cc < CPL; ++cc) out[cc] = acc[cc] * inv;
+        }
+    }
+    {   // B3: dev <- dev, relation dd
+        RelConst<CPL> k; k.load(A, 2, F, c0);
+        float yd[CPL]; load_ch<CPL, BF>(A.Y_dev, ((int64_t)rep * A.n_dev + j) * 2 * F + c0, yd);
+        float q = 0.f;
+        for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], yd[c], q);
+        q = head_sum<LPH>(q);
+        Online<CPL> o; o.init();
+        const int32_t beg = A.rp[3][j], end = A.rp[3][j + 1];
+        const float *xd = A.x_dd + (int64_t)rep * A.s_dd;
+        for (int32_t e = beg; e < end; ++e) {
+            const int32_t v = A.col[3][e];
+            const int32_t id = A.eid[3][e];
+            const float x0 = xd[(int64_t)id * 2], x1 = xd[(int64_t)id * 2 + 1];
+            float y[CPL]; load_ch<CPL, BF>(A.Y_dev, ((int64_t)rep * A.n_dev + v) * 2 * F + c0, y);
+            float m[CPL];
+            float s2 = entry_score<CPL, LPH>(y, x0, x1, k, q, A.slope, m);
+            o.push(s2, m);
+        }
+        if (end > beg) {
+            float inv = A.g_same / o.den;
+            for (int c = 0; c < CPL; ++c) out[c] = fmaf(o.acc[c], inv, out[c]);
+        }
+    }
+    store_row<CPL, BF>(A.H_dev, ((int64_t)rep * A.n_dev + j) * F + c0, A.out_f32 != 0, out);
+}
+
+// ------------------------------------------------------------------ planning
+struct FwdLayout {
+    float *U, *cp;
+    uint16_t *Wb;
+    void *H_op[2], *H_dev[2];
+    void *Y_op, *Y_dev;
+    float *part;
+    int32_t maxc;
+};
+
+tag_status check_dims(const tag_model_dims *d) {
+    if (!d) TAG_FAIL(TAG_EINVAL, "dims is NULL");
+    if (d->f != 64 && d->f != 128 && d->f != 256) TAG_FAIL(TAG_ESHAPE, "f must be 64, 128 or 256");
+    if (d->heads < 1 || d->heads > 64 || (d->heads & (d->heads - 1)))
+        TAG_FAIL(TAG_ESHAPE, "heads must be a power of two in [1, 64]");
+    if (d->layers < 1 || d->layers > 16) TAG_FAIL(TAG_ESHAPE, "layers must be in [1, 16]");
+    if (d->f_op < 1 || d->f_op > 64 || d->f_dev < 1 || d->f_dev > 64)
+        TAG_FAIL(TAG_ESHAPE, "f_op and f_dev must be in [1, 64]");
+    if (d->dec_hidden < 0 || d->dec_hidden > 1024) TAG_FAIL(TAG_ESHAPE, "dec_hidden must be in [0, 1024]");
+    if (d->dtype != TAG_F32 && d->dtype != TAG_BF16) TAG_FAIL(TAG_EINVAL, "dtype must be TAG_F32 or TAG_BF16");
+    if (!(d->gamma_same == d->gamma_same) || !(d->gamma_cross == d->gamma_cross) ||
+        !(d->leaky_slope == d->leaky_slope))
+        TAG_FAIL(TAG_EINVAL, "gamma and slope must not be NaN");
+    return TAG_OK;
+}
+
+size_t carve_fwd(const tag_graph *g, const tag_model_dims *d, int32_t R, void *base, FwdLayout *L) {
+    Carver c(base);
+    const int F = d->f;
+    const size_t es = d->dtype == TAG_BF16 ? 2 : 4;
+    L->U = c.take<float>((size_t)d->layers * 3 * F * 2);
+    L->cp = c.take<float>((size_t)d->layers * 3 * F);
+    L->Wb = d->dtype == TAG_BF16 ? c.take<uint16_t>((size_t)d->layers * 3 * F * F) : nullptr;
+    for (int i = 0; i < 2; ++i) {
+        L->H_op[i] = c.take<char>((size_t)R * g->n_op * F * es);
+        L->H_dev[i] = c.take<char>((size_t)R * g->n_dev * F * es);
+    }
+    L->Y_op = c.take<char>((size_t)R * g->n_op * 2 * F * es);
+    L->Y_dev = c.take<char>((size_t)R * g->n_dev * 2 * F * es);
+    L->maxc = std::max<int32_t>(1, (g->max_degree[2] + kChunk - 1) / kChunk);
+    L->part = c.take<float>((size_t)R * g->n_dev * L->maxc * (F + 2 * d->heads));
+    return c.used;
+}
+
+template <int F, int K, bool BF>
+void launch_agg(const AggArgs &A, hipStream_t st) {
+    const int64_t op_waves = (int64_t)A.R * A.n_op;
+    const int64_t part_waves = (int64_t)A.R * A.maxc * A.n_dev;
+    const int64_t dev_waves = (int64_t)A.R * A.n_dev;
+    agg_op<F, K, BF><<<(unsigned)((op_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
+    agg_dev_part<F, K, BF><<<(unsigned)((part_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
+    agg_dev_final<F, K, BF><<<(unsigned)((dev_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
+}
+
+template <int F, bool BF>
+tag_status dispatch_heads(int K, const AggArgs &A, hipStream_t st) {
+    switch (K) {
+        case 1: launch_agg<F, 1, BF>(A, st); break;
+        case 2: launch_agg<F, 2, BF>(A, st); break;
+        case 4: launch_agg<F, 4, BF>(A, st); break;
+        case 8: launch_agg<F, 8, BF>(A, st); break;
+        case 16: launch_agg<F, 16, BF>(A, st); break;
+        case 32: launch_agg<F, 32, BF>(A, st); break;
+        case 64: launch_agg<F, 64, BF>(A, st); break;
+        default: TAG_FAIL(TAG_ESHAPE, "unsupported head count");
+    }
+    return TAG_OK;
+}
+
+tag_status dispatch_agg(int F, int K, bool bf, const AggArgs &A, hipStream_t st) {
+    if (F == 64) return bf ? dispatch_heads<64, true>(K, A, st) : dispatch_heads<64, false>(K, A, st);
+    if (F == 128) return bf ? dispatch_heads<128, true>(K, A, st) : dispatch_heads<128, false>(K, A, st);
+    return bf ? dispatch_heads<256, true>(K, A, st) : dispatch_heads<256, false>(K, A, st);
+}
+
+}  // namespace
+}  // namespace tag
+
+using namespace tag;
+
+extern "C" tag_status tag_gnn_workspace(const tag_graph *g, const tag_model_dims *dims, int32_t n_replicas,
+                                        size_t *bytes) {
+    clear_error();
+    if (!g || !bytes) TAG_FAIL(TAG_EINVAL, "graph and bytes must be non-NULL");
+    tag_status st = check_dims(dims);
+    if (st != TAG_OK) return st;
+    if (n_replicas < 1) TAG_FAIL(TAG_EINVAL, "n_replicas must be >= 1");
+    FwdLayout L;
+    *bytes = carve_fwd(g, dims, n_replicas, nullptr, &L);
+    return TAG_OK;
+}
+
+extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *dims, const tag_weights *w,
+                                      const tag_features *x, void *workspace, size_t ws_bytes, float *E_op,
+                                      float *E_dev, void *hip_stream) {
+    clear_error();
+    if (!g || !w || !x || !E_op || !E_dev || !workspace)
+        TAG_FAIL(TAG_EINVAL, "graph, weights, features, outputs and workspace must be non-NULL");
+    tag_status st = check_dims(dims);
+    if (st != TAG_OK) return st;
+    const int32_t R = x->n_replicas;
+    if (R < 1) TAG_FAIL(TAG_EINVAL, "n_replicas must be >= 1");
+    if (!x->x_op || !x->x_dev || (g->e_oo && !x->x_oo) || (g->e_dd && !x->x_dd) || (g->e_od && !x->x_od))
+        TAG_FAIL(TAG_EINVAL, "feature arrays must be non-NULL");
+    if (x->stride_oo < 0 || x->stride_dd < 0 || x->stride_od < 0) TAG_FAIL(TAG_EINVAL, "strides must be >= 0");
+    if (!w->enc_op_w || !w->enc_op_b || !w->enc_dev_w || !w->enc_dev_b || !w->layer_w || !w->layer_b ||
+        !w->att_src || !w->att_dst)
+        TAG_FAIL(TAG_EINVAL, "weight arrays must be non-NULL");
+    for (int r = 0; r < 3; ++r)
+        if (!w->enc_edge_w[r] || !w->enc_edge_b[r]) TAG_FAIL(TAG_EINVAL, "edge encoder weights must be non-NULL");
+    if ((reinterpret_cast<uintptr_t>(x->x_op) | reinterpret_cast<uintptr_t>(E_op) |
+         reinterpret_cast<uintptr_t>(E_dev) | reinterpret_cast<uintptr_t>(w->layer_w) |
+         reinterpret_cast<uintptr_t>(workspace)) & 15)
+        TAG_FAIL(TAG_EINVAL, "x_op, E_op, E_dev, layer_w and workspace must be 16-byte aligned");
+    FwdLayout L;
+    if (carve_fwd(g, dims, R, nullptr, &L) > ws_bytes) TAG_FAIL(TAG_ENOSPACE, "workspace too small (see tag_gnn_workspace)");
+    carve_fwd(g, dims, R, workspace, &L);
+    hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+    const int F = dims->f, K = dims->heads, NL = dims->layers;
+    const bool bf = dims->dtype == TAG_BF16;
+
+    FoldArgs fa{w->layer_w, w->layer_b, {w->enc_edge_w[0], w->enc_edge_w[1], w->enc_edge_w[2]},
+                {w->enc_edge_b[0], w->enc_edge_b[1], w->enc_edge_b[2]}, L.U, L.cp, F};
+    fold_edge_terms<<<NL * 3, 256, 0, stream>>>(fa);
+    if (bf) convert_wh_bf16<<<256, 256, 0, stream>>>(w->layer_w, L.Wb, F, NL * 3);
+
+    // encoders: hidden h0 in the working precision
+    const int64_t rows_op = (int64_t)R * g->n_op, rows_dev = (int64_t)R * g->n_dev;
+    {
+        size_t sh_op = sizeof(float) * dims->f_op * F, sh_dev = sizeof(float) * dims->f_dev * F;
+        unsigned b_op = (unsigned)((rows_op + 255) / 256), b_dev = (unsigned)((rows_dev + 255) / 256);
+        if (bf) {
+            encode_rows<true><<<b_op, 256, sh_op, stream>>>(x->x_op, rows_op, dims->f_op, w->enc_op_w, w->enc_op_b, L.H_op[0], F);
+            encode_rows<true><<<b_dev, 256, sh_dev, stream>>>(x->x_dev, rows_dev, dims->f_dev, w->enc_dev_w, w->enc_dev_b, L.H_dev[0], F);
+        } else {
+            encode_rows<false><<<b_op, 256, sh_op, stream>>>(x->x_op, rows_op, dims->f_op, w->enc_op_w, w->enc_op_b, L.H_op[0], F);
+            encode_rows<false><<<b_dev, 256, sh_dev, stream>>>(x->x_dev, rows_dev, dims->f_dev, w->enc_dev_w, w->enc_dev_b, L.H_dev[0], F);
+        }
+    }
+    AggArgs A{};
+    A.R = R;
+    A.n_op = g->n_op; A.n_dev = g->n_dev;
+    for (int b = 0; b < 4; ++b) { A.rp[b] = g->rowptr[b]; A.col[b] = g->col[b]; A.eid[b] = g->eid[b]; }
+    A.Y_op = L.Y_op; A.Y_dev = L.Y_dev;
+    A.x_oo = x->x_oo; A.s_oo = x->stride_oo;
+    A.x_dd = x->x_dd; A.s_dd = x->stride_dd;
+    A.x_od = x->x_od; A.s_od = x->stride_od;
+    A.g_same = dims->gamma_same; A.g_cross = dims->gamma_cross; A.slope = dims->leaky_slope;
+    A.part = L.part; A.maxc = L.maxc;
+
+    for (int l = 0; l < NL; ++l) {
+        const int cur = l & 1, nxt = cur ^ 1;
+        const bool last = (l == NL - 1);
+        // relation transforms: op rows [W^h_oo ; W^h_od], device rows [W^h_dd ; W^h_od]
+        dim3 g_op((unsigned)((rows_op + TM - 1) / TM), (unsigned)(2 * F / TN));
+        dim3 g_dev((unsigned)((rows_dev + TM - 1) / TM), (unsigned)(2 * F / TN));
+        if (bf) {
+            const uint16_t *Wl = L.Wb + (size_t)l * 3 * F * F;
+            gemm_bf16<<<g_op, 256, 0, stream>>>(static_cast<const uint16_t *>(L.H_op[cur]), rows_op, F,
+                                               Wl + 0 * F * F, Wl + 1 * F * F, F, static_cast<uint16_t *>(L.Y_op));
+            gemm_bf16<<<g_dev, 256, 0, stream>>>(static_cast<const uint16_t *>(L.H_dev[cur]), rows_dev, F,
+                                                Wl + 2 * F * F, Wl + 1 * F * F, F, static_cast<uint16_t *>(L.Y_dev));
+        } else {
+            const float *Wl = w->layer_w + (size_t)l * 3 * F * 2 * F;
+            gemm_f32<<<g_op, 256, 0, stream>>>(static_cast<const float *>(L.H_op[cur]), rows_op, F,
+                                              Wl + 0 * F * 2 * F, Wl + 1 * F * 2 * F, 2 * F, static_cast<float *>(L.Y_op));
+            gemm_f32<<<g_dev, 256, 0, stream>>>(static_cast<const float *>(L.H_dev[cur]), rows_dev, F,
+                                               Wl + 2 * F * 2 * F, Wl + 1 * F * 2 * F, 2 * F, static_cast<float *>(L.Y_dev));
+        }
+        A.att_src = w->att_src + (size_t)l * 3 * F;
+        A.att_dst = w->att_dst + (size_t)l * 3 * F;
+        A.U = L.U + (size_t)l * 3 * F * 2;
+        A.cp = L.cp + (size_t)l * 3 * F;
+        A.H_op = last ? static_cast<void *>(E_op) : L.H_op[nxt];
+        A.H_dev = last ? static_cast<void *>(E_dev) : L.H_dev[nxt];
+        A.out_f32 = last ? 1 : (bf ? 0 : 1);
+        st = dispatch_agg(F, K, bf, A, stream);
+        if (st != TAG_OK) return st;
+    }
+    return launch_status("tag_gnn_forward");
+}

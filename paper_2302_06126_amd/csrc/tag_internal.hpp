@@ -1,0 +1,97 @@
+// Internal declarations shared by the translation units of libtag.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/tag.h"
+
+namespace tag {
+
+// ------------------------------------------------------------------ errors
+void set_error(const std::string &msg);
+void clear_error();
+
+#define TAG_FAIL(code, msg)          \
+    do {                             \
+        ::tag::set_error(msg);       \
+        return (code);               \
+    } while (0)
+
+#define TAG_HIP_CHECK(expr)                                                            \
+    do {                                                                               \
+        hipError_t e_ = (expr);                                                        \
+        if (e_ != hipSuccess)                                                          \
+            TAG_FAIL(TAG_EHIP, std::string(#expr ": ") + hipGetErrorString(e_));       \
+    } while (0)
+
+// Check for a launch error right after enqueueing kernels.
+tag_status launch_status(const char *what);
+
+// ------------------------------------------------------------ memory plans
+inline size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
+
+// A bump allocator over a caller buffer (or a size counter when base == null).
+struct Carver {
+    char *base;
+    size_t used = 0;
+    explicit Carver(void *b) : base(static_cast<char *>(b)) {}
+    template <typename T>
+    T *take(size_t count) {
+        size_t off = used;
+        used = align_up(used + count * sizeof(T));
+        return base ? reinterpret_cast<T *>(base + off) : nullptr;
+    }
+};
+
+}  // namespace tag
+
+// ------------------------------------------------------------ graph handle
+struct tag_graph {
+    int32_t G = 0;
+    int32_t max_dev = 0;
+    int64_t n_op = 0, n_dev = 0, e_oo = 0, e_dd = 0, e_od = 0;
+    std::vector<int64_t> op_off, dev_off;     // host [G+1]
+    int64_t rows[4] = {0, 0, 0, 0}, nnz[4] = {0, 0, 0, 0};
+    int32_t max_degree[4] = {0, 0, 0, 0};
+    // device arrays inside the caller's csr buffer
+    const int32_t *rowptr[4] = {nullptr, nullptr, nullptr, nullptr};
+    const int32_t *col[4] = {nullptr, nullptr, nullptr, nullptr};
+    const int32_t *eid[4] = {nullptr, nullptr, nullptr, nullptr};
+    const int32_t *op_off_d = nullptr;   // [G+1]
+    const int32_t *dev_off_d = nullptr;  // [G+1]
+    int device = 0;
+};
+
+// ----------------------------------------------------------- device helpers
+namespace tag {
+
+__device__ __forceinline__ float leaky(float x, float slope) { return x > 0.f ? x : slope * x; }
+
+// round-to-nearest-even fp32 -> bf16 bits
+__device__ __forceinline__ uint16_t f2bf(float x) {
+    uint32_t u = __float_as_uint(x);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return static_cast<uint16_t>(u >> 16);
+}
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
+
+// XCD-aware block order: the hardware deals consecutive workgroups to the
+// 8 XCDs round-robin; remap so that logically consecutive blocks share an
+// XCD (and its L2).  Bijective on [0, n).
+__device__ __forceinline__ uint32_t xcd_swizzle(uint32_t bid, uint32_t n) {
+    constexpr uint32_t X = 8;
+    uint32_t per = n / X, rem = n % X;
+    uint32_t x = bid % X, k = bid / X;
+    // blocks bid >= X*per (the ragged tail) keep their order after the full part
+    if (k >= per) return bid;
+    (void)rem;
+    return x * per + k;
+}
+
+}  // namespace tag
