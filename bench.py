@@ -1,0 +1,254 @@
+"""Throughput benchmark of the hot path on one MI355X.
+
+One step = one pass of the whole path over one batch of candidate graphs:
+graph ingest (relation-bucketed CSR build), encoders + L GNN layers for
+every candidate, and the decision head for the ops of each candidate's
+next group.  Inputs are seeded synthetic graphs resident in HBM before the
+timed region starts.  Prints one JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload cnn]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+METRIC = "candidate deployment graphs/sec and edges/sec; achieved HBM GB/s %"
+PEAK_HBM_GBS = 8000.0
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
+STAGE_NAMES = ["graph_build", "encode", "transform", "agg_op", "agg_dev_part", "agg_dev_final", "decide"]
+KERNEL_NAMES = {"transform": "gemm_f32 / gemm_bf16", "agg_op": "agg_op", "agg_dev_part": "agg_dev_part",
+                "agg_dev_final": "agg_dev_final", "encode": "encode_rows", "decide": "dec_*",
+                "graph_build": "graph build kernels"}
+
+
+def algorithmic_work(stage: str, wl, topo, R: int, info) -> tuple:
+    """(flops, bytes) one launch of `stage` must do at minimum: each unique
+    row read or written once, shared graph structure counted once."""
+    N, M, F, K = topo.n_op, topo.n_dev, wl.f, wl.heads
+    s = 2 if wl.dtype == "bf16" else 4
+    rows = R * (N + M)
+    if stage == "transform":
+        return 2.0 * rows * F * 2 * F, float(rows * F * s + rows * 2 * F * s + 2 * 2 * F * F * s)
+    if stage == "agg_op":
+        # Y_op both halves of every op row, Y_dev od half, H' out, bits, x_oo, CSR B0+B1
+        by = (R * N * 2 * F * s + R * M * F * s + R * N * F * (4 if s == 4 else 2) + R * topo.e_od
+              + topo.e_oo * 4 + (2 * topo.e_oo + topo.e_od) * 8 + 2 * (N + 1) * 4)
+        fl = R * (2 * topo.e_oo * 7 * F + topo.e_od * 7 * F)
+        return float(fl), float(by)
+    if stage == "agg_dev_part":
+        maxc = max(1, (int(info.max_degree[2]) + 255) // 256)
+        by = R * N * F * s + R * M * F * s + R * topo.e_od + topo.e_od * 8 + R * M * maxc * (F + 2 * K) * 4
+        fl = R * topo.e_od * 7 * F
+        return float(fl), float(by)
+    if stage == "agg_dev_final":
+        maxc = max(1, (int(info.max_degree[2]) + 255) // 256)
+        by = R * M * maxc * (F + 2 * K) * 4 + R * M * 2 * F * s + R * M * F * 4 + R * topo.e_dd * 8 + 2 * topo.e_dd * 8
+        return float(R * 2 * topo.e_dd * 9 * F), float(by)
+    if stage == "encode":
+        return (2.0 * R * (N * wl.f_op + M * 8) * F,
+                float(R * (N * wl.f_op + M * 8) * 4 + rows * F * s))
+    return 0.0, 0.0
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(name, wl, topo, batch, masks, opts, w, budget_s: float) -> dict:
+    """The oracle as it stands: one candidate at a time (CSR build + forward
+    + decide), single-threaded, until the time budget is spent."""
+    import oracle
+    oracle.build(force=False)
+    t0 = time.perf_counter()
+    n = 0
+    while n < batch.x_op.shape[0]:
+        sel = batch.query_rep == n
+        E_op, E_dev = oracle.forward(topo, batch.x_op[n], batch.x_dev[n], batch.x_oo, batch.x_dd[n], batch.x_od[n],
+                                     w, f=wl.f, heads=wl.heads, layers=wl.layers, bf16=wl.dtype == "bf16")
+        oracle.decide(E_op, E_dev, masks, opts, batch.query_op[sel], w, f=wl.f, dec_hidden=wl.f,
+                      n_dev=topo.n_dev, want_prior=True)
+        n += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    el = time.perf_counter() - t0
+    return {"value": n / el, "unit": "graphs/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n} of {batch.x_op.shape[0]} candidates of the {name} batch, each: CSR build + "
+                      f"forward + decide of its next-group ops, fp64, one thread, {el:.1f} s",
+            "cpu": cpu_model()}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="cnn", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--stage", default="auto", choices=["auto"] + STAGE_NAMES,
+                    help="kernel stage timed for the roofline (auto: the longest one)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        sys.exit("bench.py measures one GPU only: this build has no multi-GPU path "
+                 "(candidates would shard across GPUs with no per-layer exchange); run with --gpus 1")
+
+    import torch
+
+    import paper_2302_06126_amd as P
+    from paper_2302_06126_amd import _abi
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    name = args.workload
+    wl = synth.WORKLOADS[name]
+    topo = synth.make_topology(name)
+    batch = synth.make_batch(name, topo, wl.batch, wl.f_op)
+    masks, opts = synth.make_slices(name, topo.n_dev, wl.n_slices)
+    w = synth.make_weights(wl.f, wl.heads, wl.layers, wl.f_op, wl.f)
+    R = wl.batch
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    # ---- inputs resident in HBM ----
+    edges = {k: t(getattr(topo, k)) for k in ("oo_src", "oo_dst", "dd_a", "dd_b", "od_op", "od_dev")}
+    n_op = np.array([topo.n_op], np.int32)
+    n_dev = np.array([topo.n_dev], np.int32)
+    offs = [np.array([0, x], np.int64) for x in (topo.e_oo, topo.e_dd, topo.e_od)]
+    desc = P.tag_graph_desc()
+    desc.n_graphs = 1
+    desc.n_op = n_op.ctypes.data_as(C.POINTER(C.c_int32))
+    desc.n_dev = n_dev.ctypes.data_as(C.POINTER(C.c_int32))
+    desc.oo_off, desc.dd_off, desc.od_off = (o.ctypes.data_as(C.POINTER(C.c_int64)) for o in offs)
+    for k, v in edges.items():
+        setattr(desc, k, v.data_ptr())
+    x_op, x_dev, x_oo, x_dd, x_od = t(batch.x_op), t(batch.x_dev), t(batch.x_oo), t(batch.x_dd), t(batch.x_od)
+    feats = P.make_features(x_op, x_dev, x_oo, x_dd, x_od)
+    model = P.Model(w, f=wl.f, heads=wl.heads, layers=wl.layers, f_op=wl.f_op, dtype=wl.dtype, device="cuda:0")
+    stream = torch.cuda.current_stream()
+    sh = int(stream.cuda_stream)
+
+    st, csr_b, tmp_b = P.tag_graph_plan(desc)
+    _abi.check(st, "tag_graph_plan")
+    csr = torch.empty(csr_b, dtype=torch.uint8, device=dev)
+    tmp = torch.empty(tmp_b, dtype=torch.uint8, device=dev)
+    st, h0 = P.tag_graph_build(desc, csr.data_ptr(), csr_b, tmp.data_ptr(), tmp_b, sh)
+    _abi.check(st, "tag_graph_build")
+    st, info = P.tag_graph_get_info(h0)
+    st, ws_b = P.tag_gnn_workspace(h0, model.dims, R)
+    _abi.check(st, "tag_gnn_workspace")
+    ws = torch.empty(ws_b, dtype=torch.uint8, device=dev)
+    E_op = torch.empty((R, topo.n_op, wl.f), dtype=torch.float32, device=dev)
+    E_dev = torch.empty((R, topo.n_dev, wl.f), dtype=torch.float32, device=dev)
+    Q = len(batch.query_op)
+    masks_t = t(masks.view(np.int64))
+    opts_t = t(opts)
+    slices = P.tag_slices(len(masks), masks_t.data_ptr(), opts_t.data_ptr())
+    q_rep, q_graph, q_op = t(batch.query_rep), t(np.zeros(Q, np.int32)), t(batch.query_op)
+    st, dws_b = P.tag_gnn_decide_workspace(h0, model.dims, R, len(masks), Q)
+    _abi.check(st, "tag_gnn_decide_workspace")
+    dws = torch.empty(max(dws_b, 1), dtype=torch.uint8, device=dev)
+    argmax = torch.empty(Q, dtype=torch.int32, device=dev)
+    best = torch.empty(Q, dtype=torch.float32, device=dev)
+    prior = torch.empty((Q, len(masks)), dtype=torch.float32, device=dev)
+    decision = torch.empty((Q, C.sizeof(P.tag_decision)), dtype=torch.uint8, device=dev)
+    P.tag_graph_destroy(h0)
+
+    def step():
+        st, h = P.tag_graph_build(desc, csr.data_ptr(), csr_b, tmp.data_ptr(), tmp_b, sh)
+        _abi.check(st, "tag_graph_build")
+        st = P.tag_gnn_forward(h, model.dims, model.weights, feats, ws.data_ptr(), ws_b, E_op.data_ptr(),
+                               E_dev.data_ptr(), sh)
+        _abi.check(st, "tag_gnn_forward")
+        st = P.tag_gnn_decide(h, model.dims, model.weights, R, E_op.data_ptr(), E_dev.data_ptr(), slices, Q,
+                              q_rep.data_ptr(), q_graph.data_ptr(), q_op.data_ptr(), argmax.data_ptr(),
+                              best.data_ptr(), prior.data_ptr(), decision.data_ptr(), dws.data_ptr(), dws_b, sh)
+        _abi.check(st, "tag_gnn_decide")
+        P.tag_graph_destroy(h)
+
+    print(f"[bench] workload {name}: B={R} N={topo.n_op} M={topo.n_dev} f={wl.f} L={wl.layers} {wl.dtype}; "
+          f"warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(max(args.warmup, 1)):
+        step()
+    torch.cuda.synchronize()
+
+    # which stage dominates: one profiled step per stage (outside the timed region)
+    stage_ms = {}
+    for sid, sname in enumerate(STAGE_NAMES):
+        _abi.check(P.tag_profile_begin(sid, 64), "tag_profile_begin")
+        step()
+        st, ms, n = P.tag_profile_end()
+        _abi.check(st, "tag_profile_end")
+        stage_ms[sname] = ms
+    stage = max(stage_ms, key=stage_ms.get) if args.stage == "auto" else args.stage
+    launches_per_step = {"graph_build": 1, "encode": 1, "decide": 1}.get(stage, wl.layers)
+
+    # ---- timed region ----
+    torch.cuda.synchronize()
+    _abi.check(P.tag_profile_begin(STAGE_NAMES.index(stage), launches_per_step * args.steps), "tag_profile_begin")
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    st, kern_ms, n_launch = P.tag_profile_end()
+    _abi.check(st, "tag_profile_end")
+    el = t1 - t0
+    ms_step = el * 1e3 / args.steps
+    graphs_s = R * args.steps / el
+    T = topo.entries()
+    flops, byts = algorithmic_work(stage, wl, topo, R, info)
+    avg_s = kern_ms / 1e3 / max(n_launch, 1)
+    fl_tf = flops / avg_s / 1e12
+    bw_gbs = byts / avg_s / 1e9
+    peak_fl = PEAK_TFLOPS[wl.dtype] if stage == "transform" else None
+    if stage == "transform" and flops / byts >= peak_fl * 1e12 / (PEAK_HBM_GBS * 1e9):
+        roof = {"bound": "mfma", "achieved": round(fl_tf, 3), "peak": peak_fl, "unit": "TFLOP/s",
+                "frac": round(fl_tf / peak_fl, 4)}
+    else:
+        roof = {"bound": "hbm", "achieved": round(bw_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(bw_gbs / PEAK_HBM_GBS, 4)}
+    roof.update({"traffic": None, "kernel": KERNEL_NAMES[stage], "stage": stage,
+                 "avg_launch_ms": round(avg_s * 1e3, 4), "launches": n_launch,
+                 "algorithmic_bytes_per_launch": byts, "algorithmic_flops_per_launch": flops})
+    out = {
+        "metric": METRIC, "value": round(graphs_s, 2), "unit": "graphs/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": name, "description": wl.description, "graphs_per_step": R,
+                   "n_op": topo.n_op, "n_dev": topo.n_dev, "entries_per_layer": T, "layers": wl.layers,
+                   "f": wl.f, "heads": wl.heads, "slices": len(masks), "queries": Q, "parallelism": "none"},
+        "edges_per_s": round(T * R * args.steps / el, 1),
+        "edge_layer_updates_per_s": round(T * wl.layers * R * args.steps / el, 1),
+        "stage_ms_one_step": {k: round(v, 4) for k, v in stage_ms.items()},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(name, wl, topo, batch, masks, opts, w, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,46 @@
+/*
+ * tag_profile.h -- optional per-kernel timing for libtag.so.
+ *
+ * While a profile is active, the library records a pair of HIP events on the
+ * launch stream around every launch of one kernel stage, so a caller can
+ * measure that kernel's average duration inside a timed region without an
+ * external profiler.  The state is process-wide and not thread-safe: use it
+ * from one host thread, with no other library calls in flight on other
+ * threads.  Event handles are host objects; no device memory is allocated.
+ */
+#ifndef TAG_PROFILE_H
+#define TAG_PROFILE_H
+
+#include <stdint.h>
+
+#include "tag.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Kernel stages that can be timed. */
+enum {
+    TAG_STAGE_GRAPH_BUILD = 0,   /* every kernel of tag_graph_build (one pair per call)  */
+    TAG_STAGE_ENCODE = 1,        /* node encoders                                         */
+    TAG_STAGE_TRANSFORM = 2,     /* relation transforms W^h h, op and device rows (1/layer) */
+    TAG_STAGE_AGG_OP = 3,        /* op destinations: op<-op and op<-dev (1/layer)         */
+    TAG_STAGE_AGG_DEV_PART = 4,  /* device<-op chunk partials (1/layer)                   */
+    TAG_STAGE_AGG_DEV_FINAL = 5, /* device destinations: merge + dev<-dev (1/layer)      */
+    TAG_STAGE_DECIDE = 6,        /* every kernel of tag_gnn_decide (one pair per call)   */
+    TAG_STAGE_COUNT = 7
+};
+
+/* Start recording event pairs around launches of `stage`, for at most
+ * `capacity` launches (later launches are not recorded).  Replaces any
+ * active profile. */
+tag_status tag_profile_begin(int32_t stage, int32_t capacity);
+
+/* Synchronise the recorded events, return the summed elapsed time of the
+ * recorded launches (ms) and their count, and end the profile. */
+tag_status tag_profile_end(double *total_ms, int32_t *n_launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TAG_PROFILE_H */

@@ -21,7 +21,8 @@ from ._abi import (TAG_BF16, TAG_F32, TagError, check, tag_decision, tag_feature
 
 __all__ = ["Graph", "Model", "tag_graph_plan", "tag_graph_build", "tag_graph_get_info", "tag_graph_export",
            "tag_graph_destroy", "tag_gnn_workspace", "tag_gnn_forward", "tag_gnn_decide_workspace",
-           "tag_gnn_decide", "tag_last_error", "tag_version", "forward", "decide", "TagError",
+           "tag_gnn_decide", "tag_last_error", "tag_version", "tag_profile_begin", "tag_profile_end",
+           "forward", "decide", "TagError",
            "TAG_F32", "TAG_BF16"]
 
 
@@ -48,6 +49,16 @@ def tag_last_error() -> str:
 
 def tag_version() -> str:
     return _abi.load().tag_version().decode()
+
+
+def tag_profile_begin(stage: int, capacity: int) -> int:
+    return _abi.load().tag_profile_begin(stage, capacity)
+
+
+def tag_profile_end():
+    ms, n = C.c_double(0.0), C.c_int32(0)
+    st = _abi.load().tag_profile_end(C.byref(ms), C.byref(n))
+    return st, ms.value, n.value
 
 
 def tag_graph_plan(desc: tag_graph_desc):

@@ -20,7 +20,11 @@ STATUS_NAMES = {0: "TAG_OK", -1: "TAG_EINVAL", -2: "TAG_ERANGE", -3: "TAG_EDUP",
 
 EXPORTS = ("tag_graph_plan", "tag_graph_build", "tag_graph_get_info", "tag_graph_export",
            "tag_graph_destroy", "tag_gnn_workspace", "tag_gnn_forward", "tag_gnn_decide_workspace",
-           "tag_gnn_decide", "tag_last_error", "tag_version")
+           "tag_gnn_decide", "tag_last_error", "tag_version", "tag_profile_begin", "tag_profile_end")
+
+# kernel stages (include/tag_profile.h)
+STAGE_GRAPH_BUILD, STAGE_ENCODE, STAGE_TRANSFORM, STAGE_AGG_OP, STAGE_AGG_DEV_PART, STAGE_AGG_DEV_FINAL, \
+    STAGE_DECIDE = range(7)
 
 _P32 = C.POINTER(C.c_int32)
 _P64 = C.POINTER(C.c_int64)
@@ -103,6 +107,10 @@ def load() -> C.CDLL:
     lib.tag_last_error.argtypes = []
     lib.tag_version.restype = C.c_char_p
     lib.tag_version.argtypes = []
+    lib.tag_profile_begin.argtypes = [S, S]
+    lib.tag_profile_begin.restype = S
+    lib.tag_profile_end.argtypes = [C.POINTER(C.c_double), C.POINTER(C.c_int32)]
+    lib.tag_profile_end.restype = S
     _lib = lib
     return lib
 

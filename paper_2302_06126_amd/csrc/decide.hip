@@ -250,9 +250,11 @@ extern "C" tag_status tag_gnn_decide(const tag_graph *g, const tag_model_dims *d
     A.q_rep = query_rep; A.q_graph = query_graph; A.q_op = query_op;
     A.t = L.t; A.u = L.u; A.v = L.v;
     A.argmax = argmax; A.best = best_score; A.prior = prior; A.dec = decision;
+    prof_begin(TAG_STAGE_DECIDE, stream);
     dec_dev_proj<<<grid_for((int64_t)A.R * A.n_dev * Hx), 256, 0, stream>>>(A);
     dec_slice<<<grid_for((int64_t)A.R * A.G * Hx * A.S), 256, 0, stream>>>(A);
     dec_query_proj<<<grid_for((int64_t)A.Q * Hx), 256, 0, stream>>>(A);
     dec_score<<<(unsigned)A.Q, kScoreThreads, sizeof(float) * (Hx + H), stream>>>(A);
+    prof_end(TAG_STAGE_DECIDE, stream);
     return launch_status("tag_gnn_decide");
 }

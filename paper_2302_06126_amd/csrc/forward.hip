@@ -108,15 +108,35 @@ __global__ void encode_rows(const float *__restrict__ x, int64_t rows, int fin,
 // 4 (l / 16) + v, column l % 16.
 constexpr int TM = 64, TN = 64;
 
-__global__ void __launch_bounds__(256) gemm_f32(const float *__restrict__ H, int64_t rows, int F,
-                                                const float *__restrict__ B0, const float *__restrict__ B1,
-                                                int ldb, float *__restrict__ Y) {
+// One launch covers both row sets of a layer: blocks [0, tiles0) take the op
+// rows (side 0), the rest the device rows (side 1).
+struct GemmSide {
+    const void *H;       // [rows][F]
+    int64_t rows;
+    const void *B0, *B1; // output channels [0, F) and [F, 2F)
+    int ldb;
+    void *Y;             // [rows][2F]
+};
+struct GemmArgs {
+    GemmSide side[2];
+    int64_t tiles0;
+    int F;
+};
+
+__global__ void __launch_bounds__(256) gemm_f32(GemmArgs G) {
     constexpr int BK = 16;
     __shared__ float As[TM][BK + 1];
     __shared__ float Bs[TN][BK + 1];
+    const int sd = (int64_t)blockIdx.x < G.tiles0 ? 0 : 1;
+    const float *__restrict__ H = static_cast<const float *>(G.side[sd].H);
+    const int64_t rows = G.side[sd].rows;
+    const float *__restrict__ B0 = static_cast<const float *>(G.side[sd].B0);
+    const float *__restrict__ B1 = static_cast<const float *>(G.side[sd].B1);
+    const int ldb = G.side[sd].ldb, F = G.F;
+    float *__restrict__ Y = static_cast<float *>(G.side[sd].Y);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    const int64_t m0 = (int64_t)blockIdx.x * TM;
+    const int64_t m0 = ((int64_t)blockIdx.x - (sd ? G.tiles0 : 0)) * TM;
     const int n0 = blockIdx.y * TN;
     f4 acc[2][2];
     for (int i = 0; i < 2; ++i)
@@ -155,15 +175,20 @@ __global__ void __launch_bounds__(256) gemm_f32(const float *__restrict__ H, int
             }
 }
 
-__global__ void __launch_bounds__(256) gemm_bf16(const uint16_t *__restrict__ H, int64_t rows, int F,
-                                                 const uint16_t *__restrict__ B0, const uint16_t *__restrict__ B1,
-                                                 int ldb, uint16_t *__restrict__ Y) {
+__global__ void __launch_bounds__(256) gemm_bf16(GemmArgs G) {
     constexpr int BK = 32, PADK = BK + 8;
     __shared__ __attribute__((aligned(16))) uint16_t As[TM][PADK];
     __shared__ __attribute__((aligned(16))) uint16_t Bs[TN][PADK];
+    const int sd = (int64_t)blockIdx.x < G.tiles0 ? 0 : 1;
+    const uint16_t *__restrict__ H = static_cast<const uint16_t *>(G.side[sd].H);
+    const int64_t rows = G.side[sd].rows;
+    const uint16_t *__restrict__ B0 = static_cast<const uint16_t *>(G.side[sd].B0);
+    const uint16_t *__restrict__ B1 = static_cast<const uint16_t *>(G.side[sd].B1);
+    const int ldb = G.side[sd].ldb, F = G.F;
+    uint16_t *__restrict__ Y = static_cast<uint16_t *>(G.side[sd].Y);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    const int64_t m0 = (int64_t)blockIdx.x * TM;
+    const int64_t m0 = ((int64_t)blockIdx.x - (sd ? G.tiles0 : 0)) * TM;
     const int n0 = blockIdx.y * TN;
     f4 acc[2][2];
     for (int i = 0; i < 2; ++i)
@@ -520,9 +545,15 @@ void launch_agg(const AggArgs &A, hipStream_t st) {
     const int64_t op_waves = (int64_t)A.R * A.n_op;
     const int64_t part_waves = (int64_t)A.R * A.maxc * A.n_dev;
     const int64_t dev_waves = (int64_t)A.R * A.n_dev;
+    prof_begin(TAG_STAGE_AGG_OP, st);
     agg_op<F, K, BF><<<(unsigned)((op_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
+    prof_end(TAG_STAGE_AGG_OP, st);
+    prof_begin(TAG_STAGE_AGG_DEV_PART, st);
     agg_dev_part<F, K, BF><<<(unsigned)((part_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
+    prof_end(TAG_STAGE_AGG_DEV_PART, st);
+    prof_begin(TAG_STAGE_AGG_DEV_FINAL, st);
     agg_dev_final<F, K, BF><<<(unsigned)((dev_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
+    prof_end(TAG_STAGE_AGG_DEV_FINAL, st);
 }
 
 template <int F, bool BF>
@@ -602,6 +633,7 @@ extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *
     {
         size_t sh_op = sizeof(float) * dims->f_op * F, sh_dev = sizeof(float) * dims->f_dev * F;
         unsigned b_op = (unsigned)((rows_op + 255) / 256), b_dev = (unsigned)((rows_dev + 255) / 256);
+        prof_begin(TAG_STAGE_ENCODE, stream);
         if (bf) {
             encode_rows<true><<<b_op, 256, sh_op, stream>>>(x->x_op, rows_op, dims->f_op, w->enc_op_w, w->enc_op_b, L.H_op[0], F);
             encode_rows<true><<<b_dev, 256, sh_dev, stream>>>(x->x_dev, rows_dev, dims->f_dev, w->enc_dev_w, w->enc_dev_b, L.H_dev[0], F);
@@ -609,6 +641,7 @@ extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *
             encode_rows<false><<<b_op, 256, sh_op, stream>>>(x->x_op, rows_op, dims->f_op, w->enc_op_w, w->enc_op_b, L.H_op[0], F);
             encode_rows<false><<<b_dev, 256, sh_dev, stream>>>(x->x_dev, rows_dev, dims->f_dev, w->enc_dev_w, w->enc_dev_b, L.H_dev[0], F);
         }
+        prof_end(TAG_STAGE_ENCODE, stream);
     }
     AggArgs A{};
     A.R = R;
@@ -625,20 +658,27 @@ extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *
         const int cur = l & 1, nxt = cur ^ 1;
         const bool last = (l == NL - 1);
         // relation transforms: op rows [W^h_oo ; W^h_od], device rows [W^h_dd ; W^h_od]
-        dim3 g_op((unsigned)((rows_op + TM - 1) / TM), (unsigned)(2 * F / TN));
-        dim3 g_dev((unsigned)((rows_dev + TM - 1) / TM), (unsigned)(2 * F / TN));
-        if (bf) {
-            const uint16_t *Wl = L.Wb + (size_t)l * 3 * F * F;
-            gemm_bf16<<<g_op, 256, 0, stream>>>(static_cast<const uint16_t *>(L.H_op[cur]), rows_op, F,
-                                               Wl + 0 * F * F, Wl + 1 * F * F, F, static_cast<uint16_t *>(L.Y_op));
-            gemm_bf16<<<g_dev, 256, 0, stream>>>(static_cast<const uint16_t *>(L.H_dev[cur]), rows_dev, F,
-                                                Wl + 2 * F * F, Wl + 1 * F * F, F, static_cast<uint16_t *>(L.Y_dev));
-        } else {
-            const float *Wl = w->layer_w + (size_t)l * 3 * F * 2 * F;
-            gemm_f32<<<g_op, 256, 0, stream>>>(static_cast<const float *>(L.H_op[cur]), rows_op, F,
-                                              Wl + 0 * F * 2 * F, Wl + 1 * F * 2 * F, 2 * F, static_cast<float *>(L.Y_op));
-            gemm_f32<<<g_dev, 256, 0, stream>>>(static_cast<const float *>(L.H_dev[cur]), rows_dev, F,
-                                               Wl + 2 * F * 2 * F, Wl + 1 * F * 2 * F, 2 * F, static_cast<float *>(L.Y_dev));
+        {
+            GemmArgs ga{};
+            ga.F = F;
+            ga.tiles0 = (rows_op + TM - 1) / TM;
+            const int64_t tiles1 = (rows_dev + TM - 1) / TM;
+            dim3 grid((unsigned)(ga.tiles0 + tiles1), (unsigned)(2 * F / TN));
+            if (bf) {
+                const uint16_t *Wl = L.Wb + (size_t)l * 3 * F * F;
+                ga.side[0] = GemmSide{L.H_op[cur], rows_op, Wl + 0 * F * F, Wl + 1 * F * F, F, L.Y_op};
+                ga.side[1] = GemmSide{L.H_dev[cur], rows_dev, Wl + 2 * F * F, Wl + 1 * F * F, F, L.Y_dev};
+                prof_begin(TAG_STAGE_TRANSFORM, stream);
+                gemm_bf16<<<grid, 256, 0, stream>>>(ga);
+                prof_end(TAG_STAGE_TRANSFORM, stream);
+            } else {
+                const float *Wl = w->layer_w + (size_t)l * 3 * F * 2 * F;
+                ga.side[0] = GemmSide{L.H_op[cur], rows_op, Wl + 0 * F * 2 * F, Wl + 1 * F * 2 * F, 2 * F, L.Y_op};
+                ga.side[1] = GemmSide{L.H_dev[cur], rows_dev, Wl + 2 * F * 2 * F, Wl + 1 * F * 2 * F, 2 * F, L.Y_dev};
+                prof_begin(TAG_STAGE_TRANSFORM, stream);
+                gemm_f32<<<grid, 256, 0, stream>>>(ga);
+                prof_end(TAG_STAGE_TRANSFORM, stream);
+            }
         }
         A.att_src = w->att_src + (size_t)l * 3 * F;
         A.att_dst = w->att_dst + (size_t)l * 3 * F;

@@ -354,6 +354,7 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
     BUILD_HIP(hipMemcpyAsync(tl.dd_off, desc->dd_off, sizeof(int64_t) * (s.G + 1), hipMemcpyHostToDevice, stream));
     BUILD_HIP(hipMemcpyAsync(tl.od_off, desc->od_off, sizeof(int64_t) * (s.G + 1), hipMemcpyHostToDevice, stream));
 
+    prof_begin(TAG_STAGE_GRAPH_BUILD, stream);
     for (int b = 0; b < 4; ++b)
         fill_i32<<<grid_for(s.rows[b] + 1), kThreads, 0, stream>>>(tl.cnt[b], s.rows[b] + 1, 0);
     fill_i32<<<1, kThreads, 0, stream>>>(tl.flags, FLAG_COUNT, 0);
@@ -384,6 +385,7 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
             rank_rows<<<(unsigned)((s.nnz[b] + kThreads - 1) / kThreads), kThreads, 0, stream>>>(
                 cl.rowptr[b], s.rows[b], tl.tcol[b], tl.teid[b], tl.rowof[b], s.nnz[b], cl.col[b], cl.eid[b],
                 tl.flags, b);
+    prof_end(TAG_STAGE_GRAPH_BUILD, stream);
     {
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return fail(TAG_EHIP, std::string("graph build launch: ") + hipGetErrorString(e));

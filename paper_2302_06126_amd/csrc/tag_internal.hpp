@@ -9,6 +9,7 @@
 #include <vector>
 
 #include "../../include/tag.h"
+#include "../../include/tag_profile.h"
 
 namespace tag {
 
@@ -31,6 +32,10 @@ void clear_error();
 
 // Check for a launch error right after enqueueing kernels.
 tag_status launch_status(const char *what);
+
+// Optional per-stage event timing (stage ids from include/tag_profile.h).
+void prof_begin(int stage, hipStream_t s);
+void prof_end(int stage, hipStream_t s);
 
 // ------------------------------------------------------------ memory plans
 inline size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
