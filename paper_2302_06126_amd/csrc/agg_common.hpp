@@ -1,0 +1,143 @@
+// Device helpers shared by the aggregation kernels (first-version path in
+// forward.hip, MFMA path in agg_mfma.hip).
+#pragma once
+
+#include "tag_internal.hpp"
+
+namespace tag {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kWaves = 4;        // wavefronts per aggregation block
+constexpr int kChunk = 256;      // entries per device<-op partial (first-version path)
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+
+// -------------------------------------------------------------- aggregation
+struct AggArgs {
+    int32_t R;
+    int64_t n_op, n_dev;
+    const int32_t *rp[4], *col[4], *eid[4];
+    const void *Y_op, *Y_dev;         // [R*n][2F]
+    const float *x_oo; int64_t s_oo;
+    const float *x_dd; int64_t s_dd;
+    const uint8_t *x_od; int64_t s_od;
+    const float *att_src, *att_dst;   // [3][F] of this layer
+    const float *U;                   // [3][F][2] of this layer
+    const float *cp;                  // [3][F] of this layer
+    float g_same, g_cross, slope;
+    void *H_op, *H_dev;               // outputs (bf16 hidden or fp32)
+    int out_f32;
+    float *part;                      // device<-op partials
+    int32_t maxc;                     // partial records per device row
+    // MFMA path
+    int32_t G, n_tiles;
+    const int32_t *tiles, *tile_off, *op_off, *dev_off;
+    uint64_t *omask;                  // [R*n_op][2]: present / placement-bit masks over local devices
+    float *Sdev;                      // [R*n_dev][4][K]: p0, p1, q_od, q_dd of device rows
+    float *T;                         // [R*n_dev][2][F]: device messages for bit 0 / 1
+    float *qop;                       // [R*n_op][K]: q_od of op rows
+    float *O0;                        // [R*n_op][F]: gamma_same * op<-op aggregate
+    int32_t rec_mode;                 // 0: records per 256-entry chunk, 1: per op tile
+};
+
+// MFMA path (agg_mfma.hip)
+bool mfma_path_supported(int F, int K);
+void launch_pack_masks(const AggArgs &A, hipStream_t st);
+bool launch_agg_mfma(int F, int K, bool bf, const AggArgs &A, hipStream_t st);
+
+template <int CPL, bool BF>
+__device__ __forceinline__ void load_ch(const void *base, int64_t off, float (&v)[CPL]) {
+    if (BF) {
+        const uint16_t *p = static_cast<const uint16_t *>(base) + off;
+        if (CPL == 4) {
+            uint2 q = *reinterpret_cast<const uint2 *>(p);
+            v[0] = bf2f(q.x & 0xffff); v[1] = bf2f(q.x >> 16);
+            v[2 % CPL] = bf2f(q.y & 0xffff); v[3 % CPL] = bf2f(q.y >> 16);
+        } else if (CPL == 2) {
+            uint32_t q = *reinterpret_cast<const uint32_t *>(p);
+            v[0] = bf2f(q & 0xffff); v[1 % CPL] = bf2f(q >> 16);
+        } else {
+            v[0] = bf2f(p[0]);
+        }
+    } else {
+        const float *p = static_cast<const float *>(base) + off;
+        if (CPL == 4) {
+            float4 q = *reinterpret_cast<const float4 *>(p);
+            v[0] = q.x; v[1] = q.y; v[2 % CPL] = q.z; v[3 % CPL] = q.w;
+        } else if (CPL == 2) {
+            float2 q = *reinterpret_cast<const float2 *>(p);
+            v[0] = q.x; v[1 % CPL] = q.y;
+        } else {
+            v[0] = p[0];
+        }
+    }
+}
+
+template <int LPH>
+__device__ __forceinline__ float head_sum(float v) {
+#pragma unroll
+    for (int o = LPH / 2; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// per-lane constants of one relation
+template <int CPL>
+struct RelConst {
+    float a[CPL], ad[CPL], u0[CPL], u1[CPL], cp[CPL];
+    __device__ void load(const AggArgs &A, int r, int F, int c0) {
+        for (int c = 0; c < CPL; ++c) {
+            a[c] = A.att_src[r * F + c0 + c];
+            ad[c] = A.att_dst[r * F + c0 + c];
+            u0[c] = A.U[((size_t)r * F + c0 + c) * 2 + 0];
+            u1[c] = A.U[((size_t)r * F + c0 + c) * 2 + 1];
+            cp[c] = A.cp[(size_t)r * F + c0 + c];
+        }
+    }
+};
+
+template <int CPL>
+struct Online {
+    float mx, den, acc[CPL];
+    __device__ void init() {
+        mx = -INFINITY; den = 0.f;
+        for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
+    }
+    // s2: score already multiplied by log2(e)
+    __device__ void push(float s2, const float (&m)[CPL]) {
+        float nm = fmaxf(mx, s2);
+        float sc = __builtin_amdgcn_exp2f(mx - nm);
+        float p = __builtin_amdgcn_exp2f(s2 - nm);
+        den = fmaf(den, sc, p);
+        for (int c = 0; c < CPL; ++c) acc[c] = fmaf(acc[c], sc, p * m[c]);
+        mx = nm;
+    }
+};
+
+// message + score of one entry; returns the log2-domain score
+template <int CPL, int LPH>
+__device__ __forceinline__ float entry_score(const float (&y)[CPL], float x0, float x1, const RelConst<CPL> &k,
+                                             float qd, float slope, float (&m)[CPL]) {
+    float part = 0.f;
+    for (int c = 0; c < CPL; ++c) {
+        float z = y[c] + fmaf(k.u0[c], x0, fmaf(k.u1[c], x1, k.cp[c]));
+        m[c] = fmaxf(z, 0.f);
+        part = fmaf(k.a[c], m[c], part);
+    }
+    float s = head_sum<LPH>(part) + qd;
+    return leaky(s, slope) * kLog2e;
+}
+
+template <int CPL, bool BF>
+__device__ __forceinline__ void store_row(void *base, int64_t off, bool f32, const float (&v)[CPL]) {
+    if (f32) {
+        float *p = static_cast<float *>(base) + off;
+        for (int c = 0; c < CPL; ++c) p[c] = v[c];
+    } else {
+        uint16_t *p = static_cast<uint16_t *>(base) + off;
+        for (int c = 0; c < CPL; ++c) p[c] = f2bf(v[c]);
+    }
+}
+
+
+}  // namespace tag

@@ -1,0 +1,408 @@
+// Attention aggregation on the matrix cores (heads of at least 16 channels).
+//
+// The placement links between ops and devices carry only a bit, so every
+// op<->device message is one of two rows per source node:
+//   m_b[v] = ReLU(W^h_od h_v + c'_od + b U_od),  b in {0, 1}
+// and its attention logit a . m_b[v] is a per-(source, bit, head) scalar.
+// Both op<->device aggregations are therefore dense contractions over a
+// 64-op tile of one topology:
+//   device <- op:  acc[j][c] = sum_{u, b} alpha_k(j, u, b) m_b[u][c]   (M x 128) x (128 x f)
+//   op <- device:  acc[u][c] = sum_{j, b} alpha_k(u, j, b) m_b[j][c]   (64 x 2M) x (2M x f)
+// with alpha = 0 unless (u, j) is a placement link whose bit is b.  They run
+// as fp32 MFMA 16x16x4 products; the attention weights are formed in
+// registers as the A operand.  device <- op tiles write (max, sum, partial)
+// records that a merge pass combines in tile order; op <- device rows are
+// complete inside one tile and are normalised directly.  The op <- op
+// bucket stays a wavefront-per-row gather.
+#include "agg_common.hpp"
+
+namespace tag {
+namespace {
+
+__device__ __forceinline__ int32_t owner32(const int32_t *off, int32_t G, int32_t i) {
+    int32_t lo = 0, hi = G;
+    while (hi - lo > 1) {
+        int32_t mid = (lo + hi) >> 1;
+        if (off[mid] <= i) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+// omask[r][u] = (present, bits) over the local devices of u's topology
+__global__ void pack_op_masks(AggArgs A) {
+    const int64_t n = (int64_t)A.R * A.n_op;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t r = (int32_t)(i / A.n_op), u = (int32_t)(i % A.n_op);
+        const int32_t d0 = A.dev_off[owner32(A.op_off, A.G, u)];
+        const uint8_t *xb = A.x_od + (int64_t)r * A.s_od;
+        uint64_t pres = 0, bits = 0;
+        for (int32_t e = A.rp[1][u]; e < A.rp[1][u + 1]; ++e) {
+            const int32_t j = A.col[1][e] - d0;
+            pres |= 1ull << j;
+            if (xb[A.eid[1][e]]) bits |= 1ull << j;
+        }
+        A.omask[2 * i] = pres;
+        A.omask[2 * i + 1] = bits;
+    }
+}
+
+// per device row: message table T (bit 0 / 1), their logits p0, p1, and the
+// destination terms q_od, q_dd
+template <int F, int K, bool BF>
+__global__ void __launch_bounds__(256) dev_prep(AggArgs A) {
+    constexpr int CPL = F / 64, LPH = 64 / K;
+    const int lane = threadIdx.x & 63;
+    const int64_t i = (int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6);
+    if (i >= (int64_t)A.R * A.n_dev) return;
+    const int c0 = lane * CPL;
+    RelConst<CPL> od; od.load(A, 1, F, c0);
+    RelConst<CPL> dd; dd.load(A, 2, F, c0);
+    float yo[CPL], yd[CPL];
+    load_ch<CPL, BF>(A.Y_dev, i * 2 * F + F + c0, yo);
+    load_ch<CPL, BF>(A.Y_dev, i * 2 * F + c0, yd);
+    float p0 = 0.f, p1 = 0.f, qo = 0.f, qd = 0.f;
+    for (int c = 0; c < CPL; ++c) {
+        const float yc = yo[c] + od.cp[c];
+        const float t0 = fmaxf(yc, 0.f), t1 = fmaxf(yc + od.u0[c], 0.f);
+        A.T[(i * 2 + 0) * F + c0 + c] = t0;
+        A.T[(i * 2 + 1) * F + c0 + c] = t1;
+        p0 = fmaf(od.a[c], t0, p0);
+        p1 = fmaf(od.a[c], t1, p1);
+        qo = fmaf(od.ad[c], yo[c], qo);
+        qd = fmaf(dd.ad[c], yd[c], qd);
+    }
+    p0 = head_sum<LPH>(p0); p1 = head_sum<LPH>(p1);
+    qo = head_sum<LPH>(qo); qd = head_sum<LPH>(qd);
+    if ((lane % LPH) == 0) {
+        const int h = lane / LPH;
+        float *S = A.Sdev + i * 4 * K;
+        S[h] = p0; S[K + h] = p1; S[2 * K + h] = qo; S[3 * K + h] = qd;
+    }
+}
+
+// op <- op: one wavefront per op row, up to four neighbour rows in flight;
+// writes gamma_same * aggregate to O0 (fp32)
+template <int F, int K, bool BF>
+__global__ void __launch_bounds__(256) agg_b0(AggArgs A) {
+    constexpr int CPL = F / 64, LPH = 64 / K;
+    const int lane = threadIdx.x & 63;
+    const int64_t w = (int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6);
+    if (w >= (int64_t)A.R * A.n_op) return;
+    const int32_t rep = (int32_t)(w / A.n_op);
+    const int32_t u = (int32_t)(w % A.n_op);
+    const int c0 = lane * CPL;
+    RelConst<CPL> k; k.load(A, 0, F, c0);
+    float yd[CPL]; load_ch<CPL, BF>(A.Y_op, w * 2 * F + c0, yd);
+    float q = 0.f;
+    for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], yd[c], q);
+    q = head_sum<LPH>(q);
+    Online<CPL> o; o.init();
+    const int32_t beg = A.rp[0][u], end = A.rp[0][u + 1];
+    const float *xo = A.x_oo + (int64_t)rep * A.s_oo;
+    const int64_t ybase = (int64_t)rep * A.n_op * 2 * F + c0;
+    for (int32_t e = beg; e < end; e += 4) {
+        const int n = min(4, end - e);
+        int32_t v[4], id[4];
+        for (int i = 0; i < 4; ++i) {
+            v[i] = i < n ? A.col[0][e + i] : 0;
+            id[i] = i < n ? A.eid[0][e + i] : 0;
+        }
+        float x[4], y[4][CPL];
+        for (int i = 0; i < 4; ++i) {
+            x[i] = i < n ? xo[id[i]] : 0.f;
+            if (i < n) load_ch<CPL, BF>(A.Y_op, ybase + (int64_t)v[i] * 2 * F, y[i]);
+        }
+        for (int i = 0; i < 4; ++i) {
+            if (i < n) {
+                float m[CPL];
+                const float s2 = entry_score<CPL, LPH>(y[i], x[i], 0.f, k, q, A.slope, m);
+                o.push(s2, m);
+            }
+        }
+    }
+    float *out = A.O0 + w * F + c0;
+    if (end > beg) {
+        const float inv = A.g_same / o.den;
+        for (int c = 0; c < CPL; ++c) out[c] = o.acc[c] * inv;
+    } else {
+        for (int c = 0; c < CPL; ++c) out[c] = 0.f;
+    }
+}
+
+// device <- op over one 64-op tile: partial (max, sum, accumulator) records
+template <int F, int K, bool BF>
+__global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
+    constexpr int D = F / K;                       // head width (>= 16 here)
+    constexpr int WC = F / 4;                      // columns per wavefront
+    constexpr int NCB = WC / 16;                   // 16-column blocks per wavefront
+    constexpr int HPW = WC >= D ? WC / D : 1;      // heads per wavefront
+    constexpr int YS = F + 4;                      // padded LDS row
+    __shared__ float Ys[kOpTile * YS];
+    __shared__ uint64_t pres[kOpTile], bits[kOpTile];
+    __shared__ float pb[kOpTile][2][K];
+    __shared__ float qd[64][K], mxS[64][K], zS[64][K];
+    __shared__ float cpS[F], US[F], aS[F], adS[F];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int32_t t = blockIdx.x, r = blockIdx.y;
+    const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1], g = A.tiles[3 * t + 2];
+    const int32_t d0 = A.dev_off[g], Mg = A.dev_off[g + 1] - d0;
+    const int32_t chunk = t - A.tile_off[g];
+
+    for (int i = tid; i < F; i += 256) {
+        cpS[i] = A.cp[F + i];
+        US[i] = A.U[(size_t)(F + i) * 2];
+        aS[i] = A.att_src[F + i];
+        adS[i] = A.att_dst[F + i];
+    }
+    for (int i = tid; i < kOpTile; i += 256) {
+        const bool ok = i < nu;
+        const int64_t mi = 2 * ((int64_t)r * A.n_op + u0 + i);
+        pres[i] = ok ? A.omask[mi] : 0ull;
+        bits[i] = ok ? A.omask[mi + 1] : 0ull;
+    }
+    for (int i = tid; i < 64 * K; i += 256) {
+        const int j = i / K, h = i % K;
+        qd[j][h] = j < Mg ? A.Sdev[((int64_t)r * A.n_dev + d0 + j) * 4 * K + 2 * K + h] : 0.f;
+    }
+    for (int i = tid; i < kOpTile * (F / 4); i += 256) {
+        const int u = i / (F / 4), c = (i % (F / 4)) * 4;
+        float v[4] = {0.f, 0.f, 0.f, 0.f};
+        if (u < nu) load_ch<4, BF>(A.Y_op, ((int64_t)r * A.n_op + u0 + u) * 2 * F + F + c, v);
+        for (int q = 0; q < 4; ++q) Ys[u * YS + c + q] = v[q];
+    }
+    __syncthreads();
+    // op-side logits of both message variants, and q_od of the op rows
+    for (int i = tid; i < kOpTile * K; i += 256) {
+        const int u = i / K, h = i % K;
+        float p0 = 0.f, p1 = 0.f, q = 0.f;
+        for (int c = h * D; c < (h + 1) * D; ++c) {
+            const float y = Ys[u * YS + c];
+            const float yc = y + cpS[c];
+            p0 = fmaf(aS[c], fmaxf(yc, 0.f), p0);
+            p1 = fmaf(aS[c], fmaxf(yc + US[c], 0.f), p1);
+            q = fmaf(adS[c], y, q);
+        }
+        pb[u][0][h] = p0;
+        pb[u][1][h] = p1;
+        if (u < nu) A.qop[((int64_t)r * A.n_op + u0 + u) * K + h] = q;
+    }
+    __syncthreads();
+    // per (device, head): max and sum of exp over the tile's links
+    for (int i = tid; i < Mg * K; i += 256) {
+        const int j = i / K, h = i % K;
+        float mx = -INFINITY;
+        for (int u = 0; u < nu; ++u)
+            if ((pres[u] >> j) & 1ull) {
+                const int b = (int)((bits[u] >> j) & 1ull);
+                mx = fmaxf(mx, leaky(pb[u][b][h] + qd[j][h], A.slope) * kLog2e);
+            }
+        float z = 0.f;
+        for (int u = 0; u < nu; ++u)
+            if ((pres[u] >> j) & 1ull) {
+                const int b = (int)((bits[u] >> j) & 1ull);
+                z += __builtin_amdgcn_exp2f(leaky(pb[u][b][h] + qd[j][h], A.slope) * kLog2e - mx);
+            }
+        mxS[j][h] = mx;
+        zS[j][h] = z;
+    }
+    __syncthreads();
+
+    const int cbase = wave * WC;
+    const int h0 = cbase / D;
+    constexpr int CPH = NCB / HPW;                 // column blocks per head inside a wavefront
+    float cpv[NCB], Uv[NCB];
+    for (int cb = 0; cb < NCB; ++cb) {
+        const int col = cbase + cb * 16 + (lane & 15);
+        cpv[cb] = cpS[col];
+        Uv[cb] = US[col];
+    }
+    const int NRB = (Mg + 15) / 16;
+    f4 acc[4][NCB];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) acc[rb][cb] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < kOpTile / 2; ++s) {
+        const int ul = 2 * s + (lane >> 5);
+        const int b = (lane >> 4) & 1;
+        const uint64_t pr = pres[ul], bt = bits[ul];
+        float bv[NCB];
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+            const float yc = Ys[ul * YS + cbase + cb * 16 + (lane & 15)] + cpv[cb];
+            bv[cb] = fmaxf(b ? yc + Uv[cb] : yc, 0.f);
+        }
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb) {
+            if (rb < NRB) {
+                const int j = rb * 16 + (lane & 15);
+                const bool on = j < Mg && ((pr >> j) & 1ull) && ((int)((bt >> j) & 1ull) == b);
+#pragma unroll
+                for (int hh = 0; hh < HPW; ++hh) {
+                    const int h = h0 + hh;
+                    const float af = on ? __builtin_amdgcn_exp2f(leaky(pb[ul][b][h] + qd[j][h], A.slope) * kLog2e - mxS[j][h])
+                                        : 0.f;
+#pragma unroll
+                    for (int c2 = 0; c2 < CPH; ++c2)
+                        acc[rb][hh * CPH + c2] =
+                            __builtin_amdgcn_mfma_f32_16x16x4f32(af, bv[hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
+                }
+            }
+        }
+    }
+    const int REC = F + 2 * K;
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int j = rb * 16 + 4 * (lane >> 4) + v;
+            if (rb < NRB && j < Mg) {
+                float *rec = A.part + (((int64_t)r * A.n_dev + d0 + j) * A.maxc + chunk) * REC + 2 * K;
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb) rec[cbase + cb * 16 + (lane & 15)] = acc[rb][cb][v];
+            }
+        }
+    for (int i = tid; i < Mg * K; i += 256) {
+        const int j = i / K, h = i % K;
+        float *rec = A.part + (((int64_t)r * A.n_dev + d0 + j) * A.maxc + chunk) * REC;
+        rec[h] = mxS[j][h];
+        rec[K + h] = zS[j][h];
+    }
+}
+
+// op <- device over one 64-op tile, plus the op <- op part from O0
+template <int F, int K, bool BF>
+__global__ void __launch_bounds__(256) agg_b1(AggArgs A) {
+    constexpr int D = F / K;
+    constexpr int WC = F / 4;
+    constexpr int NCB = WC / 16;
+    constexpr int HPW = WC >= D ? WC / D : 1;
+    __shared__ uint64_t pres[kOpTile], bits[kOpTile];
+    __shared__ float qo[kOpTile][K], mxS[kOpTile][K], izS[kOpTile][K];
+    __shared__ float P[64][2][K];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int32_t t = blockIdx.x, r = blockIdx.y;
+    const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1], g = A.tiles[3 * t + 2];
+    const int32_t d0 = A.dev_off[g], Mg = A.dev_off[g + 1] - d0;
+    for (int i = tid; i < kOpTile; i += 256) {
+        const bool ok = i < nu;
+        const int64_t mi = 2 * ((int64_t)r * A.n_op + u0 + i);
+        pres[i] = ok ? A.omask[mi] : 0ull;
+        bits[i] = ok ? A.omask[mi + 1] : 0ull;
+    }
+    for (int i = tid; i < kOpTile * K; i += 256) {
+        const int u = i / K, h = i % K;
+        qo[u][h] = u < nu ? A.qop[((int64_t)r * A.n_op + u0 + u) * K + h] : 0.f;
+    }
+    for (int i = tid; i < 64 * 2 * K; i += 256) {
+        const int j = i / (2 * K), bh = i % (2 * K);
+        P[j][bh / K][bh % K] = j < Mg ? A.Sdev[((int64_t)r * A.n_dev + d0 + j) * 4 * K + bh] : 0.f;
+    }
+    __syncthreads();
+    for (int i = tid; i < kOpTile * K; i += 256) {
+        const int u = i / K, h = i % K;
+        const uint64_t pr = pres[u], bt = bits[u];
+        float mx = -INFINITY;
+        for (int j = 0; j < Mg; ++j)
+            if ((pr >> j) & 1ull) mx = fmaxf(mx, leaky(P[j][(bt >> j) & 1ull][h] + qo[u][h], A.slope) * kLog2e);
+        float z = 0.f;
+        for (int j = 0; j < Mg; ++j)
+            if ((pr >> j) & 1ull)
+                z += __builtin_amdgcn_exp2f(leaky(P[j][(bt >> j) & 1ull][h] + qo[u][h], A.slope) * kLog2e - mx);
+        mxS[u][h] = mx;
+        izS[u][h] = z > 0.f ? 1.f / z : 0.f;
+    }
+    __syncthreads();
+
+    const int cbase = wave * WC;
+    const int h0 = cbase / D;
+    constexpr int CPH = NCB / HPW;
+    f4 acc[4][NCB];
+    for (int rb = 0; rb < 4; ++rb)
+        for (int cb = 0; cb < NCB; ++cb) acc[rb][cb] = f4{0.f, 0.f, 0.f, 0.f};
+    const float *Tb = A.T + ((int64_t)r * A.n_dev + d0) * 2 * F;
+    const int steps = (Mg + 1) / 2;
+    for (int s = 0; s < steps; ++s) {
+        const int j = 2 * s + (lane >> 5);
+        const int b = (lane >> 4) & 1;
+        const bool jok = j < Mg;
+        float bv[NCB];
+        for (int cb = 0; cb < NCB; ++cb)
+            bv[cb] = jok ? Tb[((int64_t)j * 2 + b) * F + cbase + cb * 16 + (lane & 15)] : 0.f;
+        for (int rb = 0; rb < 4; ++rb) {
+            const int u = rb * 16 + (lane & 15);
+            const bool on = jok && ((pres[u] >> j) & 1ull) && ((int)((bits[u] >> j) & 1ull) == b);
+#pragma unroll
+            for (int hh = 0; hh < HPW; ++hh) {
+                const int h = h0 + hh;
+                const float af = on ? __builtin_amdgcn_exp2f(leaky(P[j][b][h] + qo[u][h], A.slope) * kLog2e - mxS[u][h]) *
+                                          izS[u][h]
+                                    : 0.f;
+#pragma unroll
+                for (int c2 = 0; c2 < CPH; ++c2)
+                    acc[rb][hh * CPH + c2] =
+                        __builtin_amdgcn_mfma_f32_16x16x4f32(af, bv[hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
+            }
+        }
+    }
+    for (int rb = 0; rb < 4; ++rb)
+        for (int v = 0; v < 4; ++v) {
+            const int u = rb * 16 + 4 * (lane >> 4) + v;
+            if (u >= nu) continue;
+            const int64_t row = (int64_t)r * A.n_op + u0 + u;
+            for (int cb = 0; cb < NCB; ++cb) {
+                const int col = cbase + cb * 16 + (lane & 15);
+                const float val = fmaf(A.g_cross, acc[rb][cb][v], A.O0[row * F + col]);
+                if (A.out_f32) static_cast<float *>(A.H_op)[row * F + col] = val;
+                else static_cast<uint16_t *>(A.H_op)[row * F + col] = f2bf(val);
+            }
+        }
+}
+
+template <int F, int K, bool BF>
+void launch_mfma(const AggArgs &A, hipStream_t st) {
+    const int64_t op_waves = (int64_t)A.R * A.n_op;
+    const int64_t dev_waves = (int64_t)A.R * A.n_dev;
+    const dim3 tiles((unsigned)A.n_tiles, (unsigned)A.R);
+    dev_prep<F, K, BF><<<(unsigned)((dev_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
+    prof_begin(TAG_STAGE_AGG_DEV_PART, st);
+    agg_b2<F, K, BF><<<tiles, 256, 0, st>>>(A);
+    prof_end(TAG_STAGE_AGG_DEV_PART, st);
+    prof_begin(TAG_STAGE_AGG_OP, st);
+    agg_b0<F, K, BF><<<(unsigned)((op_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
+    agg_b1<F, K, BF><<<tiles, 256, 0, st>>>(A);
+    prof_end(TAG_STAGE_AGG_OP, st);
+}
+
+template <int F, bool BF>
+bool dispatch_mfma_heads(int K, const AggArgs &A, hipStream_t st) {
+    switch (K) {
+        case 1: launch_mfma<F, 1, BF>(A, st); return true;
+        case 2: launch_mfma<F, 2, BF>(A, st); return true;
+        case 4: launch_mfma<F, 4, BF>(A, st); return true;
+        case 8: if (F / 8 >= 16) { launch_mfma<F, (F / 8 >= 16 ? 8 : 4), BF>(A, st); return true; } return false;
+        case 16: if (F / 16 >= 16) { launch_mfma<F, (F / 16 >= 16 ? 16 : 4), BF>(A, st); return true; } return false;
+        default: return false;
+    }
+}
+
+}  // namespace
+
+bool mfma_path_supported(int F, int K) { return K >= 1 && F / K >= 16 && K <= 16; }
+
+void launch_pack_masks(const AggArgs &A, hipStream_t st) {
+    const int64_t n = (int64_t)A.R * A.n_op;
+    const unsigned blocks = (unsigned)std::max<int64_t>(1, std::min<int64_t>((n + 255) / 256, 1 << 16));
+    pack_op_masks<<<blocks, 256, 0, st>>>(A);
+}
+
+bool launch_agg_mfma(int F, int K, bool bf, const AggArgs &A, hipStream_t st) {
+    if (!mfma_path_supported(F, K)) return false;
+    if (F == 64) return bf ? dispatch_mfma_heads<64, true>(K, A, st) : dispatch_mfma_heads<64, false>(K, A, st);
+    if (F == 128) return bf ? dispatch_mfma_heads<128, true>(K, A, st) : dispatch_mfma_heads<128, false>(K, A, st);
+    return bf ? dispatch_mfma_heads<256, true>(K, A, st) : dispatch_mfma_heads<256, false>(K, A, st);
+}
+
+}  // namespace tag

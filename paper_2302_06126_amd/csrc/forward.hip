@@ -21,17 +21,10 @@
 //    fixed order, so results do not depend on scheduling.
 #include <algorithm>
 
-#include "tag_internal.hpp"
+#include "agg_common.hpp"
 
 namespace tag {
 namespace {
-
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kWaves = 4;        // wavefronts per aggregation block
-constexpr int kChunk = 256;      // entries per device<-op partial
-
-typedef float f4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 
 // ------------------------------------------------------------------ folding
 // U[l][r][c][t] = sum_k W^e[c][k] A_r[k][t];  cp[l][r][c] = b[c] + sum_k W^e[c][k] c_r[k]
@@ -71,32 +64,6 @@ __global__ void convert_wh_bf16(const float *layer_w, uint16_t *Wb, int F, int L
         int64_t rem = i % ((int64_t)F * F);
         int64_t n = rem / F, k = rem % F;
         Wb[i] = f2bf(layer_w[(lr * F + n) * 2 * F + k]);
-    }
-}
-
-// ----------------------------------------------------------------- encoders
-// out[row][c] = ReLU(b[c] + sum_t W[c][t] x[row][t]); W^T staged in LDS.
-template <bool OUT_BF16>
-__global__ void encode_rows(const float *__restrict__ x, int64_t rows, int fin,
-                            const float *__restrict__ W, const float *__restrict__ b,
-                            void *out, int F) {
-    extern __shared__ float wt[];   // [fin][F]
-    for (int i = threadIdx.x; i < fin * F; i += blockDim.x) {
-        int t = i / F, c = i % F;
-        wt[i] = W[(size_t)c * fin + t];
-    }
-    __syncthreads();
-    const int c = threadIdx.x % F;
-    const int rstep = blockDim.x / F;
-    const float bc = b[c];
-    const int64_t r0 = (int64_t)blockIdx.x * 256;
-    for (int64_t r = r0 + threadIdx.x / F; r < std::min<int64_t>(r0 + 256, rows); r += rstep) {
-        const float *xr = x + r * fin;
-        float s = bc;
-        for (int t = 0; t < fin; ++t) s = fmaf(wt[t * F + c], xr[t], s);
-        s = fmaxf(s, 0.f);
-        if (OUT_BF16) static_cast<uint16_t *>(out)[r * F + c] = f2bf(s);
-        else static_cast<float *>(out)[r * F + c] = s;
     }
 }
 
@@ -225,118 +192,6 @@ __global__ void __launch_bounds__(256) gemm_bf16(GemmArgs G) {
             }
 }
 
-// -------------------------------------------------------------- aggregation
-struct AggArgs {
-    int32_t R;
-    int64_t n_op, n_dev;
-    const int32_t *rp[4], *col[4], *eid[4];
-    const void *Y_op, *Y_dev;         // [R*n][2F]
-    const float *x_oo; int64_t s_oo;
-    const float *x_dd; int64_t s_dd;
-    const uint8_t *x_od; int64_t s_od;
-    const float *att_src, *att_dst;   // [3][F] of this layer
-    const float *U;                   // [3][F][2] of this layer
-    const float *cp;                  // [3][F] of this layer
-    float g_same, g_cross, slope;
-    void *H_op, *H_dev;               // outputs (bf16 hidden or fp32)
-    int out_f32;
-    float *part;                      // device<-op partials
-    int32_t maxc;                     // chunks per device row
-};
-
-template <int CPL, bool BF>
-__device__ __forceinline__ void load_ch(const void *base, int64_t off, float (&v)[CPL]) {
-    if (BF) {
-        const uint16_t *p = static_cast<const uint16_t *>(base) + off;
-        if (CPL == 4) {
-            uint2 q = *reinterpret_cast<const uint2 *>(p);
-            v[0] = bf2f(q.x & 0xffff); v[1] = bf2f(q.x >> 16);
-            v[2 % CPL] = bf2f(q.y & 0xffff); v[3 % CPL] = bf2f(q.y >> 16);
-        } else if (CPL == 2) {
-            uint32_t q = *reinterpret_cast<const uint32_t *>(p);
-            v[0] = bf2f(q & 0xffff); v[1 % CPL] = bf2f(q >> 16);
-        } else {
-            v[0] = bf2f(p[0]);
-        }
-    } else {
-        const float *p = static_cast<const float *>(base) + off;
-        if (CPL == 4) {
-            float4 q = *reinterpret_cast<const float4 *>(p);
-            v[0] = q.x; v[1] = q.y; v[2 % CPL] = q.z; v[3 % CPL] = q.w;
-        } else if (CPL == 2) {
-            float2 q = *reinterpret_cast<const float2 *>(p);
-            v[0] = q.x; v[1 % CPL] = q.y;
-        } else {
-            v[0] = p[0];
-        }
-    }
-}
-
-template <int LPH>
-__device__ __forceinline__ float head_sum(float v) {
-#pragma unroll
-    for (int o = LPH / 2; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
-}
-
-// per-lane constants of one relation
-template <int CPL>
-struct RelConst {
-    float a[CPL], ad[CPL], u0[CPL], u1[CPL], cp[CPL];
-    __device__ void load(const AggArgs &A, int r, int F, int c0) {
-        for (int c = 0; c < CPL; ++c) {
-            a[c] = A.att_src[r * F + c0 + c];
-            ad[c] = A.att_dst[r * F + c0 + c];
-            u0[c] = A.U[((size_t)r * F + c0 + c) * 2 + 0];
-            u1[c] = A.U[((size_t)r * F + c0 + c) * 2 + 1];
-            cp[c] = A.cp[(size_t)r * F + c0 + c];
-        }
-    }
-};
-
-template <int CPL>
-struct Online {
-    float mx, den, acc[CPL];
-    __device__ void init() {
-        mx = -INFINITY; den = 0.f;
-        for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
-    }
-    // s2: score already multiplied by log2(e)
-    __device__ void push(float s2, const float (&m)[CPL]) {
-        float nm = fmaxf(mx, s2);
-        float sc = __builtin_amdgcn_exp2f(mx - nm);
-        float p = __builtin_amdgcn_exp2f(s2 - nm);
-        den = fmaf(den, sc, p);
-        for (int c = 0; c < CPL; ++c) acc[c] = fmaf(acc[c], sc, p * m[c]);
-        mx = nm;
-    }
-};
-
-// message + score of one entry; returns the log2-domain score
-template <int CPL, int LPH>
-__device__ __forceinline__ float entry_score(const float (&y)[CPL], float x0, float x1, const RelConst<CPL> &k,
-                                             float qd, float slope, float (&m)[CPL]) {
-    float part = 0.f;
-    for (int c = 0; c < CPL; ++c) {
-        float z = y[c] + fmaf(k.u0[c], x0, fmaf(k.u1[c], x1, k.cp[c]));
-        m[c] = fmaxf(z, 0.f);
-        part = fmaf(k.a[c], m[c], part);
-    }
-    float s = head_sum<LPH>(part) + qd;
-    return leaky(s, slope) * kLog2e;
-}
-
-template <int CPL, bool BF>
-__device__ __forceinline__ void store_row(void *base, int64_t off, bool f32, const float (&v)[CPL]) {
-    if (f32) {
-        float *p = static_cast<float *>(base) + off;
-        for (int c = 0; c < CPL; ++c) p[c] = v[c];
-    } else {
-        uint16_t *p = static_cast<uint16_t *>(base) + off;
-        for (int c = 0; c < CPL; ++c) p[c] = f2bf(v[c]);
-    }
-}
-
 // op destinations: B0 (op<-op) and B1 (op<-dev)
 template <int F, int K, bool BF>
 __global__ void __launch_bounds__(256) agg_op(AggArgs A) {
@@ -451,10 +306,18 @@ __global__ void __launch_bounds__(256) agg_dev_final(AggArgs A) {
     const int head = lane / LPH;
     float out[CPL];
     for (int c = 0; c < CPL; ++c) out[c] = 0.f;
-    {   // B2 merge in chunk order
+    {   // B2 merge in record order (records with a zero sum hold no links)
         const int32_t deg = A.rp[2][j + 1] - A.rp[2][j];
-        const int32_t nch = (deg + kChunk - 1) / kChunk;
-        if (nch > 0) {
+        int32_t nch = (deg + kChunk - 1) / kChunk;
+        if (A.rec_mode) {
+            int32_t lo = 0, hi = A.G;
+            while (hi - lo > 1) {
+                const int32_t mid = (lo + hi) >> 1;
+                if (A.dev_off[mid] <= j) lo = mid; else hi = mid;
+            }
+            nch = A.tile_off[lo + 1] - A.tile_off[lo];
+        }
+        if (deg > 0 && nch > 0) {
             const float *p0 = A.part + ((int64_t)rep * A.n_dev + j) * A.maxc * (F + 2 * K);
             float M = -INFINITY;
             for (int32_t c = 0; c < nch; ++c) M = fmaxf(M, p0[(int64_t)c * (F + 2 * K) + head]);
@@ -504,6 +367,9 @@ struct FwdLayout {
     void *Y_op, *Y_dev;
     float *part;
     int32_t maxc;
+    bool mfma;
+    uint64_t *omask;
+    float *Sdev, *T, *qop, *O0;
 };
 
 tag_status check_dims(const tag_model_dims *d) {
@@ -535,8 +401,20 @@ size_t carve_fwd(const tag_graph *g, const tag_model_dims *d, int32_t R, void *b
     }
     L->Y_op = c.take<char>((size_t)R * g->n_op * 2 * F * es);
     L->Y_dev = c.take<char>((size_t)R * g->n_dev * 2 * F * es);
-    L->maxc = std::max<int32_t>(1, (g->max_degree[2] + kChunk - 1) / kChunk);
+    L->mfma = mfma_path_supported(F, d->heads);
+    L->maxc = L->mfma ? std::max<int32_t>(1, g->max_tiles)
+                      : std::max<int32_t>(1, (g->max_degree[2] + kChunk - 1) / kChunk);
     L->part = c.take<float>((size_t)R * g->n_dev * L->maxc * (F + 2 * d->heads));
+    if (L->mfma) {
+        L->omask = c.take<uint64_t>((size_t)R * g->n_op * 2);
+        L->Sdev = c.take<float>((size_t)R * g->n_dev * 4 * d->heads);
+        L->T = c.take<float>((size_t)R * g->n_dev * 2 * F);
+        L->qop = c.take<float>((size_t)R * g->n_op * d->heads);
+        L->O0 = c.take<float>((size_t)R * g->n_op * F);
+    } else {
+        L->omask = nullptr;
+        L->Sdev = L->T = L->qop = L->O0 = nullptr;
+    }
     return c.used;
 }
 
@@ -551,30 +429,45 @@ void launch_agg(const AggArgs &A, hipStream_t st) {
     prof_begin(TAG_STAGE_AGG_DEV_PART, st);
     agg_dev_part<F, K, BF><<<(unsigned)((part_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
     prof_end(TAG_STAGE_AGG_DEV_PART, st);
+    (void)dev_waves;
+}
+
+template <int F, int K, bool BF>
+void launch_dev_final(const AggArgs &A, hipStream_t st) {
+    const int64_t dev_waves = (int64_t)A.R * A.n_dev;
     prof_begin(TAG_STAGE_AGG_DEV_FINAL, st);
     agg_dev_final<F, K, BF><<<(unsigned)((dev_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
     prof_end(TAG_STAGE_AGG_DEV_FINAL, st);
 }
 
+// first-version aggregation (used when heads are narrower than 16 channels),
+// then the device merge + dev<-dev pass shared by both paths
+template <int F, int K, bool BF>
+void launch_layer(bool mfma, const AggArgs &A, hipStream_t st) {
+    if (!mfma) launch_agg<F, K, BF>(A, st);
+    else launch_agg_mfma(F, K, BF, A, st);
+    launch_dev_final<F, K, BF>(A, st);
+}
+
 template <int F, bool BF>
-tag_status dispatch_heads(int K, const AggArgs &A, hipStream_t st) {
+tag_status dispatch_heads(int K, bool mfma, const AggArgs &A, hipStream_t st) {
     switch (K) {
-        case 1: launch_agg<F, 1, BF>(A, st); break;
-        case 2: launch_agg<F, 2, BF>(A, st); break;
-        case 4: launch_agg<F, 4, BF>(A, st); break;
-        case 8: launch_agg<F, 8, BF>(A, st); break;
-        case 16: launch_agg<F, 16, BF>(A, st); break;
-        case 32: launch_agg<F, 32, BF>(A, st); break;
-        case 64: launch_agg<F, 64, BF>(A, st); break;
+        case 1: launch_layer<F, 1, BF>(mfma, A, st); break;
+        case 2: launch_layer<F, 2, BF>(mfma, A, st); break;
+        case 4: launch_layer<F, 4, BF>(mfma, A, st); break;
+        case 8: launch_layer<F, 8, BF>(mfma, A, st); break;
+        case 16: launch_layer<F, 16, BF>(mfma, A, st); break;
+        case 32: launch_layer<F, 32, BF>(mfma, A, st); break;
+        case 64: launch_layer<F, 64, BF>(mfma, A, st); break;
         default: TAG_FAIL(TAG_ESHAPE, "unsupported head count");
     }
     return TAG_OK;
 }
 
-tag_status dispatch_agg(int F, int K, bool bf, const AggArgs &A, hipStream_t st) {
-    if (F == 64) return bf ? dispatch_heads<64, true>(K, A, st) : dispatch_heads<64, false>(K, A, st);
-    if (F == 128) return bf ? dispatch_heads<128, true>(K, A, st) : dispatch_heads<128, false>(K, A, st);
-    return bf ? dispatch_heads<256, true>(K, A, st) : dispatch_heads<256, false>(K, A, st);
+tag_status dispatch_agg(int F, int K, bool bf, bool mfma, const AggArgs &A, hipStream_t st) {
+    if (F == 64) return bf ? dispatch_heads<64, true>(K, mfma, A, st) : dispatch_heads<64, false>(K, mfma, A, st);
+    if (F == 128) return bf ? dispatch_heads<128, true>(K, mfma, A, st) : dispatch_heads<128, false>(K, mfma, A, st);
+    return bf ? dispatch_heads<256, true>(K, mfma, A, st) : dispatch_heads<256, false>(K, mfma, A, st);
 }
 
 }  // namespace
@@ -631,16 +524,14 @@ extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *
     // encoders: hidden h0 in the working precision
     const int64_t rows_op = (int64_t)R * g->n_op, rows_dev = (int64_t)R * g->n_dev;
     {
-        size_t sh_op = sizeof(float) * dims->f_op * F, sh_dev = sizeof(float) * dims->f_dev * F;
-        unsigned b_op = (unsigned)((rows_op + 255) / 256), b_dev = (unsigned)((rows_dev + 255) / 256);
+        // h0 = ReLU(A x + c) as a small-K MFMA GEMM per node type
+        SmallGemm eo{x->x_op, dims->f_op, rows_op, nullptr, dims->f_op, w->enc_op_w, dims->f_op, F,
+                     w->enc_op_b, 1, L.H_op[0], F, bf ? 1 : 0};
+        SmallGemm ed{x->x_dev, dims->f_dev, rows_dev, nullptr, dims->f_dev, w->enc_dev_w, dims->f_dev, F,
+                     w->enc_dev_b, 1, L.H_dev[0], F, bf ? 1 : 0};
         prof_begin(TAG_STAGE_ENCODE, stream);
-        if (bf) {
-            encode_rows<true><<<b_op, 256, sh_op, stream>>>(x->x_op, rows_op, dims->f_op, w->enc_op_w, w->enc_op_b, L.H_op[0], F);
-            encode_rows<true><<<b_dev, 256, sh_dev, stream>>>(x->x_dev, rows_dev, dims->f_dev, w->enc_dev_w, w->enc_dev_b, L.H_dev[0], F);
-        } else {
-            encode_rows<false><<<b_op, 256, sh_op, stream>>>(x->x_op, rows_op, dims->f_op, w->enc_op_w, w->enc_op_b, L.H_op[0], F);
-            encode_rows<false><<<b_dev, 256, sh_dev, stream>>>(x->x_dev, rows_dev, dims->f_dev, w->enc_dev_w, w->enc_dev_b, L.H_dev[0], F);
-        }
+        launch_small_gemm(eo, stream);
+        launch_small_gemm(ed, stream);
         prof_end(TAG_STAGE_ENCODE, stream);
     }
     AggArgs A{};
@@ -653,6 +544,11 @@ extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *
     A.x_od = x->x_od; A.s_od = x->stride_od;
     A.g_same = dims->gamma_same; A.g_cross = dims->gamma_cross; A.slope = dims->leaky_slope;
     A.part = L.part; A.maxc = L.maxc;
+    A.G = g->G; A.n_tiles = g->n_tiles;
+    A.tiles = g->tiles_d; A.tile_off = g->tile_off_d; A.op_off = g->op_off_d; A.dev_off = g->dev_off_d;
+    A.omask = L.omask; A.Sdev = L.Sdev; A.T = L.T; A.qop = L.qop; A.O0 = L.O0;
+    A.rec_mode = L.mfma ? 1 : 0;
+    if (L.mfma) launch_pack_masks(A, stream);
 
     for (int l = 0; l < NL; ++l) {
         const int cur = l & 1, nxt = cur ^ 1;
@@ -687,7 +583,7 @@ extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *
         A.H_op = last ? static_cast<void *>(E_op) : L.H_op[nxt];
         A.H_dev = last ? static_cast<void *>(E_dev) : L.H_dev[nxt];
         A.out_f32 = last ? 1 : (bf ? 0 : 1);
-        st = dispatch_agg(F, K, bf, A, stream);
+        st = dispatch_agg(F, K, bf, L.mfma, A, stream);
         if (st != TAG_OK) return st;
     }
     return launch_status("tag_gnn_forward");

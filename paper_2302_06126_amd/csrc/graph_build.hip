@@ -235,7 +235,14 @@ tag_status check_desc(const tag_graph_desc *d, Sizes *s) {
 struct CsrLayout {
     int32_t *rowptr[4], *col[4], *eid[4];
     int32_t *op_off, *dev_off;
+    int32_t *tiles, *tile_off;
 };
+
+int64_t count_tiles(const tag_graph_desc *d) {
+    int64_t n = 0;
+    for (int32_t g = 0; g < d->n_graphs; ++g) n += (d->n_op[g] + kOpTile - 1) / kOpTile;
+    return n;
+}
 struct TmpLayout {
     int32_t *cnt[4], *tcol[4], *teid[4], *rowof[4];
     int32_t *tile_sums;
@@ -243,7 +250,7 @@ struct TmpLayout {
     int64_t *oo_off, *dd_off, *od_off;
 };
 
-size_t carve_csr(const Sizes &s, void *base, CsrLayout *L) {
+size_t carve_csr(const Sizes &s, int64_t n_tiles, void *base, CsrLayout *L) {
     Carver c(base);
     for (int b = 0; b < 4; ++b) {
         L->rowptr[b] = c.take<int32_t>(s.rows[b] + 1);
@@ -252,6 +259,8 @@ size_t carve_csr(const Sizes &s, void *base, CsrLayout *L) {
     }
     L->op_off = c.take<int32_t>(s.G + 1);
     L->dev_off = c.take<int32_t>(s.G + 1);
+    L->tiles = c.take<int32_t>(3 * std::max<int64_t>(n_tiles, 1));
+    L->tile_off = c.take<int32_t>(s.G + 1);
     return c.used;
 }
 
@@ -298,7 +307,7 @@ extern "C" tag_status tag_graph_plan(const tag_graph_desc *desc, size_t *csr_byt
     if (st != TAG_OK) return st;
     CsrLayout cl;
     TmpLayout tl;
-    *csr_bytes = carve_csr(s, nullptr, &cl);
+    *csr_bytes = carve_csr(s, count_tiles(desc), nullptr, &cl);
     *tmp_bytes = carve_tmp(s, nullptr, &tl);
     return TAG_OK;
 }
@@ -315,9 +324,10 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
     if (!csr_buf || !tmp_buf) TAG_FAIL(TAG_EINVAL, "csr_buf and tmp_buf must be non-NULL");
     CsrLayout cl;
     TmpLayout tl;
-    if (carve_csr(s, nullptr, &cl) > csr_bytes) TAG_FAIL(TAG_ENOSPACE, "csr buffer too small (see tag_graph_plan)");
+    const int64_t n_tiles = count_tiles(desc);
+    if (carve_csr(s, n_tiles, nullptr, &cl) > csr_bytes) TAG_FAIL(TAG_ENOSPACE, "csr buffer too small (see tag_graph_plan)");
     if (carve_tmp(s, nullptr, &tl) > tmp_bytes) TAG_FAIL(TAG_ENOSPACE, "tmp buffer too small (see tag_graph_plan)");
-    carve_csr(s, csr_buf, &cl);
+    carve_csr(s, n_tiles, csr_buf, &cl);
     carve_tmp(s, tmp_buf, &tl);
     hipStream_t stream = static_cast<hipStream_t>(hip_stream);
 
@@ -334,6 +344,21 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
     }
     std::vector<int32_t> op_off32(g->op_off.begin(), g->op_off.end());
     std::vector<int32_t> dev_off32(g->dev_off.begin(), g->dev_off.end());
+    // op tiles never cross a topology boundary
+    std::vector<int32_t> tiles;
+    std::vector<int32_t> tile_off(s.G + 1, 0);
+    tiles.reserve(3 * n_tiles);
+    for (int32_t gi = 0; gi < s.G; ++gi) {
+        int32_t nt = 0;
+        for (int32_t u = 0; u < desc->n_op[gi]; u += kOpTile, ++nt) {
+            tiles.push_back(static_cast<int32_t>(g->op_off[gi]) + u);
+            tiles.push_back(std::min<int32_t>(kOpTile, desc->n_op[gi] - u));
+            tiles.push_back(gi);
+        }
+        tile_off[gi + 1] = tile_off[gi] + nt;
+        g->max_tiles = std::max(g->max_tiles, nt);
+    }
+    g->n_tiles = static_cast<int32_t>(n_tiles);
     for (int b = 0; b < 4; ++b) { g->rows[b] = s.rows[b]; g->nnz[b] = s.nnz[b]; }
     if (hipGetDevice(&g->device) != hipSuccess) g->device = 0;
 
@@ -350,6 +375,8 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
 
     BUILD_HIP(hipMemcpyAsync(cl.op_off, op_off32.data(), sizeof(int32_t) * (s.G + 1), hipMemcpyHostToDevice, stream));
     BUILD_HIP(hipMemcpyAsync(cl.dev_off, dev_off32.data(), sizeof(int32_t) * (s.G + 1), hipMemcpyHostToDevice, stream));
+    BUILD_HIP(hipMemcpyAsync(cl.tiles, tiles.data(), sizeof(int32_t) * tiles.size(), hipMemcpyHostToDevice, stream));
+    BUILD_HIP(hipMemcpyAsync(cl.tile_off, tile_off.data(), sizeof(int32_t) * (s.G + 1), hipMemcpyHostToDevice, stream));
     BUILD_HIP(hipMemcpyAsync(tl.oo_off, desc->oo_off, sizeof(int64_t) * (s.G + 1), hipMemcpyHostToDevice, stream));
     BUILD_HIP(hipMemcpyAsync(tl.dd_off, desc->dd_off, sizeof(int64_t) * (s.G + 1), hipMemcpyHostToDevice, stream));
     BUILD_HIP(hipMemcpyAsync(tl.od_off, desc->od_off, sizeof(int64_t) * (s.G + 1), hipMemcpyHostToDevice, stream));
@@ -403,6 +430,8 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
     }
     g->op_off_d = cl.op_off;
     g->dev_off_d = cl.dev_off;
+    g->tiles_d = cl.tiles;
+    g->tile_off_d = cl.tile_off;
     *out = g;
 #undef BUILD_HIP
     return TAG_OK;

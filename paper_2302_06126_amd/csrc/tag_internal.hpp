@@ -69,8 +69,34 @@ struct tag_graph {
     const int32_t *eid[4] = {nullptr, nullptr, nullptr, nullptr};
     const int32_t *op_off_d = nullptr;   // [G+1]
     const int32_t *dev_off_d = nullptr;  // [G+1]
+    // op tiles: runs of at most kOpTile consecutive ops of one topology
+    int32_t n_tiles = 0;                 // total over topologies
+    int32_t max_tiles = 0;               // largest per-topology tile count
+    const int32_t *tiles_d = nullptr;    // [n_tiles][3] = (first op (global), op count, topology)
+    const int32_t *tile_off_d = nullptr; // [G+1] first tile of each topology
     int device = 0;
 };
+
+namespace tag {
+constexpr int kOpTile = 64;
+
+// C[m][n] = act(bias[n] + sum_k A[row(m)][k] * B[n][k]) on MFMA (gemm_small.hip)
+struct SmallGemm {
+    const float *A;
+    int64_t lda, rows;
+    const int32_t *row_map;   // optional gather of A rows (negative: zero row)
+    int K;
+    const float *B;
+    int64_t ldb;
+    int N;
+    const float *bias;        // optional
+    int relu;
+    void *C;
+    int64_t ldc;
+    int c_bf16;
+};
+void launch_small_gemm(const SmallGemm &G, hipStream_t st);
+}
 
 // ----------------------------------------------------------- device helpers
 namespace tag {
