@@ -146,7 +146,7 @@ void tag_graph_destroy(tag_graph *g);
  *               bf16; attention and aggregation stay fp32.
  *   gamma_same  gamma for op-op and device-device links (paper: 1)
  *   gamma_cross gamma for op-device links (paper: 0.1)
- *   leaky_slope LeakyReLU slope of the attention score (GAT: 0.2)
+ *   leaky_slope LeakyReLU slope of the attention score, in [0, 1] (GAT: 0.2)
  */
 typedef struct tag_model_dims {
     int32_t f, heads, layers, f_op, f_dev, dec_hidden;

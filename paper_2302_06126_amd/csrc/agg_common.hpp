@@ -46,28 +46,37 @@ bool mfma_path_supported(int F, int K);
 void launch_pack_masks(const AggArgs &A, hipStream_t st);
 bool launch_agg_mfma(int F, int K, bool bf, const AggArgs &A, hipStream_t st);
 
+// CPL consecutive channels starting at element `off` (fp32 or bf16 storage);
+// CPL is 1, 2 or a multiple of 4, and `off` is a multiple of min(CPL, 4).
 template <int CPL, bool BF>
 __device__ __forceinline__ void load_ch(const void *base, int64_t off, float (&v)[CPL]) {
-    if (BF) {
+    static_assert(CPL == 1 || CPL == 2 || CPL % 4 == 0, "unsupported channels per lane");
+    if constexpr (BF) {
         const uint16_t *p = static_cast<const uint16_t *>(base) + off;
-        if (CPL == 4) {
-            uint2 q = *reinterpret_cast<const uint2 *>(p);
-            v[0] = bf2f(q.x & 0xffff); v[1] = bf2f(q.x >> 16);
-            v[2 % CPL] = bf2f(q.y & 0xffff); v[3 % CPL] = bf2f(q.y >> 16);
-        } else if (CPL == 2) {
-            uint32_t q = *reinterpret_cast<const uint32_t *>(p);
-            v[0] = bf2f(q & 0xffff); v[1 % CPL] = bf2f(q >> 16);
+        if constexpr (CPL % 4 == 0) {
+#pragma unroll
+            for (int i = 0; i < CPL / 4; ++i) {
+                const uint2 q = reinterpret_cast<const uint2 *>(p)[i];
+                v[4 * i + 0] = bf2f(q.x & 0xffff); v[4 * i + 1] = bf2f(q.x >> 16);
+                v[4 * i + 2] = bf2f(q.y & 0xffff); v[4 * i + 3] = bf2f(q.y >> 16);
+            }
+        } else if constexpr (CPL == 2) {
+            const uint32_t q = *reinterpret_cast<const uint32_t *>(p);
+            v[0] = bf2f(q & 0xffff); v[1] = bf2f(q >> 16);
         } else {
             v[0] = bf2f(p[0]);
         }
     } else {
         const float *p = static_cast<const float *>(base) + off;
-        if (CPL == 4) {
-            float4 q = *reinterpret_cast<const float4 *>(p);
-            v[0] = q.x; v[1] = q.y; v[2 % CPL] = q.z; v[3 % CPL] = q.w;
-        } else if (CPL == 2) {
-            float2 q = *reinterpret_cast<const float2 *>(p);
-            v[0] = q.x; v[1 % CPL] = q.y;
+        if constexpr (CPL % 4 == 0) {
+#pragma unroll
+            for (int i = 0; i < CPL / 4; ++i) {
+                const float4 q = reinterpret_cast<const float4 *>(p)[i];
+                v[4 * i + 0] = q.x; v[4 * i + 1] = q.y; v[4 * i + 2] = q.z; v[4 * i + 3] = q.w;
+            }
+        } else if constexpr (CPL == 2) {
+            const float2 q = *reinterpret_cast<const float2 *>(p);
+            v[0] = q.x; v[1] = q.y;
         } else {
             v[0] = p[0];
         }

@@ -19,30 +19,34 @@
 namespace tag {
 namespace {
 
-__device__ __forceinline__ int32_t owner32(const int32_t *off, int32_t G, int32_t i) {
-    int32_t lo = 0, hi = G;
-    while (hi - lo > 1) {
-        int32_t mid = (lo + hi) >> 1;
-        if (off[mid] <= i) lo = mid; else hi = mid;
-    }
-    return lo;
-}
-
-// omask[r][u] = (present, bits) over the local devices of u's topology
-__global__ void pack_op_masks(AggArgs A) {
-    const int64_t n = (int64_t)A.R * A.n_op;
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
-        const int32_t r = (int32_t)(i / A.n_op), u = (int32_t)(i % A.n_op);
-        const int32_t d0 = A.dev_off[owner32(A.op_off, A.G, u)];
-        const uint8_t *xb = A.x_od + (int64_t)r * A.s_od;
-        uint64_t pres = 0, bits = 0;
-        for (int32_t e = A.rp[1][u]; e < A.rp[1][u + 1]; ++e) {
-            const int32_t j = A.col[1][e] - d0;
-            pres |= 1ull << j;
-            if (xb[A.eid[1][e]]) bits |= 1ull << j;
+// omask[r][u] = (present, bits) over the local devices of u's topology.
+// One block per (op tile, candidate): the tile's op<-dev entries are one
+// contiguous CSR range, read coalesced and OR-ed into LDS masks.
+__global__ void __launch_bounds__(256) pack_op_masks(AggArgs A) {
+    __shared__ int32_t rp[kOpTile + 1];
+    __shared__ unsigned long long pres[kOpTile], bits[kOpTile];
+    const int32_t t = blockIdx.x, r = blockIdx.y;
+    const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1], g = A.tiles[3 * t + 2];
+    const int32_t d0 = A.dev_off[g];
+    for (int i = threadIdx.x; i <= nu; i += blockDim.x) rp[i] = A.rp[1][u0 + i];
+    for (int i = threadIdx.x; i < kOpTile; i += blockDim.x) { pres[i] = 0ull; bits[i] = 0ull; }
+    __syncthreads();
+    const uint8_t *xb = A.x_od + (int64_t)r * A.s_od;
+    for (int32_t e = rp[0] + threadIdx.x; e < rp[nu]; e += blockDim.x) {
+        int lo = 0, hi = nu;   // last local row with rp[row] <= e
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (rp[mid] <= e) lo = mid; else hi = mid;
         }
-        A.omask[2 * i] = pres;
-        A.omask[2 * i + 1] = bits;
+        const unsigned long long m = 1ull << (A.col[1][e] - d0);
+        atomicOr(&pres[lo], m);
+        if (xb[A.eid[1][e]]) atomicOr(&bits[lo], m);
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < nu; i += blockDim.x) {
+        const int64_t mi = 2 * ((int64_t)r * A.n_op + u0 + i);
+        A.omask[mi] = pres[i];
+        A.omask[mi + 1] = bits[i];
     }
 }
 
@@ -80,52 +84,68 @@ __global__ void __launch_bounds__(256) dev_prep(AggArgs A) {
     }
 }
 
-// op <- op: one wavefront per op row, up to four neighbour rows in flight;
-// writes gamma_same * aggregate to O0 (fp32)
+// op <- op: four op rows per wavefront (16 lanes and f/16 channels per lane
+// each), several neighbour rows in flight per op row; writes
+// gamma_same * aggregate to O0 (fp32)
 template <int F, int K, bool BF>
 __global__ void __launch_bounds__(256) agg_b0(AggArgs A) {
-    constexpr int CPL = F / 64, LPH = 64 / K;
+    constexpr int CPL = F / 16;              // channels per lane
+    constexpr int LPH = 16 / K;              // lanes per head (K <= 16 on this path)
+    constexpr int EB = CPL >= 16 ? 2 : 4;    // neighbour rows loaded together
     const int lane = threadIdx.x & 63;
-    const int64_t w = (int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6);
-    if (w >= (int64_t)A.R * A.n_op) return;
-    const int32_t rep = (int32_t)(w / A.n_op);
-    const int32_t u = (int32_t)(w % A.n_op);
-    const int c0 = lane * CPL;
-    RelConst<CPL> k; k.load(A, 0, F, c0);
-    float yd[CPL]; load_ch<CPL, BF>(A.Y_op, w * 2 * F + c0, yd);
+    const int li = lane & 15;
+    const int64_t nrows = (int64_t)A.R * A.n_op;
+    const int64_t w = ((int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6)) * 4 + (lane >> 4);
+    const bool live = w < nrows;
+    const int64_t wr = live ? w : nrows - 1;     // dead slots shadow a real row and store nothing
+    const int32_t rep = (int32_t)(wr / A.n_op);
+    const int32_t u = (int32_t)(wr % A.n_op);
+    const int c0 = li * CPL;
+    float a[CPL], u0[CPL], cp[CPL];
     float q = 0.f;
-    for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], yd[c], q);
+    {
+        float yd[CPL];
+        load_ch<CPL, BF>(A.Y_op, wr * 2 * F + c0, yd);
+        for (int c = 0; c < CPL; ++c) {
+            a[c] = A.att_src[c0 + c];
+            u0[c] = A.U[(size_t)(c0 + c) * 2];
+            cp[c] = A.cp[c0 + c];
+            q = fmaf(A.att_dst[c0 + c], yd[c], q);
+        }
+    }
     q = head_sum<LPH>(q);
     Online<CPL> o; o.init();
     const int32_t beg = A.rp[0][u], end = A.rp[0][u + 1];
     const float *xo = A.x_oo + (int64_t)rep * A.s_oo;
     const int64_t ybase = (int64_t)rep * A.n_op * 2 * F + c0;
-    for (int32_t e = beg; e < end; e += 4) {
-        const int n = min(4, end - e);
-        int32_t v[4], id[4];
-        for (int i = 0; i < 4; ++i) {
+    for (int32_t e = beg; e < end; e += EB) {
+        const int n = min(EB, end - e);
+        int32_t v[EB], id[EB];
+        for (int i = 0; i < EB; ++i) {
             v[i] = i < n ? A.col[0][e + i] : 0;
             id[i] = i < n ? A.eid[0][e + i] : 0;
         }
-        float x[4], y[4][CPL];
-        for (int i = 0; i < 4; ++i) {
+        float x[EB], y[EB][CPL];
+        for (int i = 0; i < EB; ++i) {
             x[i] = i < n ? xo[id[i]] : 0.f;
             if (i < n) load_ch<CPL, BF>(A.Y_op, ybase + (int64_t)v[i] * 2 * F, y[i]);
         }
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < EB; ++i) {
             if (i < n) {
-                float m[CPL];
-                const float s2 = entry_score<CPL, LPH>(y[i], x[i], 0.f, k, q, A.slope, m);
+                float m[CPL], part = 0.f;
+                for (int c = 0; c < CPL; ++c) {
+                    m[c] = fmaxf(y[i][c] + fmaf(u0[c], x[i], cp[c]), 0.f);
+                    part = fmaf(a[c], m[c], part);
+                }
+                const float s2 = leaky(head_sum<LPH>(part) + q, A.slope) * kLog2e;
                 o.push(s2, m);
             }
         }
     }
-    float *out = A.O0 + w * F + c0;
-    if (end > beg) {
-        const float inv = A.g_same / o.den;
+    if (live) {
+        float *out = A.O0 + w * F + c0;
+        const float inv = end > beg ? A.g_same / o.den : 0.f;
         for (int c = 0; c < CPL; ++c) out[c] = o.acc[c] * inv;
-    } else {
-        for (int c = 0; c < CPL; ++c) out[c] = 0.f;
     }
 }
 
@@ -140,7 +160,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     __shared__ float Ys[kOpTile * YS];
     __shared__ uint64_t pres[kOpTile], bits[kOpTile];
     __shared__ float pb[kOpTile][2][K];
-    __shared__ float qd[64][K], mxS[64][K], zS[64][K];
+    __shared__ float qd[64][K], mxS[64][K];
     __shared__ float cpS[F], US[F], aS[F], adS[F];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -188,23 +208,17 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
         if (u < nu) A.qop[((int64_t)r * A.n_op + u0 + u) * K + h] = q;
     }
     __syncthreads();
-    // per (device, head): max and sum of exp over the tile's links
+    // per (device, head): exact max of the logit over the tile's links
+    // (LeakyReLU is monotone, so it is LeakyReLU of the largest pre-activation)
     for (int i = tid; i < Mg * K; i += 256) {
         const int j = i / K, h = i % K;
         float mx = -INFINITY;
-        for (int u = 0; u < nu; ++u)
-            if ((pres[u] >> j) & 1ull) {
-                const int b = (int)((bits[u] >> j) & 1ull);
-                mx = fmaxf(mx, leaky(pb[u][b][h] + qd[j][h], A.slope) * kLog2e);
-            }
-        float z = 0.f;
-        for (int u = 0; u < nu; ++u)
-            if ((pres[u] >> j) & 1ull) {
-                const int b = (int)((bits[u] >> j) & 1ull);
-                z += __builtin_amdgcn_exp2f(leaky(pb[u][b][h] + qd[j][h], A.slope) * kLog2e - mx);
-            }
-        mxS[j][h] = mx;
-        zS[j][h] = z;
+        for (int u = 0; u < nu; ++u) {
+            const uint64_t pr = pres[u], bt = bits[u];
+            const float v = ((bt >> j) & 1ull) ? pb[u][1][h] : pb[u][0][h];
+            mx = ((pr >> j) & 1ull) ? fmaxf(mx, v) : mx;
+        }
+        mxS[j][h] = mx == -INFINITY ? -INFINITY : leaky(mx + qd[j][h], A.slope) * kLog2e;
     }
     __syncthreads();
 
@@ -219,10 +233,14 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     }
     const int NRB = (Mg + 15) / 16;
     f4 acc[4][NCB];
+    float zl[4][HPW];
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
+    for (int rb = 0; rb < 4; ++rb) {
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) acc[rb][cb] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int hh = 0; hh < HPW; ++hh) zl[rb][hh] = 0.f;
+    }
     for (int s = 0; s < kOpTile / 2; ++s) {
         const int ul = 2 * s + (lane >> 5);
         const int b = (lane >> 4) & 1;
@@ -243,6 +261,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
                     const int h = h0 + hh;
                     const float af = on ? __builtin_amdgcn_exp2f(leaky(pb[ul][b][h] + qd[j][h], A.slope) * kLog2e - mxS[j][h])
                                         : 0.f;
+                    zl[rb][hh] += af;
 #pragma unroll
                     for (int c2 = 0; c2 < CPH; ++c2)
                         acc[rb][hh * CPH + c2] =
@@ -263,12 +282,22 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
                 for (int cb = 0; cb < NCB; ++cb) rec[cbase + cb * 16 + (lane & 15)] = acc[rb][cb][v];
             }
         }
-    for (int i = tid; i < Mg * K; i += 256) {
-        const int j = i / K, h = i % K;
-        float *rec = A.part + (((int64_t)r * A.n_dev + d0 + j) * A.maxc + chunk) * REC;
-        rec[h] = mxS[j][h];
-        rec[K + h] = zS[j][h];
-    }
+    // softmax sums: lanes l, l+16, l+32, l+48 hold parts of device row l % 16
+    const bool head_owner = (cbase % D) == 0;   // first wavefront covering its heads
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+        for (int hh = 0; hh < HPW; ++hh) {
+            float z = zl[rb][hh];
+            z += __shfl_xor(z, 16, 64);
+            z += __shfl_xor(z, 32, 64);
+            const int j = rb * 16 + (lane & 15);
+            if (head_owner && lane < 16 && rb < NRB && j < Mg) {
+                float *rec = A.part + (((int64_t)r * A.n_dev + d0 + j) * A.maxc + chunk) * REC;
+                rec[h0 + hh] = mxS[j][h0 + hh];
+                rec[K + h0 + hh] = z;
+            }
+        }
 }
 
 // op <- device over one 64-op tile, plus the op <- op part from O0
@@ -279,7 +308,7 @@ __global__ void __launch_bounds__(256) agg_b1(AggArgs A) {
     constexpr int NCB = WC / 16;
     constexpr int HPW = WC >= D ? WC / D : 1;
     __shared__ uint64_t pres[kOpTile], bits[kOpTile];
-    __shared__ float qo[kOpTile][K], mxS[kOpTile][K], izS[kOpTile][K];
+    __shared__ float qo[kOpTile][K], mxS[kOpTile][K];
     __shared__ float P[64][2][K];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -306,13 +335,8 @@ __global__ void __launch_bounds__(256) agg_b1(AggArgs A) {
         const uint64_t pr = pres[u], bt = bits[u];
         float mx = -INFINITY;
         for (int j = 0; j < Mg; ++j)
-            if ((pr >> j) & 1ull) mx = fmaxf(mx, leaky(P[j][(bt >> j) & 1ull][h] + qo[u][h], A.slope) * kLog2e);
-        float z = 0.f;
-        for (int j = 0; j < Mg; ++j)
-            if ((pr >> j) & 1ull)
-                z += __builtin_amdgcn_exp2f(leaky(P[j][(bt >> j) & 1ull][h] + qo[u][h], A.slope) * kLog2e - mx);
-        mxS[u][h] = mx;
-        izS[u][h] = z > 0.f ? 1.f / z : 0.f;
+            if ((pr >> j) & 1ull) mx = fmaxf(mx, P[j][(bt >> j) & 1ull][h]);
+        mxS[u][h] = mx == -INFINITY ? -INFINITY : leaky(mx + qo[u][h], A.slope) * kLog2e;
     }
     __syncthreads();
 
@@ -320,8 +344,14 @@ __global__ void __launch_bounds__(256) agg_b1(AggArgs A) {
     const int h0 = cbase / D;
     constexpr int CPH = NCB / HPW;
     f4 acc[4][NCB];
-    for (int rb = 0; rb < 4; ++rb)
+    float zl[4][HPW];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+#pragma unroll
         for (int cb = 0; cb < NCB; ++cb) acc[rb][cb] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int hh = 0; hh < HPW; ++hh) zl[rb][hh] = 0.f;
+    }
     const float *Tb = A.T + ((int64_t)r * A.n_dev + d0) * 2 * F;
     const int steps = (Mg + 1) / 2;
     for (int s = 0; s < steps; ++s) {
@@ -337,9 +367,9 @@ __global__ void __launch_bounds__(256) agg_b1(AggArgs A) {
 #pragma unroll
             for (int hh = 0; hh < HPW; ++hh) {
                 const int h = h0 + hh;
-                const float af = on ? __builtin_amdgcn_exp2f(leaky(P[j][b][h] + qo[u][h], A.slope) * kLog2e - mxS[u][h]) *
-                                          izS[u][h]
+                const float af = on ? __builtin_amdgcn_exp2f(leaky(P[j][b][h] + qo[u][h], A.slope) * kLog2e - mxS[u][h])
                                     : 0.f;
+                zl[rb][hh] += af;
 #pragma unroll
                 for (int c2 = 0; c2 < CPH; ++c2)
                     acc[rb][hh * CPH + c2] =
@@ -347,18 +377,36 @@ __global__ void __launch_bounds__(256) agg_b1(AggArgs A) {
             }
         }
     }
-    for (int rb = 0; rb < 4; ++rb)
+    // softmax sums of op row rb*16 + l%16 are spread over lanes l, l+16,
+    // l+32, l+48; the output row of register v in lane l is rb*16 + 4(l/16) + v
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+        float scale[HPW][4];
+#pragma unroll
+        for (int hh = 0; hh < HPW; ++hh) {
+            float z = zl[rb][hh];
+            z += __shfl_xor(z, 16, 64);
+            z += __shfl_xor(z, 32, 64);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const float zv = __shfl(z, 4 * (lane >> 4) + v, 64);
+                scale[hh][v] = zv > 0.f ? A.g_cross / zv : 0.f;
+            }
+        }
+#pragma unroll
         for (int v = 0; v < 4; ++v) {
             const int u = rb * 16 + 4 * (lane >> 4) + v;
             if (u >= nu) continue;
             const int64_t row = (int64_t)r * A.n_op + u0 + u;
+#pragma unroll
             for (int cb = 0; cb < NCB; ++cb) {
                 const int col = cbase + cb * 16 + (lane & 15);
-                const float val = fmaf(A.g_cross, acc[rb][cb][v], A.O0[row * F + col]);
+                const float val = fmaf(scale[cb / CPH][v], acc[rb][cb][v], A.O0[row * F + col]);
                 if (A.out_f32) static_cast<float *>(A.H_op)[row * F + col] = val;
                 else static_cast<uint16_t *>(A.H_op)[row * F + col] = f2bf(val);
             }
         }
+    }
 }
 
 template <int F, int K, bool BF>
@@ -371,7 +419,7 @@ void launch_mfma(const AggArgs &A, hipStream_t st) {
     agg_b2<F, K, BF><<<tiles, 256, 0, st>>>(A);
     prof_end(TAG_STAGE_AGG_DEV_PART, st);
     prof_begin(TAG_STAGE_AGG_OP, st);
-    agg_b0<F, K, BF><<<(unsigned)((op_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
+    agg_b0<F, K, BF><<<(unsigned)((op_waves + 4 * kWaves - 1) / (4 * kWaves)), 256, 0, st>>>(A);
     agg_b1<F, K, BF><<<tiles, 256, 0, st>>>(A);
     prof_end(TAG_STAGE_AGG_OP, st);
 }
@@ -393,9 +441,7 @@ bool dispatch_mfma_heads(int K, const AggArgs &A, hipStream_t st) {
 bool mfma_path_supported(int F, int K) { return K >= 1 && F / K >= 16 && K <= 16; }
 
 void launch_pack_masks(const AggArgs &A, hipStream_t st) {
-    const int64_t n = (int64_t)A.R * A.n_op;
-    const unsigned blocks = (unsigned)std::max<int64_t>(1, std::min<int64_t>((n + 255) / 256, 1 << 16));
-    pack_op_masks<<<blocks, 256, 0, st>>>(A);
+    pack_op_masks<<<dim3((unsigned)A.n_tiles, (unsigned)A.R), 256, 0, st>>>(A);
 }
 
 bool launch_agg_mfma(int F, int K, bool bf, const AggArgs &A, hipStream_t st) {

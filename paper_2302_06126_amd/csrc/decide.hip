@@ -36,21 +36,6 @@ struct DecArgs {
     tag_decision *dec;
 };
 
-// t[row][h] = sum_c P[h][c] E_dev[row][c]
-__global__ void dec_dev_proj(DecArgs A) {
-    const int64_t n = (int64_t)A.R * A.n_dev * A.Hx;
-    const int din = 2 * A.F + 4;
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t row = i / A.Hx;
-        const int h = (int)(i % A.Hx);
-        const float *e = A.E_dev + row * A.F;
-        const float *p = A.P + (size_t)h * din;
-        float s = 0.f;
-        for (int c = 0; c < A.F; ++c) s = fmaf(p[c], e[c], s);
-        A.t[i] = s;
-    }
-}
-
 // u[rg][h][a] = sum_{j in mask_a} t[dev(rg, j)][h] + P[h][2F + opt_a] (+ b1[h])
 __global__ void dec_slice(DecArgs A) {
     const int64_t n = (int64_t)A.R * A.G * A.Hx * A.S;
@@ -78,21 +63,11 @@ __device__ __forceinline__ bool query_valid(const DecArgs &A, int32_t q, int32_t
     return *op >= 0 && *op < A.op_off[*g + 1] - A.op_off[*g];
 }
 
-// v[q][h] = sum_c P[h][F + c] E_op[row(q)][c]
-__global__ void dec_query_proj(DecArgs A) {
-    const int64_t n = (int64_t)A.Q * A.Hx;
-    const int din = 2 * A.F + 4;
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
-        const int32_t q = (int32_t)(i / A.Hx);
-        const int h = (int)(i % A.Hx);
+// row of E_op read by each query (-1: invalid query)
+__global__ void dec_query_rows(DecArgs A, int32_t *qrow) {
+    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < A.Q; q += (int64_t)gridDim.x * blockDim.x) {
         int32_t r, g, op;
-        float s = 0.f;
-        if (query_valid(A, q, &r, &g, &op)) {
-            const float *e = A.E_op + ((int64_t)r * A.n_op + A.op_off[g] + op) * A.F;
-            const float *p = A.P + (size_t)h * din + A.F;
-            for (int c = 0; c < A.F; ++c) s = fmaf(p[c], e[c], s);
-        }
-        A.v[i] = s;
+        qrow[q] = query_valid(A, (int32_t)q, &r, &g, &op) ? (int32_t)((int64_t)r * A.n_op + A.op_off[g] + op) : -1;
     }
 }
 
@@ -184,6 +159,7 @@ __global__ void __launch_bounds__(kScoreThreads) dec_score(DecArgs A) {
 
 struct DecLayout {
     float *t, *u, *v;
+    int32_t *qrow;
 };
 
 size_t carve_dec(const tag_graph *g, int32_t Hx, int32_t R, int32_t S, int32_t Q, void *base, DecLayout *L) {
@@ -191,6 +167,7 @@ size_t carve_dec(const tag_graph *g, int32_t Hx, int32_t R, int32_t S, int32_t Q
     L->t = c.take<float>((size_t)R * g->n_dev * Hx);
     L->u = c.take<float>((size_t)R * g->G * Hx * S);
     L->v = c.take<float>((size_t)std::max(Q, 1) * Hx);
+    L->qrow = c.take<int32_t>((size_t)std::max(Q, 1));
     return c.used;
 }
 
@@ -250,10 +227,14 @@ extern "C" tag_status tag_gnn_decide(const tag_graph *g, const tag_model_dims *d
     A.q_rep = query_rep; A.q_graph = query_graph; A.q_op = query_op;
     A.t = L.t; A.u = L.u; A.v = L.v;
     A.argmax = argmax; A.best = best_score; A.prior = prior; A.dec = decision;
+    const int din = 2 * A.F + 4;
     prof_begin(TAG_STAGE_DECIDE, stream);
-    dec_dev_proj<<<grid_for((int64_t)A.R * A.n_dev * Hx), 256, 0, stream>>>(A);
+    // t = E_dev W1_dev^T and v = E_op[query rows] W1_op^T as MFMA GEMMs
+    launch_small_gemm(SmallGemm{E_dev, A.F, (int64_t)A.R * A.n_dev, nullptr, A.F, A.P, din, Hx, nullptr, 0,
+                                A.t, Hx, 0}, stream);
+    dec_query_rows<<<grid_for(A.Q), 256, 0, stream>>>(A, L.qrow);
+    launch_small_gemm(SmallGemm{E_op, A.F, A.Q, L.qrow, A.F, A.P + A.F, din, Hx, nullptr, 0, A.v, Hx, 0}, stream);
     dec_slice<<<grid_for((int64_t)A.R * A.G * Hx * A.S), 256, 0, stream>>>(A);
-    dec_query_proj<<<grid_for((int64_t)A.Q * Hx), 256, 0, stream>>>(A);
     dec_score<<<(unsigned)A.Q, kScoreThreads, sizeof(float) * (Hx + H), stream>>>(A);
     prof_end(TAG_STAGE_DECIDE, stream);
     return launch_status("tag_gnn_decide");

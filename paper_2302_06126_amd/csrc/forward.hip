@@ -382,9 +382,10 @@ tag_status check_dims(const tag_model_dims *d) {
         TAG_FAIL(TAG_ESHAPE, "f_op and f_dev must be in [1, 64]");
     if (d->dec_hidden < 0 || d->dec_hidden > 1024) TAG_FAIL(TAG_ESHAPE, "dec_hidden must be in [0, 1024]");
     if (d->dtype != TAG_F32 && d->dtype != TAG_BF16) TAG_FAIL(TAG_EINVAL, "dtype must be TAG_F32 or TAG_BF16");
-    if (!(d->gamma_same == d->gamma_same) || !(d->gamma_cross == d->gamma_cross) ||
-        !(d->leaky_slope == d->leaky_slope))
-        TAG_FAIL(TAG_EINVAL, "gamma and slope must not be NaN");
+    if (!(d->gamma_same == d->gamma_same) || !(d->gamma_cross == d->gamma_cross))
+        TAG_FAIL(TAG_EINVAL, "gamma must not be NaN");
+    if (!(d->leaky_slope >= 0.f && d->leaky_slope <= 1.f))
+        TAG_FAIL(TAG_EINVAL, "leaky_slope must be in [0, 1]");
     return TAG_OK;
 }
 

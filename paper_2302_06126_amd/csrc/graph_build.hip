@@ -160,8 +160,12 @@ __global__ void scan_add(int32_t *out, int64_t n, const int32_t *tile_sums) {
 }
 
 // ---- exact per-row rank sort ----
+constexpr int kShortRow = 256;        // rows up to this length: per-entry rank
+constexpr int kBitmapRange = 16384;   // source-id range sorted through an LDS bitmap
+
 // Only the first rp[n_rows] slots hold entries: links rejected during the
-// count pass (bad ids, self links) were never scattered.
+// count pass (bad ids, self links) were never scattered.  Rows longer than
+// kShortRow are left to rank_long_rows.
 __global__ void rank_rows(const int32_t *rp, int64_t n_rows, const int32_t *tcol, const int32_t *teid,
                           const int32_t *rowof, int64_t nnz, int32_t *col, int32_t *eid,
                           int32_t *flags, int bucket) {
@@ -169,6 +173,7 @@ __global__ void rank_rows(const int32_t *rp, int64_t n_rows, const int32_t *tcol
     if (p >= nnz || p >= rp[n_rows]) return;
     int32_t r = rowof[p];
     int32_t beg = rp[r], end = rp[r + 1];
+    if (end - beg > kShortRow) return;
     int32_t c = tcol[p], e = teid[p];
     int32_t rank = 0, dup = 0;
     for (int32_t q = beg; q < end; ++q) {
@@ -180,6 +185,87 @@ __global__ void rank_rows(const int32_t *rp, int64_t n_rows, const int32_t *tcol
     eid[beg + rank] = e;
     if (dup) atomicOr(&flags[FLAG_DUP], 1);
     if (rank == 0) atomicMax(&flags[FLAG_MAXDEG + bucket], end - beg);
+}
+
+// One block per long row.  Sources of a row all belong to the row's
+// topology, so a bitmap over that topology's source-id range sorts the row
+// by source id (sources are unique in a valid row; a repeated source is
+// caught by the atomic OR).  Ranges beyond kBitmapRange fall back to the
+// per-entry rank inside the block.
+__global__ void __launch_bounds__(256) rank_long_rows(const int32_t *rp, const int32_t *tcol, const int32_t *teid,
+                                                      int32_t *col, int32_t *eid, int32_t *flags, int bucket,
+                                                      const int32_t *row_off, const int32_t *src_off, int32_t G) {
+    __shared__ uint32_t bm[kBitmapRange / 32];
+    __shared__ int32_t wpre[kBitmapRange / 32];
+    __shared__ int32_t eid_of[kBitmapRange];
+    __shared__ int32_t scan[256];
+    const int32_t r = blockIdx.x;
+    const int32_t beg = rp[r], end = rp[r + 1];
+    if (end - beg <= kShortRow) return;
+    int32_t lo = 0, hi = G;
+    while (hi - lo > 1) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (row_off[mid] <= r) lo = mid; else hi = mid;
+    }
+    const int32_t base = src_off[lo], range = src_off[lo + 1] - base;
+    if (threadIdx.x == 0) atomicMax(&flags[FLAG_MAXDEG + bucket], end - beg);
+    if (range > kBitmapRange) {
+        for (int32_t p = beg + threadIdx.x; p < end; p += blockDim.x) {
+            const int32_t c = tcol[p], e = teid[p];
+            int32_t rank = 0, dup = 0;
+            for (int32_t q = beg; q < end; ++q) {
+                const int32_t cq = tcol[q], eq = teid[q];
+                rank += (cq < c) || (cq == c && eq < e);
+                dup |= (cq == c) && (q != p);
+            }
+            col[beg + rank] = c;
+            eid[beg + rank] = e;
+            if (dup) atomicOr(&flags[FLAG_DUP], 1);
+        }
+        return;
+    }
+    const int nw = (range + 31) / 32;
+    for (int w = threadIdx.x; w < nw; w += blockDim.x) bm[w] = 0u;
+    __syncthreads();
+    int dup = 0;
+    for (int32_t p = beg + threadIdx.x; p < end; p += blockDim.x) {
+        const int32_t c = tcol[p] - base;
+        const uint32_t bit = 1u << (c & 31);
+        const uint32_t old = atomicOr(&bm[c >> 5], bit);
+        dup |= (old & bit) != 0u;
+        eid_of[c] = teid[p];
+    }
+    if (dup) atomicOr(&flags[FLAG_DUP], 1);
+    __syncthreads();
+    // exclusive prefix of per-word popcounts (chunks of 256 words)
+    int32_t carry = 0;
+    for (int w0 = 0; w0 < nw; w0 += 256) {
+        const int w = w0 + threadIdx.x;
+        const int32_t v = w < nw ? __popc(bm[w]) : 0;
+        scan[threadIdx.x] = v;
+        __syncthreads();
+        for (int off = 1; off < 256; off <<= 1) {
+            const int32_t t = threadIdx.x >= off ? scan[threadIdx.x - off] : 0;
+            __syncthreads();
+            scan[threadIdx.x] += t;
+            __syncthreads();
+        }
+        if (w < nw) wpre[w] = carry + scan[threadIdx.x] - v;
+        carry += scan[255];
+        __syncthreads();
+    }
+    for (int w = threadIdx.x; w < nw; w += blockDim.x) {
+        uint32_t b = bm[w];
+        int32_t pos = beg + wpre[w];
+        while (b) {
+            const int k = __ffs(b) - 1;
+            b &= b - 1u;
+            const int32_t c = w * 32 + k;
+            col[pos] = base + c;
+            eid[pos] = eid_of[c];
+            ++pos;
+        }
+    }
 }
 
 inline unsigned grid_for(int64_t n, int64_t cap = 65536) {
@@ -412,6 +498,13 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
             rank_rows<<<(unsigned)((s.nnz[b] + kThreads - 1) / kThreads), kThreads, 0, stream>>>(
                 cl.rowptr[b], s.rows[b], tl.tcol[b], tl.teid[b], tl.rowof[b], s.nnz[b], cl.col[b], cl.eid[b],
                 tl.flags, b);
+    // op<-op and dev<-op rows can be long; op<-dev and dev<-dev rows have at most 64 entries
+    if (s.nnz[0])
+        rank_long_rows<<<(unsigned)s.rows[0], kThreads, 0, stream>>>(cl.rowptr[0], tl.tcol[0], tl.teid[0], cl.col[0],
+                                                                      cl.eid[0], tl.flags, 0, cl.op_off, cl.op_off, s.G);
+    if (s.nnz[2])
+        rank_long_rows<<<(unsigned)s.rows[2], kThreads, 0, stream>>>(cl.rowptr[2], tl.tcol[2], tl.teid[2], cl.col[2],
+                                                                      cl.eid[2], tl.flags, 2, cl.dev_off, cl.op_off, s.G);
     prof_end(TAG_STAGE_GRAPH_BUILD, stream);
     {
         hipError_t e = hipGetLastError();
