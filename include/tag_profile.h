@@ -19,16 +19,20 @@
 extern "C" {
 #endif
 
-/* Kernel stages that can be timed. */
+/* Kernel stages that can be timed (one kernel per stage and launch, except
+ * where noted). */
 enum {
-    TAG_STAGE_GRAPH_BUILD = 0,   /* every kernel of tag_graph_build (one pair per call)  */
-    TAG_STAGE_ENCODE = 1,        /* node encoders                                         */
-    TAG_STAGE_TRANSFORM = 2,     /* relation transforms W^h h, op and device rows (1/layer) */
-    TAG_STAGE_AGG_OP = 3,        /* op destinations: op<-op and op<-dev (1/layer)         */
-    TAG_STAGE_AGG_DEV_PART = 4,  /* device<-op chunk partials (1/layer)                   */
-    TAG_STAGE_AGG_DEV_FINAL = 5, /* device destinations: merge + dev<-dev (1/layer)      */
-    TAG_STAGE_DECIDE = 6,        /* every kernel of tag_gnn_decide (one pair per call)   */
-    TAG_STAGE_COUNT = 7
+    TAG_STAGE_GRAPH_BUILD = 0,    /* all kernels of tag_graph_build (one pair per call)      */
+    TAG_STAGE_ENCODE = 1,         /* node encoders (op and device launches, one pair)        */
+    TAG_STAGE_TRANSFORM = 2,      /* relation transforms W^h h, op and device rows (1/layer) */
+    TAG_STAGE_AGG_OP_OP = 3,      /* op <- op aggregation (1/layer); on the path for heads   */
+                                  /* narrower than 16 channels this also covers op <- dev    */
+    TAG_STAGE_AGG_OP_DEV = 4,     /* op <- dev aggregation + combine (1/layer)               */
+    TAG_STAGE_AGG_DEV_OP = 5,     /* dev <- op partial records (1/layer)                     */
+    TAG_STAGE_AGG_DEV_MERGE = 6,  /* dev <- op merge + dev <- dev (1/layer)                  */
+    TAG_STAGE_DEV_PREP = 7,       /* device message table (1/layer)                          */
+    TAG_STAGE_DECIDE = 8,         /* all kernels of tag_gnn_decide (one pair per call)       */
+    TAG_STAGE_COUNT = 9
 };
 
 /* Start recording event pairs around launches of `stage`, for at most

@@ -23,8 +23,8 @@ EXPORTS = ("tag_graph_plan", "tag_graph_build", "tag_graph_get_info", "tag_graph
            "tag_gnn_decide", "tag_last_error", "tag_version", "tag_profile_begin", "tag_profile_end")
 
 # kernel stages (include/tag_profile.h)
-STAGE_GRAPH_BUILD, STAGE_ENCODE, STAGE_TRANSFORM, STAGE_AGG_OP, STAGE_AGG_DEV_PART, STAGE_AGG_DEV_FINAL, \
-    STAGE_DECIDE = range(7)
+STAGE_NAMES = ("graph_build", "encode", "transform", "agg_op_op", "agg_op_dev", "agg_dev_op", "agg_dev_merge",
+               "dev_prep", "decide")
 
 _P32 = C.POINTER(C.c_int32)
 _P64 = C.POINTER(C.c_int64)

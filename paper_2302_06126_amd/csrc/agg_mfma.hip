@@ -414,14 +414,18 @@ void launch_mfma(const AggArgs &A, hipStream_t st) {
     const int64_t op_waves = (int64_t)A.R * A.n_op;
     const int64_t dev_waves = (int64_t)A.R * A.n_dev;
     const dim3 tiles((unsigned)A.n_tiles, (unsigned)A.R);
+    prof_begin(TAG_STAGE_DEV_PREP, st);
     dev_prep<F, K, BF><<<(unsigned)((dev_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
-    prof_begin(TAG_STAGE_AGG_DEV_PART, st);
+    prof_end(TAG_STAGE_DEV_PREP, st);
+    prof_begin(TAG_STAGE_AGG_DEV_OP, st);
     agg_b2<F, K, BF><<<tiles, 256, 0, st>>>(A);
-    prof_end(TAG_STAGE_AGG_DEV_PART, st);
-    prof_begin(TAG_STAGE_AGG_OP, st);
+    prof_end(TAG_STAGE_AGG_DEV_OP, st);
+    prof_begin(TAG_STAGE_AGG_OP_OP, st);
     agg_b0<F, K, BF><<<(unsigned)((op_waves + 4 * kWaves - 1) / (4 * kWaves)), 256, 0, st>>>(A);
+    prof_end(TAG_STAGE_AGG_OP_OP, st);
+    prof_begin(TAG_STAGE_AGG_OP_DEV, st);
     agg_b1<F, K, BF><<<tiles, 256, 0, st>>>(A);
-    prof_end(TAG_STAGE_AGG_OP, st);
+    prof_end(TAG_STAGE_AGG_OP_DEV, st);
 }
 
 template <int F, bool BF>

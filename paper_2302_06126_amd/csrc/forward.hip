@@ -424,21 +424,21 @@ void launch_agg(const AggArgs &A, hipStream_t st) {
     const int64_t op_waves = (int64_t)A.R * A.n_op;
     const int64_t part_waves = (int64_t)A.R * A.maxc * A.n_dev;
     const int64_t dev_waves = (int64_t)A.R * A.n_dev;
-    prof_begin(TAG_STAGE_AGG_OP, st);
+    prof_begin(TAG_STAGE_AGG_OP_OP, st);
     agg_op<F, K, BF><<<(unsigned)((op_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
-    prof_end(TAG_STAGE_AGG_OP, st);
-    prof_begin(TAG_STAGE_AGG_DEV_PART, st);
+    prof_end(TAG_STAGE_AGG_OP_OP, st);
+    prof_begin(TAG_STAGE_AGG_DEV_OP, st);
     agg_dev_part<F, K, BF><<<(unsigned)((part_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
-    prof_end(TAG_STAGE_AGG_DEV_PART, st);
+    prof_end(TAG_STAGE_AGG_DEV_OP, st);
     (void)dev_waves;
 }
 
 template <int F, int K, bool BF>
 void launch_dev_final(const AggArgs &A, hipStream_t st) {
     const int64_t dev_waves = (int64_t)A.R * A.n_dev;
-    prof_begin(TAG_STAGE_AGG_DEV_FINAL, st);
+    prof_begin(TAG_STAGE_AGG_DEV_MERGE, st);
     agg_dev_final<F, K, BF><<<(unsigned)((dev_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
-    prof_end(TAG_STAGE_AGG_DEV_FINAL, st);
+    prof_end(TAG_STAGE_AGG_DEV_MERGE, st);
 }
 
 // first-version aggregation (used when heads are narrower than 16 channels),
