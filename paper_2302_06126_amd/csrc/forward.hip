@@ -22,6 +22,7 @@
 #include <algorithm>
 
 #include "agg_common.hpp"
+#include "transform.hpp"
 
 namespace tag {
 namespace {
@@ -35,23 +36,29 @@ struct FoldArgs {
     int F;
 };
 
-__global__ void fold_edge_terms(FoldArgs a) {
-    const int lr = blockIdx.x;          // l*3 + r
-    const int r = lr % 3;
+// one wavefront per (layer, relation, output channel); lanes split the k sum
+__global__ void __launch_bounds__(64) fold_edge_terms(FoldArgs a) {
     const int F = a.F;
+    const int lr = blockIdx.x / F, c = blockIdx.x % F;   // lr = l*3 + r
+    const int r = lr % 3;
     const int d = (r == 2) ? 2 : 1;
-    const float *W = a.layer_w + (size_t)lr * F * 2 * F;
-    for (int c = threadIdx.x; c < F; c += blockDim.x) {
-        float u0 = 0.f, u1 = 0.f, s = a.layer_b[(size_t)lr * F + c];
-        for (int k = 0; k < F; ++k) {
-            float we = W[(size_t)c * 2 * F + F + k];
-            u0 = fmaf(we, a.A[r][(size_t)k * d + 0], u0);
-            if (d == 2) u1 = fmaf(we, a.A[r][(size_t)k * d + 1], u1);
-            s = fmaf(we, a.c[r][k], s);
-        }
+    const float *W = a.layer_w + (size_t)lr * F * 2 * F + (size_t)c * 2 * F + F;   // row c of W^e
+    float u0 = 0.f, u1 = 0.f, s = 0.f;
+    for (int k = threadIdx.x; k < F; k += 64) {
+        const float we = W[k];
+        u0 = fmaf(we, a.A[r][(size_t)k * d + 0], u0);
+        if (d == 2) u1 = fmaf(we, a.A[r][(size_t)k * d + 1], u1);
+        s = fmaf(we, a.c[r][k], s);
+    }
+    for (int o = 32; o >= 1; o >>= 1) {
+        u0 += __shfl_xor(u0, o, 64);
+        u1 += __shfl_xor(u1, o, 64);
+        s += __shfl_xor(s, o, 64);
+    }
+    if (threadIdx.x == 0) {
         a.U[((size_t)lr * F + c) * 2 + 0] = u0;
         a.U[((size_t)lr * F + c) * 2 + 1] = u1;
-        a.cp[(size_t)lr * F + c] = s;
+        a.cp[(size_t)lr * F + c] = a.layer_b[(size_t)lr * F + c] + s;
     }
 }
 
@@ -65,131 +72,6 @@ __global__ void convert_wh_bf16(const float *layer_w, uint16_t *Wb, int F, int L
         int64_t n = rem / F, k = rem % F;
         Wb[i] = f2bf(layer_w[(lr * F + n) * 2 * F + k]);
     }
-}
-
-// --------------------------------------------------------- relation GEMM
-// Y[m][n] = sum_k H[m][k] * B[n][k], n < F from B0 (row stride ldb), n >= F
-// from B1.  64 x 64 block tile, 4 wavefronts each 32 x 32 (2 x 2 MFMA
-// 16x16 tiles).  MFMA 16x16 operand layout: lane l supplies row/column
-// l % 16 and k-slice l / 16; result register v of lane l is row
-// 4 (l / 16) + v, column l % 16.
-constexpr int TM = 64, TN = 64;
-
-// One launch covers both row sets of a layer: blocks [0, tiles0) take the op
-// rows (side 0), the rest the device rows (side 1).
-struct GemmSide {
-    const void *H;       // [rows][F]
-    int64_t rows;
-    const void *B0, *B1; // output channels [0, F) and [F, 2F)
-    int ldb;
-    void *Y;             // [rows][2F]
-};
-struct GemmArgs {
-    GemmSide side[2];
-    int64_t tiles0;
-    int F;
-};
-
-__global__ void __launch_bounds__(256) gemm_f32(GemmArgs G) {
-    constexpr int BK = 16;
-    __shared__ float As[TM][BK + 1];
-    __shared__ float Bs[TN][BK + 1];
-    const int sd = (int64_t)blockIdx.x < G.tiles0 ? 0 : 1;
-    const float *__restrict__ H = static_cast<const float *>(G.side[sd].H);
-    const int64_t rows = G.side[sd].rows;
-    const float *__restrict__ B0 = static_cast<const float *>(G.side[sd].B0);
-    const float *__restrict__ B1 = static_cast<const float *>(G.side[sd].B1);
-    const int ldb = G.side[sd].ldb, F = G.F;
-    float *__restrict__ Y = static_cast<float *>(G.side[sd].Y);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-    const int64_t m0 = ((int64_t)blockIdx.x - (sd ? G.tiles0 : 0)) * TM;
-    const int n0 = blockIdx.y * TN;
-    f4 acc[2][2];
-    for (int i = 0; i < 2; ++i)
-        for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
-    const int lrow = tid >> 2, lk = (tid & 3) * 4;
-    for (int k0 = 0; k0 < F; k0 += BK) {
-        {
-            int64_t gm = m0 + lrow;
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (gm < rows) v = *reinterpret_cast<const float4 *>(H + gm * F + k0 + lk);
-            As[lrow][lk + 0] = v.x; As[lrow][lk + 1] = v.y; As[lrow][lk + 2] = v.z; As[lrow][lk + 3] = v.w;
-            int gn = n0 + lrow;
-            const float *src = gn < F ? B0 + (size_t)gn * ldb : B1 + (size_t)(gn - F) * ldb;
-            float4 w = *reinterpret_cast<const float4 *>(src + k0 + lk);
-            Bs[lrow][lk + 0] = w.x; Bs[lrow][lk + 1] = w.y; Bs[lrow][lk + 2] = w.z; Bs[lrow][lk + 3] = w.w;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int kk = 0; kk < BK; kk += 4) {
-            float a[2], bv[2];
-            for (int i = 0; i < 2; ++i) a[i] = As[wm * 32 + i * 16 + (lane & 15)][kk + (lane >> 4)];
-            for (int j = 0; j < 2; ++j) bv[j] = Bs[wn * 32 + j * 16 + (lane & 15)][kk + (lane >> 4)];
-            for (int i = 0; i < 2; ++i)
-                for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], bv[j], acc[i][j], 0, 0, 0);
-        }
-        __syncthreads();
-    }
-    const int ldy = 2 * F;
-    for (int i = 0; i < 2; ++i)
-        for (int j = 0; j < 2; ++j)
-            for (int v = 0; v < 4; ++v) {
-                int64_t gm = m0 + wm * 32 + i * 16 + 4 * (lane >> 4) + v;
-                int gn = n0 + wn * 32 + j * 16 + (lane & 15);
-                if (gm < rows) Y[gm * ldy + gn] = acc[i][j][v];
-            }
-}
-
-__global__ void __launch_bounds__(256) gemm_bf16(GemmArgs G) {
-    constexpr int BK = 32, PADK = BK + 8;
-    __shared__ __attribute__((aligned(16))) uint16_t As[TM][PADK];
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[TN][PADK];
-    const int sd = (int64_t)blockIdx.x < G.tiles0 ? 0 : 1;
-    const uint16_t *__restrict__ H = static_cast<const uint16_t *>(G.side[sd].H);
-    const int64_t rows = G.side[sd].rows;
-    const uint16_t *__restrict__ B0 = static_cast<const uint16_t *>(G.side[sd].B0);
-    const uint16_t *__restrict__ B1 = static_cast<const uint16_t *>(G.side[sd].B1);
-    const int ldb = G.side[sd].ldb, F = G.F;
-    uint16_t *__restrict__ Y = static_cast<uint16_t *>(G.side[sd].Y);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-    const int64_t m0 = ((int64_t)blockIdx.x - (sd ? G.tiles0 : 0)) * TM;
-    const int n0 = blockIdx.y * TN;
-    f4 acc[2][2];
-    for (int i = 0; i < 2; ++i)
-        for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
-    const int lrow = tid >> 2, lk = (tid & 3) * 8;
-    for (int k0 = 0; k0 < F; k0 += BK) {
-        {
-            int64_t gm = m0 + lrow;
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (gm < rows) v = *reinterpret_cast<const uint4 *>(H + gm * F + k0 + lk);
-            *reinterpret_cast<uint4 *>(&As[lrow][lk]) = v;
-            int gn = n0 + lrow;
-            const uint16_t *src = gn < F ? B0 + (size_t)gn * ldb : B1 + (size_t)(gn - F) * ldb;
-            *reinterpret_cast<uint4 *>(&Bs[lrow][lk]) = *reinterpret_cast<const uint4 *>(src + k0 + lk);
-        }
-        __syncthreads();
-        bf8 a[2], bv[2];
-        for (int i = 0; i < 2; ++i)
-            a[i] = *reinterpret_cast<const bf8 *>(&As[wm * 32 + i * 16 + (lane & 15)][8 * (lane >> 4)]);
-        for (int j = 0; j < 2; ++j)
-            bv[j] = *reinterpret_cast<const bf8 *>(&Bs[wn * 32 + j * 16 + (lane & 15)][8 * (lane >> 4)]);
-        for (int i = 0; i < 2; ++i)
-            for (int j = 0; j < 2; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bv[j], acc[i][j], 0, 0, 0);
-        __syncthreads();
-    }
-    const int ldy = 2 * F;
-    for (int i = 0; i < 2; ++i)
-        for (int j = 0; j < 2; ++j)
-            for (int v = 0; v < 4; ++v) {
-                int64_t gm = m0 + wm * 32 + i * 16 + 4 * (lane >> 4) + v;
-                int gn = n0 + wn * 32 + j * 16 + (lane & 15);
-                if (gm < rows) Y[gm * ldy + gn] = f2bf(acc[i][j][v]);
-            }
 }
 
 // op destinations: B0 (op<-op) and B1 (op<-dev)
@@ -519,7 +401,7 @@ extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *
 
     FoldArgs fa{w->layer_w, w->layer_b, {w->enc_edge_w[0], w->enc_edge_w[1], w->enc_edge_w[2]},
                 {w->enc_edge_b[0], w->enc_edge_b[1], w->enc_edge_b[2]}, L.U, L.cp, F};
-    fold_edge_terms<<<NL * 3, 256, 0, stream>>>(fa);
+    fold_edge_terms<<<NL * 3 * F, 64, 0, stream>>>(fa);
     if (bf) convert_wh_bf16<<<256, 256, 0, stream>>>(w->layer_w, L.Wb, F, NL * 3);
 
     // encoders: hidden h0 in the working precision
@@ -558,24 +440,19 @@ extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *
         {
             GemmArgs ga{};
             ga.F = F;
-            ga.tiles0 = (rows_op + TM - 1) / TM;
-            const int64_t tiles1 = (rows_dev + TM - 1) / TM;
-            dim3 grid((unsigned)(ga.tiles0 + tiles1), (unsigned)(2 * F / TN));
+            ga.tiles0 = transform_row_tiles(rows_op);
             if (bf) {
                 const uint16_t *Wl = L.Wb + (size_t)l * 3 * F * F;
                 ga.side[0] = GemmSide{L.H_op[cur], rows_op, Wl + 0 * F * F, Wl + 1 * F * F, F, L.Y_op};
                 ga.side[1] = GemmSide{L.H_dev[cur], rows_dev, Wl + 2 * F * F, Wl + 1 * F * F, F, L.Y_dev};
-                prof_begin(TAG_STAGE_TRANSFORM, stream);
-                gemm_bf16<<<grid, 256, 0, stream>>>(ga);
-                prof_end(TAG_STAGE_TRANSFORM, stream);
             } else {
                 const float *Wl = w->layer_w + (size_t)l * 3 * F * 2 * F;
                 ga.side[0] = GemmSide{L.H_op[cur], rows_op, Wl + 0 * F * 2 * F, Wl + 1 * F * 2 * F, 2 * F, L.Y_op};
                 ga.side[1] = GemmSide{L.H_dev[cur], rows_dev, Wl + 2 * F * 2 * F, Wl + 1 * F * 2 * F, 2 * F, L.Y_dev};
-                prof_begin(TAG_STAGE_TRANSFORM, stream);
-                gemm_f32<<<grid, 256, 0, stream>>>(ga);
-                prof_end(TAG_STAGE_TRANSFORM, stream);
             }
+            prof_begin(TAG_STAGE_TRANSFORM, stream);
+            launch_transform(ga, bf, stream);
+            prof_end(TAG_STAGE_TRANSFORM, stream);
         }
         A.att_src = w->att_src + (size_t)l * 3 * F;
         A.att_dst = w->att_dst + (size_t)l * 3 * F;

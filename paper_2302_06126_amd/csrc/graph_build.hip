@@ -10,15 +10,14 @@
 // Entries of a row are ordered by (source id, edge id), which makes the
 // result a deterministic function of the input link sets.
 //
-// Pipeline (all on the caller's stream): fill counters, count per-row
-// degrees with integer atomics while validating ids, exclusive scan to row
-// pointers, scatter with per-row atomic cursors (arbitrary order inside a
-// row), then an exact per-row rank sort: each entry's final slot is the
-// number of entries of its row with a smaller (source, edge) key.  The rank
-// pass also detects repeated (row, source) pairs.  One stream sync at the
-// end reads the validation flags and per-bucket maximum degrees.
+// Pipeline (all on the caller's stream, seven kernels): clear counters;
+// count per-row degrees while validating ids (device rows counted in LDS
+// first, since few device rows receive many links); exclusive scans to row
+// pointers; clear cursors; scatter (arbitrary order inside a row); exact
+// per-row rank sort of short rows; LDS-bitmap counting sort of long rows.
+// The sorts also detect repeated (row, source) pairs.  One stream sync at
+// the end reads the validation flags and per-bucket maximum degrees.
 #include <algorithm>
-#include <mutex>
 
 #include "tag_internal.hpp"
 
@@ -39,8 +38,12 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kScanItems = 4;                       // per thread
 constexpr int kScanTile = kThreads * kScanItems;    // per block
+constexpr int kSmallScan = 1 << 16;                 // arrays up to this length: one block per bucket
+constexpr int kPrivRows = 4096;                     // device rows counted in LDS when the total fits
+constexpr int kShortRow = 256;                      // rows up to this length: per-entry rank
+constexpr int kBitmapRange = 16384;                 // source-id range sorted through an LDS bitmap
 
-// flags layout in the tmp buffer
+// flags after the counters in the tmp buffer
 enum { FLAG_RANGE = 0, FLAG_DUP = 1, FLAG_MAXDEG = 4 /* 4 entries */, FLAG_COUNT = 8 };
 
 __global__ void fill_i32(int32_t *p, int64_t n, int32_t v) {
@@ -50,7 +53,8 @@ __global__ void fill_i32(int32_t *p, int64_t n, int32_t v) {
 }
 
 // topology owning entry i of a prefix-offset array off[0..G]
-__device__ __forceinline__ int32_t owner(const int64_t *off, int32_t G, int64_t i) {
+template <typename T>
+__device__ __forceinline__ int32_t owner(const T *off, int32_t G, int64_t i) {
     int32_t lo = 0, hi = G;   // find last g with off[g] <= i
     while (hi - lo > 1) {
         int32_t mid = (lo + hi) >> 1;
@@ -59,54 +63,100 @@ __device__ __forceinline__ int32_t owner(const int64_t *off, int32_t G, int64_t 
     return lo;
 }
 
-struct EdgeArgs {
-    const int32_t *a, *b;      // per-edge endpoints (local ids)
-    const int64_t *off;        // device copy of the link prefix offsets [G+1]
-    const int32_t *a_off;      // node prefix offsets of endpoint a's type [G+1]
-    const int32_t *b_off;      // node prefix offsets of endpoint b's type [G+1]
-    int64_t n_edges;
-    int32_t G;
-    int32_t same_type;         // 1: a and b are the same node type (self links rejected)
-    // bucket fed as (row = b, col = a) and bucket fed as (row = a, col = b)
-    int32_t *cnt_ba, *cnt_ab;
-    const int32_t *rp_ba, *rp_ab;
-    int32_t *col_ba, *eid_ba, *rowof_ba;
-    int32_t *col_ab, *eid_ab, *rowof_ab;
+struct Buckets {
+    int64_t rows[4], nnz[4];
+    int32_t *cnt[4];
+    int32_t *rp[4];
+    int32_t *tcol[4], *teid[4], *rowof[4];
+    int32_t *col[4], *eid[4];
 };
 
-// mode 0: count degrees; mode 1: scatter entries
+struct Rel {                   // one link type
+    const int32_t *a, *b;      // endpoints (local ids)
+    const int64_t *off;        // link prefix offsets [G+1]
+    const int32_t *a_off, *b_off;   // node prefix offsets of a's and b's type [G+1]
+    int64_t n;
+    int32_t same_type;         // self links rejected
+    int32_t bk_ba, bk_ab;      // bucket fed as (row = b, col = a) and as (row = a, col = b)
+    int32_t priv_ba, priv_ab;  // that side's rows are device rows counted in LDS
+};
+
+struct EdgeArgs {
+    Rel rel[3];
+    int64_t blk_off[4];        // block ranges of the three relations
+    int32_t G;
+    int32_t n_dev;             // total device rows (LDS counter range)
+    Buckets B;
+    int32_t *flags;
+};
+
+// MODE 0: count degrees; MODE 1: scatter entries.  One thread per link.
 template <int MODE>
-__global__ void edges_pass(EdgeArgs A, int32_t *flags) {
-    int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (; i < A.n_edges; i += stride) {
-        int32_t g = owner(A.off, A.G, i);
-        int32_t la = A.a[i], lb = A.b[i];
-        int32_t na = A.a_off[g + 1] - A.a_off[g], nb = A.b_off[g + 1] - A.b_off[g];
+__global__ void __launch_bounds__(kThreads) edges_pass(EdgeArgs A) {
+    __shared__ int32_t lcnt[kPrivRows];
+    __shared__ int32_t lbase[kPrivRows];
+    const int64_t bid = blockIdx.x;
+    const int r = bid < A.blk_off[1] ? 0 : (bid < A.blk_off[2] ? 1 : 2);
+    const Rel R = r == 0 ? A.rel[0] : (r == 1 ? A.rel[1] : A.rel[2]);
+    const bool priv = R.priv_ba || R.priv_ab;
+    if (priv) {
+        for (int i = threadIdx.x; i < A.n_dev; i += blockDim.x) lcnt[i] = 0;
+        __syncthreads();
+    }
+    const int64_t i = (bid - A.blk_off[r]) * kThreads + threadIdx.x;
+    bool ok = i < R.n;
+    int32_t ga = 0, gb = 0;
+    if (ok) {
+        const int32_t g = owner(R.off, A.G, i);
+        const int32_t la = R.a[i], lb = R.b[i];
+        const int32_t na = R.a_off[g + 1] - R.a_off[g], nb = R.b_off[g + 1] - R.b_off[g];
         if (la < 0 || la >= na || lb < 0 || lb >= nb) {
-            if (MODE == 0) atomicOr(&flags[FLAG_RANGE], 1);
-            continue;
-        }
-        if (A.same_type && la == lb) {
-            if (MODE == 0) atomicOr(&flags[FLAG_DUP], 1);
-            continue;
-        }
-        int32_t ga = A.a_off[g] + la, gb = A.b_off[g] + lb;
-        if (MODE == 0) {
-            atomicAdd(&A.cnt_ba[gb], 1);
-            atomicAdd(&A.cnt_ab[ga], 1);
+            if (MODE == 0) atomicOr(&A.flags[FLAG_RANGE], 1);
+            ok = false;
+        } else if (R.same_type && la == lb) {
+            if (MODE == 0) atomicOr(&A.flags[FLAG_DUP], 1);
+            ok = false;
         } else {
-            int32_t p = A.rp_ba[gb] + atomicAdd(&A.cnt_ba[gb], 1);
-            A.col_ba[p] = ga; A.eid_ba[p] = (int32_t)i; A.rowof_ba[p] = gb;
-            int32_t q = A.rp_ab[ga] + atomicAdd(&A.cnt_ab[ga], 1);
-            A.col_ab[q] = gb; A.eid_ab[q] = (int32_t)i; A.rowof_ab[q] = ga;
+            ga = R.a_off[g] + la;
+            gb = R.b_off[g] + lb;
         }
+    }
+    // (row, col) of the two entries this link feeds
+    const int32_t row0 = gb, col0 = ga, bk0 = R.bk_ba, row1 = ga, col1 = gb, bk1 = R.bk_ab;
+    int32_t slot0 = 0, slot1 = 0;
+    if (ok) {
+        if (R.priv_ba) slot0 = atomicAdd(&lcnt[row0], 1);
+        else slot0 = atomicAdd(&A.B.cnt[bk0][row0], 1);
+        if (R.priv_ab) slot1 = atomicAdd(&lcnt[row1], 1);
+        else slot1 = atomicAdd(&A.B.cnt[bk1][row1], 1);
+    }
+    if (priv) {
+        // flush the LDS counters (both private sides of a relation share one bucket)
+        __syncthreads();
+        const int pb = R.priv_ba ? bk0 : bk1;
+        for (int d = threadIdx.x; d < A.n_dev; d += blockDim.x) {
+            const int32_t c = lcnt[d];
+            if (c) {
+                const int32_t base = atomicAdd(&A.B.cnt[pb][d], c);
+                if (MODE == 1) lbase[d] = base;
+            }
+        }
+        __syncthreads();
+        if (MODE == 1 && ok) {
+            if (R.priv_ba) slot0 += lbase[row0];
+            if (R.priv_ab) slot1 += lbase[row1];
+        }
+    }
+    if (MODE == 1 && ok) {
+        const int32_t p = A.B.rp[bk0][row0] + slot0;
+        A.B.tcol[bk0][p] = col0; A.B.teid[bk0][p] = (int32_t)i; A.B.rowof[bk0][p] = row0;
+        const int32_t q = A.B.rp[bk1][row1] + slot1;
+        A.B.tcol[bk1][q] = col1; A.B.teid[bk1][q] = (int32_t)i; A.B.rowof[bk1][q] = row1;
     }
 }
 
-// ---- exclusive scan of int32 counts (n + 1 outputs, out[n] = total) ----
+// ---- exclusive scans of int32 counts (n + 1 outputs, out[n] = total) ----
 __device__ __forceinline__ int32_t block_exclusive_scan(int32_t v, int32_t *total, int32_t *sh) {
-    // sh: kThreads ints
     int tid = threadIdx.x;
     sh[tid] = v;
     __syncthreads();
@@ -120,6 +170,29 @@ __device__ __forceinline__ int32_t block_exclusive_scan(int32_t v, int32_t *tota
     *total = sh[kThreads - 1];
     __syncthreads();
     return incl - v;
+}
+
+// one block per bucket, looping over tiles with a carry (moderate sizes)
+__global__ void __launch_bounds__(kThreads) scan_buckets(Buckets B) {
+    __shared__ int32_t sh[kThreads];
+    const int b = blockIdx.x;
+    const int64_t n = B.rows[b] + 1;
+    int32_t carry = 0;
+    for (int64_t base = 0; base < n; base += kScanTile) {
+        const int64_t i0 = base + threadIdx.x * kScanItems;
+        int32_t v[kScanItems], s = 0;
+        for (int k = 0; k < kScanItems; ++k) {
+            v[k] = (i0 + k < n) ? B.cnt[b][i0 + k] : 0;
+            s += v[k];
+        }
+        int32_t tot;
+        int32_t ex = block_exclusive_scan(s, &tot, sh) + carry;
+        for (int k = 0; k < kScanItems; ++k) {
+            if (i0 + k < n) B.rp[b][i0 + k] = ex;
+            ex += v[k];
+        }
+        carry += tot;
+    }
 }
 
 __global__ void scan_tiles(const int32_t *in, int64_t n, int32_t *out, int32_t *tile_sums) {
@@ -159,56 +232,55 @@ __global__ void scan_add(int32_t *out, int64_t n, const int32_t *tile_sums) {
     if (i < n) out[i] += tile_sums[i / kScanTile];
 }
 
-// ---- exact per-row rank sort ----
-constexpr int kShortRow = 256;        // rows up to this length: per-entry rank
-constexpr int kBitmapRange = 16384;   // source-id range sorted through an LDS bitmap
-
-// Only the first rp[n_rows] slots hold entries: links rejected during the
-// count pass (bad ids, self links) were never scattered.  Rows longer than
-// kShortRow are left to rank_long_rows.
-__global__ void rank_rows(const int32_t *rp, int64_t n_rows, const int32_t *tcol, const int32_t *teid,
-                          const int32_t *rowof, int64_t nnz, int32_t *col, int32_t *eid,
-                          int32_t *flags, int bucket) {
+// ---- exact per-row rank sort of short rows, all buckets in one launch ----
+// Only the first rp[rows] slots of a bucket hold entries: links rejected
+// during the count pass (bad ids, self links) were never scattered.
+__global__ void rank_rows(Buckets B, int64_t e1, int64_t e2, int64_t e3, int32_t *flags) {
     int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    if (p >= nnz || p >= rp[n_rows]) return;
-    int32_t r = rowof[p];
-    int32_t beg = rp[r], end = rp[r + 1];
+    const int b = p < e1 ? 0 : (p < e2 ? 1 : (p < e3 ? 2 : 3));
+    p -= b == 0 ? 0 : (b == 1 ? e1 : (b == 2 ? e2 : e3));
+    const int32_t *rp = B.rp[b];
+    if (p >= B.nnz[b] || p >= rp[B.rows[b]]) return;
+    const int32_t *tcol = B.tcol[b], *teid = B.teid[b];
+    const int32_t r = B.rowof[b][p];
+    const int32_t beg = rp[r], end = rp[r + 1];
     if (end - beg > kShortRow) return;
-    int32_t c = tcol[p], e = teid[p];
+    const int32_t c = tcol[p], e = teid[p];
     int32_t rank = 0, dup = 0;
     for (int32_t q = beg; q < end; ++q) {
-        int32_t cq = tcol[q], eq = teid[q];
+        const int32_t cq = tcol[q], eq = teid[q];
         rank += (cq < c) || (cq == c && eq < e);
         dup |= (cq == c) && (q != p);
     }
-    col[beg + rank] = c;
-    eid[beg + rank] = e;
+    B.col[b][beg + rank] = c;
+    B.eid[b][beg + rank] = e;
     if (dup) atomicOr(&flags[FLAG_DUP], 1);
-    if (rank == 0) atomicMax(&flags[FLAG_MAXDEG + bucket], end - beg);
+    if (rank == 0) atomicMax(&flags[FLAG_MAXDEG + b], end - beg);
 }
 
-// One block per long row.  Sources of a row all belong to the row's
+// One block per row of B0 (blocks [0, rows0)) or B2 (the rest); only rows
+// longer than kShortRow do work.  Sources of a row all belong to the row's
 // topology, so a bitmap over that topology's source-id range sorts the row
 // by source id (sources are unique in a valid row; a repeated source is
 // caught by the atomic OR).  Ranges beyond kBitmapRange fall back to the
 // per-entry rank inside the block.
-__global__ void __launch_bounds__(256) rank_long_rows(const int32_t *rp, const int32_t *tcol, const int32_t *teid,
-                                                      int32_t *col, int32_t *eid, int32_t *flags, int bucket,
-                                                      const int32_t *row_off, const int32_t *src_off, int32_t G) {
+__global__ void __launch_bounds__(256) rank_long_rows(Buckets B, const int32_t *op_off, const int32_t *dev_off,
+                                                      int32_t G, int32_t *flags) {
     __shared__ uint32_t bm[kBitmapRange / 32];
     __shared__ int32_t wpre[kBitmapRange / 32];
     __shared__ int32_t eid_of[kBitmapRange];
     __shared__ int32_t scan[256];
-    const int32_t r = blockIdx.x;
+    const int b = blockIdx.x < B.rows[0] ? 0 : 2;
+    const int32_t r = b == 0 ? (int32_t)blockIdx.x : (int32_t)(blockIdx.x - B.rows[0]);
+    const int32_t *rp = B.rp[b];
+    const int32_t *tcol = B.tcol[b], *teid = B.teid[b];
+    int32_t *col = B.col[b], *eid = B.eid[b];
     const int32_t beg = rp[r], end = rp[r + 1];
     if (end - beg <= kShortRow) return;
-    int32_t lo = 0, hi = G;
-    while (hi - lo > 1) {
-        const int32_t mid = (lo + hi) >> 1;
-        if (row_off[mid] <= r) lo = mid; else hi = mid;
-    }
-    const int32_t base = src_off[lo], range = src_off[lo + 1] - base;
-    if (threadIdx.x == 0) atomicMax(&flags[FLAG_MAXDEG + bucket], end - beg);
+    const int32_t *row_off = b == 0 ? op_off : dev_off;
+    const int32_t g = owner(row_off, G, r);
+    const int32_t base = op_off[g], range = op_off[g + 1] - base;   // sources are ops in both buckets
+    if (threadIdx.x == 0) atomicMax(&flags[FLAG_MAXDEG + b], end - beg);
     if (range > kBitmapRange) {
         for (int32_t p = beg + threadIdx.x; p < end; p += blockDim.x) {
             const int32_t c = tcol[p], e = teid[p];
@@ -255,11 +327,11 @@ __global__ void __launch_bounds__(256) rank_long_rows(const int32_t *rp, const i
         __syncthreads();
     }
     for (int w = threadIdx.x; w < nw; w += blockDim.x) {
-        uint32_t b = bm[w];
+        uint32_t bits = bm[w];
         int32_t pos = beg + wpre[w];
-        while (b) {
-            const int k = __ffs(b) - 1;
-            b &= b - 1u;
+        while (bits) {
+            const int k = __ffs(bits) - 1;
+            bits &= bits - 1u;
             const int32_t c = w * 32 + k;
             col[pos] = base + c;
             eid[pos] = eid_of[c];
@@ -318,22 +390,28 @@ tag_status check_desc(const tag_graph_desc *d, Sizes *s) {
     return TAG_OK;
 }
 
-struct CsrLayout {
-    int32_t *rowptr[4], *col[4], *eid[4];
-    int32_t *op_off, *dev_off;
-    int32_t *tiles, *tile_off;
-};
-
 int64_t count_tiles(const tag_graph_desc *d) {
     int64_t n = 0;
     for (int32_t g = 0; g < d->n_graphs; ++g) n += (d->n_op[g] + kOpTile - 1) / kOpTile;
     return n;
 }
+
+// persistent metadata block inside the CSR buffer (one host->device copy):
+// op_off [G+1] | dev_off [G+1] | tile_off [G+1] | tiles [n_tiles][3]
+struct CsrLayout {
+    int32_t *rowptr[4], *col[4], *eid[4];
+    int32_t *meta;
+    int32_t *op_off, *dev_off, *tile_off, *tiles;
+    size_t meta_ints;
+};
+// scratch: counters of all buckets, then the flags (one clear); link offsets (one copy)
 struct TmpLayout {
-    int32_t *cnt[4], *tcol[4], *teid[4], *rowof[4];
+    int32_t *cnt_all;          // [sum(rows + 1)] then flags [FLAG_COUNT]
+    int64_t cnt_ints;
+    int32_t *cnt[4], *flags;
+    int32_t *tcol[4], *teid[4], *rowof[4];
     int32_t *tile_sums;
-    int32_t *flags;
-    int64_t *oo_off, *dd_off, *od_off;
+    int64_t *links;            // oo_off [G+1] | dd_off [G+1] | od_off [G+1]
 };
 
 size_t carve_csr(const Sizes &s, int64_t n_tiles, void *base, CsrLayout *L) {
@@ -343,32 +421,39 @@ size_t carve_csr(const Sizes &s, int64_t n_tiles, void *base, CsrLayout *L) {
         L->col[b] = c.take<int32_t>(std::max<int64_t>(s.nnz[b], 1));
         L->eid[b] = c.take<int32_t>(std::max<int64_t>(s.nnz[b], 1));
     }
-    L->op_off = c.take<int32_t>(s.G + 1);
-    L->dev_off = c.take<int32_t>(s.G + 1);
-    L->tiles = c.take<int32_t>(3 * std::max<int64_t>(n_tiles, 1));
-    L->tile_off = c.take<int32_t>(s.G + 1);
+    L->meta_ints = 3 * (size_t)(s.G + 1) + 3 * (size_t)std::max<int64_t>(n_tiles, 1);
+    L->meta = c.take<int32_t>(L->meta_ints);
+    L->op_off = L->meta ? L->meta : nullptr;
+    L->dev_off = L->meta ? L->meta + (s.G + 1) : nullptr;
+    L->tile_off = L->meta ? L->meta + 2 * (s.G + 1) : nullptr;
+    L->tiles = L->meta ? L->meta + 3 * (s.G + 1) : nullptr;
     return c.used;
 }
 
 size_t carve_tmp(const Sizes &s, void *base, TmpLayout *L) {
     Carver c(base);
+    L->cnt_ints = 0;
+    for (int b = 0; b < 4; ++b) L->cnt_ints += s.rows[b] + 1;
+    L->cnt_all = c.take<int32_t>(L->cnt_ints + FLAG_COUNT);
+    int64_t off = 0;
+    for (int b = 0; b < 4; ++b) {
+        L->cnt[b] = L->cnt_all ? L->cnt_all + off : nullptr;
+        off += s.rows[b] + 1;
+    }
+    L->flags = L->cnt_all ? L->cnt_all + L->cnt_ints : nullptr;
     int64_t max_tiles = 1;
     for (int b = 0; b < 4; ++b) {
-        L->cnt[b] = c.take<int32_t>(s.rows[b] + 1);
         L->tcol[b] = c.take<int32_t>(std::max<int64_t>(s.nnz[b], 1));
         L->teid[b] = c.take<int32_t>(std::max<int64_t>(s.nnz[b], 1));
         L->rowof[b] = c.take<int32_t>(std::max<int64_t>(s.nnz[b], 1));
         max_tiles = std::max<int64_t>(max_tiles, (s.rows[b] + 1 + kScanTile - 1) / kScanTile);
     }
     L->tile_sums = c.take<int32_t>(max_tiles + 1);
-    L->flags = c.take<int32_t>(FLAG_COUNT);
-    L->oo_off = c.take<int64_t>(s.G + 1);
-    L->dd_off = c.take<int64_t>(s.G + 1);
-    L->od_off = c.take<int64_t>(s.G + 1);
+    L->links = c.take<int64_t>(3 * (size_t)(s.G + 1));
     return c.used;
 }
 
-// exclusive scan of cnt[0..n) into rp[0..n], rp[n] = total
+// exclusive scan of cnt[0..n) into rp[0..n], rp[n] = total (large arrays)
 void enqueue_scan(const int32_t *cnt, int64_t n, int32_t *rp, int32_t *tile_sums, hipStream_t st) {
     int64_t m = n + 1;   // scan n+1 values (cnt[n] is 0) so rp[n] = total
     unsigned tiles = (unsigned)((m + kScanTile - 1) / kScanTile);
@@ -428,25 +513,38 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
         g->op_off[i + 1] = g->op_off[i] + desc->n_op[i];
         g->dev_off[i + 1] = g->dev_off[i] + desc->n_dev[i];
     }
-    std::vector<int32_t> op_off32(g->op_off.begin(), g->op_off.end());
-    std::vector<int32_t> dev_off32(g->dev_off.begin(), g->dev_off.end());
-    // op tiles never cross a topology boundary
-    std::vector<int32_t> tiles;
-    std::vector<int32_t> tile_off(s.G + 1, 0);
-    tiles.reserve(3 * n_tiles);
-    for (int32_t gi = 0; gi < s.G; ++gi) {
-        int32_t nt = 0;
-        for (int32_t u = 0; u < desc->n_op[gi]; u += kOpTile, ++nt) {
-            tiles.push_back(static_cast<int32_t>(g->op_off[gi]) + u);
-            tiles.push_back(std::min<int32_t>(kOpTile, desc->n_op[gi] - u));
-            tiles.push_back(gi);
-        }
-        tile_off[gi + 1] = tile_off[gi] + nt;
-        g->max_tiles = std::max(g->max_tiles, nt);
-    }
-    g->n_tiles = static_cast<int32_t>(n_tiles);
     for (int b = 0; b < 4; ++b) { g->rows[b] = s.rows[b]; g->nnz[b] = s.nnz[b]; }
     if (hipGetDevice(&g->device) != hipSuccess) g->device = 0;
+
+    // host staging of the persistent metadata and of the link offsets
+    std::vector<int32_t> meta(cl.meta_ints, 0);
+    std::vector<int64_t> links(3 * (size_t)(s.G + 1));
+    {
+        int32_t *op_off = meta.data(), *dev_off = op_off + (s.G + 1), *tile_off = dev_off + (s.G + 1);
+        int32_t *tiles = tile_off + (s.G + 1);
+        int32_t nt = 0;
+        for (int32_t gi = 0; gi <= s.G; ++gi) {
+            op_off[gi] = (int32_t)g->op_off[gi];
+            dev_off[gi] = (int32_t)g->dev_off[gi];
+        }
+        for (int32_t gi = 0; gi < s.G; ++gi) {   // op tiles never cross a topology boundary
+            tile_off[gi] = nt;
+            int32_t cnt = 0;
+            for (int32_t u = 0; u < desc->n_op[gi]; u += kOpTile, ++cnt, ++nt) {
+                tiles[3 * nt] = op_off[gi] + u;
+                tiles[3 * nt + 1] = std::min<int32_t>(kOpTile, desc->n_op[gi] - u);
+                tiles[3 * nt + 2] = gi;
+            }
+            g->max_tiles = std::max(g->max_tiles, cnt);
+        }
+        tile_off[s.G] = nt;
+        g->n_tiles = nt;
+        for (int32_t gi = 0; gi <= s.G; ++gi) {
+            links[gi] = desc->oo_off[gi];
+            links[(s.G + 1) + gi] = desc->dd_off[gi];
+            links[2 * (s.G + 1) + gi] = desc->od_off[gi];
+        }
+    }
 
     auto fail = [&](tag_status code, const std::string &msg) {
         delete g;
@@ -459,52 +557,52 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
         if (e_ != hipSuccess) return fail(TAG_EHIP, std::string(#expr ": ") + hipGetErrorString(e_)); \
     } while (0)
 
-    BUILD_HIP(hipMemcpyAsync(cl.op_off, op_off32.data(), sizeof(int32_t) * (s.G + 1), hipMemcpyHostToDevice, stream));
-    BUILD_HIP(hipMemcpyAsync(cl.dev_off, dev_off32.data(), sizeof(int32_t) * (s.G + 1), hipMemcpyHostToDevice, stream));
-    BUILD_HIP(hipMemcpyAsync(cl.tiles, tiles.data(), sizeof(int32_t) * tiles.size(), hipMemcpyHostToDevice, stream));
-    BUILD_HIP(hipMemcpyAsync(cl.tile_off, tile_off.data(), sizeof(int32_t) * (s.G + 1), hipMemcpyHostToDevice, stream));
-    BUILD_HIP(hipMemcpyAsync(tl.oo_off, desc->oo_off, sizeof(int64_t) * (s.G + 1), hipMemcpyHostToDevice, stream));
-    BUILD_HIP(hipMemcpyAsync(tl.dd_off, desc->dd_off, sizeof(int64_t) * (s.G + 1), hipMemcpyHostToDevice, stream));
-    BUILD_HIP(hipMemcpyAsync(tl.od_off, desc->od_off, sizeof(int64_t) * (s.G + 1), hipMemcpyHostToDevice, stream));
+    BUILD_HIP(hipMemcpyAsync(cl.meta, meta.data(), sizeof(int32_t) * meta.size(), hipMemcpyHostToDevice, stream));
+    BUILD_HIP(hipMemcpyAsync(tl.links, links.data(), sizeof(int64_t) * links.size(), hipMemcpyHostToDevice, stream));
+
+    Buckets B{};
+    for (int b = 0; b < 4; ++b) {
+        B.rows[b] = s.rows[b]; B.nnz[b] = s.nnz[b];
+        B.cnt[b] = tl.cnt[b]; B.rp[b] = cl.rowptr[b];
+        B.tcol[b] = tl.tcol[b]; B.teid[b] = tl.teid[b]; B.rowof[b] = tl.rowof[b];
+        B.col[b] = cl.col[b]; B.eid[b] = cl.eid[b];
+    }
+    const int32_t priv = s.n_dev <= kPrivRows ? 1 : 0;
+    EdgeArgs ea{};
+    ea.G = s.G;
+    ea.n_dev = (int32_t)std::min<int64_t>(s.n_dev, kPrivRows);
+    ea.B = B;
+    ea.flags = tl.flags;
+    const int64_t *oo_off = tl.links, *dd_off = tl.links + (s.G + 1), *od_off = tl.links + 2 * (s.G + 1);
+    // op->op: (row = consumer, col = producer) and the reverse, both into B0
+    ea.rel[0] = Rel{desc->oo_src, desc->oo_dst, oo_off, cl.op_off, cl.op_off, s.e_oo, 1, 0, 0, 0, 0};
+    // dev-dev: both directions into B3 (device rows)
+    ea.rel[1] = Rel{desc->dd_a, desc->dd_b, dd_off, cl.dev_off, cl.dev_off, s.e_dd, 1, 3, 3, priv, priv};
+    // op-dev (op a, dev b): B2 row = dev (device rows), B1 row = op
+    ea.rel[2] = Rel{desc->od_op, desc->od_dev, od_off, cl.op_off, cl.dev_off, s.e_od, 0, 2, 1, priv, 0};
+    ea.blk_off[0] = 0;
+    ea.blk_off[1] = (s.e_oo + kThreads - 1) / kThreads;
+    ea.blk_off[2] = ea.blk_off[1] + (s.e_dd + kThreads - 1) / kThreads;
+    ea.blk_off[3] = ea.blk_off[2] + (s.e_od + kThreads - 1) / kThreads;
+    const int64_t nnz_all = s.nnz[0] + s.nnz[1] + s.nnz[2] + s.nnz[3];
 
     prof_begin(TAG_STAGE_GRAPH_BUILD, stream);
-    for (int b = 0; b < 4; ++b)
-        fill_i32<<<grid_for(s.rows[b] + 1), kThreads, 0, stream>>>(tl.cnt[b], s.rows[b] + 1, 0);
-    fill_i32<<<1, kThreads, 0, stream>>>(tl.flags, FLAG_COUNT, 0);
-
-    // op->op: row = consumer / col = producer (B0), and the reverse (B0)
-    EdgeArgs eo{desc->oo_src, desc->oo_dst, tl.oo_off, cl.op_off, cl.op_off, s.e_oo, s.G, 1,
-                tl.cnt[0], tl.cnt[0], cl.rowptr[0], cl.rowptr[0],
-                tl.tcol[0], tl.teid[0], tl.rowof[0], tl.tcol[0], tl.teid[0], tl.rowof[0]};
-    // op-dev: (op a, dev b): B2 row = dev, col = op; B1 row = op, col = dev
-    EdgeArgs ep{desc->od_op, desc->od_dev, tl.od_off, cl.op_off, cl.dev_off, s.e_od, s.G, 0,
-                tl.cnt[2], tl.cnt[1], cl.rowptr[2], cl.rowptr[1],
-                tl.tcol[2], tl.teid[2], tl.rowof[2], tl.tcol[1], tl.teid[1], tl.rowof[1]};
-    // dev-dev: both directions into B3
-    EdgeArgs ed{desc->dd_a, desc->dd_b, tl.dd_off, cl.dev_off, cl.dev_off, s.e_dd, s.G, 1,
-                tl.cnt[3], tl.cnt[3], cl.rowptr[3], cl.rowptr[3],
-                tl.tcol[3], tl.teid[3], tl.rowof[3], tl.tcol[3], tl.teid[3], tl.rowof[3]};
-    EdgeArgs *passes[3] = {&eo, &ep, &ed};
-    for (EdgeArgs *a : passes)
-        if (a->n_edges) edges_pass<0><<<grid_for(a->n_edges), kThreads, 0, stream>>>(*a, tl.flags);
-    for (int b = 0; b < 4; ++b) {
-        enqueue_scan(tl.cnt[b], s.rows[b], cl.rowptr[b], tl.tile_sums, stream);
-        fill_i32<<<grid_for(s.rows[b] + 1), kThreads, 0, stream>>>(tl.cnt[b], s.rows[b] + 1, 0);
+    fill_i32<<<grid_for(tl.cnt_ints + FLAG_COUNT), kThreads, 0, stream>>>(tl.cnt_all, tl.cnt_ints + FLAG_COUNT, 0);
+    if (ea.blk_off[3] > 0) edges_pass<0><<<(unsigned)ea.blk_off[3], kThreads, 0, stream>>>(ea);
+    if (std::max(s.rows[0], s.rows[2]) + 1 <= kSmallScan) {
+        scan_buckets<<<4, kThreads, 0, stream>>>(B);
+    } else {
+        for (int b = 0; b < 4; ++b) enqueue_scan(tl.cnt[b], s.rows[b], cl.rowptr[b], tl.tile_sums, stream);
     }
-    for (EdgeArgs *a : passes)
-        if (a->n_edges) edges_pass<1><<<grid_for(a->n_edges), kThreads, 0, stream>>>(*a, tl.flags);
-    for (int b = 0; b < 4; ++b)
-        if (s.nnz[b])
-            rank_rows<<<(unsigned)((s.nnz[b] + kThreads - 1) / kThreads), kThreads, 0, stream>>>(
-                cl.rowptr[b], s.rows[b], tl.tcol[b], tl.teid[b], tl.rowof[b], s.nnz[b], cl.col[b], cl.eid[b],
-                tl.flags, b);
+    fill_i32<<<grid_for(tl.cnt_ints), kThreads, 0, stream>>>(tl.cnt_all, tl.cnt_ints, 0);
+    if (ea.blk_off[3] > 0) edges_pass<1><<<(unsigned)ea.blk_off[3], kThreads, 0, stream>>>(ea);
+    if (nnz_all > 0)
+        rank_rows<<<(unsigned)((nnz_all + kThreads - 1) / kThreads), kThreads, 0, stream>>>(
+            B, s.nnz[0], s.nnz[0] + s.nnz[1], s.nnz[0] + s.nnz[1] + s.nnz[2], tl.flags);
     // op<-op and dev<-op rows can be long; op<-dev and dev<-dev rows have at most 64 entries
-    if (s.nnz[0])
-        rank_long_rows<<<(unsigned)s.rows[0], kThreads, 0, stream>>>(cl.rowptr[0], tl.tcol[0], tl.teid[0], cl.col[0],
-                                                                      cl.eid[0], tl.flags, 0, cl.op_off, cl.op_off, s.G);
-    if (s.nnz[2])
-        rank_long_rows<<<(unsigned)s.rows[2], kThreads, 0, stream>>>(cl.rowptr[2], tl.tcol[2], tl.teid[2], cl.col[2],
-                                                                      cl.eid[2], tl.flags, 2, cl.dev_off, cl.op_off, s.G);
+    if (s.nnz[0] + s.nnz[2] > 0)
+        rank_long_rows<<<(unsigned)(s.rows[0] + s.rows[2]), kThreads, 0, stream>>>(B, cl.op_off, cl.dev_off, s.G,
+                                                                                    tl.flags);
     prof_end(TAG_STAGE_GRAPH_BUILD, stream);
     {
         hipError_t e = hipGetLastError();

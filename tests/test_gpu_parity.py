@@ -73,6 +73,44 @@ def test_csr_union_of_topologies():
             assert np.array_equal(geid[seg[0]:seg[-1]] - eo[t], eid)
 
 
+def _check_union(topos):
+    g = P.Graph(topos)
+    op_off, dev_off = g.op_off, g.dev_off
+    e_off = {k: np.concatenate([[0], np.cumsum([len(getattr(t, k)) for t in topos])]) for k in ("oo_src", "od_op", "dd_a")}
+    for b in range(4):
+        grp, gcol, geid = g.export(b)
+        row_off = op_off if b in (0, 1) else dev_off
+        col_off = {0: op_off, 1: dev_off, 2: op_off, 3: dev_off}[b]
+        eo = {0: e_off["oo_src"], 1: e_off["od_op"], 2: e_off["od_op"], 3: e_off["dd_a"]}[b]
+        for t, topo in enumerate(topos):
+            rp, col, eid = _oracle_buckets(topo)[b]
+            seg = grp[row_off[t]:row_off[t + 1] + 1]
+            assert np.array_equal(seg - seg[0], rp), (b, t)
+            assert np.array_equal(gcol[seg[0]:seg[-1]] - col_off[t], col), (b, t)
+            assert np.array_equal(geid[seg[0]:seg[-1]] - eo[t], eid), (b, t)
+    return g
+
+
+def test_csr_hub_rows_and_large_ranges():
+    """An op with 700 op neighbours (long op<-op row), and a 20,000-op
+    topology whose device rows span more sources than the LDS bitmap holds."""
+    hub = mk_topo(900, 3, oo=[(i, 899) for i in range(700)] + [(i, i + 1) for i in range(700, 898)],
+                  dd=[(0, 1), (1, 2)], od=[(u, u % 3) for u in range(900)])
+    say("csr hub + 20k-op topology")
+    n = 20000
+    wide = mk_topo(n, 2, oo=[(i, i + 1) for i in range(0, n - 1, 7)], dd=[(0, 1)],
+                   od=[(u, j) for u in range(n) for j in range(2)])
+    g = _check_union([hub, wide])
+    assert g.info.max_degree[0] == 700 and g.info.max_degree[2] == n
+
+
+def test_csr_many_device_rows():
+    """More than 4,096 device rows in one batch (device counters in global memory)."""
+    topos = [synth.random_topology(200 + s, 6, 64, 8, od_per_op=5, dd_density=0.05) for s in range(70)]
+    say("csr 70 topologies x 64 devices")
+    _check_union(topos)
+
+
 @pytest.mark.parametrize("case,status", [
     ("oo_range", -2), ("od_range", -2), ("dd_range", -2), ("self_oo", -3), ("self_dd", -3),
     ("dup_oo", -3), ("both_dirs", -3), ("dup_od", -3), ("dup_dd_swapped", -3), ("range_beats_dup", -2)])
