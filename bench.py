@@ -29,11 +29,11 @@ METRIC = "candidate deployment graphs/sec and edges/sec; achieved HBM GB/s %"
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
 KERNEL_NAMES = {"graph_build": "graph build kernels", "encode": "small_gemm (encoders)",
-                "transform": "gemm_f32 / gemm_bf16", "agg_op_op": "agg_b0", "agg_op_dev": "agg_b1",
+                "transform": "gemm_f32 / gemm_bf16", "agg_op_op": "agg_op (per-row path)", "agg_op_dev": "agg_op_tile",
                 "agg_dev_op": "agg_b2", "agg_dev_merge": "agg_dev_final", "dev_prep": "dev_prep",
                 "decide": "decide kernels"}
 ONCE_PER_STEP = {"graph_build", "encode", "decide"}
-KERNEL_BASES = {"transform": ("gemm_f32", "gemm_bf16"), "agg_op_op": ("agg_b0", "agg_op"), "agg_op_dev": ("agg_b1",),
+KERNEL_BASES = {"transform": ("gemm_f32", "gemm_bf16"), "agg_op_op": ("agg_op",), "agg_op_dev": ("agg_op_tile",),
                 "agg_dev_op": ("agg_b2", "agg_dev_part"), "agg_dev_merge": ("agg_dev_final",),
                 "dev_prep": ("dev_prep",)}
 
@@ -73,10 +73,10 @@ def algorithmic_work(stage: str, wl, topo, R: int, info, n_slices: int, n_query:
     if stage == "agg_op_op":
         by = R * N * F * s + topo.e_oo * 4 + (N + 1) * 4 + 2 * topo.e_oo * 8 + R * N * F * 4
         return float(R * 2 * topo.e_oo * 8 * F), float(by)
-    if stage == "agg_op_dev":
-        by = (R * N * F * 4 + R * M * 2 * F * 4 + R * N * 16 + R * N * K * 4 + R * M * 4 * K * 4
-              + R * N * F * s)
-        return float(2 * R * topo.e_od * F), float(by)
+    if stage == "agg_op_dev":   # op destinations: op<-op gather + op<-dev contraction, one write
+        by = (R * N * F * s + topo.e_oo * 4 + (N + 1) * 4 + 2 * topo.e_oo * 8 + R * M * 2 * F * 4
+              + R * N * 16 + R * N * K * 4 + R * M * 4 * K * 4 + R * N * F * s)
+        return float(R * 2 * topo.e_oo * 8 * F + 2 * R * topo.e_od * F), float(by)
     if stage == "agg_dev_op":
         by = R * N * F * s + R * N * 16 + R * M * K * 4 + R * N * K * 4 + rec
         return float(2 * R * topo.e_od * F), float(by)

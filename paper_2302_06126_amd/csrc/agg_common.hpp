@@ -37,7 +37,6 @@ struct AggArgs {
     float *Sdev;                      // [R*n_dev][4][K]: p0, p1, q_od, q_dd of device rows
     float *T;                         // [R*n_dev][2][F]: device messages for bit 0 / 1
     float *qop;                       // [R*n_op][K]: q_od of op rows
-    float *O0;                        // [R*n_op][F]: gamma_same * op<-op aggregate
     int32_t rec_mode;                 // 0: records per 256-entry chunk, 1: per op tile
 };
 

@@ -12,8 +12,8 @@
 // as fp32 MFMA 16x16x4 products; the attention weights are formed in
 // registers as the A operand.  device <- op tiles write (max, sum, partial)
 // records that a merge pass combines in tile order; op <- device rows are
-// complete inside one tile and are normalised directly.  The op <- op
-// bucket stays a wavefront-per-row gather.
+// complete inside one tile and are normalised directly; the same kernel
+// gathers the tile's op <- op rows and writes each op row once.
 #include "agg_common.hpp"
 
 namespace tag {
@@ -81,71 +81,6 @@ __global__ void __launch_bounds__(256) dev_prep(AggArgs A) {
         const int h = lane / LPH;
         float *S = A.Sdev + i * 4 * K;
         S[h] = p0; S[K + h] = p1; S[2 * K + h] = qo; S[3 * K + h] = qd;
-    }
-}
-
-// op <- op: four op rows per wavefront (16 lanes and f/16 channels per lane
-// each), several neighbour rows in flight per op row; writes
-// gamma_same * aggregate to O0 (fp32)
-template <int F, int K, bool BF>
-__global__ void __launch_bounds__(256) agg_b0(AggArgs A) {
-    constexpr int CPL = F / 16;              // channels per lane
-    constexpr int LPH = 16 / K;              // lanes per head (K <= 16 on this path)
-    constexpr int EB = CPL >= 16 ? 2 : 4;    // neighbour rows loaded together
-    const int lane = threadIdx.x & 63;
-    const int li = lane & 15;
-    const int64_t nrows = (int64_t)A.R * A.n_op;
-    const int64_t w = ((int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6)) * 4 + (lane >> 4);
-    const bool live = w < nrows;
-    const int64_t wr = live ? w : nrows - 1;     // dead slots shadow a real row and store nothing
-    const int32_t rep = (int32_t)(wr / A.n_op);
-    const int32_t u = (int32_t)(wr % A.n_op);
-    const int c0 = li * CPL;
-    float a[CPL], u0[CPL], cp[CPL];
-    float q = 0.f;
-    {
-        float yd[CPL];
-        load_ch<CPL, BF>(A.Y_op, wr * 2 * F + c0, yd);
-        for (int c = 0; c < CPL; ++c) {
-            a[c] = A.att_src[c0 + c];
-            u0[c] = A.U[(size_t)(c0 + c) * 2];
-            cp[c] = A.cp[c0 + c];
-            q = fmaf(A.att_dst[c0 + c], yd[c], q);
-        }
-    }
-    q = head_sum<LPH>(q);
-    Online<CPL> o; o.init();
-    const int32_t beg = A.rp[0][u], end = A.rp[0][u + 1];
-    const float *xo = A.x_oo + (int64_t)rep * A.s_oo;
-    const int64_t ybase = (int64_t)rep * A.n_op * 2 * F + c0;
-    for (int32_t e = beg; e < end; e += EB) {
-        const int n = min(EB, end - e);
-        int32_t v[EB], id[EB];
-        for (int i = 0; i < EB; ++i) {
-            v[i] = i < n ? A.col[0][e + i] : 0;
-            id[i] = i < n ? A.eid[0][e + i] : 0;
-        }
-        float x[EB], y[EB][CPL];
-        for (int i = 0; i < EB; ++i) {
-            x[i] = i < n ? xo[id[i]] : 0.f;
-            if (i < n) load_ch<CPL, BF>(A.Y_op, ybase + (int64_t)v[i] * 2 * F, y[i]);
-        }
-        for (int i = 0; i < EB; ++i) {
-            if (i < n) {
-                float m[CPL], part = 0.f;
-                for (int c = 0; c < CPL; ++c) {
-                    m[c] = fmaxf(y[i][c] + fmaf(u0[c], x[i], cp[c]), 0.f);
-                    part = fmaf(a[c], m[c], part);
-                }
-                const float s2 = leaky(head_sum<LPH>(part) + q, A.slope) * kLog2e;
-                o.push(s2, m);
-            }
-        }
-    }
-    if (live) {
-        float *out = A.O0 + w * F + c0;
-        const float inv = end > beg ? A.g_same / o.den : 0.f;
-        for (int c = 0; c < CPL; ++c) out[c] = o.acc[c] * inv;
     }
 }
 
@@ -300,13 +235,21 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
         }
 }
 
-// op <- device over one 64-op tile, plus the op <- op part from O0
+// Op destinations of one 64-op tile.  op <- op: each wavefront gathers 16 of
+// the tile's rows, four at a time (16 lanes and f/16 channels per row), into
+// an LDS tile.  op <- device: MFMA contraction of the attention weights with
+// the device message table.  Both are combined and written once.
 template <int F, int K, bool BF>
-__global__ void __launch_bounds__(256) agg_b1(AggArgs A) {
+__global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
     constexpr int D = F / K;
     constexpr int WC = F / 4;
     constexpr int NCB = WC / 16;
     constexpr int HPW = WC >= D ? WC / D : 1;
+    constexpr int CPL = F / 16;              // op<-op channels per lane
+    constexpr int LPH = 16 / K;              // op<-op lanes per head (K <= 16 on this path)
+    constexpr int EB = CPL >= 16 ? 2 : 4;    // neighbour rows loaded together
+    constexpr int OS = F + 4;                // LDS tile row stride
+    __shared__ float Ot[kOpTile * OS];
     __shared__ uint64_t pres[kOpTile], bits[kOpTile];
     __shared__ float qo[kOpTile][K], mxS[kOpTile][K];
     __shared__ float P[64][2][K];
@@ -330,6 +273,7 @@ __global__ void __launch_bounds__(256) agg_b1(AggArgs A) {
         P[j][bh / K][bh % K] = j < Mg ? A.Sdev[((int64_t)r * A.n_dev + d0 + j) * 4 * K + bh] : 0.f;
     }
     __syncthreads();
+    // op <- device softmax maxima (LeakyReLU of the largest pre-activation)
     for (int i = tid; i < kOpTile * K; i += 256) {
         const int u = i / K, h = i % K;
         const uint64_t pr = pres[u], bt = bits[u];
@@ -337,6 +281,61 @@ __global__ void __launch_bounds__(256) agg_b1(AggArgs A) {
         for (int j = 0; j < Mg; ++j)
             if ((pr >> j) & 1ull) mx = fmaxf(mx, P[j][(bt >> j) & 1ull][h]);
         mxS[u][h] = mx == -INFINITY ? -INFINITY : leaky(mx + qo[u][h], A.slope) * kLog2e;
+    }
+    // op <- op into the LDS tile (gamma_same applied)
+    {
+        const int li = lane & 15;
+        const int c0 = li * CPL;
+        float a[CPL], u0c[CPL], cp[CPL], ad[CPL];
+        for (int c = 0; c < CPL; ++c) {
+            a[c] = A.att_src[c0 + c];
+            u0c[c] = A.U[(size_t)(c0 + c) * 2];
+            cp[c] = A.cp[c0 + c];
+            ad[c] = A.att_dst[c0 + c];
+        }
+        const float *xo = A.x_oo + (int64_t)r * A.s_oo;
+        const int64_t ybase = (int64_t)r * A.n_op * 2 * F + c0;
+        for (int it = 0; it < 4; ++it) {
+            const int ul = wave * 16 + it * 4 + (lane >> 4);
+            const bool live = ul < nu;
+            const int32_t u = u0 + (live ? ul : 0);
+            float q = 0.f;
+            {
+                float yd[CPL];
+                load_ch<CPL, BF>(A.Y_op, ybase + (int64_t)u * 2 * F, yd);
+                for (int c = 0; c < CPL; ++c) q = fmaf(ad[c], yd[c], q);
+            }
+            q = head_sum<LPH>(q);
+            Online<CPL> o; o.init();
+            const int32_t beg = A.rp[0][u], end = A.rp[0][u + 1];
+            for (int32_t e = beg; e < end; e += EB) {
+                const int n = min(EB, end - e);
+                int32_t v[EB], id[EB];
+                for (int i = 0; i < EB; ++i) {
+                    v[i] = i < n ? A.col[0][e + i] : 0;
+                    id[i] = i < n ? A.eid[0][e + i] : 0;
+                }
+                float x[EB], y[EB][CPL];
+                for (int i = 0; i < EB; ++i) {
+                    x[i] = i < n ? xo[id[i]] : 0.f;
+                    if (i < n) load_ch<CPL, BF>(A.Y_op, ybase + (int64_t)v[i] * 2 * F, y[i]);
+                }
+                for (int i = 0; i < EB; ++i) {
+                    if (i < n) {
+                        float m[CPL], part = 0.f;
+                        for (int c = 0; c < CPL; ++c) {
+                            m[c] = fmaxf(y[i][c] + fmaf(u0c[c], x[i], cp[c]), 0.f);
+                            part = fmaf(a[c], m[c], part);
+                        }
+                        const float s2 = leaky(head_sum<LPH>(part) + q, A.slope) * kLog2e;
+                        o.push(s2, m);
+                    }
+                }
+            }
+            const float inv = end > beg ? A.g_same / o.den : 0.f;
+            if (live)
+                for (int c = 0; c < CPL; ++c) Ot[ul * OS + c0 + c] = o.acc[c] * inv;
+        }
     }
     __syncthreads();
 
@@ -401,7 +400,7 @@ __global__ void __launch_bounds__(256) agg_b1(AggArgs A) {
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) {
                 const int col = cbase + cb * 16 + (lane & 15);
-                const float val = fmaf(scale[cb / CPH][v], acc[rb][cb][v], A.O0[row * F + col]);
+                const float val = fmaf(scale[cb / CPH][v], acc[rb][cb][v], Ot[u * OS + col]);
                 if (A.out_f32) static_cast<float *>(A.H_op)[row * F + col] = val;
                 else static_cast<uint16_t *>(A.H_op)[row * F + col] = f2bf(val);
             }
@@ -420,12 +419,10 @@ void launch_mfma(const AggArgs &A, hipStream_t st) {
     prof_begin(TAG_STAGE_AGG_DEV_OP, st);
     agg_b2<F, K, BF><<<tiles, 256, 0, st>>>(A);
     prof_end(TAG_STAGE_AGG_DEV_OP, st);
-    prof_begin(TAG_STAGE_AGG_OP_OP, st);
-    agg_b0<F, K, BF><<<(unsigned)((op_waves + 4 * kWaves - 1) / (4 * kWaves)), 256, 0, st>>>(A);
-    prof_end(TAG_STAGE_AGG_OP_OP, st);
     prof_begin(TAG_STAGE_AGG_OP_DEV, st);
-    agg_b1<F, K, BF><<<tiles, 256, 0, st>>>(A);
+    agg_op_tile<F, K, BF><<<tiles, 256, 0, st>>>(A);
     prof_end(TAG_STAGE_AGG_OP_DEV, st);
+    (void)op_waves;
 }
 
 template <int F, bool BF>

@@ -251,7 +251,7 @@ struct FwdLayout {
     int32_t maxc;
     bool mfma;
     uint64_t *omask;
-    float *Sdev, *T, *qop, *O0;
+    float *Sdev, *T, *qop;
 };
 
 tag_status check_dims(const tag_model_dims *d) {
@@ -293,10 +293,9 @@ size_t carve_fwd(const tag_graph *g, const tag_model_dims *d, int32_t R, void *b
         L->Sdev = c.take<float>((size_t)R * g->n_dev * 4 * d->heads);
         L->T = c.take<float>((size_t)R * g->n_dev * 2 * F);
         L->qop = c.take<float>((size_t)R * g->n_op * d->heads);
-        L->O0 = c.take<float>((size_t)R * g->n_op * F);
     } else {
         L->omask = nullptr;
-        L->Sdev = L->T = L->qop = L->O0 = nullptr;
+        L->Sdev = L->T = L->qop = nullptr;
     }
     return c.used;
 }
@@ -429,7 +428,7 @@ extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *
     A.part = L.part; A.maxc = L.maxc;
     A.G = g->G; A.n_tiles = g->n_tiles;
     A.tiles = g->tiles_d; A.tile_off = g->tile_off_d; A.op_off = g->op_off_d; A.dev_off = g->dev_off_d;
-    A.omask = L.omask; A.Sdev = L.Sdev; A.T = L.T; A.qop = L.qop; A.O0 = L.O0;
+    A.omask = L.omask; A.Sdev = L.Sdev; A.T = L.T; A.qop = L.qop;
     A.rec_mode = L.mfma ? 1 : 0;
     if (L.mfma) launch_pack_masks(A, stream);
 
