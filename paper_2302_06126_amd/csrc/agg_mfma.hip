@@ -118,7 +118,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     }
     for (int i = tid; i < 64 * K; i += 256) {
         const int j = i / K, h = i % K;
-        qd[j][h] = j < Mg ? A.Sdev[((int64_t)r * A.n_dev + d0 + j) * 4 * K + 2 * K + h] : 0.f;
+        qd[j][h] = j < Mg ? A.Sdev[((int64_t)r * A.n_dev + d0 + j) * 4 * K + 2 * K + h] * kLog2e : 0.f;
     }
     for (int i = tid; i < kOpTile * (F / 4); i += 256) {
         const int u = i / (F / 4), c = (i % (F / 4)) * 4;
@@ -138,8 +138,8 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
             p1 = fmaf(aS[c], fmaxf(yc + US[c], 0.f), p1);
             q = fmaf(adS[c], y, q);
         }
-        pb[u][0][h] = p0;
-        pb[u][1][h] = p1;
+        pb[u][0][h] = p0 * kLog2e;   // exp2-domain logits
+        pb[u][1][h] = p1 * kLog2e;
         if (u < nu) A.qop[((int64_t)r * A.n_op + u0 + u) * K + h] = q;
     }
     __syncthreads();
@@ -153,7 +153,8 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
             const float v = ((bt >> j) & 1ull) ? pb[u][1][h] : pb[u][0][h];
             mx = ((pr >> j) & 1ull) ? fmaxf(mx, v) : mx;
         }
-        mxS[j][h] = mx == -INFINITY ? -INFINITY : leaky(mx + qd[j][h], A.slope) * kLog2e;
+        const float x = mx + qd[j][h];
+        mxS[j][h] = mx == -INFINITY ? -INFINITY : fmaxf(x, A.slope * x);
     }
     __syncthreads();
 
@@ -176,26 +177,42 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
 #pragma unroll
         for (int hh = 0; hh < HPW; ++hh) zl[rb][hh] = 0.f;
     }
+    const int b = (lane >> 4) & 1;
+    const float slope = A.slope;
+    // per-lane constants of the lane's device rows j = rb*16 + l%16
+    float q2[4][HPW], m2[4][HPW];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+        const int j = rb * 16 + (lane & 15);
+#pragma unroll
+        for (int hh = 0; hh < HPW; ++hh) {
+            q2[rb][hh] = qd[j][h0 + hh];
+            m2[rb][hh] = j < Mg ? mxS[j][h0 + hh] : 0.f;
+        }
+    }
     for (int s = 0; s < kOpTile / 2; ++s) {
         const int ul = 2 * s + (lane >> 5);
-        const int b = (lane >> 4) & 1;
-        const uint64_t pr = pres[ul], bt = bits[ul];
+        const uint64_t pr = pres[ul], bt = b ? bits[ul] : ~bits[ul];   // bt bit j: link bit equals b
         float bv[NCB];
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) {
             const float yc = Ys[ul * YS + cbase + cb * 16 + (lane & 15)] + cpv[cb];
             bv[cb] = fmaxf(b ? yc + Uv[cb] : yc, 0.f);
         }
+        float pu[HPW];
+#pragma unroll
+        for (int hh = 0; hh < HPW; ++hh) pu[hh] = pb[ul][b][h0 + hh];
+        const uint64_t sel = pr & bt;
 #pragma unroll
         for (int rb = 0; rb < 4; ++rb) {
             if (rb < NRB) {
                 const int j = rb * 16 + (lane & 15);
-                const bool on = j < Mg && ((pr >> j) & 1ull) && ((int)((bt >> j) & 1ull) == b);
+                const bool on = (sel >> j) & 1ull;   // j < Mg holds for every set bit
 #pragma unroll
                 for (int hh = 0; hh < HPW; ++hh) {
                     const int h = h0 + hh;
-                    const float af = on ? __builtin_amdgcn_exp2f(leaky(pb[ul][b][h] + qd[j][h], A.slope) * kLog2e - mxS[j][h])
-                                        : 0.f;
+                    const float x = pu[hh] + q2[rb][hh];
+                    const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
                     zl[rb][hh] += af;
 #pragma unroll
                     for (int c2 = 0; c2 < CPH; ++c2)
@@ -264,13 +281,14 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
         pres[i] = ok ? A.omask[mi] : 0ull;
         bits[i] = ok ? A.omask[mi + 1] : 0ull;
     }
+    // logits in the exp2 domain: LeakyReLU commutes with the positive factor log2(e)
     for (int i = tid; i < kOpTile * K; i += 256) {
         const int u = i / K, h = i % K;
-        qo[u][h] = u < nu ? A.qop[((int64_t)r * A.n_op + u0 + u) * K + h] : 0.f;
+        qo[u][h] = u < nu ? A.qop[((int64_t)r * A.n_op + u0 + u) * K + h] * kLog2e : 0.f;
     }
     for (int i = tid; i < 64 * 2 * K; i += 256) {
         const int j = i / (2 * K), bh = i % (2 * K);
-        P[j][bh / K][bh % K] = j < Mg ? A.Sdev[((int64_t)r * A.n_dev + d0 + j) * 4 * K + bh] : 0.f;
+        P[j][bh / K][bh % K] = j < Mg ? A.Sdev[((int64_t)r * A.n_dev + d0 + j) * 4 * K + bh] * kLog2e : 0.f;
     }
     __syncthreads();
     // op <- device softmax maxima (LeakyReLU of the largest pre-activation)
@@ -280,7 +298,8 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
         float mx = -INFINITY;
         for (int j = 0; j < Mg; ++j)
             if ((pr >> j) & 1ull) mx = fmaxf(mx, P[j][(bt >> j) & 1ull][h]);
-        mxS[u][h] = mx == -INFINITY ? -INFINITY : leaky(mx + qo[u][h], A.slope) * kLog2e;
+        const float x = mx + qo[u][h];
+        mxS[u][h] = mx == -INFINITY ? -INFINITY : fmaxf(x, A.slope * x);
     }
     // op <- op into the LDS tile (gamma_same applied)
     {
@@ -353,21 +372,42 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
     }
     const float *Tb = A.T + ((int64_t)r * A.n_dev + d0) * 2 * F;
     const int steps = (Mg + 1) / 2;
+    const int b = (lane >> 4) & 1;
+    // per-lane constants of the lane's op rows u = rb*16 + l%16; the masks are
+    // pre-shifted to this lane's first device (j = l/32) and advance two per step
+    uint64_t prs[4], bts[4];
+    float q2[4][HPW], m2[4][HPW];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+        const int u = rb * 16 + (lane & 15);
+        prs[rb] = pres[u] >> (lane >> 5);
+        bts[rb] = bits[u] >> (lane >> 5);
+#pragma unroll
+        for (int hh = 0; hh < HPW; ++hh) {
+            q2[rb][hh] = qo[u][h0 + hh];
+            m2[rb][hh] = mxS[u][h0 + hh];
+        }
+    }
+    const float slope = A.slope;
     for (int s = 0; s < steps; ++s) {
         const int j = 2 * s + (lane >> 5);
-        const int b = (lane >> 4) & 1;
         const bool jok = j < Mg;
         float bv[NCB];
+#pragma unroll
         for (int cb = 0; cb < NCB; ++cb)
             bv[cb] = jok ? Tb[((int64_t)j * 2 + b) * F + cbase + cb * 16 + (lane & 15)] : 0.f;
+        float pj[HPW];
+#pragma unroll
+        for (int hh = 0; hh < HPW; ++hh) pj[hh] = P[j][b][h0 + hh];
+#pragma unroll
         for (int rb = 0; rb < 4; ++rb) {
-            const int u = rb * 16 + (lane & 15);
-            const bool on = jok && ((pres[u] >> j) & 1ull) && ((int)((bits[u] >> j) & 1ull) == b);
+            const bool on = jok && (prs[rb] & 1ull) && ((int)(bts[rb] & 1ull) == b);
+            prs[rb] >>= 2;
+            bts[rb] >>= 2;
 #pragma unroll
             for (int hh = 0; hh < HPW; ++hh) {
-                const int h = h0 + hh;
-                const float af = on ? __builtin_amdgcn_exp2f(leaky(P[j][b][h] + qo[u][h], A.slope) * kLog2e - mxS[u][h])
-                                    : 0.f;
+                const float x = pj[hh] + q2[rb][hh];
+                const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
                 zl[rb][hh] += af;
 #pragma unroll
                 for (int c2 = 0; c2 < CPH; ++c2)
