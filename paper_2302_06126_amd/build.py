@@ -15,6 +15,7 @@ LIB = os.path.join(HERE, "libtag.so")
 # host pass warns that it does not know the feature, which is harmless).
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-mllvm", "-amdgpu-mfma-vgpr-form",
          "-Wno-unused-result", "-I" + os.path.join(ROOT, "include")]
 
 

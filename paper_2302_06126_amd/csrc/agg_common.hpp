@@ -36,8 +36,11 @@ struct AggArgs {
     uint64_t *omask;                  // [R*n_op][2]: present / placement-bit masks over local devices
     float *Sdev;                      // [R*n_dev][4][K]: p0, p1, q_od, q_dd of device rows
     float *T;                         // [R*n_dev][2][F]: device messages for bit 0 / 1
-    float *qop;                       // [R*n_op][K]: q_od of op rows
-    int32_t rec_mode;                 // 0: records per 256-entry chunk, 1: per op tile
+    float *Sop;                       // [R*n_op][4][K]: p0, p1, q_od, q_oo of op rows
+    int32_t prep_done;                // Sop, Sdev and T already written by the transform
+    int32_t rec_mode;                 // 0: records per 256-entry chunk, 1: per tile group
+    int32_t n_groups;
+    const int32_t *groups, *group_off;   // tile groups of the device<-op blocks
 };
 
 // MFMA path (agg_mfma.hip)
@@ -118,6 +121,30 @@ struct Online {
         float p = __builtin_amdgcn_exp2f(s2 - nm);
         den = fmaf(den, sc, p);
         for (int c = 0; c < CPL; ++c) acc[c] = fmaf(acc[c], sc, p * m[c]);
+        mx = nm;
+    }
+    // the first n of EB entries, one rescale for the batch
+    template <int EB>
+    __device__ void push_n(const float (&s2)[EB], const float (&m)[EB][CPL], int n) {
+        float nm = mx;
+#pragma unroll
+        for (int i = 0; i < EB; ++i)
+            if (i < n) nm = fmaxf(nm, s2[i]);
+        const float sc = __builtin_amdgcn_exp2f(mx - nm);
+        float p[EB];
+#pragma unroll
+        for (int i = 0; i < EB; ++i) p[i] = i < n ? __builtin_amdgcn_exp2f(s2[i] - nm) : 0.f;
+        float ps = 0.f;
+#pragma unroll
+        for (int i = 0; i < EB; ++i) ps += p[i];
+        den = fmaf(den, sc, ps);
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            float a = acc[c] * sc;
+#pragma unroll
+            for (int i = 0; i < EB; ++i) a = fmaf(p[i], m[i][c], a);
+            acc[c] = a;
+        }
         mx = nm;
     }
 };

@@ -50,126 +50,133 @@ __global__ void __launch_bounds__(256) pack_op_masks(AggArgs A) {
     }
 }
 
-// per device row: message table T (bit 0 / 1), their logits p0, p1, and the
-// destination terms q_od, q_dd
+// Attention terms of node rows when the transform epilogue cannot form them
+// (heads wider than 64 channels): per row, S = (p0, p1, q_od, q_same) and, for
+// device rows, the message table T (bit 0 / 1).  One wavefront per row.
 template <int F, int K, bool BF>
-__global__ void __launch_bounds__(256) dev_prep(AggArgs A) {
+__global__ void __launch_bounds__(256) prep_rows(AggArgs A, int dev_side) {
     constexpr int CPL = F / 64, LPH = 64 / K;
     const int lane = threadIdx.x & 63;
     const int64_t i = (int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6);
-    if (i >= (int64_t)A.R * A.n_dev) return;
+    const int64_t rows = (int64_t)A.R * (dev_side ? A.n_dev : A.n_op);
+    if (i >= rows) return;
+    const void *Y = dev_side ? A.Y_dev : A.Y_op;
+    float *Sr = dev_side ? A.Sdev : A.Sop;
     const int c0 = lane * CPL;
     RelConst<CPL> od; od.load(A, 1, F, c0);
-    RelConst<CPL> dd; dd.load(A, 2, F, c0);
-    float yo[CPL], yd[CPL];
-    load_ch<CPL, BF>(A.Y_dev, i * 2 * F + F + c0, yo);
-    load_ch<CPL, BF>(A.Y_dev, i * 2 * F + c0, yd);
-    float p0 = 0.f, p1 = 0.f, qo = 0.f, qd = 0.f;
+    RelConst<CPL> same; same.load(A, dev_side ? 2 : 0, F, c0);
+    float yo[CPL], ys[CPL];
+    load_ch<CPL, BF>(Y, i * 2 * F + F + c0, yo);
+    load_ch<CPL, BF>(Y, i * 2 * F + c0, ys);
+    float p0 = 0.f, p1 = 0.f, qo = 0.f, qs = 0.f;
     for (int c = 0; c < CPL; ++c) {
         const float yc = yo[c] + od.cp[c];
         const float t0 = fmaxf(yc, 0.f), t1 = fmaxf(yc + od.u0[c], 0.f);
-        A.T[(i * 2 + 0) * F + c0 + c] = t0;
-        A.T[(i * 2 + 1) * F + c0 + c] = t1;
+        if (dev_side) {
+            A.T[(i * 2 + 0) * F + c0 + c] = t0;
+            A.T[(i * 2 + 1) * F + c0 + c] = t1;
+        }
         p0 = fmaf(od.a[c], t0, p0);
         p1 = fmaf(od.a[c], t1, p1);
         qo = fmaf(od.ad[c], yo[c], qo);
-        qd = fmaf(dd.ad[c], yd[c], qd);
+        qs = fmaf(same.ad[c], ys[c], qs);
     }
     p0 = head_sum<LPH>(p0); p1 = head_sum<LPH>(p1);
-    qo = head_sum<LPH>(qo); qd = head_sum<LPH>(qd);
+    qo = head_sum<LPH>(qo); qs = head_sum<LPH>(qs);
     if ((lane % LPH) == 0) {
         const int h = lane / LPH;
-        float *S = A.Sdev + i * 4 * K;
-        S[h] = p0; S[K + h] = p1; S[2 * K + h] = qo; S[3 * K + h] = qd;
+        float *S = Sr + i * 4 * K;
+        S[h] = p0; S[K + h] = p1; S[2 * K + h] = qo; S[3 * K + h] = qs;
     }
 }
 
-// device <- op over one 64-op tile: partial (max, sum, accumulator) records
+// order-preserving float <-> int keys (LDS integer max atomics on floats)
+__device__ __forceinline__ int fkey(float x) {
+    const int i = __float_as_int(x);
+    return i < 0 ? i ^ 0x7fffffff : i;
+}
+__device__ __forceinline__ float fdekey(int k) { return __int_as_float(k < 0 ? k ^ 0x7fffffff : k); }
+
+// device <- op over one group of consecutive 64-op tiles of a topology.  A
+// first pass takes the exact softmax maxima of the group's links (every
+// (op, head) raises the maxima of its linked devices); the MFMA passes then
+// accumulate every tile against those fixed maxima, so the device-row
+// accumulators stay in registers across the group, and one (max, sum,
+// partial) record per device row is written at the end.
 template <int F, int K, bool BF>
 __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     constexpr int D = F / K;                       // head width (>= 16 here)
     constexpr int WC = F / 4;                      // columns per wavefront
     constexpr int NCB = WC / 16;                   // 16-column blocks per wavefront
     constexpr int HPW = WC >= D ? WC / D : 1;      // heads per wavefront
+    constexpr int CPH = NCB / HPW;                 // column blocks per head inside a wavefront
     constexpr int YS = F + 4;                      // padded LDS row
     __shared__ float Ys[kOpTile * YS];
     __shared__ uint64_t pres[kOpTile], bits[kOpTile];
     __shared__ float pb[kOpTile][2][K];
-    __shared__ float qd[64][K], mxS[64][K];
-    __shared__ float cpS[F], US[F], aS[F], adS[F];
+    __shared__ int mxk[64][K];
+    __shared__ float qd[64][K], mrun[64][K];
+    __shared__ float cpS[F], US[F];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int32_t t = blockIdx.x, r = blockIdx.y;
-    const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1], g = A.tiles[3 * t + 2];
+    const int32_t r = blockIdx.y;
+    const int32_t t0 = A.groups[2 * blockIdx.x];
+    const int32_t t1 = t0 + A.groups[2 * blockIdx.x + 1];
+    const int32_t g = A.tiles[3 * t0 + 2];
     const int32_t d0 = A.dev_off[g], Mg = A.dev_off[g + 1] - d0;
-    const int32_t chunk = t - A.tile_off[g];
+    const int32_t chunk = (int32_t)blockIdx.x - A.group_off[g];
+    const float *Sop = A.Sop + (int64_t)r * A.n_op * 4 * K;
+    const uint64_t *om = A.omask + (int64_t)r * A.n_op * 2;
+    const float slope = A.slope;
 
     for (int i = tid; i < F; i += 256) {
         cpS[i] = A.cp[F + i];
         US[i] = A.U[(size_t)(F + i) * 2];
-        aS[i] = A.att_src[F + i];
-        adS[i] = A.att_dst[F + i];
-    }
-    for (int i = tid; i < kOpTile; i += 256) {
-        const bool ok = i < nu;
-        const int64_t mi = 2 * ((int64_t)r * A.n_op + u0 + i);
-        pres[i] = ok ? A.omask[mi] : 0ull;
-        bits[i] = ok ? A.omask[mi + 1] : 0ull;
     }
     for (int i = tid; i < 64 * K; i += 256) {
         const int j = i / K, h = i % K;
         qd[j][h] = j < Mg ? A.Sdev[((int64_t)r * A.n_dev + d0 + j) * 4 * K + 2 * K + h] * kLog2e : 0.f;
-    }
-    for (int i = tid; i < kOpTile * (F / 4); i += 256) {
-        const int u = i / (F / 4), c = (i % (F / 4)) * 4;
-        float v[4] = {0.f, 0.f, 0.f, 0.f};
-        if (u < nu) load_ch<4, BF>(A.Y_op, ((int64_t)r * A.n_op + u0 + u) * 2 * F + F + c, v);
-        for (int q = 0; q < 4; ++q) Ys[u * YS + c + q] = v[q];
+        mxk[j][h] = INT_MIN;
     }
     __syncthreads();
-    // op-side logits of both message variants, and q_od of the op rows
-    for (int i = tid; i < kOpTile * K; i += 256) {
-        const int u = i / K, h = i % K;
-        float p0 = 0.f, p1 = 0.f, q = 0.f;
-        for (int c = h * D; c < (h + 1) * D; ++c) {
-            const float y = Ys[u * YS + c];
-            const float yc = y + cpS[c];
-            p0 = fmaf(aS[c], fmaxf(yc, 0.f), p0);
-            p1 = fmaf(aS[c], fmaxf(yc + US[c], 0.f), p1);
-            q = fmaf(adS[c], y, q);
+    for (int32_t t = t0; t < t1; ++t) {
+        const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1];
+        for (int i = tid; i < nu * K; i += 256) {
+            const int64_t u = u0 + i / K;
+            const int h = i % K;
+            uint64_t pr = om[2 * u];
+            const uint64_t bt = om[2 * u + 1];
+            const int k0 = fkey(Sop[u * 4 * K + h]), k1 = fkey(Sop[u * 4 * K + K + h]);
+            while (pr) {
+                const int j = __builtin_ctzll(pr);
+                pr &= pr - 1;
+                atomicMax(&mxk[j][h], ((bt >> j) & 1ull) ? k1 : k0);
+            }
         }
-        pb[u][0][h] = p0 * kLog2e;   // exp2-domain logits
-        pb[u][1][h] = p1 * kLog2e;
-        if (u < nu) A.qop[((int64_t)r * A.n_op + u0 + u) * K + h] = q;
     }
     __syncthreads();
-    // per (device, head): exact max of the logit over the tile's links
-    // (LeakyReLU is monotone, so it is LeakyReLU of the largest pre-activation)
-    for (int i = tid; i < Mg * K; i += 256) {
+    // LeakyReLU is monotone: the largest logit is LeakyReLU of the largest
+    // pre-activation (exp2 domain)
+    for (int i = tid; i < 64 * K; i += 256) {
         const int j = i / K, h = i % K;
-        float mx = -INFINITY;
-        for (int u = 0; u < nu; ++u) {
-            const uint64_t pr = pres[u], bt = bits[u];
-            const float v = ((bt >> j) & 1ull) ? pb[u][1][h] : pb[u][0][h];
-            mx = ((pr >> j) & 1ull) ? fmaxf(mx, v) : mx;
-        }
-        const float x = mx + qd[j][h];
-        mxS[j][h] = mx == -INFINITY ? -INFINITY : fmaxf(x, A.slope * x);
+        const int key = mxk[j][h];
+        const float x = key == INT_MIN ? 0.f : fdekey(key) * kLog2e + qd[j][h];
+        mrun[j][h] = key == INT_MIN ? -INFINITY : fmaxf(x, slope * x);
     }
-    __syncthreads();
 
     const int cbase = wave * WC;
     const int h0 = cbase / D;
-    constexpr int CPH = NCB / HPW;                 // column blocks per head inside a wavefront
+    const int NRB = (Mg + 15) / 16;
+    const int b = (lane >> 4) & 1;
     float cpv[NCB], Uv[NCB];
+#pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
         const int col = cbase + cb * 16 + (lane & 15);
         cpv[cb] = cpS[col];
         Uv[cb] = US[col];
     }
-    const int NRB = (Mg + 15) / 16;
     f4 acc[4][NCB];
-    float zl[4][HPW];
+    float zl[4][HPW], q2[4][HPW], m2[4][HPW];
 #pragma unroll
     for (int rb = 0; rb < 4; ++rb) {
 #pragma unroll
@@ -177,51 +184,71 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
 #pragma unroll
         for (int hh = 0; hh < HPW; ++hh) zl[rb][hh] = 0.f;
     }
-    const int b = (lane >> 4) & 1;
-    const float slope = A.slope;
-    // per-lane constants of the lane's device rows j = rb*16 + l%16
-    float q2[4][HPW], m2[4][HPW];
-#pragma unroll
-    for (int rb = 0; rb < 4; ++rb) {
-        const int j = rb * 16 + (lane & 15);
-#pragma unroll
-        for (int hh = 0; hh < HPW; ++hh) {
-            q2[rb][hh] = qd[j][h0 + hh];
-            m2[rb][hh] = j < Mg ? mxS[j][h0 + hh] : 0.f;
+
+    for (int32_t t = t0; t < t1; ++t) {
+        const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1];
+        for (int i = tid; i < kOpTile; i += 256) {
+            const bool ok = i < nu;
+            pres[i] = ok ? om[2 * (int64_t)(u0 + i)] : 0ull;
+            bits[i] = ok ? om[2 * (int64_t)(u0 + i) + 1] : 0ull;
         }
-    }
-    for (int s = 0; s < kOpTile / 2; ++s) {
-        const int ul = 2 * s + (lane >> 5);
-        const uint64_t pr = pres[ul], bt = b ? bits[ul] : ~bits[ul];   // bt bit j: link bit equals b
-        float bv[NCB];
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) {
-            const float yc = Ys[ul * YS + cbase + cb * 16 + (lane & 15)] + cpv[cb];
-            bv[cb] = fmaxf(b ? yc + Uv[cb] : yc, 0.f);
+        for (int i = tid; i < kOpTile * 2 * K; i += 256) {
+            const int u = i / (2 * K), bh = i % (2 * K);
+            pb[u][bh / K][bh % K] = u < nu ? Sop[(int64_t)(u0 + u) * 4 * K + bh] * kLog2e : 0.f;
         }
-        float pu[HPW];
+        for (int i = tid; i < kOpTile * (F / 4); i += 256) {
+            const int u = i / (F / 4), c = (i % (F / 4)) * 4;
+            float v[4] = {0.f, 0.f, 0.f, 0.f};
+            if (u < nu) load_ch<4, BF>(A.Y_op, ((int64_t)r * A.n_op + u0 + u) * 2 * F + F + c, v);
+            for (int q = 0; q < 4; ++q) Ys[u * YS + c + q] = v[q];
+        }
+        __syncthreads();
+        if (t == t0) {
+            // per-lane constants of the lane's device rows j = rb*16 + l%16
 #pragma unroll
-        for (int hh = 0; hh < HPW; ++hh) pu[hh] = pb[ul][b][h0 + hh];
-        const uint64_t sel = pr & bt;
-#pragma unroll
-        for (int rb = 0; rb < 4; ++rb) {
-            if (rb < NRB) {
+            for (int rb = 0; rb < 4; ++rb) {
                 const int j = rb * 16 + (lane & 15);
-                const bool on = (sel >> j) & 1ull;   // j < Mg holds for every set bit
 #pragma unroll
                 for (int hh = 0; hh < HPW; ++hh) {
-                    const int h = h0 + hh;
-                    const float x = pu[hh] + q2[rb][hh];
-                    const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
-                    zl[rb][hh] += af;
-#pragma unroll
-                    for (int c2 = 0; c2 < CPH; ++c2)
-                        acc[rb][hh * CPH + c2] =
-                            __builtin_amdgcn_mfma_f32_16x16x4f32(af, bv[hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
+                    q2[rb][hh] = qd[j][h0 + hh];
+                    m2[rb][hh] = j < Mg ? mrun[j][h0 + hh] : 0.f;
                 }
             }
         }
+        for (int s = 0; s < kOpTile / 2; ++s) {
+            const int ul = 2 * s + (lane >> 5);
+            const uint64_t pr = pres[ul], bt = b ? bits[ul] : ~bits[ul];   // bt bit j: link bit equals b
+            float bv[NCB];
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) {
+                const float yc = Ys[ul * YS + cbase + cb * 16 + (lane & 15)] + cpv[cb];
+                bv[cb] = fmaxf(b ? yc + Uv[cb] : yc, 0.f);
+            }
+            float pu[HPW];
+#pragma unroll
+            for (int hh = 0; hh < HPW; ++hh) pu[hh] = pb[ul][b][h0 + hh];
+            const uint64_t sel = pr & bt;
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) {
+                if (rb < NRB) {
+                    const int j = rb * 16 + (lane & 15);
+                    const bool on = (sel >> j) & 1ull;   // j < Mg holds for every set bit
+#pragma unroll
+                    for (int hh = 0; hh < HPW; ++hh) {
+                        const float x = pu[hh] + q2[rb][hh];
+                        const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
+                        zl[rb][hh] += af;
+#pragma unroll
+                        for (int c2 = 0; c2 < CPH; ++c2)
+                            acc[rb][hh * CPH + c2] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                af, bv[hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
+                    }
+                }
+            }
+        }
+        __syncthreads();   // the next tile overwrites the LDS tile and masks
     }
+
     const int REC = F + 2 * K;
 #pragma unroll
     for (int rb = 0; rb < 4; ++rb)
@@ -246,7 +273,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
             const int j = rb * 16 + (lane & 15);
             if (head_owner && lane < 16 && rb < NRB && j < Mg) {
                 float *rec = A.part + (((int64_t)r * A.n_dev + d0 + j) * A.maxc + chunk) * REC;
-                rec[h0 + hh] = mxS[j][h0 + hh];
+                rec[h0 + hh] = mrun[j][h0 + hh];
                 rec[K + h0 + hh] = z;
             }
         }
@@ -282,9 +309,10 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
         bits[i] = ok ? A.omask[mi + 1] : 0ull;
     }
     // logits in the exp2 domain: LeakyReLU commutes with the positive factor log2(e)
+    const float *Sop = A.Sop + (int64_t)r * A.n_op * 4 * K;
     for (int i = tid; i < kOpTile * K; i += 256) {
         const int u = i / K, h = i % K;
-        qo[u][h] = u < nu ? A.qop[((int64_t)r * A.n_op + u0 + u) * K + h] * kLog2e : 0.f;
+        qo[u][h] = u < nu ? Sop[(int64_t)(u0 + u) * 4 * K + 2 * K + h] * kLog2e : 0.f;
     }
     for (int i = tid; i < 64 * 2 * K; i += 256) {
         const int j = i / (2 * K), bh = i % (2 * K);
@@ -294,10 +322,14 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
     // op <- device softmax maxima (LeakyReLU of the largest pre-activation)
     for (int i = tid; i < kOpTile * K; i += 256) {
         const int u = i / K, h = i % K;
-        const uint64_t pr = pres[u], bt = bits[u];
+        uint64_t pr = pres[u];
+        const uint64_t bt = bits[u];
         float mx = -INFINITY;
-        for (int j = 0; j < Mg; ++j)
-            if ((pr >> j) & 1ull) mx = fmaxf(mx, P[j][(bt >> j) & 1ull][h]);
+        while (pr) {
+            const int j = __builtin_ctzll(pr);
+            pr &= pr - 1;
+            mx = fmaxf(mx, P[j][(bt >> j) & 1ull][h]);
+        }
         const float x = mx + qo[u][h];
         mxS[u][h] = mx == -INFINITY ? -INFINITY : fmaxf(x, A.slope * x);
     }
@@ -305,12 +337,11 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
     {
         const int li = lane & 15;
         const int c0 = li * CPL;
-        float a[CPL], u0c[CPL], cp[CPL], ad[CPL];
+        float a[CPL], u0c[CPL], cp[CPL];
         for (int c = 0; c < CPL; ++c) {
             a[c] = A.att_src[c0 + c];
             u0c[c] = A.U[(size_t)(c0 + c) * 2];
             cp[c] = A.cp[c0 + c];
-            ad[c] = A.att_dst[c0 + c];
         }
         const float *xo = A.x_oo + (int64_t)r * A.s_oo;
         const int64_t ybase = (int64_t)r * A.n_op * 2 * F + c0;
@@ -318,38 +349,36 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
             const int ul = wave * 16 + it * 4 + (lane >> 4);
             const bool live = ul < nu;
             const int32_t u = u0 + (live ? ul : 0);
-            float q = 0.f;
-            {
-                float yd[CPL];
-                load_ch<CPL, BF>(A.Y_op, ybase + (int64_t)u * 2 * F, yd);
-                for (int c = 0; c < CPL; ++c) q = fmaf(ad[c], yd[c], q);
-            }
-            q = head_sum<LPH>(q);
+            const float q = Sop[(int64_t)u * 4 * K + 3 * K + c0 / (F / K)];
             Online<CPL> o; o.init();
             const int32_t beg = A.rp[0][u], end = A.rp[0][u + 1];
             for (int32_t e = beg; e < end; e += EB) {
                 const int n = min(EB, end - e);
                 int32_t v[EB], id[EB];
+#pragma unroll
                 for (int i = 0; i < EB; ++i) {
-                    v[i] = i < n ? A.col[0][e + i] : 0;
+                    v[i] = i < n ? A.col[0][e + i] : u;
                     id[i] = i < n ? A.eid[0][e + i] : 0;
                 }
-                float x[EB], y[EB][CPL];
+                float x[EB], m[EB][CPL];
+#pragma unroll
                 for (int i = 0; i < EB; ++i) {
                     x[i] = i < n ? xo[id[i]] : 0.f;
-                    if (i < n) load_ch<CPL, BF>(A.Y_op, ybase + (int64_t)v[i] * 2 * F, y[i]);
+                    load_ch<CPL, BF>(A.Y_op, ybase + (int64_t)v[i] * 2 * F, m[i]);   // row of v = u0 when i >= n
                 }
+                float s2[EB];
+#pragma unroll
                 for (int i = 0; i < EB; ++i) {
-                    if (i < n) {
-                        float m[CPL], part = 0.f;
-                        for (int c = 0; c < CPL; ++c) {
-                            m[c] = fmaxf(y[i][c] + fmaf(u0c[c], x[i], cp[c]), 0.f);
-                            part = fmaf(a[c], m[c], part);
-                        }
-                        const float s2 = leaky(head_sum<LPH>(part) + q, A.slope) * kLog2e;
-                        o.push(s2, m);
+                    float part = 0.f;
+#pragma unroll
+                    for (int c = 0; c < CPL; ++c) {
+                        m[i][c] = fmaxf(m[i][c] + fmaf(u0c[c], x[i], cp[c]), 0.f);
+                        part = fmaf(a[c], m[i][c], part);
                     }
+                    const float sv = head_sum<LPH>(part) + q;
+                    s2[i] = fmaxf(sv, A.slope * sv) * kLog2e;
                 }
+                o.template push_n<EB>(s2, m, n);
             }
             const float inv = end > beg ? A.g_same / o.den : 0.f;
             if (live)
@@ -453,16 +482,19 @@ void launch_mfma(const AggArgs &A, hipStream_t st) {
     const int64_t op_waves = (int64_t)A.R * A.n_op;
     const int64_t dev_waves = (int64_t)A.R * A.n_dev;
     const dim3 tiles((unsigned)A.n_tiles, (unsigned)A.R);
-    prof_begin(TAG_STAGE_DEV_PREP, st);
-    dev_prep<F, K, BF><<<(unsigned)((dev_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
-    prof_end(TAG_STAGE_DEV_PREP, st);
+    const dim3 groups((unsigned)A.n_groups, (unsigned)A.R);
+    if (!A.prep_done) {
+        prof_begin(TAG_STAGE_DEV_PREP, st);
+        prep_rows<F, K, BF><<<(unsigned)((op_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A, 0);
+        prep_rows<F, K, BF><<<(unsigned)((dev_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A, 1);
+        prof_end(TAG_STAGE_DEV_PREP, st);
+    }
     prof_begin(TAG_STAGE_AGG_DEV_OP, st);
-    agg_b2<F, K, BF><<<tiles, 256, 0, st>>>(A);
+    agg_b2<F, K, BF><<<groups, 256, 0, st>>>(A);
     prof_end(TAG_STAGE_AGG_DEV_OP, st);
     prof_begin(TAG_STAGE_AGG_OP_DEV, st);
     agg_op_tile<F, K, BF><<<tiles, 256, 0, st>>>(A);
     prof_end(TAG_STAGE_AGG_OP_DEV, st);
-    (void)op_waves;
 }
 
 template <int F, bool BF>

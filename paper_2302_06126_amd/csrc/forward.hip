@@ -188,7 +188,9 @@ __global__ void __launch_bounds__(256) agg_dev_final(AggArgs A) {
     const int head = lane / LPH;
     float out[CPL];
     for (int c = 0; c < CPL; ++c) out[c] = 0.f;
-    {   // B2 merge in record order (records with a zero sum hold no links)
+    {   // B2 merge in record order (records with a zero sum hold no links);
+        // records are read four at a time so their loads overlap
+        constexpr int RB = 4;
         const int32_t deg = A.rp[2][j + 1] - A.rp[2][j];
         int32_t nch = (deg + kChunk - 1) / kChunk;
         if (A.rec_mode) {
@@ -197,25 +199,49 @@ __global__ void __launch_bounds__(256) agg_dev_final(AggArgs A) {
                 const int32_t mid = (lo + hi) >> 1;
                 if (A.dev_off[mid] <= j) lo = mid; else hi = mid;
             }
-            nch = A.tile_off[lo + 1] - A.tile_off[lo];
+            nch = A.group_off[lo + 1] - A.group_off[lo];
         }
         if (deg > 0 && nch > 0) {
-            const float *p0 = A.part + ((int64_t)rep * A.n_dev + j) * A.maxc * (F + 2 * K);
+            constexpr int REC = F + 2 * K;
+            const float *p0 = A.part + ((int64_t)rep * A.n_dev + j) * A.maxc * REC;
             float M = -INFINITY;
-            for (int32_t c = 0; c < nch; ++c) M = fmaxf(M, p0[(int64_t)c * (F + 2 * K) + head]);
+            for (int32_t c = 0; c < nch; c += RB) {
+                float mv[RB];
+#pragma unroll
+                for (int i = 0; i < RB; ++i) mv[i] = c + i < nch ? p0[(int64_t)(c + i) * REC + head] : -INFINITY;
+#pragma unroll
+                for (int i = 0; i < RB; ++i) M = fmaxf(M, mv[i]);
+            }
             float den = 0.f, acc[CPL];
             for (int cc = 0; cc < CPL; ++cc) acc[cc] = 0.f;
-            for (int32_t c = 0; c < nch; ++c) {
-                const float *p = p0 + (int64_t)c * (F + 2 * K);
-                float sc = __builtin_amdgcn_exp2f(p[head] - M);
-                den = fmaf(p[K + head], sc, den);
-                for (int cc = 0; cc < CPL; ++cc) acc[cc] = fmaf(p[2 * K + c0 + cc], sc, acc[cc]);
+            for (int32_t c = 0; c < nch; c += RB) {
+                float mv[RB], dv[RB], av[RB][CPL];
+#pragma unroll
+                for (int i = 0; i < RB; ++i) {
+                    const float *p = p0 + (int64_t)(c + i) * REC;
+                    if (c + i < nch) {
+                        mv[i] = p[head];
+                        dv[i] = p[K + head];
+                        load_ch<CPL, false>(p, 2 * K + c0, av[i]);
+                    } else {
+                        mv[i] = -INFINITY;
+                        dv[i] = 0.f;
+                        for (int cc = 0; cc < CPL; ++cc) av[i][cc] = 0.f;
+                    }
+                }
+#pragma unroll
+                for (int i = 0; i < RB; ++i) {
+                    const float sc = c + i < nch ? __builtin_amdgcn_exp2f(mv[i] - M) : 0.f;
+                    den = fmaf(dv[i], sc, den);
+                    for (int cc = 0; cc < CPL; ++cc) acc[cc] = fmaf(av[i][cc], sc, acc[cc]);
+                }
             }
             float inv = A.g_cross / den;
             for (int cc = 0; cc < CPL; ++cc) out[cc] = acc[cc] * inv;
         }
     }
-    {   // B3: dev <- dev, relation dd
+    {   // B3: dev <- dev, relation dd, EB entries per step
+        constexpr int EB = 4;
         RelConst<CPL> k; k.load(A, 2, F, c0);
         float yd[CPL]; load_ch<CPL, BF>(A.Y_dev, ((int64_t)rep * A.n_dev + j) * 2 * F + c0, yd);
         float q = 0.f;
@@ -224,14 +250,25 @@ __global__ void __launch_bounds__(256) agg_dev_final(AggArgs A) {
         Online<CPL> o; o.init();
         const int32_t beg = A.rp[3][j], end = A.rp[3][j + 1];
         const float *xd = A.x_dd + (int64_t)rep * A.s_dd;
-        for (int32_t e = beg; e < end; ++e) {
-            const int32_t v = A.col[3][e];
-            const int32_t id = A.eid[3][e];
-            const float x0 = xd[(int64_t)id * 2], x1 = xd[(int64_t)id * 2 + 1];
-            float y[CPL]; load_ch<CPL, BF>(A.Y_dev, ((int64_t)rep * A.n_dev + v) * 2 * F + c0, y);
-            float m[CPL];
-            float s2 = entry_score<CPL, LPH>(y, x0, x1, k, q, A.slope, m);
-            o.push(s2, m);
+        for (int32_t e = beg; e < end; e += EB) {
+            const int n = min(EB, end - e);
+            int32_t v[EB], id[EB];
+#pragma unroll
+            for (int i = 0; i < EB; ++i) {
+                v[i] = i < n ? A.col[3][e + i] : 0;
+                id[i] = i < n ? A.eid[3][e + i] : 0;
+            }
+            float x0[EB], x1[EB], y[EB][CPL];
+#pragma unroll
+            for (int i = 0; i < EB; ++i) {
+                x0[i] = i < n ? xd[(int64_t)id[i] * 2] : 0.f;
+                x1[i] = i < n ? xd[(int64_t)id[i] * 2 + 1] : 0.f;
+                load_ch<CPL, BF>(A.Y_dev, ((int64_t)rep * A.n_dev + v[i]) * 2 * F + c0, y[i]);
+            }
+            float s2[EB], m[EB][CPL];
+#pragma unroll
+            for (int i = 0; i < EB; ++i) s2[i] = entry_score<CPL, LPH>(y[i], x0[i], x1[i], k, q, A.slope, m[i]);
+            o.template push_n<EB>(s2, m, n);
         }
         if (end > beg) {
             float inv = A.g_same / o.den;
@@ -251,7 +288,7 @@ struct FwdLayout {
     int32_t maxc;
     bool mfma;
     uint64_t *omask;
-    float *Sdev, *T, *qop;
+    float *Sdev, *T, *Sop;
 };
 
 tag_status check_dims(const tag_model_dims *d) {
@@ -285,17 +322,17 @@ size_t carve_fwd(const tag_graph *g, const tag_model_dims *d, int32_t R, void *b
     L->Y_op = c.take<char>((size_t)R * g->n_op * 2 * F * es);
     L->Y_dev = c.take<char>((size_t)R * g->n_dev * 2 * F * es);
     L->mfma = mfma_path_supported(F, d->heads);
-    L->maxc = L->mfma ? std::max<int32_t>(1, g->max_tiles)
+    L->maxc = L->mfma ? std::max<int32_t>(1, g->max_groups)
                       : std::max<int32_t>(1, (g->max_degree[2] + kChunk - 1) / kChunk);
     L->part = c.take<float>((size_t)R * g->n_dev * L->maxc * (F + 2 * d->heads));
     if (L->mfma) {
         L->omask = c.take<uint64_t>((size_t)R * g->n_op * 2);
         L->Sdev = c.take<float>((size_t)R * g->n_dev * 4 * d->heads);
         L->T = c.take<float>((size_t)R * g->n_dev * 2 * F);
-        L->qop = c.take<float>((size_t)R * g->n_op * d->heads);
+        L->Sop = c.take<float>((size_t)R * g->n_op * 4 * d->heads);
     } else {
         L->omask = nullptr;
-        L->Sdev = L->T = L->qop = nullptr;
+        L->Sdev = L->T = L->Sop = nullptr;
     }
     return c.used;
 }
@@ -428,17 +465,38 @@ extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *
     A.part = L.part; A.maxc = L.maxc;
     A.G = g->G; A.n_tiles = g->n_tiles;
     A.tiles = g->tiles_d; A.tile_off = g->tile_off_d; A.op_off = g->op_off_d; A.dev_off = g->dev_off_d;
-    A.omask = L.omask; A.Sdev = L.Sdev; A.T = L.T; A.qop = L.qop;
+    A.n_groups = g->n_groups; A.groups = g->groups_d; A.group_off = g->group_off_d;
+    A.omask = L.omask; A.Sdev = L.Sdev; A.T = L.T; A.Sop = L.Sop;
     A.rec_mode = L.mfma ? 1 : 0;
     if (L.mfma) launch_pack_masks(A, stream);
 
+    // the transform epilogue forms the attention terms when a head fits one
+    // wavefront's 64 columns
+    const int D = F / K;
+    const int jph = (L.mfma && D <= 64) ? D / 16 : 0;
+    A.prep_done = jph > 0 ? 1 : 0;
     for (int l = 0; l < NL; ++l) {
         const int cur = l & 1, nxt = cur ^ 1;
         const bool last = (l == NL - 1);
+        A.att_src = w->att_src + (size_t)l * 3 * F;
+        A.att_dst = w->att_dst + (size_t)l * 3 * F;
+        A.U = L.U + (size_t)l * 3 * F * 2;
+        A.cp = L.cp + (size_t)l * 3 * F;
         // relation transforms: op rows [W^h_oo ; W^h_od], device rows [W^h_dd ; W^h_od]
         {
             GemmArgs ga{};
             ga.F = F;
+            ga.prep.jph = jph;
+            ga.prep.K = K;
+            ga.prep.a_od = A.att_src + F;
+            ga.prep.ad_od = A.att_dst + F;
+            ga.prep.cp_od = A.cp + F;
+            ga.prep.u_od = A.U + 2 * F;
+            ga.prep.ad_same[0] = A.att_dst;
+            ga.prep.ad_same[1] = A.att_dst + 2 * F;
+            ga.prep.S[0] = L.Sop;
+            ga.prep.S[1] = L.Sdev;
+            ga.prep.T = L.T;
             ga.tiles0 = transform_row_tiles(rows_op);
             if (bf) {
                 const uint16_t *Wl = L.Wb + (size_t)l * 3 * F * F;
@@ -453,10 +511,6 @@ extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *
             launch_transform(ga, bf, stream);
             prof_end(TAG_STAGE_TRANSFORM, stream);
         }
-        A.att_src = w->att_src + (size_t)l * 3 * F;
-        A.att_dst = w->att_dst + (size_t)l * 3 * F;
-        A.U = L.U + (size_t)l * 3 * F * 2;
-        A.cp = L.cp + (size_t)l * 3 * F;
         A.H_op = last ? static_cast<void *>(E_op) : L.H_op[nxt];
         A.H_dev = last ? static_cast<void *>(E_dev) : L.H_dev[nxt];
         A.out_f32 = last ? 1 : (bf ? 0 : 1);

@@ -396,12 +396,23 @@ int64_t count_tiles(const tag_graph_desc *d) {
     return n;
 }
 
+int64_t count_groups(const tag_graph_desc *d) {
+    int64_t n = 0;
+    for (int32_t g = 0; g < d->n_graphs; ++g) {
+        const int64_t nt = (d->n_op[g] + kOpTile - 1) / kOpTile;
+        const int32_t tpg = tiles_per_group(nt);
+        n += (nt + tpg - 1) / tpg;
+    }
+    return n;
+}
+
 // persistent metadata block inside the CSR buffer (one host->device copy):
-// op_off [G+1] | dev_off [G+1] | tile_off [G+1] | tiles [n_tiles][3]
+// op_off [G+1] | dev_off [G+1] | tile_off [G+1] | group_off [G+1] |
+// tiles [n_tiles][3] | groups [n_groups][2]
 struct CsrLayout {
     int32_t *rowptr[4], *col[4], *eid[4];
     int32_t *meta;
-    int32_t *op_off, *dev_off, *tile_off, *tiles;
+    int32_t *op_off, *dev_off, *tile_off, *group_off, *tiles, *groups;
     size_t meta_ints;
 };
 // scratch: counters of all buckets, then the flags (one clear); link offsets (one copy)
@@ -414,19 +425,22 @@ struct TmpLayout {
     int64_t *links;            // oo_off [G+1] | dd_off [G+1] | od_off [G+1]
 };
 
-size_t carve_csr(const Sizes &s, int64_t n_tiles, void *base, CsrLayout *L) {
+size_t carve_csr(const Sizes &s, int64_t n_tiles, int64_t n_groups, void *base, CsrLayout *L) {
     Carver c(base);
     for (int b = 0; b < 4; ++b) {
         L->rowptr[b] = c.take<int32_t>(s.rows[b] + 1);
         L->col[b] = c.take<int32_t>(std::max<int64_t>(s.nnz[b], 1));
         L->eid[b] = c.take<int32_t>(std::max<int64_t>(s.nnz[b], 1));
     }
-    L->meta_ints = 3 * (size_t)(s.G + 1) + 3 * (size_t)std::max<int64_t>(n_tiles, 1);
+    const size_t nt = (size_t)std::max<int64_t>(n_tiles, 1);
+    L->meta_ints = 4 * (size_t)(s.G + 1) + 3 * nt + 2 * (size_t)std::max<int64_t>(n_groups, 1);
     L->meta = c.take<int32_t>(L->meta_ints);
     L->op_off = L->meta ? L->meta : nullptr;
     L->dev_off = L->meta ? L->meta + (s.G + 1) : nullptr;
     L->tile_off = L->meta ? L->meta + 2 * (s.G + 1) : nullptr;
-    L->tiles = L->meta ? L->meta + 3 * (s.G + 1) : nullptr;
+    L->group_off = L->meta ? L->meta + 3 * (s.G + 1) : nullptr;
+    L->tiles = L->meta ? L->meta + 4 * (s.G + 1) : nullptr;
+    L->groups = L->meta ? L->meta + 4 * (s.G + 1) + 3 * nt : nullptr;
     return c.used;
 }
 
@@ -478,7 +492,7 @@ extern "C" tag_status tag_graph_plan(const tag_graph_desc *desc, size_t *csr_byt
     if (st != TAG_OK) return st;
     CsrLayout cl;
     TmpLayout tl;
-    *csr_bytes = carve_csr(s, count_tiles(desc), nullptr, &cl);
+    *csr_bytes = carve_csr(s, count_tiles(desc), count_groups(desc), nullptr, &cl);
     *tmp_bytes = carve_tmp(s, nullptr, &tl);
     return TAG_OK;
 }
@@ -495,10 +509,11 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
     if (!csr_buf || !tmp_buf) TAG_FAIL(TAG_EINVAL, "csr_buf and tmp_buf must be non-NULL");
     CsrLayout cl;
     TmpLayout tl;
-    const int64_t n_tiles = count_tiles(desc);
-    if (carve_csr(s, n_tiles, nullptr, &cl) > csr_bytes) TAG_FAIL(TAG_ENOSPACE, "csr buffer too small (see tag_graph_plan)");
+    const int64_t n_tiles = count_tiles(desc), n_groups = count_groups(desc);
+    if (carve_csr(s, n_tiles, n_groups, nullptr, &cl) > csr_bytes)
+        TAG_FAIL(TAG_ENOSPACE, "csr buffer too small (see tag_graph_plan)");
     if (carve_tmp(s, nullptr, &tl) > tmp_bytes) TAG_FAIL(TAG_ENOSPACE, "tmp buffer too small (see tag_graph_plan)");
-    carve_csr(s, n_tiles, csr_buf, &cl);
+    carve_csr(s, n_tiles, n_groups, csr_buf, &cl);
     carve_tmp(s, tmp_buf, &tl);
     hipStream_t stream = static_cast<hipStream_t>(hip_stream);
 
@@ -521,8 +536,10 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
     std::vector<int64_t> links(3 * (size_t)(s.G + 1));
     {
         int32_t *op_off = meta.data(), *dev_off = op_off + (s.G + 1), *tile_off = dev_off + (s.G + 1);
-        int32_t *tiles = tile_off + (s.G + 1);
-        int32_t nt = 0;
+        int32_t *group_off = tile_off + (s.G + 1);
+        int32_t *tiles = group_off + (s.G + 1);
+        int32_t *groups = tiles + 3 * std::max<int64_t>(n_tiles, 1);
+        int32_t nt = 0, ng = 0;
         for (int32_t gi = 0; gi <= s.G; ++gi) {
             op_off[gi] = (int32_t)g->op_off[gi];
             dev_off[gi] = (int32_t)g->dev_off[gi];
@@ -536,9 +553,19 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
                 tiles[3 * nt + 2] = gi;
             }
             g->max_tiles = std::max(g->max_tiles, cnt);
+            group_off[gi] = ng;
+            const int32_t tpg = tiles_per_group(cnt);
+            int32_t gcnt = 0;
+            for (int32_t k = 0; k < cnt; k += tpg, ++gcnt, ++ng) {
+                groups[2 * ng] = tile_off[gi] + k;
+                groups[2 * ng + 1] = std::min(tpg, cnt - k);
+            }
+            g->max_groups = std::max(g->max_groups, gcnt);
         }
         tile_off[s.G] = nt;
+        group_off[s.G] = ng;
         g->n_tiles = nt;
+        g->n_groups = ng;
         for (int32_t gi = 0; gi <= s.G; ++gi) {
             links[gi] = desc->oo_off[gi];
             links[(s.G + 1) + gi] = desc->dd_off[gi];
@@ -623,6 +650,8 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
     g->dev_off_d = cl.dev_off;
     g->tiles_d = cl.tiles;
     g->tile_off_d = cl.tile_off;
+    g->groups_d = cl.groups;
+    g->group_off_d = cl.group_off;
     *out = g;
 #undef BUILD_HIP
     return TAG_OK;

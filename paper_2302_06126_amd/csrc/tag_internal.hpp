@@ -74,11 +74,23 @@ struct tag_graph {
     int32_t max_tiles = 0;               // largest per-topology tile count
     const int32_t *tiles_d = nullptr;    // [n_tiles][3] = (first op (global), op count, topology)
     const int32_t *tile_off_d = nullptr; // [G+1] first tile of each topology
+    // tile groups: runs of consecutive tiles of one topology handled by one
+    // device<-op block (at most kMaxDevRecords groups per topology)
+    int32_t n_groups = 0;
+    int32_t max_groups = 0;
+    const int32_t *groups_d = nullptr;   // [n_groups][2] = (first tile, tile count)
+    const int32_t *group_off_d = nullptr; // [G+1] first group of each topology
     int device = 0;
 };
 
 namespace tag {
 constexpr int kOpTile = 64;
+constexpr int kMaxDevRecords = 16;   // device<-op partial records per device row
+
+// tiles per group for a topology of nt op tiles
+inline int32_t tiles_per_group(int64_t nt) {
+    return nt <= kMaxDevRecords ? 1 : (int32_t)((nt + kMaxDevRecords - 1) / kMaxDevRecords);
+}
 
 // C[m][n] = act(bias[n] + sum_k A[row(m)][k] * B[n][k]) on MFMA (gemm_small.hip)
 struct SmallGemm {

@@ -38,6 +38,125 @@ __device__ __forceinline__ Tile tile_of(const GemmArgs &G) {
     return t;
 }
 
+// Sums of 4 row values over the 16 lanes of a lane group: after two exchange
+// steps and a two-step butterfly, lanes k with k / 4 = v hold the total of row v.
+__device__ __forceinline__ float xpose_sum4(const float (&v)[4], int lane) {
+    const bool b3 = lane & 8, b2 = lane & 4;
+    float w2[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const float keep = b3 ? v[i + 2] : v[i], send = b3 ? v[i] : v[i + 2];
+        w2[i] = keep + __shfl_xor(send, 8, 64);
+    }
+    float w = (b2 ? w2[1] : w2[0]) + __shfl_xor(b2 ? w2[0] : w2[1], 4, 64);
+    w += __shfl_xor(w, 2, 64);
+    w += __shfl_xor(w, 1, 64);
+    return w;
+}
+
+// Attention-term epilogue (see GemmPrep).  Result register v of block (i, j)
+// in lane l holds row 16 i + 4 (l / 16) + v and column 16 j + l % 16 of the
+// wavefront's 64 x 64 tile.  BF: the terms use the bf16-rounded values that
+// are stored.
+template <int JPH, bool BF>
+__device__ void store_tile(const GemmArgs &G, const Tile &t, int wm, int wn, int lane, const f4 (&acc)[4][4]) {
+    constexpr int HW = JPH > 0 ? 4 / JPH : 1;      // heads per wavefront
+    const GemmPrep &P = G.prep;
+    const int64_t rows = t.sd ? G.side[1].rows : G.side[0].rows;
+    const int F = G.F, K = P.K, D = 16 * (JPH > 0 ? JPH : 1);
+    const int64_t ldy = 2 * F;
+    void *Yp = t.sd ? G.side[1].Y : G.side[0].Y;
+    const int col0 = t.n0 + wn * 64;
+    const bool od = col0 >= F;
+    const int cw = od ? col0 - F : col0;           // first channel of the relation
+    const int k = lane & 15;
+    const int64_t rbase = t.m0 + wm * 64 + 4 * (lane >> 4);
+    const bool writer = (k & 3) == 0;
+    float *S = P.S[t.sd];
+    auto yv = [&](int i, int j, int v) {
+        const float y = acc[i][j][v];
+        return BF ? bf2f(f2bf(y)) : y;
+    };
+    float c1[4], c2[4], c3[4], c4[4];   // od: a, a~, c', U;  same-type: a~
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int c = cw + j * 16 + k;
+        if (JPH == 0) {
+            c1[j] = c2[j] = c3[j] = c4[j] = 0.f;
+        } else if (od) {
+            c1[j] = P.a_od[c]; c2[j] = P.ad_od[c]; c3[j] = P.cp_od[c]; c4[j] = P.u_od[2 * c];
+        } else {
+            c1[j] = 0.f; c2[j] = P.ad_same[t.sd][c]; c3[j] = 0.f; c4[j] = 0.f;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int64_t m = rbase + i * 16 + v;
+            if (m >= rows) continue;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (BF) static_cast<uint16_t *>(Yp)[m * ldy + col0 + j * 16 + k] = f2bf(acc[i][j][v]);
+                else static_cast<float *>(Yp)[m * ldy + col0 + j * 16 + k] = acc[i][j][v];
+            }
+        }
+        if constexpr (JPH == 0) continue;
+        const int64_t row = rbase + i * 16 + (k >> 2);   // row of this lane's totals
+        if (od && t.sd == 1) {
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int64_t rv = rbase + i * 16 + v;
+                if (rv >= rows) continue;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const float yc = yv(i, j, v) + c3[j];
+                    P.T[(rv * 2 + 0) * F + cw + j * 16 + k] = fmaxf(yc, 0.f);
+                    P.T[(rv * 2 + 1) * F + cw + j * 16 + k] = fmaxf(yc + c4[j], 0.f);
+                }
+            }
+        }
+#pragma unroll
+        for (int hw = 0; hw < HW; ++hw) {
+            const int h = cw / D + hw;
+            if (od) {
+                float p0[4], p1[4], q[4];
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    p0[v] = p1[v] = q[v] = 0.f;
+#pragma unroll
+                    for (int jj = 0; jj < JPH; ++jj) {
+                        const int j = hw * JPH + jj;
+                        const float y = yv(i, j, v);
+                        const float yc = y + c3[j];
+                        p0[v] = fmaf(c1[j], fmaxf(yc, 0.f), p0[v]);
+                        p1[v] = fmaf(c1[j], fmaxf(yc + c4[j], 0.f), p1[v]);
+                        q[v] = fmaf(c2[j], y, q[v]);
+                    }
+                }
+                const float s0 = xpose_sum4(p0, lane), s1 = xpose_sum4(p1, lane), s2 = xpose_sum4(q, lane);
+                if (writer && row < rows) {
+                    S[row * 4 * K + h] = s0;
+                    S[row * 4 * K + K + h] = s1;
+                    S[row * 4 * K + 2 * K + h] = s2;
+                }
+            } else {
+                float q[4];
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    q[v] = 0.f;
+#pragma unroll
+                    for (int jj = 0; jj < JPH; ++jj) q[v] = fmaf(c2[hw * JPH + jj], yv(i, hw * JPH + jj, v), q[v]);
+                }
+                const float s2 = xpose_sum4(q, lane);
+                if (writer && row < rows) S[row * 4 * K + 3 * K + h] = s2;
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);   // keep one row block's values live at a time
+    }
+}
+
+template <int JPH>
 __global__ void __launch_bounds__(256) gemm_f32(GemmArgs G) {
     constexpr int BK = 16, LS = BM + 16;   // k-major LDS rows, stride = 16 (mod 64) banks
     __shared__ float As[2][BK * LS];
@@ -103,18 +222,10 @@ __global__ void __launch_bounds__(256) gemm_f32(GemmArgs G) {
         if (kc + 1 < nk) sstore(buf ^ 1);
         __syncthreads();
     }
-    const int ldy = 2 * F;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int64_t m = t.m0 + wm * 64 + i * 16 + 4 * (lane >> 4) + v;
-            if (m >= S.rows) continue;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) Y[m * ldy + t.n0 + wn * 64 + j * 16 + (lane & 15)] = acc[i][j][v];
-        }
+    store_tile<JPH, false>(G, t, wm, wn, lane, acc);
 }
 
+template <int JPH>
 __global__ void __launch_bounds__(256) gemm_bf16(GemmArgs G) {
     constexpr int BK = 32, LS = BK + 8;    // row-major LDS rows of 40 bf16 (80 B)
     __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LS];
@@ -179,27 +290,28 @@ __global__ void __launch_bounds__(256) gemm_bf16(GemmArgs G) {
         if (kc + 1 < nk) sstore(buf ^ 1);
         __syncthreads();
     }
-    const int ldy = 2 * F;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int64_t m = t.m0 + wm * 64 + i * 16 + 4 * (lane >> 4) + v;
-            if (m >= S.rows) continue;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) Y[m * ldy + t.n0 + wn * 64 + j * 16 + (lane & 15)] = f2bf(acc[i][j][v]);
-        }
+    store_tile<JPH, true>(G, t, wm, wn, lane, acc);
 }
 
 }  // namespace
 
 int64_t transform_row_tiles(int64_t rows) { return (rows + BM - 1) / BM; }
 
+template <int JPH>
+void launch_gemm(const GemmArgs &G, bool bf, unsigned blocks, hipStream_t st) {
+    if (bf) gemm_bf16<JPH><<<blocks, 256, 0, st>>>(G);
+    else gemm_f32<JPH><<<blocks, 256, 0, st>>>(G);
+}
+
 void launch_transform(const GemmArgs &G, bool bf, hipStream_t st) {
     const int64_t tiles1 = transform_row_tiles(G.side[1].rows);
     const unsigned blocks = (unsigned)((G.tiles0 + tiles1) * (2 * G.F / BN));
-    if (bf) gemm_bf16<<<blocks, 256, 0, st>>>(G);
-    else gemm_f32<<<blocks, 256, 0, st>>>(G);
+    switch (G.prep.jph) {
+        case 1: launch_gemm<1>(G, bf, blocks, st); break;
+        case 2: launch_gemm<2>(G, bf, blocks, st); break;
+        case 4: launch_gemm<4>(G, bf, blocks, st); break;
+        default: launch_gemm<0>(G, bf, blocks, st); break;
+    }
 }
 
 }  // namespace tag

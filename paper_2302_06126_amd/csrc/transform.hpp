@@ -14,10 +14,28 @@ struct GemmSide {
     int ldb;
     void *Y;             // [rows][2F]
 };
+// Optional epilogue: per-(row, head) attention terms of the layer, taken from
+// the output rows while they are still in registers (heads of 16, 32 or 64
+// channels, so one head lies inside one wavefront's 64 columns):
+//   S[row][0][h] = a_od . ReLU(Y_od + c'_od)          logit of message bit 0
+//   S[row][1][h] = a_od . ReLU(Y_od + c'_od + U_od)   logit of message bit 1
+//   S[row][2][h] = a~_od . Y_od                       destination term, od
+//   S[row][3][h] = a~_same . Y_same                   destination term, oo / dd
+// and, for device rows, the two message rows T[row][b] = ReLU(Y_od + c'_od + b U_od).
+struct GemmPrep {
+    int jph;             // 16-column blocks per head (1, 2, 4); 0: no epilogue
+    int K;
+    const float *a_od, *ad_od, *cp_od;   // [F]
+    const float *u_od;                   // U_od[c] at u_od[2c]
+    const float *ad_same[2];             // [F]: oo (side 0), dd (side 1)
+    float *S[2];                         // [rows][4][K]
+    float *T;                            // device rows: [rows][2][F]
+};
 struct GemmArgs {
     GemmSide side[2];
     int64_t tiles0;      // row tiles of side 0
     int F;
+    GemmPrep prep;
 };
 
 int64_t transform_row_tiles(int64_t rows);
