@@ -12,6 +12,9 @@ constexpr int kChunk = 256;      // entries per device<-op partial (first-versio
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ bf8 as_bf8(unsigned w0, unsigned w1, unsigned w2, unsigned w3) {
+    return __builtin_bit_cast(bf8, u4v{w0, w1, w2, w3});
+}
 
 // -------------------------------------------------------------- aggregation
 struct AggArgs {
@@ -35,7 +38,8 @@ struct AggArgs {
     const int32_t *tiles, *tile_off, *op_off, *dev_off;
     uint64_t *omask;                  // [R*n_op][2]: present / placement-bit masks over local devices
     float *Sdev;                      // [R*n_dev][4][K]: p0, p1, q_od, q_dd of device rows
-    float *T;                         // [R*n_dev][2][F]: device messages for bit 0 / 1
+    float *T;                         // [R*n_dev][2][F]: device messages for bit 0 / 1 (fp32 path);
+                                      // bf16 path: [R*n_dev][F] packed (bit 0, bit 1) bf16 pairs
     float *Sop;                       // [R*n_op][4][K]: p0, p1, q_od, q_oo of op rows
     int32_t prep_done;                // Sop, Sdev and T already written by the transform
     int32_t rec_mode;                 // 0: records per 256-entry chunk, 1: per tile group

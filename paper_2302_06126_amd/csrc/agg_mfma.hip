@@ -14,6 +14,8 @@
 // records that a merge pass combines in tile order; op <- device rows are
 // complete inside one tile and are normalised directly; the same kernel
 // gathers the tile's op <- op rows and writes each op row once.
+#include <type_traits>
+
 #include "agg_common.hpp"
 
 namespace tag {
@@ -73,8 +75,12 @@ __global__ void __launch_bounds__(256) prep_rows(AggArgs A, int dev_side) {
         const float yc = yo[c] + od.cp[c];
         const float t0 = fmaxf(yc, 0.f), t1 = fmaxf(yc + od.u0[c], 0.f);
         if (dev_side) {
-            A.T[(i * 2 + 0) * F + c0 + c] = t0;
-            A.T[(i * 2 + 1) * F + c0 + c] = t1;
+            if (BF) {
+                reinterpret_cast<unsigned *>(A.T)[i * F + c0 + c] = pack_bf2(t0, t1);
+            } else {
+                A.T[(i * 2 + 0) * F + c0 + c] = t0;
+                A.T[(i * 2 + 1) * F + c0 + c] = t1;
+            }
         }
         p0 = fmaf(od.a[c], t0, p0);
         p1 = fmaf(od.a[c], t1, p1);
@@ -110,8 +116,9 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     constexpr int NCB = WC / 16;                   // 16-column blocks per wavefront
     constexpr int HPW = WC >= D ? WC / D : 1;      // heads per wavefront
     constexpr int CPH = NCB / HPW;                 // column blocks per head inside a wavefront
-    constexpr int YS = F + 4;                      // padded LDS row
-    __shared__ float Ys[kOpTile * YS];
+    constexpr int YS = BF ? F + 8 : F + 4;         // padded LDS row (bf16 rows stay 16-byte aligned)
+    typedef typename std::conditional<BF, uint16_t, float>::type YT;
+    __shared__ __attribute__((aligned(16))) YT Ys[kOpTile * YS];
     __shared__ uint64_t pres[kOpTile], bits[kOpTile];
     __shared__ float pb[kOpTile][2][K];
     __shared__ int mxk[64][K];
@@ -196,11 +203,22 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
             const int u = i / (2 * K), bh = i % (2 * K);
             pb[u][bh / K][bh % K] = u < nu ? Sop[(int64_t)(u0 + u) * 4 * K + bh] * kLog2e : 0.f;
         }
-        for (int i = tid; i < kOpTile * (F / 4); i += 256) {
-            const int u = i / (F / 4), c = (i % (F / 4)) * 4;
-            float v[4] = {0.f, 0.f, 0.f, 0.f};
-            if (u < nu) load_ch<4, BF>(A.Y_op, ((int64_t)r * A.n_op + u0 + u) * 2 * F + F + c, v);
-            for (int q = 0; q < 4; ++q) Ys[u * YS + c + q] = v[q];
+        if constexpr (BF) {
+            for (int i = tid; i < kOpTile * (F / 8); i += 256) {
+                const int u = i / (F / 8), c = (i % (F / 8)) * 8;
+                u4v v = u4v{0u, 0u, 0u, 0u};
+                if (u < nu)
+                    v = *reinterpret_cast<const u4v *>(static_cast<const uint16_t *>(A.Y_op) +
+                                                       ((int64_t)r * A.n_op + u0 + u) * 2 * F + F + c);
+                *reinterpret_cast<u4v *>(&Ys[u * YS + c]) = v;
+            }
+        } else {
+            for (int i = tid; i < kOpTile * (F / 4); i += 256) {
+                const int u = i / (F / 4), c = (i % (F / 4)) * 4;
+                float v[4] = {0.f, 0.f, 0.f, 0.f};
+                if (u < nu) load_ch<4, false>(A.Y_op, ((int64_t)r * A.n_op + u0 + u) * 2 * F + F + c, v);
+                for (int q = 0; q < 4; ++q) Ys[u * YS + c + q] = v[q];
+            }
         }
         __syncthreads();
         if (t == t0) {
@@ -215,13 +233,70 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
                 }
             }
         }
+        if constexpr (BF) {
+            // bf16 16x16x32 products: k = 2u + b over the tile's 64 ops; lane l
+            // supplies k = 8(l/16) .. 8(l/16)+7 of a 32-wide step, i.e. ops
+            // ub .. ub+3 with both bits
+#pragma unroll 1
+            for (int ks = 0; ks < kOpTile / 16; ++ks) {
+                const int ub = 16 * ks + 4 * (lane >> 4);
+                bf8 bop[NCB];
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb) {
+                    const int c = cbase + cb * 16 + (lane & 15);
+                    unsigned w[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const float yc = bf2f(Ys[(ub + q) * YS + c]) + cpv[cb];
+                        w[q] = pack_bf2(fmaxf(yc, 0.f), fmaxf(yc + Uv[cb], 0.f));
+                    }
+                    bop[cb] = as_bf8(w[0], w[1], w[2], w[3]);
+                }
+                uint64_t prq[4], btq[4];
+                float p0q[4][HPW], p1q[4][HPW];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    prq[q] = pres[ub + q];
+                    btq[q] = bits[ub + q];
+#pragma unroll
+                    for (int hh = 0; hh < HPW; ++hh) {
+                        p0q[q][hh] = pb[ub + q][0][h0 + hh];
+                        p1q[q][hh] = pb[ub + q][1][h0 + hh];
+                    }
+                }
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) {
+                    if (rb < NRB) {
+                        const int j = rb * 16 + (lane & 15);
+#pragma unroll
+                        for (int hh = 0; hh < HPW; ++hh) {
+                            unsigned w[4];
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) {
+                                const bool on = (prq[q] >> j) & 1ull;
+                                const bool bit = (btq[q] >> j) & 1ull;
+                                const float x = (bit ? p1q[q][hh] : p0q[q][hh]) + q2[rb][hh];
+                                const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
+                                zl[rb][hh] += af;
+                                w[q] = pack_bf2(bit ? 0.f : af, bit ? af : 0.f);
+                            }
+                            const bf8 aop = as_bf8(w[0], w[1], w[2], w[3]);
+#pragma unroll
+                            for (int c2 = 0; c2 < CPH; ++c2)
+                                acc[rb][hh * CPH + c2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                    aop, bop[hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
+                        }
+                    }
+                }
+            }
+        } else
         for (int s = 0; s < kOpTile / 2; ++s) {
             const int ul = 2 * s + (lane >> 5);
             const uint64_t pr = pres[ul], bt = b ? bits[ul] : ~bits[ul];   // bt bit j: link bit equals b
             float bv[NCB];
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) {
-                const float yc = Ys[ul * YS + cbase + cb * 16 + (lane & 15)] + cpv[cb];
+                const float yc = static_cast<float>(Ys[ul * YS + cbase + cb * 16 + (lane & 15)]) + cpv[cb];
                 bv[cb] = fmaxf(b ? yc + Uv[cb] : yc, 0.f);
             }
             float pu[HPW];
@@ -399,6 +474,68 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
 #pragma unroll
         for (int hh = 0; hh < HPW; ++hh) zl[rb][hh] = 0.f;
     }
+    const float slope = A.slope;
+    if constexpr (BF) {
+        // bf16 16x16x32 products: k = 2j + b over the tile's devices; lane l
+        // supplies devices jb .. jb+3 (both bits) of a 32-wide step
+        const unsigned *Tp = reinterpret_cast<const unsigned *>(A.T) + ((int64_t)r * A.n_dev + d0) * F;
+        uint64_t prs[4], bts[4];
+        float q2[4][HPW], m2[4][HPW];
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb) {
+            const int u = rb * 16 + (lane & 15);
+            prs[rb] = pres[u];
+            bts[rb] = bits[u];
+#pragma unroll
+            for (int hh = 0; hh < HPW; ++hh) {
+                q2[rb][hh] = qo[u][h0 + hh];
+                m2[rb][hh] = mxS[u][h0 + hh];
+            }
+        }
+        const int ksteps = (Mg + 15) / 16;
+#pragma unroll 1
+        for (int ks = 0; ks < ksteps; ++ks) {
+            const int jb = 16 * ks + 4 * (lane >> 4);
+            bf8 bop[NCB];
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) {
+                const int c = cbase + cb * 16 + (lane & 15);
+                unsigned w[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) w[q] = jb + q < Mg ? Tp[(int64_t)(jb + q) * F + c] : 0u;
+                bop[cb] = as_bf8(w[0], w[1], w[2], w[3]);
+            }
+            float p0q[4][HPW], p1q[4][HPW];
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int hh = 0; hh < HPW; ++hh) {
+                    p0q[q][hh] = P[jb + q][0][h0 + hh];
+                    p1q[q][hh] = P[jb + q][1][h0 + hh];
+                }
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) {
+#pragma unroll
+                for (int hh = 0; hh < HPW; ++hh) {
+                    unsigned w[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const bool on = (prs[rb] >> (jb + q)) & 1ull;    // never set for jb + q >= Mg
+                        const bool bit = (bts[rb] >> (jb + q)) & 1ull;
+                        const float x = (bit ? p1q[q][hh] : p0q[q][hh]) + q2[rb][hh];
+                        const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
+                        zl[rb][hh] += af;
+                        w[q] = pack_bf2(bit ? 0.f : af, bit ? af : 0.f);
+                    }
+                    const bf8 aop = as_bf8(w[0], w[1], w[2], w[3]);
+#pragma unroll
+                    for (int c2 = 0; c2 < CPH; ++c2)
+                        acc[rb][hh * CPH + c2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            aop, bop[hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
+                }
+            }
+        }
+    } else {
     const float *Tb = A.T + ((int64_t)r * A.n_dev + d0) * 2 * F;
     const int steps = (Mg + 1) / 2;
     const int b = (lane >> 4) & 1;
@@ -417,7 +554,6 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
             m2[rb][hh] = mxS[u][h0 + hh];
         }
     }
-    const float slope = A.slope;
     for (int s = 0; s < steps; ++s) {
         const int j = 2 * s + (lane >> 5);
         const bool jok = j < Mg;
@@ -444,6 +580,7 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
                         __builtin_amdgcn_mfma_f32_16x16x4f32(af, bv[hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
             }
         }
+    }
     }
     // softmax sums of op row rb*16 + l%16 are spread over lanes l, l+16,
     // l+32, l+48; the output row of register v in lane l is rb*16 + 4(l/16) + v

@@ -124,6 +124,15 @@ __device__ __forceinline__ uint16_t f2bf(float x) {
 }
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
 
+typedef unsigned u4v __attribute__((ext_vector_type(4)));
+
+// two floats -> packed bf16 pair (round to nearest even), lo in the low half
+__device__ __forceinline__ unsigned pack_bf2(float lo, float hi) {
+    typedef float f2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(unsigned, __builtin_convertvector(f2{lo, hi}, b2));
+}
+
 // XCD-aware block order: the hardware deals consecutive workgroups to the
 // 8 XCDs round-robin; remap so that logically consecutive blocks share an
 // XCD (and its L2).  Bijective on [0, n).

@@ -17,7 +17,7 @@ namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
-typedef unsigned u4 __attribute__((ext_vector_type(4)));
+typedef u4v u4;
 
 constexpr int BM = 128, BN = 128;
 
@@ -111,8 +111,13 @@ __device__ void store_tile(const GemmArgs &G, const Tile &t, int wm, int wn, int
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const float yc = yv(i, j, v) + c3[j];
-                    P.T[(rv * 2 + 0) * F + cw + j * 16 + k] = fmaxf(yc, 0.f);
-                    P.T[(rv * 2 + 1) * F + cw + j * 16 + k] = fmaxf(yc + c4[j], 0.f);
+                    const float t0 = fmaxf(yc, 0.f), t1 = fmaxf(yc + c4[j], 0.f);
+                    if (BF) {   // packed (bit 0, bit 1) bf16 pairs
+                        reinterpret_cast<unsigned *>(P.T)[rv * F + cw + j * 16 + k] = pack_bf2(t0, t1);
+                    } else {
+                        P.T[(rv * 2 + 0) * F + cw + j * 16 + k] = t0;
+                        P.T[(rv * 2 + 1) * F + cw + j * 16 + k] = t1;
+                    }
                 }
             }
         }
