@@ -89,6 +89,33 @@ __device__ __forceinline__ void load_ch(const void *base, int64_t off, float (&v
     }
 }
 
+// CPL consecutive channels of one row kept as loaded (bf16 pairs or fp32
+// words); get(c) widens channel c
+template <int CPL, bool BF>
+struct RowRaw {
+    static constexpr int NW = BF ? CPL / 2 : CPL;
+    unsigned w[NW];
+    __device__ __forceinline__ void load(const void *base, int64_t off) {
+        static_assert(CPL % 4 == 0, "RowRaw needs a multiple of 4 channels");
+        if constexpr (BF) {
+            const uint2 *p = reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(base) + off);
+#pragma unroll
+            for (int i = 0; i < CPL / 4; ++i) { const uint2 q = p[i]; w[2 * i] = q.x; w[2 * i + 1] = q.y; }
+        } else {
+            const uint4 *p = reinterpret_cast<const uint4 *>(static_cast<const float *>(base) + off);
+#pragma unroll
+            for (int i = 0; i < CPL / 4; ++i) {
+                const uint4 q = p[i];
+                w[4 * i] = q.x; w[4 * i + 1] = q.y; w[4 * i + 2] = q.z; w[4 * i + 3] = q.w;
+            }
+        }
+    }
+    __device__ __forceinline__ float get(int c) const {
+        if constexpr (BF) return __uint_as_float((c & 1) ? (w[c >> 1] & 0xffff0000u) : (w[c >> 1] << 16));
+        else return __uint_as_float(w[c]);
+    }
+};
+
 template <int LPH>
 __device__ __forceinline__ float head_sum(float v) {
 #pragma unroll

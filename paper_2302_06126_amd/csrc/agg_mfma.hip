@@ -366,17 +366,33 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
     constexpr int HPW = WC >= D ? WC / D : 1;
     constexpr int CPL = F / 16;              // op<-op channels per lane
     constexpr int LPH = 16 / K;              // op<-op lanes per head (K <= 16 on this path)
-    constexpr int EB = CPL >= 16 ? 2 : 4;    // neighbour rows loaded together
+    // neighbour rows per batch; with 16 channels per lane the next batch is
+    // loaded while the current one is combined (PF)
+    constexpr bool PF = CPL >= 16;
+    constexpr int EB = CPL >= 16 ? 2 : 4;
     constexpr int OS = F + 4;                // LDS tile row stride
+    constexpr int ECAP = F >= 256 ? 512 : 192;   // op<-op entries of the tile staged in LDS (the rest
+                                                 // are read from the CSR; 192 keeps four blocks per CU at f = 128)
     __shared__ float Ot[kOpTile * OS];
     __shared__ uint64_t pres[kOpTile], bits[kOpTile];
     __shared__ float qo[kOpTile][K], mxS[kOpTile][K];
     __shared__ float P[64][2][K];
+    __shared__ int32_t Erp[kOpTile + 1], Ecol[ECAP];
+    __shared__ float Ex[ECAP];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int32_t t = blockIdx.x, r = blockIdx.y;
     const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1], g = A.tiles[3 * t + 2];
     const int32_t d0 = A.dev_off[g], Mg = A.dev_off[g + 1] - d0;
+    const float *xo = A.x_oo + (int64_t)r * A.s_oo;
+    // the tile's op <- op entries are one contiguous CSR range
+    const int32_t eb = A.rp[0][u0];
+    const int32_t ne = min(A.rp[0][u0 + nu] - eb, ECAP);
+    for (int i = tid; i <= nu; i += 256) Erp[i] = A.rp[0][u0 + i] - eb;
+    for (int i = tid; i < ne; i += 256) {
+        Ecol[i] = A.col[0][eb + i];
+        Ex[i] = xo[A.eid[0][eb + i]];
+    }
     for (int i = tid; i < kOpTile; i += 256) {
         const bool ok = i < nu;
         const int64_t mi = 2 * ((int64_t)r * A.n_op + u0 + i);
@@ -408,7 +424,8 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
         const float x = mx + qo[u][h];
         mxS[u][h] = mx == -INFINITY ? -INFINITY : fmaxf(x, A.slope * x);
     }
-    // op <- op into the LDS tile (gamma_same applied)
+    // op <- op into the LDS tile (gamma_same applied); the next batch's rows
+    // are loaded while the current one is combined
     {
         const int li = lane & 15;
         const int c0 = li * CPL;
@@ -418,42 +435,59 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
             u0c[c] = A.U[(size_t)(c0 + c) * 2];
             cp[c] = A.cp[c0 + c];
         }
-        const float *xo = A.x_oo + (int64_t)r * A.s_oo;
         const int64_t ybase = (int64_t)r * A.n_op * 2 * F + c0;
+        const float slope = A.slope;
         for (int it = 0; it < 4; ++it) {
             const int ul = wave * 16 + it * 4 + (lane >> 4);
             const bool live = ul < nu;
             const int32_t u = u0 + (live ? ul : 0);
             const float q = Sop[(int64_t)u * 4 * K + 3 * K + c0 / (F / K)];
             Online<CPL> o; o.init();
-            const int32_t beg = A.rp[0][u], end = A.rp[0][u + 1];
-            for (int32_t e = beg; e < end; e += EB) {
-                const int n = min(EB, end - e);
-                int32_t v[EB], id[EB];
+            const int32_t beg = live ? Erp[ul] : 0, end = live ? Erp[ul + 1] : 0;
+            RowRaw<CPL, BF> ra[EB], rb2[EB];
+            float xa[EB], xb[EB];
+            auto fetch = [&](int32_t e, RowRaw<CPL, BF> (&buf)[EB], float (&xx)[EB]) {
 #pragma unroll
                 for (int i = 0; i < EB; ++i) {
-                    v[i] = i < n ? A.col[0][e + i] : u;
-                    id[i] = i < n ? A.eid[0][e + i] : 0;
+                    const int32_t le = e + i;
+                    int32_t v = u;
+                    xx[i] = 0.f;
+                    if (le < end) {
+                        if (le < ECAP) { v = Ecol[le]; xx[i] = Ex[le]; }
+                        else { v = A.col[0][eb + le]; xx[i] = xo[A.eid[0][eb + le]]; }
+                    }
+                    buf[i].load(A.Y_op, ybase + (int64_t)v * 2 * F);   // row of u when past the end
                 }
-                float x[EB], m[EB][CPL];
-#pragma unroll
-                for (int i = 0; i < EB; ++i) {
-                    x[i] = i < n ? xo[id[i]] : 0.f;
-                    load_ch<CPL, BF>(A.Y_op, ybase + (int64_t)v[i] * 2 * F, m[i]);   // row of v = u0 when i >= n
-                }
-                float s2[EB];
+            };
+            auto combine = [&](int32_t e, const RowRaw<CPL, BF> (&buf)[EB], const float (&xx)[EB]) {
+                float m[EB][CPL], s2[EB];
 #pragma unroll
                 for (int i = 0; i < EB; ++i) {
                     float part = 0.f;
 #pragma unroll
                     for (int c = 0; c < CPL; ++c) {
-                        m[i][c] = fmaxf(m[i][c] + fmaf(u0c[c], x[i], cp[c]), 0.f);
+                        m[i][c] = fmaxf(buf[i].get(c) + fmaf(u0c[c], xx[i], cp[c]), 0.f);
                         part = fmaf(a[c], m[i][c], part);
                     }
                     const float sv = head_sum<LPH>(part) + q;
-                    s2[i] = fmaxf(sv, A.slope * sv) * kLog2e;
+                    s2[i] = fmaxf(sv, slope * sv) * kLog2e;
                 }
-                o.template push_n<EB>(s2, m, n);
+                o.template push_n<EB>(s2, m, min(EB, end - e));
+            };
+            if constexpr (PF) {
+                if (beg < end) fetch(beg, ra, xa);
+                for (int32_t e = beg; e < end; e += 2 * EB) {
+                    if (e + EB < end) fetch(e + EB, rb2, xb);
+                    combine(e, ra, xa);
+                    if (e + EB >= end) break;
+                    if (e + 2 * EB < end) fetch(e + 2 * EB, ra, xa);
+                    combine(e + EB, rb2, xb);
+                }
+            } else {
+                for (int32_t e = beg; e < end; e += EB) {
+                    fetch(e, ra, xa);
+                    combine(e, ra, xa);
+                }
             }
             const float inv = end > beg ? A.g_same / o.den : 0.f;
             if (live)
@@ -493,18 +527,24 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
             }
         }
         const int ksteps = (Mg + 15) / 16;
-#pragma unroll 1
-        for (int ks = 0; ks < ksteps; ++ks) {
+        bf8 bops[4][NCB];   // every step's message operands, loaded together
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
             const int jb = 16 * ks + 4 * (lane >> 4);
-            bf8 bop[NCB];
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) {
                 const int c = cbase + cb * 16 + (lane & 15);
                 unsigned w[4];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) w[q] = jb + q < Mg ? Tp[(int64_t)(jb + q) * F + c] : 0u;
-                bop[cb] = as_bf8(w[0], w[1], w[2], w[3]);
+                bops[ks][cb] = as_bf8(w[0], w[1], w[2], w[3]);
             }
+        }
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            if (ks >= ksteps) break;
+            const int jb = 16 * ks + 4 * (lane >> 4);
+            const bf8 (&bop)[NCB] = bops[ks];
             float p0q[4][HPW], p1q[4][HPW];
 #pragma unroll
             for (int q = 0; q < 4; ++q)

@@ -157,6 +157,17 @@ def test_forward_long_rows_and_sparse_placements():
     c.check(E_op, E_dev, range(2))
 
 
+@pytest.mark.parametrize("f,dtype", [(128, "f32"), (256, "f32"), (256, "bf16")])
+def test_forward_dense_op_rows(f, dtype):
+    # ~40 op neighbours per op: an op tile holds ~2,500 op<-op entries, more
+    # than the kernel stages in LDS, so the rest come straight from the CSR
+    topo = synth.random_topology(11, 150, 4, 3000, od_per_op=None)
+    c = Case(topo, 2, f, 4, 2, dtype=dtype, seed=11)
+    say(f"forward dense op rows f={f} {dtype}")
+    _, _, E_op, E_dev = c.gpu_forward()
+    c.check(E_op, E_dev, range(2))
+
+
 @pytest.mark.parametrize("n,m,oo,dd,od", [
     (1, 1, [], [], None),                      # single op, single device
     (5, 1, [(0, 1), (1, 2)], [], []),          # no placement links at all
