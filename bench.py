@@ -30,12 +30,12 @@ PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
 KERNEL_NAMES = {"graph_build": "graph build kernels", "encode": "small_gemm (encoders)",
                 "transform": "gemm_f32 / gemm_bf16", "agg_op_op": "agg_op (per-row path)", "agg_op_dev": "agg_op_tile",
-                "agg_dev_op": "agg_b2", "agg_dev_merge": "agg_dev_final", "dev_prep": "dev_prep",
+                "agg_dev_op": "agg_b2", "agg_dev_merge": "agg_dev_final", "dev_prep": "prep_rows",
                 "decide": "decide kernels"}
 ONCE_PER_STEP = {"graph_build", "encode", "decide"}
 KERNEL_BASES = {"transform": ("gemm_f32", "gemm_bf16"), "agg_op_op": ("agg_op",), "agg_op_dev": ("agg_op_tile",),
                 "agg_dev_op": ("agg_b2", "agg_dev_part"), "agg_dev_merge": ("agg_dev_final",),
-                "dev_prep": ("dev_prep",)}
+                "dev_prep": ("prep_rows",)}
 
 
 def measured_traffic(workload: str, stage: str):
@@ -66,25 +66,31 @@ def algorithmic_work(stage: str, wl, topo, R: int, info, n_slices: int, n_query:
     N, M, F, K = topo.n_op, topo.n_dev, wl.f, wl.heads
     s = 2 if wl.dtype == "bf16" else 4            # storage of W^h h and hidden rows
     tiles = (N + 63) // 64
-    rec = R * M * tiles * (F + 2 * K) * 4          # device<-op partial records
+    tpg = 1 if tiles <= 16 else -(-tiles // 16)    # op tiles per device<-op block
+    groups = -(-tiles // tpg)
+    rec = R * M * groups * (F + 2 * K) * 4         # device<-op partial records
+    tbytes = R * M * F * (4 if wl.dtype == "bf16" else 8)   # device message table (bit 0 / 1)
     if stage == "transform":
+        # H in, W in, Y out, plus the attention terms (4K per row) and the
+        # device message table that the epilogue writes
         rows = R * (N + M)
-        return 2.0 * rows * F * 2 * F, float(rows * F * s + rows * 2 * F * s + 2 * 2 * F * F * s)
+        by = rows * F * s + rows * 2 * F * s + 3 * F * F * s + rows * 4 * K * 4 + tbytes
+        return 2.0 * rows * F * 2 * F, float(by)
     if stage == "agg_op_op":
         by = R * N * F * s + topo.e_oo * 4 + (N + 1) * 4 + 2 * topo.e_oo * 8 + R * N * F * 4
         return float(R * 2 * topo.e_oo * 8 * F), float(by)
     if stage == "agg_op_dev":   # op destinations: op<-op gather + op<-dev contraction, one write
-        by = (R * N * F * s + topo.e_oo * 4 + (N + 1) * 4 + 2 * topo.e_oo * 8 + R * M * 2 * F * 4
-              + R * N * 16 + R * N * K * 4 + R * M * 4 * K * 4 + R * N * F * s)
+        by = (R * N * F * s + topo.e_oo * 4 + (N + 1) * 4 + 2 * topo.e_oo * 8 + tbytes
+              + R * N * 16 + R * N * 2 * K * 4 + R * M * 2 * K * 4 + R * N * F * s)
         return float(R * 2 * topo.e_oo * 8 * F + 2 * R * topo.e_od * F), float(by)
     if stage == "agg_dev_op":
-        by = R * N * F * s + R * N * 16 + R * M * K * 4 + R * N * K * 4 + rec
+        by = R * N * F * s + R * N * 16 + R * N * 2 * K * 4 + R * M * K * 4 + rec
         return float(2 * R * topo.e_od * F), float(by)
     if stage == "agg_dev_merge":
         by = rec + R * M * 2 * F * s + R * topo.e_dd * 8 + (M + 1) * 4 + 2 * topo.e_dd * 8 + R * M * F * s
         return float(R * 2 * topo.e_dd * 8 * F), float(by)
-    if stage == "dev_prep":
-        return 0.0, float(R * M * 2 * F * s + R * M * 2 * F * 4 + R * M * 4 * K * 4)
+    if stage == "dev_prep":   # attention terms of all rows (only when heads exceed 64 channels)
+        return 0.0, float(R * (N + M) * 2 * F * s + tbytes + R * (N + M) * 4 * K * 4)
     if stage == "encode":
         return (2.0 * R * (N * wl.f_op + M * 8) * F,
                 float(R * (N * wl.f_op + M * 8) * 4 + R * (N + M) * F * s))
