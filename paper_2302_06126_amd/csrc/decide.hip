@@ -37,23 +37,45 @@ struct DecArgs {
 };
 
 // u[rg][h][a] = sum_{j in mask_a} t[dev(rg, j)][h] + P[h][2F + opt_a] (+ b1[h])
-__global__ void dec_slice(DecArgs A) {
-    const int64_t n = (int64_t)A.R * A.G * A.Hx * A.S;
+// One block per (candidate graph rg, chunk of kSliceH hidden units): the
+// chunk of the graph's device rows t and the option columns sit in LDS; each
+// thread walks the set bits of its slices' masks in ascending device order.
+constexpr int kSliceH = 32;
+__global__ void __launch_bounds__(256) dec_slice(DecArgs A) {
+    __shared__ float tl[64][kSliceH + 1];
+    __shared__ float po[4][kSliceH];
+    const int nch = (A.Hx + kSliceH - 1) / kSliceH;
+    const int64_t rg = blockIdx.x / nch;
+    const int h0 = (int)(blockIdx.x % nch) * kSliceH;
+    const int32_t r = (int32_t)(rg / A.G), g = (int32_t)(rg % A.G);
+    const int32_t d0 = A.dev_off[g], nd = A.dev_off[g + 1] - d0;
     const int din = 2 * A.F + 4;
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
-        const int32_t a = (int32_t)(i % A.S);
-        const int32_t h = (int32_t)((i / A.S) % A.Hx);
-        const int64_t rg = i / ((int64_t)A.S * A.Hx);
-        const int32_t r = (int32_t)(rg / A.G), g = (int32_t)(rg % A.G);
-        const int32_t d0 = A.dev_off[g], nd = A.dev_off[g + 1] - d0;
-        const uint64_t m = A.mask[a];
+    for (int i = threadIdx.x; i < nd * kSliceH; i += blockDim.x) {
+        const int j = i / kSliceH, hh = i % kSliceH;
+        tl[j][hh] = h0 + hh < A.Hx ? A.t[((int64_t)r * A.n_dev + d0 + j) * A.Hx + h0 + hh] : 0.f;
+    }
+    for (int i = threadIdx.x; i < 4 * kSliceH; i += blockDim.x) {
+        const int o = i / kSliceH, hh = i % kSliceH, h = h0 + hh;
+        po[o][hh] = h < A.Hx ? A.P[(size_t)h * din + 2 * A.F + o] + (A.H > 0 ? A.b1[h] : 0.f) : 0.f;
+    }
+    __syncthreads();
+    const uint64_t keep = nd >= 64 ? ~0ull : ((1ull << nd) - 1ull);
+    for (int32_t a = threadIdx.x; a < A.S; a += blockDim.x) {
+        uint64_t m = A.mask[a] & keep;
         const int opt = min((int)A.option[a], 3);
-        float s = A.P[(size_t)h * din + 2 * A.F + opt];
-        if (A.H > 0) s += A.b1[h];
-        const float *tt = A.t + ((int64_t)r * A.n_dev + d0) * A.Hx + h;
-        for (int32_t j = 0; j < nd; ++j)
-            if ((m >> j) & 1ull) s += tt[(int64_t)j * A.Hx];
-        A.u[i] = s;
+        float acc[kSliceH];
+#pragma unroll
+        for (int hh = 0; hh < kSliceH; ++hh) acc[hh] = po[opt][hh];
+        while (m) {
+            const int j = __builtin_ctzll(m);
+            m &= m - 1;
+#pragma unroll
+            for (int hh = 0; hh < kSliceH; ++hh) acc[hh] += tl[j][hh];
+        }
+        float *u = A.u + (rg * A.Hx + h0) * A.S + a;
+#pragma unroll
+        for (int hh = 0; hh < kSliceH; ++hh)
+            if (h0 + hh < A.Hx) u[(int64_t)hh * A.S] = acc[hh];
     }
 }
 
@@ -76,8 +98,17 @@ constexpr int kScoreThreads = 256;
 __device__ __forceinline__ float slice_score(const DecArgs &A, const float *urg, const float *vq,
                                              const float *w2s, int32_t a) {
     if (A.H == 0) return A.b2[0] + urg[a] + vq[0];
+    // independent loads in batches of 16 hidden units, summed in order
     float s = 0.f;
-    for (int h = 0; h < A.H; ++h) s = fmaf(w2s[h], fmaxf(urg[(int64_t)h * A.S + a] + vq[h], 0.f), s);
+    int h = 0;
+    for (; h + 16 <= A.H; h += 16) {
+        float uu[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) uu[k] = urg[(int64_t)(h + k) * A.S + a];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) s = fmaf(w2s[h + k], fmaxf(uu[k] + vq[h + k], 0.f), s);
+    }
+    for (; h < A.H; ++h) s = fmaf(w2s[h], fmaxf(urg[(int64_t)h * A.S + a] + vq[h], 0.f), s);
     return A.b2[0] + s;
 }
 
@@ -234,7 +265,7 @@ extern "C" tag_status tag_gnn_decide(const tag_graph *g, const tag_model_dims *d
                                 A.t, Hx, 0}, stream);
     dec_query_rows<<<grid_for(A.Q), 256, 0, stream>>>(A, L.qrow);
     launch_small_gemm(SmallGemm{E_op, A.F, A.Q, L.qrow, A.F, A.P + A.F, din, Hx, nullptr, 0, A.v, Hx, 0}, stream);
-    dec_slice<<<grid_for((int64_t)A.R * A.G * Hx * A.S), 256, 0, stream>>>(A);
+    dec_slice<<<(unsigned)((int64_t)A.R * A.G * ((Hx + kSliceH - 1) / kSliceH)), 256, 0, stream>>>(A);
     dec_score<<<(unsigned)A.Q, kScoreThreads, sizeof(float) * (Hx + H), stream>>>(A);
     prof_end(TAG_STAGE_DECIDE, stream);
     return launch_status("tag_gnn_decide");

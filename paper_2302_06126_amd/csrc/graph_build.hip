@@ -40,8 +40,8 @@ constexpr int kScanItems = 4;                       // per thread
 constexpr int kScanTile = kThreads * kScanItems;    // per block
 constexpr int kSmallScan = 1 << 16;                 // arrays up to this length: one block per bucket
 constexpr int kPrivRows = 4096;                     // device rows counted in LDS when the total fits
-constexpr int kShortRow = 256;                      // rows up to this length: per-entry rank
-constexpr int kBitmapRange = 16384;                 // source-id range sorted through an LDS bitmap
+constexpr int kShortRow = 64;                       // rows up to this length: one wavefront per row
+constexpr int kBitmapRange = 14336;                 // source-id range sorted through an LDS bitmap (<= 60 KB)
 
 // flags after the counters in the tmp buffer
 enum { FLAG_RANGE = 0, FLAG_DUP = 1, FLAG_MAXDEG = 4 /* 4 entries */, FLAG_COUNT = 8 };
@@ -233,43 +233,61 @@ __global__ void scan_add(int32_t *out, int64_t n, const int32_t *tile_sums) {
 }
 
 // ---- exact per-row rank sort of short rows, all buckets in one launch ----
-// Only the first rp[rows] slots of a bucket hold entries: links rejected
-// during the count pass (bad ids, self links) were never scattered.
-__global__ void rank_rows(Buckets B, int64_t e1, int64_t e2, int64_t e3, int32_t *flags) {
-    int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    const int b = p < e1 ? 0 : (p < e2 ? 1 : (p < e3 ? 2 : 3));
-    p -= b == 0 ? 0 : (b == 1 ? e1 : (b == 2 ? e2 : e3));
-    const int32_t *rp = B.rp[b];
-    if (p >= B.nnz[b] || p >= rp[B.rows[b]]) return;
-    const int32_t *tcol = B.tcol[b], *teid = B.teid[b];
-    const int32_t r = B.rowof[b][p];
-    const int32_t beg = rp[r], end = rp[r + 1];
-    if (end - beg > kShortRow) return;
-    const int32_t c = tcol[p], e = teid[p];
-    int32_t rank = 0, dup = 0;
-    for (int32_t q = beg; q < end; ++q) {
-        const int32_t cq = tcol[q], eq = teid[q];
-        rank += (cq < c) || (cq == c && eq < e);
-        dup |= (cq == c) && (q != p);
+// One wavefront per row: lane i holds entry i of a row of at most 64
+// entries, and its rank is counted against the others through lane
+// shuffles.  Only the rp[rows] entries of a bucket were scattered (links
+// rejected during the count pass never were).
+__global__ void __launch_bounds__(256) rank_rows(Buckets B, int64_t r1, int64_t r2, int64_t r3, int64_t rtot,
+                                                 int32_t *flags) {
+    __shared__ int32_t bmax[4];
+    if (threadIdx.x < 4) bmax[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t w = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (w < rtot) {
+        const int b = w < r1 ? 0 : (w < r2 ? 1 : (w < r3 ? 2 : 3));
+        const int64_t r = w - (b == 0 ? 0 : (b == 1 ? r1 : (b == 2 ? r2 : r3)));
+        const int32_t beg = B.rp[b][r], end = B.rp[b][r + 1];
+        const int32_t deg = end - beg;
+        // rows of op<-dev and dev<-dev hold distinct devices of one topology
+        // (at most 64): a longer row can only come from repeated pairs
+        if ((b == 1 || b == 3) && deg > kShortRow && lane == 0) atomicOr(&flags[FLAG_DUP], 1);
+        if (deg > 0 && deg <= kShortRow) {
+            const bool mine = lane < deg;
+            const int32_t c = mine ? B.tcol[b][beg + lane] : INT32_MAX;
+            const int32_t e = mine ? B.teid[b][beg + lane] : INT32_MAX;
+            int32_t rank = 0, dup = 0;
+            for (int q = 0; q < deg; ++q) {
+                const int32_t cq = __shfl(c, q, 64), eq = __shfl(e, q, 64);
+                rank += (cq < c) || (cq == c && eq < e);
+                dup |= (cq == c) && (q != lane);
+            }
+            if (mine) {
+                B.col[b][beg + rank] = c;
+                B.eid[b][beg + rank] = e;
+                if (dup) atomicOr(&flags[FLAG_DUP], 1);
+            }
+            if (lane == 0) atomicMax(&bmax[b], deg);
+        }
     }
-    B.col[b][beg + rank] = c;
-    B.eid[b][beg + rank] = e;
-    if (dup) atomicOr(&flags[FLAG_DUP], 1);
-    if (rank == 0) atomicMax(&flags[FLAG_MAXDEG + b], end - beg);
+    __syncthreads();
+    if (threadIdx.x < 4 && bmax[threadIdx.x] > 0) atomicMax(&flags[FLAG_MAXDEG + threadIdx.x], bmax[threadIdx.x]);
 }
 
 // One block per row of B0 (blocks [0, rows0)) or B2 (the rest); only rows
 // longer than kShortRow do work.  Sources of a row all belong to the row's
 // topology, so a bitmap over that topology's source-id range sorts the row
 // by source id (sources are unique in a valid row; a repeated source is
-// caught by the atomic OR).  Ranges beyond kBitmapRange fall back to the
-// per-entry rank inside the block.
+// caught by the atomic OR).  Ranges beyond the LDS bitmap (rmax source ids,
+// at most kBitmapRange) fall back to the per-entry rank inside the block.
 __global__ void __launch_bounds__(256) rank_long_rows(Buckets B, const int32_t *op_off, const int32_t *dev_off,
-                                                      int32_t G, int32_t *flags) {
-    __shared__ uint32_t bm[kBitmapRange / 32];
-    __shared__ int32_t wpre[kBitmapRange / 32];
-    __shared__ int32_t eid_of[kBitmapRange];
+                                                      int32_t G, int32_t rmax, int32_t *flags) {
+    extern __shared__ int32_t dyn[];   // bm [rmax/32] | wpre [rmax/32] | eid_of [rmax]
     __shared__ int32_t scan[256];
+    const int nwmax = (rmax + 31) / 32;
+    uint32_t *bm = reinterpret_cast<uint32_t *>(dyn);
+    int32_t *wpre = dyn + nwmax;
+    int32_t *eid_of = dyn + 2 * nwmax;
     const int b = blockIdx.x < B.rows[0] ? 0 : 2;
     const int32_t r = b == 0 ? (int32_t)blockIdx.x : (int32_t)(blockIdx.x - B.rows[0]);
     const int32_t *rp = B.rp[b];
@@ -281,7 +299,7 @@ __global__ void __launch_bounds__(256) rank_long_rows(Buckets B, const int32_t *
     const int32_t g = owner(row_off, G, r);
     const int32_t base = op_off[g], range = op_off[g + 1] - base;   // sources are ops in both buckets
     if (threadIdx.x == 0) atomicMax(&flags[FLAG_MAXDEG + b], end - beg);
-    if (range > kBitmapRange) {
+    if (range > rmax) {
         for (int32_t p = beg + threadIdx.x; p < end; p += blockDim.x) {
             const int32_t c = tcol[p], e = teid[p];
             int32_t rank = 0, dup = 0;
@@ -623,13 +641,21 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
     }
     fill_i32<<<grid_for(tl.cnt_ints), kThreads, 0, stream>>>(tl.cnt_all, tl.cnt_ints, 0);
     if (ea.blk_off[3] > 0) edges_pass<1><<<(unsigned)ea.blk_off[3], kThreads, 0, stream>>>(ea);
-    if (nnz_all > 0)
-        rank_rows<<<(unsigned)((nnz_all + kThreads - 1) / kThreads), kThreads, 0, stream>>>(
-            B, s.nnz[0], s.nnz[0] + s.nnz[1], s.nnz[0] + s.nnz[1] + s.nnz[2], tl.flags);
-    // op<-op and dev<-op rows can be long; op<-dev and dev<-dev rows have at most 64 entries
-    if (s.nnz[0] + s.nnz[2] > 0)
-        rank_long_rows<<<(unsigned)(s.rows[0] + s.rows[2]), kThreads, 0, stream>>>(B, cl.op_off, cl.dev_off, s.G,
-                                                                                    tl.flags);
+    if (nnz_all > 0) {
+        const int64_t r1 = s.rows[0], r2 = r1 + s.rows[1], r3 = r2 + s.rows[2], rtot = r3 + s.rows[3];
+        rank_rows<<<(unsigned)((rtot + kThreads / 64 - 1) / (kThreads / 64)), kThreads, 0, stream>>>(
+            B, r1, r2, r3, rtot, tl.flags);
+    }
+    // op<-op and dev<-op rows can be long; valid op<-dev and dev<-dev rows have at most 64 entries
+    if (s.nnz[0] + s.nnz[2] > 0) {
+        // bitmap sized for the largest topology (sources of both buckets are ops)
+        int32_t rmax = 1;
+        for (int32_t gi = 0; gi < s.G; ++gi) rmax = std::max(rmax, desc->n_op[gi]);
+        rmax = std::min(rmax, kBitmapRange);
+        const size_t lds = sizeof(int32_t) * (2 * (size_t)((rmax + 31) / 32) + (size_t)rmax);
+        rank_long_rows<<<(unsigned)(s.rows[0] + s.rows[2]), kThreads, lds, stream>>>(B, cl.op_off, cl.dev_off, s.G,
+                                                                                      rmax, tl.flags);
+    }
     prof_end(TAG_STAGE_GRAPH_BUILD, stream);
     {
         hipError_t e = hipGetLastError();

@@ -113,7 +113,8 @@ def test_csr_many_device_rows():
 
 @pytest.mark.parametrize("case,status", [
     ("oo_range", -2), ("od_range", -2), ("dd_range", -2), ("self_oo", -3), ("self_dd", -3),
-    ("dup_oo", -3), ("both_dirs", -3), ("dup_od", -3), ("dup_dd_swapped", -3), ("range_beats_dup", -2)])
+    ("dup_oo", -3), ("both_dirs", -3), ("dup_od", -3), ("dup_dd_swapped", -3), ("range_beats_dup", -2),
+    ("dup_od_long_row", -3), ("dup_dd_long_row", -3)])
 def test_build_rejects_like_oracle(case, status):
     oo, dd, od = [(0, 1), (1, 2)], [(0, 1)], [(0, 0), (1, 1)]
     extra = {"oo_range": ("oo", (2, 3)), "od_range": ("od", (0, 2)), "dd_range": ("dd", (-1, 0)),
@@ -121,6 +122,10 @@ def test_build_rejects_like_oracle(case, status):
              "both_dirs": ("oo", (1, 0)), "dup_od": ("od", (1, 1)), "dup_dd_swapped": ("dd", (1, 0))}
     if case == "range_beats_dup":
         oo += [(0, 1), (5, 0)]
+    elif case == "dup_od_long_row":     # one op<-dev row of 70 entries (more than 64 devices)
+        od += [(1, 1)] * 68
+    elif case == "dup_dd_long_row":     # one dev<-dev row of 70 entries
+        dd += [(0, 1)] * 69
     else:
         k, v = extra[case]
         {"oo": oo, "dd": dd, "od": od}[k].append(v)
