@@ -366,10 +366,7 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
     constexpr int HPW = WC >= D ? WC / D : 1;
     constexpr int CPL = F / 16;              // op<-op channels per lane
     constexpr int LPH = 16 / K;              // op<-op lanes per head (K <= 16 on this path)
-    // neighbour rows per batch; with 16 channels per lane the next batch is
-    // loaded while the current one is combined (PF)
-    constexpr bool PF = CPL >= 16;
-    constexpr int EB = CPL >= 16 ? 2 : 4;
+    constexpr int EB = (CPL >= 16 || (CPL == 8 && !BF)) ? 2 : 4;   // neighbour rows per batch
     constexpr int OS = F + 4;                // LDS tile row stride
     constexpr int ECAP = F >= 256 ? 512 : 192;   // op<-op entries of the tile staged in LDS (the rest
                                                  // are read from the CSR; 192 keeps four blocks per CU at f = 128)
@@ -424,8 +421,9 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
         const float x = mx + qo[u][h];
         mxS[u][h] = mx == -INFINITY ? -INFINITY : fmaxf(x, A.slope * x);
     }
-    // op <- op into the LDS tile (gamma_same applied); the next batch's rows
-    // are loaded while the current one is combined
+    // op <- op into the LDS tile (gamma_same applied).  Each 16-lane group
+    // streams four consecutive tile rows (one contiguous entry range) batch
+    // by batch, so groups whose rows are short move on instead of idling.
     {
         const int li = lane & 15;
         const int c0 = li * CPL;
@@ -437,61 +435,74 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
         }
         const int64_t ybase = (int64_t)r * A.n_op * 2 * F + c0;
         const float slope = A.slope;
-        for (int it = 0; it < 4; ++it) {
-            const int ul = wave * 16 + it * 4 + (lane >> 4);
-            const bool live = ul < nu;
-            const int32_t u = u0 + (live ? ul : 0);
-            const float q = Sop[(int64_t)u * 4 * K + 3 * K + c0 / (F / K)];
-            Online<CPL> o; o.init();
-            const int32_t beg = live ? Erp[ul] : 0, end = live ? Erp[ul + 1] : 0;
-            RowRaw<CPL, BF> ra[EB], rb2[EB];
-            float xa[EB], xb[EB];
-            auto fetch = [&](int32_t e, RowRaw<CPL, BF> (&buf)[EB], float (&xx)[EB]) {
+        const int gr0 = wave * 16 + (lane >> 4) * 4;   // the group's first tile row
+        auto rbeg = [&](int i) -> int32_t { return Erp[min(gr0 + i, nu)]; };   // rows >= nu are empty
+        float qv[4];
 #pragma unroll
-                for (int i = 0; i < EB; ++i) {
-                    const int32_t le = e + i;
-                    int32_t v = u;
-                    xx[i] = 0.f;
-                    if (le < end) {
-                        if (le < ECAP) { v = Ecol[le]; xx[i] = Ex[le]; }
-                        else { v = A.col[0][eb + le]; xx[i] = xo[A.eid[0][eb + le]]; }
-                    }
-                    buf[i].load(A.Y_op, ybase + (int64_t)v * 2 * F);   // row of u when past the end
-                }
-            };
-            auto combine = [&](int32_t e, const RowRaw<CPL, BF> (&buf)[EB], const float (&xx)[EB]) {
-                float m[EB][CPL], s2[EB];
+        for (int i = 0; i < 4; ++i) {
+            const int ul = gr0 + i;
+            qv[i] = ul < nu ? Sop[(int64_t)(u0 + ul) * 4 * K + 3 * K + c0 / (F / K)] : 0.f;
+            if (ul < nu)
+                for (int c = 0; c < CPL; ++c) Ot[ul * OS + c0 + c] = 0.f;   // rows without entries stay zero
+        }
+        // (row, first entry, row end) of the group's batches; ri == 4: done
+        auto first_from = [&](int i, int &ri, int32_t &e, int32_t &rend) {
+            while (i < 4 && rbeg(i + 1) == rbeg(i)) ++i;
+            ri = i;
+            e = i < 4 ? rbeg(i) : 0;
+            rend = i < 4 ? rbeg(i + 1) : 0;
+        };
+        RowRaw<CPL, BF> buf[EB];
+        float xx[EB];
+        auto fetch = [&](int32_t e, int32_t end) {
 #pragma unroll
-                for (int i = 0; i < EB; ++i) {
-                    float part = 0.f;
-#pragma unroll
-                    for (int c = 0; c < CPL; ++c) {
-                        m[i][c] = fmaxf(buf[i].get(c) + fmaf(u0c[c], xx[i], cp[c]), 0.f);
-                        part = fmaf(a[c], m[i][c], part);
-                    }
-                    const float sv = head_sum<LPH>(part) + q;
-                    s2[i] = fmaxf(sv, slope * sv) * kLog2e;
+            for (int i = 0; i < EB; ++i) {
+                const int32_t le = e + i;
+                int32_t v = u0;
+                xx[i] = 0.f;
+                if (le < end) {
+                    if (le < ECAP) { v = Ecol[le]; xx[i] = Ex[le]; }
+                    else { v = A.col[0][eb + le]; xx[i] = xo[A.eid[0][eb + le]]; }
                 }
-                o.template push_n<EB>(s2, m, min(EB, end - e));
-            };
-            if constexpr (PF) {
-                if (beg < end) fetch(beg, ra, xa);
-                for (int32_t e = beg; e < end; e += 2 * EB) {
-                    if (e + EB < end) fetch(e + EB, rb2, xb);
-                    combine(e, ra, xa);
-                    if (e + EB >= end) break;
-                    if (e + 2 * EB < end) fetch(e + 2 * EB, ra, xa);
-                    combine(e + EB, rb2, xb);
-                }
-            } else {
-                for (int32_t e = beg; e < end; e += EB) {
-                    fetch(e, ra, xa);
-                    combine(e, ra, xa);
-                }
+                buf[i].load(A.Y_op, ybase + (int64_t)v * 2 * F);   // a tile row when past the end
             }
-            const float inv = end > beg ? A.g_same / o.den : 0.f;
-            if (live)
-                for (int c = 0; c < CPL; ++c) Ot[ul * OS + c0 + c] = o.acc[c] * inv;
+        };
+        int ri;
+        int32_t e, rend;
+        first_from(0, ri, e, rend);
+        Online<CPL> o; o.init();
+        if (ri < 4) fetch(e, rend);
+        // one batch per iteration: the batch's messages are formed from buf,
+        // then buf is refilled with the following batch (possibly of a later
+        // row) while scores and the softmax update of this one proceed
+        while (ri < 4) {
+            const int n = min(EB, rend - e);
+            int nri = ri;
+            int32_t ne = e + n, nrend = rend;
+            if (ne >= rend) first_from(ri + 1, nri, ne, nrend);
+            float m[EB][CPL];
+#pragma unroll
+            for (int i = 0; i < EB; ++i)
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) m[i][c] = fmaxf(buf[i].get(c) + fmaf(u0c[c], xx[i], cp[c]), 0.f);
+            if (nri < 4) fetch(ne, nrend);
+            const float q = ri == 0 ? qv[0] : (ri == 1 ? qv[1] : (ri == 2 ? qv[2] : qv[3]));
+            float s2[EB];
+#pragma unroll
+            for (int i = 0; i < EB; ++i) {
+                float part = 0.f;
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) part = fmaf(a[c], m[i][c], part);
+                const float sv = head_sum<LPH>(part) + q;
+                s2[i] = fmaxf(sv, slope * sv) * kLog2e;
+            }
+            o.template push_n<EB>(s2, m, n);
+            if (nri != ri) {   // row ri complete
+                const float inv = A.g_same / o.den;
+                for (int c = 0; c < CPL; ++c) Ot[(gr0 + ri) * OS + c0 + c] = o.acc[c] * inv;
+                o.init();
+            }
+            ri = nri; e = ne; rend = nrend;
         }
     }
     __syncthreads();
