@@ -186,7 +186,7 @@ __device__ __forceinline__ float entry_score(const float (&y)[CPL], float x0, fl
                                              float qd, float slope, float (&m)[CPL]) {
     float part = 0.f;
     for (int c = 0; c < CPL; ++c) {
-        float z = y[c] + fmaf(k.u0[c], x0, fmaf(k.u1[c], x1, k.cp[c]));
+        float z = y[c] + fmaf(k.u0[c], x0, k.u1[c] * x1);   // y = Y + c' as stored
         m[c] = fmaxf(z, 0.f);
         part = fmaf(k.a[c], m[c], part);
     }

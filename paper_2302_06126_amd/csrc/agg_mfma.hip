@@ -72,7 +72,7 @@ __global__ void __launch_bounds__(256) prep_rows(AggArgs A, int dev_side) {
     load_ch<CPL, BF>(Y, i * 2 * F + c0, ys);
     float p0 = 0.f, p1 = 0.f, qo = 0.f, qs = 0.f;
     for (int c = 0; c < CPL; ++c) {
-        const float yc = yo[c] + od.cp[c];
+        const float yc = yo[c];   // stored rows hold Y + c'
         const float t0 = fmaxf(yc, 0.f), t1 = fmaxf(yc + od.u0[c], 0.f);
         if (dev_side) {
             if (BF) {
@@ -84,8 +84,8 @@ __global__ void __launch_bounds__(256) prep_rows(AggArgs A, int dev_side) {
         }
         p0 = fmaf(od.a[c], t0, p0);
         p1 = fmaf(od.a[c], t1, p1);
-        qo = fmaf(od.ad[c], yo[c], qo);
-        qs = fmaf(same.ad[c], ys[c], qs);
+        qo = fmaf(od.ad[c], yo[c] - od.cp[c], qo);
+        qs = fmaf(same.ad[c], ys[c] - same.cp[c], qs);
     }
     p0 = head_sum<LPH>(p0); p1 = head_sum<LPH>(p1);
     qo = head_sum<LPH>(qo); qs = head_sum<LPH>(qs);
@@ -123,7 +123,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     __shared__ float pb[kOpTile][2][K];
     __shared__ int mxk[64][K];
     __shared__ float qd[64][K], mrun[64][K];
-    __shared__ float cpS[F], US[F];
+    __shared__ float US[F];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int32_t r = blockIdx.y;
@@ -137,7 +137,6 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     const float slope = A.slope;
 
     for (int i = tid; i < F; i += 256) {
-        cpS[i] = A.cp[F + i];
         US[i] = A.U[(size_t)(F + i) * 2];
     }
     for (int i = tid; i < 64 * K; i += 256) {
@@ -175,11 +174,10 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     const int h0 = cbase / D;
     const int NRB = (Mg + 15) / 16;
     const int b = (lane >> 4) & 1;
-    float cpv[NCB], Uv[NCB];
+    float Uv[NCB];
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
         const int col = cbase + cb * 16 + (lane & 15);
-        cpv[cb] = cpS[col];
         Uv[cb] = US[col];
     }
     f4 acc[4][NCB];
@@ -247,7 +245,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
                     unsigned w[4];
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
-                        const float yc = bf2f(Ys[(ub + q) * YS + c]) + cpv[cb];
+                        const float yc = bf2f(Ys[(ub + q) * YS + c]);
                         w[q] = pack_bf2(fmaxf(yc, 0.f), fmaxf(yc + Uv[cb], 0.f));
                     }
                     bop[cb] = as_bf8(w[0], w[1], w[2], w[3]);
@@ -296,7 +294,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
             float bv[NCB];
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) {
-                const float yc = static_cast<float>(Ys[ul * YS + cbase + cb * 16 + (lane & 15)]) + cpv[cb];
+                const float yc = static_cast<float>(Ys[ul * YS + cbase + cb * 16 + (lane & 15)]);
                 bv[cb] = fmaxf(b ? yc + Uv[cb] : yc, 0.f);
             }
             float pu[HPW];
@@ -427,11 +425,10 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
     {
         const int li = lane & 15;
         const int c0 = li * CPL;
-        float a[CPL], u0c[CPL], cp[CPL];
+        float a[CPL], u0c[CPL];
         for (int c = 0; c < CPL; ++c) {
             a[c] = A.att_src[c0 + c];
             u0c[c] = A.U[(size_t)(c0 + c) * 2];
-            cp[c] = A.cp[c0 + c];
         }
         const int64_t ybase = (int64_t)r * A.n_op * 2 * F + c0;
         const float slope = A.slope;
@@ -484,7 +481,7 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
 #pragma unroll
             for (int i = 0; i < EB; ++i)
 #pragma unroll
-                for (int c = 0; c < CPL; ++c) m[i][c] = fmaxf(buf[i].get(c) + fmaf(u0c[c], xx[i], cp[c]), 0.f);
+                for (int c = 0; c < CPL; ++c) m[i][c] = fmaxf(fmaf(u0c[c], xx[i], buf[i].get(c)), 0.f);
             if (nri < 4) fetch(ne, nrend);
             const float q = ri == 0 ? qv[0] : (ri == 1 ? qv[1] : (ri == 2 ? qv[2] : qv[3]));
             float s2[EB];

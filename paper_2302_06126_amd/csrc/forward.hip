@@ -91,7 +91,7 @@ __global__ void __launch_bounds__(256) agg_op(AggArgs A) {
         RelConst<CPL> k; k.load(A, 0, F, c0);
         float yd[CPL]; load_ch<CPL, BF>(A.Y_op, yrow_u + c0, yd);
         float q = 0.f;
-        for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], yd[c], q);
+        for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], yd[c] - k.cp[c], q);   // stored rows hold Y + c'
         q = head_sum<LPH>(q);
         Online<CPL> o; o.init();
         const int32_t beg = A.rp[0][u], end = A.rp[0][u + 1];
@@ -113,7 +113,7 @@ __global__ void __launch_bounds__(256) agg_op(AggArgs A) {
         RelConst<CPL> k; k.load(A, 1, F, c0);
         float yd[CPL]; load_ch<CPL, BF>(A.Y_op, yrow_u + F + c0, yd);
         float q = 0.f;
-        for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], yd[c], q);
+        for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], yd[c] - k.cp[c], q);   // stored rows hold Y + c'
         q = head_sum<LPH>(q);
         Online<CPL> o; o.init();
         const int32_t beg = A.rp[1][u], end = A.rp[1][u + 1];
@@ -156,7 +156,7 @@ __global__ void __launch_bounds__(256) agg_dev_part(AggArgs A) {
     RelConst<CPL> k; k.load(A, 1, F, c0);
     float yd[CPL]; load_ch<CPL, BF>(A.Y_dev, ((int64_t)rep * A.n_dev + j) * 2 * F + F + c0, yd);
     float q = 0.f;
-    for (int cc = 0; cc < CPL; ++cc) q = fmaf(k.ad[cc], yd[cc], q);
+    for (int cc = 0; cc < CPL; ++cc) q = fmaf(k.ad[cc], yd[cc] - k.cp[cc], q);   // stored rows hold Y + c'
     q = head_sum<LPH>(q);
     Online<CPL> o; o.init();
     const uint8_t *xb = A.x_od + (int64_t)rep * A.s_od;
@@ -245,7 +245,7 @@ __global__ void __launch_bounds__(256) agg_dev_final(AggArgs A) {
         RelConst<CPL> k; k.load(A, 2, F, c0);
         float yd[CPL]; load_ch<CPL, BF>(A.Y_dev, ((int64_t)rep * A.n_dev + j) * 2 * F + c0, yd);
         float q = 0.f;
-        for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], yd[c], q);
+        for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], yd[c] - k.cp[c], q);   // stored rows hold Y + c'
         q = head_sum<LPH>(q);
         Online<CPL> o; o.init();
         const int32_t beg = A.rp[3][j], end = A.rp[3][j + 1];
@@ -492,6 +492,8 @@ extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *
             ga.prep.ad_od = A.att_dst + F;
             ga.prep.cp_od = A.cp + F;
             ga.prep.u_od = A.U + 2 * F;
+            ga.prep.cp_same[0] = A.cp;
+            ga.prep.cp_same[1] = A.cp + 2 * F;
             ga.prep.ad_same[0] = A.att_dst;
             ga.prep.ad_same[1] = A.att_dst + 2 * F;
             ga.prep.S[0] = L.Sop;

@@ -26,13 +26,26 @@ __global__ void __launch_bounds__(256) small_gemm(SmallGemm G) {
     int64_t arow = -1;
     if (gm < G.rows) arow = G.row_map ? G.row_map[gm] : gm;
     const int gn = n0 + lr;
-    for (int k0 = 0; k0 < G.K; k0 += SK) {
+    // the next chunk's operands are loaded into registers while the current
+    // one feeds the matrix cores
+    float ra[4], rb[4];
+    auto gload = [&](int k0) {
+#pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int k = k0 + lk + q;
-            As[lr][lk + q] = (arow >= 0 && k < G.K) ? G.A[arow * G.lda + k] : 0.f;
-            Bs[lr][lk + q] = (gn < G.N && k < G.K) ? G.B[(int64_t)gn * G.ldb + k] : 0.f;
+            ra[q] = (arow >= 0 && k < G.K) ? G.A[arow * G.lda + k] : 0.f;
+            rb[q] = (gn < G.N && k < G.K) ? G.B[(int64_t)gn * G.ldb + k] : 0.f;
+        }
+    };
+    gload(0);
+    for (int k0 = 0; k0 < G.K; k0 += SK) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            As[lr][lk + q] = ra[q];
+            Bs[lr][lk + q] = rb[q];
         }
         __syncthreads();
+        if (k0 + SK < G.K) gload(k0 + SK);
 #pragma unroll
         for (int kk = 0; kk < SK; kk += 4) {
             float a[2], b[2];

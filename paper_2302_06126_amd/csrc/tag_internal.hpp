@@ -115,23 +115,18 @@ namespace tag {
 
 __device__ __forceinline__ float leaky(float x, float slope) { return x > 0.f ? x : slope * x; }
 
-// round-to-nearest-even fp32 -> bf16 bits
-__device__ __forceinline__ uint16_t f2bf(float x) {
-    uint32_t u = __float_as_uint(x);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return static_cast<uint16_t>(u >> 16);
-}
-__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
-
 typedef unsigned u4v __attribute__((ext_vector_type(4)));
 
-// two floats -> packed bf16 pair (round to nearest even), lo in the low half
+// two floats -> packed bf16 pair (round to nearest even, one gfx950
+// conversion instruction), lo in the low half
 __device__ __forceinline__ unsigned pack_bf2(float lo, float hi) {
     typedef float f2 __attribute__((ext_vector_type(2)));
     typedef __bf16 b2 __attribute__((ext_vector_type(2)));
     return __builtin_bit_cast(unsigned, __builtin_convertvector(f2{lo, hi}, b2));
 }
+// round-to-nearest-even fp32 -> bf16 bits
+__device__ __forceinline__ uint16_t f2bf(float x) { return static_cast<uint16_t>(pack_bf2(x, 0.f) & 0xffffu); }
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
 
 // XCD-aware block order: the hardware deals consecutive workgroups to the
 // 8 XCDs round-robin; remap so that logically consecutive blocks share an

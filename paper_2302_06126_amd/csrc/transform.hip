@@ -1,5 +1,7 @@
 // Relation transforms (Section 4.2.1 layer equation, the W^h h part):
 //   op rows:     Y = H [W^h_oo ; W^h_od]^T     device rows: Y = H [W^h_dd ; W^h_od]^T
+// stored with the folded bias c' of each relation added (Y + c' starts every
+// message ReLU(Y + c' + U x)); the attention destination terms use Y itself.
 // One launch covers both row sets of a layer.  128 x 128 block tiles, four
 // wavefronts of 64 x 64, k-chunks staged through LDS with the next chunk's
 // global loads in flight while the current one feeds the matrix cores.  The
@@ -73,22 +75,29 @@ __device__ void store_tile(const GemmArgs &G, const Tile &t, int wm, int wn, int
     const int64_t rbase = t.m0 + wm * 64 + 4 * (lane >> 4);
     const bool writer = (k & 3) == 0;
     float *S = P.S[t.sd];
+    float c1[4], c2[4], c3[4], c4[4];   // od: a, a~, c', U;  same-type: a~ and c'
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int c = cw + j * 16 + k;
+        c3[j] = od ? P.cp_od[c] : P.cp_same[t.sd][c];
+        if (JPH == 0) {
+            c1[j] = c2[j] = c4[j] = 0.f;
+        } else if (od) {
+            c1[j] = P.a_od[c]; c2[j] = P.ad_od[c]; c4[j] = P.u_od[2 * c];
+        } else {
+            c1[j] = 0.f; c2[j] = P.ad_same[t.sd][c]; c4[j] = 0.f;
+        }
+    }
+    // yv: W^h h (bf16-rounded in BF) for the destination terms; ys: the stored
+    // row Y + c' (messages and their logits start from it)
     auto yv = [&](int i, int j, int v) {
         const float y = acc[i][j][v];
         return BF ? bf2f(f2bf(y)) : y;
     };
-    float c1[4], c2[4], c3[4], c4[4];   // od: a, a~, c', U;  same-type: a~
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int c = cw + j * 16 + k;
-        if (JPH == 0) {
-            c1[j] = c2[j] = c3[j] = c4[j] = 0.f;
-        } else if (od) {
-            c1[j] = P.a_od[c]; c2[j] = P.ad_od[c]; c3[j] = P.cp_od[c]; c4[j] = P.u_od[2 * c];
-        } else {
-            c1[j] = 0.f; c2[j] = P.ad_same[t.sd][c]; c3[j] = 0.f; c4[j] = 0.f;
-        }
-    }
+    auto ys = [&](int i, int j, int v) {
+        const float y = acc[i][j][v] + c3[j];
+        return BF ? bf2f(f2bf(y)) : y;
+    };
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -97,8 +106,9 @@ __device__ void store_tile(const GemmArgs &G, const Tile &t, int wm, int wn, int
             if (m >= rows) continue;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                if (BF) static_cast<uint16_t *>(Yp)[m * ldy + col0 + j * 16 + k] = f2bf(acc[i][j][v]);
-                else static_cast<float *>(Yp)[m * ldy + col0 + j * 16 + k] = acc[i][j][v];
+                const float y = acc[i][j][v] + c3[j];
+                if (BF) static_cast<uint16_t *>(Yp)[m * ldy + col0 + j * 16 + k] = f2bf(y);
+                else static_cast<float *>(Yp)[m * ldy + col0 + j * 16 + k] = y;
             }
         }
         if constexpr (JPH == 0) continue;
@@ -110,7 +120,7 @@ __device__ void store_tile(const GemmArgs &G, const Tile &t, int wm, int wn, int
                 if (rv >= rows) continue;
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    const float yc = yv(i, j, v) + c3[j];
+                    const float yc = ys(i, j, v);
                     const float t0 = fmaxf(yc, 0.f), t1 = fmaxf(yc + c4[j], 0.f);
                     if (BF) {   // packed (bit 0, bit 1) bf16 pairs
                         reinterpret_cast<unsigned *>(P.T)[rv * F + cw + j * 16 + k] = pack_bf2(t0, t1);
@@ -132,11 +142,10 @@ __device__ void store_tile(const GemmArgs &G, const Tile &t, int wm, int wn, int
 #pragma unroll
                     for (int jj = 0; jj < JPH; ++jj) {
                         const int j = hw * JPH + jj;
-                        const float y = yv(i, j, v);
-                        const float yc = y + c3[j];
+                        const float yc = ys(i, j, v);
                         p0[v] = fmaf(c1[j], fmaxf(yc, 0.f), p0[v]);
                         p1[v] = fmaf(c1[j], fmaxf(yc + c4[j], 0.f), p1[v]);
-                        q[v] = fmaf(c2[j], y, q[v]);
+                        q[v] = fmaf(c2[j], yv(i, j, v), q[v]);
                     }
                 }
                 const float s0 = xpose_sum4(p0, lane), s1 = xpose_sum4(p1, lane), s2 = xpose_sum4(q, lane);

@@ -14,17 +14,20 @@ struct GemmSide {
     int ldb;
     void *Y;             // [rows][2F]
 };
-// Optional epilogue: per-(row, head) attention terms of the layer, taken from
+// Y is stored as W^h h + c' (c' of the column's relation: same-type half or
+// od half).  Optional epilogue: per-(row, head) attention terms of the layer, taken from
 // the output rows while they are still in registers (heads of 16, 32 or 64
 // channels, so one head lies inside one wavefront's 64 columns):
 //   S[row][0][h] = a_od . ReLU(Y_od + c'_od)          logit of message bit 0
 //   S[row][1][h] = a_od . ReLU(Y_od + c'_od + U_od)   logit of message bit 1
+// (with Y the unbiased W^h h)
 //   S[row][2][h] = a~_od . Y_od                       destination term, od
 //   S[row][3][h] = a~_same . Y_same                   destination term, oo / dd
 // and, for device rows, the two message rows T[row][b] = ReLU(Y_od + c'_od + b U_od).
 struct GemmPrep {
-    int jph;             // 16-column blocks per head (1, 2, 4); 0: no epilogue
+    int jph;             // 16-column blocks per head (1, 2, 4); 0: no attention terms
     int K;
+    const float *cp_same[2];             // [F]: folded bias c' of oo (side 0) / dd (side 1), added to Y
     const float *a_od, *ad_od, *cp_od;   // [F]
     const float *u_od;                   // U_od[c] at u_od[2c]
     const float *ad_same[2];             // [F]: oo (side 0), dd (side 1)
