@@ -2,6 +2,8 @@
 // forward.hip, MFMA path in agg_mfma.hip).
 #pragma once
 
+#include <type_traits>
+
 #include "tag_internal.hpp"
 
 namespace tag {
@@ -120,6 +122,22 @@ template <int LPH>
 __device__ __forceinline__ float head_sum(float v) {
 #pragma unroll
     for (int o = LPH / 2; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// Sum over aligned groups of LPH <= 16 lanes with DPP moves inside a 16-lane
+// row (quad swaps, then the half-row and row mirrors pair the remaining
+// lanes); every lane of a group ends with the group's total.
+template <int LPH>
+__device__ __forceinline__ float row_sum(float v) {
+    static_assert(LPH >= 1 && LPH <= 16 && (LPH & (LPH - 1)) == 0, "LPH must be a power of two <= 16");
+    auto dpp = [](float x, auto ctrl) {
+        return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), decltype(ctrl)::value, 0xf, 0xf, true));
+    };
+    if constexpr (LPH >= 2) v += dpp(v, std::integral_constant<int, 0xB1>{});    // quad_perm [1,0,3,2]
+    if constexpr (LPH >= 4) v += dpp(v, std::integral_constant<int, 0x4E>{});    // quad_perm [2,3,0,1]
+    if constexpr (LPH >= 8) v += dpp(v, std::integral_constant<int, 0x141>{});   // row_half_mirror
+    if constexpr (LPH >= 16) v += dpp(v, std::integral_constant<int, 0x140>{});  // row_mirror
     return v;
 }
 

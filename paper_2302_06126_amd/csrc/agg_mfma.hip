@@ -352,22 +352,33 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
         }
 }
 
-// Op destinations of one 64-op tile.  op <- op: each wavefront gathers 16 of
-// the tile's rows, four at a time (16 lanes and f/16 channels per row), into
-// an LDS tile.  op <- device: MFMA contraction of the attention weights with
-// the device message table.  Both are combined and written once.
+// Op destinations of one 64-op tile of one candidate.
+//  * op <- op: each 16-lane group streams the entries of four consecutive
+//    tile rows (one contiguous CSR range, staged in LDS as (source, edge
+//    feature) pairs, ECAP at a time) with EB neighbour rows always in
+//    flight: a slot is refilled as soon as its row has been read, and the
+//    refill reads only LDS, so the row loads never wait on each other.  Each
+//    row's softmax is taken relative to its first logit (exact; a logit more
+//    than 64 above the reference moves it up), so an entry costs one
+//    multiply-add per channel for the aggregate.  Rows land in an LDS tile.
+//  * op <- device: MFMA contraction of the attention weights (formed in
+//    registers) with the device message table.
+// Both parts are combined and each op row is written once.
 template <int F, int K, bool BF>
 __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
     constexpr int D = F / K;
     constexpr int WC = F / 4;
     constexpr int NCB = WC / 16;
     constexpr int HPW = WC >= D ? WC / D : 1;
+    constexpr int CPH = NCB / HPW;
     constexpr int CPL = F / 16;              // op<-op channels per lane
     constexpr int LPH = 16 / K;              // op<-op lanes per head (K <= 16 on this path)
-    constexpr int EB = (CPL >= 16 || (CPL == 8 && !BF)) ? 2 : 4;   // neighbour rows per batch
+    // neighbour rows in flight per 16-lane group (a slot holds CPL or CPL/2 words)
+    constexpr int EB = BF ? (F >= 256 && K >= 8 ? 4 : 8) : (F >= 256 ? 2 : 4);
+    constexpr int SB = 4;                    // fp32 op<-dev: device steps per batch of table loads
     constexpr int OS = F + 4;                // LDS tile row stride
-    constexpr int ECAP = F >= 256 ? 512 : 192;   // op<-op entries of the tile staged in LDS (the rest
-                                                 // are read from the CSR; 192 keeps four blocks per CU at f = 128)
+    constexpr int ECAP = F >= 256 ? 512 : 192;   // op<-op entries staged in LDS per chunk (192 keeps
+                                                 // four blocks per CU at f = 128)
     __shared__ float Ot[kOpTile * OS];
     __shared__ uint64_t pres[kOpTile], bits[kOpTile];
     __shared__ float qo[kOpTile][K], mxS[kOpTile][K];
@@ -380,29 +391,64 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
     const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1], g = A.tiles[3 * t + 2];
     const int32_t d0 = A.dev_off[g], Mg = A.dev_off[g + 1] - d0;
     const float *xo = A.x_oo + (int64_t)r * A.s_oo;
-    // the tile's op <- op entries are one contiguous CSR range
-    const int32_t eb = A.rp[0][u0];
-    const int32_t ne = min(A.rp[0][u0 + nu] - eb, ECAP);
-    for (int i = tid; i <= nu; i += 256) Erp[i] = A.rp[0][u0 + i] - eb;
-    for (int i = tid; i < ne; i += 256) {
-        Ecol[i] = A.col[0][eb + i];
-        Ex[i] = xo[A.eid[0][eb + i]];
-    }
-    for (int i = tid; i < kOpTile; i += 256) {
-        const bool ok = i < nu;
-        const int64_t mi = 2 * ((int64_t)r * A.n_op + u0 + i);
-        pres[i] = ok ? A.omask[mi] : 0ull;
-        bits[i] = ok ? A.omask[mi + 1] : 0ull;
-    }
-    // logits in the exp2 domain: LeakyReLU commutes with the positive factor log2(e)
     const float *Sop = A.Sop + (int64_t)r * A.n_op * 4 * K;
-    for (int i = tid; i < kOpTile * K; i += 256) {
-        const int u = i / K, h = i % K;
-        qo[u][h] = u < nu ? Sop[(int64_t)(u0 + u) * 4 * K + 2 * K + h] * kLog2e : 0.f;
-    }
-    for (int i = tid; i < 64 * 2 * K; i += 256) {
-        const int j = i / (2 * K), bh = i % (2 * K);
-        P[j][bh / K][bh % K] = j < Mg ? A.Sdev[((int64_t)r * A.n_dev + d0 + j) * 4 * K + bh] * kLog2e : 0.f;
+    const float slope = A.slope;
+    const int cbase = wave * WC;
+    const int h0 = cbase / D;
+
+    // ---- prologue: every global load is issued before the first LDS store
+    // (the logits go to the exp2 domain: LeakyReLU commutes with log2(e) > 0)
+    const int32_t eb = A.rp[0][u0];
+    const int32_t ntot = A.rp[0][u0 + nu] - eb;    // the tile's op<-op entries: one CSR range
+    const int32_t ne = min(ntot, ECAP);
+    {
+        constexpr int NQ = (kOpTile * K + 255) / 256, NP = (64 * 2 * K + 255) / 256, NE = (ECAP + 255) / 256;
+        int32_t rp0 = 0;
+        uint64_t om0 = 0, om1 = 0;
+        float q2v[NQ], pv[NP], exv[NE];
+        int32_t ecv[NE], eiv[NE];
+        if (tid <= nu) rp0 = A.rp[0][u0 + tid] - eb;
+        if (tid < nu) {
+            const int64_t mi = 2 * ((int64_t)r * A.n_op + u0 + tid);
+            om0 = A.omask[mi];
+            om1 = A.omask[mi + 1];
+        }
+#pragma unroll
+        for (int k = 0; k < NQ; ++k) {
+            const int i = tid + 256 * k, u = i / K, h = i % K;
+            const bool ok = i < kOpTile * K && u < nu;
+            q2v[k] = ok ? Sop[(int64_t)(u0 + u) * 4 * K + 2 * K + h] : 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < NP; ++k) {
+            const int i = tid + 256 * k, j = i / (2 * K), bh = i % (2 * K);
+            pv[k] = (i < 64 * 2 * K && j < Mg) ? A.Sdev[((int64_t)r * A.n_dev + d0 + j) * 4 * K + bh] : 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < NE; ++k) {
+            const int i = tid + 256 * k;
+            ecv[k] = i < ne ? A.col[0][eb + i] : 0;
+            eiv[k] = i < ne ? A.eid[0][eb + i] : 0;
+        }
+#pragma unroll
+        for (int k = 0; k < NE; ++k) exv[k] = (tid + 256 * k) < ne ? xo[eiv[k]] : 0.f;
+        if (tid <= nu) Erp[tid] = rp0;
+        if (tid < kOpTile) { pres[tid] = om0; bits[tid] = om1; }
+#pragma unroll
+        for (int k = 0; k < NQ; ++k) {
+            const int i = tid + 256 * k;
+            if (i < kOpTile * K) qo[i / K][i % K] = q2v[k] * kLog2e;
+        }
+#pragma unroll
+        for (int k = 0; k < NP; ++k) {
+            const int i = tid + 256 * k;
+            if (i < 64 * 2 * K) P[i / (2 * K)][(i % (2 * K)) / K][i % K] = pv[k] * kLog2e;
+        }
+#pragma unroll
+        for (int k = 0; k < NE; ++k) {
+            const int i = tid + 256 * k;
+            if (i < ne) { Ecol[i] = ecv[k]; Ex[i] = exv[k]; }
+        }
     }
     __syncthreads();
     // op <- device softmax maxima (LeakyReLU of the largest pre-activation)
@@ -417,96 +463,117 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
             mx = fmaxf(mx, P[j][(bt >> j) & 1ull][h]);
         }
         const float x = mx + qo[u][h];
-        mxS[u][h] = mx == -INFINITY ? -INFINITY : fmaxf(x, A.slope * x);
+        mxS[u][h] = mx == -INFINITY ? -INFINITY : fmaxf(x, slope * x);
     }
-    // op <- op into the LDS tile (gamma_same applied).  Each 16-lane group
-    // streams four consecutive tile rows (one contiguous entry range) batch
-    // by batch, so groups whose rows are short move on instead of idling.
+
+    // ---- op <- op into the LDS tile (gamma_same applied)
     {
         const int li = lane & 15;
         const int c0 = li * CPL;
+        const int hd = c0 / D;                          // this lane's head
+        const int64_t ybase = (int64_t)r * A.n_op * 2 * F + c0;
+        const int gr0 = wave * 16 + (lane >> 4) * 4;   // the group's first tile row
+        int32_t rb_[5];               // the group's row boundaries (rows >= nu are empty)
+#pragma unroll
+        for (int i = 0; i < 5; ++i) rb_[i] = Erp[min(gr0 + i, nu)];
+        const int32_t ebeg = rb_[0], eend = rb_[4];
+        float qv[4];                  // op<-op destination terms of the group's rows (exp2 domain)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            qv[i] = gr0 + i < nu ? Sop[(int64_t)(u0 + gr0 + i) * 4 * K + 3 * K + hd] * kLog2e : 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (gr0 + i < nu)
+                for (int c = 0; c < CPL; ++c) Ot[(gr0 + i) * OS + c0 + c] = 0.f;   // rows without entries stay zero
         float a[CPL], u0c[CPL];
+#pragma unroll
         for (int c = 0; c < CPL; ++c) {
-            a[c] = A.att_src[c0 + c];
+            a[c] = A.att_src[c0 + c] * kLog2e;
             u0c[c] = A.U[(size_t)(c0 + c) * 2];
         }
-        const int64_t ybase = (int64_t)r * A.n_op * 2 * F + c0;
-        const float slope = A.slope;
-        const int gr0 = wave * 16 + (lane >> 4) * 4;   // the group's first tile row
-        auto rbeg = [&](int i) -> int32_t { return Erp[min(gr0 + i, nu)]; };   // rows >= nu are empty
-        float qv[4];
+        const float gs = A.g_same;
+        int ri = -1;                  // row being accumulated (-1: none yet)
+        float mref = 0.f, den = 0.f, acc[CPL];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int ul = gr0 + i;
-            qv[i] = ul < nu ? Sop[(int64_t)(u0 + ul) * 4 * K + 3 * K + c0 / (F / K)] : 0.f;
-            if (ul < nu)
-                for (int c = 0; c < CPL; ++c) Ot[ul * OS + c0 + c] = 0.f;   // rows without entries stay zero
-        }
-        // (row, first entry, row end) of the group's batches; ri == 4: done
-        auto first_from = [&](int i, int &ri, int32_t &e, int32_t &rend) {
-            while (i < 4 && rbeg(i + 1) == rbeg(i)) ++i;
-            ri = i;
-            e = i < 4 ? rbeg(i) : 0;
-            rend = i < 4 ? rbeg(i + 1) : 0;
+        for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
+        auto finish = [&]() {
+            const float inv = gs * __builtin_amdgcn_rcpf(den);
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) Ot[ri * OS + c0 + c] = acc[c] * inv;
         };
-        RowRaw<CPL, BF> buf[EB];
-        float xx[EB];
-        auto fetch = [&](int32_t e, int32_t end) {
-#pragma unroll
-            for (int i = 0; i < EB; ++i) {
-                const int32_t le = e + i;
-                int32_t v = u0;
-                xx[i] = 0.f;
-                if (le < end) {
-                    if (le < ECAP) { v = Ecol[le]; xx[i] = Ex[le]; }
-                    else { v = A.col[0][eb + le]; xx[i] = xo[A.eid[0][eb + le]]; }
+        for (int32_t cb0 = 0; cb0 < ntot; cb0 += ECAP) {
+            if (cb0 > 0) {   // next chunk of the tile's entries (block-uniform)
+                __syncthreads();
+                const int32_t n = min(ntot - cb0, ECAP);
+                for (int i = tid; i < n; i += 256) {
+                    Ecol[i] = A.col[0][eb + cb0 + i];
+                    Ex[i] = xo[A.eid[0][eb + cb0 + i]];
                 }
-                buf[i].load(A.Y_op, ybase + (int64_t)v * 2 * F);   // a tile row when past the end
+                __syncthreads();
             }
-        };
-        int ri;
-        int32_t e, rend;
-        first_from(0, ri, e, rend);
-        Online<CPL> o; o.init();
-        if (ri < 4) fetch(e, rend);
-        // one batch per iteration: the batch's messages are formed from buf,
-        // then buf is refilled with the following batch (possibly of a later
-        // row) while scores and the softmax update of this one proceed
-        while (ri < 4) {
-            const int n = min(EB, rend - e);
-            int nri = ri;
-            int32_t ne = e + n, nrend = rend;
-            if (ne >= rend) first_from(ri + 1, nri, ne, nrend);
-            float m[EB][CPL];
+            const int32_t lo = max(ebeg, cb0), hi = min(eend, cb0 + ECAP);
+            RowRaw<CPL, BF> slot[EB];
+            float xs[EB];
+            // slot s <- entry le (past hi: the tile's first row, never
+            // consumed, so every refill is the same unconditional load)
+            auto fetch = [&](int s, int32_t le) {
+                const int32_t lc = max(min(le, hi - 1) - cb0, 0);
+                const bool ok = le < hi;
+                const int32_t v = ok ? Ecol[lc] : u0;
+                xs[s] = ok ? Ex[lc] : 0.f;
+                slot[s].load(A.Y_op, ybase + (int64_t)v * 2 * F);
+            };
 #pragma unroll
-            for (int i = 0; i < EB; ++i)
+            for (int s = 0; s < EB; ++s) fetch(s, lo + s);
+            for (int32_t base = lo; base < hi; base += EB) {
 #pragma unroll
-                for (int c = 0; c < CPL; ++c) m[i][c] = fmaxf(fmaf(u0c[c], xx[i], buf[i].get(c)), 0.f);
-            if (nri < 4) fetch(ne, nrend);
-            const float q = ri == 0 ? qv[0] : (ri == 1 ? qv[1] : (ri == 2 ? qv[2] : qv[3]));
-            float s2[EB];
+                for (int s = 0; s < EB; ++s) {
+                    const int32_t e = base + s;
+                    const bool act = e < hi;
+                    float m[CPL];
+                    float part = 0.f;
 #pragma unroll
-            for (int i = 0; i < EB; ++i) {
-                float part = 0.f;
+                    for (int c = 0; c < CPL; ++c) {
+                        m[c] = fmaxf(fmaf(u0c[c], xs[s], slot[s].get(c)), 0.f);
+                        part = fmaf(a[c], m[c], part);
+                    }
+                    const int rl = (e >= rb_[1]) + (e >= rb_[2]) + (e >= rb_[3]);   // row of e in the group
+                    const int rowe = gr0 + rl;
+                    fetch(s, e + EB);
+                    const float q = rl == 0 ? qv[0] : (rl == 1 ? qv[1] : (rl == 2 ? qv[2] : qv[3]));
+                    const float sv = row_sum<LPH>(part) + q;
+                    const float s2 = fmaxf(sv, slope * sv);
+                    if (act) {
+                        if (rowe != ri) {   // first entry of row rowe: finish row ri
+                            if (ri >= 0) finish();
+                            ri = rowe;
+                            mref = s2;
+                            den = 0.f;
 #pragma unroll
-                for (int c = 0; c < CPL; ++c) part = fmaf(a[c], m[i][c], part);
-                const float sv = head_sum<LPH>(part) + q;
-                s2[i] = fmaxf(sv, slope * sv) * kLog2e;
+                            for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
+                        }
+                        float d = s2 - mref;
+                        if (d > 64.f) {   // keep the weights finite: move the reference up
+                            const float sc = __builtin_amdgcn_exp2f(-d);
+                            den *= sc;
+#pragma unroll
+                            for (int c = 0; c < CPL; ++c) acc[c] *= sc;
+                            mref = s2;
+                            d = 0.f;
+                        }
+                        const float p = __builtin_amdgcn_exp2f(d);
+                        den += p;
+#pragma unroll
+                        for (int c = 0; c < CPL; ++c) acc[c] = fmaf(p, m[c], acc[c]);
+                    }
+                }
             }
-            o.template push_n<EB>(s2, m, n);
-            if (nri != ri) {   // row ri complete
-                const float inv = A.g_same / o.den;
-                for (int c = 0; c < CPL; ++c) Ot[(gr0 + ri) * OS + c0 + c] = o.acc[c] * inv;
-                o.init();
-            }
-            ri = nri; e = ne; rend = nrend;
         }
+        if (ri >= 0) finish();
     }
-    __syncthreads();
 
-    const int cbase = wave * WC;
-    const int h0 = cbase / D;
-    constexpr int CPH = NCB / HPW;
+    // ---- op <- device on the matrix cores; the message-table operands are
+    // loaded before the barrier so their latency overlaps the slowest group
     f4 acc[4][NCB];
     float zl[4][HPW];
 #pragma unroll
@@ -516,11 +583,24 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
 #pragma unroll
         for (int hh = 0; hh < HPW; ++hh) zl[rb][hh] = 0.f;
     }
-    const float slope = A.slope;
     if constexpr (BF) {
         // bf16 16x16x32 products: k = 2j + b over the tile's devices; lane l
         // supplies devices jb .. jb+3 (both bits) of a 32-wide step
         const unsigned *Tp = reinterpret_cast<const unsigned *>(A.T) + ((int64_t)r * A.n_dev + d0) * F;
+        bf8 bops[4][NCB];
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            const int jb = 16 * ks + 4 * (lane >> 4);
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) {
+                const int c = cbase + cb * 16 + (lane & 15);
+                unsigned w[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) w[q] = jb + q < Mg ? Tp[(int64_t)(jb + q) * F + c] : 0u;
+                bops[ks][cb] = as_bf8(w[0], w[1], w[2], w[3]);
+            }
+        }
+        __syncthreads();
         uint64_t prs[4], bts[4];
         float q2[4][HPW], m2[4][HPW];
 #pragma unroll
@@ -535,24 +615,10 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
             }
         }
         const int ksteps = (Mg + 15) / 16;
-        bf8 bops[4][NCB];   // every step's message operands, loaded together
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            const int jb = 16 * ks + 4 * (lane >> 4);
-#pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) {
-                const int c = cbase + cb * 16 + (lane & 15);
-                unsigned w[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) w[q] = jb + q < Mg ? Tp[(int64_t)(jb + q) * F + c] : 0u;
-                bops[ks][cb] = as_bf8(w[0], w[1], w[2], w[3]);
-            }
-        }
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
             if (ks >= ksteps) break;
             const int jb = 16 * ks + 4 * (lane >> 4);
-            const bf8 (&bop)[NCB] = bops[ks];
             float p0q[4][HPW], p1q[4][HPW];
 #pragma unroll
             for (int q = 0; q < 4; ++q)
@@ -579,56 +645,73 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
 #pragma unroll
                     for (int c2 = 0; c2 < CPH; ++c2)
                         acc[rb][hh * CPH + c2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                            aop, bop[hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
+                            aop, bops[ks][hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
                 }
             }
         }
     } else {
-    const float *Tb = A.T + ((int64_t)r * A.n_dev + d0) * 2 * F;
-    const int steps = (Mg + 1) / 2;
-    const int b = (lane >> 4) & 1;
-    // per-lane constants of the lane's op rows u = rb*16 + l%16; the masks are
-    // pre-shifted to this lane's first device (j = l/32) and advance two per step
-    uint64_t prs[4], bts[4];
-    float q2[4][HPW], m2[4][HPW];
+        // fp32 16x16x4 products: k = 4 (device, bit) pairs per step, two
+        // devices per step; the table loads of SB steps are issued together
+        const float *Tb = A.T + ((int64_t)r * A.n_dev + d0) * 2 * F;
+        const int steps = (Mg + 1) / 2;
+        const int b = (lane >> 4) & 1;
+        float bv[SB][NCB];
+        auto load_batch = [&](int s0) {
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb) {
-        const int u = rb * 16 + (lane & 15);
-        prs[rb] = pres[u] >> (lane >> 5);
-        bts[rb] = bits[u] >> (lane >> 5);
+            for (int k = 0; k < SB; ++k) {
+                const int j = 2 * (s0 + k) + (lane >> 5);
 #pragma unroll
-        for (int hh = 0; hh < HPW; ++hh) {
-            q2[rb][hh] = qo[u][h0 + hh];
-            m2[rb][hh] = mxS[u][h0 + hh];
-        }
-    }
-    for (int s = 0; s < steps; ++s) {
-        const int j = 2 * s + (lane >> 5);
-        const bool jok = j < Mg;
-        float bv[NCB];
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb)
-            bv[cb] = jok ? Tb[((int64_t)j * 2 + b) * F + cbase + cb * 16 + (lane & 15)] : 0.f;
-        float pj[HPW];
-#pragma unroll
-        for (int hh = 0; hh < HPW; ++hh) pj[hh] = P[j][b][h0 + hh];
+                for (int cb = 0; cb < NCB; ++cb)
+                    bv[k][cb] = j < Mg ? Tb[((int64_t)j * 2 + b) * F + cbase + cb * 16 + (lane & 15)] : 0.f;
+            }
+        };
+        load_batch(0);
+        __syncthreads();
+        // per-lane constants of the lane's op rows u = rb*16 + l%16
+        uint64_t prs[4], bts[4];
+        float q2[4][HPW], m2[4][HPW];
 #pragma unroll
         for (int rb = 0; rb < 4; ++rb) {
-            const bool on = jok && (prs[rb] & 1ull) && ((int)(bts[rb] & 1ull) == b);
-            prs[rb] >>= 2;
-            bts[rb] >>= 2;
+            const int u = rb * 16 + (lane & 15);
+            prs[rb] = pres[u];
+            bts[rb] = bits[u];
 #pragma unroll
             for (int hh = 0; hh < HPW; ++hh) {
-                const float x = pj[hh] + q2[rb][hh];
-                const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
-                zl[rb][hh] += af;
-#pragma unroll
-                for (int c2 = 0; c2 < CPH; ++c2)
-                    acc[rb][hh * CPH + c2] =
-                        __builtin_amdgcn_mfma_f32_16x16x4f32(af, bv[hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
+                q2[rb][hh] = qo[u][h0 + hh];
+                m2[rb][hh] = mxS[u][h0 + hh];
             }
         }
-    }
+        for (int s0 = 0; s0 < steps; s0 += SB) {
+            float bc[SB][NCB];
+#pragma unroll
+            for (int k = 0; k < SB; ++k)
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb) bc[k][cb] = bv[k][cb];
+            if (s0 + SB < steps) load_batch(s0 + SB);
+#pragma unroll
+            for (int k = 0; k < SB; ++k) {
+                const int j = 2 * (s0 + k) + (lane >> 5);
+                if (2 * (s0 + k) >= Mg) break;
+                const bool jok = j < Mg;
+                float pj[HPW];
+#pragma unroll
+                for (int hh = 0; hh < HPW; ++hh) pj[hh] = P[j][b][h0 + hh];
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) {
+                    const bool on = jok && ((prs[rb] >> j) & 1ull) && ((int)((bts[rb] >> j) & 1ull) == b);
+#pragma unroll
+                    for (int hh = 0; hh < HPW; ++hh) {
+                        const float x = pj[hh] + q2[rb][hh];
+                        const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
+                        zl[rb][hh] += af;
+#pragma unroll
+                        for (int c2 = 0; c2 < CPH; ++c2)
+                            acc[rb][hh * CPH + c2] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                af, bc[k][hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
+                    }
+                }
+            }
+        }
     }
     // softmax sums of op row rb*16 + l%16 are spread over lanes l, l+16,
     // l+32, l+48; the output row of register v in lane l is rb*16 + 4(l/16) + v
