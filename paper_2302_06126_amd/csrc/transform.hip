@@ -10,7 +10,10 @@
 //
 // MFMA 16x16 operand layout: lane l supplies row/column l % 16 of A/B and
 // k-slice l / 16 (4 k per slice for fp32 16x16x4, 8 for bf16 16x16x32);
-// result register v of lane l holds row 4 (l / 16) + v, column l % 16.
+// result register v of lane l holds row 4 (l / 16) + v, column l % 16.  The
+// fp32 kernel feeds the weights as the first operand and the hidden rows as
+// the second, so its result blocks are tiles of Y^T (see store_tile); the bf16
+// kernel takes Y = H W^T directly (store_tile_rows).
 #include "tag_internal.hpp"
 #include "transform.hpp"
 
@@ -56,12 +59,13 @@ __device__ __forceinline__ float xpose_sum4(const float (&v)[4], int lane) {
     return w;
 }
 
-// Attention-term epilogue (see GemmPrep).  Result register v of block (i, j)
-// in lane l holds row 16 i + 4 (l / 16) + v and column 16 j + l % 16 of the
-// wavefront's 64 x 64 tile.  BF: the terms use the bf16-rounded values that
-// are stored.
+// Epilogue of the bf16 kernel, whose products are taken as Y = H W^T: result
+// register v of block (i, j) in lane l holds row 16 i + 4 (l / 16) + v and
+// column 16 j + l % 16 of the wavefront's 64 x 64 tile (one bf16 column per
+// lane and block, two-byte stores).  The terms use the bf16-rounded values
+// that are stored.
 template <int JPH, bool BF>
-__device__ void store_tile(const GemmArgs &G, const Tile &t, int wm, int wn, int lane, const f4 (&acc)[4][4]) {
+__device__ void store_tile_rows(const GemmArgs &G, const Tile &t, int wm, int wn, int lane, const f4 (&acc)[4][4]) {
     constexpr int HW = JPH > 0 ? 4 / JPH : 1;      // heads per wavefront
     const GemmPrep &P = G.prep;
     const int64_t rows = t.sd ? G.side[1].rows : G.side[0].rows;
@@ -170,6 +174,114 @@ __device__ void store_tile(const GemmArgs &G, const Tile &t, int wm, int wn, int
     }
 }
 
+// Epilogue of the fp32 kernel.  The products are taken as Y^T = W H^T (operands swapped), so
+// result register v of block (j, i) in lane l holds output row 16 i + l % 16
+// and output column 16 j + 4 (l / 16) + v of the wavefront's 64 x 64 tile:
+// each lane owns four consecutive columns of one row per block, written with
+// one vector store, and a head's attention sums reduce inside the lane and
+// then over the four lanes l % 16 + {0, 16, 32, 48}.
+//
+// The per-column constants of the wavefront's 64 columns are staged in LDS
+// (`cst`, 256 floats per wavefront, free once the k loop is done) before any
+// store is issued: on this GPU a wait for an outstanding load also waits for
+// earlier stores, so no global load may follow the first store.
+template <int JPH>
+__device__ void store_tile(const GemmArgs &G, const Tile &t, int wm, int wn, int lane, const f4 (&acc)[4][4],
+                           float *cst) {
+    const GemmPrep &P = G.prep;
+    const int64_t rows = t.sd ? G.side[1].rows : G.side[0].rows;
+    const int F = G.F, K = P.K, D = 16 * (JPH > 0 ? JPH : 1);
+    const int64_t ldy = 2 * F;
+    void *Yp = t.sd ? G.side[1].Y : G.side[0].Y;
+    const int col0 = t.n0 + wn * 64;
+    const bool od = col0 >= F;
+    const int cw = od ? col0 - F : col0;           // first channel of the relation
+    const int g = lane >> 4;
+    const int64_t rbase = t.m0 + wm * 64 + (lane & 15);
+    const float *cp = od ? P.cp_od : P.cp_same[t.sd];
+    const bool dev_od = od && t.sd == 1;           // device rows also get the message table
+    float *S = P.S[t.sd];
+    {   // cst[kind][64]: c'; od: a, a~, U; same-type: a~ (lane l holds column l)
+        const int cl = cw + lane;
+        const float v3 = cp[cl];
+        float v1 = 0.f, v2 = 0.f, v4 = 0.f;
+        if (JPH > 0) {
+            if (od) { v1 = P.a_od[cl]; v2 = P.ad_od[cl]; v4 = P.u_od[2 * cl]; }
+            else v2 = P.ad_same[t.sd][cl];
+        }
+        cst[lane] = v3; cst[64 + lane] = v1; cst[128 + lane] = v2; cst[192 + lane] = v4;
+    }
+    // row blocks outer, column blocks inner: the four stores of a row block
+    // complete whole 128-byte row segments back to back
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t m = rbase + 16 * i;
+        const bool mok = m < rows;
+        float p0 = 0.f, p1 = 0.f, q = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int c = cw + 16 * j + 4 * g;         // the lane's first channel in this block
+            const int cc = 16 * j + 4 * g;             // ... within the wavefront's columns
+            float c3[4], c1[4], c2[4], c4[4];           // c'; od: a, a~, U; same-type: a~
+            {
+                const float4 x3 = *reinterpret_cast<const float4 *>(cst + cc);
+                const float4 x1 = *reinterpret_cast<const float4 *>(cst + 64 + cc);
+                const float4 x2 = *reinterpret_cast<const float4 *>(cst + 128 + cc);
+                const float4 x4 = *reinterpret_cast<const float4 *>(cst + 192 + cc);
+                c3[0] = x3.x; c3[1] = x3.y; c3[2] = x3.z; c3[3] = x3.w;
+                c1[0] = x1.x; c1[1] = x1.y; c1[2] = x1.z; c1[3] = x1.w;
+                c2[0] = x2.x; c2[1] = x2.y; c2[2] = x2.z; c2[3] = x2.w;
+                c4[0] = x4.x; c4[1] = x4.y; c4[2] = x4.z; c4[3] = x4.w;
+            }
+            if (mok) {
+                float ys[4], yv[4];
+#pragma unroll
+                for (int v = 0; v < 4; ++v) { ys[v] = acc[j][i][v] + c3[v]; yv[v] = acc[j][i][v]; }
+                *reinterpret_cast<float4 *>(static_cast<float *>(Yp) + m * ldy + col0 + cc) =
+                    make_float4(ys[0], ys[1], ys[2], ys[3]);
+                if constexpr (JPH > 0) {
+                    if (od) {
+                        float t0[4], t1[4];
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) {
+                            t0[v] = fmaxf(ys[v], 0.f);
+                            t1[v] = fmaxf(ys[v] + c4[v], 0.f);
+                            p0 = fmaf(c1[v], t0[v], p0);
+                            p1 = fmaf(c1[v], t1[v], p1);
+                            q = fmaf(c2[v], yv[v], q);
+                        }
+                        if (dev_od) {   // message rows of bit 0 / 1
+                            *reinterpret_cast<float4 *>(P.T + (m * 2 + 0) * F + c) = make_float4(t0[0], t0[1], t0[2], t0[3]);
+                            *reinterpret_cast<float4 *>(P.T + (m * 2 + 1) * F + c) = make_float4(t1[0], t1[1], t1[2], t1[3]);
+                        }
+                    } else {
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) q = fmaf(c2[v], yv[v], q);
+                    }
+                }
+            }
+            if constexpr (JPH > 0) {
+                if ((j + 1) % JPH == 0) {   // the head of blocks j+1-JPH .. j is complete for row m
+                    const int h = (cw + 16 * (j + 1 - JPH)) / D;
+                    p0 += __shfl_xor(p0, 16, 64); p0 += __shfl_xor(p0, 32, 64);
+                    p1 += __shfl_xor(p1, 16, 64); p1 += __shfl_xor(p1, 32, 64);
+                    q += __shfl_xor(q, 16, 64); q += __shfl_xor(q, 32, 64);
+                    if (g == 0 && mok) {
+                        if (od) {
+                            S[m * 4 * K + h] = p0;
+                            S[m * 4 * K + K + h] = p1;
+                            S[m * 4 * K + 2 * K + h] = q;
+                        } else {
+                            S[m * 4 * K + 3 * K + h] = q;
+                        }
+                    }
+                    p0 = p1 = q = 0.f;
+                }
+            }
+        }
+    }
+}
+
 template <int JPH>
 __global__ void __launch_bounds__(256) gemm_f32(GemmArgs G) {
     constexpr int BK = 16, LS = BM + 16;   // k-major LDS rows, stride = 16 (mod 64) banks
@@ -231,12 +343,12 @@ __global__ void __launch_bounds__(256) gemm_f32(GemmArgs G) {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
+                for (int j = 0; j < 4; ++j) acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[j], a[i], acc[j][i], 0, 0, 0);
         }
         if (kc + 1 < nk) sstore(buf ^ 1);
         __syncthreads();
     }
-    store_tile<JPH, false>(G, t, wm, wn, lane, acc);
+    store_tile<JPH>(G, t, wm, wn, lane, acc, &As[0][wave * 256]);
 }
 
 template <int JPH>
@@ -304,7 +416,7 @@ __global__ void __launch_bounds__(256) gemm_bf16(GemmArgs G) {
         if (kc + 1 < nk) sstore(buf ^ 1);
         __syncthreads();
     }
-    store_tile<JPH, true>(G, t, wm, wn, lane, acc);
+    store_tile_rows<JPH, true>(G, t, wm, wn, lane, acc);
 }
 
 }  // namespace
