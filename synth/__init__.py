@@ -514,3 +514,42 @@ def workload_inputs(name: str, n_cand: Optional[int] = None, first: int = 0):
     masks, opts = make_slices(name, topo.n_dev, wl.n_slices)
     weights = make_weights(wl.f, wl.heads, wl.layers, wl.f_op, wl.f)
     return wl, topo, batch, (masks, opts), weights
+
+
+# --------------------------------------------------------------------------
+# search problems (op grouping, parameter sizes, slice tables)
+# --------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class SearchProblem:
+    """Inputs of the strategy search over one joint graph: the topology, a
+    contiguous op grouping (the paper groups ops before the search; the
+    grouping here is given, not computed), per-op parameter bytes, the
+    training batch's activation scale and the slice table the search picks
+    from for every group."""
+    name: str
+    topo: Topology
+    group_of: np.ndarray    # int32 [N] group id of every op
+    n_groups: int
+    op_params: np.ndarray   # float64 [N] parameter bytes of every op
+    masks: np.ndarray       # uint64 [S]
+    options: np.ndarray     # uint8 [S]
+
+
+def make_search_problem(name: str, n_groups: Optional[int] = None) -> SearchProblem:
+    """The workload's topology cut into `n_groups` contiguous groups (10 for
+    tiny, 60 otherwise) with log-normal parameter sizes (seed (2302, cfg,
+    3_000_000)) and the workload's slice table."""
+    wl = WORKLOADS[name]
+    topo = make_topology(name)
+    k = n_groups if n_groups is not None else (10 if name == "tiny" else 60)
+    n = topo.n_op
+    bounds = [round(i * n / k) for i in range(k + 1)]
+    group_of = np.empty(n, np.int32)
+    for g in range(k):
+        group_of[bounds[g]:bounds[g + 1]] = g
+    rng = rng_for(wl.cfg_id, 3_000_000)
+    params = rng.lognormal(math.log(2e5), 2.0, size=n)
+    masks, opts = make_slices(name, topo.n_dev, wl.n_slices)
+    return SearchProblem(name=name, topo=topo, group_of=group_of, n_groups=k,
+                         op_params=params, masks=masks, options=opts)
