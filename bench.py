@@ -135,6 +135,64 @@ def cpu_baseline(name, wl, topo, batch, masks, opts, w, budget_s: float) -> dict
             "cpu": cpu_model()}
 
 
+def search_bench(args) -> int:
+    """Batched strategy search (Section 4.2.2) on a workload's graph: each
+    round selects B leaves, computes their rewards and packed states on the
+    host, expands the states into GNN inputs, runs forward + decide for the
+    B candidates on the GPU and updates the tree.  Reports leaf evaluations
+    per second with the host and GPU shares of a round."""
+    import torch
+
+    import paper_2302_06126_amd as P
+    import paper_2302_06126_amd.search as PS
+
+    torch.cuda.set_device(0)
+    name = args.workload
+    wl = synth.WORKLOADS[name]
+    B = args.search_batch or wl.batch
+    sp = synth.make_search_problem(name)
+    w = synth.make_weights(wl.f, wl.heads, wl.layers, wl.f_op, wl.f)
+    model = P.Model(w, f=wl.f, heads=wl.heads, layers=wl.layers, f_op=wl.f_op, dtype=wl.dtype, device="cuda:0")
+    prob = PS.SearchProblem(sp, f_op=wl.f_op)
+    svc = PS.SearchService(prob, sp, model, B)
+    tree = PS.Mcts(sp.n_groups, len(sp.masks), args.c_puct, 0.0)
+    print(f"[bench] search on {name}: B={B} groups={sp.n_groups} slices={len(sp.masks)}; warmup {args.warmup}",
+          file=sys.stderr, flush=True)
+    for _ in range(max(args.warmup, 1)):
+        svc.round(tree)
+    torch.cuda.synchronize()
+    host_s = 0.0
+    best = -np.inf
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        h0 = time.perf_counter()
+        leaf, depth, path = tree.select(B)
+        h1 = time.perf_counter()
+        rewards, priors = svc.evaluate(depth, path)
+        h2 = time.perf_counter()
+        tree.update(leaf, depth, path, priors, rewards)
+        h3 = time.perf_counter()
+        host_s += (h1 - h0) + (h3 - h2)
+        best = max(best, float(rewards.max()))
+    el = time.perf_counter() - t0
+    v, e = tree.size()
+    out = {
+        "metric": "search leaf evaluations/sec (batched PUCT with GNN priors)",
+        "value": round(B * args.steps / el, 2), "unit": "leaves/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(el * 1e3 / args.steps, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
+        "config": {"workload": name, "leaves_per_round": B, "groups": sp.n_groups, "slices": len(sp.masks),
+                   "n_op": sp.topo.n_op, "n_dev": sp.topo.n_dev, "f": wl.f, "layers": wl.layers,
+                   "c_puct": args.c_puct, "parallelism": "none"},
+        "tree_ms_per_round": round(host_s * 1e3 / args.steps, 4),
+        "evaluate_ms_per_round": round((el - host_s) * 1e3 / args.steps, 4),
+        "tree_vertices": v, "expanded": e, "best_reward": best,
+    }
+    print(json.dumps(out), flush=True)
+    svc.close()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -147,11 +205,18 @@ def main() -> int:
                     help="run one plain device copy of this size first (counter calibration)")
     ap.add_argument("--stage", default="auto", choices=["auto"] + list(KERNEL_NAMES),
                     help="kernel stage timed for the roofline (auto: the longest one)")
+    ap.add_argument("--mode", default="forward", choices=["forward", "search"],
+                    help="forward: the GNN hot path (default line); search: batched PUCT search rounds")
+    ap.add_argument("--search-batch", type=int, default=0, help="leaves per search round (default: the batch)")
+    ap.add_argument("--c-puct", type=float, default=1.5)
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         sys.exit("bench.py measures one GPU only: this build has no multi-GPU path "
                  "(candidates would shard across GPUs with no per-layer exchange); run with --gpus 1")
+
+    if args.mode == "search":
+        return search_bench(args)
 
     import torch
 

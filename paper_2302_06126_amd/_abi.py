@@ -21,6 +21,11 @@ STATUS_NAMES = {0: "TAG_OK", -1: "TAG_EINVAL", -2: "TAG_ERANGE", -3: "TAG_EDUP",
 EXPORTS = ("tag_graph_plan", "tag_graph_build", "tag_graph_get_info", "tag_graph_export",
            "tag_graph_destroy", "tag_gnn_workspace", "tag_gnn_forward", "tag_gnn_decide_workspace",
            "tag_gnn_decide", "tag_last_error", "tag_version", "tag_profile_begin", "tag_profile_end")
+# include/tag_search.h
+SEARCH_EXPORTS = ("tag_search_problem_create", "tag_search_problem_destroy", "tag_search_order",
+                  "tag_search_evaluate", "tag_mcts_create", "tag_mcts_destroy", "tag_mcts_select",
+                  "tag_mcts_update", "tag_mcts_root_stats", "tag_mcts_best_path", "tag_mcts_size",
+                  "tag_search_device_bytes", "tag_search_upload", "tag_search_pack", "tag_search_features")
 
 # kernel stages (include/tag_profile.h)
 STAGE_NAMES = ("graph_build", "encode", "transform", "agg_op_op", "agg_op_dev", "agg_dev_op", "agg_dev_merge",
@@ -67,6 +72,17 @@ class tag_slices(C.Structure):
     _fields_ = [("n_slices", C.c_int32), ("mask", C.c_void_p), ("option", C.c_void_p)]
 
 
+class tag_search_problem_desc(C.Structure):
+    _fields_ = [("n_op", C.c_int32), ("n_dev", C.c_int32), ("n_groups", C.c_int32), ("n_slices", C.c_int32),
+                ("f_op", C.c_int32), ("group_of", C.c_void_p), ("op_type", C.c_void_p),
+                ("op_flops", C.c_void_p), ("op_bytes", C.c_void_p), ("op_params", C.c_void_p),
+                ("dev_tflops", C.c_void_p), ("dev_mem_gb", C.c_void_p), ("dev_intra_gbs", C.c_void_p),
+                ("e_dd", C.c_int64), ("dd_a", C.c_void_p), ("dd_b", C.c_void_p), ("dd_gbs", C.c_void_p),
+                ("e_oo", C.c_int64), ("oo_src", C.c_void_p), ("oo_dst", C.c_void_p),
+                ("e_od", C.c_int64), ("od_op", C.c_void_p), ("od_dev", C.c_void_p),
+                ("slice_mask", C.c_void_p), ("slice_option", C.c_void_p)]
+
+
 class tag_decision(C.Structure):
     _fields_ = [("mask", C.c_uint64), ("option", C.c_int32), ("replicas", C.c_int32),
                 ("sync", C.c_int32), ("sfb", C.c_int32)]
@@ -111,6 +127,28 @@ def load() -> C.CDLL:
     lib.tag_profile_begin.restype = S
     lib.tag_profile_end.argtypes = [C.POINTER(C.c_double), C.POINTER(C.c_int32)]
     lib.tag_profile_end.restype = S
+    # include/tag_search.h
+    lib.tag_search_problem_create.argtypes = [C.POINTER(tag_search_problem_desc), C.POINTER(vp)]
+    lib.tag_search_problem_destroy.argtypes = [vp]
+    lib.tag_search_problem_destroy.restype = None
+    lib.tag_search_order.argtypes = [vp, vp, vp]
+    lib.tag_search_evaluate.argtypes = [vp, vp, S, C.POINTER(C.c_double), C.POINTER(C.c_double),
+                                        C.POINTER(C.c_int32)]
+    lib.tag_mcts_create.argtypes = [S, S, C.c_double, C.c_double, C.POINTER(vp)]
+    lib.tag_mcts_destroy.argtypes = [vp]
+    lib.tag_mcts_destroy.restype = None
+    lib.tag_mcts_select.argtypes = [vp, S, vp, vp, vp]
+    lib.tag_mcts_update.argtypes = [vp, S, vp, vp, vp, vp, vp]
+    lib.tag_mcts_root_stats.argtypes = [vp, vp, vp]
+    lib.tag_mcts_best_path.argtypes = [vp, vp, C.POINTER(C.c_int32)]
+    lib.tag_mcts_size.argtypes = [vp, C.POINTER(C.c_int64), C.POINTER(C.c_int64)]
+    lib.tag_search_device_bytes.argtypes = [vp, szp, szp]
+    lib.tag_search_upload.argtypes = [vp, vp, C.c_size_t, vp]
+    lib.tag_search_pack.argtypes = [vp, S, vp, vp, S, vp, vp, vp]
+    lib.tag_search_features.argtypes = [vp, S, vp, vp, vp, vp, vp, vp]
+    for name in SEARCH_EXPORTS:
+        if name not in ("tag_search_problem_destroy", "tag_mcts_destroy"):
+            getattr(lib, name).restype = S
     _lib = lib
     return lib
 

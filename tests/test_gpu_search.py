@@ -1,0 +1,111 @@
+"""GPU parity of the batched search service (Section 4.2.2): the feature
+kernel against the reference encoding of search states, and whole search
+rounds (select -> reward + features -> forward -> decide -> update) against
+the reference tree fed with the same priors, whose priors in turn match the
+reference GNN."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from oracle import search as OS
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+    assert torch.cuda.is_available()
+    return torch
+
+
+@pytest.mark.parametrize("name,f_op", [("tiny", 40), ("cnn", 42), ("large", 42)])
+def test_features_kernel_matches_reference(torch, name, f_op):
+    import paper_2302_06126_amd.search as PS
+    _say(f"[search] features {name}")
+    sp = synth.make_search_problem(name)
+    P = OS.Problem(sp)
+    prob = PS.SearchProblem(sp, f_op=f_op)
+    rng = synth.rng_for(58, len(name))
+    depth = np.array([0, 1, 3, P.K // 2, P.K - 1, P.K], np.int32)
+    B = len(depth)
+    path = rng.integers(0, P.S, size=(B, P.K)).astype(np.int32)
+    sb, rb = prob.device_bytes()
+    dev = torch.device("cuda")
+    static = torch.empty(sb, dtype=torch.uint8, device=dev)
+    PS.check(PS._abi.load().tag_search_upload(prob.h, static.data_ptr(), sb, 0), "upload")
+    host = np.zeros(B * rb, np.uint8)
+    prob.pack(depth, path, host.ctypes.data)
+    states = torch.from_numpy(host).to(dev)
+    t = sp.topo
+    x_op = torch.full((B, t.n_op, f_op), np.nan, dtype=torch.float32, device=dev)
+    x_dev = torch.full((B, t.n_dev, 8), np.nan, dtype=torch.float32, device=dev)
+    x_od = torch.full((B, t.e_od), 7, dtype=torch.uint8, device=dev)
+    PS.check(PS._abi.load().tag_search_features(prob.h, B, static.data_ptr(), states.data_ptr(), x_op.data_ptr(),
+                                                x_dev.data_ptr(), x_od.data_ptr(), 0), "features")
+    torch.cuda.synchronize()
+    g_op, g_dev, g_od = x_op.cpu().numpy(), x_dev.cpu().numpy(), x_od.cpu().numpy()
+    for b in range(B):
+        x, xd, xod, _ = OS.features(P, path[b, :depth[b]].tolist(), f_op=f_op)
+        exact = list(range(32)) + list(range(34, 40))          # one-hots and flags
+        assert np.array_equal(g_op[b][:, exact], x[:, exact]), b
+        np.testing.assert_allclose(g_op[b], x, rtol=2e-6, atol=1e-6)
+        np.testing.assert_allclose(g_dev[b], xd, rtol=2e-6, atol=1e-6)
+        assert np.array_equal(g_od[b], xod), b
+    prob.close()
+
+
+@pytest.mark.parametrize("name,B,rounds", [("tiny", 8, 6), ("cnn", 16, 4)])
+def test_search_rounds_match_reference_tree(torch, name, B, rounds):
+    """The service's rounds, replayed through the reference tree with the
+    priors the GPU produced and the reference rewards, select the same
+    leaves and end with the same statistics; round 0's priors (the root
+    expansion) match the reference GNN's."""
+    import paper_2302_06126_amd as P0
+    import paper_2302_06126_amd.search as PS
+    _say(f"[search] rounds {name} B={B}")
+    wl = synth.WORKLOADS[name]
+    sp = synth.make_search_problem(name)
+    P = OS.Problem(sp)
+    w = synth.make_weights(wl.f, wl.heads, wl.layers, wl.f_op, wl.f)
+    model = P0.Model(w, f=wl.f, heads=wl.heads, layers=wl.layers, f_op=wl.f_op, dtype=wl.dtype)
+    prob = PS.SearchProblem(sp, f_op=wl.f_op)
+    svc = PS.SearchService(prob, sp, model, B)
+    lib = PS.Mcts(P.K, P.S, 1.5, 0.0)
+    ref = OS.Tree(P.K, P.S, 1.5, 0.0)
+    T_base = OS.evaluate(P, OS.full_strategy(P, []))["T"]
+    first = None
+    for rnd in range(rounds):
+        leaf, depth, path = lib.select(B)
+        leaves = ref.select(B)
+        for b, (_, p) in enumerate(leaves):
+            assert list(path[b, :depth[b]]) == p, (rnd, b)
+        rewards, priors = svc.evaluate(depth, path)
+        priors = priors.copy()
+        for b, (_, p) in enumerate(leaves):
+            assert rewards[b] == pytest.approx(OS.reward(P, p, T_base), rel=1e-12)
+        if first is None:
+            first = (path[0, :depth[0]].tolist(), priors[0].copy())
+        lib.update(leaf, depth, path, priors, rewards)
+        ref.update(leaves, priors, rewards)
+    n, q = lib.root_stats()
+    rn, rq = ref.root_stats()
+    assert list(n) == rn and list(q) == rq
+    # round 0, leaf 0 is the root: its priors against the reference GNN on the reference features
+    p0, pr0 = first
+    x, xd, xod, rep = OS.features(P, p0, f_op=wl.f_op)
+    t = sp.topo
+    x_oo = (np.log10(t.op_bytes[t.oo_src]) - 6.0).astype(np.float32)
+    x_dd = np.stack([np.log10(t.dd_bw) - 1.0, np.zeros(t.e_dd)], axis=1).astype(np.float32)
+    E_op, E_dev = oracle.forward(t, x, xd, x_oo, x_dd, xod, w, f=wl.f, heads=wl.heads, layers=wl.layers)
+    od = oracle.decide(E_op, E_dev, sp.masks, sp.options, np.array([rep], np.int32), w, f=wl.f,
+                       dec_hidden=wl.f, n_dev=t.n_dev, want_prior=True)
+    np.testing.assert_allclose(pr0, od["prior"][0], rtol=1e-3, atol=1e-6)
+    svc.close()
+    lib.close()
+    prob.close()
