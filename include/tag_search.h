@@ -117,10 +117,11 @@ void tag_mcts_destroy(tag_mcts *t);
  * Each edge on the path now holds one in-flight visit. */
 tag_status tag_mcts_select(tag_mcts *t, int32_t B, int32_t *leaf, int32_t *depth, int32_t *path);
 
-/* Apply the B leaves of the last select, in order: a leaf with depth <
+/* Apply the B leaves of an earlier select, in order: a leaf with depth <
  * n_levels that is not expanded yet is expanded with priors[b * n_actions +
  * a] (>= 0, finite); then every edge of its path gets reward rewards[b].
- * The arguments must be exactly those select returned (TAG_EINVAL if a path
+ * The arguments must be exactly those a select returned and that no update
+ * has applied yet; several selects may be outstanding (TAG_EINVAL if a path
  * does not match the tree or holds no in-flight visit). */
 tag_status tag_mcts_update(tag_mcts *t, int32_t B, const int32_t *leaf, const int32_t *depth,
                            const int32_t *path, const float *priors, const double *rewards);
@@ -159,6 +160,48 @@ tag_status tag_search_pack(const tag_search_problem *p, int32_t B, const int32_t
 tag_status tag_search_features(const tag_search_problem *p, int32_t B, const void *static_dev,
                                const void *states_dev, float *x_op, float *x_dev, uint8_t *x_od,
                                void *hip_stream);
+
+/* ---- native search rounds ---------------------------------------------- */
+
+/* Everything a run of search rounds needs.  The GNN inputs of a leaf are the
+ * features tag_search_features writes plus the shared x_oo / x_dd rows. */
+typedef struct tag_search_run_args {
+    const tag_search_problem *problem;
+    tag_mcts *tree;                   /* n_levels = n_groups, n_actions = n_slices       */
+    const tag_graph *graph;           /* built from the problem's topology (one topology) */
+    const tag_model_dims *dims;       /* f_op must equal the problem's f_op               */
+    const tag_weights *weights;       /* DEVICE parameters                                */
+    const float *x_oo;                /* DEVICE [e_oo] tensor features of every leaf      */
+    const float *x_dd;                /* DEVICE [e_dd][2] link features of every leaf     */
+    const tag_slices *slices;         /* DEVICE copy of the problem's slice table         */
+    int32_t batch;                    /* B >= 1 leaves per round                          */
+    int32_t rounds;                   /* >= 1                                             */
+    int32_t pipelined;                /* 1: round k+1 is selected, packed and enqueued    */
+                                      /* before round k's update (its paths then also     */
+                                      /* carry round k's in-flight visits); 0: strictly   */
+                                      /* select, evaluate, update per round               */
+    void *workspace;                  /* DEVICE, >= tag_search_run_workspace dev_bytes   */
+    size_t ws_bytes;
+    void *host_buf;                   /* pinned HOST, >= host_bytes                       */
+    size_t host_bytes;
+    /* optional HOST outputs (NULL to skip), in selection order:                          */
+    int32_t *depth_out;               /* [rounds * B]                                     */
+    int32_t *path_out;                /* [rounds * B * n_groups]                          */
+    double *reward_out;               /* [rounds * B]                                     */
+    float *prior_out;                 /* [rounds * B * n_slices]                          */
+} tag_search_run_args;
+
+tag_status tag_search_run_workspace(const tag_search_problem *p, const tag_graph *g, const tag_model_dims *dims,
+                                    int32_t batch, size_t *dev_bytes, size_t *host_bytes);
+
+/* Run `rounds` rounds: select B leaves, compute their rewards and states on
+ * the host, expand the states, forward + decide on the GPU (one query per
+ * leaf: the next group's representative op), update the tree with the
+ * priors and rewards.  Synchronous: returns when the last update is done.
+ * Uses only the caller's buffers (no allocation on the device).  On a
+ * non-OK status the stream has been drained, and the tree may still hold
+ * the in-flight visits of rounds that were selected but not updated. */
+tag_status tag_search_run(const tag_search_run_args *a, void *hip_stream);
 
 #ifdef __cplusplus
 }

@@ -25,7 +25,8 @@ EXPORTS = ("tag_graph_plan", "tag_graph_build", "tag_graph_get_info", "tag_graph
 SEARCH_EXPORTS = ("tag_search_problem_create", "tag_search_problem_destroy", "tag_search_order",
                   "tag_search_evaluate", "tag_mcts_create", "tag_mcts_destroy", "tag_mcts_select",
                   "tag_mcts_update", "tag_mcts_root_stats", "tag_mcts_best_path", "tag_mcts_size",
-                  "tag_search_device_bytes", "tag_search_upload", "tag_search_pack", "tag_search_features")
+                  "tag_search_device_bytes", "tag_search_upload", "tag_search_pack", "tag_search_features",
+                  "tag_search_run_workspace", "tag_search_run")
 
 # kernel stages (include/tag_profile.h)
 STAGE_NAMES = ("graph_build", "encode", "transform", "agg_op_op", "agg_op_dev", "agg_dev_op", "agg_dev_merge",
@@ -81,6 +82,15 @@ class tag_search_problem_desc(C.Structure):
                 ("e_oo", C.c_int64), ("oo_src", C.c_void_p), ("oo_dst", C.c_void_p),
                 ("e_od", C.c_int64), ("od_op", C.c_void_p), ("od_dev", C.c_void_p),
                 ("slice_mask", C.c_void_p), ("slice_option", C.c_void_p)]
+
+
+class tag_search_run_args(C.Structure):
+    _fields_ = [("problem", C.c_void_p), ("tree", C.c_void_p), ("graph", C.c_void_p), ("dims", C.c_void_p),
+                ("weights", C.c_void_p), ("x_oo", C.c_void_p), ("x_dd", C.c_void_p), ("slices", C.c_void_p),
+                ("batch", C.c_int32), ("rounds", C.c_int32), ("pipelined", C.c_int32),
+                ("workspace", C.c_void_p), ("ws_bytes", C.c_size_t), ("host_buf", C.c_void_p),
+                ("host_bytes", C.c_size_t), ("depth_out", C.c_void_p), ("path_out", C.c_void_p),
+                ("reward_out", C.c_void_p), ("prior_out", C.c_void_p)]
 
 
 class tag_decision(C.Structure):
@@ -146,6 +156,8 @@ def load() -> C.CDLL:
     lib.tag_search_upload.argtypes = [vp, vp, C.c_size_t, vp]
     lib.tag_search_pack.argtypes = [vp, S, vp, vp, S, vp, vp, vp]
     lib.tag_search_features.argtypes = [vp, S, vp, vp, vp, vp, vp, vp]
+    lib.tag_search_run_workspace.argtypes = [vp, vp, C.POINTER(tag_model_dims), S, szp, szp]
+    lib.tag_search_run.argtypes = [C.POINTER(tag_search_run_args), vp]
     for name in SEARCH_EXPORTS:
         if name not in ("tag_search_problem_destroy", "tag_mcts_destroy"):
             getattr(lib, name).restype = S

@@ -236,5 +236,42 @@ class SearchService:
         tree.update(leaf, depth, path, priors, rewards)
         return rewards
 
+    def run(self, tree: Mcts, rounds: int, pipelined: bool = True, record: bool = False, stream=None):
+        """`rounds` rounds in native code (tag_search_run).  With `record`,
+        returns the rounds' depths, paths, rewards and priors (host arrays in
+        selection order)."""
+        import ctypes as C
+        from ._abi import tag_search_run_args
+        torch = self.torch
+        if not hasattr(self, "run_ws"):
+            db, hb = C.c_size_t(0), C.c_size_t(0)
+            check(_abi.load().tag_search_run_workspace(self.problem.h, self.graph.handle, C.byref(self.model.dims),
+                                                       self.B, C.byref(db), C.byref(hb)), "tag_search_run_workspace")
+            self.run_ws = torch.empty(db.value, dtype=torch.uint8, device=self.dev)
+            self.run_host = torch.empty(hb.value, dtype=torch.uint8, pin_memory=True)
+        B, L, S = self.B, tree.L, tree.S
+        rec = None
+        if record:
+            rec = {"depth": np.zeros(rounds * B, np.int32), "path": np.zeros(rounds * B * L, np.int32),
+                   "reward": np.zeros(rounds * B, np.float64), "prior": np.zeros(rounds * B * S, np.float32)}
+        a = tag_search_run_args()
+        a.problem, a.tree, a.graph = self.problem.h, tree.h, self.graph.handle
+        a.dims = C.addressof(self.model.dims)
+        a.weights = C.addressof(self.model.weights)
+        a.x_oo, a.x_dd = self.x_oo.data_ptr(), self.x_dd.data_ptr()
+        a.slices = C.addressof(self.slices)
+        a.batch, a.rounds, a.pipelined = B, rounds, 1 if pipelined else 0
+        a.workspace, a.ws_bytes = self.run_ws.data_ptr(), self.run_ws.numel()
+        a.host_buf, a.host_bytes = self.run_host.data_ptr(), self.run_host.numel()
+        if rec is not None:
+            a.depth_out, a.path_out = rec["depth"].ctypes.data, rec["path"].ctypes.data
+            a.reward_out, a.prior_out = rec["reward"].ctypes.data, rec["prior"].ctypes.data
+        st = torch.cuda.current_stream() if stream is None else stream
+        check(_abi.load().tag_search_run(C.byref(a), int(st.cuda_stream)), "tag_search_run")
+        if rec is None:
+            return None
+        return {"depth": rec["depth"].reshape(rounds, B), "path": rec["path"].reshape(rounds, B, L),
+                "reward": rec["reward"].reshape(rounds, B), "prior": rec["prior"].reshape(rounds, B, S)}
+
     def close(self) -> None:
         self.graph.close()

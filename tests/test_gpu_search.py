@@ -109,3 +109,50 @@ def test_search_rounds_match_reference_tree(torch, name, B, rounds):
     svc.close()
     lib.close()
     prob.close()
+
+
+@pytest.mark.parametrize("name,B,rounds,pipelined", [("tiny", 8, 6, True), ("cnn", 16, 5, True),
+                                                      ("cnn", 16, 4, False)])
+def test_native_rounds_match_reference_schedule(torch, name, B, rounds, pipelined):
+    """tag_search_run: the recorded leaves, replayed through the reference
+    tree in the same select / update schedule (pipelined: round k+1 is
+    selected before round k's update) with the recorded priors and the
+    reference rewards, give the same paths and the same root statistics."""
+    import paper_2302_06126_amd as P0
+    import paper_2302_06126_amd.search as PS
+    _say(f"[search] native rounds {name} B={B} pipelined={pipelined}")
+    wl = synth.WORKLOADS[name]
+    sp = synth.make_search_problem(name)
+    P = OS.Problem(sp)
+    w = synth.make_weights(wl.f, wl.heads, wl.layers, wl.f_op, wl.f)
+    model = P0.Model(w, f=wl.f, heads=wl.heads, layers=wl.layers, f_op=wl.f_op, dtype=wl.dtype)
+    prob = PS.SearchProblem(sp, f_op=wl.f_op)
+    svc = PS.SearchService(prob, sp, model, B)
+    lib = PS.Mcts(P.K, P.S, 1.5, 0.0)
+    rec = svc.run(lib, rounds, pipelined=pipelined, record=True)
+    ref = OS.Tree(P.K, P.S, 1.5, 0.0)
+    T_base = OS.evaluate(P, OS.full_strategy(P, []))["T"]
+    sel = {0: ref.select(B)}
+    for k in range(rounds):
+        if pipelined and k + 1 < rounds:
+            sel[k + 1] = ref.select(B)
+        for b, (_, p) in enumerate(sel[k]):
+            assert rec["depth"][k, b] == len(p) and list(rec["path"][k, b, :len(p)]) == p, (k, b)
+            assert rec["reward"][k, b] == pytest.approx(OS.reward(P, p, T_base), rel=1e-12)
+        ref.update(sel[k], rec["prior"][k], rec["reward"][k])
+        if not pipelined and k + 1 < rounds:
+            sel[k + 1] = ref.select(B)
+    n, q = lib.root_stats()
+    rn, rq = ref.root_stats()
+    assert list(n) == rn and list(q) == rq
+    # the step-wise binding, strictly per round, builds the same tree as the native rounds
+    if not pipelined:
+        lib2 = PS.Mcts(P.K, P.S, 1.5, 0.0)
+        for _ in range(rounds):
+            svc.round(lib2)
+        n2, q2 = lib2.root_stats()
+        assert list(n2) == list(n) and list(q2) == list(q)
+        lib2.close()
+    svc.close()
+    lib.close()
+    prob.close()
