@@ -28,6 +28,9 @@ SEARCH_EXPORTS = ("tag_search_problem_create", "tag_search_problem_destroy", "ta
                   "tag_search_device_bytes", "tag_search_upload", "tag_search_pack", "tag_search_features",
                   "tag_search_run_workspace", "tag_search_run")
 
+# include/tag_train.h
+TRAIN_EXPORTS = ("tag_train_workspace", "tag_train_step")
+
 # kernel stages (include/tag_profile.h)
 STAGE_NAMES = ("graph_build", "encode", "transform", "agg_op_op", "agg_op_dev", "agg_dev_op", "agg_dev_merge",
                "dev_prep", "decide")
@@ -71,6 +74,15 @@ class tag_features(C.Structure):
 
 class tag_slices(C.Structure):
     _fields_ = [("n_slices", C.c_int32), ("mask", C.c_void_p), ("option", C.c_void_p)]
+
+
+class tag_grads(C.Structure):
+    _fields_ = tag_weights._fields_
+
+
+class tag_train_batch(C.Structure):
+    _fields_ = [("n_query", C.c_int32), ("query_rep", _PF), ("query_graph", _PF), ("query_op", _PF),
+                ("target", _PF)]
 
 
 class tag_search_problem_desc(C.Structure):
@@ -158,6 +170,12 @@ def load() -> C.CDLL:
     lib.tag_search_features.argtypes = [vp, S, vp, vp, vp, vp, vp, vp]
     lib.tag_search_run_workspace.argtypes = [vp, vp, C.POINTER(tag_model_dims), S, szp, szp]
     lib.tag_search_run.argtypes = [C.POINTER(tag_search_run_args), vp]
+    lib.tag_train_workspace.argtypes = [vp, C.POINTER(tag_model_dims), S, S, S, szp]
+    lib.tag_train_step.argtypes = [vp, C.POINTER(tag_model_dims), C.POINTER(tag_weights), C.POINTER(tag_features),
+                                   C.POINTER(tag_slices), C.POINTER(tag_train_batch), C.POINTER(tag_grads),
+                                   C.c_float, vp, vp, C.c_size_t, vp]
+    for name in TRAIN_EXPORTS:
+        getattr(lib, name).restype = S
     for name in SEARCH_EXPORTS:
         if name not in ("tag_search_problem_destroy", "tag_mcts_destroy"):
             getattr(lib, name).restype = S

@@ -22,6 +22,7 @@
 #include <algorithm>
 
 #include "agg_common.hpp"
+#include "fwd_internal.hpp"
 #include "transform.hpp"
 
 namespace tag {
@@ -278,65 +279,6 @@ __global__ void __launch_bounds__(256) agg_dev_final(AggArgs A) {
     store_row<CPL, BF>(A.H_dev, ((int64_t)rep * A.n_dev + j) * F + c0, A.out_f32 != 0, out);
 }
 
-// ------------------------------------------------------------------ planning
-struct FwdLayout {
-    float *U, *cp;
-    uint16_t *Wb;
-    void *H_op[2], *H_dev[2];
-    void *Y_op, *Y_dev;
-    float *part;
-    int32_t maxc;
-    bool mfma;
-    uint64_t *omask;
-    float *Sdev, *T, *Sop;
-};
-
-tag_status check_dims(const tag_model_dims *d) {
-    if (!d) TAG_FAIL(TAG_EINVAL, "dims is NULL");
-    if (d->f != 64 && d->f != 128 && d->f != 256) TAG_FAIL(TAG_ESHAPE, "f must be 64, 128 or 256");
-    if (d->heads < 1 || d->heads > 64 || (d->heads & (d->heads - 1)))
-        TAG_FAIL(TAG_ESHAPE, "heads must be a power of two in [1, 64]");
-    if (d->layers < 1 || d->layers > 16) TAG_FAIL(TAG_ESHAPE, "layers must be in [1, 16]");
-    if (d->f_op < 1 || d->f_op > 64 || d->f_dev < 1 || d->f_dev > 64)
-        TAG_FAIL(TAG_ESHAPE, "f_op and f_dev must be in [1, 64]");
-    if (d->dec_hidden < 0 || d->dec_hidden > 1024) TAG_FAIL(TAG_ESHAPE, "dec_hidden must be in [0, 1024]");
-    if (d->dtype != TAG_F32 && d->dtype != TAG_BF16) TAG_FAIL(TAG_EINVAL, "dtype must be TAG_F32 or TAG_BF16");
-    if (!(d->gamma_same == d->gamma_same) || !(d->gamma_cross == d->gamma_cross))
-        TAG_FAIL(TAG_EINVAL, "gamma must not be NaN");
-    if (!(d->leaky_slope >= 0.f && d->leaky_slope <= 1.f))
-        TAG_FAIL(TAG_EINVAL, "leaky_slope must be in [0, 1]");
-    return TAG_OK;
-}
-
-size_t carve_fwd(const tag_graph *g, const tag_model_dims *d, int32_t R, void *base, FwdLayout *L) {
-    Carver c(base);
-    const int F = d->f;
-    const size_t es = d->dtype == TAG_BF16 ? 2 : 4;
-    L->U = c.take<float>((size_t)d->layers * 3 * F * 2);
-    L->cp = c.take<float>((size_t)d->layers * 3 * F);
-    L->Wb = d->dtype == TAG_BF16 ? c.take<uint16_t>((size_t)d->layers * 3 * F * F) : nullptr;
-    for (int i = 0; i < 2; ++i) {
-        L->H_op[i] = c.take<char>((size_t)R * g->n_op * F * es);
-        L->H_dev[i] = c.take<char>((size_t)R * g->n_dev * F * es);
-    }
-    L->Y_op = c.take<char>((size_t)R * g->n_op * 2 * F * es);
-    L->Y_dev = c.take<char>((size_t)R * g->n_dev * 2 * F * es);
-    L->mfma = mfma_path_supported(F, d->heads);
-    L->maxc = L->mfma ? std::max<int32_t>(1, g->max_groups)
-                      : std::max<int32_t>(1, (g->max_degree[2] + kChunk - 1) / kChunk);
-    L->part = c.take<float>((size_t)R * g->n_dev * L->maxc * (F + 2 * d->heads));
-    if (L->mfma) {
-        L->omask = c.take<uint64_t>((size_t)R * g->n_op * 2);
-        L->Sdev = c.take<float>((size_t)R * g->n_dev * 4 * d->heads);
-        L->T = c.take<float>((size_t)R * g->n_dev * 2 * F);
-        L->Sop = c.take<float>((size_t)R * g->n_op * 4 * d->heads);
-    } else {
-        L->omask = nullptr;
-        L->Sdev = L->T = L->Sop = nullptr;
-    }
-    return c.used;
-}
-
 template <int F, int K, bool BF>
 void launch_agg(const AggArgs &A, hipStream_t st) {
     const int64_t op_waves = (int64_t)A.R * A.n_op;
@@ -390,6 +332,54 @@ tag_status dispatch_agg(int F, int K, bool bf, bool mfma, const AggArgs &A, hipS
 }
 
 }  // namespace
+
+// ------------------------------------------------------------------ planning
+tag_status check_dims(const tag_model_dims *d) {
+    if (!d) TAG_FAIL(TAG_EINVAL, "dims is NULL");
+    if (d->f != 64 && d->f != 128 && d->f != 256) TAG_FAIL(TAG_ESHAPE, "f must be 64, 128 or 256");
+    if (d->heads < 1 || d->heads > 64 || (d->heads & (d->heads - 1)))
+        TAG_FAIL(TAG_ESHAPE, "heads must be a power of two in [1, 64]");
+    if (d->layers < 1 || d->layers > 16) TAG_FAIL(TAG_ESHAPE, "layers must be in [1, 16]");
+    if (d->f_op < 1 || d->f_op > 64 || d->f_dev < 1 || d->f_dev > 64)
+        TAG_FAIL(TAG_ESHAPE, "f_op and f_dev must be in [1, 64]");
+    if (d->dec_hidden < 0 || d->dec_hidden > 1024) TAG_FAIL(TAG_ESHAPE, "dec_hidden must be in [0, 1024]");
+    if (d->dtype != TAG_F32 && d->dtype != TAG_BF16) TAG_FAIL(TAG_EINVAL, "dtype must be TAG_F32 or TAG_BF16");
+    if (!(d->gamma_same == d->gamma_same) || !(d->gamma_cross == d->gamma_cross))
+        TAG_FAIL(TAG_EINVAL, "gamma must not be NaN");
+    if (!(d->leaky_slope >= 0.f && d->leaky_slope <= 1.f))
+        TAG_FAIL(TAG_EINVAL, "leaky_slope must be in [0, 1]");
+    return TAG_OK;
+}
+
+size_t carve_fwd(const tag_graph *g, const tag_model_dims *d, int32_t R, void *base, FwdLayout *L) {
+    Carver c(base);
+    const int F = d->f;
+    const size_t es = d->dtype == TAG_BF16 ? 2 : 4;
+    L->U = c.take<float>((size_t)d->layers * 3 * F * 2);
+    L->cp = c.take<float>((size_t)d->layers * 3 * F);
+    L->Wb = d->dtype == TAG_BF16 ? c.take<uint16_t>((size_t)d->layers * 3 * F * F) : nullptr;
+    for (int i = 0; i < 2; ++i) {
+        L->H_op[i] = c.take<char>((size_t)R * g->n_op * F * es);
+        L->H_dev[i] = c.take<char>((size_t)R * g->n_dev * F * es);
+    }
+    L->Y_op = c.take<char>((size_t)R * g->n_op * 2 * F * es);
+    L->Y_dev = c.take<char>((size_t)R * g->n_dev * 2 * F * es);
+    L->mfma = mfma_path_supported(F, d->heads);
+    L->maxc = L->mfma ? std::max<int32_t>(1, g->max_groups)
+                      : std::max<int32_t>(1, (g->max_degree[2] + kChunk - 1) / kChunk);
+    L->part = c.take<float>((size_t)R * g->n_dev * L->maxc * (F + 2 * d->heads));
+    if (L->mfma) {
+        L->omask = c.take<uint64_t>((size_t)R * g->n_op * 2);
+        L->Sdev = c.take<float>((size_t)R * g->n_dev * 4 * d->heads);
+        L->T = c.take<float>((size_t)R * g->n_dev * 2 * F);
+        L->Sop = c.take<float>((size_t)R * g->n_op * 4 * d->heads);
+    } else {
+        L->omask = nullptr;
+        L->Sdev = L->T = L->Sop = nullptr;
+    }
+    return c.used;
+}
+
 }  // namespace tag
 
 using namespace tag;
@@ -410,6 +400,57 @@ extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *
                                       const tag_features *x, void *workspace, size_t ws_bytes, float *E_op,
                                       float *E_dev, void *hip_stream) {
     clear_error();
+    return forward_run(g, dims, w, x, workspace, ws_bytes, E_op, E_dev, static_cast<hipStream_t>(hip_stream),
+                       nullptr);
+}
+
+namespace tag {
+
+// Relation transforms of layer l (Y = W^h h + c', attention terms, device
+// message table) for the hidden rows H_op / H_dev, into the layout's buffers.
+void launch_layer_transform(const tag_graph *g, const tag_model_dims *dims, const tag_weights *w,
+                            const FwdLayout &L, int32_t R, int l, const void *H_op, const void *H_dev,
+                            hipStream_t stream) {
+    const int F = dims->f, K = dims->heads;
+    const bool bf = dims->dtype == TAG_BF16;
+    const int64_t rows_op = (int64_t)R * g->n_op, rows_dev = (int64_t)R * g->n_dev;
+    const int D = F / K;
+    const int jph = (L.mfma && D <= 64) ? D / 16 : 0;
+    const float *att_src = w->att_src + (size_t)l * 3 * F, *att_dst = w->att_dst + (size_t)l * 3 * F;
+    const float *U = L.U + (size_t)l * 3 * F * 2, *cp = L.cp + (size_t)l * 3 * F;
+    GemmArgs ga{};
+    ga.F = F;
+    ga.prep.jph = jph;
+    ga.prep.K = K;
+    ga.prep.a_od = att_src + F;
+    ga.prep.ad_od = att_dst + F;
+    ga.prep.cp_od = cp + F;
+    ga.prep.u_od = U + 2 * F;
+    ga.prep.cp_same[0] = cp;
+    ga.prep.cp_same[1] = cp + 2 * F;
+    ga.prep.ad_same[0] = att_dst;
+    ga.prep.ad_same[1] = att_dst + 2 * F;
+    ga.prep.S[0] = L.Sop;
+    ga.prep.S[1] = L.Sdev;
+    ga.prep.T = L.T;
+    ga.tiles0 = transform_row_tiles(rows_op);
+    if (bf) {
+        const uint16_t *Wl = L.Wb + (size_t)l * 3 * F * F;
+        ga.side[0] = GemmSide{H_op, rows_op, Wl + 0 * F * F, Wl + 1 * F * F, F, L.Y_op};
+        ga.side[1] = GemmSide{H_dev, rows_dev, Wl + 2 * F * F, Wl + 1 * F * F, F, L.Y_dev};
+    } else {
+        const float *Wl = w->layer_w + (size_t)l * 3 * F * 2 * F;
+        ga.side[0] = GemmSide{H_op, rows_op, Wl + 0 * F * 2 * F, Wl + 1 * F * 2 * F, 2 * F, L.Y_op};
+        ga.side[1] = GemmSide{H_dev, rows_dev, Wl + 2 * F * 2 * F, Wl + 1 * F * 2 * F, 2 * F, L.Y_dev};
+    }
+    prof_begin(TAG_STAGE_TRANSFORM, stream);
+    launch_transform(ga, bf, stream);
+    prof_end(TAG_STAGE_TRANSFORM, stream);
+}
+
+tag_status forward_run(const tag_graph *g, const tag_model_dims *dims, const tag_weights *w, const tag_features *x,
+                       void *workspace, size_t ws_bytes, float *E_op, float *E_dev, hipStream_t stream,
+                       const FwdSave *save) {
     if (!g || !w || !x || !E_op || !E_dev || !workspace)
         TAG_FAIL(TAG_EINVAL, "graph, weights, features, outputs and workspace must be non-NULL");
     tag_status st = check_dims(dims);
@@ -431,9 +472,12 @@ extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *
     FwdLayout L;
     if (carve_fwd(g, dims, R, nullptr, &L) > ws_bytes) TAG_FAIL(TAG_ENOSPACE, "workspace too small (see tag_gnn_workspace)");
     carve_fwd(g, dims, R, workspace, &L);
-    hipStream_t stream = static_cast<hipStream_t>(hip_stream);
     const int F = dims->f, K = dims->heads, NL = dims->layers;
     const bool bf = dims->dtype == TAG_BF16;
+    if (save && bf) TAG_FAIL(TAG_ESHAPE, "saved activations need the fp32 variant");
+    // hidden rows of layer l: the ping-pong buffers, or the caller's slots
+    auto h_op = [&](int l) -> void * { return save ? static_cast<void *>(save->H_op[l]) : L.H_op[l & 1]; };
+    auto h_dev = [&](int l) -> void * { return save ? static_cast<void *>(save->H_dev[l]) : L.H_dev[l & 1]; };
 
     FoldArgs fa{w->layer_w, w->layer_b, {w->enc_edge_w[0], w->enc_edge_w[1], w->enc_edge_w[2]},
                 {w->enc_edge_b[0], w->enc_edge_b[1], w->enc_edge_b[2]}, L.U, L.cp, F};
@@ -445,9 +489,9 @@ extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *
     {
         // h0 = ReLU(A x + c) as a small-K MFMA GEMM per node type
         SmallGemm eo{x->x_op, dims->f_op, rows_op, nullptr, dims->f_op, w->enc_op_w, dims->f_op, F,
-                     w->enc_op_b, 1, L.H_op[0], F, bf ? 1 : 0};
+                     w->enc_op_b, 1, h_op(0), F, bf ? 1 : 0};
         SmallGemm ed{x->x_dev, dims->f_dev, rows_dev, nullptr, dims->f_dev, w->enc_dev_w, dims->f_dev, F,
-                     w->enc_dev_b, 1, L.H_dev[0], F, bf ? 1 : 0};
+                     w->enc_dev_b, 1, h_dev(0), F, bf ? 1 : 0};
         prof_begin(TAG_STAGE_ENCODE, stream);
         launch_small_gemm(eo, stream);
         launch_small_gemm(ed, stream);
@@ -476,48 +520,23 @@ extern "C" tag_status tag_gnn_forward(const tag_graph *g, const tag_model_dims *
     const int jph = (L.mfma && D <= 64) ? D / 16 : 0;
     A.prep_done = jph > 0 ? 1 : 0;
     for (int l = 0; l < NL; ++l) {
-        const int cur = l & 1, nxt = cur ^ 1;
         const bool last = (l == NL - 1);
         A.att_src = w->att_src + (size_t)l * 3 * F;
         A.att_dst = w->att_dst + (size_t)l * 3 * F;
         A.U = L.U + (size_t)l * 3 * F * 2;
         A.cp = L.cp + (size_t)l * 3 * F;
         // relation transforms: op rows [W^h_oo ; W^h_od], device rows [W^h_dd ; W^h_od]
-        {
-            GemmArgs ga{};
-            ga.F = F;
-            ga.prep.jph = jph;
-            ga.prep.K = K;
-            ga.prep.a_od = A.att_src + F;
-            ga.prep.ad_od = A.att_dst + F;
-            ga.prep.cp_od = A.cp + F;
-            ga.prep.u_od = A.U + 2 * F;
-            ga.prep.cp_same[0] = A.cp;
-            ga.prep.cp_same[1] = A.cp + 2 * F;
-            ga.prep.ad_same[0] = A.att_dst;
-            ga.prep.ad_same[1] = A.att_dst + 2 * F;
-            ga.prep.S[0] = L.Sop;
-            ga.prep.S[1] = L.Sdev;
-            ga.prep.T = L.T;
-            ga.tiles0 = transform_row_tiles(rows_op);
-            if (bf) {
-                const uint16_t *Wl = L.Wb + (size_t)l * 3 * F * F;
-                ga.side[0] = GemmSide{L.H_op[cur], rows_op, Wl + 0 * F * F, Wl + 1 * F * F, F, L.Y_op};
-                ga.side[1] = GemmSide{L.H_dev[cur], rows_dev, Wl + 2 * F * F, Wl + 1 * F * F, F, L.Y_dev};
-            } else {
-                const float *Wl = w->layer_w + (size_t)l * 3 * F * 2 * F;
-                ga.side[0] = GemmSide{L.H_op[cur], rows_op, Wl + 0 * F * 2 * F, Wl + 1 * F * 2 * F, 2 * F, L.Y_op};
-                ga.side[1] = GemmSide{L.H_dev[cur], rows_dev, Wl + 2 * F * 2 * F, Wl + 1 * F * 2 * F, 2 * F, L.Y_dev};
-            }
-            prof_begin(TAG_STAGE_TRANSFORM, stream);
-            launch_transform(ga, bf, stream);
-            prof_end(TAG_STAGE_TRANSFORM, stream);
-        }
-        A.H_op = last ? static_cast<void *>(E_op) : L.H_op[nxt];
-        A.H_dev = last ? static_cast<void *>(E_dev) : L.H_dev[nxt];
+        FwdLayout Ll = L;
+        if (save) { Ll.Y_op = save->Y_op[l]; Ll.Y_dev = save->Y_dev[l]; }
+        A.Y_op = Ll.Y_op; A.Y_dev = Ll.Y_dev;
+        launch_layer_transform(g, dims, w, Ll, R, l, h_op(l), h_dev(l), stream);
+        A.H_op = last ? static_cast<void *>(E_op) : h_op(l + 1);
+        A.H_dev = last ? static_cast<void *>(E_dev) : h_dev(l + 1);
         A.out_f32 = last ? 1 : (bf ? 0 : 1);
         st = dispatch_agg(F, K, bf, L.mfma, A, stream);
         if (st != TAG_OK) return st;
     }
     return launch_status("tag_gnn_forward");
 }
+
+}  // namespace tag

@@ -1,0 +1,1261 @@
+// Training step of the GNN (Section 4.2.2: the prior G(s, a) of the decoder
+// is trained toward the search's selection probabilities pi(s, a) by
+// minimising their cross entropy), fp32.
+//
+//   loss = -(1/Q) sum_q sum_a target[q][a] log softmax_a(score[q][a])
+//
+// Forward: the forward pass of forward.hip with every layer's input rows H^l
+// and relation transforms Y^l = W^h H^l + c' kept (no recomputation).
+//
+// Backward, per layer from the last to the first, with dO_u = gamma_r dH'_u
+// the gradient reaching destination u's gamma-weighted sum of relation r:
+//   scores   (per entry e = (u <- v), per head k)
+//              s_e = LeakyReLU(a . m_e + adst . (Y_u - c')),  m_e = ReLU(Y_v + U x_e)
+//              dalpha_e = dO_u . m_e
+//   softmax  (per destination row) alpha_e = softmax(s), c_u = sum_e alpha_e dalpha_e,
+//              dz_e = alpha_e (dalpha_e - c_u) LeakyReLU'(s_e),  Z_u = sum_e dz_e
+//   messages (per source row v, over the entries it feeds)
+//              dm_e = alpha_e dO_u + dz_e a,  dpre_e = dm_e [m_e > 0]
+//              dY_v = sum_e dpre_e + Z_v adst      (Z_v: v as a destination)
+//            and the parameter sums d a = sum dz m, d adst = sum Z (Y - c'),
+//            dU = sum dpre x^T, dc' = sum dpre
+//   GEMMs    dH = dY [W^h ; W^h'] (both relations of a node type in one
+//            K = 2f contraction), dW^h = dY^T H (split-K, partials summed in
+//            a fixed order)
+// then the node encoders (ReLU mask, dA = dpre^T x, dc = column sums) and
+// the folded edge encoders (U = W^e A_r, c' = W^e c_r + b):
+//   dW^e = dU A_r^T + dc' c_r^T,  db = dc',  dA_r = sum_l W^e^T dU,  dc_r = sum_l W^e^T dc'.
+// Per-entry scalars live in slots keyed by edge id, so the source-side pass
+// finds the scalars of the entries a row feeds through the transposed
+// bucket: op-device links through the opposite bucket, undirected links
+// (op-op, device-device) through the row's own bucket with the direction bit
+// (destination id > source id).
+//
+// Every reduction runs in a fixed order (per-block partials summed by one
+// thread per output), so the step is bitwise repeatable.
+#include <algorithm>
+
+#include "../../include/tag_train.h"
+#include "agg_common.hpp"
+#include "fwd_internal.hpp"
+
+namespace tag {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- GEMM
+// C_z (+)= sum_{k in split z} A(m, k) B(k, n) on MFMA 16x16x4 (fp32).
+// A(m, k) = A[m lda + k] (a_kc) or A[k lda + m]; B(k, n) = B[n ldb + k]
+// (b_kc) or B[k ldb + n].  Column ones_col of an n-contiguous B reads 1
+// (it turns the product into column sums of A).  64 x 64 block tiles of
+// four 32 x 32 wavefront tiles, k-chunks of 16 staged through LDS with the
+// next chunk's loads in flight.
+struct Gemm {
+    const float *A;
+    int64_t lda;
+    const float *B;
+    int64_t ldb;
+    int64_t M, N, K;
+    int64_t ones_col;
+    float *C;
+    int64_t ldc, c_split;
+    int64_t k_per;
+    int accumulate;
+};
+
+constexpr int GM = 64, GN = 64, GK = 16;
+
+template <bool AKC, bool BKC>
+__global__ void __launch_bounds__(256) gemm_f32(Gemm G) {
+    __shared__ float As[GK][GM + 4];
+    __shared__ float Bs[GK][GN + 4];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int64_t m0 = (int64_t)blockIdx.x * GM, n0 = (int64_t)blockIdx.y * GN;
+    const int64_t kb = (int64_t)blockIdx.z * G.k_per, ke = std::min<int64_t>(G.K, kb + G.k_per);
+    f4 acc[2][2];
+    for (int i = 0; i < 2; ++i)
+        for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+    float ra[4], rb[4];
+    auto gload = [&](int64_t k0) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (AKC) {
+                const int64_t m = m0 + (tid >> 4) + 16 * q, k = k0 + (tid & 15);
+                ra[q] = (m < G.M && k < ke) ? G.A[m * G.lda + k] : 0.f;
+            } else {
+                const int64_t m = m0 + (tid & 63), k = k0 + (tid >> 6) + 4 * q;
+                ra[q] = (m < G.M && k < ke) ? G.A[k * G.lda + m] : 0.f;
+            }
+            if (BKC) {
+                const int64_t n = n0 + (tid >> 4) + 16 * q, k = k0 + (tid & 15);
+                rb[q] = (n < G.N && k < ke) ? G.B[n * G.ldb + k] : 0.f;
+            } else {
+                const int64_t n = n0 + (tid & 63), k = k0 + (tid >> 6) + 4 * q;
+                rb[q] = (k < ke && n < G.N) ? (n == G.ones_col ? 1.f : G.B[k * G.ldb + n]) : 0.f;
+            }
+        }
+    };
+    if (kb < ke) gload(kb);
+    for (int64_t k0 = kb; k0 < ke; k0 += GK) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (AKC) As[tid & 15][(tid >> 4) + 16 * q] = ra[q];
+            else As[(tid >> 6) + 4 * q][tid & 63] = ra[q];
+            if (BKC) Bs[tid & 15][(tid >> 4) + 16 * q] = rb[q];
+            else Bs[(tid >> 6) + 4 * q][tid & 63] = rb[q];
+        }
+        __syncthreads();
+        if (k0 + GK < ke) gload(k0 + GK);
+#pragma unroll
+        for (int kk = 0; kk < GK; kk += 4) {
+            float a[2], b[2];
+            for (int i = 0; i < 2; ++i) a[i] = As[kk + (lane >> 4)][wm * 32 + i * 16 + (lane & 15)];
+            for (int j = 0; j < 2; ++j) b[j] = Bs[kk + (lane >> 4)][wn * 32 + j * 16 + (lane & 15)];
+            for (int i = 0; i < 2; ++i)
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+        __syncthreads();
+    }
+    float *C = G.C + (int64_t)blockIdx.z * G.c_split;
+    for (int i = 0; i < 2; ++i)
+        for (int j = 0; j < 2; ++j) {
+            const int64_t n = n0 + wn * 32 + j * 16 + (lane & 15);
+            if (n >= G.N) continue;
+            for (int v = 0; v < 4; ++v) {
+                const int64_t m = m0 + wm * 32 + i * 16 + 4 * (lane >> 4) + v;
+                if (m >= G.M) continue;
+                float *p = C + m * G.ldc + n;
+                *p = G.accumulate ? *p + acc[i][j][v] : acc[i][j][v];
+            }
+        }
+}
+
+// split count for a k-range of K rows over `tiles` output tiles: enough
+// blocks to fill the chip, at least 4 k-chunks per split
+int64_t split_k_per(int64_t K, int64_t tiles, int64_t *splits) {
+    int64_t s = std::max<int64_t>(1, std::min<int64_t>(2048 / std::max<int64_t>(tiles, 1), (K + 63) / 64));
+    int64_t per = ((K + s - 1) / s + GK - 1) / GK * GK;
+    per = std::max<int64_t>(per, GK);
+    *splits = std::max<int64_t>(1, (K + per - 1) / per);
+    return per;
+}
+
+void launch_gemm(Gemm G, bool a_kc, bool b_kc, int64_t splits, hipStream_t st) {
+    if (G.M <= 0 || G.N <= 0) return;
+    dim3 grid((unsigned)((G.M + GM - 1) / GM), (unsigned)((G.N + GN - 1) / GN), (unsigned)splits);
+    if (a_kc && b_kc) gemm_f32<true, true><<<grid, 256, 0, st>>>(G);
+    else if (a_kc) gemm_f32<true, false><<<grid, 256, 0, st>>>(G);
+    else if (b_kc) gemm_f32<false, true><<<grid, 256, 0, st>>>(G);
+    else gemm_f32<false, false><<<grid, 256, 0, st>>>(G);
+}
+
+// out[m ldo + n] (+)= sum_z P[z ps + m ldp + n], z in order
+__global__ void sum_splits(const float *P, int64_t ps, int64_t ldp, int32_t nz, int64_t M, int64_t N, float *out,
+                           int64_t ldo, int accumulate) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < M * N; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t m = i / N, n = i % N;
+        float s = 0.f;
+        for (int32_t z = 0; z < nz; ++z) s += P[z * ps + m * ldp + n];
+        float *o = out + m * ldo + n;
+        *o = accumulate ? *o + s : s;
+    }
+}
+
+inline unsigned grid_for(int64_t n, int per = 256) {
+    return (unsigned)std::max<int64_t>(1, std::min<int64_t>((n + per - 1) / per, 1 << 20));
+}
+
+// dW = A^T B over K rows (A: [K][M] rows of stride lda, B: [K][nb] of stride
+// ldb, optional ones column at nb), summed over splits into out
+// ([M][nb] of stride ldo) and, with a ones column, bias_out [M].
+void weight_grad(const float *A, int64_t lda, const float *B, int64_t ldb, int64_t M, int64_t nb, bool ones,
+                 int64_t K, float *P, float *out, int64_t ldo, float *bias_out, int accumulate, hipStream_t st) {
+    const int64_t N = nb + (ones ? 1 : 0);
+    const int64_t tiles = ((M + GM - 1) / GM) * ((N + GN - 1) / GN);
+    int64_t splits;
+    const int64_t per = split_k_per(K, tiles, &splits);
+    Gemm g{A, lda, B, ldb, M, N, K, ones ? nb : -1, P, N, M * N, per, 0};
+    launch_gemm(g, false, false, splits, st);
+    sum_splits<<<grid_for(M * nb), 256, 0, st>>>(P, M * N, N, (int32_t)splits, M, nb, out, ldo, accumulate);
+    if (ones) sum_splits<<<grid_for(M), 256, 0, st>>>(P + nb, M * N, N, (int32_t)splits, M, 1, bias_out, 1, accumulate);
+}
+
+// ------------------------------------------------------------- layer backward
+struct BwdLayer {
+    int32_t R;
+    int F;
+    const float *att_src, *att_dst;   // [3][F] of the layer
+    const float *U, *cp;              // [3][F][2], [3][F]
+    const float *x_oo; int64_t s_oo;
+    const float *x_dd; int64_t s_dd;
+    const uint8_t *x_od; int64_t s_od;
+    float slope;
+};
+
+// One destination bucket of the forward pass.
+struct BwdBucket {
+    const int32_t *rp, *col, *eid;
+    int64_t n_dst, n_src;             // rows per replica
+    const float *Ydst; int ydst_off;  // saved Y rows ([R*n][2F]) and the relation's half
+    const float *Ysrc; int ysrc_off;
+    const float *dO; float gamma;     // gradient rows of the destinations [R*n_dst][F]
+    int rel, xkind, twin;             // xkind 0 oo (log size), 1 od (bit), 2 dd (two values)
+    float *SA, *SD;                   // [R][n_slots][K]
+    int64_t n_slots;
+    int32_t chunks;                   // kChunkA-entry chunks per row (max degree)
+    float *Z; int zsel;               // [R*n_dst][2][K] per-destination dz sums
+};
+
+constexpr int kChunkA = 64;     // entries per score item
+constexpr int kChunkB = 256;    // entries per message item
+constexpr int kPersist = 1024;  // blocks of the passes that sum parameter gradients
+
+__device__ __forceinline__ void edge_x(const BwdLayer &P, int xkind, int32_t rep, int32_t id, float &x0, float &x1) {
+    if (xkind == 0) {
+        x0 = P.x_oo[(int64_t)rep * P.s_oo + id];
+        x1 = 0.f;
+    } else if (xkind == 1) {
+        x0 = P.x_od[(int64_t)rep * P.s_od + id] ? 1.f : 0.f;
+        x1 = 0.f;
+    } else {
+        const float *p = P.x_dd + (int64_t)rep * P.s_dd + 2 * (int64_t)id;
+        x0 = p[0];
+        x1 = p[1];
+    }
+}
+
+// sum over the LPH lanes of a head (DPP inside 16-lane rows, then shuffles)
+template <int LPH>
+__device__ __forceinline__ float hsum(float v) {
+    v = row_sum<(LPH < 16 ? LPH : 16)>(v);
+    if constexpr (LPH >= 32) v += __shfl_xor(v, 16, 64);
+    if constexpr (LPH >= 64) v += __shfl_xor(v, 32, 64);
+    return v;
+}
+
+__device__ __forceinline__ int64_t slot_of(int twin, int32_t id, int32_t dst, int32_t src) {
+    return twin ? 2 * (int64_t)id + (dst > src ? 1 : 0) : (int64_t)id;
+}
+
+// scores: one wavefront per (replica, destination row, chunk of kChunkA
+// entries); lanes own F/64 channels; writes s and dalpha per (entry, head)
+template <int F, int K>
+__global__ void __launch_bounds__(256) bwd_scores(BwdLayer P, BwdBucket B) {
+    constexpr int CPL = F / 64, LPH = 64 / K;
+    const int lane = threadIdx.x & 63;
+    const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t rows = (int64_t)P.R * B.n_dst;
+    if (w >= rows * B.chunks) return;
+    const int64_t ru = w / B.chunks;
+    const int32_t ch = (int32_t)(w % B.chunks);
+    const int32_t rep = (int32_t)(ru / B.n_dst), u = (int32_t)(ru % B.n_dst);
+    const int32_t beg = B.rp[u] + ch * kChunkA, end = min(B.rp[u + 1], beg + kChunkA);
+    if (beg >= end) return;
+    const int c0 = lane * CPL;
+    const int r = B.rel;
+    float a[CPL], u0[CPL], u1[CPL], yd[CPL], dO[CPL];
+    load_ch<CPL, false>(B.Ydst, ru * 2 * F + B.ydst_off + c0, yd);
+    load_ch<CPL, false>(B.dO, ru * F + c0, dO);
+    float q = 0.f;
+    for (int c = 0; c < CPL; ++c) {
+        a[c] = P.att_src[r * F + c0 + c];
+        u0[c] = P.U[((int64_t)r * F + c0 + c) * 2 + 0];
+        u1[c] = P.U[((int64_t)r * F + c0 + c) * 2 + 1];
+        q = fmaf(P.att_dst[r * F + c0 + c], yd[c] - P.cp[r * F + c0 + c], q);
+        dO[c] *= B.gamma;
+    }
+    q = hsum<LPH>(q);
+    const int64_t sbase = (int64_t)rep * B.n_slots;
+    constexpr int EB = 4;
+    for (int32_t e0 = beg; e0 < end; e0 += EB) {
+        float ys[EB][CPL], x0[EB], x1[EB];
+        int32_t vv[EB], id[EB];
+#pragma unroll
+        for (int i = 0; i < EB; ++i) {
+            const int32_t e = min(e0 + i, end - 1);
+            vv[i] = B.col[e];
+            id[i] = B.eid[e];
+        }
+#pragma unroll
+        for (int i = 0; i < EB; ++i) {
+            load_ch<CPL, false>(B.Ysrc, ((int64_t)rep * B.n_src + vv[i]) * 2 * F + B.ysrc_off + c0, ys[i]);
+            edge_x(P, B.xkind, rep, id[i], x0[i], x1[i]);
+        }
+#pragma unroll
+        for (int i = 0; i < EB; ++i) {
+            float pa = 0.f, pd = 0.f;
+            for (int c = 0; c < CPL; ++c) {
+                const float m = fmaxf(ys[i][c] + fmaf(u0[c], x0[i], u1[c] * x1[i]), 0.f);
+                pa = fmaf(a[c], m, pa);
+                pd = fmaf(dO[c], m, pd);
+            }
+            pa = hsum<LPH>(pa);
+            pd = hsum<LPH>(pd);
+            const float s = leaky(pa + q, P.slope);
+            if (e0 + i < end && (lane & (LPH - 1)) == 0) {
+                const int64_t idx = (sbase + slot_of(B.twin, id[i], u, vv[i])) * K + lane / LPH;
+                B.SA[idx] = s;
+                B.SD[idx] = pd;
+            }
+        }
+    }
+}
+
+// softmax backward: one wavefront per (replica, destination row), lanes
+// over (entry, head) pairs; turns (s, dalpha) into (alpha, dz) in place,
+// writes Z_u and sums d adst = Z_u (Y_u - c') per block
+template <int F, int K>
+__global__ void __launch_bounds__(256) bwd_softmax(BwdLayer P, BwdBucket B, float *part_ad) {
+    constexpr int CPL = F / 64, EPS = 64 / K, D = F / K;
+    __shared__ float red[4][F];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int ei = lane / K, k = lane % K;
+    const int c0 = lane * CPL;
+    const int r = B.rel;
+    float acc[CPL], ad[CPL], cp[CPL];
+    for (int c = 0; c < CPL; ++c) {
+        acc[c] = 0.f;
+        ad[c] = P.att_dst[r * F + c0 + c];
+        cp[c] = P.cp[r * F + c0 + c];
+    }
+    const int64_t rows = (int64_t)P.R * B.n_dst;
+    const int64_t nw = (int64_t)gridDim.x * 4;
+    for (int64_t ru = (int64_t)blockIdx.x * 4 + wv; ru < rows; ru += nw) {
+        const int32_t rep = (int32_t)(ru / B.n_dst), u = (int32_t)(ru % B.n_dst);
+        const int32_t beg = B.rp[u], end = B.rp[u + 1];
+        const int64_t sbase = (int64_t)rep * B.n_slots;
+        float mx = -INFINITY, den = 0.f, num = 0.f;
+        for (int32_t e0 = beg; e0 < end; e0 += EPS) {
+            const int32_t e = e0 + ei;
+            if (e < end) {
+                const int64_t idx = (sbase + slot_of(B.twin, B.eid[e], u, B.col[e])) * K + k;
+                const float s = B.SA[idx], da = B.SD[idx];
+                if (s > mx) {
+                    const float sc = __expf(mx - s);
+                    den = fmaf(den, sc, 1.f);
+                    num = fmaf(num, sc, da);
+                    mx = s;
+                } else {
+                    const float p = __expf(s - mx);
+                    den += p;
+                    num = fmaf(p, da, num);
+                }
+            }
+        }
+        for (int o = K; o < 64; o <<= 1) {
+            const float m2 = __shfl_xor(mx, o, 64), d2 = __shfl_xor(den, o, 64), n2 = __shfl_xor(num, o, 64);
+            const float M = fmaxf(mx, m2);
+            if (M == -INFINITY) continue;
+            const float s1 = mx == -INFINITY ? 0.f : __expf(mx - M), s2 = m2 == -INFINITY ? 0.f : __expf(m2 - M);
+            den = den * s1 + d2 * s2;
+            num = num * s1 + n2 * s2;
+            mx = M;
+        }
+        const float inv = den > 0.f ? 1.f / den : 0.f;
+        const float cc = num * inv;
+        float zs = 0.f;
+        for (int32_t e0 = beg; e0 < end; e0 += EPS) {
+            const int32_t e = e0 + ei;
+            if (e < end) {
+                const int64_t idx = (sbase + slot_of(B.twin, B.eid[e], u, B.col[e])) * K + k;
+                const float s = B.SA[idx], da = B.SD[idx];
+                const float al = __expf(s - mx) * inv;
+                const float dz = al * (da - cc) * (s > 0.f ? 1.f : P.slope);
+                B.SA[idx] = al;
+                B.SD[idx] = dz;
+                zs += dz;
+            }
+        }
+        for (int o = K; o < 64; o <<= 1) zs += __shfl_xor(zs, o, 64);
+        if (ei == 0) B.Z[(ru * 2 + B.zsel) * K + k] = zs;
+        const float zh = __shfl(zs, c0 / D, 64);   // lane h < K holds head h
+        if (end > beg) {
+            float yd[CPL];
+            load_ch<CPL, false>(B.Ydst, ru * 2 * F + B.ydst_off + c0, yd);
+            for (int c = 0; c < CPL; ++c) acc[c] = fmaf(zh, yd[c] - cp[c], acc[c]);
+        }
+    }
+    for (int c = 0; c < CPL; ++c) red[wv][c0 + c] = acc[c];
+    __syncthreads();
+    for (int c = threadIdx.x; c < F; c += 256)
+        part_ad[(int64_t)blockIdx.x * F + c] = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
+}
+
+// Rows of one node type as sources: the entries they feed, listed by the
+// bucket in which the row is the destination of the same relation.
+struct BwdSrc {
+    const int32_t *rp, *col, *eid;
+    int64_t n_self, n_nbr;
+    const float *Yself; int yoff;
+    const float *dOn; float gamma;    // gradient rows of the neighbours (forward destinations)
+    const float *SA, *SD;             // (alpha, dz) of the forward bucket nbr <- self
+    int64_t n_slots;
+    int twin, rel, xkind;
+    const float *Z; int zsel;         // Z of the row as a destination of the relation
+    float *dY; int dyoff;             // [R*n_self][2F]
+    float *PB;                        // [R*n_self][chunks][F] chunk partials (chunks > 1)
+    int32_t chunks;
+};
+
+// messages: persistent wavefronts over (replica, source row, chunk of
+// kChunkB entries); dY rows (or chunk partials) and per-block sums of
+// d a, dU (two columns) and dc'
+template <int F, int K>
+__global__ void __launch_bounds__(256) bwd_messages(BwdLayer P, BwdSrc S, float *part) {
+    constexpr int CPL = F / 64, D = F / K;
+    __shared__ float red[4][F];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int c0 = lane * CPL, h = c0 / D;
+    const int r = S.rel;
+    float a[CPL], ad[CPL], u0[CPL], u1[CPL];
+    float ga[CPL], gu0[CPL], gu1[CPL], gcp[CPL];
+    for (int c = 0; c < CPL; ++c) {
+        a[c] = P.att_src[r * F + c0 + c];
+        ad[c] = P.att_dst[r * F + c0 + c];
+        u0[c] = P.U[((int64_t)r * F + c0 + c) * 2 + 0];
+        u1[c] = P.U[((int64_t)r * F + c0 + c) * 2 + 1];
+        ga[c] = gu0[c] = gu1[c] = gcp[c] = 0.f;
+    }
+    const int64_t items = (int64_t)P.R * S.n_self * S.chunks;
+    const int64_t nw = (int64_t)gridDim.x * 4;
+    for (int64_t it = (int64_t)blockIdx.x * 4 + wv; it < items; it += nw) {
+        const int64_t rv = it / S.chunks;
+        const int32_t ch = (int32_t)(it % S.chunks);
+        const int32_t rep = (int32_t)(rv / S.n_self), v = (int32_t)(rv % S.n_self);
+        const int32_t beg = S.rp[v] + ch * kChunkB, end = min(S.rp[v + 1], beg + kChunkB);
+        if (ch > 0 && beg >= end) continue;
+        float ys[CPL], dys[CPL];
+        load_ch<CPL, false>(S.Yself, rv * 2 * F + S.yoff + c0, ys);
+        for (int c = 0; c < CPL; ++c) dys[c] = 0.f;
+        const int64_t sbase = (int64_t)rep * S.n_slots;
+        constexpr int EB = 4;
+        for (int32_t e0 = beg; e0 < end; e0 += EB) {
+            float dou[EB][CPL], x0[EB], x1[EB], al[EB], dz[EB];
+            int32_t uu[EB], id[EB];
+#pragma unroll
+            for (int i = 0; i < EB; ++i) {
+                const int32_t e = min(e0 + i, end - 1);
+                uu[i] = S.col[e];
+                id[i] = S.eid[e];
+            }
+#pragma unroll
+            for (int i = 0; i < EB; ++i) {
+                load_ch<CPL, false>(S.dOn, ((int64_t)rep * S.n_nbr + uu[i]) * F + c0, dou[i]);
+                edge_x(P, S.xkind, rep, id[i], x0[i], x1[i]);
+                const int64_t idx = (sbase + slot_of(S.twin, id[i], uu[i], v)) * K + h;
+                al[i] = S.SA[idx];
+                dz[i] = S.SD[idx];
+            }
+#pragma unroll
+            for (int i = 0; i < EB; ++i) {
+                if (e0 + i >= end) break;
+                for (int c = 0; c < CPL; ++c) {
+                    const float pre = ys[c] + fmaf(u0[c], x0[i], u1[c] * x1[i]);
+                    const float m = fmaxf(pre, 0.f);
+                    const float dm = fmaf(al[i] * S.gamma, dou[i][c], dz[i] * a[c]);
+                    const float dp = pre > 0.f ? dm : 0.f;
+                    dys[c] += dp;
+                    ga[c] = fmaf(dz[i], m, ga[c]);
+                    gu0[c] = fmaf(dp, x0[i], gu0[c]);
+                    gu1[c] = fmaf(dp, x1[i], gu1[c]);
+                    gcp[c] += dp;
+                }
+            }
+        }
+        if (S.chunks == 1) {
+            const float zv = S.Z[(rv * 2 + S.zsel) * K + h];
+            float *o = S.dY + rv * 2 * F + S.dyoff + c0;
+            for (int c = 0; c < CPL; ++c) o[c] = fmaf(zv, ad[c], dys[c]);
+        } else {
+            float *o = S.PB + (rv * S.chunks + ch) * F + c0;
+            for (int c = 0; c < CPL; ++c) o[c] = dys[c];
+        }
+    }
+    float *q[4] = {ga, gu0, gu1, gcp};
+    for (int t = 0; t < 4; ++t) {
+        for (int c = 0; c < CPL; ++c) red[wv][c0 + c] = q[t][c];
+        __syncthreads();
+        for (int c = threadIdx.x; c < F; c += 256)
+            part[((int64_t)t * gridDim.x + blockIdx.x) * F + c] = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
+        __syncthreads();
+    }
+}
+
+// dY rows of sources with several chunks: the row's chunk partials summed
+// in order, plus Z adst (heads of D = F / K channels)
+__global__ void bwd_combine(BwdLayer P, BwdSrc S, int K) {
+    const int F = P.F, D = F / K;
+    const int r = S.rel;
+    const int64_t total = (int64_t)P.R * S.n_self * F;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t rv = i / F;
+        const int c = (int)(i % F);
+        const int32_t v = (int32_t)(rv % S.n_self);
+        const int32_t deg = S.rp[v + 1] - S.rp[v];
+        const int32_t nch = max(1, (deg + kChunkB - 1) / kChunkB);
+        float s = 0.f;
+        for (int32_t ch = 0; ch < nch; ++ch) s += S.PB[(rv * S.chunks + ch) * F + c];
+        S.dY[rv * 2 * F + S.dyoff + c] = fmaf(S.Z[(rv * 2 + S.zsel) * K + c / D], P.att_dst[r * F + c], s);
+    }
+}
+
+// Parameter sums of one layer from the per-block partials:
+//   att_dst grad (scores' softmax passes), att_src grad, dU, dc' (message passes)
+struct ParamReduce {
+    const float *pa[4];     // bwd_softmax partials of buckets 0..3: [nb][F]
+    const float *pm[4];     // bwd_messages partials of the four source passes: [4][nb][F]
+    int32_t nb_a[4], nb_m[4];
+    int F;
+    float *g_att_src, *g_att_dst;   // [3][F] of the layer
+    float *dU, *dcp;                // [3][F][2], [3][F] of the layer
+};
+
+__global__ void bwd_params(ParamReduce R) {
+    // relations of the buckets (op<-op, op<-dev, dev<-op, dev<-dev) and of
+    // the source passes (op oo, op od, dev od, dev dd)
+    const int rel_of[4] = {0, 1, 1, 2};
+    const int F = R.F;
+    const int r = blockIdx.x / 5, qty = blockIdx.x % 5;
+    for (int c = threadIdx.x; c < F; c += blockDim.x) {
+        float s = 0.f;
+        for (int p = 0; p < 4; ++p) {
+            if (rel_of[p] != r) continue;
+            if (qty == 0) {
+                for (int32_t b = 0; b < R.nb_a[p]; ++b) s += R.pa[p][(int64_t)b * F + c];
+            } else {
+                const float *base = R.pm[p] + (int64_t)(qty - 1) * R.nb_m[p] * F;
+                for (int32_t b = 0; b < R.nb_m[p]; ++b) s += base[(int64_t)b * F + c];
+            }
+        }
+        if (qty == 0) R.g_att_dst[r * F + c] = s;
+        else if (qty == 1) R.g_att_src[r * F + c] = s;
+        else if (qty == 2) R.dU[((int64_t)r * F + c) * 2 + 0] = s;
+        else if (qty == 3) R.dU[((int64_t)r * F + c) * 2 + 1] = s;
+        else R.dcp[r * F + c] = s;
+    }
+}
+
+// ReLU mask of the encoders: g = H0 > 0 ? g : 0
+__global__ void relu_mask(float *g, const float *h, int64_t n) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        if (!(h[i] > 0.f)) g[i] = 0.f;
+}
+
+// Folded edge encoders, per layer l and relation r (d_r = 1, 1, 2):
+//   grad layer_b = dc';  grad W^e[o][k] = sum_t dU[o][t] A_r[k][t] + dc'[o] c_r[k]
+struct FoldBwd {
+    const float *layer_w;
+    const float *A[3], *c[3];
+    const float *dU, *dcp;   // [L][3][F][2], [L][3][F]
+    float *g_layer_w, *g_layer_b;
+    float *g_A[3], *g_c[3];
+    int F, L;
+};
+
+__global__ void fold_bwd_we(FoldBwd a) {
+    const int F = a.F;
+    const int64_t total = (int64_t)a.L * 3 * F * F;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t lr = i / ((int64_t)F * F);
+        const int o = (int)((i / F) % F), k = (int)(i % F);
+        const int r = (int)(lr % 3), d = r == 2 ? 2 : 1;
+        const float *du = a.dU + (lr * F + o) * 2;
+        float s = a.dcp[lr * F + o] * a.c[r][k];
+        for (int t = 0; t < d; ++t) s = fmaf(du[t], a.A[r][(int64_t)k * d + t], s);
+        a.g_layer_w[(lr * F + o) * 2 * F + F + k] = s;
+        if (k == 0) a.g_layer_b[lr * F + o] = a.dcp[lr * F + o];
+    }
+}
+
+// grad A_r[k][t] = sum_l sum_o W^e_{l,r}[o][k] dU_{l,r}[o][t];  grad c_r[k] likewise with dc'
+__global__ void fold_bwd_enc(FoldBwd a) {
+    const int F = a.F;
+    const int r = blockIdx.x, d = r == 2 ? 2 : 1;
+    for (int k = threadIdx.x; k < F; k += blockDim.x) {
+        float s0 = 0.f, s1 = 0.f, sc = 0.f;
+        for (int l = 0; l < a.L; ++l) {
+            const int64_t lr = (int64_t)l * 3 + r;
+            for (int o = 0; o < F; ++o) {
+                const float we = a.layer_w[(lr * F + o) * 2 * F + F + k];
+                s0 = fmaf(we, a.dU[(lr * F + o) * 2 + 0], s0);
+                s1 = fmaf(we, a.dU[(lr * F + o) * 2 + 1], s1);
+                sc = fmaf(we, a.dcp[lr * F + o], sc);
+            }
+        }
+        a.g_A[r][(int64_t)k * d + 0] = s0;
+        if (d == 2) a.g_A[r][(int64_t)k * d + 1] = s1;
+        a.g_c[r][k] = sc;
+    }
+}
+
+// ------------------------------------------------------------------ decoder
+struct DecTrain {
+    int32_t R, G, S, Q, F, H, max_dev;
+    int64_t n_op, n_dev;
+    const int32_t *op_off, *dev_off;
+    const float *E_op, *E_dev;
+    const uint64_t *mask;
+    const uint8_t *option;
+    const float *W1, *b1, *w2, *b2;
+    const int32_t *q_rep, *q_graph, *q_op;
+    const float *target;
+    const float *t;        // [R*n_dev][H] = E_dev W1_dev^T
+    const float *v;        // [Q][H] = W1_op E_op[query row]
+    int32_t *qrow;         // [Q] E_op row of each query (-1: invalid)
+    float inv_q;
+    float *loss_q;         // [Q]
+    float *db1q, *dw2q;    // [Q][H]
+    float *doptq;          // [Q][4][H]
+    float *db2q;           // [Q]
+    float *dTq;            // [Q][max_dev][H]
+    float *g_op, *g_dev;   // dE_op [R*n_op][F], dE_dev [R*n_dev][F]
+    float *g_w1, *g_b1, *g_w2, *g_b2;
+};
+
+__device__ __forceinline__ bool dec_query(const DecTrain &A, int32_t q, int32_t *r, int32_t *g, int32_t *op) {
+    *r = A.q_rep[q]; *g = A.q_graph[q]; *op = A.q_op[q];
+    if (*r < 0 || *r >= A.R || *g < 0 || *g >= A.G) return false;
+    return *op >= 0 && *op < A.op_off[*g + 1] - A.op_off[*g];
+}
+
+__global__ void dec_rows(DecTrain A) {
+    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < A.Q; q += (int64_t)gridDim.x * blockDim.x) {
+        int32_t r, g, op;
+        A.qrow[q] = dec_query(A, (int32_t)q, &r, &g, &op) ? (int32_t)((int64_t)r * A.n_op + A.op_off[g] + op) : -1;
+    }
+}
+
+constexpr int kDecH = 32;     // hidden units per score chunk
+constexpr int kDecHB = 64;    // hidden units per gradient chunk
+
+// One block of 256 per query.  Scores (thread per slice), softmax, loss
+// and dscore; then per chunk of 64 hidden units, thread (hh, jg) walks the
+// slices in order: pre = b1 + W1_opt[opt] + v + sum_{j in mask} t_j,
+// dpre = dscore w2 [pre > 0]; it sums dpre into dT[j] for its devices
+// j = jg mod 4, and threads jg = 0 also sum db1, dw2, dW1_opt.
+__global__ void __launch_bounds__(256) dec_train_query(DecTrain A) {
+    extern __shared__ float sh[];
+    __shared__ float red[256];
+    __shared__ float red2[256];
+    float *sc = sh;                       // [S] scores, then dscore
+    float *work = sh + A.S;
+    const int tid = threadIdx.x;
+    const int32_t q = blockIdx.x;
+    const int din = 2 * A.F + 4;
+    int32_t r, g, op;
+    const bool ok = dec_query(A, q, &r, &g, &op);
+    const int H = A.H, M = A.max_dev;
+    if (!ok) {
+        for (int h = tid; h < H; h += 256) {
+            A.db1q[(int64_t)q * H + h] = 0.f;
+            A.dw2q[(int64_t)q * H + h] = 0.f;
+            for (int o = 0; o < 4; ++o) A.doptq[((int64_t)q * 4 + o) * H + h] = 0.f;
+        }
+        for (int i = tid; i < M * H; i += 256) A.dTq[(int64_t)q * M * H + i] = 0.f;
+        if (tid == 0) { A.loss_q[q] = 0.f; A.db2q[q] = 0.f; }
+        return;
+    }
+    const int32_t d0 = A.dev_off[g], nd = A.dev_off[g + 1] - d0;
+    const uint64_t keep = nd >= 64 ? ~0ull : ((1ull << nd) - 1ull);
+    const float *trow = A.t + ((int64_t)r * A.n_dev + d0) * H;
+    const float *vq = A.v + (int64_t)q * H;
+    // scores
+    {
+        float *tl = work;                       // [64][kDecH + 1]
+        float *po = work + 64 * (kDecH + 1);    // [4][kDecH]: W1_opt + b1 + v
+        float *w2c = po + 4 * kDecH;            // [kDecH]
+        for (int32_t a = tid; a < A.S; a += 256) sc[a] = A.b2[0];
+        for (int h0 = 0; h0 < H; h0 += kDecH) {
+            __syncthreads();
+            for (int i = tid; i < nd * kDecH; i += 256) {
+                const int j = i / kDecH, hh = i % kDecH;
+                tl[j * (kDecH + 1) + hh] = h0 + hh < H ? trow[(int64_t)j * H + h0 + hh] : 0.f;
+            }
+            for (int i = tid; i < 4 * kDecH; i += 256) {
+                const int o = i / kDecH, hh = i % kDecH, h = h0 + hh;
+                po[i] = h < H ? A.W1[(int64_t)h * din + 2 * A.F + o] + A.b1[h] + vq[h] : 0.f;
+            }
+            for (int i = tid; i < kDecH; i += 256) w2c[i] = h0 + i < H ? A.w2[h0 + i] : 0.f;
+            __syncthreads();
+            for (int32_t a = tid; a < A.S; a += 256) {
+                uint64_t m = A.mask[a] & keep;
+                const int opt = min((int)A.option[a], 3);
+                float acc[kDecH];
+#pragma unroll
+                for (int hh = 0; hh < kDecH; ++hh) acc[hh] = po[opt * kDecH + hh];
+                while (m) {
+                    const int j = __builtin_ctzll(m);
+                    m &= m - 1;
+#pragma unroll
+                    for (int hh = 0; hh < kDecH; ++hh) acc[hh] += tl[j * (kDecH + 1) + hh];
+                }
+                float s = 0.f;
+#pragma unroll
+                for (int hh = 0; hh < kDecH; ++hh) s = fmaf(w2c[hh], fmaxf(acc[hh], 0.f), s);
+                sc[a] += s;
+            }
+        }
+    }
+    __syncthreads();
+    // softmax, loss, dscore
+    float mx = -INFINITY;
+    for (int32_t a = tid; a < A.S; a += 256) mx = fmaxf(mx, sc[a]);
+    red[tid] = mx;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if (tid < o) red[tid] = fmaxf(red[tid], red[tid + o]);
+        __syncthreads();
+    }
+    const float M0 = red[0];
+    __syncthreads();
+    float z = 0.f, tt = 0.f, ts = 0.f;
+    const float *tg = A.target + (int64_t)q * A.S;
+    for (int32_t a = tid; a < A.S; a += 256) {
+        z += __expf(sc[a] - M0);
+        tt += tg[a];
+        ts = fmaf(tg[a], sc[a] - M0, ts);
+    }
+    red[tid] = z;
+    red2[tid] = tt;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if (tid < o) { red[tid] += red[tid + o]; red2[tid] += red2[tid + o]; }
+        __syncthreads();
+    }
+    const float Z = red[0], T = red2[0];
+    __syncthreads();
+    red[tid] = ts;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if (tid < o) red[tid] += red[tid + o];
+        __syncthreads();
+    }
+    const float logZ = __logf(Z);
+    if (tid == 0) A.loss_q[q] = -A.inv_q * (red[0] - T * logZ);
+    __syncthreads();
+    float db2 = 0.f;
+    for (int32_t a = tid; a < A.S; a += 256) {
+        const float p = __expf(sc[a] - M0) / Z;
+        const float ds = A.inv_q * (p * T - tg[a]);
+        sc[a] = ds;
+        db2 += ds;
+    }
+    red[tid] = db2;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if (tid < o) red[tid] += red[tid + o];
+        __syncthreads();
+    }
+    if (tid == 0) A.db2q[q] = red[0];
+    // gradients per chunk of hidden units
+    float *tl = work;                     // [64][kDecHB]
+    float *dT = work + 64 * kDecHB;       // [64][kDecHB]
+    const int hh = tid & (kDecHB - 1), jg = tid / kDecHB;
+    for (int h0 = 0; h0 < H; h0 += kDecHB) {
+        __syncthreads();
+        for (int i = tid; i < nd * kDecHB; i += 256) {
+            const int j = i / kDecHB, c = i % kDecHB;
+            tl[i] = h0 + c < H ? trow[(int64_t)j * H + h0 + c] : 0.f;
+            dT[i] = 0.f;
+        }
+        __syncthreads();
+        const int h = h0 + hh;
+        const bool live = h < H;
+        float base[4], w2h = 0.f;
+        for (int o = 0; o < 4; ++o) base[o] = live ? A.W1[(int64_t)h * din + 2 * A.F + o] + A.b1[h] + vq[h] : 0.f;
+        if (live) w2h = A.w2[h];
+        float gb1 = 0.f, gw2 = 0.f, gopt[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int32_t a = 0; a < A.S; ++a) {
+            const uint64_t mall = A.mask[a] & keep;
+            const int opt = min((int)A.option[a], 3);
+            float pre = base[opt];
+            uint64_t m = mall;
+            while (m) {
+                const int j = __builtin_ctzll(m);
+                m &= m - 1;
+                pre += tl[j * kDecHB + hh];
+            }
+            const float ds = sc[a];
+            const float dp = pre > 0.f ? ds * w2h : 0.f;
+            if (jg == 0) {
+                gb1 += dp;
+                gw2 = fmaf(ds, fmaxf(pre, 0.f), gw2);
+                for (int o = 0; o < 4; ++o) gopt[o] += o == opt ? dp : 0.f;
+            }
+            // this thread's devices: j = jg (mod 4)
+            m = mall & (0x1111111111111111ull << jg);
+            while (m) {
+                const int j = __builtin_ctzll(m);
+                m &= m - 1;
+                dT[j * kDecHB + hh] += dp;
+            }
+        }
+        if (jg == 0 && live) {
+            A.db1q[(int64_t)q * H + h] = gb1;
+            A.dw2q[(int64_t)q * H + h] = gw2;
+            for (int o = 0; o < 4; ++o) A.doptq[((int64_t)q * 4 + o) * H + h] = gopt[o];
+        }
+        __syncthreads();
+        for (int i = tid; i < M * kDecHB; i += 256) {
+            const int j = i / kDecHB, c = i % kDecHB;
+            if (h0 + c < H) A.dTq[((int64_t)q * M + j) * H + h0 + c] = j < nd ? dT[i] : 0.f;
+        }
+    }
+}
+
+// decoder parameter gradients, one thread per (h, column of W1):
+//   W1_dev: sum_q sum_j dT_q[j] E_dev[row(q, j)];  W1_op: sum_q db1_q E_op[row(q)];
+//   W1_opt: sum_q dopt_q;  b1, w2, b2: sums over queries
+__global__ void dec_train_params(DecTrain A) {
+    const int din = 2 * A.F + 4, H = A.H, F = A.F;
+    const int64_t total = (int64_t)H * din;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const int h = (int)(i / din), col = (int)(i % din);
+        float s = 0.f;
+        if (col < F) {
+            for (int32_t q = 0; q < A.Q; ++q) {
+                if (A.qrow[q] < 0) continue;
+                const int32_t r = A.q_rep[q], g = A.q_graph[q];
+                const int32_t d0 = A.dev_off[g], nd = A.dev_off[g + 1] - d0;
+                for (int j = 0; j < nd; ++j)
+                    s = fmaf(A.dTq[((int64_t)q * A.max_dev + j) * H + h],
+                             A.E_dev[((int64_t)r * A.n_dev + d0 + j) * F + col], s);
+            }
+        } else if (col < 2 * F) {
+            for (int32_t q = 0; q < A.Q; ++q) {
+                if (A.qrow[q] < 0) continue;
+                s = fmaf(A.db1q[(int64_t)q * H + h], A.E_op[(int64_t)A.qrow[q] * F + col - F], s);
+            }
+        } else {
+            for (int32_t q = 0; q < A.Q; ++q) s += A.doptq[((int64_t)q * 4 + col - 2 * F) * H + h];
+        }
+        A.g_w1[i] = s;
+        if (col == 0) {
+            float b1 = 0.f, w2 = 0.f;
+            for (int32_t q = 0; q < A.Q; ++q) {
+                b1 += A.db1q[(int64_t)q * H + h];
+                w2 += A.dw2q[(int64_t)q * H + h];
+            }
+            A.g_b1[h] = b1;
+            A.g_w2[h] = w2;
+            if (h == 0) {
+                float b2 = 0.f;
+                for (int32_t q = 0; q < A.Q; ++q) b2 += A.db2q[q];
+                A.g_b2[0] = b2;
+            }
+        }
+    }
+}
+
+// dE_dev rows: sum over the queries of the row's candidate graph of W1_dev^T dT_q[j]
+__global__ void dec_train_grad_dev(DecTrain A) {
+    const int din = 2 * A.F + 4, H = A.H, F = A.F;
+    const int64_t total = (int64_t)A.R * A.n_dev * F;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = i / F;
+        const int c = (int)(i % F);
+        const int32_t r = (int32_t)(row / A.n_dev), d = (int32_t)(row % A.n_dev);
+        int32_t g = 0;
+        while (g + 1 < A.G && A.dev_off[g + 1] <= d) ++g;
+        const int j = d - A.dev_off[g];
+        float s = 0.f;
+        for (int32_t q = 0; q < A.Q; ++q) {
+            if (A.qrow[q] < 0 || A.q_rep[q] != r || A.q_graph[q] != g) continue;
+            const float *dt = A.dTq + ((int64_t)q * A.max_dev + j) * H;
+            for (int h = 0; h < H; ++h) s = fmaf(dt[h], A.W1[(int64_t)h * din + c], s);
+        }
+        A.g_dev[i] = s;
+    }
+}
+
+__global__ void fill_zero(float *p, int64_t n) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) p[i] = 0.f;
+}
+
+// dE_op rows of the queries: the first query of each row sums, in query
+// order, W1_op^T db1 of every query reading that row
+__global__ void dec_train_grad_op(DecTrain A) {
+    const int32_t q = blockIdx.x;
+    const int32_t row = A.qrow[q];
+    if (row < 0) return;
+    for (int32_t p = 0; p < q; ++p)
+        if (A.qrow[p] == row) return;
+    const int din = 2 * A.F + 4, H = A.H, F = A.F;
+    for (int c = threadIdx.x; c < F; c += blockDim.x) {
+        float s = 0.f;
+        for (int32_t p = q; p < A.Q; ++p) {
+            if (A.qrow[p] != row) continue;
+            for (int h = 0; h < H; ++h) s = fmaf(A.db1q[(int64_t)p * H + h], A.W1[(int64_t)h * din + F + c], s);
+        }
+        A.g_op[(int64_t)row * F + c] = s;
+    }
+}
+
+__global__ void dec_train_loss(const float *loss_q, int32_t Q, float *loss) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        float s = 0.f;
+        for (int32_t q = 0; q < Q; ++q) s += loss_q[q];
+        loss[0] = s;
+    }
+}
+
+// ------------------------------------------------------------------ update
+struct SgdList {
+    float *w[18];
+    const float *g[18];
+    int64_t n[18];
+    int count;
+    float lr;
+};
+
+__global__ void sgd_update(SgdList L) {
+    const int a = blockIdx.y;
+    if (a >= L.count) return;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < L.n[a]; i += (int64_t)gridDim.x * blockDim.x)
+        L.w[a][i] = fmaf(-L.lr, L.g[a][i], L.w[a][i]);
+}
+
+// ------------------------------------------------------------------ layout
+struct TrainLayout {
+    void *fwd;
+    size_t fwd_bytes;
+    float *H_op[16], *H_dev[16], *Y_op[16], *Y_dev[16];
+    float *E_op, *E_dev, *G_op, *G_dev, *dY_op, *dY_dev;
+    float *SA[4], *SD[4];
+    float *Zop, *Zdev;
+    float *PB;
+    float *part_a[4], *part_m[4];
+    int32_t nb_a[4], nb_m[4];
+    float *dU, *dcp;
+    float *P0, *P1;
+    // decoder
+    float *t, *v, *loss_q, *db1q, *dw2q, *doptq, *db2q, *dTq;
+    int32_t *qrow;
+};
+
+int32_t chunks_of(int32_t max_degree, int per) { return std::max<int32_t>(1, (max_degree + per - 1) / per); }
+
+int64_t n_slots(const tag_graph *g, int b) {
+    return b == 0 ? 2 * g->e_oo : (b == 3 ? 2 * g->e_dd : g->e_od);
+}
+
+int32_t persist_blocks(int64_t items) {
+    return (int32_t)std::max<int64_t>(1, std::min<int64_t>(kPersist, (items + 3) / 4));
+}
+
+// size of the split-K partials of every weight gradient
+int64_t split_floats(const tag_graph *g, const tag_model_dims *d, int32_t R) {
+    const int64_t F = d->f;
+    auto one = [&](int64_t M, int64_t N, int64_t K) {
+        int64_t s;
+        split_k_per(K, ((M + GM - 1) / GM) * ((N + GN - 1) / GN), &s);
+        return s * M * N;
+    };
+    int64_t m = one(2 * F, F, (int64_t)R * g->n_op);
+    m = std::max(m, one(2 * F, F, (int64_t)R * g->n_dev));
+    m = std::max(m, one(F, d->f_op + 1, (int64_t)R * g->n_op));
+    m = std::max(m, one(F, d->f_dev + 1, (int64_t)R * g->n_dev));
+    return m;
+}
+
+size_t carve_train(const tag_graph *g, const tag_model_dims *d, int32_t R, int32_t S, int32_t Q, void *base,
+                   TrainLayout *L) {
+    FwdLayout fl;
+    const size_t fb = carve_fwd(g, d, R, nullptr, &fl);
+    Carver c(base);
+    L->fwd = c.take<char>(fb);
+    L->fwd_bytes = fb;
+    const int64_t F = d->f, K = d->heads, ro = (int64_t)R * g->n_op, rd = (int64_t)R * g->n_dev;
+    for (int l = 0; l < 16; ++l) L->H_op[l] = L->H_dev[l] = L->Y_op[l] = L->Y_dev[l] = nullptr;
+    for (int l = 0; l < d->layers; ++l) {
+        L->H_op[l] = c.take<float>(ro * F);
+        L->H_dev[l] = c.take<float>(rd * F);
+        L->Y_op[l] = c.take<float>(ro * 2 * F);
+        L->Y_dev[l] = c.take<float>(rd * 2 * F);
+    }
+    L->E_op = c.take<float>(ro * F);
+    L->E_dev = c.take<float>(rd * F);
+    L->G_op = c.take<float>(ro * F);
+    L->G_dev = c.take<float>(rd * F);
+    L->dY_op = c.take<float>(ro * 2 * F);
+    L->dY_dev = c.take<float>(rd * 2 * F);
+    for (int b = 0; b < 4; ++b) {
+        L->SA[b] = c.take<float>((size_t)R * n_slots(g, b) * K);
+        L->SD[b] = c.take<float>((size_t)R * n_slots(g, b) * K);
+    }
+    L->Zop = c.take<float>(ro * 2 * K);
+    L->Zdev = c.take<float>(rd * 2 * K);
+    int64_t pb = 0;
+    for (int b = 0; b < 4; ++b) {
+        const int64_t rows = (b < 2) ? ro : rd;
+        const int32_t ch = chunks_of(g->max_degree[b], kChunkB);
+        if (ch > 1) pb = std::max(pb, rows * ch * F);
+    }
+    L->PB = c.take<float>(std::max<int64_t>(pb, 1));
+    for (int b = 0; b < 4; ++b) {
+        const int64_t rows = (b < 2) ? ro : rd;
+        L->nb_a[b] = persist_blocks(rows);
+        L->nb_m[b] = persist_blocks(rows * chunks_of(g->max_degree[b], kChunkB));
+        L->part_a[b] = c.take<float>((size_t)L->nb_a[b] * F);
+        L->part_m[b] = c.take<float>((size_t)4 * L->nb_m[b] * F);
+    }
+    L->dU = c.take<float>((size_t)d->layers * 3 * F * 2);
+    L->dcp = c.take<float>((size_t)d->layers * 3 * F);
+    const int64_t sp = split_floats(g, d, R);
+    L->P0 = c.take<float>(sp);
+    L->P1 = c.take<float>(sp);
+    const int64_t H = std::max(d->dec_hidden, 1), Qm = std::max(Q, 1);
+    L->t = c.take<float>(rd * H);
+    L->v = c.take<float>(Qm * H);
+    L->loss_q = c.take<float>(Qm);
+    L->db1q = c.take<float>(Qm * H);
+    L->dw2q = c.take<float>(Qm * H);
+    L->doptq = c.take<float>(Qm * 4 * H);
+    L->db2q = c.take<float>(Qm);
+    L->dTq = c.take<float>(Qm * std::max(g->max_dev, 1) * H);
+    L->qrow = c.take<int32_t>(Qm);
+    (void)S;
+    return c.used;
+}
+
+template <int F, int K>
+void launch_layer_bwd(const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], const ParamReduce &pr, hipStream_t st) {
+    for (int b = 0; b < 4; ++b) {
+        const int64_t waves = (int64_t)P.R * B[b].n_dst * B[b].chunks;
+        if (waves > 0) bwd_scores<F, K><<<(unsigned)((waves + 3) / 4), 256, 0, st>>>(P, B[b]);
+    }
+    for (int b = 0; b < 4; ++b) bwd_softmax<F, K><<<pr.nb_a[b], 256, 0, st>>>(P, B[b], const_cast<float *>(pr.pa[b]));
+    for (int s = 0; s < 4; ++s) {
+        bwd_messages<F, K><<<pr.nb_m[s], 256, 0, st>>>(P, S[s], const_cast<float *>(pr.pm[s]));
+        if (S[s].chunks > 1) bwd_combine<<<grid_for((int64_t)P.R * S[s].n_self * F), 256, 0, st>>>(P, S[s], K);
+    }
+    bwd_params<<<15, 256, 0, st>>>(pr);
+}
+
+template <int F>
+bool dispatch_layer_bwd_f(int K, const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], const ParamReduce &pr,
+                          hipStream_t st) {
+    switch (K) {
+        case 1: launch_layer_bwd<F, 1>(P, B, S, pr, st); return true;
+        case 2: launch_layer_bwd<F, 2>(P, B, S, pr, st); return true;
+        case 4: launch_layer_bwd<F, 4>(P, B, S, pr, st); return true;
+        case 8: launch_layer_bwd<F, 8>(P, B, S, pr, st); return true;
+        case 16: launch_layer_bwd<F, 16>(P, B, S, pr, st); return true;
+        case 32: launch_layer_bwd<F, 32>(P, B, S, pr, st); return true;
+        case 64: launch_layer_bwd<F, 64>(P, B, S, pr, st); return true;
+    }
+    return false;
+}
+
+bool dispatch_layer_bwd(int F, int K, const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], const ParamReduce &pr,
+                        hipStream_t st) {
+    if (F == 64) return dispatch_layer_bwd_f<64>(K, P, B, S, pr, st);
+    if (F == 128) return dispatch_layer_bwd_f<128>(K, P, B, S, pr, st);
+    if (F == 256) return dispatch_layer_bwd_f<256>(K, P, B, S, pr, st);
+    return false;
+}
+
+tag_status check_train(const tag_graph *g, const tag_model_dims *dims, int32_t R, int32_t S, int32_t Q) {
+    if (!g || !dims) TAG_FAIL(TAG_EINVAL, "graph and dims must be non-NULL");
+    tag_status st = check_dims(dims);
+    if (st != TAG_OK) return st;
+    if (dims->dtype != TAG_F32) TAG_FAIL(TAG_ESHAPE, "training supports the fp32 variant only");
+    if (dims->dec_hidden < 1) TAG_FAIL(TAG_ESHAPE, "training needs the MLP decoder (dec_hidden >= 1)");
+    if (R < 1 || S < 1 || Q < 1) TAG_FAIL(TAG_EINVAL, "need n_replicas, n_slices and n_query >= 1");
+    if (S > 4096) TAG_FAIL(TAG_ESHAPE, "training supports at most 4096 slices");
+    return TAG_OK;
+}
+
+}  // namespace
+}  // namespace tag
+
+using namespace tag;
+
+extern "C" tag_status tag_train_workspace(const tag_graph *g, const tag_model_dims *dims, int32_t n_replicas,
+                                          int32_t n_slices, int32_t n_query, size_t *bytes) {
+    clear_error();
+    if (!bytes) TAG_FAIL(TAG_EINVAL, "bytes must be non-NULL");
+    tag_status st = check_train(g, dims, n_replicas, n_slices, n_query);
+    if (st != TAG_OK) return st;
+    TrainLayout L;
+    *bytes = carve_train(g, dims, n_replicas, n_slices, n_query, nullptr, &L);
+    return TAG_OK;
+}
+
+extern "C" tag_status tag_train_step(const tag_graph *g, const tag_model_dims *dims, const tag_weights *w,
+                                     const tag_features *x, const tag_slices *slices, const tag_train_batch *batch,
+                                     const tag_grads *gr, float lr, float *loss, void *workspace, size_t ws_bytes,
+                                     void *hip_stream) {
+    clear_error();
+    if (!w || !x || !slices || !batch || !gr || !loss || !workspace)
+        TAG_FAIL(TAG_EINVAL, "weights, features, slices, batch, grads, loss and workspace must be non-NULL");
+    const int32_t R = x->n_replicas, S = slices->n_slices, Q = batch->n_query;
+    tag_status st = check_train(g, dims, R, S, Q);
+    if (st != TAG_OK) return st;
+    if (!slices->mask || !slices->option) TAG_FAIL(TAG_EINVAL, "NULL slice table");
+    if (!batch->query_rep || !batch->query_graph || !batch->query_op || !batch->target)
+        TAG_FAIL(TAG_EINVAL, "query arrays and targets must be non-NULL");
+    if (!w->dec_w1 || !w->dec_b1 || !w->dec_w2 || !w->dec_b2) TAG_FAIL(TAG_EINVAL, "decoder weights must be non-NULL");
+    const float *gp[] = {gr->enc_op_w, gr->enc_op_b, gr->enc_dev_w, gr->enc_dev_b, gr->enc_edge_w[0],
+                         gr->enc_edge_w[1], gr->enc_edge_w[2], gr->enc_edge_b[0], gr->enc_edge_b[1],
+                         gr->enc_edge_b[2], gr->layer_w, gr->layer_b, gr->att_src, gr->att_dst,
+                         gr->dec_w1, gr->dec_b1, gr->dec_w2, gr->dec_b2};
+    for (const float *p : gp)
+        if (!p) TAG_FAIL(TAG_EINVAL, "gradient arrays must be non-NULL");
+    if (!(lr >= 0.f) || lr == INFINITY) TAG_FAIL(TAG_EINVAL, "lr must be finite and >= 0");
+    TrainLayout L;
+    if (carve_train(g, dims, R, S, Q, nullptr, &L) > ws_bytes)
+        TAG_FAIL(TAG_ENOSPACE, "training workspace too small (see tag_train_workspace)");
+    carve_train(g, dims, R, S, Q, workspace, &L);
+    hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+    const int F = dims->f, K = dims->heads, NL = dims->layers, H = dims->dec_hidden;
+    const int64_t ro = (int64_t)R * g->n_op, rd = (int64_t)R * g->n_dev;
+
+    // forward with saved activations
+    FwdSave save{};
+    for (int l = 0; l < NL; ++l) {
+        save.H_op[l] = L.H_op[l]; save.H_dev[l] = L.H_dev[l];
+        save.Y_op[l] = L.Y_op[l]; save.Y_dev[l] = L.Y_dev[l];
+    }
+    st = forward_run(g, dims, w, x, L.fwd, L.fwd_bytes, L.E_op, L.E_dev, stream, &save);
+    if (st != TAG_OK) return st;
+    FwdLayout FL;
+    carve_fwd(g, dims, R, L.fwd, &FL);   // folded edge terms U, c' of every layer
+
+    // decoder: loss, its parameter gradients and dE
+    DecTrain D{};
+    D.R = R; D.G = g->G; D.S = S; D.Q = Q; D.F = F; D.H = H; D.max_dev = std::max(g->max_dev, 1);
+    D.n_op = g->n_op; D.n_dev = g->n_dev;
+    D.op_off = g->op_off_d; D.dev_off = g->dev_off_d;
+    D.E_op = L.E_op; D.E_dev = L.E_dev;
+    D.mask = slices->mask; D.option = slices->option;
+    D.W1 = w->dec_w1; D.b1 = w->dec_b1; D.w2 = w->dec_w2; D.b2 = w->dec_b2;
+    D.q_rep = batch->query_rep; D.q_graph = batch->query_graph; D.q_op = batch->query_op;
+    D.target = batch->target;
+    D.t = L.t; D.v = L.v; D.qrow = L.qrow;
+    D.inv_q = 1.f / (float)Q;
+    D.loss_q = L.loss_q; D.db1q = L.db1q; D.dw2q = L.dw2q; D.doptq = L.doptq; D.db2q = L.db2q; D.dTq = L.dTq;
+    D.g_op = L.G_op; D.g_dev = L.G_dev;
+    D.g_w1 = gr->dec_w1; D.g_b1 = gr->dec_b1; D.g_w2 = gr->dec_w2; D.g_b2 = gr->dec_b2;
+    const int din = 2 * F + 4;
+    launch_small_gemm(SmallGemm{L.E_dev, F, rd, nullptr, F, w->dec_w1, din, H, nullptr, 0, L.t, H, 0}, stream);
+    dec_rows<<<grid_for(Q), 256, 0, stream>>>(D);
+    launch_small_gemm(SmallGemm{L.E_op, F, Q, L.qrow, F, w->dec_w1 + F, din, H, nullptr, 0, L.v, H, 0}, stream);
+    const size_t dec_sh = sizeof(float) * (S + std::max(64 * (kDecH + 1) + 5 * kDecH, 2 * 64 * kDecHB));
+    dec_train_query<<<Q, 256, dec_sh, stream>>>(D);
+    dec_train_loss<<<1, 64, 0, stream>>>(L.loss_q, Q, loss);
+    dec_train_params<<<grid_for((int64_t)H * din), 256, 0, stream>>>(D);
+    dec_train_grad_dev<<<grid_for(rd * F), 256, 0, stream>>>(D);
+    fill_zero<<<grid_for(ro * F), 256, 0, stream>>>(L.G_op, ro * F);
+    dec_train_grad_op<<<Q, 256, 0, stream>>>(D);
+
+    // layers, last to first
+    BwdLayer P{};
+    P.R = R; P.F = F;
+    P.x_oo = x->x_oo; P.s_oo = x->stride_oo;
+    P.x_dd = x->x_dd; P.s_dd = x->stride_dd;
+    P.x_od = x->x_od; P.s_od = x->stride_od;
+    P.slope = dims->leaky_slope;
+    const float gs = dims->gamma_same, gc = dims->gamma_cross;
+    for (int l = NL - 1; l >= 0; --l) {
+        P.att_src = w->att_src + (size_t)l * 3 * F;
+        P.att_dst = w->att_dst + (size_t)l * 3 * F;
+        P.U = FL.U + (size_t)l * 3 * F * 2;
+        P.cp = FL.cp + (size_t)l * 3 * F;
+        const float *Yo = L.Y_op[l], *Yd = L.Y_dev[l];
+        // forward buckets: Y_op = [oo | od], Y_dev = [dd | od]
+        BwdBucket B[4];
+        B[0] = BwdBucket{g->rowptr[0], g->col[0], g->eid[0], g->n_op, g->n_op, Yo, 0, Yo, 0, L.G_op, gs, 0, 0, 1,
+                         L.SA[0], L.SD[0], n_slots(g, 0), chunks_of(g->max_degree[0], kChunkA), L.Zop, 0};
+        B[1] = BwdBucket{g->rowptr[1], g->col[1], g->eid[1], g->n_op, g->n_dev, Yo, F, Yd, F, L.G_op, gc, 1, 1, 0,
+                         L.SA[1], L.SD[1], n_slots(g, 1), chunks_of(g->max_degree[1], kChunkA), L.Zop, 1};
+        B[2] = BwdBucket{g->rowptr[2], g->col[2], g->eid[2], g->n_dev, g->n_op, Yd, F, Yo, F, L.G_dev, gc, 1, 1, 0,
+                         L.SA[2], L.SD[2], n_slots(g, 2), chunks_of(g->max_degree[2], kChunkA), L.Zdev, 1};
+        B[3] = BwdBucket{g->rowptr[3], g->col[3], g->eid[3], g->n_dev, g->n_dev, Yd, 0, Yd, 0, L.G_dev, gs, 2, 2, 1,
+                         L.SA[3], L.SD[3], n_slots(g, 3), chunks_of(g->max_degree[3], kChunkA), L.Zdev, 0};
+        // source passes; dY_op = [oo | od], dY_dev = [od | dd]
+        BwdSrc Sx[4];
+        Sx[0] = BwdSrc{g->rowptr[0], g->col[0], g->eid[0], g->n_op, g->n_op, Yo, 0, L.G_op, gs, L.SA[0], L.SD[0],
+                       n_slots(g, 0), 1, 0, 0, L.Zop, 0, L.dY_op, 0, L.PB, chunks_of(g->max_degree[0], kChunkB)};
+        Sx[1] = BwdSrc{g->rowptr[1], g->col[1], g->eid[1], g->n_op, g->n_dev, Yo, F, L.G_dev, gc, L.SA[2], L.SD[2],
+                       n_slots(g, 2), 0, 1, 1, L.Zop, 1, L.dY_op, F, L.PB, chunks_of(g->max_degree[1], kChunkB)};
+        Sx[2] = BwdSrc{g->rowptr[2], g->col[2], g->eid[2], g->n_dev, g->n_op, Yd, F, L.G_op, gc, L.SA[1], L.SD[1],
+                       n_slots(g, 1), 0, 1, 1, L.Zdev, 1, L.dY_dev, 0, L.PB, chunks_of(g->max_degree[2], kChunkB)};
+        Sx[3] = BwdSrc{g->rowptr[3], g->col[3], g->eid[3], g->n_dev, g->n_dev, Yd, 0, L.G_dev, gs, L.SA[3], L.SD[3],
+                       n_slots(g, 3), 1, 2, 2, L.Zdev, 0, L.dY_dev, F, L.PB, chunks_of(g->max_degree[3], kChunkB)};
+        ParamReduce pr{};
+        for (int b = 0; b < 4; ++b) {
+            pr.pa[b] = L.part_a[b]; pr.nb_a[b] = L.nb_a[b];
+            pr.pm[b] = L.part_m[b]; pr.nb_m[b] = L.nb_m[b];
+        }
+        pr.F = F;
+        pr.g_att_src = gr->att_src + (size_t)l * 3 * F;
+        pr.g_att_dst = gr->att_dst + (size_t)l * 3 * F;
+        pr.dU = L.dU + (size_t)l * 3 * F * 2;
+        pr.dcp = L.dcp + (size_t)l * 3 * F;
+        if (!dispatch_layer_bwd(F, K, P, B, Sx, pr, stream)) TAG_FAIL(TAG_ESHAPE, "unsupported f / heads");
+        const float *Wl = w->layer_w + (size_t)l * 3 * F * 2 * F;
+        float *gW = gr->layer_w + (size_t)l * 3 * F * 2 * F;
+        // dW^h: op side rows [oo ; od], device side rows [od ; dd]
+        weight_grad(L.dY_op, 2 * F, L.H_op[l], F, 2 * F, F, false, ro, L.P0, gW, 2 * F, nullptr, 0, stream);
+        {
+            int64_t splits;
+            const int64_t per = split_k_per(rd, ((2 * F + GM - 1) / GM) * ((F + GN - 1) / GN), &splits);
+            Gemm gd{L.dY_dev, 2 * F, L.H_dev[l], F, 2 * F, F, rd, -1, L.P1, F, 2 * F * F, per, 0};
+            launch_gemm(gd, false, false, splits, stream);
+            float *g1 = gW + (size_t)F * 2 * F;
+            sum_splits<<<grid_for((int64_t)F * F), 256, 0, stream>>>(L.P1, 2 * F * F, F, (int32_t)splits, F, F, g1,
+                                                                    2 * F, 1);
+            sum_splits<<<grid_for((int64_t)F * F), 256, 0, stream>>>(L.P1 + (size_t)F * F, 2 * F * F, F,
+                                                                    (int32_t)splits, F, F, g1 + (size_t)F * 2 * F,
+                                                                    2 * F, 0);
+        }
+        // dH = dY [W^h ; W^h'] (overwrites the layer-output gradients, no longer needed)
+        launch_gemm(Gemm{L.dY_op, 2 * F, Wl, 2 * F, ro, F, 2 * F, -1, L.G_op, F, 0, 2 * F, 0}, true, false, 1, stream);
+        launch_gemm(Gemm{L.dY_dev, 2 * F, Wl + (size_t)F * 2 * F, 2 * F, rd, F, 2 * F, -1, L.G_dev, F, 0, 2 * F, 0},
+                    true, false, 1, stream);
+    }
+
+    // node encoders: h0 = ReLU(A x + c)
+    relu_mask<<<grid_for(ro * F), 256, 0, stream>>>(L.G_op, L.H_op[0], ro * F);
+    relu_mask<<<grid_for(rd * F), 256, 0, stream>>>(L.G_dev, L.H_dev[0], rd * F);
+    weight_grad(L.G_op, F, x->x_op, dims->f_op, F, dims->f_op, true, ro, L.P0, gr->enc_op_w, dims->f_op,
+                gr->enc_op_b, 0, stream);
+    weight_grad(L.G_dev, F, x->x_dev, dims->f_dev, F, dims->f_dev, true, rd, L.P1, gr->enc_dev_w, dims->f_dev,
+                gr->enc_dev_b, 0, stream);
+    // folded edge encoders
+    FoldBwd fb{w->layer_w, {w->enc_edge_w[0], w->enc_edge_w[1], w->enc_edge_w[2]},
+               {w->enc_edge_b[0], w->enc_edge_b[1], w->enc_edge_b[2]}, L.dU, L.dcp, gr->layer_w, gr->layer_b,
+               {gr->enc_edge_w[0], gr->enc_edge_w[1], gr->enc_edge_w[2]},
+               {gr->enc_edge_b[0], gr->enc_edge_b[1], gr->enc_edge_b[2]}, F, NL};
+    fold_bwd_we<<<grid_for((int64_t)NL * 3 * F * F), 256, 0, stream>>>(fb);
+    fold_bwd_enc<<<3, 256, 0, stream>>>(fb);
+
+    if (lr > 0.f) {
+        SgdList sl{};
+        const int64_t fo = dims->f_op, fd = dims->f_dev, Hd = H;
+        float *wp[18] = {const_cast<float *>(w->enc_op_w), const_cast<float *>(w->enc_op_b),
+                         const_cast<float *>(w->enc_dev_w), const_cast<float *>(w->enc_dev_b),
+                         const_cast<float *>(w->enc_edge_w[0]), const_cast<float *>(w->enc_edge_w[1]),
+                         const_cast<float *>(w->enc_edge_w[2]), const_cast<float *>(w->enc_edge_b[0]),
+                         const_cast<float *>(w->enc_edge_b[1]), const_cast<float *>(w->enc_edge_b[2]),
+                         const_cast<float *>(w->layer_w), const_cast<float *>(w->layer_b),
+                         const_cast<float *>(w->att_src), const_cast<float *>(w->att_dst),
+                         const_cast<float *>(w->dec_w1), const_cast<float *>(w->dec_b1),
+                         const_cast<float *>(w->dec_w2), const_cast<float *>(w->dec_b2)};
+        const int64_t n[18] = {F * fo, F, F * fd, F, F, F, 2 * F, F, F, F, (int64_t)NL * 3 * F * 2 * F,
+                               (int64_t)NL * 3 * F, (int64_t)NL * 3 * F, (int64_t)NL * 3 * F, Hd * din, Hd, Hd, 1};
+        for (int i = 0; i < 18; ++i) {
+            sl.w[i] = wp[i];
+            sl.g[i] = gp[i];
+            sl.n[i] = n[i];
+        }
+        sl.count = 18;
+        sl.lr = lr;
+        sgd_update<<<dim3(64, 18), 256, 0, stream>>>(sl);
+    }
+    return launch_status("tag_train_step");
+}

@@ -549,7 +549,7 @@ def make_search_problem(name: str, n_groups: Optional[int] = None) -> SearchProb
     for g in range(k):
         group_of[bounds[g]:bounds[g + 1]] = g
     rng = rng_for(wl.cfg_id, 3_000_000)
-    params = rng.lognormal(math.log(2e5), 2.0, size=n)
+    params = rng.lognormal(math.log(2e4), 2.0, size=n)
     masks, opts = make_slices(name, topo.n_dev, wl.n_slices)
     return SearchProblem(name=name, topo=topo, group_of=group_of, n_groups=k,
                          op_params=params, masks=masks, options=opts)

@@ -30,7 +30,7 @@ def test_exports_every_declared_symbol(P):
     assert len(names) >= 13
     for n in names:
         assert hasattr(lib, n), n
-    assert set(names) == set(P._abi.EXPORTS) | set(P._abi.SEARCH_EXPORTS)
+    assert set(names) == set(P._abi.EXPORTS) | set(P._abi.SEARCH_EXPORTS) | set(P._abi.TRAIN_EXPORTS)
     assert "gfx950" in P.tag_version()
 
 
