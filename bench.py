@@ -199,6 +199,155 @@ def search_bench(args) -> int:
     return 0
 
 
+TRAIN_KERNELS = {"bwd_decoder": "decoder loss + backward kernels", "bwd_scores": "bwd_scores",
+                 "bwd_softmax": "bwd_softmax", "bwd_messages": "bwd_messages", "bwd_dh": "gemm_f32 (dH)",
+                 "bwd_dw": "gemm_f32 (split-K dW)"}
+TRAIN_LAUNCHES = {"bwd_decoder": 1, "bwd_scores": 4, "bwd_softmax": 4, "bwd_messages": 4, "bwd_dh": 2, "bwd_dw": 2}
+
+
+def train_work(stage: str, wl, topo, R: int) -> tuple:
+    """(flops, bytes) of ALL launches of a backward stage in one layer (the
+    average launch is this over the stage's launches per layer): every
+    unique row read or written once, per-entry scalars (s/alpha, dalpha/dz:
+    K floats each) written or read once per pass, graph structure once."""
+    N, M, F, K = topo.n_op, topo.n_dev, wl.f, wl.heads
+    eo, ed, ev = topo.e_oo, topo.e_dd, topo.e_od
+    nnz = 2 * eo + 2 * ev + 2 * ed                 # entries of the four buckets
+    csr = (N + 1 + M + 1) * 8 + nnz * 8            # row pointers and (col, eid) per entry
+    feat = R * (eo * 4 + ed * 8 + ev)              # edge features per candidate
+    rows = R * (N + M)
+    if stage == "bwd_scores":      # Y halves (src and dst), dO rows, features in; s, dalpha out
+        by = rows * 2 * F * 4 + rows * F * 4 + csr + feat + R * nnz * K * 8
+        return float(R * nnz * F * 6), float(by)
+    if stage == "bwd_softmax":     # s, dalpha in; alpha, dz out; Z out; Y halves for d adst
+        by = R * nnz * K * 16 + rows * 2 * K * 4 + rows * 2 * F * 4 + csr
+        return float(R * nnz * K * 12), float(by)
+    if stage == "bwd_messages":    # Y halves, dO rows of the neighbours, alpha, dz, features in; dY out
+        by = rows * 2 * F * 4 + rows * F * 4 + R * nnz * K * 8 + csr + feat + rows * 2 * F * 4
+        return float(R * nnz * F * 12), float(by)
+    if stage == "bwd_dh":          # dY [rows][2F] in, W^h in, dH [rows][F] out
+        return 2.0 * rows * 2 * F * F, float(rows * 2 * F * 4 + 3 * F * 2 * F * 4 + rows * F * 4)
+    if stage == "bwd_dw":          # dY and H in, split partials out
+        return 2.0 * rows * 2 * F * F, float(rows * 2 * F * 4 + rows * F * 4)
+    return 0.0, 0.0
+
+
+def train_bench(args) -> int:
+    """GNN training step (Section 4.2.2): forward pass over the batch of
+    candidates with saved activations, cross entropy of the decoder's priors
+    for the candidates' next-group ops against synthetic visit
+    distributions, the gradient of every parameter and the SGD update.  The
+    graph is built once (it does not change between steps); the step is
+    everything tag_train_step does.  Reports candidate graphs trained per
+    second."""
+    import torch
+
+    import paper_2302_06126_amd as P
+    import paper_2302_06126_amd.train as PT
+    from paper_2302_06126_amd import _abi
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    name = args.workload
+    wl = synth.WORKLOADS[name]
+    if wl.dtype != "f32":
+        sys.exit("the training step runs the fp32 variant; choose an fp32 workload")
+    topo = synth.make_topology(name)
+    R = wl.batch
+    batch = synth.make_batch(name, topo, R, wl.f_op)
+    masks, opts = synth.make_slices(name, topo.n_dev, wl.n_slices)
+    w = synth.make_weights(wl.f, wl.heads, wl.layers, wl.f_op, wl.f)
+    # one target distribution per candidate (a search state), for the first
+    # op of the candidate's next group
+    first = np.array([int(np.flatnonzero(batch.query_rep == r)[0]) for r in range(R)])
+    q_rep, q_op = batch.query_rep[first].astype(np.int32), batch.query_op[first].astype(np.int32)
+    Q, S = R, len(masks)
+    # synthetic visit distributions: normalised gamma-distributed counts
+    rng = synth.rng_for(wl.cfg_id, 4_000_000)
+    visits = rng.gamma(0.3, size=(Q, S))
+    target = (visits / visits.sum(1, keepdims=True)).astype(np.float32)
+    graph = P.Graph([topo], device="cuda:0")
+    model = P.Model(w, f=wl.f, heads=wl.heads, layers=wl.layers, f_op=wl.f_op, device="cuda:0")
+    tr = PT.Trainer(graph, model, R, masks, opts, q_rep, np.zeros(Q, np.int32), q_op)
+    tr.set_targets(target)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    keep = (t(batch.x_op), t(batch.x_dev), t(batch.x_oo), t(batch.x_dd), t(batch.x_od))
+    feats = P.make_features(*keep)
+    stream = torch.cuda.current_stream()
+    lr = 1e-3
+    print(f"[bench] train on {name}: B={R} N={topo.n_op} M={topo.n_dev} f={wl.f} L={wl.layers} Q={Q} S={S}; "
+          f"warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(max(args.warmup, 1)):
+        tr.step(feats, lr=lr, stream=stream)
+    torch.cuda.synchronize()
+    stage_ms = {}
+    for sname in _abi.TRAIN_STAGES:
+        _abi.check(P.tag_profile_begin(_abi.STAGE_NAMES.index(sname), 256), "tag_profile_begin")
+        tr.step(feats, lr=lr, stream=stream)
+        st, ms, n = P.tag_profile_end()
+        _abi.check(st, "tag_profile_end")
+        stage_ms[sname] = ms
+    stage = max((k for k in stage_ms if k != "bwd_decoder"), key=stage_ms.get)
+    per_step = TRAIN_LAUNCHES[stage] * wl.layers
+    torch.cuda.synchronize()
+    _abi.check(P.tag_profile_begin(_abi.STAGE_NAMES.index(stage), per_step * args.steps), "tag_profile_begin")
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        tr.step(feats, lr=lr, stream=stream)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    st, kern_ms, n_launch = P.tag_profile_end()
+    _abi.check(st, "tag_profile_end")
+    loss = float(tr.loss.cpu()[0])
+    flops, byts = train_work(stage, wl, topo, R)
+    flops /= TRAIN_LAUNCHES[stage]
+    byts /= TRAIN_LAUNCHES[stage]
+    avg_s = kern_ms / 1e3 / max(n_launch, 1)
+    if stage in ("bwd_dh", "bwd_dw"):
+        ach = flops / avg_s / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 3), "peak": PEAK_TFLOPS["f32"], "unit": "TFLOP/s",
+                "frac": round(ach / PEAK_TFLOPS["f32"], 4)}
+    else:
+        ach = byts / avg_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(ach / PEAK_HBM_GBS, 4)}
+    roof.update({"traffic": None, "kernel": TRAIN_KERNELS[stage], "stage": stage,
+                 "avg_launch_ms": round(avg_s * 1e3, 4), "launches": n_launch,
+                 "algorithmic_bytes_per_launch": byts, "algorithmic_flops_per_launch": flops})
+    out = {
+        "metric": "GNN training candidate graphs/sec (forward + backward + SGD update)",
+        "value": round(R * args.steps / el, 2), "unit": "graphs/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(el * 1e3 / args.steps, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": name, "graphs_per_step": R, "n_op": topo.n_op, "n_dev": topo.n_dev,
+                   "layers": wl.layers, "f": wl.f, "heads": wl.heads, "slices": S, "queries": Q,
+                   "lr": lr, "parallelism": "none"},
+        "loss_after": loss,
+        "stage_ms_one_step": {k: round(v, 4) for k, v in stage_ms.items()},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (reference training step)", file=sys.stderr, flush=True)
+        from oracle import train as OT
+        torch.set_num_threads(1)
+        t0 = time.perf_counter()
+        n = 0
+        while n < R:
+            item = dict(topo=topo, x_op=batch.x_op[n], x_dev=batch.x_dev[n], x_oo=batch.x_oo, x_dd=batch.x_dd[n],
+                        x_od=batch.x_od[n], query_op=q_op[n:n + 1], target=target[n:n + 1])
+            OT.loss_and_grads([item], w, f=wl.f, heads=wl.heads, layers=wl.layers, masks=masks, options=opts)
+            n += 1
+            if time.perf_counter() - t0 >= args.cpu_seconds:
+                break
+        cel = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round(n / cel, 4), "unit": "graphs/s", "cores": 1, "kind": "oracle",
+                               "sample": f"{n} of {R} candidates of the {name} batch, each: the reference "
+                                         f"training step (fp64 forward, loss, autograd gradients), one thread, "
+                                         f"{cel:.1f} s", "cpu": cpu_model()}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -211,8 +360,9 @@ def main() -> int:
                     help="run one plain device copy of this size first (counter calibration)")
     ap.add_argument("--stage", default="auto", choices=["auto"] + list(KERNEL_NAMES),
                     help="kernel stage timed for the roofline (auto: the longest one)")
-    ap.add_argument("--mode", default="forward", choices=["forward", "search"],
-                    help="forward: the GNN hot path (default line); search: batched PUCT search rounds")
+    ap.add_argument("--mode", default="forward", choices=["forward", "search", "train"],
+                    help="forward: the GNN hot path (default line); search: batched PUCT search rounds; "
+                         "train: the GNN training step")
     ap.add_argument("--search-batch", type=int, default=0, help="leaves per search round (default: the batch)")
     ap.add_argument("--c-puct", type=float, default=1.5)
     args = ap.parse_args()
@@ -223,6 +373,8 @@ def main() -> int:
 
     if args.mode == "search":
         return search_bench(args)
+    if args.mode == "train":
+        return train_bench(args)
 
     import torch
 
@@ -312,7 +464,7 @@ def main() -> int:
 
     # which stage dominates: one profiled step per stage (outside the timed region)
     stage_ms = {}
-    for sid, sname in enumerate(_abi.STAGE_NAMES):
+    for sid, sname in enumerate(_abi.FORWARD_STAGES):
         _abi.check(P.tag_profile_begin(sid, 64), "tag_profile_begin")
         step()
         st, ms, n = P.tag_profile_end()

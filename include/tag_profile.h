@@ -32,7 +32,15 @@ enum {
     TAG_STAGE_AGG_DEV_MERGE = 6,  /* dev <- op merge + dev <- dev (1/layer)                  */
     TAG_STAGE_DEV_PREP = 7,       /* device message table (1/layer)                          */
     TAG_STAGE_DECIDE = 8,         /* all kernels of tag_gnn_decide (one pair per call)       */
-    TAG_STAGE_COUNT = 9
+    /* tag_train_step (include/tag_train.h); its forward pass records the   */
+    /* stages above                                                         */
+    TAG_STAGE_BWD_DECODER = 9,    /* decoder loss + backward kernels (one pair per call)     */
+    TAG_STAGE_BWD_SCORES = 10,    /* per-entry scores, one launch per bucket (4/layer)       */
+    TAG_STAGE_BWD_SOFTMAX = 11,   /* per-destination softmax backward (4/layer)              */
+    TAG_STAGE_BWD_MESSAGES = 12,  /* per-source message backward (4/layer)                   */
+    TAG_STAGE_BWD_DH = 13,        /* dH = dY W GEMMs, op and device rows (2/layer)           */
+    TAG_STAGE_BWD_DW = 14,        /* split-K dW^h = dY^T H GEMMs (2/layer)                   */
+    TAG_STAGE_COUNT = 15
 };
 
 /* Start recording event pairs around launches of `stage`, for at most

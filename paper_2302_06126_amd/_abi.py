@@ -33,7 +33,9 @@ TRAIN_EXPORTS = ("tag_train_workspace", "tag_train_step")
 
 # kernel stages (include/tag_profile.h)
 STAGE_NAMES = ("graph_build", "encode", "transform", "agg_op_op", "agg_op_dev", "agg_dev_op", "agg_dev_merge",
-               "dev_prep", "decide")
+               "dev_prep", "decide", "bwd_decoder", "bwd_scores", "bwd_softmax", "bwd_messages", "bwd_dh", "bwd_dw")
+FORWARD_STAGES = STAGE_NAMES[:9]
+TRAIN_STAGES = STAGE_NAMES[9:]
 
 _P32 = C.POINTER(C.c_int32)
 _P64 = C.POINTER(C.c_int64)

@@ -207,6 +207,20 @@ inline unsigned grid_for(int64_t n) {
 }
 
 }  // namespace
+
+void launch_slice_terms(int32_t R, int32_t G, int32_t S, int32_t F, int32_t H, int64_t n_dev, const int32_t *dev_off,
+                        const float *t, const float *W1, const float *b1, const uint64_t *mask,
+                        const uint8_t *option, float *u, hipStream_t st) {
+    DecArgs A{};
+    A.R = R; A.G = G; A.S = S; A.F = F; A.H = H; A.Hx = std::max(H, 1);
+    A.n_dev = n_dev;
+    A.dev_off = dev_off;
+    A.t = const_cast<float *>(t); A.P = W1; A.b1 = b1;
+    A.mask = mask; A.option = option;
+    A.u = u;
+    dec_slice<<<(unsigned)((int64_t)R * G * ((A.Hx + kSliceH - 1) / kSliceH)), 256, 0, st>>>(A);
+}
+
 }  // namespace tag
 
 using namespace tag;

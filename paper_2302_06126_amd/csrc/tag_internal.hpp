@@ -108,6 +108,13 @@ struct SmallGemm {
     int c_bf16;
 };
 void launch_small_gemm(const SmallGemm &G, hipStream_t st);
+
+// Slice part of the decoder's hidden pre-activation for every candidate
+// graph rg = r G + g (decide.hip): u[rg][h][a] = sum_{j in mask_a} t[dev(rg, j)][h]
+// + W1[h][2F + option_a] + b1[h], with t = E_dev W1_dev^T ([R n_dev][H]).
+void launch_slice_terms(int32_t R, int32_t G, int32_t S, int32_t F, int32_t H, int64_t n_dev, const int32_t *dev_off,
+                        const float *t, const float *W1, const float *b1, const uint64_t *mask,
+                        const uint8_t *option, float *u, hipStream_t st);
 }
 
 // ----------------------------------------------------------- device helpers

@@ -136,7 +136,7 @@ __global__ void __launch_bounds__(256) gemm_f32(Gemm G) {
 // split count for a k-range of K rows over `tiles` output tiles: enough
 // blocks to fill the chip, at least 4 k-chunks per split
 int64_t split_k_per(int64_t K, int64_t tiles, int64_t *splits) {
-    int64_t s = std::max<int64_t>(1, std::min<int64_t>(2048 / std::max<int64_t>(tiles, 1), (K + 63) / 64));
+    int64_t s = std::max<int64_t>(1, std::min<int64_t>(256 / std::max<int64_t>(tiles, 1), (K + 63) / 64));
     int64_t per = ((K + s - 1) / s + GK - 1) / GK * GK;
     per = std::max<int64_t>(per, GK);
     *splits = std::max<int64_t>(1, (K + per - 1) / per);
@@ -172,13 +172,16 @@ inline unsigned grid_for(int64_t n, int per = 256) {
 // ldb, optional ones column at nb), summed over splits into out
 // ([M][nb] of stride ldo) and, with a ones column, bias_out [M].
 void weight_grad(const float *A, int64_t lda, const float *B, int64_t ldb, int64_t M, int64_t nb, bool ones,
-                 int64_t K, float *P, float *out, int64_t ldo, float *bias_out, int accumulate, hipStream_t st) {
+                 int64_t K, float *P, float *out, int64_t ldo, float *bias_out, int accumulate, hipStream_t st,
+                 int stage = -1) {
     const int64_t N = nb + (ones ? 1 : 0);
     const int64_t tiles = ((M + GM - 1) / GM) * ((N + GN - 1) / GN);
     int64_t splits;
     const int64_t per = split_k_per(K, tiles, &splits);
     Gemm g{A, lda, B, ldb, M, N, K, ones ? nb : -1, P, N, M * N, per, 0};
+    prof_begin(stage, st);
     launch_gemm(g, false, false, splits, st);
+    prof_end(stage, st);
     sum_splits<<<grid_for(M * nb), 256, 0, st>>>(P, M * N, N, (int32_t)splits, M, nb, out, ldo, accumulate);
     if (ones) sum_splits<<<grid_for(M), 256, 0, st>>>(P + nb, M * N, N, (int32_t)splits, M, 1, bias_out, 1, accumulate);
 }
@@ -513,29 +516,37 @@ struct ParamReduce {
     float *dU, *dcp;                // [3][F][2], [3][F] of the layer
 };
 
-__global__ void bwd_params(ParamReduce R) {
-    // relations of the buckets (op<-op, op<-dev, dev<-op, dev<-dev) and of
-    // the source passes (op oo, op od, dev od, dev dd)
+// block (relation r, quantity, 16 columns); thread (column, row group of
+// 16) sums its rows of every partial array of the relation, then the 16
+// groups are added in order
+__global__ void __launch_bounds__(256) bwd_params(ParamReduce R) {
+    __shared__ float red[16][17];
     const int rel_of[4] = {0, 1, 1, 2};
     const int F = R.F;
-    const int r = blockIdx.x / 5, qty = blockIdx.x % 5;
-    for (int c = threadIdx.x; c < F; c += blockDim.x) {
-        float s = 0.f;
+    const int cb = (F + 15) / 16;
+    const int rq = blockIdx.x / cb, c = (blockIdx.x % cb) * 16 + (threadIdx.x & 15), grp = threadIdx.x >> 4;
+    const int r = rq / 5, qty = rq % 5;
+    float s = 0.f;
+    if (c < F) {
         for (int p = 0; p < 4; ++p) {
             if (rel_of[p] != r) continue;
-            if (qty == 0) {
-                for (int32_t b = 0; b < R.nb_a[p]; ++b) s += R.pa[p][(int64_t)b * F + c];
-            } else {
-                const float *base = R.pm[p] + (int64_t)(qty - 1) * R.nb_m[p] * F;
-                for (int32_t b = 0; b < R.nb_m[p]; ++b) s += base[(int64_t)b * F + c];
-            }
+            const float *base;
+            int32_t nb;
+            if (qty == 0) { base = R.pa[p]; nb = R.nb_a[p]; }
+            else { base = R.pm[p] + (int64_t)(qty - 1) * R.nb_m[p] * F; nb = R.nb_m[p]; }
+            for (int32_t b = grp; b < nb; b += 16) s += base[(int64_t)b * F + c];
         }
-        if (qty == 0) R.g_att_dst[r * F + c] = s;
-        else if (qty == 1) R.g_att_src[r * F + c] = s;
-        else if (qty == 2) R.dU[((int64_t)r * F + c) * 2 + 0] = s;
-        else if (qty == 3) R.dU[((int64_t)r * F + c) * 2 + 1] = s;
-        else R.dcp[r * F + c] = s;
     }
+    red[grp][threadIdx.x & 15] = s;
+    __syncthreads();
+    if (grp != 0 || c >= F) return;
+    float t = 0.f;
+    for (int g = 0; g < 16; ++g) t += red[g][threadIdx.x & 15];
+    if (qty == 0) R.g_att_dst[r * F + c] = t;
+    else if (qty == 1) R.g_att_src[r * F + c] = t;
+    else if (qty == 2) R.dU[((int64_t)r * F + c) * 2 + 0] = t;
+    else if (qty == 3) R.dU[((int64_t)r * F + c) * 2 + 1] = t;
+    else R.dcp[r * F + c] = t;
 }
 
 // ReLU mask of the encoders: g = H0 > 0 ? g : 0
@@ -570,49 +581,70 @@ __global__ void fold_bwd_we(FoldBwd a) {
     }
 }
 
-// grad A_r[k][t] = sum_l sum_o W^e_{l,r}[o][k] dU_{l,r}[o][t];  grad c_r[k] likewise with dc'
-__global__ void fold_bwd_enc(FoldBwd a) {
+// grad A_r[k][t] = sum_l sum_o W^e_{l,r}[o][k] dU_{l,r}[o][t];  grad c_r[k] likewise with dc'.
+// Block (relation, 64 k); thread (k, o group of 4) sums its o over the
+// layers, then the groups are added in order.
+__global__ void __launch_bounds__(256) fold_bwd_enc(FoldBwd a) {
+    __shared__ float red[3][4][64];
     const int F = a.F;
-    const int r = blockIdx.x, d = r == 2 ? 2 : 1;
-    for (int k = threadIdx.x; k < F; k += blockDim.x) {
-        float s0 = 0.f, s1 = 0.f, sc = 0.f;
+    const int kb = (F + 63) / 64;
+    const int r = blockIdx.x / kb, k = (blockIdx.x % kb) * 64 + (threadIdx.x & 63), grp = threadIdx.x >> 6;
+    const int d = r == 2 ? 2 : 1;
+    float s0 = 0.f, s1 = 0.f, sc = 0.f;
+    if (k < F) {
         for (int l = 0; l < a.L; ++l) {
             const int64_t lr = (int64_t)l * 3 + r;
-            for (int o = 0; o < F; ++o) {
+            for (int o = grp; o < F; o += 4) {
                 const float we = a.layer_w[(lr * F + o) * 2 * F + F + k];
                 s0 = fmaf(we, a.dU[(lr * F + o) * 2 + 0], s0);
                 s1 = fmaf(we, a.dU[(lr * F + o) * 2 + 1], s1);
                 sc = fmaf(we, a.dcp[lr * F + o], sc);
             }
         }
-        a.g_A[r][(int64_t)k * d + 0] = s0;
-        if (d == 2) a.g_A[r][(int64_t)k * d + 1] = s1;
-        a.g_c[r][k] = sc;
     }
+    const int kk = threadIdx.x & 63;
+    red[0][grp][kk] = s0;
+    red[1][grp][kk] = s1;
+    red[2][grp][kk] = sc;
+    __syncthreads();
+    if (grp != 0 || k >= F) return;
+    float t0 = 0.f, t1 = 0.f, tc = 0.f;
+    for (int g = 0; g < 4; ++g) { t0 += red[0][g][kk]; t1 += red[1][g][kk]; tc += red[2][g][kk]; }
+    a.g_A[r][(int64_t)k * d + 0] = t0;
+    if (d == 2) a.g_A[r][(int64_t)k * d + 1] = t1;
+    a.g_c[r][k] = tc;
 }
 
 // ------------------------------------------------------------------ decoder
+// With t = E_dev W1_dev^T, the slice part u[rg][h][a] = sum_{j in mask_a}
+// t_j[h] + W1_opt[h][option_a] + b1[h] (shared by every query of the
+// candidate graph rg) and v_q = W1_op E_op[i_q], the hidden pre-activation
+// is u[rg][h][a] + v_q[h].  Backward, per candidate graph, with
+// dpre_qah = dscore_qa w2_h [pre > 0] and D_ah = sum_{q of rg} dpre_qah:
+//   dT_j = sum_{a: j in mask_a} D_a   (then dE_dev = dT W1_dev, dW1_dev = dT^T E_dev)
+//   dv_q = sum_a dpre_qa             (then dE_op = dv W1_op, dW1_op = dv^T E_op[i_q])
+//   dW1_opt[o] = sum_{a: option o} D_a, db1 = sum_a D_a, dw2 = sum dscore ReLU(pre),
+//   db2 = sum dscore.
 struct DecTrain {
-    int32_t R, G, S, Q, F, H, max_dev;
+    int32_t R, G, S, Q, F, H, RG;
     int64_t n_op, n_dev;
     const int32_t *op_off, *dev_off;
-    const float *E_op, *E_dev;
     const uint64_t *mask;
     const uint8_t *option;
-    const float *W1, *b1, *w2, *b2;
+    const float *w2, *b2;
     const int32_t *q_rep, *q_graph, *q_op;
     const float *target;
-    const float *t;        // [R*n_dev][H] = E_dev W1_dev^T
-    const float *v;        // [Q][H] = W1_op E_op[query row]
-    int32_t *qrow;         // [Q] E_op row of each query (-1: invalid)
+    const float *u;          // [RG][H][S]
+    const float *v;          // [Q][H]
+    int32_t *qrow;           // [Q] E_op row of each query (-1: invalid)
+    int32_t *qcnt, *qoff, *qlist;   // queries per candidate graph: [RG], [RG+1], [Q]
     float inv_q;
-    float *loss_q;         // [Q]
-    float *db1q, *dw2q;    // [Q][H]
-    float *doptq;          // [Q][4][H]
-    float *db2q;           // [Q]
-    float *dTq;            // [Q][max_dev][H]
-    float *g_op, *g_dev;   // dE_op [R*n_op][F], dE_dev [R*n_dev][F]
-    float *g_w1, *g_b1, *g_w2, *g_b2;
+    float *ds;               // [Q][S] d loss / d score
+    float *loss_q, *db2q;    // [Q]
+    float *dvq;              // [Q][H]
+    float *dT;               // [R n_dev][H]
+    float *dopt_part;        // [RG][4][H]
+    float *dw2_part;         // [RG][H]
 };
 
 __device__ __forceinline__ bool dec_query(const DecTrain &A, int32_t q, int32_t *r, int32_t *g, int32_t *op) {
@@ -628,81 +660,71 @@ __global__ void dec_rows(DecTrain A) {
     }
 }
 
-constexpr int kDecH = 32;     // hidden units per score chunk
-constexpr int kDecHB = 64;    // hidden units per gradient chunk
+// query lists per candidate graph, in query order: counts, offsets, lists
+__global__ void dec_count(DecTrain A, int fill) {
+    for (int64_t rg = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; rg < A.RG; rg += (int64_t)gridDim.x * blockDim.x) {
+        int32_t n = 0;
+        int32_t *out = fill ? A.qlist + A.qoff[rg] : nullptr;
+        for (int32_t q = 0; q < A.Q; ++q) {
+            if (A.qrow[q] < 0 || (int64_t)A.q_rep[q] * A.G + A.q_graph[q] != rg) continue;
+            if (fill) out[n] = q;
+            ++n;
+        }
+        if (!fill) A.qcnt[rg] = n;
+    }
+}
 
-// One block of 256 per query.  Scores (thread per slice), softmax, loss
-// and dscore; then per chunk of 64 hidden units, thread (hh, jg) walks the
-// slices in order: pre = b1 + W1_opt[opt] + v + sum_{j in mask} t_j,
-// dpre = dscore w2 [pre > 0]; it sums dpre into dT[j] for its devices
-// j = jg mod 4, and threads jg = 0 also sum db1, dw2, dW1_opt.
-__global__ void __launch_bounds__(256) dec_train_query(DecTrain A) {
-    extern __shared__ float sh[];
-    __shared__ float red[256];
-    __shared__ float red2[256];
-    float *sc = sh;                       // [S] scores, then dscore
-    float *work = sh + A.S;
+__global__ void __launch_bounds__(256) dec_scan(DecTrain A) {
+    __shared__ int32_t part[256];
+    const int t = threadIdx.x;
+    const int64_t per = (A.RG + 255) / 256, b = t * per, e = b + per < A.RG ? b + per : A.RG;
+    int32_t s = 0;
+    for (int64_t i = b; i < e; ++i) s += A.qcnt[i];
+    part[t] = s;
+    __syncthreads();
+    if (t == 0) {
+        int32_t run = 0;
+        for (int i = 0; i < 256; ++i) { const int32_t x = part[i]; part[i] = run; run += x; }
+        A.qoff[A.RG] = run;
+    }
+    __syncthreads();
+    int32_t run = part[t];
+    for (int64_t i = b; i < e; ++i) { A.qoff[i] = run; run += A.qcnt[i]; }
+}
+
+// one block per query: scores of every slice, softmax, loss term and dscore
+__global__ void __launch_bounds__(256) dec_scores(DecTrain A) {
+    extern __shared__ float sh[];   // sc[S] | v[H] | w2[H]
+    __shared__ float red[256], red2[256];
     const int tid = threadIdx.x;
     const int32_t q = blockIdx.x;
-    const int din = 2 * A.F + 4;
     int32_t r, g, op;
-    const bool ok = dec_query(A, q, &r, &g, &op);
-    const int H = A.H, M = A.max_dev;
-    if (!ok) {
-        for (int h = tid; h < H; h += 256) {
-            A.db1q[(int64_t)q * H + h] = 0.f;
-            A.dw2q[(int64_t)q * H + h] = 0.f;
-            for (int o = 0; o < 4; ++o) A.doptq[((int64_t)q * 4 + o) * H + h] = 0.f;
-        }
-        for (int i = tid; i < M * H; i += 256) A.dTq[(int64_t)q * M * H + i] = 0.f;
+    if (!dec_query(A, q, &r, &g, &op)) {
+        for (int32_t a = tid; a < A.S; a += 256) A.ds[(int64_t)q * A.S + a] = 0.f;
         if (tid == 0) { A.loss_q[q] = 0.f; A.db2q[q] = 0.f; }
         return;
     }
-    const int32_t d0 = A.dev_off[g], nd = A.dev_off[g + 1] - d0;
-    const uint64_t keep = nd >= 64 ? ~0ull : ((1ull << nd) - 1ull);
-    const float *trow = A.t + ((int64_t)r * A.n_dev + d0) * H;
-    const float *vq = A.v + (int64_t)q * H;
-    // scores
-    {
-        float *tl = work;                       // [64][kDecH + 1]
-        float *po = work + 64 * (kDecH + 1);    // [4][kDecH]: W1_opt + b1 + v
-        float *w2c = po + 4 * kDecH;            // [kDecH]
-        for (int32_t a = tid; a < A.S; a += 256) sc[a] = A.b2[0];
-        for (int h0 = 0; h0 < H; h0 += kDecH) {
-            __syncthreads();
-            for (int i = tid; i < nd * kDecH; i += 256) {
-                const int j = i / kDecH, hh = i % kDecH;
-                tl[j * (kDecH + 1) + hh] = h0 + hh < H ? trow[(int64_t)j * H + h0 + hh] : 0.f;
-            }
-            for (int i = tid; i < 4 * kDecH; i += 256) {
-                const int o = i / kDecH, hh = i % kDecH, h = h0 + hh;
-                po[i] = h < H ? A.W1[(int64_t)h * din + 2 * A.F + o] + A.b1[h] + vq[h] : 0.f;
-            }
-            for (int i = tid; i < kDecH; i += 256) w2c[i] = h0 + i < H ? A.w2[h0 + i] : 0.f;
-            __syncthreads();
-            for (int32_t a = tid; a < A.S; a += 256) {
-                uint64_t m = A.mask[a] & keep;
-                const int opt = min((int)A.option[a], 3);
-                float acc[kDecH];
-#pragma unroll
-                for (int hh = 0; hh < kDecH; ++hh) acc[hh] = po[opt * kDecH + hh];
-                while (m) {
-                    const int j = __builtin_ctzll(m);
-                    m &= m - 1;
-#pragma unroll
-                    for (int hh = 0; hh < kDecH; ++hh) acc[hh] += tl[j * (kDecH + 1) + hh];
-                }
-                float s = 0.f;
-#pragma unroll
-                for (int hh = 0; hh < kDecH; ++hh) s = fmaf(w2c[hh], fmaxf(acc[hh], 0.f), s);
-                sc[a] += s;
-            }
-        }
-    }
+    const int H = A.H;
+    float *sc = sh, *vq = sh + A.S, *w2s = vq + H;
+    for (int h = tid; h < H; h += 256) { vq[h] = A.v[(int64_t)q * H + h]; w2s[h] = A.w2[h]; }
     __syncthreads();
-    // softmax, loss, dscore
+    const float *urg = A.u + ((int64_t)r * A.G + g) * H * A.S;
     float mx = -INFINITY;
-    for (int32_t a = tid; a < A.S; a += 256) mx = fmaxf(mx, sc[a]);
+    for (int32_t a = tid; a < A.S; a += 256) {
+        float s = 0.f;
+        int h = 0;
+        for (; h + 8 <= H; h += 8) {
+            float uu[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) uu[k] = urg[(int64_t)(h + k) * A.S + a];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) s = fmaf(w2s[h + k], fmaxf(uu[k] + vq[h + k], 0.f), s);
+        }
+        for (; h < H; ++h) s = fmaf(w2s[h], fmaxf(urg[(int64_t)h * A.S + a] + vq[h], 0.f), s);
+        s += A.b2[0];
+        sc[a] = s;
+        mx = fmaxf(mx, s);
+    }
     red[tid] = mx;
     __syncthreads();
     for (int o = 128; o > 0; o >>= 1) {
@@ -711,12 +733,11 @@ __global__ void __launch_bounds__(256) dec_train_query(DecTrain A) {
     }
     const float M0 = red[0];
     __syncthreads();
-    float z = 0.f, tt = 0.f, ts = 0.f;
     const float *tg = A.target + (int64_t)q * A.S;
+    float z = 0.f, tt = 0.f;
     for (int32_t a = tid; a < A.S; a += 256) {
         z += __expf(sc[a] - M0);
         tt += tg[a];
-        ts = fmaf(tg[a], sc[a] - M0, ts);
     }
     red[tid] = z;
     red2[tid] = tt;
@@ -726,180 +747,194 @@ __global__ void __launch_bounds__(256) dec_train_query(DecTrain A) {
         __syncthreads();
     }
     const float Z = red[0], T = red2[0];
-    __syncthreads();
-    red[tid] = ts;
-    __syncthreads();
-    for (int o = 128; o > 0; o >>= 1) {
-        if (tid < o) red[tid] += red[tid + o];
-        __syncthreads();
-    }
     const float logZ = __logf(Z);
-    if (tid == 0) A.loss_q[q] = -A.inv_q * (red[0] - T * logZ);
     __syncthreads();
-    float db2 = 0.f;
+    float lt = 0.f, db = 0.f;
     for (int32_t a = tid; a < A.S; a += 256) {
-        const float p = __expf(sc[a] - M0) / Z;
-        const float ds = A.inv_q * (p * T - tg[a]);
-        sc[a] = ds;
-        db2 += ds;
+        const float ls = sc[a] - M0 - logZ;          // log prior
+        const float d = A.inv_q * (__expf(ls) * T - tg[a]);
+        lt = fmaf(tg[a], ls, lt);
+        A.ds[(int64_t)q * A.S + a] = d;
+        db += d;
     }
-    red[tid] = db2;
+    red[tid] = lt;
+    red2[tid] = db;
     __syncthreads();
     for (int o = 128; o > 0; o >>= 1) {
-        if (tid < o) red[tid] += red[tid + o];
+        if (tid < o) { red[tid] += red[tid + o]; red2[tid] += red2[tid + o]; }
         __syncthreads();
     }
-    if (tid == 0) A.db2q[q] = red[0];
-    // gradients per chunk of hidden units
-    float *tl = work;                     // [64][kDecHB]
-    float *dT = work + 64 * kDecHB;       // [64][kDecHB]
-    const int hh = tid & (kDecHB - 1), jg = tid / kDecHB;
-    for (int h0 = 0; h0 < H; h0 += kDecHB) {
+    if (tid == 0) { A.loss_q[q] = -A.inv_q * red[0]; A.db2q[q] = red2[0]; }
+}
+
+constexpr int kDecHC = 32;    // hidden units per gradient block
+constexpr int kDecSC = 256;   // slices per LDS chunk
+
+// One block per (candidate graph, 32 hidden units); thread (hh, grp) walks
+// the graph's queries in order over its slices a = grp (mod 8) of each
+// 256-slice chunk, keeping D[a][h] in registers; then D goes through LDS
+// into dT[j][h] (thread owns j = grp (mod 8)) and the option sums.
+__global__ void __launch_bounds__(256) dec_grad(DecTrain A) {
+    __shared__ float buf[kDecSC * (kDecHC + 1)];      // u chunk [32][257], then D chunk [256][33]
+    __shared__ uint64_t mk[kDecSC];
+    __shared__ uint8_t op[kDecSC];
+    __shared__ float red[8][kDecHC];
+    const int tid = threadIdx.x, hh = tid & (kDecHC - 1), grp = tid >> 5;
+    const int nch = (A.H + kDecHC - 1) / kDecHC;
+    const int64_t rg = blockIdx.x / nch;
+    const int h0 = (int)(blockIdx.x % nch) * kDecHC, h = h0 + hh, H = A.H;
+    const bool live = h < H;
+    const int32_t r = (int32_t)(rg / A.G), g = (int32_t)(rg % A.G);
+    const int32_t d0 = A.dev_off[g], nd = A.dev_off[g + 1] - d0;
+    const uint64_t keep = nd >= 64 ? ~0ull : ((1ull << nd) - 1ull);
+    const int32_t nq = A.qcnt[rg];
+    const int32_t *list = A.qlist + A.qoff[rg];
+    const float w2h = live ? A.w2[h] : 0.f;
+    const float *urg = A.u + rg * H * A.S;
+    float dT[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    float dopt = 0.f, dw2 = 0.f;
+    for (int32_t a0 = 0; a0 < A.S; a0 += kDecSC) {
         __syncthreads();
-        for (int i = tid; i < nd * kDecHB; i += 256) {
-            const int j = i / kDecHB, c = i % kDecHB;
-            tl[i] = h0 + c < H ? trow[(int64_t)j * H + h0 + c] : 0.f;
-            dT[i] = 0.f;
+        for (int i = tid; i < kDecHC * kDecSC; i += 256) {
+            const int c = i / kDecSC, a = i % kDecSC;
+            buf[c * (kDecSC + 1) + a] = (h0 + c < H && a0 + a < A.S) ? urg[(int64_t)(h0 + c) * A.S + a0 + a] : 0.f;
         }
-        __syncthreads();
-        const int h = h0 + hh;
-        const bool live = h < H;
-        float base[4], w2h = 0.f;
-        for (int o = 0; o < 4; ++o) base[o] = live ? A.W1[(int64_t)h * din + 2 * A.F + o] + A.b1[h] + vq[h] : 0.f;
-        if (live) w2h = A.w2[h];
-        float gb1 = 0.f, gw2 = 0.f, gopt[4] = {0.f, 0.f, 0.f, 0.f};
-        for (int32_t a = 0; a < A.S; ++a) {
-            const uint64_t mall = A.mask[a] & keep;
-            const int opt = min((int)A.option[a], 3);
-            float pre = base[opt];
-            uint64_t m = mall;
-            while (m) {
-                const int j = __builtin_ctzll(m);
-                m &= m - 1;
-                pre += tl[j * kDecHB + hh];
-            }
-            const float ds = sc[a];
-            const float dp = pre > 0.f ? ds * w2h : 0.f;
-            if (jg == 0) {
-                gb1 += dp;
-                gw2 = fmaf(ds, fmaxf(pre, 0.f), gw2);
-                for (int o = 0; o < 4; ++o) gopt[o] += o == opt ? dp : 0.f;
-            }
-            // this thread's devices: j = jg (mod 4)
-            m = mall & (0x1111111111111111ull << jg);
-            while (m) {
-                const int j = __builtin_ctzll(m);
-                m &= m - 1;
-                dT[j * kDecHB + hh] += dp;
-            }
-        }
-        if (jg == 0 && live) {
-            A.db1q[(int64_t)q * H + h] = gb1;
-            A.dw2q[(int64_t)q * H + h] = gw2;
-            for (int o = 0; o < 4; ++o) A.doptq[((int64_t)q * 4 + o) * H + h] = gopt[o];
+        for (int a = tid; a < kDecSC; a += 256) {
+            mk[a] = a0 + a < A.S ? A.mask[a0 + a] & keep : 0ull;
+            op[a] = a0 + a < A.S ? (uint8_t)min((int)A.option[a0 + a], 3) : 4;
         }
         __syncthreads();
-        for (int i = tid; i < M * kDecHB; i += 256) {
-            const int j = i / kDecHB, c = i % kDecHB;
-            if (h0 + c < H) A.dTq[((int64_t)q * M + j) * H + h0 + c] = j < nd ? dT[i] : 0.f;
+        float D[kDecSC / 8];
+#pragma unroll
+        for (int i = 0; i < kDecSC / 8; ++i) D[i] = 0.f;
+        for (int32_t k = 0; k < nq; ++k) {
+            const int32_t q = list[k];
+            const float vqh = live ? A.v[(int64_t)q * H + h] : 0.f;
+            const float *dsq = A.ds + (int64_t)q * A.S + a0;
+            float dv = 0.f;
+#pragma unroll
+            for (int i = 0; i < kDecSC / 8; ++i) {
+                const int a = grp + 8 * i;
+                if (a0 + a < A.S) {
+                    const float pre = buf[hh * (kDecSC + 1) + a] + vqh;
+                    const float d = dsq[a];
+                    const float dp = pre > 0.f ? d * w2h : 0.f;
+                    D[i] += dp;
+                    dv += dp;
+                    dw2 = fmaf(d, fmaxf(pre, 0.f), dw2);
+                }
+            }
+            red[grp][hh] = dv;
+            __syncthreads();
+            if (grp == 0 && live) {
+                float sum = 0.f;
+                for (int gg = 0; gg < 8; ++gg) sum += red[gg][hh];
+                float *o = A.dvq + (int64_t)q * H + h;
+                *o = a0 == 0 ? sum : *o + sum;
+            }
+            __syncthreads();
         }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < kDecSC / 8; ++i) buf[(grp + 8 * i) * (kDecHC + 1) + hh] = D[i];
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int j = grp + 8 * i;
+            if (j >= nd) continue;
+            float sum = 0.f;
+            for (int a = 0; a < kDecSC; ++a)
+                if ((mk[a] >> j) & 1ull) sum += buf[a * (kDecHC + 1) + hh];
+            dT[i] += sum;
+        }
+        if (grp < 4) {
+            float sum = 0.f;
+            for (int a = 0; a < kDecSC; ++a)
+                if (op[a] == grp) sum += buf[a * (kDecHC + 1) + hh];
+            dopt += sum;
+        }
+    }
+    if (live) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int j = grp + 8 * i;
+            if (j < nd) A.dT[((int64_t)r * A.n_dev + d0 + j) * H + h] = dT[i];
+        }
+        if (grp < 4) A.dopt_part[(rg * 4 + grp) * H + h] = dopt;
+    }
+    __syncthreads();
+    red[grp][hh] = dw2;
+    __syncthreads();
+    if (grp == 0 && live) {
+        float sum = 0.f;
+        for (int gg = 0; gg < 8; ++gg) sum += red[gg][hh];
+        A.dw2_part[rg * H + h] = sum;
     }
 }
 
-// decoder parameter gradients, one thread per (h, column of W1):
-//   W1_dev: sum_q sum_j dT_q[j] E_dev[row(q, j)];  W1_op: sum_q db1_q E_op[row(q)];
-//   W1_opt: sum_q dopt_q;  b1, w2, b2: sums over queries
-__global__ void dec_train_params(DecTrain A) {
-    const int din = 2 * A.F + 4, H = A.H, F = A.F;
-    const int64_t total = (int64_t)H * din;
+// rows of E_op read by the queries (zero rows for invalid ones)
+__global__ void dec_gather_rows(const float *E_op, const int32_t *qrow, int32_t Q, int F, float *Eq) {
+    const int64_t total = (int64_t)Q * F;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-        const int h = (int)(i / din), col = (int)(i % din);
-        float s = 0.f;
-        if (col < F) {
-            for (int32_t q = 0; q < A.Q; ++q) {
-                if (A.qrow[q] < 0) continue;
-                const int32_t r = A.q_rep[q], g = A.q_graph[q];
-                const int32_t d0 = A.dev_off[g], nd = A.dev_off[g + 1] - d0;
-                for (int j = 0; j < nd; ++j)
-                    s = fmaf(A.dTq[((int64_t)q * A.max_dev + j) * H + h],
-                             A.E_dev[((int64_t)r * A.n_dev + d0 + j) * F + col], s);
-            }
-        } else if (col < 2 * F) {
-            for (int32_t q = 0; q < A.Q; ++q) {
-                if (A.qrow[q] < 0) continue;
-                s = fmaf(A.db1q[(int64_t)q * H + h], A.E_op[(int64_t)A.qrow[q] * F + col - F], s);
-            }
-        } else {
-            for (int32_t q = 0; q < A.Q; ++q) s += A.doptq[((int64_t)q * 4 + col - 2 * F) * H + h];
-        }
-        A.g_w1[i] = s;
-        if (col == 0) {
-            float b1 = 0.f, w2 = 0.f;
-            for (int32_t q = 0; q < A.Q; ++q) {
-                b1 += A.db1q[(int64_t)q * H + h];
-                w2 += A.dw2q[(int64_t)q * H + h];
-            }
-            A.g_b1[h] = b1;
-            A.g_w2[h] = w2;
-            if (h == 0) {
-                float b2 = 0.f;
-                for (int32_t q = 0; q < A.Q; ++q) b2 += A.db2q[q];
-                A.g_b2[0] = b2;
-            }
-        }
+        const int32_t row = qrow[i / F];
+        Eq[i] = row >= 0 ? E_op[(int64_t)row * F + i % F] : 0.f;
     }
 }
 
-// dE_dev rows: sum over the queries of the row's candidate graph of W1_dev^T dT_q[j]
-__global__ void dec_train_grad_dev(DecTrain A) {
-    const int din = 2 * A.F + 4, H = A.H, F = A.F;
-    const int64_t total = (int64_t)A.R * A.n_dev * F;
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t row = i / F;
-        const int c = (int)(i % F);
-        const int32_t r = (int32_t)(row / A.n_dev), d = (int32_t)(row % A.n_dev);
-        int32_t g = 0;
-        while (g + 1 < A.G && A.dev_off[g + 1] <= d) ++g;
-        const int j = d - A.dev_off[g];
+// dE_op rows of the queries: the first query of each row sums, in query
+// order, the dE rows of every query reading that row
+__global__ void dec_grad_op(const int32_t *qrow, int32_t Q, int F, const float *dEq, float *g_op) {
+    const int32_t q = blockIdx.x;
+    const int32_t row = qrow[q];
+    if (row < 0) return;
+    for (int32_t p = 0; p < q; ++p)
+        if (qrow[p] == row) return;
+    for (int c = threadIdx.x; c < F; c += blockDim.x) {
         float s = 0.f;
-        for (int32_t q = 0; q < A.Q; ++q) {
-            if (A.qrow[q] < 0 || A.q_rep[q] != r || A.q_graph[q] != g) continue;
-            const float *dt = A.dTq + ((int64_t)q * A.max_dev + j) * H;
-            for (int h = 0; h < H; ++h) s = fmaf(dt[h], A.W1[(int64_t)h * din + c], s);
-        }
-        A.g_dev[i] = s;
+        for (int32_t p = q; p < Q; ++p)
+            if (qrow[p] == row) s += dEq[(int64_t)p * F + c];
+        g_op[(int64_t)row * F + c] = s;
     }
+}
+
+// decoder parameter sums over candidate graphs (W1 option columns, b1, w2)
+__global__ void dec_params(DecTrain A, float *g_w1, float *g_b1, float *g_w2) {
+    const int din = 2 * A.F + 4, H = A.H;
+    for (int h = blockIdx.x * blockDim.x + threadIdx.x; h < H; h += gridDim.x * blockDim.x) {
+        float o4[4] = {0.f, 0.f, 0.f, 0.f}, w2 = 0.f;
+        for (int32_t rg = 0; rg < A.RG; ++rg) {
+            for (int o = 0; o < 4; ++o) o4[o] += A.dopt_part[((int64_t)rg * 4 + o) * H + h];
+            w2 += A.dw2_part[(int64_t)rg * H + h];
+        }
+        float b1 = 0.f;
+        for (int o = 0; o < 4; ++o) {
+            g_w1[(int64_t)h * din + 2 * A.F + o] = o4[o];
+            b1 += o4[o];
+        }
+        g_b1[h] = b1;
+        g_w2[h] = w2;
+    }
+}
+
+// loss and output-bias gradient: fixed-order block sums over the queries
+__global__ void __launch_bounds__(256) dec_totals(const float *loss_q, const float *db2q, int32_t Q, float *loss,
+                                                  float *g_b2) {
+    __shared__ float r1[256], r2[256];
+    const int t = threadIdx.x;
+    float a = 0.f, b = 0.f;
+    for (int32_t q = t; q < Q; q += 256) { a += loss_q[q]; b += db2q[q]; }
+    r1[t] = a;
+    r2[t] = b;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if (t < o) { r1[t] += r1[t + o]; r2[t] += r2[t + o]; }
+        __syncthreads();
+    }
+    if (t == 0) { loss[0] = r1[0]; g_b2[0] = r2[0]; }
 }
 
 __global__ void fill_zero(float *p, int64_t n) {
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) p[i] = 0.f;
-}
-
-// dE_op rows of the queries: the first query of each row sums, in query
-// order, W1_op^T db1 of every query reading that row
-__global__ void dec_train_grad_op(DecTrain A) {
-    const int32_t q = blockIdx.x;
-    const int32_t row = A.qrow[q];
-    if (row < 0) return;
-    for (int32_t p = 0; p < q; ++p)
-        if (A.qrow[p] == row) return;
-    const int din = 2 * A.F + 4, H = A.H, F = A.F;
-    for (int c = threadIdx.x; c < F; c += blockDim.x) {
-        float s = 0.f;
-        for (int32_t p = q; p < A.Q; ++p) {
-            if (A.qrow[p] != row) continue;
-            for (int h = 0; h < H; ++h) s = fmaf(A.db1q[(int64_t)p * H + h], A.W1[(int64_t)h * din + F + c], s);
-        }
-        A.g_op[(int64_t)row * F + c] = s;
-    }
-}
-
-__global__ void dec_train_loss(const float *loss_q, int32_t Q, float *loss) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        float s = 0.f;
-        for (int32_t q = 0; q < Q; ++q) s += loss_q[q];
-        loss[0] = s;
-    }
 }
 
 // ------------------------------------------------------------------ update
@@ -932,8 +967,8 @@ struct TrainLayout {
     float *dU, *dcp;
     float *P0, *P1;
     // decoder
-    float *t, *v, *loss_q, *db1q, *dw2q, *doptq, *db2q, *dTq;
-    int32_t *qrow;
+    float *t, *u, *v, *ds, *loss_q, *db2q, *dvq, *dT, *dopt_part, *dw2_part, *Eq, *dEq;
+    int32_t *qrow, *qcnt, *qoff, *qlist;
 };
 
 int32_t chunks_of(int32_t max_degree, int per) { return std::max<int32_t>(1, (max_degree + per - 1) / per); }
@@ -947,7 +982,7 @@ int32_t persist_blocks(int64_t items) {
 }
 
 // size of the split-K partials of every weight gradient
-int64_t split_floats(const tag_graph *g, const tag_model_dims *d, int32_t R) {
+int64_t split_floats(const tag_graph *g, const tag_model_dims *d, int32_t R, int32_t Q) {
     const int64_t F = d->f;
     auto one = [&](int64_t M, int64_t N, int64_t K) {
         int64_t s;
@@ -958,6 +993,9 @@ int64_t split_floats(const tag_graph *g, const tag_model_dims *d, int32_t R) {
     m = std::max(m, one(2 * F, F, (int64_t)R * g->n_dev));
     m = std::max(m, one(F, d->f_op + 1, (int64_t)R * g->n_op));
     m = std::max(m, one(F, d->f_dev + 1, (int64_t)R * g->n_dev));
+    const int64_t H = std::max(d->dec_hidden, 1);
+    m = std::max(m, one(H, F, (int64_t)R * g->n_dev));
+    m = std::max(m, one(H, F, std::max(Q, 1)));
     return m;
 }
 
@@ -1004,20 +1042,26 @@ size_t carve_train(const tag_graph *g, const tag_model_dims *d, int32_t R, int32
     }
     L->dU = c.take<float>((size_t)d->layers * 3 * F * 2);
     L->dcp = c.take<float>((size_t)d->layers * 3 * F);
-    const int64_t sp = split_floats(g, d, R);
+    const int64_t sp = split_floats(g, d, R, Q);
     L->P0 = c.take<float>(sp);
     L->P1 = c.take<float>(sp);
-    const int64_t H = std::max(d->dec_hidden, 1), Qm = std::max(Q, 1);
+    const int64_t H = std::max(d->dec_hidden, 1), Qm = std::max(Q, 1), RG = (int64_t)R * g->G;
     L->t = c.take<float>(rd * H);
+    L->u = c.take<float>(RG * H * S);
     L->v = c.take<float>(Qm * H);
+    L->ds = c.take<float>(Qm * S);
     L->loss_q = c.take<float>(Qm);
-    L->db1q = c.take<float>(Qm * H);
-    L->dw2q = c.take<float>(Qm * H);
-    L->doptq = c.take<float>(Qm * 4 * H);
     L->db2q = c.take<float>(Qm);
-    L->dTq = c.take<float>(Qm * std::max(g->max_dev, 1) * H);
+    L->dvq = c.take<float>(Qm * H);
+    L->dT = c.take<float>(rd * H);
+    L->dopt_part = c.take<float>(RG * 4 * H);
+    L->dw2_part = c.take<float>(RG * H);
+    L->Eq = c.take<float>(Qm * F);
+    L->dEq = c.take<float>(Qm * F);
     L->qrow = c.take<int32_t>(Qm);
-    (void)S;
+    L->qcnt = c.take<int32_t>(RG);
+    L->qoff = c.take<int32_t>(RG + 1);
+    L->qlist = c.take<int32_t>(Qm);
     return c.used;
 }
 
@@ -1025,14 +1069,23 @@ template <int F, int K>
 void launch_layer_bwd(const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], const ParamReduce &pr, hipStream_t st) {
     for (int b = 0; b < 4; ++b) {
         const int64_t waves = (int64_t)P.R * B[b].n_dst * B[b].chunks;
-        if (waves > 0) bwd_scores<F, K><<<(unsigned)((waves + 3) / 4), 256, 0, st>>>(P, B[b]);
+        if (waves <= 0) continue;
+        prof_begin(TAG_STAGE_BWD_SCORES, st);
+        bwd_scores<F, K><<<(unsigned)((waves + 3) / 4), 256, 0, st>>>(P, B[b]);
+        prof_end(TAG_STAGE_BWD_SCORES, st);
     }
-    for (int b = 0; b < 4; ++b) bwd_softmax<F, K><<<pr.nb_a[b], 256, 0, st>>>(P, B[b], const_cast<float *>(pr.pa[b]));
+    for (int b = 0; b < 4; ++b) {
+        prof_begin(TAG_STAGE_BWD_SOFTMAX, st);
+        bwd_softmax<F, K><<<pr.nb_a[b], 256, 0, st>>>(P, B[b], const_cast<float *>(pr.pa[b]));
+        prof_end(TAG_STAGE_BWD_SOFTMAX, st);
+    }
     for (int s = 0; s < 4; ++s) {
+        prof_begin(TAG_STAGE_BWD_MESSAGES, st);
         bwd_messages<F, K><<<pr.nb_m[s], 256, 0, st>>>(P, S[s], const_cast<float *>(pr.pm[s]));
+        prof_end(TAG_STAGE_BWD_MESSAGES, st);
         if (S[s].chunks > 1) bwd_combine<<<grid_for((int64_t)P.R * S[s].n_self * F), 256, 0, st>>>(P, S[s], K);
     }
-    bwd_params<<<15, 256, 0, st>>>(pr);
+    bwd_params<<<15 * ((F + 15) / 16), 256, 0, st>>>(pr);
 }
 
 template <int F>
@@ -1127,30 +1180,44 @@ extern "C" tag_status tag_train_step(const tag_graph *g, const tag_model_dims *d
 
     // decoder: loss, its parameter gradients and dE
     DecTrain D{};
-    D.R = R; D.G = g->G; D.S = S; D.Q = Q; D.F = F; D.H = H; D.max_dev = std::max(g->max_dev, 1);
+    D.R = R; D.G = g->G; D.S = S; D.Q = Q; D.F = F; D.H = H; D.RG = R * g->G;
     D.n_op = g->n_op; D.n_dev = g->n_dev;
     D.op_off = g->op_off_d; D.dev_off = g->dev_off_d;
-    D.E_op = L.E_op; D.E_dev = L.E_dev;
     D.mask = slices->mask; D.option = slices->option;
-    D.W1 = w->dec_w1; D.b1 = w->dec_b1; D.w2 = w->dec_w2; D.b2 = w->dec_b2;
+    D.w2 = w->dec_w2; D.b2 = w->dec_b2;
     D.q_rep = batch->query_rep; D.q_graph = batch->query_graph; D.q_op = batch->query_op;
     D.target = batch->target;
-    D.t = L.t; D.v = L.v; D.qrow = L.qrow;
+    D.u = L.u; D.v = L.v; D.qrow = L.qrow;
+    D.qcnt = L.qcnt; D.qoff = L.qoff; D.qlist = L.qlist;
     D.inv_q = 1.f / (float)Q;
-    D.loss_q = L.loss_q; D.db1q = L.db1q; D.dw2q = L.dw2q; D.doptq = L.doptq; D.db2q = L.db2q; D.dTq = L.dTq;
-    D.g_op = L.G_op; D.g_dev = L.G_dev;
-    D.g_w1 = gr->dec_w1; D.g_b1 = gr->dec_b1; D.g_w2 = gr->dec_w2; D.g_b2 = gr->dec_b2;
+    D.ds = L.ds; D.loss_q = L.loss_q; D.db2q = L.db2q; D.dvq = L.dvq; D.dT = L.dT;
+    D.dopt_part = L.dopt_part; D.dw2_part = L.dw2_part;
     const int din = 2 * F + 4;
+    const int64_t RG = (int64_t)R * g->G;
+    prof_begin(TAG_STAGE_BWD_DECODER, stream);
     launch_small_gemm(SmallGemm{L.E_dev, F, rd, nullptr, F, w->dec_w1, din, H, nullptr, 0, L.t, H, 0}, stream);
     dec_rows<<<grid_for(Q), 256, 0, stream>>>(D);
     launch_small_gemm(SmallGemm{L.E_op, F, Q, L.qrow, F, w->dec_w1 + F, din, H, nullptr, 0, L.v, H, 0}, stream);
-    const size_t dec_sh = sizeof(float) * (S + std::max(64 * (kDecH + 1) + 5 * kDecH, 2 * 64 * kDecHB));
-    dec_train_query<<<Q, 256, dec_sh, stream>>>(D);
-    dec_train_loss<<<1, 64, 0, stream>>>(L.loss_q, Q, loss);
-    dec_train_params<<<grid_for((int64_t)H * din), 256, 0, stream>>>(D);
-    dec_train_grad_dev<<<grid_for(rd * F), 256, 0, stream>>>(D);
+    launch_slice_terms(R, g->G, S, F, H, g->n_dev, g->dev_off_d, L.t, w->dec_w1, w->dec_b1, slices->mask,
+                       slices->option, L.u, stream);
+    dec_count<<<grid_for(RG), 256, 0, stream>>>(D, 0);
+    dec_scan<<<1, 256, 0, stream>>>(D);
+    dec_count<<<grid_for(RG), 256, 0, stream>>>(D, 1);
+    dec_scores<<<Q, 256, sizeof(float) * (S + 2 * H), stream>>>(D);
+    fill_zero<<<grid_for((int64_t)Q * H), 256, 0, stream>>>(L.dvq, (int64_t)Q * H);
+    dec_grad<<<(unsigned)(RG * ((H + kDecHC - 1) / kDecHC)), 256, 0, stream>>>(D);
+    dec_totals<<<1, 256, 0, stream>>>(L.loss_q, L.db2q, Q, loss, gr->dec_b2);
+    dec_params<<<grid_for(H), 256, 0, stream>>>(D, gr->dec_w1, gr->dec_b1, gr->dec_w2);
+    // device side: dE_dev = dT W1_dev, dW1_dev = dT^T E_dev
+    launch_gemm(Gemm{L.dT, H, w->dec_w1, din, rd, F, H, -1, L.G_dev, F, 0, H, 0}, true, false, 1, stream);
+    weight_grad(L.dT, H, L.E_dev, F, H, F, false, rd, L.P0, gr->dec_w1, din, nullptr, 0, stream);
+    // op side: dE_op rows of the queries = dv W1_op, dW1_op = dv^T E_op[query rows]
+    dec_gather_rows<<<grid_for((int64_t)Q * F), 256, 0, stream>>>(L.E_op, L.qrow, Q, F, L.Eq);
+    weight_grad(L.dvq, H, L.Eq, F, H, F, false, Q, L.P1, gr->dec_w1 + F, din, nullptr, 0, stream);
+    launch_gemm(Gemm{L.dvq, H, w->dec_w1 + F, din, Q, F, H, -1, L.dEq, F, 0, H, 0}, true, false, 1, stream);
     fill_zero<<<grid_for(ro * F), 256, 0, stream>>>(L.G_op, ro * F);
-    dec_train_grad_op<<<Q, 256, 0, stream>>>(D);
+    dec_grad_op<<<Q, 256, 0, stream>>>(L.qrow, Q, F, L.dEq, L.G_op);
+    prof_end(TAG_STAGE_BWD_DECODER, stream);
 
     // layers, last to first
     BwdLayer P{};
@@ -1200,12 +1267,15 @@ extern "C" tag_status tag_train_step(const tag_graph *g, const tag_model_dims *d
         const float *Wl = w->layer_w + (size_t)l * 3 * F * 2 * F;
         float *gW = gr->layer_w + (size_t)l * 3 * F * 2 * F;
         // dW^h: op side rows [oo ; od], device side rows [od ; dd]
-        weight_grad(L.dY_op, 2 * F, L.H_op[l], F, 2 * F, F, false, ro, L.P0, gW, 2 * F, nullptr, 0, stream);
+        weight_grad(L.dY_op, 2 * F, L.H_op[l], F, 2 * F, F, false, ro, L.P0, gW, 2 * F, nullptr, 0, stream,
+                    TAG_STAGE_BWD_DW);
         {
             int64_t splits;
             const int64_t per = split_k_per(rd, ((2 * F + GM - 1) / GM) * ((F + GN - 1) / GN), &splits);
             Gemm gd{L.dY_dev, 2 * F, L.H_dev[l], F, 2 * F, F, rd, -1, L.P1, F, 2 * F * F, per, 0};
+            prof_begin(TAG_STAGE_BWD_DW, stream);
             launch_gemm(gd, false, false, splits, stream);
+            prof_end(TAG_STAGE_BWD_DW, stream);
             float *g1 = gW + (size_t)F * 2 * F;
             sum_splits<<<grid_for((int64_t)F * F), 256, 0, stream>>>(L.P1, 2 * F * F, F, (int32_t)splits, F, F, g1,
                                                                     2 * F, 1);
@@ -1214,9 +1284,13 @@ extern "C" tag_status tag_train_step(const tag_graph *g, const tag_model_dims *d
                                                                     2 * F, 0);
         }
         // dH = dY [W^h ; W^h'] (overwrites the layer-output gradients, no longer needed)
+        prof_begin(TAG_STAGE_BWD_DH, stream);
         launch_gemm(Gemm{L.dY_op, 2 * F, Wl, 2 * F, ro, F, 2 * F, -1, L.G_op, F, 0, 2 * F, 0}, true, false, 1, stream);
+        prof_end(TAG_STAGE_BWD_DH, stream);
+        prof_begin(TAG_STAGE_BWD_DH, stream);
         launch_gemm(Gemm{L.dY_dev, 2 * F, Wl + (size_t)F * 2 * F, 2 * F, rd, F, 2 * F, -1, L.G_dev, F, 0, 2 * F, 0},
                     true, false, 1, stream);
+        prof_end(TAG_STAGE_BWD_DH, stream);
     }
 
     // node encoders: h0 = ReLU(A x + c)
@@ -1232,7 +1306,7 @@ extern "C" tag_status tag_train_step(const tag_graph *g, const tag_model_dims *d
                {gr->enc_edge_w[0], gr->enc_edge_w[1], gr->enc_edge_w[2]},
                {gr->enc_edge_b[0], gr->enc_edge_b[1], gr->enc_edge_b[2]}, F, NL};
     fold_bwd_we<<<grid_for((int64_t)NL * 3 * F * F), 256, 0, stream>>>(fb);
-    fold_bwd_enc<<<3, 256, 0, stream>>>(fb);
+    fold_bwd_enc<<<3 * ((F + 63) / 64), 256, 0, stream>>>(fb);
 
     if (lr > 0.f) {
         SgdList sl{};

@@ -41,7 +41,7 @@ class TrainCase:
     """R candidates of each of the topologies (candidate (r, g) uses
     topology g), Q_per queries per candidate, random targets."""
 
-    def __init__(self, topos, R, f, heads, layers, S, Q_per, seed, f_op=40, invalid=0):
+    def __init__(self, topos, R, f, heads, layers, S, Q_per, seed, f_op=40, invalid=0, dup=False):
         self.topos, self.R, self.f, self.heads, self.layers = topos, R, f, heads, layers
         self.f_op = f_op
         self.w = synth.make_weights(f, heads, layers, f_op, f, bias_scale=0.3, seed_extra=seed)
@@ -61,6 +61,8 @@ class TrainCase:
                          x_dd=rng.uniform(-1, 1, (t.e_dd, 2)).astype(np.float32),
                          x_od=rng.integers(0, 2, t.e_od).astype(np.uint8),
                          query_op=rng.integers(0, t.n_op, size=Q_per).astype(np.int32))
+                if dup:                   # two queries of one candidate read the same op row
+                    x["query_op"][-1] = x["query_op"][0]
                 tt = rng.random((Q_per, S)) ** 3
                 x["target"] = tt / tt.sum(1, keepdims=True)
                 feats.append(x)
@@ -131,7 +133,7 @@ def test_train_step_matches_reference_union_of_topologies(torch, f, heads, layer
     topos = [synth.random_topology(21, 300, 5, 500, od_per_op=3, dd_density=0.7),
              synth.random_topology(22, 40, 9, 70)]
     _say(f"[train] union f={f} K={heads} L={layers}")
-    c = TrainCase(topos, 2, f, heads, layers, 24, 2, seed=f + heads)
+    c = TrainCase(topos, 2, f, heads, layers, 24, 3, seed=f + heads, dup=True)
     graph, model, tr, feats = c.trainer(torch)
     loss = float(tr.step(feats).cpu()[0])
     ref_loss, ref_g = c.reference()
