@@ -155,7 +155,7 @@ def search_bench(args) -> int:
     sp = synth.make_search_problem(name)
     w = synth.make_weights(wl.f, wl.heads, wl.layers, wl.f_op, wl.f)
     model = P.Model(w, f=wl.f, heads=wl.heads, layers=wl.layers, f_op=wl.f_op, dtype=wl.dtype, device="cuda:0")
-    prob = PS.SearchProblem(sp, f_op=wl.f_op)
+    prob = PS.SearchProblem(sp, f_op=wl.f_op, model=args.reward)
     svc = PS.SearchService(prob, sp, model, B)
     tree = PS.Mcts(sp.n_groups, len(sp.masks), args.c_puct, 0.0)
     print(f"[bench] search on {name}: B={B} groups={sp.n_groups} slices={len(sp.masks)}; warmup {args.warmup}",
@@ -189,13 +189,67 @@ def search_bench(args) -> int:
         "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
         "config": {"workload": name, "leaves_per_round": B, "groups": sp.n_groups, "slices": len(sp.masks),
                    "n_op": sp.topo.n_op, "n_dev": sp.topo.n_dev, "f": wl.f, "layers": wl.layers,
-                   "c_puct": args.c_puct, "parallelism": "none"},
+                   "c_puct": args.c_puct, "reward_model": args.reward, "parallelism": "none"},
         "sequential_ms_per_round": round(seq_el * 1e3 / seq_rounds, 4),
         "sequential_tree_ms_per_round": round(host_s * 1e3 / seq_rounds, 4),
         "tree_vertices": v, "expanded": e, "best_reward": best,
     }
     print(json.dumps(out), flush=True)
     svc.close()
+    return 0
+
+
+def sim_bench(args) -> int:
+    """Host simulator (Section 4.3.2): iterations simulated per second for
+    random complete strategies of the workload's search problem, on
+    --sim-threads host threads.  No GPU work: the line carries no roofline."""
+    import paper_2302_06126_amd.search as PS
+
+    name = args.workload
+    sp = synth.make_search_problem(name)
+    prob = PS.SearchProblem(sp)
+    K, S = sp.n_groups, len(sp.masks)
+    rng = synth.rng_for(synth.WORKLOADS[name].cfg_id, 5_000_000)
+    B = args.sim_batch
+    depth = np.full(B, K, np.int32)
+    path = rng.integers(0, S, size=(B, K)).astype(np.int32)
+    print(f"[bench] simulator on {name}: {B} strategies per step, {args.sim_threads} threads; warmup {args.warmup}",
+          file=sys.stderr, flush=True)
+    for _ in range(max(args.warmup, 1)):
+        prob.simulate_batch(depth, path, args.sim_threads)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        T, oom = prob.simulate_batch(depth, path, args.sim_threads)
+    el = time.perf_counter() - t0
+    tasks = prob.simulate(path[0].tolist())["n_tasks"]
+    out = {
+        "metric": "simulated training iterations/sec (host simulator, random complete strategies)",
+        "value": round(B * args.steps / el, 2), "unit": "simulations/s", "n_gpus": 0, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(el * 1e3 / args.steps, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": name, "strategies_per_step": B, "threads": args.sim_threads, "n_op": sp.topo.n_op,
+                   "n_dev": sp.topo.n_dev, "groups": K, "tasks_first_strategy": tasks, "parallelism": "host threads"},
+        "oom_share": round(float(oom.mean()), 4),
+        "roofline": None,
+    }
+    if not args.no_cpu_baseline:
+        from oracle import search as OSR
+        from oracle import simulate as SIM
+        P = SIM.SimProblem(sp)
+        order = OSR.Problem(sp).order
+        t0 = time.perf_counter()
+        n = 0
+        while n < B:
+            SIM.simulate(P, SIM.strategy_of(sp, path[n].tolist(), order))
+            n += 1
+            if time.perf_counter() - t0 >= args.cpu_seconds:
+                break
+        cel = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round(n / cel, 3), "unit": "simulations/s", "cores": 1, "kind": "oracle",
+                               "sample": f"{n} of the {B} strategies, the reference simulator, one thread, "
+                                         f"{cel:.1f} s", "cpu": cpu_model()}
+    print(json.dumps(out), flush=True)
+    prob.close()
     return 0
 
 
@@ -360,9 +414,13 @@ def main() -> int:
                     help="run one plain device copy of this size first (counter calibration)")
     ap.add_argument("--stage", default="auto", choices=["auto"] + list(KERNEL_NAMES),
                     help="kernel stage timed for the roofline (auto: the longest one)")
-    ap.add_argument("--mode", default="forward", choices=["forward", "search", "train"],
+    ap.add_argument("--mode", default="forward", choices=["forward", "search", "train", "sim"],
                     help="forward: the GNN hot path (default line); search: batched PUCT search rounds; "
-                         "train: the GNN training step")
+                         "train: the GNN training step; sim: the host simulator")
+    ap.add_argument("--reward", default="analytic", choices=["analytic", "simulator"],
+                    help="search mode: reward and runtime-feedback model")
+    ap.add_argument("--sim-batch", type=int, default=512, help="sim mode: strategies per step")
+    ap.add_argument("--sim-threads", type=int, default=16, help="sim mode: host threads")
     ap.add_argument("--search-batch", type=int, default=0, help="leaves per search round (default: the batch)")
     ap.add_argument("--c-puct", type=float, default=1.5)
     args = ap.parse_args()
@@ -375,6 +433,8 @@ def main() -> int:
         return search_bench(args)
     if args.mode == "train":
         return train_bench(args)
+    if args.mode == "sim":
+        return sim_bench(args)
 
     import torch
 

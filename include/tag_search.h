@@ -104,6 +104,21 @@ tag_status tag_search_order(const tag_search_problem *p, int32_t *order /*[n_gro
 tag_status tag_search_evaluate(const tag_search_problem *p, const int32_t *path, int32_t depth,
                                double *reward, double *iter_time, int32_t *oom);
 
+/* Reward and runtime-feedback model: 0 (the default) the analytic model
+ * above; 1 the simulator (tag_simulate below).  The model gives the reward
+ * (baseline time over iteration time, recomputed for the baseline when the
+ * model changes) and the runtime feedback that tag_search_pack writes into
+ * the state records (op features: log10 of the group's makespan in ms and
+ * its idle share; device features: memory share and idle share):
+ *   analytic:  makespan = slowest replica's compute, idle share = sync /
+ *              (compute + sync), memory = the modelled use, device idle =
+ *              1 - load / time
+ *   simulator: the simulated group makespan, group idle before its output
+ *              transfers / iteration time, peak memory / capacity (both
+ *              memory shares capped at 1) and device idle share.
+ * TAG_EINVAL for another value or a tensor graph with a cycle (simulator). */
+tag_status tag_search_set_model(tag_search_problem *p, int32_t model);
+
 /* ---- search tree -------------------------------------------------------- */
 
 /* n_levels = number of groups, n_actions = number of slices (<= 4096),
@@ -202,6 +217,63 @@ tag_status tag_search_run_workspace(const tag_search_problem *p, const tag_graph
  * non-OK status the stream has been drained, and the tree may still hold
  * the in-flight visits of rounds that were selected but not updated. */
 tag_status tag_search_run(const tag_search_run_args *a, void *hip_stream);
+
+/* ---- simulator (Section 4.3.2, with the auxiliary ops of Section 4.3.1) -- */
+
+/*
+ * Simulates one training iteration of a strategy and reports the runtime
+ * feedback the GNN takes as input (Section 4.2.1: group makespan, idle time
+ * before a group's output transfers, device peak memory and idle share,
+ * link idle share).  Readings of the paper:
+ *  - Every op takes its group's device set D (r = |D|) and option.  Compute
+ *    task per device j of D: FLOPs / speed_j (duplicate or r = 1), else
+ *    FLOPs / (r speed_j).
+ *  - Model parallel, r > 1: a gather task per device after all partitions,
+ *    (r - 1) / r out_bytes / min bandwidth inside D; consumers read its output.
+ *  - Options 0 / 1, r > 1, parameters > 0: a sync task per device after all
+ *    replicas, 2 (r - 1) / r params / (min bandwidth inside D for AllReduce,
+ *    min bandwidth from D's first device for the parameter server).
+ *  - Tensor p -> c, device j of c: local when j holds p; else a transfer
+ *    from p's device with the highest bandwidth to j (first maximum) on that
+ *    link, out_bytes(p) / r_c bytes when c splits its batch (options 0, 1),
+ *    the whole tensor otherwise, taking bytes / bandwidth.
+ *  - One FIFO queue per device and per device pair.  Tasks are numbered per
+ *    op (compute tasks in device order, gathers, syncs), then per tensor in
+ *    input order (transfers in device order); completions are processed by
+ *    (finish time, task number), the tasks they make ready enter their
+ *    queues in task-number order, an idle resource starts at once.
+ *  - Memory: 4 x parameters resident on every device of D (divided by r for
+ *    model parallel); a task's output (compute: out_bytes, or out_bytes / r
+ *    when split; gather: out_bytes; transfer: its bytes) is allocated when
+ *    it finishes, then its inputs are released; a tensor is freed after its
+ *    last use (a tensor without uses at once).
+ *  - Outputs: iteration time = last finish; group makespan = last finish of
+ *    its compute / gather / sync tasks - first start of its compute tasks;
+ *    group idle = mean over transfers to another group's op of transfer
+ *    start - producer finish (0 without); idle share = 1 - busy / time; OOM
+ *    when a peak exceeds the device memory.
+ * It needs no GPU.
+ */
+typedef struct tag_sim_out {
+    double iter_time;          /* seconds; +inf for an invalid strategy          */
+    int32_t valid;             /* 0: a group's device set is empty               */
+    int32_t oom;               /* 1 when out of memory (or invalid)              */
+    int64_t n_tasks;
+    double *group_makespan;    /* HOST [n_groups] seconds, or NULL               */
+    double *group_idle;        /* HOST [n_groups] seconds, or NULL               */
+    double *dev_peak;          /* HOST [n_dev] bytes, or NULL                    */
+    double *dev_idle;          /* HOST [n_dev] share of the iteration, or NULL   */
+    double *link_idle;         /* HOST [e_dd] share, links in input order, or NULL */
+} tag_sim_out;
+
+/* Simulate the strategy path[0..depth) completed as in tag_search_evaluate.
+ * TAG_EINVAL if the tensor graph has a cycle. */
+tag_status tag_simulate(const tag_search_problem *p, const int32_t *path, int32_t depth, tag_sim_out *out);
+
+/* B strategies (depth[b], path + b * path_stride) on n_threads host threads
+ * (1..256): iteration times and OOM flags (HOST arrays [B]). */
+tag_status tag_simulate_batch(const tag_search_problem *p, int32_t B, const int32_t *depth, const int32_t *path,
+                              int32_t path_stride, int32_t n_threads, double *iter_time, int32_t *oom);
 
 #ifdef __cplusplus
 }

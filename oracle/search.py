@@ -33,7 +33,8 @@ Pieces and the readings they take where the paper is silent:
 
 Feature encoding of a search state for the GNN follows the op / device /
 placement-edge layouts of the generators (``synth``), with the runtime
-feedback taken from the cost model.
+feedback taken from the problem's model (the analytic cost model, or the
+reference simulator of Section 4.3.2 in oracle/simulate.py).
 """
 from __future__ import annotations
 
@@ -47,11 +48,20 @@ MEM_FACTOR = 4.0   # weights + gradients + two optimizer moments per parameter b
 
 
 class Problem:
-    """Static quantities of one search problem (double precision)."""
+    """Static quantities of one search problem (double precision).
+    ``model`` picks the reward and runtime-feedback model: "analytic"
+    (``evaluate`` below) or "simulator" (oracle/simulate.py)."""
 
-    def __init__(self, sp):
+    def __init__(self, sp, model: str = "analytic"):
         t = sp.topo
         self.sp = sp
+        if model not in ("analytic", "simulator"):
+            raise ValueError(model)
+        self.model = model
+        self.sim = None
+        if model == "simulator":
+            from oracle import simulate as _sim
+            self.sim = _sim.SimProblem(sp)
         self.N, self.M, self.K = t.n_op, t.n_dev, sp.n_groups
         self.S = len(sp.masks)
         g = sp.group_of.astype(np.int64)
@@ -165,13 +175,39 @@ def evaluate(P: Problem, strat: List[Tuple[int, int]]) -> dict:
     return {"T": T, "load": load, "mem": memu, "comp": comp, "sync": sync, "oom": oom}
 
 
+def feedback(P: Problem, strat: List[Tuple[int, int]]) -> dict:
+    """Iteration time, OOM flag and runtime feedback of a full strategy
+    under the problem's model: per group its makespan (s) and idle share, per
+    device its memory share (capped at 1) and idle share.
+      analytic:  makespan = slowest replica's compute, idle share = sync /
+                 (compute + sync), memory = modelled use, idle = 1 - load / T
+      simulator: simulated makespan, mean idle before the group's output
+                 transfers / T, peak / capacity, simulated idle share"""
+    if P.model == "analytic":
+        ev = evaluate(P, strat)
+        gidle = [ev["sync"][g] / (ev["comp"][g] + ev["sync"][g]) if ev["comp"][g] + ev["sync"][g] > 0 else 0.0
+                 for g in range(P.K)]
+        memf = [min(ev["mem"][j] / P.mem[j], 1.0) for j in range(P.M)]
+        didle = [1.0 - ev["load"][j] / ev["T"] if ev["T"] > 0 else 0.0 for j in range(P.M)]
+        return dict(T=ev["T"], oom=ev["oom"], makespan=list(ev["comp"]), gidle=gidle, memf=memf, didle=didle)
+    from oracle import simulate as _sim
+    r = _sim.simulate(P.sim, strat)
+    if not r["valid"]:
+        return dict(T=math.inf, oom=True, makespan=[0.0] * P.K, gidle=[0.0] * P.K, memf=[0.0] * P.M,
+                    didle=[0.0] * P.M)
+    T = r["T"]
+    return dict(T=T, oom=r["oom"], makespan=r["group_makespan"],
+                gidle=[min(x / T, 1.0) if T > 0 else 0.0 for x in r["group_idle"]],
+                memf=[min(r["dev_peak"][j] / P.mem[j], 1.0) for j in range(P.M)], didle=r["dev_idle"])
+
+
 def reward(P: Problem, path: Sequence[int], T_base: Optional[float] = None) -> float:
     """Speed-up of the partial strategy's iteration time over the baseline
     (every group on every device with AllReduce); -1 when a device runs out
     of memory or a group's mask names no device of the topology."""
     if T_base is None:
-        T_base = evaluate(P, full_strategy(P, []))["T"]
-    ev = evaluate(P, full_strategy(P, path))
+        T_base = feedback(P, full_strategy(P, []))["T"]
+    ev = feedback(P, full_strategy(P, path))
     if ev["oom"]:
         return -1.0
     return T_base / ev["T"]
@@ -184,7 +220,7 @@ def features(P: Problem, path: Sequence[int], f_op: int = 42):
     t = P.sp.topo
     d = len(path)
     strat = full_strategy(P, path)
-    ev = evaluate(P, strat)
+    fb = feedback(P, strat)
     decided_g = np.zeros(P.K, bool)
     for i in range(d):
         decided_g[P.order[i]] = True
@@ -199,9 +235,8 @@ def features(P: Problem, path: Sequence[int], f_op: int = 42):
             x[u, 34 + strat[g][1]] = 1.0
             x[u, 38] = 1.0
             if f_op >= 42:
-                x[u, 40] = np.float32(math.log10(max(ev["comp"][g], 1e-12) * 1e3))
-                cs = ev["comp"][g] + ev["sync"][g]
-                x[u, 41] = np.float32(ev["sync"][g] / cs if cs > 0 else 0.0)
+                x[u, 40] = np.float32(math.log10(max(fb["makespan"][g], 1e-12) * 1e3))
+                x[u, 41] = np.float32(fb["gidle"][g])
         if g == nxt:
             x[u, 39] = 1.0
     xd = np.zeros((P.M, 8), np.float32)
@@ -210,8 +245,8 @@ def features(P: Problem, path: Sequence[int], f_op: int = 42):
         xd[j, 1] = np.float32(t.dev_mem[j] / 32.0)
         xd[j, 2] = 1.0
         xd[j, 3] = np.float32(math.log10(t.dev_intra_bw[j]))
-        xd[j, 4] = np.float32(min(ev["mem"][j] / P.mem[j], 1.0))
-        xd[j, 5] = np.float32(1.0 - ev["load"][j] / ev["T"] if ev["T"] > 0 else 0.0)
+        xd[j, 4] = np.float32(fb["memf"][j])
+        xd[j, 5] = np.float32(fb["didle"][j])
     xod = np.zeros(t.e_od, np.uint8)
     for e in range(t.e_od):
         u, j = int(t.od_op[e]), int(t.od_dev[e])

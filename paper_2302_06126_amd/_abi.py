@@ -26,7 +26,8 @@ SEARCH_EXPORTS = ("tag_search_problem_create", "tag_search_problem_destroy", "ta
                   "tag_search_evaluate", "tag_mcts_create", "tag_mcts_destroy", "tag_mcts_select",
                   "tag_mcts_update", "tag_mcts_root_stats", "tag_mcts_best_path", "tag_mcts_size",
                   "tag_search_device_bytes", "tag_search_upload", "tag_search_pack", "tag_search_features",
-                  "tag_search_run_workspace", "tag_search_run")
+                  "tag_search_run_workspace", "tag_search_run", "tag_simulate", "tag_simulate_batch",
+                  "tag_search_set_model")
 
 # include/tag_train.h
 TRAIN_EXPORTS = ("tag_train_workspace", "tag_train_step")
@@ -107,6 +108,12 @@ class tag_search_run_args(C.Structure):
                 ("reward_out", C.c_void_p), ("prior_out", C.c_void_p)]
 
 
+class tag_sim_out(C.Structure):
+    _fields_ = [("iter_time", C.c_double), ("valid", C.c_int32), ("oom", C.c_int32), ("n_tasks", C.c_int64),
+                ("group_makespan", _PF), ("group_idle", _PF), ("dev_peak", _PF), ("dev_idle", _PF),
+                ("link_idle", _PF)]
+
+
 class tag_decision(C.Structure):
     _fields_ = [("mask", C.c_uint64), ("option", C.c_int32), ("replicas", C.c_int32),
                 ("sync", C.c_int32), ("sfb", C.c_int32)]
@@ -172,6 +179,9 @@ def load() -> C.CDLL:
     lib.tag_search_features.argtypes = [vp, S, vp, vp, vp, vp, vp, vp]
     lib.tag_search_run_workspace.argtypes = [vp, vp, C.POINTER(tag_model_dims), S, szp, szp]
     lib.tag_search_run.argtypes = [C.POINTER(tag_search_run_args), vp]
+    lib.tag_simulate.argtypes = [vp, vp, S, C.POINTER(tag_sim_out)]
+    lib.tag_search_set_model.argtypes = [vp, S]
+    lib.tag_simulate_batch.argtypes = [vp, S, vp, vp, S, S, vp, vp]
     lib.tag_train_workspace.argtypes = [vp, C.POINTER(tag_model_dims), S, S, S, szp]
     lib.tag_train_step.argtypes = [vp, C.POINTER(tag_model_dims), C.POINTER(tag_weights), C.POINTER(tag_features),
                                    C.POINTER(tag_slices), C.POINTER(tag_train_batch), C.POINTER(tag_grads),

@@ -101,6 +101,51 @@ Eval evaluate_strategy(const tag_search_problem *P, const uint64_t *mask, const 
     return e;
 }
 
+// Iteration time, OOM flag and the runtime feedback of a full strategy
+// under the problem's model: group makespan (s) and idle share, device
+// memory share and idle share.
+//  analytic:  makespan = slowest replica's compute, idle share = sync /
+//             (compute + sync), memory = the model's use, idle = 1 - load / T
+//  simulator: makespan and memory peak as simulated, group idle share =
+//             mean idle before its output transfers / T, device idle share
+bool strategy_feedback(const tag_search_problem *P, const uint64_t *mask, const int32_t *opt, SimScratch *W,
+                       Feedback *f) {
+    f->gms.assign(P->K, 0.0);
+    f->gidle.assign(P->K, 0.0);
+    f->memf.assign(P->M, 0.0);
+    f->didle.assign(P->M, 0.0);
+    if (P->model == 0) {
+        const Eval e = evaluate_strategy(P, mask, opt);
+        f->T = e.T;
+        f->oom = e.oom;
+        for (int g = 0; g < P->K; ++g) {
+            const double cs = e.comp[g] + e.sync[g];
+            f->gms[g] = e.comp[g];
+            f->gidle[g] = cs > 0 ? e.sync[g] / cs : 0.0;
+        }
+        for (int j = 0; j < P->M; ++j) {
+            f->memf[j] = std::min(e.mem[j] / P->mem[j], 1.0);
+            f->didle[j] = e.T > 0 ? 1.0 - e.load[j] / e.T : 0.0;
+        }
+        return true;
+    }
+    bool valid = true, oom = false;
+    f->peak.assign(P->M, 0.0);
+    if (!sim_run(P, mask, opt, W, &f->T, &valid, &oom, f->gms.data(), f->gidle.data(), f->peak.data(),
+                 f->didle.data(), nullptr))
+        return false;
+    f->oom = oom || !valid;
+    if (!valid) {
+        std::fill(f->gms.begin(), f->gms.end(), 0.0);
+        std::fill(f->gidle.begin(), f->gidle.end(), 0.0);
+        std::fill(f->didle.begin(), f->didle.end(), 0.0);
+        return true;
+    }
+    for (int g = 0; g < P->K; ++g) f->gidle[g] = f->T > 0 ? std::min(f->gidle[g] / f->T, 1.0) : 0.0;
+    for (int j = 0; j < P->M; ++j) f->memf[j] = std::min(f->peak[j] / P->mem[j], 1.0);
+    return true;
+}
+
 }  // namespace tag
 
 // ------------------------------------------------------------------ problem
@@ -193,6 +238,11 @@ extern "C" tag_status tag_search_problem_create(const tag_search_problem_desc *d
         }
         P->xbytes[it->second] += d->op_bytes[s];
     }
+    P->op_params.assign(d->op_params, d->op_params + N);
+    P->oo_src.assign(d->oo_src, d->oo_src + d->e_oo);
+    P->oo_dst.assign(d->oo_dst, d->oo_dst + d->e_oo);
+    P->dd_a.assign(d->dd_a, d->dd_a + d->e_dd);
+    P->dd_b.assign(d->dd_b, d->dd_b + d->e_dd);
     P->od_op.assign(d->od_op, d->od_op + d->e_od);
     P->od_dev.assign(d->od_dev, d->od_dev + d->e_od);
     for (int64_t e = 0; e < d->e_od; ++e)
@@ -240,10 +290,35 @@ extern "C" tag_status tag_search_evaluate(const tag_search_problem *p, const int
     std::vector<uint64_t> mk(p->K);
     std::vector<int32_t> op(p->K);
     full_strategy(p, path, depth, mk.data(), op.data());
-    const Eval e = evaluate_strategy(p, mk.data(), op.data());
-    *iter_time = e.T;
-    *oom = e.oom ? 1 : 0;
-    *reward = e.oom ? -1.0 : p->T_base / e.T;
+    Feedback f;
+    SimScratch *W = p->model ? sim_scratch_new() : nullptr;
+    const bool ok = strategy_feedback(p, mk.data(), op.data(), W, &f);
+    sim_scratch_free(W);
+    if (!ok) TAG_FAIL(TAG_EINVAL, "the tensor graph has a cycle");
+    *iter_time = f.T;
+    *oom = f.oom ? 1 : 0;
+    *reward = f.oom ? -1.0 : p->T_base / f.T;
+    return TAG_OK;
+}
+
+extern "C" tag_status tag_search_set_model(tag_search_problem *p, int32_t model) {
+    clear_error();
+    if (!p) TAG_FAIL(TAG_EINVAL, "problem must be non-NULL");
+    if (model != 0 && model != 1) TAG_FAIL(TAG_EINVAL, "model must be 0 (analytic) or 1 (simulator)");
+    const int32_t old = p->model;
+    p->model = model;
+    std::vector<uint64_t> mk(p->K);
+    std::vector<int32_t> op(p->K);
+    full_strategy(p, nullptr, 0, mk.data(), op.data());
+    Feedback f;
+    SimScratch *W = model ? sim_scratch_new() : nullptr;
+    const bool ok = strategy_feedback(p, mk.data(), op.data(), W, &f);
+    sim_scratch_free(W);
+    if (!ok) {
+        p->model = old;
+        TAG_FAIL(TAG_EINVAL, "the tensor graph has a cycle");
+    }
+    p->T_base = f.T;
     return TAG_OK;
 }
 
@@ -304,12 +379,17 @@ extern "C" tag_status tag_search_pack(const tag_search_problem *p, int32_t B, co
     const StateLayout L = state_layout(p);
     std::vector<uint64_t> mk(p->K);
     std::vector<int32_t> op(p->K);
+    Feedback f;
+    SimScratch *W = p->model ? sim_scratch_new() : nullptr;
     for (int b = 0; b < B; ++b) {
         const int32_t *pb = path + (size_t)b * path_stride;
         const int d = depth[b];
         full_strategy(p, pb, d, mk.data(), op.data());
-        const Eval e = evaluate_strategy(p, mk.data(), op.data());
-        rewards[b] = e.oom ? -1.0 : p->T_base / e.T;
+        if (!strategy_feedback(p, mk.data(), op.data(), W, &f)) {
+            sim_scratch_free(W);
+            TAG_FAIL(TAG_EINVAL, "the tensor graph has a cycle");
+        }
+        rewards[b] = f.oom ? -1.0 : p->T_base / f.T;
         char *rec = static_cast<char *>(states) + (size_t)b * L.total;
         int32_t *hdr = reinterpret_cast<int32_t *>(rec);
         uint64_t *msk = reinterpret_cast<uint64_t *>(rec + L.mask);
@@ -325,15 +405,15 @@ extern "C" tag_status tag_search_pack(const tag_search_problem *p, int32_t B, co
         for (int i = 0; i < d; ++i) {
             const int g = p->order[i];
             dec[g] = 1;
-            const double cs = e.comp[g] + e.sync[g];
-            gf[2 * g] = (float)std::log10(std::max(e.comp[g], 1e-12) * 1e3);
-            gf[2 * g + 1] = (float)(cs > 0 ? e.sync[g] / cs : 0.0);
+            gf[2 * g] = (float)std::log10(std::max(f.gms[g], 1e-12) * 1e3);
+            gf[2 * g + 1] = (float)f.gidle[g];
         }
         for (int j = 0; j < p->M; ++j) {
-            df[2 * j] = (float)std::min(e.mem[j] / p->mem[j], 1.0);
-            df[2 * j + 1] = (float)(e.T > 0 ? 1.0 - e.load[j] / e.T : 0.0);
+            df[2 * j] = (float)f.memf[j];
+            df[2 * j + 1] = (float)f.didle[j];
         }
     }
+    sim_scratch_free(W);
     return TAG_OK;
 }
 

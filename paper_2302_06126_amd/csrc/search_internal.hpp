@@ -20,9 +20,13 @@ struct tag_search_problem {
     std::vector<std::pair<int, int>> xpairs; // cross-group tensor traffic, first-appearance order
     std::vector<double> xbytes;
     std::vector<int32_t> od_op, od_dev;
+    std::vector<double> op_params;           // per op (the simulator works per op)
+    std::vector<int32_t> oo_src, oo_dst;     // tensors in input order
+    std::vector<int32_t> dd_a, dd_b;         // device links in input order
     std::vector<uint64_t> slice_mask;
     std::vector<int32_t> slice_opt;
     double T_base = 0.0;                     // baseline iteration time
+    int32_t model = 0;                       // 0 analytic model, 1 simulator
 };
 
 namespace tag {
@@ -35,6 +39,24 @@ struct Eval {
 
 void full_strategy(const tag_search_problem *P, const int32_t *path, int32_t depth, uint64_t *mask, int32_t *opt);
 Eval evaluate_strategy(const tag_search_problem *P, const uint64_t *mask, const int32_t *opt);
+
+// Simulator (simulate.hip).  Scratch reused across simulations of one
+// thread.  Returns false when the tensor graph has a cycle.
+struct SimScratch;
+SimScratch *sim_scratch_new();
+void sim_scratch_free(SimScratch *w);
+bool sim_run(const tag_search_problem *P, const uint64_t *mask, const int32_t *opt, SimScratch *W, double *T,
+             bool *valid, bool *oom, double *g_makespan, double *g_idle, double *d_peak, double *d_idle,
+             double *l_idle);
+
+// Runtime feedback of a full strategy under the problem's model (search_host.hip).
+struct Feedback {
+    double T = 0.0;
+    bool oom = false;
+    std::vector<double> gms, gidle, memf, didle, peak;
+};
+bool strategy_feedback(const tag_search_problem *P, const uint64_t *mask, const int32_t *opt, SimScratch *W,
+                       Feedback *f);
 
 // Static device part: group_of, op_type [N] int32; lflops, lbytes [N] float;
 // device rows [M][4] float; od_op, od_dev [E_od] int32.

@@ -30,9 +30,10 @@ class SearchProblem:
     """Host handle of a search problem.  `sp` carries the topology (ops,
     devices, links, op-device pairs and their attributes), the op grouping,
     per-op parameter bytes and the slice table (``synth.SearchProblem``
-    layout)."""
+    layout).  `model` picks the reward and runtime-feedback model: the
+    analytic iteration-time model or the simulator."""
 
-    def __init__(self, sp, f_op: int = 42):
+    def __init__(self, sp, f_op: int = 42, model: str = "analytic"):
         t = sp.topo
         self.keep = keep = {
             "group_of": _i32(sp.group_of), "op_type": _i32(t.op_type), "op_flops": _f64(t.op_flops),
@@ -51,7 +52,12 @@ class SearchProblem:
         check(_abi.load().tag_search_problem_create(C.byref(d), C.byref(h)), "tag_search_problem_create")
         self.h = h.value
         self.n_op, self.n_dev, self.n_groups, self.n_slices, self.f_op = t.n_op, t.n_dev, sp.n_groups, len(sp.masks), f_op
-        self.e_od = t.e_od
+        self.e_od, self.e_dd = t.e_od, t.e_dd
+        if model not in ("analytic", "simulator"):
+            raise ValueError("model must be 'analytic' or 'simulator'")
+        if model == "simulator":
+            check(_abi.load().tag_search_set_model(self.h, 1), "tag_search_set_model")
+        self.model = model
 
     def order(self) -> Tuple[np.ndarray, np.ndarray]:
         order = np.zeros(self.n_groups, np.int32)
@@ -65,6 +71,31 @@ class SearchProblem:
         check(_abi.load().tag_search_evaluate(self.h, p.ctypes.data if p.size else None, int(p.size),
                                               C.byref(r), C.byref(T), C.byref(oom)), "tag_search_evaluate")
         return r.value, T.value, bool(oom.value)
+
+    def simulate(self, path) -> dict:
+        """Runtime feedback of the strategy ``path`` (tag_simulate)."""
+        p = _i32(path)
+        out = _abi.tag_sim_out()
+        arrs = {"group_makespan": np.zeros(self.n_groups), "group_idle": np.zeros(self.n_groups),
+                "dev_peak": np.zeros(self.n_dev), "dev_idle": np.zeros(self.n_dev),
+                "link_idle": np.zeros(max(self.e_dd, 1))}
+        for k, v in arrs.items():
+            setattr(out, k, v.ctypes.data)
+        check(_abi.load().tag_simulate(self.h, p.ctypes.data if p.size else None, int(p.size), C.byref(out)),
+              "tag_simulate")
+        arrs["link_idle"] = arrs["link_idle"][:self.e_dd]
+        return dict(T=out.iter_time, valid=bool(out.valid), oom=bool(out.oom), n_tasks=int(out.n_tasks), **arrs)
+
+    def simulate_batch(self, depth, path, n_threads: int = 1) -> Tuple[np.ndarray, np.ndarray]:
+        """Iteration times and OOM flags of B strategies (tag_simulate_batch)."""
+        d = _i32(depth)
+        p = _i32(path).reshape(len(d), -1)
+        B = int(d.size)
+        T = np.zeros(B)
+        oom = np.zeros(B, np.int32)
+        check(_abi.load().tag_simulate_batch(self.h, B, d.ctypes.data, p.ctypes.data, p.shape[1], n_threads,
+                                             T.ctypes.data, oom.ctypes.data), "tag_simulate_batch")
+        return T, oom.astype(bool)
 
     def device_bytes(self) -> Tuple[int, int]:
         a, b = C.c_size_t(0), C.c_size_t(0)

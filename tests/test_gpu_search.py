@@ -24,13 +24,14 @@ def torch():
     return torch
 
 
-@pytest.mark.parametrize("name,f_op", [("tiny", 40), ("cnn", 42), ("large", 42)])
-def test_features_kernel_matches_reference(torch, name, f_op):
+@pytest.mark.parametrize("name,f_op,model", [("tiny", 40, "analytic"), ("cnn", 42, "analytic"),
+                                             ("large", 42, "analytic"), ("cnn", 42, "simulator")])
+def test_features_kernel_matches_reference(torch, name, f_op, model):
     import paper_2302_06126_amd.search as PS
-    _say(f"[search] features {name}")
+    _say(f"[search] features {name} {model}")
     sp = synth.make_search_problem(name)
-    P = OS.Problem(sp)
-    prob = PS.SearchProblem(sp, f_op=f_op)
+    P = OS.Problem(sp, model=model)
+    prob = PS.SearchProblem(sp, f_op=f_op, model=model)
     rng = synth.rng_for(58, len(name))
     depth = np.array([0, 1, 3, P.K // 2, P.K - 1, P.K], np.int32)
     B = len(depth)
@@ -111,27 +112,29 @@ def test_search_rounds_match_reference_tree(torch, name, B, rounds):
     prob.close()
 
 
-@pytest.mark.parametrize("name,B,rounds,pipelined", [("tiny", 8, 6, True), ("cnn", 16, 5, True),
-                                                      ("cnn", 16, 4, False)])
-def test_native_rounds_match_reference_schedule(torch, name, B, rounds, pipelined):
+@pytest.mark.parametrize("name,B,rounds,pipelined,model", [("tiny", 8, 6, True, "analytic"),
+                                                            ("cnn", 16, 5, True, "analytic"),
+                                                            ("cnn", 16, 4, False, "analytic"),
+                                                            ("tiny", 8, 6, True, "simulator")])
+def test_native_rounds_match_reference_schedule(torch, name, B, rounds, pipelined, model):
     """tag_search_run: the recorded leaves, replayed through the reference
     tree in the same select / update schedule (pipelined: round k+1 is
     selected before round k's update) with the recorded priors and the
     reference rewards, give the same paths and the same root statistics."""
     import paper_2302_06126_amd as P0
     import paper_2302_06126_amd.search as PS
-    _say(f"[search] native rounds {name} B={B} pipelined={pipelined}")
+    _say(f"[search] native rounds {name} B={B} pipelined={pipelined} {model}")
     wl = synth.WORKLOADS[name]
     sp = synth.make_search_problem(name)
-    P = OS.Problem(sp)
+    P = OS.Problem(sp, model=model)
     w = synth.make_weights(wl.f, wl.heads, wl.layers, wl.f_op, wl.f)
-    model = P0.Model(w, f=wl.f, heads=wl.heads, layers=wl.layers, f_op=wl.f_op, dtype=wl.dtype)
-    prob = PS.SearchProblem(sp, f_op=wl.f_op)
-    svc = PS.SearchService(prob, sp, model, B)
+    gnn = P0.Model(w, f=wl.f, heads=wl.heads, layers=wl.layers, f_op=wl.f_op, dtype=wl.dtype)
+    prob = PS.SearchProblem(sp, f_op=wl.f_op, model=model)
+    svc = PS.SearchService(prob, sp, gnn, B)
     lib = PS.Mcts(P.K, P.S, 1.5, 0.0)
     rec = svc.run(lib, rounds, pipelined=pipelined, record=True)
     ref = OS.Tree(P.K, P.S, 1.5, 0.0)
-    T_base = OS.evaluate(P, OS.full_strategy(P, []))["T"]
+    T_base = OS.feedback(P, OS.full_strategy(P, []))["T"]
     sel = {0: ref.select(B)}
     for k in range(rounds):
         if pipelined and k + 1 < rounds:
