@@ -164,7 +164,9 @@ tag_status tag_search_upload(const tag_search_problem *p, void *static_dev, size
 
 /* For the B leaves of a select: write their rewards, the query op of the
  * next group (its representative op; 0 for complete strategies) and one
- * packed state record each into HOST memory `states` (B * state_bytes). */
+ * packed state record each into HOST memory `states` (B * state_bytes).
+ * Under the simulator model the leaves are simulated on up to 16 host
+ * threads (results do not depend on the thread count). */
 tag_status tag_search_pack(const tag_search_problem *p, int32_t B, const int32_t *depth,
                            const int32_t *path, int32_t path_stride, void *states, double *rewards,
                            int32_t *query_op);

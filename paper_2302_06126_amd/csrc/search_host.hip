@@ -4,10 +4,12 @@
 // feature kernel expands (Section 4.2.2 of the paper, Monte-Carlo Tree
 // Search; the readings are listed in include/tag_search.h).
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <limits>
 #include <map>
 #include <new>
+#include <thread>
 #include <utility>
 
 #include "search_internal.hpp"
@@ -377,43 +379,61 @@ extern "C" tag_status tag_search_pack(const tag_search_problem *p, int32_t B, co
         if (st != TAG_OK) return st;
     }
     const StateLayout L = state_layout(p);
-    std::vector<uint64_t> mk(p->K);
-    std::vector<int32_t> op(p->K);
-    Feedback f;
-    SimScratch *W = p->model ? sim_scratch_new() : nullptr;
-    for (int b = 0; b < B; ++b) {
-        const int32_t *pb = path + (size_t)b * path_stride;
-        const int d = depth[b];
-        full_strategy(p, pb, d, mk.data(), op.data());
-        if (!strategy_feedback(p, mk.data(), op.data(), W, &f)) {
-            sim_scratch_free(W);
-            TAG_FAIL(TAG_EINVAL, "the tensor graph has a cycle");
+    // workers claim leaves from a shared counter; the simulator model spreads
+    // the leaves over host threads (each leaf writes only its own records)
+    std::atomic<int> next{0};
+    auto work = [&](char *cycle) {
+        std::vector<uint64_t> mk(p->K);
+        std::vector<int32_t> op(p->K);
+        Feedback f;
+        SimScratch *W = p->model ? sim_scratch_new() : nullptr;
+        for (int b = next.fetch_add(1); b < B; b = next.fetch_add(1)) {
+            const int32_t *pb = path + (size_t)b * path_stride;
+            const int d = depth[b];
+            full_strategy(p, pb, d, mk.data(), op.data());
+            if (!strategy_feedback(p, mk.data(), op.data(), W, &f)) {
+                *cycle = 1;
+                break;
+            }
+            rewards[b] = f.oom ? -1.0 : p->T_base / f.T;
+            char *rec = static_cast<char *>(states) + (size_t)b * L.total;
+            int32_t *hdr = reinterpret_cast<int32_t *>(rec);
+            uint64_t *msk = reinterpret_cast<uint64_t *>(rec + L.mask);
+            int32_t *opt = reinterpret_cast<int32_t *>(rec + L.option);
+            int32_t *dec = reinterpret_cast<int32_t *>(rec + L.decided);
+            float *gf = reinterpret_cast<float *>(rec + L.gfeat);
+            float *df = reinterpret_cast<float *>(rec + L.dfeat);
+            const int nxt = d < p->K ? p->order[d] : -1;
+            hdr[0] = nxt;
+            hdr[1] = 0;
+            query_op[b] = nxt >= 0 ? p->rep[nxt] : 0;
+            for (int g = 0; g < p->K; ++g) { dec[g] = 0; msk[g] = mk[g]; opt[g] = op[g]; gf[2 * g] = gf[2 * g + 1] = 0.f; }
+            for (int i = 0; i < d; ++i) {
+                const int g = p->order[i];
+                dec[g] = 1;
+                gf[2 * g] = (float)std::log10(std::max(f.gms[g], 1e-12) * 1e3);
+                gf[2 * g + 1] = (float)f.gidle[g];
+            }
+            for (int j = 0; j < p->M; ++j) {
+                df[2 * j] = (float)f.memf[j];
+                df[2 * j + 1] = (float)f.didle[j];
+            }
         }
-        rewards[b] = f.oom ? -1.0 : p->T_base / f.T;
-        char *rec = static_cast<char *>(states) + (size_t)b * L.total;
-        int32_t *hdr = reinterpret_cast<int32_t *>(rec);
-        uint64_t *msk = reinterpret_cast<uint64_t *>(rec + L.mask);
-        int32_t *opt = reinterpret_cast<int32_t *>(rec + L.option);
-        int32_t *dec = reinterpret_cast<int32_t *>(rec + L.decided);
-        float *gf = reinterpret_cast<float *>(rec + L.gfeat);
-        float *df = reinterpret_cast<float *>(rec + L.dfeat);
-        const int nxt = d < p->K ? p->order[d] : -1;
-        hdr[0] = nxt;
-        hdr[1] = 0;
-        query_op[b] = nxt >= 0 ? p->rep[nxt] : 0;
-        for (int g = 0; g < p->K; ++g) { dec[g] = 0; msk[g] = mk[g]; opt[g] = op[g]; gf[2 * g] = gf[2 * g + 1] = 0.f; }
-        for (int i = 0; i < d; ++i) {
-            const int g = p->order[i];
-            dec[g] = 1;
-            gf[2 * g] = (float)std::log10(std::max(f.gms[g], 1e-12) * 1e3);
-            gf[2 * g + 1] = (float)f.gidle[g];
-        }
-        for (int j = 0; j < p->M; ++j) {
-            df[2 * j] = (float)f.memf[j];
-            df[2 * j + 1] = (float)f.didle[j];
-        }
+        sim_scratch_free(W);
+    };
+    const int hw = std::max(1u, std::thread::hardware_concurrency());
+    const int nt = p->model ? std::min({B, kPackThreads, hw}) : 1;
+    std::vector<char> cycle(nt, 0);
+    if (nt == 1) {
+        work(cycle.data());
+    } else {
+        std::vector<std::thread> th;
+        th.reserve(nt);
+        for (int t = 0; t < nt; ++t) th.emplace_back(work, cycle.data() + t);
+        for (auto &x : th) x.join();
     }
-    sim_scratch_free(W);
+    for (char c : cycle)
+        if (c) TAG_FAIL(TAG_EINVAL, "the tensor graph has a cycle");
     return TAG_OK;
 }
 

@@ -49,6 +49,9 @@ bool sim_run(const tag_search_problem *P, const uint64_t *mask, const int32_t *o
              bool *valid, bool *oom, double *g_makespan, double *g_idle, double *d_peak, double *d_idle,
              double *l_idle);
 
+// Host threads tag_search_pack uses under the simulator model.
+constexpr int kPackThreads = 16;
+
 // Runtime feedback of a full strategy under the problem's model (search_host.hip).
 struct Feedback {
     double T = 0.0;

@@ -12,6 +12,7 @@
 // task number).  Per-thread scratch makes the batched entry point
 // allocation-free after the first simulation of each thread.
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <limits>
 #include <thread>
@@ -387,11 +388,12 @@ extern "C" tag_status tag_simulate_batch(const tag_search_problem *p, int32_t B,
         if (st != TAG_OK) return st;
     }
     std::vector<char> cyc(std::max(B, 1), 0);
-    auto run = [&](int t) {
+    std::atomic<int32_t> next{0};
+    auto run = [&](int) {
         SimWork W;
         std::vector<uint64_t> mask(p->K);
         std::vector<int32_t> opt(p->K);
-        for (int32_t b = t; b < B; b += n_threads) {
+        for (int32_t b = next.fetch_add(1); b < B; b = next.fetch_add(1)) {
             full_strategy(p, path ? path + (size_t)b * path_stride : nullptr, depth[b], mask.data(), opt.data());
             const SimResult R = simulate_full(p, mask.data(), opt.data(), W, nullptr, nullptr, nullptr, nullptr, nullptr);
             iter_time[b] = R.T;
