@@ -199,6 +199,103 @@ def search_bench(args) -> int:
     return 0
 
 
+def decide_full_bench(args) -> int:
+    """Full-enumeration decision head (tag_gnn_decide_full) on a workload of
+    at most 16 devices: the batch's embeddings from one forward pass (outside
+    the timed region), one query per candidate (the first op of its next
+    group), every non-empty device mask with each option scored, softmax
+    priors written.  Reports slices scored per second; the dominant kernel
+    is ALU-bound (no matrix product: a ReLU readout per slice)."""
+    import torch
+
+    import paper_2302_06126_amd as P
+    from paper_2302_06126_amd import _abi
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    name = args.workload
+    wl = synth.WORKLOADS[name]
+    topo = synth.make_topology(name)
+    if topo.n_dev > 16:
+        sys.exit("full enumeration needs a workload with at most 16 devices")
+    R = wl.batch
+    batch = synth.make_batch(name, topo, R, wl.f_op)
+    w = synth.make_weights(wl.f, wl.heads, wl.layers, wl.f_op, wl.f)
+    g = P.Graph([topo], device="cuda:0")
+    model = P.Model(w, f=wl.f, heads=wl.heads, layers=wl.layers, f_op=wl.f_op, dtype=wl.dtype, device="cuda:0")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    E_op, E_dev = P.forward(g, model, t(batch.x_op), t(batch.x_dev), t(batch.x_oo), t(batch.x_dd), t(batch.x_od))
+    first = np.array([int(np.flatnonzero(batch.query_rep == r)[0]) for r in range(R)])
+    Q = R
+    q = [t(batch.query_rep[first].astype(np.int32)), t(np.zeros(Q, np.int32)), t(batch.query_op[first].astype(np.int32))]
+    lib = _abi.load()
+    b = C.c_size_t(0)
+    _abi.check(lib.tag_gnn_decide_full_workspace(g.handle, C.byref(model.dims), R, Q, C.byref(b)), "workspace")
+    ws = torch.empty(max(b.value, 1), dtype=torch.uint8, device=dev)
+    S_full = 4 * ((1 << topo.n_dev) - 1)
+    argmax = torch.empty(Q, dtype=torch.int32, device=dev)
+    best = torch.empty(Q, dtype=torch.float32, device=dev)
+    prior = torch.empty((Q, S_full), dtype=torch.float32, device=dev)
+    decision = torch.empty((Q, C.sizeof(P.tag_decision)), dtype=torch.uint8, device=dev)
+    sh = int(torch.cuda.current_stream().cuda_stream)
+
+    def step():
+        _abi.check(lib.tag_gnn_decide_full(g.handle, C.byref(model.dims), C.byref(model.weights), R, E_op.data_ptr(),
+                                           E_dev.data_ptr(), Q, q[0].data_ptr(), q[1].data_ptr(), q[2].data_ptr(),
+                                           argmax.data_ptr(), best.data_ptr(), prior.data_ptr(),
+                                           decision.data_ptr(), ws.data_ptr(), b.value, sh), "decide_full")
+
+    print(f"[bench] full-enumeration decide on {name}: Q={Q} M={topo.n_dev} slices={S_full} H={wl.f}; "
+          f"warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(max(args.warmup, 1)):
+        step()
+    torch.cuda.synchronize()
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    s0.record()
+    for _ in range(args.steps):
+        step()
+    s1.record()
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    ms = s0.elapsed_time(s1) / args.steps
+    H = wl.f
+    # per slice: H adds (device part + option column), H max, H multiply-adds of the readout
+    flops = 4.0 * H * Q * S_full
+    ach = flops / (ms / 1e3) / 1e12
+    out = {
+        "metric": "full-enumeration decision slices scored/sec (every device mask x 4 options)",
+        "value": round(Q * S_full * args.steps / el, 1), "unit": "slices/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(el * 1e3 / args.steps, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": name, "queries": Q, "n_dev": topo.n_dev, "slices_per_query": S_full,
+                   "dec_hidden": H, "parallelism": "none"},
+        "roofline": {"bound": "alu", "achieved": round(ach, 3), "peak": 157.3, "unit": "TFLOP/s",
+                     "frac": round(ach / 157.3, 4), "traffic": None, "kernel": "dec_full + dec_full_merge",
+                     "avg_launch_ms": round(ms, 4), "algorithmic_flops_per_launch": flops,
+                     "note": "whole call timed with events on its stream (projections, enumeration, merge)"},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        masks = np.array([k for k in range(1, 1 << topo.n_dev) for _ in range(4)], np.uint64)
+        opts = np.array([o for _ in range(1, 1 << topo.n_dev) for o in range(4)], np.uint8)
+        eo, ed = E_op.double().cpu().numpy(), E_dev.double().cpu().numpy()
+        qr, qo = batch.query_rep[first], batch.query_op[first]
+        t0 = time.perf_counter()
+        n = 0
+        while n < Q:
+            oracle.decide(eo[qr[n]], ed[qr[n]], masks, opts, qo[n:n + 1], w, f=wl.f, dec_hidden=H, n_dev=topo.n_dev)
+            n += 1
+            if time.perf_counter() - t0 >= args.cpu_seconds:
+                break
+        cel = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round(n * S_full / cel, 1), "unit": "slices/s", "cores": 1, "kind": "oracle",
+                               "sample": f"{n} of {Q} queries on the explicit table of {S_full} slices, the oracle's "
+                                         f"decide (fp64, one thread), {cel:.1f} s", "cpu": cpu_model()}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def sim_bench(args) -> int:
     """Host simulator (Section 4.3.2): iterations simulated per second for
     random complete strategies of the workload's search problem, on
@@ -414,9 +511,10 @@ def main() -> int:
                     help="run one plain device copy of this size first (counter calibration)")
     ap.add_argument("--stage", default="auto", choices=["auto"] + list(KERNEL_NAMES),
                     help="kernel stage timed for the roofline (auto: the longest one)")
-    ap.add_argument("--mode", default="forward", choices=["forward", "search", "train", "sim"],
+    ap.add_argument("--mode", default="forward", choices=["forward", "search", "train", "sim", "decide_full"],
                     help="forward: the GNN hot path (default line); search: batched PUCT search rounds; "
-                         "train: the GNN training step; sim: the host simulator")
+                         "train: the GNN training step; sim: the host simulator; decide_full: the "
+                         "full-enumeration decision head")
     ap.add_argument("--reward", default="analytic", choices=["analytic", "simulator"],
                     help="search mode: reward and runtime-feedback model")
     ap.add_argument("--sim-batch", type=int, default=512, help="sim mode: strategies per step")
@@ -435,6 +533,8 @@ def main() -> int:
         return train_bench(args)
     if args.mode == "sim":
         return sim_bench(args)
+    if args.mode == "decide_full":
+        return decide_full_bench(args)
 
     import torch
 

@@ -266,6 +266,26 @@ tag_status tag_gnn_decide(const tag_graph *g, const tag_model_dims *dims, const 
                           int32_t *argmax, float *best_score, float *prior, tag_decision *decision,
                           void *workspace, size_t ws_bytes, void *hip_stream);
 
+/*
+ * Full-enumeration variant of tag_gnn_decide (topologies of at most 16
+ * devices, dec_hidden <= 512): the slices are every non-empty device mask
+ * of the query's topology with each option, slice a = 4 (mask - 1) + option
+ * (bit j of mask = local device j), scored as tag_gnn_decide scores a slice
+ * table.  Prior rows have S_full = 4 (2^max_dev - 1) entries (max_dev from
+ * tag_graph_get_info); a query of a topology with fewer devices fills the
+ * first 4 (2^n_dev - 1) and gets zeros after.  argmax = lowest slice index
+ * among maxima; out-of-range queries as in tag_gnn_decide.  No slice table
+ * is materialised: masks are walked in Gray-code order, one device row added
+ * or removed per step.  Asynchronous.
+ */
+tag_status tag_gnn_decide_full_workspace(const tag_graph *g, const tag_model_dims *dims, int32_t n_replicas,
+                                         int32_t n_query, size_t *bytes);
+tag_status tag_gnn_decide_full(const tag_graph *g, const tag_model_dims *dims, const tag_weights *w,
+                               int32_t n_replicas, const float *E_op, const float *E_dev, int32_t n_query,
+                               const int32_t *query_rep, const int32_t *query_graph, const int32_t *query_op,
+                               int32_t *argmax, float *best_score, float *prior, tag_decision *decision,
+                               void *workspace, size_t ws_bytes, void *hip_stream);
+
 /* Thread-local description of the last non-OK status ("" if none). */
 const char *tag_last_error(void);
 

@@ -306,3 +306,36 @@ def decide(graph: Graph, model: Model, E_op, E_dev, masks, options, q_rep, q_gra
     d = Decide(graph, model, int(E_op.shape[0]), masks, options, q_rep, q_graph, q_op, want_prior)
     d(E_op, E_dev, stream)
     return d.results()
+
+
+def decide_full(graph: Graph, model: Model, E_op, E_dev, q_rep, q_graph, q_op, want_prior: bool = True,
+                stream=None) -> dict:
+    """Full-enumeration decision head (tag_gnn_decide_full): every non-empty
+    device mask with each option, slice a = 4 (mask - 1) + option."""
+    torch = _torch()
+    dev = graph.device
+    lib = _abi.load()
+    q = [torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(dev) for a in (q_rep, q_graph, q_op)]
+    Q = len(q_op)
+    R = int(E_op.shape[0])
+    b = C.c_size_t(0)
+    check(lib.tag_gnn_decide_full_workspace(graph.handle, C.byref(model.dims), R, Q, C.byref(b)),
+          "tag_gnn_decide_full_workspace")
+    ws = torch.empty(max(b.value, 1), dtype=torch.uint8, device=dev)
+    S_full = 4 * ((1 << int(graph.info.max_dev)) - 1)
+    argmax = torch.empty(max(Q, 1), dtype=torch.int32, device=dev)
+    best = torch.empty(max(Q, 1), dtype=torch.float32, device=dev)
+    prior = torch.empty((max(Q, 1), S_full), dtype=torch.float32, device=dev) if want_prior else None
+    decision = torch.empty((max(Q, 1), C.sizeof(tag_decision)), dtype=torch.uint8, device=dev)
+    check(lib.tag_gnn_decide_full(graph.handle, C.byref(model.dims), C.byref(model.weights), R, _ptr(E_op),
+                                  _ptr(E_dev), Q, _ptr(q[0]), _ptr(q[1]), _ptr(q[2]), _ptr(argmax), _ptr(best),
+                                  _ptr(prior), _ptr(decision), _ptr(ws), b.value, _stream(stream)),
+          "tag_gnn_decide_full")
+    raw = decision[:Q].cpu().numpy()
+    rec = np.frombuffer(raw.tobytes(), dtype=np.dtype([("mask", "<u8"), ("option", "<i4"), ("replicas", "<i4"),
+                                                      ("sync", "<i4"), ("sfb", "<i4")]))
+    out = dict(argmax=argmax[:Q].cpu().numpy(), best=best[:Q].cpu().numpy(), mask=rec["mask"],
+               option=rec["option"], replicas=rec["replicas"], sync=rec["sync"], sfb=rec["sfb"])
+    if want_prior:
+        out["prior"] = prior[:Q].cpu().numpy()
+    return out

@@ -20,7 +20,8 @@ STATUS_NAMES = {0: "TAG_OK", -1: "TAG_EINVAL", -2: "TAG_ERANGE", -3: "TAG_EDUP",
 
 EXPORTS = ("tag_graph_plan", "tag_graph_build", "tag_graph_get_info", "tag_graph_export",
            "tag_graph_destroy", "tag_gnn_workspace", "tag_gnn_forward", "tag_gnn_decide_workspace",
-           "tag_gnn_decide", "tag_last_error", "tag_version", "tag_profile_begin", "tag_profile_end")
+           "tag_gnn_decide", "tag_last_error", "tag_version", "tag_profile_begin", "tag_profile_end",
+           "tag_gnn_decide_full_workspace", "tag_gnn_decide_full")
 # include/tag_search.h
 SEARCH_EXPORTS = ("tag_search_problem_create", "tag_search_problem_destroy", "tag_search_order",
                   "tag_search_evaluate", "tag_mcts_create", "tag_mcts_destroy", "tag_mcts_select",
@@ -188,6 +189,11 @@ def load() -> C.CDLL:
                                    C.c_float, vp, vp, C.c_size_t, vp]
     for name in TRAIN_EXPORTS:
         getattr(lib, name).restype = S
+    lib.tag_gnn_decide_full_workspace.argtypes = [vp, C.POINTER(tag_model_dims), S, S, szp]
+    lib.tag_gnn_decide_full.argtypes = [vp, C.POINTER(tag_model_dims), C.POINTER(tag_weights), S, vp, vp, S, vp,
+                                        vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]
+    lib.tag_gnn_decide_full_workspace.restype = S
+    lib.tag_gnn_decide_full.restype = S
     for name in SEARCH_EXPORTS:
         if name not in ("tag_search_problem_destroy", "tag_mcts_destroy"):
             getattr(lib, name).restype = S

@@ -284,3 +284,260 @@ extern "C" tag_status tag_gnn_decide(const tag_graph *g, const tag_model_dims *d
     prof_end(TAG_STAGE_DECIDE, stream);
     return launch_status("tag_gnn_decide");
 }
+
+// ------------------------------------------------------------ full enumeration
+// Every non-empty device mask of the query's topology (n_dev <= 16) with each
+// of the four options: slice a = 4 (mask - 1) + option.  Wavefronts walk
+// Gray-code ranges of masks, so consecutive masks differ in one device and
+// the device part of the pre-activation changes by one row of t; lanes hold
+// hidden units (HPL per lane) and a wavefront sum per option gives the
+// score.  Per-block (max, sum, argmax) records are merged per query in block
+// order; priors are normalised in a second pass.
+namespace tag {
+namespace {
+
+struct FullArgs {
+    DecArgs A;
+    int32_t NB;            // blocks per query
+    int32_t S_full;        // 4 (2^max_dev - 1): prior row stride
+    float *rec;            // [Q][NB][4]: max, sum, argmax (as float bits), valid
+};
+
+__device__ __forceinline__ float wave_sum(float v) {
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+template <int HPL>
+__global__ void __launch_bounds__(256) dec_full(FullArgs FA) {
+    const DecArgs &A = FA.A;
+    extern __shared__ float sh[];   // t rows [16][Hx] | base [4][Hx] | w2 [Hx]
+    __shared__ float rm[4], rz[4];
+    __shared__ int32_t ri[4];
+    const int32_t q = blockIdx.x / FA.NB, c = blockIdx.x % FA.NB;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int Hx = A.Hx;
+    int32_t r, g, op;
+    float *rec = FA.rec + ((int64_t)q * FA.NB + c) * 4;
+    if (!query_valid(A, q, &r, &g, &op)) {
+        if (threadIdx.x == 0) { rec[0] = -INFINITY; rec[1] = 0.f; rec[2] = __int_as_float(INT32_MAX); rec[3] = 0.f; }
+        return;
+    }
+    const int32_t d0 = A.dev_off[g], nd = A.dev_off[g + 1] - d0;
+    float *tl = sh, *base = sh + 16 * Hx, *w2s = base + 4 * Hx;
+    const int din = 2 * A.F + 4;
+    for (int i = threadIdx.x; i < nd * Hx; i += blockDim.x)
+        tl[i] = A.t[((int64_t)r * A.n_dev + d0 + i / Hx) * Hx + i % Hx];
+    for (int i = threadIdx.x; i < 4 * Hx; i += blockDim.x) {
+        const int o = i / Hx, h = i % Hx;
+        base[i] = A.P[(int64_t)h * din + 2 * A.F + o] + (A.H > 0 ? A.b1[h] : 0.f) + A.v[(int64_t)q * Hx + h];
+    }
+    for (int h = threadIdx.x; h < Hx; h += blockDim.x) w2s[h] = A.H > 0 ? A.w2[h] : 0.f;
+    __syncthreads();
+    // this wavefront's Gray range
+    const int64_t total = (int64_t)1 << nd;
+    const int64_t W = (int64_t)FA.NB * 4, wid = (int64_t)c * 4 + wv;
+    const int64_t len = (total + W - 1) / W;
+    const int64_t g0 = wid * len, g1 = g0 + len < total ? g0 + len : total;
+    float m = -INFINITY, z = 0.f;
+    int32_t im = INT32_MAX;
+    if (g0 < g1) {
+        float ds[HPL];
+        uint32_t mask = (uint32_t)(g0 ^ (g0 >> 1));
+#pragma unroll
+        for (int i = 0; i < HPL; ++i) {
+            const int h = lane + 64 * i;
+            float s = 0.f;
+            for (int j = 0; j < nd; ++j)
+                if ((mask >> j) & 1u) s += h < Hx ? tl[j * Hx + h] : 0.f;
+            ds[i] = s;
+        }
+        for (int64_t gi = g0; gi < g1; ++gi) {
+            if (gi > g0) {
+                const int j = __builtin_ctzll((unsigned long long)gi);
+                mask ^= 1u << j;
+                const float sg = ((mask >> j) & 1u) ? 1.f : -1.f;
+#pragma unroll
+                for (int i = 0; i < HPL; ++i) {
+                    const int h = lane + 64 * i;
+                    if (h < Hx) ds[i] = fmaf(sg, tl[j * Hx + h], ds[i]);
+                }
+            }
+            if (mask == 0) continue;
+#pragma unroll
+            for (int o = 0; o < 4; ++o) {
+                float s;
+                if (A.H == 0) {   // linear head: Hx = 1, lane 0 holds the sums
+                    s = A.b2[0] + __shfl(ds[0] + base[o], 0, 64);
+                } else {
+                    float p = 0.f;
+#pragma unroll
+                    for (int i = 0; i < HPL; ++i) {
+                        const int h = lane + 64 * i;
+                        if (h < Hx) p = fmaf(w2s[h], fmaxf(ds[i] + base[o * Hx + h], 0.f), p);
+                    }
+                    s = A.b2[0] + wave_sum(p);
+                }
+                const int32_t a = (int32_t)(4 * (mask - 1) + o);
+                if (A.prior && lane == 0) A.prior[(int64_t)q * FA.S_full + a] = s;
+                if (s > m) { z = z * __expf(m - s) + 1.f; m = s; im = a; }
+                else { z += __expf(s - m); if (s == m && a < im) im = a; }
+            }
+        }
+    }
+    if (lane == 0) { rm[wv] = m; rz[wv] = z; ri[wv] = im; }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float M = -INFINITY, Z = 0.f;
+        int32_t I = INT32_MAX;
+        for (int k = 0; k < 4; ++k) {
+            const float m2 = rm[k];
+            if (m2 == -INFINITY) continue;
+            const float nm = fmaxf(M, m2);
+            Z = (M == -INFINITY ? 0.f : Z * __expf(M - nm)) + rz[k] * __expf(m2 - nm);
+            if (m2 > M || (m2 == M && ri[k] < I)) I = ri[k];
+            M = nm;
+        }
+        rec[0] = M; rec[1] = Z; rec[2] = __int_as_float(I); rec[3] = 1.f;
+    }
+}
+
+// per query: merge the block records in order, decode the argmax, then
+// normalise the priors of the query's slices (zeros beyond them)
+__global__ void __launch_bounds__(256) dec_full_merge(FullArgs FA) {
+    const DecArgs &A = FA.A;
+    __shared__ float sM, sZ;
+    const int32_t q = blockIdx.x;
+    int32_t r, g, op;
+    const bool ok = query_valid(A, q, &r, &g, &op);
+    const int32_t nd = ok ? A.dev_off[g + 1] - A.dev_off[g] : 0;
+    const int32_t S_q = ok ? 4 * ((1 << nd) - 1) : 0;
+    if (threadIdx.x == 0) {
+        float M = -INFINITY, Z = 0.f;
+        int32_t I = INT32_MAX;
+        for (int32_t c = 0; c < FA.NB; ++c) {
+            const float *rec = FA.rec + ((int64_t)q * FA.NB + c) * 4;
+            const float m2 = rec[0];
+            if (!(rec[3] > 0.f) || m2 == -INFINITY) continue;
+            const float nm = fmaxf(M, m2);
+            Z = (M == -INFINITY ? 0.f : Z * __expf(M - nm)) + rec[1] * __expf(m2 - nm);
+            const int32_t i2 = __float_as_int(rec[2]);
+            if (m2 > M || (m2 == M && i2 < I)) I = i2;
+            M = nm;
+        }
+        sM = M;
+        sZ = Z;
+        if (!ok || I == INT32_MAX) {
+            A.argmax[q] = -1;
+            A.best[q] = __builtin_nanf("");
+            if (A.dec) A.dec[q] = tag_decision{0, 0, 0, 0, 0};
+        } else {
+            A.argmax[q] = I;
+            A.best[q] = M;
+            if (A.dec) {
+                const uint64_t msk = (uint64_t)(I / 4 + 1);
+                const int o = I % 4;
+                const int pc = __popcll(msk);
+                A.dec[q] = tag_decision{msk, o, o == 3 ? 1 : pc, o == 0 ? 0 : (o == 1 ? 1 : 2), o == 2 ? 1 : 0};
+            }
+        }
+    }
+    __syncthreads();
+    if (!A.prior) return;
+    const float M = sM, inv = sZ > 0.f ? 1.f / sZ : 0.f;
+    float *row = A.prior + (int64_t)q * FA.S_full;
+    for (int32_t a = threadIdx.x; a < FA.S_full; a += blockDim.x)
+        row[a] = a < S_q && ok ? __expf(row[a] - M) * inv : 0.f;
+}
+
+struct FullLayout {
+    float *t, *v, *rec;
+    int32_t *qrow;
+};
+
+int32_t full_blocks(int32_t Q, int32_t max_dev) {
+    // enough blocks to fill the chip, at least 64 masks per wavefront
+    const int64_t masks = (int64_t)1 << max_dev;
+    const int64_t by_work = std::max<int64_t>(1, masks / (4 * 64));
+    const int64_t by_fill = std::max<int64_t>(1, 2048 / std::max(Q, 1));
+    return (int32_t)std::min(by_work, by_fill);
+}
+
+size_t carve_full(const tag_graph *g, int32_t Hx, int32_t R, int32_t Q, void *base, FullLayout *L) {
+    Carver c(base);
+    L->t = c.take<float>((size_t)R * g->n_dev * Hx);
+    L->v = c.take<float>((size_t)std::max(Q, 1) * Hx);
+    L->rec = c.take<float>((size_t)std::max(Q, 1) * full_blocks(Q, g->max_dev) * 4);
+    L->qrow = c.take<int32_t>((size_t)std::max(Q, 1));
+    return c.used;
+}
+
+}  // namespace
+}  // namespace tag
+
+extern "C" tag_status tag_gnn_decide_full_workspace(const tag_graph *g, const tag_model_dims *dims,
+                                                    int32_t n_replicas, int32_t n_query, size_t *bytes) {
+    clear_error();
+    if (!g || !dims || !bytes) TAG_FAIL(TAG_EINVAL, "graph, dims and bytes must be non-NULL");
+    if (n_replicas < 1 || n_query < 0) TAG_FAIL(TAG_EINVAL, "need n_replicas >= 1, n_query >= 0");
+    if (dims->dec_hidden < 0 || dims->dec_hidden > 512) TAG_FAIL(TAG_ESHAPE, "full enumeration needs dec_hidden <= 512");
+    if (g->max_dev > 16) TAG_FAIL(TAG_ESHAPE, "full enumeration needs at most 16 devices per topology");
+    FullLayout L;
+    *bytes = carve_full(g, std::max(dims->dec_hidden, 1), n_replicas, n_query, nullptr, &L);
+    return TAG_OK;
+}
+
+extern "C" tag_status tag_gnn_decide_full(const tag_graph *g, const tag_model_dims *dims, const tag_weights *w,
+                                          int32_t n_replicas, const float *E_op, const float *E_dev,
+                                          int32_t n_query, const int32_t *query_rep, const int32_t *query_graph,
+                                          const int32_t *query_op, int32_t *argmax, float *best_score,
+                                          float *prior, tag_decision *decision, void *workspace, size_t ws_bytes,
+                                          void *hip_stream) {
+    clear_error();
+    if (!g || !dims || !w || !E_op || !E_dev) TAG_FAIL(TAG_EINVAL, "NULL argument");
+    if (dims->f != 64 && dims->f != 128 && dims->f != 256) TAG_FAIL(TAG_ESHAPE, "f must be 64, 128 or 256");
+    if (dims->dec_hidden < 0 || dims->dec_hidden > 512) TAG_FAIL(TAG_ESHAPE, "full enumeration needs dec_hidden <= 512");
+    if (g->max_dev > 16) TAG_FAIL(TAG_ESHAPE, "full enumeration needs at most 16 devices per topology");
+    if (n_replicas < 1) TAG_FAIL(TAG_EINVAL, "n_replicas must be >= 1");
+    if (n_query < 0) TAG_FAIL(TAG_EINVAL, "n_query must be >= 0");
+    if (n_query == 0) return TAG_OK;
+    if (!query_rep || !query_graph || !query_op || !argmax || !best_score)
+        TAG_FAIL(TAG_EINVAL, "query arrays, argmax and best_score must be non-NULL");
+    if (!w->dec_w2 || !w->dec_b2 || (dims->dec_hidden > 0 && (!w->dec_w1 || !w->dec_b1)))
+        TAG_FAIL(TAG_EINVAL, "decoder weights must be non-NULL");
+    if (!workspace) TAG_FAIL(TAG_EINVAL, "workspace must be non-NULL");
+    const int32_t H = dims->dec_hidden, Hx = std::max(H, 1);
+    FullLayout L;
+    if (carve_full(g, Hx, n_replicas, n_query, nullptr, &L) > ws_bytes)
+        TAG_FAIL(TAG_ENOSPACE, "workspace too small (see tag_gnn_decide_full_workspace)");
+    carve_full(g, Hx, n_replicas, n_query, workspace, &L);
+    hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+    FullArgs FA{};
+    DecArgs &A = FA.A;
+    A.R = n_replicas; A.G = g->G; A.S = 0; A.Q = n_query; A.F = dims->f; A.H = H; A.Hx = Hx;
+    A.n_op = g->n_op; A.n_dev = g->n_dev;
+    A.op_off = g->op_off_d; A.dev_off = g->dev_off_d;
+    A.E_op = E_op; A.E_dev = E_dev;
+    A.P = H > 0 ? w->dec_w1 : w->dec_w2;
+    A.b1 = w->dec_b1; A.w2 = w->dec_w2; A.b2 = w->dec_b2;
+    A.q_rep = query_rep; A.q_graph = query_graph; A.q_op = query_op;
+    A.t = L.t; A.v = L.v;
+    A.argmax = argmax; A.best = best_score; A.prior = prior; A.dec = decision;
+    FA.NB = full_blocks(n_query, g->max_dev);
+    FA.S_full = 4 * ((1 << std::max(g->max_dev, 1)) - 1);
+    FA.rec = L.rec;
+    const int din = 2 * A.F + 4;
+    launch_small_gemm(SmallGemm{E_dev, A.F, (int64_t)A.R * A.n_dev, nullptr, A.F, A.P, din, Hx, nullptr, 0,
+                                A.t, Hx, 0}, stream);
+    dec_query_rows<<<grid_for(A.Q), 256, 0, stream>>>(A, L.qrow);
+    launch_small_gemm(SmallGemm{E_op, A.F, A.Q, L.qrow, A.F, A.P + A.F, din, Hx, nullptr, 0, A.v, Hx, 0}, stream);
+    const size_t sh = sizeof(float) * (size_t)21 * Hx;
+    const unsigned grid = (unsigned)((int64_t)n_query * FA.NB);
+    const int hpl = (Hx + 63) / 64;
+    if (hpl <= 1) dec_full<1><<<grid, 256, sh, stream>>>(FA);
+    else if (hpl <= 2) dec_full<2><<<grid, 256, sh, stream>>>(FA);
+    else if (hpl <= 4) dec_full<4><<<grid, 256, sh, stream>>>(FA);
+    else dec_full<8><<<grid, 256, sh, stream>>>(FA);
+    dec_full_merge<<<(unsigned)n_query, 256, 0, stream>>>(FA);
+    return launch_status("tag_gnn_decide_full");
+}
