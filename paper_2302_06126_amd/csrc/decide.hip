@@ -402,6 +402,121 @@ __global__ void __launch_bounds__(256) dec_full(FullArgs FA) {
     }
 }
 
+// One lane per run of kFullRun consecutive Gray indices from an aligned
+// start (H <= 128): the device part of the pre-activation lives in the
+// lane's registers, and since all lanes sit at the same offset inside
+// their runs, every step toggles the same device j = ctz(step) in all
+// lanes; the t row of j, the option bases and w2 are wave-uniform reads.
+constexpr int kFullRun = 16;
+
+struct FullTpm {
+    FullArgs FA;
+    const float *base;     // [Q][4][HP]: W1_opt + b1 + v_q (zero past H)
+    const float *w2p;      // [HP] (zero past H)
+};
+
+template <int HP>
+__global__ void __launch_bounds__(256) dec_full_tpm(FullTpm T) {
+    const FullArgs &FA = T.FA;
+    const DecArgs &A = FA.A;
+    __shared__ float rm[4], rz[4];
+    __shared__ int32_t ri[4];
+    const int32_t q = blockIdx.x / FA.NB, c = blockIdx.x % FA.NB;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    int32_t r, g, op;
+    float *rec = FA.rec + ((int64_t)q * FA.NB + c) * 4;
+    if (!query_valid(A, q, &r, &g, &op)) {
+        if (threadIdx.x == 0) { rec[0] = -INFINITY; rec[1] = 0.f; rec[2] = __int_as_float(INT32_MAX); rec[3] = 0.f; }
+        return;
+    }
+    const int32_t d0 = A.dev_off[g], nd = A.dev_off[g + 1] - d0;
+    const int H = A.Hx;
+    const int64_t total = (int64_t)1 << nd;
+    const int run = total < kFullRun ? (int)total : kFullRun;
+    const int64_t g0 = ((int64_t)c * 256 + threadIdx.x) * run;
+    const float *trow = A.t + ((int64_t)r * A.n_dev + d0) * H;
+    const float *bq = T.base + (int64_t)q * 4 * HP;
+    float m = -INFINITY, z = 0.f;
+    int32_t im = INT32_MAX;
+    if (g0 < total) {
+        uint32_t mask = (uint32_t)(g0 ^ (g0 >> 1));
+        float ds[HP];
+#pragma unroll
+        for (int h = 0; h < HP; ++h) ds[h] = 0.f;
+        for (int j = 0; j < nd; ++j) {
+            if (!((mask >> j) & 1u)) continue;
+#pragma unroll
+            for (int h = 0; h < HP; ++h)
+                if (h < H) ds[h] += trow[(int64_t)j * H + h];
+        }
+        for (int st = 0; st < run; ++st) {
+            if (st > 0) {
+                const int j = __builtin_ctz((unsigned)st);   // same in every lane
+                mask ^= 1u << j;
+                const float sg = ((mask >> j) & 1u) ? 1.f : -1.f;
+#pragma unroll
+                for (int h = 0; h < HP; ++h)
+                    if (h < H) ds[h] = fmaf(sg, trow[(int64_t)j * H + h], ds[h]);
+            }
+            if (mask == 0) continue;
+            float s[4];
+#pragma unroll
+            for (int o = 0; o < 4; ++o) {
+                float acc = 0.f;
+#pragma unroll
+                for (int h = 0; h < HP; ++h) acc = fmaf(T.w2p[h], fmaxf(ds[h] + bq[o * HP + h], 0.f), acc);
+                s[o] = A.b2[0] + acc;
+            }
+            const int32_t a0 = (int32_t)(4 * (mask - 1));
+            if (A.prior)
+                *reinterpret_cast<float4 *>(A.prior + (int64_t)q * FA.S_full + a0) = float4{s[0], s[1], s[2], s[3]};
+#pragma unroll
+            for (int o = 0; o < 4; ++o) {
+                if (s[o] > m) { z = z * __expf(m - s[o]) + 1.f; m = s[o]; im = a0 + o; }
+                else { z += __expf(s[o] - m); if (s[o] == m && a0 + o < im) im = a0 + o; }
+            }
+        }
+    }
+    // wavefront merge of the lanes' (max, sum, argmax), then the block's four
+    for (int o = 32; o >= 1; o >>= 1) {
+        const float m2 = __shfl_xor(m, o, 64), z2 = __shfl_xor(z, o, 64);
+        const int32_t i2 = __shfl_xor(im, o, 64);
+        const float nm = fmaxf(m, m2);
+        if (nm != -INFINITY) {
+            z = (m == -INFINITY ? 0.f : z * __expf(m - nm)) + (m2 == -INFINITY ? 0.f : z2 * __expf(m2 - nm));
+            if (m2 > m || (m2 == m && i2 < im)) im = i2;
+            m = nm;
+        }
+    }
+    if (lane == 0) { rm[wv] = m; rz[wv] = z; ri[wv] = im; }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float M = -INFINITY, Z = 0.f;
+        int32_t I = INT32_MAX;
+        for (int k = 0; k < 4; ++k) {
+            const float m2 = rm[k];
+            if (m2 == -INFINITY) continue;
+            const float nm = fmaxf(M, m2);
+            Z = (M == -INFINITY ? 0.f : Z * __expf(M - nm)) + rz[k] * __expf(m2 - nm);
+            if (m2 > M || (m2 == M && ri[k] < I)) I = ri[k];
+            M = nm;
+        }
+        rec[0] = M; rec[1] = Z; rec[2] = __int_as_float(I); rec[3] = 1.f;
+    }
+}
+
+// option bases of every query and the padded readout
+__global__ void dec_full_base(DecArgs A, int HP, float *base, float *w2p) {
+    const int din = 2 * A.F + 4;
+    const int64_t total = (int64_t)A.Q * 4 * HP;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const int h = (int)(i % HP), o = (int)((i / HP) % 4);
+        const int64_t q = i / (4 * HP);
+        base[i] = h < A.H ? A.P[(int64_t)h * din + 2 * A.F + o] + A.b1[h] + A.v[q * A.Hx + h] : 0.f;
+        if (i < HP) w2p[i] = i < A.H ? A.w2[i] : 0.f;
+    }
+}
+
 // per query: merge the block records in order, decode the argmax, then
 // normalise the priors of the query's slices (zeros beyond them)
 __global__ void __launch_bounds__(256) dec_full_merge(FullArgs FA) {
@@ -451,24 +566,33 @@ __global__ void __launch_bounds__(256) dec_full_merge(FullArgs FA) {
 }
 
 struct FullLayout {
-    float *t, *v, *rec;
+    float *t, *v, *rec, *base, *w2p;
     int32_t *qrow;
 };
 
-int32_t full_blocks(int32_t Q, int32_t max_dev) {
-    // enough blocks to fill the chip, at least 64 masks per wavefront
+// padded hidden width of the lane-per-mask kernel (0: lanes over hidden units)
+int full_hp(int32_t H) { return H == 0 || H > 128 ? 0 : (H <= 32 ? 32 : (H <= 64 ? 64 : 128)); }
+
+int32_t full_blocks(int32_t Q, int32_t max_dev, int32_t H) {
     const int64_t masks = (int64_t)1 << max_dev;
+    if (full_hp(H))   // one lane per run of kFullRun masks
+        return (int32_t)std::max<int64_t>(1, (masks / kFullRun + 255) / 256);
+    // enough blocks to fill the chip, at least 64 masks per wavefront
     const int64_t by_work = std::max<int64_t>(1, masks / (4 * 64));
     const int64_t by_fill = std::max<int64_t>(1, 2048 / std::max(Q, 1));
     return (int32_t)std::min(by_work, by_fill);
 }
 
-size_t carve_full(const tag_graph *g, int32_t Hx, int32_t R, int32_t Q, void *base, FullLayout *L) {
+size_t carve_full(const tag_graph *g, int32_t H, int32_t R, int32_t Q, void *base, FullLayout *L) {
     Carver c(base);
+    const int32_t Hx = std::max(H, 1);
     L->t = c.take<float>((size_t)R * g->n_dev * Hx);
     L->v = c.take<float>((size_t)std::max(Q, 1) * Hx);
-    L->rec = c.take<float>((size_t)std::max(Q, 1) * full_blocks(Q, g->max_dev) * 4);
+    L->rec = c.take<float>((size_t)std::max(Q, 1) * full_blocks(Q, g->max_dev, H) * 4);
     L->qrow = c.take<int32_t>((size_t)std::max(Q, 1));
+    const int hp = full_hp(H);
+    L->base = hp ? c.take<float>((size_t)std::max(Q, 1) * 4 * hp) : nullptr;
+    L->w2p = hp ? c.take<float>((size_t)hp) : nullptr;
     return c.used;
 }
 
@@ -483,7 +607,7 @@ extern "C" tag_status tag_gnn_decide_full_workspace(const tag_graph *g, const ta
     if (dims->dec_hidden < 0 || dims->dec_hidden > 512) TAG_FAIL(TAG_ESHAPE, "full enumeration needs dec_hidden <= 512");
     if (g->max_dev > 16) TAG_FAIL(TAG_ESHAPE, "full enumeration needs at most 16 devices per topology");
     FullLayout L;
-    *bytes = carve_full(g, std::max(dims->dec_hidden, 1), n_replicas, n_query, nullptr, &L);
+    *bytes = carve_full(g, dims->dec_hidden, n_replicas, n_query, nullptr, &L);
     return TAG_OK;
 }
 
@@ -508,9 +632,9 @@ extern "C" tag_status tag_gnn_decide_full(const tag_graph *g, const tag_model_di
     if (!workspace) TAG_FAIL(TAG_EINVAL, "workspace must be non-NULL");
     const int32_t H = dims->dec_hidden, Hx = std::max(H, 1);
     FullLayout L;
-    if (carve_full(g, Hx, n_replicas, n_query, nullptr, &L) > ws_bytes)
+    if (carve_full(g, H, n_replicas, n_query, nullptr, &L) > ws_bytes)
         TAG_FAIL(TAG_ENOSPACE, "workspace too small (see tag_gnn_decide_full_workspace)");
-    carve_full(g, Hx, n_replicas, n_query, workspace, &L);
+    carve_full(g, H, n_replicas, n_query, workspace, &L);
     hipStream_t stream = static_cast<hipStream_t>(hip_stream);
     FullArgs FA{};
     DecArgs &A = FA.A;
@@ -523,7 +647,7 @@ extern "C" tag_status tag_gnn_decide_full(const tag_graph *g, const tag_model_di
     A.q_rep = query_rep; A.q_graph = query_graph; A.q_op = query_op;
     A.t = L.t; A.v = L.v;
     A.argmax = argmax; A.best = best_score; A.prior = prior; A.dec = decision;
-    FA.NB = full_blocks(n_query, g->max_dev);
+    FA.NB = full_blocks(n_query, g->max_dev, H);
     FA.S_full = 4 * ((1 << std::max(g->max_dev, 1)) - 1);
     FA.rec = L.rec;
     const int din = 2 * A.F + 4;
@@ -531,8 +655,18 @@ extern "C" tag_status tag_gnn_decide_full(const tag_graph *g, const tag_model_di
                                 A.t, Hx, 0}, stream);
     dec_query_rows<<<grid_for(A.Q), 256, 0, stream>>>(A, L.qrow);
     launch_small_gemm(SmallGemm{E_op, A.F, A.Q, L.qrow, A.F, A.P + A.F, din, Hx, nullptr, 0, A.v, Hx, 0}, stream);
-    const size_t sh = sizeof(float) * (size_t)21 * Hx;
     const unsigned grid = (unsigned)((int64_t)n_query * FA.NB);
+    const int hp = full_hp(H);
+    if (hp) {
+        dec_full_base<<<grid_for((int64_t)n_query * 4 * hp), 256, 0, stream>>>(A, hp, L.base, L.w2p);
+        FullTpm T{FA, L.base, L.w2p};
+        if (hp == 32) dec_full_tpm<32><<<grid, 256, 0, stream>>>(T);
+        else if (hp == 64) dec_full_tpm<64><<<grid, 256, 0, stream>>>(T);
+        else dec_full_tpm<128><<<grid, 256, 0, stream>>>(T);
+        dec_full_merge<<<(unsigned)n_query, 256, 0, stream>>>(FA);
+        return launch_status("tag_gnn_decide_full");
+    }
+    const size_t sh = sizeof(float) * (size_t)21 * Hx;
     const int hpl = (Hx + 63) / 64;
     if (hpl <= 1) dec_full<1><<<grid, 256, sh, stream>>>(FA);
     else if (hpl <= 2) dec_full<2><<<grid, 256, sh, stream>>>(FA);
