@@ -136,7 +136,7 @@ __global__ void __launch_bounds__(256) gemm_f32(Gemm G) {
 // split count for a k-range of K rows over `tiles` output tiles: enough
 // blocks to fill the chip, at least 4 k-chunks per split
 int64_t split_k_per(int64_t K, int64_t tiles, int64_t *splits) {
-    int64_t s = std::max<int64_t>(1, std::min<int64_t>(256 / std::max<int64_t>(tiles, 1), (K + 63) / 64));
+    int64_t s = std::max<int64_t>(1, std::min<int64_t>(1024 / std::max<int64_t>(tiles, 1), (K + 63) / 64));
     int64_t per = ((K + s - 1) / s + GK - 1) / GK * GK;
     per = std::max<int64_t>(per, GK);
     *splits = std::max<int64_t>(1, (K + per - 1) / per);
@@ -212,9 +212,9 @@ struct BwdBucket {
     float *Z; int zsel;               // [R*n_dst][2][K] per-destination dz sums
 };
 
-constexpr int kChunkA = 64;     // entries per score item
-constexpr int kChunkB = 256;    // entries per message item
-constexpr int kPersist = 1024;  // blocks of the passes that sum parameter gradients
+constexpr int kChunkA = 32;     // entries per score item
+constexpr int kChunkB = 128;    // entries per message item
+constexpr int kPersist = 2048;  // blocks of the passes that sum parameter gradients
 
 __device__ __forceinline__ void edge_x(const BwdLayer &P, int xkind, int32_t rep, int32_t id, float &x0, float &x1) {
     if (xkind == 0) {
