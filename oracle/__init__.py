@@ -35,7 +35,7 @@ class _Dims(C.Structure):
     _fields_ = [("f", C.c_int32), ("heads", C.c_int32), ("layers", C.c_int32),
                 ("f_op", C.c_int32), ("f_dev", C.c_int32), ("dec_hidden", C.c_int32),
                 ("bf16", C.c_int32), ("gamma_same", C.c_double),
-                ("gamma_cross", C.c_double), ("leaky_slope", C.c_double)]
+                ("gamma_cross", C.c_double), ("leaky_slope", C.c_double), ("sigma", C.c_int32)]
 
 
 _FP = C.POINTER(C.c_float)
@@ -100,9 +100,9 @@ def csr(n_op: int, n_dev: int, oo_src, oo_dst, dd_a, dd_b, od_op, od_dev
     return OK, [(rp, c[:n], e[:n]) for (rp, c, e), (_, n) in zip(outs, shapes)]
 
 
-def _dims(f, heads, layers, f_op, f_dev, dec_hidden, bf16, gamma_same, gamma_cross, slope):
+def _dims(f, heads, layers, f_op, f_dev, dec_hidden, bf16, gamma_same, gamma_cross, slope, sigma=0):
     return _Dims(f, heads, layers, f_op, f_dev, dec_hidden, 1 if bf16 else 0,
-                 gamma_same, gamma_cross, slope)
+                 gamma_same, gamma_cross, slope, sigma)
 
 
 def _weights(w: Dict[str, np.ndarray]):
@@ -123,7 +123,7 @@ def _weights(w: Dict[str, np.ndarray]):
 def forward(topo, x_op, x_dev, x_oo, x_dd, x_od, w: Dict[str, np.ndarray], *,
             f: int, heads: int, layers: int, bf16: bool = False,
             gamma_same: float = 1.0, gamma_cross: float = 0.1, leaky_slope: float = 0.2,
-            want_alpha: bool = False):
+            want_alpha: bool = False, sigma: str = "relu"):
     """E_op [N, f], E_dev [M, f] (float64) for one candidate graph; with
     want_alpha also the layer-0 attention weights [T, heads] in bucket order
     B0, B1, B2, B3 (each bucket in CSR order)."""
@@ -131,8 +131,10 @@ def forward(topo, x_op, x_dev, x_oo, x_dd, x_od, w: Dict[str, np.ndarray], *,
     x_oo, x_dd = _f32(x_oo).reshape(-1), _f32(x_dd).reshape(-1)
     x_od = np.ascontiguousarray(np.asarray(x_od, dtype=np.uint8)).reshape(-1)
     n, m = topo.n_op, topo.n_dev
+    if sigma not in ("relu", "elu"):
+        raise ValueError(sigma)
     dims = _dims(f, heads, layers, x_op.shape[1] if x_op.ndim == 2 else 0, 8,
-                 0, bf16, gamma_same, gamma_cross, leaky_slope)
+                 0, bf16, gamma_same, gamma_cross, leaky_slope, 1 if sigma == "elu" else 0)
     ws, keep = _weights(w)
     E_op = np.zeros((n, f), np.float64)
     E_dev = np.zeros((m, f), np.float64)

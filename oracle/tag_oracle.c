@@ -33,6 +33,7 @@
 typedef struct {
     int32_t f, heads, layers, f_op, f_dev, dec_hidden, bf16;
     double gamma_same, gamma_cross, leaky_slope;
+    int32_t sigma;   /* message non-linearity: 0 ReLU, 1 ELU (alpha = 1) */
 } tago_dims;
 
 typedef struct {
@@ -193,7 +194,8 @@ static void aggregate_row(const tago_dims *d, int32_t beg, int32_t end,
         const double *te = od_bits ? edge_term + (size_t)od_bits[id] * f : edge_term + (size_t)id * f;
         for (int c = 0; c < f; ++c) {
             double z = ysrc[(size_t)v * f + c] + te[c];
-            scratch_m[(size_t)e * f + c] = z > 0.0 ? z : 0.0;
+            /* sigma of the layer equation (Section 4.2.1): ReLU, or ELU as a variant */
+            scratch_m[(size_t)e * f + c] = z > 0.0 ? z : (d->sigma == 1 ? expm1(z) : 0.0);
         }
     }
     for (int k = 0; k < K; ++k) {

@@ -44,16 +44,18 @@ def _buckets(topo):
     return b0, b1, b2, b3
 
 
-def _aggregate(bucket, n_dst, ysrc, ydst, te, a, ad, heads, slope):
+def _aggregate(bucket, n_dst, ysrc, ydst, te, a, ad, heads, slope, sigma="relu"):
     """sum over the destination's entries of softmax_e(logit_e) m_e, per head:
-    m_e = ReLU(W^h h_src + W^e e + b), logit_e = LeakyReLU(a . m_e + a~ . W^h h_dst)."""
+    m_e = sigma(W^h h_src + W^e e + b) (ReLU, or ELU as a variant),
+    logit_e = LeakyReLU(a . m_e + a~ . W^h h_dst)."""
     dst, src, eid = bucket
     f = ysrc.shape[1]
     d = f // heads
     E = dst.numel()
     if E == 0:
         return torch.zeros((n_dst, f), dtype=torch.float64)
-    m = torch.relu(ysrc[src] + te[eid])
+    pre = ysrc[src] + te[eid]
+    m = torch.nn.functional.elu(pre) if sigma == "elu" else torch.relu(pre)
     s = (m * a).view(E, heads, d).sum(-1) + (ydst * ad).view(-1, heads, d).sum(-1)[dst]
     s = torch.where(s > 0, s, slope * s)
     mx = torch.full((n_dst, heads), -np.inf, dtype=torch.float64)
@@ -66,7 +68,7 @@ def _aggregate(bucket, n_dst, ysrc, ydst, te, a, ad, heads, slope):
 
 
 def forward(topo, x_op, x_dev, x_oo, x_dd, x_od, P: Dict[str, torch.Tensor], *, f, heads, layers,
-            gamma_same=1.0, gamma_cross=0.1, slope=0.2):
+            gamma_same=1.0, gamma_cross=0.1, slope=0.2, sigma="relu"):
     """E_op [N, f], E_dev [M, f] as float64 tensors."""
     xo, xd = _t(x_op), _t(x_dev)
     h_op = torch.relu(xo @ P["enc_op_w"].T + P["enc_op_b"])
@@ -90,10 +92,10 @@ def forward(topo, x_op, x_dev, x_oo, x_dd, x_od, P: Dict[str, torch.Tensor], *, 
         y_od_op = h_op @ Wh[1].T
         y_od_dev = h_dev @ Wh[1].T
         y_dd = h_dev @ Wh[2].T
-        n_op = gamma_same * _aggregate(b0, N, y_oo, y_oo, te_oo, a[0], ad[0], heads, slope) \
-            + gamma_cross * _aggregate(b1, N, y_od_dev, y_od_op, te_od, a[1], ad[1], heads, slope)
-        n_dev = gamma_cross * _aggregate(b2, M, y_od_op, y_od_dev, te_od, a[1], ad[1], heads, slope) \
-            + gamma_same * _aggregate(b3, M, y_dd, y_dd, te_dd, a[2], ad[2], heads, slope)
+        n_op = gamma_same * _aggregate(b0, N, y_oo, y_oo, te_oo, a[0], ad[0], heads, slope, sigma) \
+            + gamma_cross * _aggregate(b1, N, y_od_dev, y_od_op, te_od, a[1], ad[1], heads, slope, sigma)
+        n_dev = gamma_cross * _aggregate(b2, M, y_od_op, y_od_dev, te_od, a[1], ad[1], heads, slope, sigma) \
+            + gamma_same * _aggregate(b3, M, y_dd, y_dd, te_dd, a[2], ad[2], heads, slope, sigma)
         h_op, h_dev = n_op, n_dev
     return h_op, h_dev
 
@@ -118,7 +120,7 @@ def scores(E_op, E_dev, masks, options, query_op, P, *, f):
 
 
 def loss_and_grads(items: Sequence[dict], w: Dict[str, np.ndarray], *, f, heads, layers, masks, options,
-                   gamma_same=1.0, gamma_cross=0.1, slope=0.2):
+                   gamma_same=1.0, gamma_cross=0.1, slope=0.2, sigma="relu"):
     """`items`: one dict per replica with its topology, features, query ops
     and targets [Q_r, S].  Returns (loss, {name: gradient as float64 numpy
     in the parameter's own shape}); the loss is the mean over all queries."""
@@ -130,7 +132,7 @@ def loss_and_grads(items: Sequence[dict], w: Dict[str, np.ndarray], *, f, heads,
     for it in items:
         E_op, E_dev = forward(it["topo"], it["x_op"], it["x_dev"], it["x_oo"], it["x_dd"], it["x_od"], P,
                               f=f, heads=heads, layers=layers, gamma_same=gamma_same,
-                              gamma_cross=gamma_cross, slope=slope)
+                              gamma_cross=gamma_cross, slope=slope, sigma=sigma)
         sc = scores(E_op, E_dev, masks, options, it["query_op"], P, f=f)
         lp = torch.log_softmax(sc, dim=1)
         terms.append(-(_t(it["target"]) * lp).sum())

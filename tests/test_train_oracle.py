@@ -29,12 +29,12 @@ def _case(seed, n=14, m=3, e=20, f=32, heads=4, layers=2, R=2, S=12, Q=3):
     return topo, w, masks, opts, items, dict(f=f, heads=heads, layers=layers)
 
 
-def _c_loss(w, masks, opts, items, dims):
+def _c_loss(w, masks, opts, items, dims, sigma="relu"):
     """Cross entropy of the C oracle's priors (float64)."""
     tot, Qn = 0.0, 0
     for it in items:
         E_op, E_dev = oracle.forward(it["topo"], it["x_op"], it["x_dev"], it["x_oo"], it["x_dd"], it["x_od"], w,
-                                     f=dims["f"], heads=dims["heads"], layers=dims["layers"])
+                                     f=dims["f"], heads=dims["heads"], layers=dims["layers"], sigma=sigma)
         od = oracle.decide(E_op, E_dev, masks, opts, it["query_op"], w, f=dims["f"], dec_hidden=dims["f"],
                            n_dev=it["topo"].n_dev, want_prior=True)
         tot -= float((it["target"] * np.log(od["prior"])).sum())
@@ -42,13 +42,16 @@ def _c_loss(w, masks, opts, items, dims):
     return tot / Qn
 
 
-def test_forward_matches_c_oracle():
+@pytest.mark.parametrize("sigma", ["relu", "elu"])
+def test_forward_matches_c_oracle(sigma):
     for seed in (1, 2):
         topo, w, masks, opts, items, dims = _case(seed)
         P = {k: OT._t(w[k]) for k in OT.PARAMS}
         it = items[0]
-        E_op, E_dev = OT.forward(topo, it["x_op"], it["x_dev"], it["x_oo"], it["x_dd"], it["x_od"], P, **dims)
-        R_op, R_dev = oracle.forward(topo, it["x_op"], it["x_dev"], it["x_oo"], it["x_dd"], it["x_od"], w, **dims)
+        E_op, E_dev = OT.forward(topo, it["x_op"], it["x_dev"], it["x_oo"], it["x_dd"], it["x_od"], P, **dims,
+                                 sigma=sigma)
+        R_op, R_dev = oracle.forward(topo, it["x_op"], it["x_dev"], it["x_oo"], it["x_dd"], it["x_od"], w, **dims,
+                                     sigma=sigma)
         np.testing.assert_allclose(E_op.detach().numpy(), R_op, rtol=1e-11, atol=1e-13)
         np.testing.assert_allclose(E_dev.detach().numpy(), R_dev, rtol=1e-11, atol=1e-13)
 
@@ -59,11 +62,12 @@ def test_loss_matches_c_oracle_cross_entropy():
     assert loss == pytest.approx(_c_loss(w, masks, opts, items, dims), rel=1e-11)
 
 
-def test_gradient_matches_central_differences():
+@pytest.mark.parametrize("sigma", ["relu", "elu"])
+def test_gradient_matches_central_differences(sigma):
     """Every parameter array: a few entries, differentiated numerically
     through the C oracle (perturbations representable in float32)."""
     topo, w, masks, opts, items, dims = _case(4, f=16, heads=2, layers=2, S=8)
-    _, g = OT.loss_and_grads(items, w, masks=masks, options=opts, **dims)
+    _, g = OT.loss_and_grads(items, w, masks=masks, options=opts, **dims, sigma=sigma)
     rng = synth.rng_for(72)
     for k in OT.PARAMS:
         flat = w[k].reshape(-1)
@@ -77,9 +81,18 @@ def test_gradient_matches_central_differences():
             wm[k].reshape(-1)[i] = np.float32(x0 - h)
             hp = float(wp[k].reshape(-1)[i]) - x0
             hm = x0 - float(wm[k].reshape(-1)[i])
-            fd = (_c_loss(wp, masks, opts, items, dims) - _c_loss(wm, masks, opts, items, dims)) / (hp + hm)
+            lp, lm = _c_loss(wp, masks, opts, items, dims, sigma), _c_loss(wm, masks, opts, items, dims, sigma)
+            fd = (lp - lm) / (hp + hm)
             an = float(g[k].reshape(-1)[i])
-            assert abs(fd - an) <= 1e-4 * max(abs(an), abs(fd)) + 2e-8, (k, int(i), fd, an)
+            if abs(fd - an) <= 1e-4 * max(abs(an), abs(fd)) + 2e-8:
+                continue
+            # a ReLU / LeakyReLU kink inside [x - h, x + h]: the one-sided
+            # differences then disagree and the derivative lies between them
+            l0 = _c_loss(w, masks, opts, items, dims, sigma)
+            up, dn = (lp - l0) / hp, (l0 - lm) / hm
+            lo, hi = min(up, dn), max(up, dn)
+            tol = 1e-4 * max(abs(up), abs(dn)) + 2e-8
+            assert lo - tol <= an <= hi + tol, (k, int(i), fd, an, up, dn)
 
 
 def test_targets_equal_to_priors_give_zero_gradient():
@@ -92,3 +105,47 @@ def test_targets_equal_to_priors_give_zero_gradient():
     _, g = OT.loss_and_grads(items, w, masks=masks, options=opts, **dims)
     for k in OT.PARAMS:
         assert np.abs(g[k]).max() <= 1e-12, k
+
+
+def _biased(seed, bias):
+    """A case whose message pre-activations all share the sign of `bias`
+    (the folded bias c' = W^e c + b dominates every W^h h + U x)."""
+    topo, w, masks, opts, items, dims = _case(seed, layers=1)
+    w = {k: v.copy() for k, v in w.items()}
+    w["layer_b"][:] = bias
+    return topo, w, items, dims
+
+
+def test_elu_equals_relu_when_every_message_is_positive():
+    topo, w, items, dims = _biased(6, 100.0)
+    it = items[0]
+    a = oracle.forward(topo, it["x_op"], it["x_dev"], it["x_oo"], it["x_dd"], it["x_od"], w, **dims, sigma="relu")
+    b = oracle.forward(topo, it["x_op"], it["x_dev"], it["x_oo"], it["x_dd"], it["x_od"], w, **dims, sigma="elu")
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def test_elu_saturates_to_minus_gamma_sum_for_negative_messages():
+    """Every message is ELU(z) with z about -100, i.e. -1 to double precision,
+    so each head's softmax average is -1 and a node's output is minus the sum
+    of gamma over the link types it has neighbours in (ReLU gives zeros)."""
+    topo, w, items, dims = _biased(7, -100.0)
+    it = items[0]
+    E_op, E_dev = oracle.forward(topo, it["x_op"], it["x_dev"], it["x_oo"], it["x_dd"], it["x_od"], w, **dims,
+                                 sigma="elu")
+    R_op, R_dev = oracle.forward(topo, it["x_op"], it["x_dev"], it["x_oo"], it["x_dd"], it["x_od"], w, **dims)
+    assert not np.any(R_op) and not np.any(R_dev)
+    n, m = topo.n_op, topo.n_dev
+    has_oo = np.zeros(n, bool)
+    has_oo[np.asarray(topo.oo_src)] = True
+    has_oo[np.asarray(topo.oo_dst)] = True
+    has_od_op = np.zeros(n, bool)
+    has_od_op[np.asarray(topo.od_op)] = True
+    has_od_dev = np.zeros(m, bool)
+    has_od_dev[np.asarray(topo.od_dev)] = True
+    has_dd = np.zeros(m, bool)
+    has_dd[np.asarray(topo.dd_a)] = True
+    has_dd[np.asarray(topo.dd_b)] = True
+    want_op = -(1.0 * has_oo + 0.1 * has_od_op)
+    want_dev = -(0.1 * has_od_dev + 1.0 * has_dd)
+    np.testing.assert_allclose(E_op, np.repeat(want_op[:, None], dims["f"], 1), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(E_dev, np.repeat(want_dev[:, None], dims["f"], 1), rtol=0, atol=1e-12)
