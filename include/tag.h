@@ -147,11 +147,15 @@ void tag_graph_destroy(tag_graph *g);
  *   gamma_same  gamma for op-op and device-device links (paper: 1)
  *   gamma_cross gamma for op-device links (paper: 0.1)
  *   leaky_slope LeakyReLU slope of the attention score, in [0, 1] (GAT: 0.2)
+ *   sigma       the message non-linearity sigma of the layer equation, which
+ *               the paper leaves open: 0 ReLU, 1 ELU (x > 0 ? x : e^x - 1)
  */
 typedef struct tag_model_dims {
     int32_t f, heads, layers, f_op, f_dev, dec_hidden;
     int32_t dtype;
     float gamma_same, gamma_cross, leaky_slope;
+    int32_t sigma;   /* message non-linearity: 0 ReLU (default), 1 ELU with   */
+                     /* alpha = 1 (a variant; needs dtype TAG_F32)           */
 } tag_model_dims;
 
 /*
@@ -204,7 +208,7 @@ tag_status tag_gnn_workspace(const tag_graph *g, const tag_model_dims *dims,
 /*
  * The forward pass of Section 4.2.1 for every candidate of the batch.
  * Per layer l, link type r, destination u and neighbour v:
- *   m_uv  = ReLU(W^h h_v + W^e e_uv + b)
+ *   m_uv  = sigma(W^h h_v + W^e e_uv + b)       (ReLU, or ELU: dims->sigma)
  *   s_uvk = LeakyReLU(a^(k) . m_uv^(k) + adst^(k) . (W^h h_u)^(k))
  *   alpha = softmax of s over u's neighbours of link type r, per head
  *   h'_u  = sum_r gamma_r sum_v alpha_uv m_uv     (empty bucket: 0)

@@ -15,7 +15,7 @@
  * gamma-weighted sums, the relation transforms and the folded edge encoders)
  * and the node encoders.
  *
- * Scope: fp32 models (dims->dtype TAG_F32) with the MLP decoder
+ * Scope: fp32 models (dims->dtype TAG_F32; ReLU or ELU messages) with the MLP decoder
  * (dec_hidden >= 1) and at most 4096 slices; TAG_ESHAPE otherwise.  A query
  * whose indices are out of range contributes nothing (its loss term and
  * gradient are zero; Q still counts it).  Every reduction runs in a fixed

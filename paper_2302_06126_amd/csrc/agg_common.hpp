@@ -33,6 +33,7 @@ struct AggArgs {
     float g_same, g_cross, slope;
     void *H_op, *H_dev;               // outputs (bf16 hidden or fp32)
     int out_f32;
+    int32_t elu;                      // message non-linearity: 0 ReLU, 1 ELU (fp32 only)
     float *part;                      // device<-op partials
     int32_t maxc;                     // partial records per device row
     // MFMA path
@@ -199,13 +200,13 @@ struct Online {
 };
 
 // message + score of one entry; returns the log2-domain score
-template <int CPL, int LPH>
+template <int CPL, int LPH, bool ELU = false>
 __device__ __forceinline__ float entry_score(const float (&y)[CPL], float x0, float x1, const RelConst<CPL> &k,
                                              float qd, float slope, float (&m)[CPL]) {
     float part = 0.f;
     for (int c = 0; c < CPL; ++c) {
         float z = y[c] + fmaf(k.u0[c], x0, k.u1[c] * x1);   // y = Y + c' as stored
-        m[c] = fmaxf(z, 0.f);
+        m[c] = msg_act<ELU>(z);
         part = fmaf(k.a[c], m[c], part);
     }
     float s = head_sum<LPH>(part) + qd;

@@ -55,7 +55,7 @@ __global__ void __launch_bounds__(256) pack_op_masks(AggArgs A) {
 // Attention terms of node rows when the transform epilogue cannot form them
 // (heads wider than 64 channels): per row, S = (p0, p1, q_od, q_same) and, for
 // device rows, the message table T (bit 0 / 1).  One wavefront per row.
-template <int F, int K, bool BF>
+template <int F, int K, bool BF, bool ELU = false>
 __global__ void __launch_bounds__(256) prep_rows(AggArgs A, int dev_side) {
     constexpr int CPL = F / 64, LPH = 64 / K;
     const int lane = threadIdx.x & 63;
@@ -73,7 +73,7 @@ __global__ void __launch_bounds__(256) prep_rows(AggArgs A, int dev_side) {
     float p0 = 0.f, p1 = 0.f, qo = 0.f, qs = 0.f;
     for (int c = 0; c < CPL; ++c) {
         const float yc = yo[c];   // stored rows hold Y + c'
-        const float t0 = fmaxf(yc, 0.f), t1 = fmaxf(yc + od.u0[c], 0.f);
+        const float t0 = msg_act<ELU>(yc), t1 = msg_act<ELU>(yc + od.u0[c]);
         if (dev_side) {
             if (BF) {
                 reinterpret_cast<unsigned *>(A.T)[i * F + c0 + c] = pack_bf2(t0, t1);
@@ -109,7 +109,7 @@ __device__ __forceinline__ float fdekey(int k) { return __int_as_float(k < 0 ? k
 // accumulate every tile against those fixed maxima, so the device-row
 // accumulators stay in registers across the group, and one (max, sum,
 // partial) record per device row is written at the end.
-template <int F, int K, bool BF>
+template <int F, int K, bool BF, bool ELU = false>
 __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     constexpr int D = F / K;                       // head width (>= 16 here)
     constexpr int WC = F / 4;                      // columns per wavefront
@@ -295,7 +295,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) {
                 const float yc = static_cast<float>(Ys[ul * YS + cbase + cb * 16 + (lane & 15)]);
-                bv[cb] = fmaxf(b ? yc + Uv[cb] : yc, 0.f);
+                bv[cb] = msg_act<ELU>(b ? yc + Uv[cb] : yc);
             }
             float pu[HPW];
 #pragma unroll
@@ -364,7 +364,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
 //  * op <- device: MFMA contraction of the attention weights (formed in
 //    registers) with the device message table.
 // Both parts are combined and each op row is written once.
-template <int F, int K, bool BF>
+template <int F, int K, bool BF, bool ELU = false>
 __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
     constexpr int D = F / K;
     constexpr int WC = F / 4;
@@ -534,7 +534,7 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
                     float part = 0.f;
 #pragma unroll
                     for (int c = 0; c < CPL; ++c) {
-                        m[c] = fmaxf(fmaf(u0c[c], xs[s], slot[s].get(c)), 0.f);
+                        m[c] = msg_act<ELU>(fmaf(u0c[c], xs[s], slot[s].get(c)));
                         part = fmaf(a[c], m[c], part);
                     }
                     const int rl = (e >= rb_[1]) + (e >= rb_[2]) + (e >= rb_[3]);   // row of e in the group
@@ -745,7 +745,7 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
     }
 }
 
-template <int F, int K, bool BF>
+template <int F, int K, bool BF, bool ELU = false>
 void launch_mfma(const AggArgs &A, hipStream_t st) {
     const int64_t op_waves = (int64_t)A.R * A.n_op;
     const int64_t dev_waves = (int64_t)A.R * A.n_dev;
@@ -753,26 +753,26 @@ void launch_mfma(const AggArgs &A, hipStream_t st) {
     const dim3 groups((unsigned)A.n_groups, (unsigned)A.R);
     if (!A.prep_done) {
         prof_begin(TAG_STAGE_DEV_PREP, st);
-        prep_rows<F, K, BF><<<(unsigned)((op_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A, 0);
-        prep_rows<F, K, BF><<<(unsigned)((dev_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A, 1);
+        prep_rows<F, K, BF, ELU><<<(unsigned)((op_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A, 0);
+        prep_rows<F, K, BF, ELU><<<(unsigned)((dev_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A, 1);
         prof_end(TAG_STAGE_DEV_PREP, st);
     }
     prof_begin(TAG_STAGE_AGG_DEV_OP, st);
-    agg_b2<F, K, BF><<<groups, 256, 0, st>>>(A);
+    agg_b2<F, K, BF, ELU><<<groups, 256, 0, st>>>(A);
     prof_end(TAG_STAGE_AGG_DEV_OP, st);
     prof_begin(TAG_STAGE_AGG_OP_DEV, st);
-    agg_op_tile<F, K, BF><<<tiles, 256, 0, st>>>(A);
+    agg_op_tile<F, K, BF, ELU><<<tiles, 256, 0, st>>>(A);
     prof_end(TAG_STAGE_AGG_OP_DEV, st);
 }
 
-template <int F, bool BF>
+template <int F, bool BF, bool ELU = false>
 bool dispatch_mfma_heads(int K, const AggArgs &A, hipStream_t st) {
     switch (K) {
-        case 1: launch_mfma<F, 1, BF>(A, st); return true;
-        case 2: launch_mfma<F, 2, BF>(A, st); return true;
-        case 4: launch_mfma<F, 4, BF>(A, st); return true;
-        case 8: if (F / 8 >= 16) { launch_mfma<F, (F / 8 >= 16 ? 8 : 4), BF>(A, st); return true; } return false;
-        case 16: if (F / 16 >= 16) { launch_mfma<F, (F / 16 >= 16 ? 16 : 4), BF>(A, st); return true; } return false;
+        case 1: launch_mfma<F, 1, BF, ELU>(A, st); return true;
+        case 2: launch_mfma<F, 2, BF, ELU>(A, st); return true;
+        case 4: launch_mfma<F, 4, BF, ELU>(A, st); return true;
+        case 8: if (F / 8 >= 16) { launch_mfma<F, (F / 8 >= 16 ? 8 : 4), BF, ELU>(A, st); return true; } return false;
+        case 16: if (F / 16 >= 16) { launch_mfma<F, (F / 16 >= 16 ? 16 : 4), BF, ELU>(A, st); return true; } return false;
         default: return false;
     }
 }
@@ -787,6 +787,12 @@ void launch_pack_masks(const AggArgs &A, hipStream_t st) {
 
 bool launch_agg_mfma(int F, int K, bool bf, const AggArgs &A, hipStream_t st) {
     if (!mfma_path_supported(F, K)) return false;
+    if (A.elu) {   // the ELU variant runs in fp32
+        if (bf) return false;
+        if (F == 64) return dispatch_mfma_heads<64, false, true>(K, A, st);
+        if (F == 128) return dispatch_mfma_heads<128, false, true>(K, A, st);
+        return dispatch_mfma_heads<256, false, true>(K, A, st);
+    }
     if (F == 64) return bf ? dispatch_mfma_heads<64, true>(K, A, st) : dispatch_mfma_heads<64, false>(K, A, st);
     if (F == 128) return bf ? dispatch_mfma_heads<128, true>(K, A, st) : dispatch_mfma_heads<128, false>(K, A, st);
     return bf ? dispatch_mfma_heads<256, true>(K, A, st) : dispatch_mfma_heads<256, false>(K, A, st);

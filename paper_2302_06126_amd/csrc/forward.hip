@@ -76,7 +76,7 @@ __global__ void convert_wh_bf16(const float *layer_w, uint16_t *Wb, int F, int L
 }
 
 // op destinations: B0 (op<-op) and B1 (op<-dev)
-template <int F, int K, bool BF>
+template <int F, int K, bool BF, bool ELU = false>
 __global__ void __launch_bounds__(256) agg_op(AggArgs A) {
     constexpr int CPL = F / 64, LPH = 64 / K;
     const int lane = threadIdx.x & 63;
@@ -102,7 +102,7 @@ __global__ void __launch_bounds__(256) agg_op(AggArgs A) {
             const float x0 = xo[A.eid[0][e]];
             float y[CPL]; load_ch<CPL, BF>(A.Y_op, ((int64_t)rep * A.n_op + v) * 2 * F + c0, y);
             float m[CPL];
-            float s2 = entry_score<CPL, LPH>(y, x0, 0.f, k, q, A.slope, m);
+            float s2 = entry_score<CPL, LPH, ELU>(y, x0, 0.f, k, q, A.slope, m);
             o.push(s2, m);
         }
         if (end > beg) {
@@ -124,7 +124,7 @@ __global__ void __launch_bounds__(256) agg_op(AggArgs A) {
             const float x0 = xb[A.eid[1][e]] ? 1.f : 0.f;
             float y[CPL]; load_ch<CPL, BF>(A.Y_dev, ((int64_t)rep * A.n_dev + j) * 2 * F + F + c0, y);
             float m[CPL];
-            float s2 = entry_score<CPL, LPH>(y, x0, 0.f, k, q, A.slope, m);
+            float s2 = entry_score<CPL, LPH, ELU>(y, x0, 0.f, k, q, A.slope, m);
             o.push(s2, m);
         }
         if (end > beg) {
@@ -136,7 +136,7 @@ __global__ void __launch_bounds__(256) agg_op(AggArgs A) {
 }
 
 // device <- op partials over chunks of kChunk entries
-template <int F, int K, bool BF>
+template <int F, int K, bool BF, bool ELU = false>
 __global__ void __launch_bounds__(256) agg_dev_part(AggArgs A) {
     constexpr int CPL = F / 64, LPH = 64 / K;
     const int lane = threadIdx.x & 63;
@@ -166,7 +166,7 @@ __global__ void __launch_bounds__(256) agg_dev_part(AggArgs A) {
         const float x0 = xb[A.eid[2][e]] ? 1.f : 0.f;
         float y[CPL]; load_ch<CPL, BF>(A.Y_op, ((int64_t)rep * A.n_op + u) * 2 * F + F + c0, y);
         float m[CPL];
-        float s2 = entry_score<CPL, LPH>(y, x0, 0.f, k, q, A.slope, m);
+        float s2 = entry_score<CPL, LPH, ELU>(y, x0, 0.f, k, q, A.slope, m);
         o.push(s2, m);
     }
     // partial record: [mx per head][den per head][acc F]
@@ -177,7 +177,7 @@ __global__ void __launch_bounds__(256) agg_dev_part(AggArgs A) {
 }
 
 // device destinations: merge B2 partials, then B3 (dev <- dev)
-template <int F, int K, bool BF>
+template <int F, int K, bool BF, bool ELU = false>
 __global__ void __launch_bounds__(256) agg_dev_final(AggArgs A) {
     constexpr int CPL = F / 64, LPH = 64 / K;
     const int lane = threadIdx.x & 63;
@@ -268,7 +268,7 @@ __global__ void __launch_bounds__(256) agg_dev_final(AggArgs A) {
             }
             float s2[EB], m[EB][CPL];
 #pragma unroll
-            for (int i = 0; i < EB; ++i) s2[i] = entry_score<CPL, LPH>(y[i], x0[i], x1[i], k, q, A.slope, m[i]);
+            for (int i = 0; i < EB; ++i) s2[i] = entry_score<CPL, LPH, ELU>(y[i], x0[i], x1[i], k, q, A.slope, m[i]);
             o.template push_n<EB>(s2, m, n);
         }
         if (end > beg) {
@@ -279,53 +279,59 @@ __global__ void __launch_bounds__(256) agg_dev_final(AggArgs A) {
     store_row<CPL, BF>(A.H_dev, ((int64_t)rep * A.n_dev + j) * F + c0, A.out_f32 != 0, out);
 }
 
-template <int F, int K, bool BF>
+template <int F, int K, bool BF, bool ELU = false>
 void launch_agg(const AggArgs &A, hipStream_t st) {
     const int64_t op_waves = (int64_t)A.R * A.n_op;
     const int64_t part_waves = (int64_t)A.R * A.maxc * A.n_dev;
     const int64_t dev_waves = (int64_t)A.R * A.n_dev;
     prof_begin(TAG_STAGE_AGG_OP_OP, st);
-    agg_op<F, K, BF><<<(unsigned)((op_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
+    agg_op<F, K, BF, ELU><<<(unsigned)((op_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
     prof_end(TAG_STAGE_AGG_OP_OP, st);
     prof_begin(TAG_STAGE_AGG_DEV_OP, st);
-    agg_dev_part<F, K, BF><<<(unsigned)((part_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
+    agg_dev_part<F, K, BF, ELU><<<(unsigned)((part_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
     prof_end(TAG_STAGE_AGG_DEV_OP, st);
     (void)dev_waves;
 }
 
-template <int F, int K, bool BF>
+template <int F, int K, bool BF, bool ELU = false>
 void launch_dev_final(const AggArgs &A, hipStream_t st) {
     const int64_t dev_waves = (int64_t)A.R * A.n_dev;
     prof_begin(TAG_STAGE_AGG_DEV_MERGE, st);
-    agg_dev_final<F, K, BF><<<(unsigned)((dev_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
+    agg_dev_final<F, K, BF, ELU><<<(unsigned)((dev_waves + kWaves - 1) / kWaves), 256, 0, st>>>(A);
     prof_end(TAG_STAGE_AGG_DEV_MERGE, st);
 }
 
 // first-version aggregation (used when heads are narrower than 16 channels),
 // then the device merge + dev<-dev pass shared by both paths
-template <int F, int K, bool BF>
+template <int F, int K, bool BF, bool ELU = false>
 void launch_layer(bool mfma, const AggArgs &A, hipStream_t st) {
-    if (!mfma) launch_agg<F, K, BF>(A, st);
+    if (!mfma) launch_agg<F, K, BF, ELU>(A, st);
     else launch_agg_mfma(F, K, BF, A, st);
-    launch_dev_final<F, K, BF>(A, st);
+    launch_dev_final<F, K, BF, ELU>(A, st);
 }
 
-template <int F, bool BF>
+template <int F, bool BF, bool ELU = false>
 tag_status dispatch_heads(int K, bool mfma, const AggArgs &A, hipStream_t st) {
     switch (K) {
-        case 1: launch_layer<F, 1, BF>(mfma, A, st); break;
-        case 2: launch_layer<F, 2, BF>(mfma, A, st); break;
-        case 4: launch_layer<F, 4, BF>(mfma, A, st); break;
-        case 8: launch_layer<F, 8, BF>(mfma, A, st); break;
-        case 16: launch_layer<F, 16, BF>(mfma, A, st); break;
-        case 32: launch_layer<F, 32, BF>(mfma, A, st); break;
-        case 64: launch_layer<F, 64, BF>(mfma, A, st); break;
+        case 1: launch_layer<F, 1, BF, ELU>(mfma, A, st); break;
+        case 2: launch_layer<F, 2, BF, ELU>(mfma, A, st); break;
+        case 4: launch_layer<F, 4, BF, ELU>(mfma, A, st); break;
+        case 8: launch_layer<F, 8, BF, ELU>(mfma, A, st); break;
+        case 16: launch_layer<F, 16, BF, ELU>(mfma, A, st); break;
+        case 32: launch_layer<F, 32, BF, ELU>(mfma, A, st); break;
+        case 64: launch_layer<F, 64, BF, ELU>(mfma, A, st); break;
         default: TAG_FAIL(TAG_ESHAPE, "unsupported head count");
     }
     return TAG_OK;
 }
 
 tag_status dispatch_agg(int F, int K, bool bf, bool mfma, const AggArgs &A, hipStream_t st) {
+    if (A.elu) {   // the ELU variant runs in fp32
+        if (bf) TAG_FAIL(TAG_ESHAPE, "the ELU variant needs the fp32 variant");
+        if (F == 64) return dispatch_heads<64, false, true>(K, mfma, A, st);
+        if (F == 128) return dispatch_heads<128, false, true>(K, mfma, A, st);
+        return dispatch_heads<256, false, true>(K, mfma, A, st);
+    }
     if (F == 64) return bf ? dispatch_heads<64, true>(K, mfma, A, st) : dispatch_heads<64, false>(K, mfma, A, st);
     if (F == 128) return bf ? dispatch_heads<128, true>(K, mfma, A, st) : dispatch_heads<128, false>(K, mfma, A, st);
     return bf ? dispatch_heads<256, true>(K, mfma, A, st) : dispatch_heads<256, false>(K, mfma, A, st);
@@ -348,6 +354,8 @@ tag_status check_dims(const tag_model_dims *d) {
         TAG_FAIL(TAG_EINVAL, "gamma must not be NaN");
     if (!(d->leaky_slope >= 0.f && d->leaky_slope <= 1.f))
         TAG_FAIL(TAG_EINVAL, "leaky_slope must be in [0, 1]");
+    if (d->sigma != 0 && d->sigma != 1) TAG_FAIL(TAG_EINVAL, "sigma must be 0 (ReLU) or 1 (ELU)");
+    if (d->sigma == 1 && d->dtype != TAG_F32) TAG_FAIL(TAG_ESHAPE, "the ELU variant needs the fp32 variant");
     return TAG_OK;
 }
 
@@ -422,6 +430,7 @@ void launch_layer_transform(const tag_graph *g, const tag_model_dims *dims, cons
     ga.F = F;
     ga.prep.jph = jph;
     ga.prep.K = K;
+    ga.prep.elu = dims->sigma == 1 ? 1 : 0;
     ga.prep.a_od = att_src + F;
     ga.prep.ad_od = att_dst + F;
     ga.prep.cp_od = cp + F;
@@ -506,6 +515,7 @@ tag_status forward_run(const tag_graph *g, const tag_model_dims *dims, const tag
     A.x_dd = x->x_dd; A.s_dd = x->stride_dd;
     A.x_od = x->x_od; A.s_od = x->stride_od;
     A.g_same = dims->gamma_same; A.g_cross = dims->gamma_cross; A.slope = dims->leaky_slope;
+    A.elu = dims->sigma == 1 ? 1 : 0;
     A.part = L.part; A.maxc = L.maxc;
     A.G = g->G; A.n_tiles = g->n_tiles;
     A.tiles = g->tiles_d; A.tile_off = g->tile_off_d; A.op_off = g->op_off_d; A.dev_off = g->dev_off_d;

@@ -122,6 +122,13 @@ namespace tag {
 
 __device__ __forceinline__ float leaky(float x, float slope) { return x > 0.f ? x : slope * x; }
 
+// message non-linearity sigma of the layer equation: ReLU, or ELU (alpha = 1)
+template <bool ELU>
+__device__ __forceinline__ float msg_act(float z) {
+    if constexpr (ELU) return z > 0.f ? z : __expf(z) - 1.f;
+    else return fmaxf(z, 0.f);
+}
+
 typedef unsigned u4v __attribute__((ext_vector_type(4)));
 
 // two floats -> packed bf16 pair (round to nearest even, one gfx950

@@ -10,12 +10,13 @@
 // Backward, per layer from the last to the first, with dO_u = gamma_r dH'_u
 // the gradient reaching destination u's gamma-weighted sum of relation r:
 //   scores   (per entry e = (u <- v), per head k)
-//              s_e = LeakyReLU(a . m_e + adst . (Y_u - c')),  m_e = ReLU(Y_v + U x_e)
+//              s_e = LeakyReLU(a . m_e + adst . (Y_u - c')),  m_e = sigma(Y_v + U x_e)
+//              (sigma: ReLU, or ELU for the variant)
 //              dalpha_e = dO_u . m_e
 //   softmax  (per destination row) alpha_e = softmax(s), c_u = sum_e alpha_e dalpha_e,
 //              dz_e = alpha_e (dalpha_e - c_u) LeakyReLU'(s_e),  Z_u = sum_e dz_e
 //   messages (per source row v, over the entries it feeds)
-//              dm_e = alpha_e dO_u + dz_e a,  dpre_e = dm_e [m_e > 0]
+//              dm_e = alpha_e dO_u + dz_e a,  dpre_e = dm_e sigma'(pre_e)
 //              dY_v = sum_e dpre_e + Z_v adst      (Z_v: v as a destination)
 //            and the parameter sums d a = sum dz m, d adst = sum Z (Y - c'),
 //            dU = sum dpre x^T, dc' = sum dpre
@@ -245,7 +246,7 @@ __device__ __forceinline__ int64_t slot_of(int twin, int32_t id, int32_t dst, in
 
 // scores: one wavefront per (replica, destination row, chunk of kChunkA
 // entries); lanes own F/64 channels; writes s and dalpha per (entry, head)
-template <int F, int K>
+template <int F, int K, bool ELU>
 __global__ void __launch_bounds__(256) bwd_scores(BwdLayer P, BwdBucket B) {
     constexpr int CPL = F / 64, LPH = 64 / K;
     const int lane = threadIdx.x & 63;
@@ -291,7 +292,7 @@ __global__ void __launch_bounds__(256) bwd_scores(BwdLayer P, BwdBucket B) {
         for (int i = 0; i < EB; ++i) {
             float pa = 0.f, pd = 0.f;
             for (int c = 0; c < CPL; ++c) {
-                const float m = fmaxf(ys[i][c] + fmaf(u0[c], x0[i], u1[c] * x1[i]), 0.f);
+                const float m = msg_act<ELU>(ys[i][c] + fmaf(u0[c], x0[i], u1[c] * x1[i]));
                 pa = fmaf(a[c], m, pa);
                 pd = fmaf(dO[c], m, pd);
             }
@@ -406,7 +407,7 @@ struct BwdSrc {
 // messages: persistent wavefronts over (replica, source row, chunk of
 // kChunkB entries); dY rows (or chunk partials) and per-block sums of
 // d a, dU (two columns) and dc'
-template <int F, int K>
+template <int F, int K, bool ELU>
 __global__ void __launch_bounds__(256) bwd_messages(BwdLayer P, BwdSrc S, float *part) {
     constexpr int CPL = F / 64, D = F / K;
     __shared__ float red[4][F];
@@ -457,9 +458,10 @@ __global__ void __launch_bounds__(256) bwd_messages(BwdLayer P, BwdSrc S, float 
                 if (e0 + i >= end) break;
                 for (int c = 0; c < CPL; ++c) {
                     const float pre = ys[c] + fmaf(u0[c], x0[i], u1[c] * x1[i]);
-                    const float m = fmaxf(pre, 0.f);
+                    const float m = msg_act<ELU>(pre);
                     const float dm = fmaf(al[i] * S.gamma, dou[i][c], dz[i] * a[c]);
-                    const float dp = pre > 0.f ? dm : 0.f;
+                    // sigma'(pre): ReLU 1 / 0, ELU 1 / e^pre (= m + 1)
+                    const float dp = pre > 0.f ? dm : (ELU ? dm * (m + 1.f) : 0.f);
                     dys[c] += dp;
                     ga[c] = fmaf(dz[i], m, ga[c]);
                     gu0[c] = fmaf(dp, x0[i], gu0[c]);
@@ -1065,13 +1067,13 @@ size_t carve_train(const tag_graph *g, const tag_model_dims *d, int32_t R, int32
     return c.used;
 }
 
-template <int F, int K>
+template <int F, int K, bool ELU>
 void launch_layer_bwd(const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], const ParamReduce &pr, hipStream_t st) {
     for (int b = 0; b < 4; ++b) {
         const int64_t waves = (int64_t)P.R * B[b].n_dst * B[b].chunks;
         if (waves <= 0) continue;
         prof_begin(TAG_STAGE_BWD_SCORES, st);
-        bwd_scores<F, K><<<(unsigned)((waves + 3) / 4), 256, 0, st>>>(P, B[b]);
+        bwd_scores<F, K, ELU><<<(unsigned)((waves + 3) / 4), 256, 0, st>>>(P, B[b]);
         prof_end(TAG_STAGE_BWD_SCORES, st);
     }
     for (int b = 0; b < 4; ++b) {
@@ -1081,33 +1083,36 @@ void launch_layer_bwd(const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], cons
     }
     for (int s = 0; s < 4; ++s) {
         prof_begin(TAG_STAGE_BWD_MESSAGES, st);
-        bwd_messages<F, K><<<pr.nb_m[s], 256, 0, st>>>(P, S[s], const_cast<float *>(pr.pm[s]));
+        bwd_messages<F, K, ELU><<<pr.nb_m[s], 256, 0, st>>>(P, S[s], const_cast<float *>(pr.pm[s]));
         prof_end(TAG_STAGE_BWD_MESSAGES, st);
         if (S[s].chunks > 1) bwd_combine<<<grid_for((int64_t)P.R * S[s].n_self * F), 256, 0, st>>>(P, S[s], K);
     }
     bwd_params<<<15 * ((F + 15) / 16), 256, 0, st>>>(pr);
 }
 
-template <int F>
+template <int F, bool ELU>
 bool dispatch_layer_bwd_f(int K, const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], const ParamReduce &pr,
                           hipStream_t st) {
     switch (K) {
-        case 1: launch_layer_bwd<F, 1>(P, B, S, pr, st); return true;
-        case 2: launch_layer_bwd<F, 2>(P, B, S, pr, st); return true;
-        case 4: launch_layer_bwd<F, 4>(P, B, S, pr, st); return true;
-        case 8: launch_layer_bwd<F, 8>(P, B, S, pr, st); return true;
-        case 16: launch_layer_bwd<F, 16>(P, B, S, pr, st); return true;
-        case 32: launch_layer_bwd<F, 32>(P, B, S, pr, st); return true;
-        case 64: launch_layer_bwd<F, 64>(P, B, S, pr, st); return true;
+        case 1: launch_layer_bwd<F, 1, ELU>(P, B, S, pr, st); return true;
+        case 2: launch_layer_bwd<F, 2, ELU>(P, B, S, pr, st); return true;
+        case 4: launch_layer_bwd<F, 4, ELU>(P, B, S, pr, st); return true;
+        case 8: launch_layer_bwd<F, 8, ELU>(P, B, S, pr, st); return true;
+        case 16: launch_layer_bwd<F, 16, ELU>(P, B, S, pr, st); return true;
+        case 32: launch_layer_bwd<F, 32, ELU>(P, B, S, pr, st); return true;
+        case 64: launch_layer_bwd<F, 64, ELU>(P, B, S, pr, st); return true;
     }
     return false;
 }
 
-bool dispatch_layer_bwd(int F, int K, const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], const ParamReduce &pr,
-                        hipStream_t st) {
-    if (F == 64) return dispatch_layer_bwd_f<64>(K, P, B, S, pr, st);
-    if (F == 128) return dispatch_layer_bwd_f<128>(K, P, B, S, pr, st);
-    if (F == 256) return dispatch_layer_bwd_f<256>(K, P, B, S, pr, st);
+bool dispatch_layer_bwd(int F, int K, bool elu, const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4],
+                        const ParamReduce &pr, hipStream_t st) {
+    if (F == 64) return elu ? dispatch_layer_bwd_f<64, true>(K, P, B, S, pr, st)
+                            : dispatch_layer_bwd_f<64, false>(K, P, B, S, pr, st);
+    if (F == 128) return elu ? dispatch_layer_bwd_f<128, true>(K, P, B, S, pr, st)
+                             : dispatch_layer_bwd_f<128, false>(K, P, B, S, pr, st);
+    if (F == 256) return elu ? dispatch_layer_bwd_f<256, true>(K, P, B, S, pr, st)
+                             : dispatch_layer_bwd_f<256, false>(K, P, B, S, pr, st);
     return false;
 }
 
@@ -1263,7 +1268,8 @@ extern "C" tag_status tag_train_step(const tag_graph *g, const tag_model_dims *d
         pr.g_att_dst = gr->att_dst + (size_t)l * 3 * F;
         pr.dU = L.dU + (size_t)l * 3 * F * 2;
         pr.dcp = L.dcp + (size_t)l * 3 * F;
-        if (!dispatch_layer_bwd(F, K, P, B, Sx, pr, stream)) TAG_FAIL(TAG_ESHAPE, "unsupported f / heads");
+        if (!dispatch_layer_bwd(F, K, dims->sigma == 1, P, B, Sx, pr, stream))
+            TAG_FAIL(TAG_ESHAPE, "unsupported f / heads");
         const float *Wl = w->layer_w + (size_t)l * 3 * F * 2 * F;
         float *gW = gr->layer_w + (size_t)l * 3 * F * 2 * F;
         // dW^h: op side rows [oo ; od], device side rows [od ; dd]

@@ -185,7 +185,7 @@ __device__ void store_tile_rows(const GemmArgs &G, const Tile &t, int wm, int wn
 // (`cst`, 256 floats per wavefront, free once the k loop is done) before any
 // store is issued: on this GPU a wait for an outstanding load also waits for
 // earlier stores, so no global load may follow the first store.
-template <int JPH>
+template <int JPH, bool ELU = false>
 __device__ void store_tile(const GemmArgs &G, const Tile &t, int wm, int wn, int lane, const f4 (&acc)[4][4],
                            float *cst) {
     const GemmPrep &P = G.prep;
@@ -244,8 +244,8 @@ __device__ void store_tile(const GemmArgs &G, const Tile &t, int wm, int wn, int
                         float t0[4], t1[4];
 #pragma unroll
                         for (int v = 0; v < 4; ++v) {
-                            t0[v] = fmaxf(ys[v], 0.f);
-                            t1[v] = fmaxf(ys[v] + c4[v], 0.f);
+                            t0[v] = msg_act<ELU>(ys[v]);
+                            t1[v] = msg_act<ELU>(ys[v] + c4[v]);
                             p0 = fmaf(c1[v], t0[v], p0);
                             p1 = fmaf(c1[v], t1[v], p1);
                             q = fmaf(c2[v], yv[v], q);
@@ -282,7 +282,7 @@ __device__ void store_tile(const GemmArgs &G, const Tile &t, int wm, int wn, int
     }
 }
 
-template <int JPH>
+template <int JPH, bool ELU = false>
 __global__ void __launch_bounds__(256) gemm_f32(GemmArgs G) {
     constexpr int BK = 16, LS = BM + 16;   // k-major LDS rows, stride = 16 (mod 64) banks
     __shared__ float As[2][BK * LS];
@@ -348,7 +348,7 @@ __global__ void __launch_bounds__(256) gemm_f32(GemmArgs G) {
         if (kc + 1 < nk) sstore(buf ^ 1);
         __syncthreads();
     }
-    store_tile<JPH>(G, t, wm, wn, lane, acc, &As[0][wave * 256]);
+    store_tile<JPH, ELU>(G, t, wm, wn, lane, acc, &As[0][wave * 256]);
 }
 
 template <int JPH>
@@ -426,6 +426,7 @@ int64_t transform_row_tiles(int64_t rows) { return (rows + BM - 1) / BM; }
 template <int JPH>
 void launch_gemm(const GemmArgs &G, bool bf, unsigned blocks, hipStream_t st) {
     if (bf) gemm_bf16<JPH><<<blocks, 256, 0, st>>>(G);
+    else if (G.prep.elu) gemm_f32<JPH, true><<<blocks, 256, 0, st>>>(G);
     else gemm_f32<JPH><<<blocks, 256, 0, st>>>(G);
 }
 

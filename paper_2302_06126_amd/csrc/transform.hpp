@@ -18,15 +18,17 @@ struct GemmSide {
 // od half).  Optional epilogue: per-(row, head) attention terms of the layer, taken from
 // the output rows while they are still in registers (heads of 16, 32 or 64
 // channels, so one head lies inside one wavefront's 64 columns):
-//   S[row][0][h] = a_od . ReLU(Y_od + c'_od)          logit of message bit 0
-//   S[row][1][h] = a_od . ReLU(Y_od + c'_od + U_od)   logit of message bit 1
+//   S[row][0][h] = a_od . sigma(Y_od + c'_od)         logit of message bit 0
+//   S[row][1][h] = a_od . sigma(Y_od + c'_od + U_od)  logit of message bit 1
 // (with Y the unbiased W^h h)
 //   S[row][2][h] = a~_od . Y_od                       destination term, od
 //   S[row][3][h] = a~_same . Y_same                   destination term, oo / dd
-// and, for device rows, the two message rows T[row][b] = ReLU(Y_od + c'_od + b U_od).
+// and, for device rows, the two message rows T[row][b] = sigma(Y_od + c'_od + b U_od)
+// (sigma: ReLU, or ELU for the variant).
 struct GemmPrep {
     int jph;             // 16-column blocks per head (1, 2, 4); 0: no attention terms
     int K;
+    int elu;             // message non-linearity of the terms: 0 ReLU, 1 ELU
     const float *cp_same[2];             // [F]: folded bias c' of oo (side 0) / dd (side 1), added to Y
     const float *a_od, *ad_od, *cp_od;   // [F]
     const float *u_od;                   // U_od[c] at u_od[2c]
