@@ -115,7 +115,8 @@ tag_status tag_search_evaluate(const tag_search_problem *p, const int32_t *path,
  *              1 - load / time
  *   simulator: the simulated group makespan, group idle before its output
  *              transfers / iteration time, peak memory / capacity (both
- *              memory shares capped at 1) and device idle share.
+ *              memory shares capped at 1) and device idle share, plus each
+ *              link's idle share (tag_search_link_features).
  * TAG_EINVAL for another value or a tensor graph with a cycle (simulator). */
 tag_status tag_search_set_model(tag_search_problem *p, int32_t model);
 
@@ -178,10 +179,18 @@ tag_status tag_search_features(const tag_search_problem *p, int32_t B, const voi
                                const void *states_dev, float *x_op, float *x_dev, uint8_t *x_od,
                                void *hip_stream);
 
+/* GPU: the link rows of the B packed records, x_dd [B][e_dd][2] (float32,
+ * DEVICE): log10(link GB/s) - 1 and the link's idle share (the simulator's;
+ * 0 under the analytic model).  Asynchronous on hip_stream. */
+tag_status tag_search_link_features(const tag_search_problem *p, int32_t B, const void *static_dev,
+                                    const void *states_dev, float *x_dd, void *hip_stream);
+
 /* ---- native search rounds ---------------------------------------------- */
 
 /* Everything a run of search rounds needs.  The GNN inputs of a leaf are the
- * features tag_search_features writes plus the shared x_oo / x_dd rows. */
+ * features tag_search_features writes plus the shared x_oo rows and x_dd
+ * rows: the caller's shared rows under the analytic model, the leaf's own
+ * (tag_search_link_features) under the simulator model. */
 typedef struct tag_search_run_args {
     const tag_search_problem *problem;
     tag_mcts *tree;                   /* n_levels = n_groups, n_actions = n_slices       */
@@ -189,7 +198,7 @@ typedef struct tag_search_run_args {
     const tag_model_dims *dims;       /* f_op must equal the problem's f_op               */
     const tag_weights *weights;       /* DEVICE parameters                                */
     const float *x_oo;                /* DEVICE [e_oo] tensor features of every leaf      */
-    const float *x_dd;                /* DEVICE [e_dd][2] link features of every leaf     */
+    const float *x_dd;                /* DEVICE [e_dd][2] link features (analytic model)  */
     const tag_slices *slices;         /* DEVICE copy of the problem's slice table         */
     int32_t batch;                    /* B >= 1 leaves per round                          */
     int32_t rounds;                   /* >= 1                                             */

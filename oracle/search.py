@@ -189,16 +189,18 @@ def feedback(P: Problem, strat: List[Tuple[int, int]]) -> dict:
                  for g in range(P.K)]
         memf = [min(ev["mem"][j] / P.mem[j], 1.0) for j in range(P.M)]
         didle = [1.0 - ev["load"][j] / ev["T"] if ev["T"] > 0 else 0.0 for j in range(P.M)]
-        return dict(T=ev["T"], oom=ev["oom"], makespan=list(ev["comp"]), gidle=gidle, memf=memf, didle=didle)
+        return dict(T=ev["T"], oom=ev["oom"], makespan=list(ev["comp"]), gidle=gidle, memf=memf, didle=didle,
+                    lidle=[0.0] * P.sp.topo.e_dd)
     from oracle import simulate as _sim
     r = _sim.simulate(P.sim, strat)
     if not r["valid"]:
         return dict(T=math.inf, oom=True, makespan=[0.0] * P.K, gidle=[0.0] * P.K, memf=[0.0] * P.M,
-                    didle=[0.0] * P.M)
+                    didle=[0.0] * P.M, lidle=[0.0] * P.sp.topo.e_dd)
     T = r["T"]
     return dict(T=T, oom=r["oom"], makespan=r["group_makespan"],
                 gidle=[min(x / T, 1.0) if T > 0 else 0.0 for x in r["group_idle"]],
-                memf=[min(r["dev_peak"][j] / P.mem[j], 1.0) for j in range(P.M)], didle=r["dev_idle"])
+                memf=[min(r["dev_peak"][j] / P.mem[j], 1.0) for j in range(P.M)], didle=r["dev_idle"],
+                lidle=r["link_idle"])
 
 
 def reward(P: Problem, path: Sequence[int], T_base: Optional[float] = None) -> float:
@@ -211,6 +213,18 @@ def reward(P: Problem, path: Sequence[int], T_base: Optional[float] = None) -> f
     if ev["oom"]:
         return -1.0
     return T_base / ev["T"]
+
+
+def link_features(P: Problem, path: Sequence[int]) -> np.ndarray:
+    """Link rows of a search state, x_dd [E_dd, 2] float32: log10(GB/s) - 1
+    and the link's idle share (the simulator's; 0 under the analytic model)."""
+    t = P.sp.topo
+    fb = feedback(P, full_strategy(P, path))
+    x = np.zeros((t.e_dd, 2), np.float32)
+    for e in range(t.e_dd):
+        x[e, 0] = np.float32(math.log10(t.dd_bw[e]) - 1.0)
+        x[e, 1] = np.float32(fb["lidle"][e])
+    return x
 
 
 def features(P: Problem, path: Sequence[int], f_op: int = 42):

@@ -28,7 +28,7 @@ SEARCH_EXPORTS = ("tag_search_problem_create", "tag_search_problem_destroy", "ta
                   "tag_mcts_update", "tag_mcts_root_stats", "tag_mcts_best_path", "tag_mcts_size",
                   "tag_search_device_bytes", "tag_search_upload", "tag_search_pack", "tag_search_features",
                   "tag_search_run_workspace", "tag_search_run", "tag_simulate", "tag_simulate_batch",
-                  "tag_search_set_model")
+                  "tag_search_set_model", "tag_search_link_features")
 
 # include/tag_train.h
 TRAIN_EXPORTS = ("tag_train_workspace", "tag_train_step")
@@ -183,6 +183,7 @@ def load() -> C.CDLL:
     lib.tag_search_run.argtypes = [C.POINTER(tag_search_run_args), vp]
     lib.tag_simulate.argtypes = [vp, vp, S, C.POINTER(tag_sim_out)]
     lib.tag_search_set_model.argtypes = [vp, S]
+    lib.tag_search_link_features.argtypes = [vp, S, vp, vp, vp, vp]
     lib.tag_simulate_batch.argtypes = [vp, S, vp, vp, S, S, vp, vp]
     lib.tag_train_workspace.argtypes = [vp, C.POINTER(tag_model_dims), S, S, S, szp]
     lib.tag_train_step.argtypes = [vp, C.POINTER(tag_model_dims), C.POINTER(tag_weights), C.POINTER(tag_features),

@@ -73,6 +73,19 @@ __global__ void __launch_bounds__(256) feat_od(FeatArgs a) {
     }
 }
 
+// link rows of every state: log10(GB/s) - 1 and the link's idle share
+__global__ void __launch_bounds__(256) feat_dd(int32_t B, int64_t E, const float *lbw, const char *states,
+                                               StateLayout L, float *x_dd) {
+    const int64_t total = (int64_t)B * E * 2;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = i / 2;
+        const int b = (int)(row / E);
+        const int64_t e = row - (int64_t)b * E;
+        x_dd[i] = (i & 1) ? reinterpret_cast<const float *>(states + (size_t)b * L.total + L.lfeat)[e] : lbw[e];
+    }
+}
+
 unsigned grid_for(int64_t n) {
     const int64_t g = (n + 255) / 256;
     return (unsigned)std::max<int64_t>(1, std::min<int64_t>(g, 65536));
@@ -112,4 +125,20 @@ extern "C" tag_status tag_search_features(const tag_search_problem *p, int32_t B
     feat_dev<<<grid_for((int64_t)B * p->M * 8), 256, 0, st>>>(a);
     if (a.E > 0) feat_od<<<grid_for((int64_t)B * a.E), 256, 0, st>>>(a);
     return launch_status("tag_search_features");
+}
+
+extern "C" tag_status tag_search_link_features(const tag_search_problem *p, int32_t B, const void *static_dev,
+                                               const void *states_dev, float *x_dd, void *hip_stream) {
+    clear_error();
+    if (!p || !static_dev || !states_dev || (!x_dd && !p->dd_a.empty())) TAG_FAIL(TAG_EINVAL, "arguments must be non-NULL");
+    if (B < 1) TAG_FAIL(TAG_EINVAL, "B must be >= 1");
+    if ((reinterpret_cast<uintptr_t>(static_dev) | reinterpret_cast<uintptr_t>(states_dev)) & 15)
+        TAG_FAIL(TAG_EINVAL, "static_dev and states_dev must be 16-byte aligned");
+    const int64_t E = (int64_t)p->dd_a.size();
+    if (E == 0) return TAG_OK;
+    const StaticLayout sl = static_layout(p);
+    feat_dd<<<grid_for((int64_t)B * E * 2), 256, 0, static_cast<hipStream_t>(hip_stream)>>>(
+        B, E, reinterpret_cast<const float *>(static_cast<const char *>(static_dev) + sl.dd_lbw),
+        static_cast<const char *>(states_dev), state_layout(p), x_dd);
+    return launch_status("tag_search_link_features");
 }

@@ -116,6 +116,7 @@ bool strategy_feedback(const tag_search_problem *P, const uint64_t *mask, const 
     f->gidle.assign(P->K, 0.0);
     f->memf.assign(P->M, 0.0);
     f->didle.assign(P->M, 0.0);
+    f->lidle.assign(P->dd_a.size(), 0.0);
     if (P->model == 0) {
         const Eval e = evaluate_strategy(P, mask, opt);
         f->T = e.T;
@@ -134,13 +135,14 @@ bool strategy_feedback(const tag_search_problem *P, const uint64_t *mask, const 
     bool valid = true, oom = false;
     f->peak.assign(P->M, 0.0);
     if (!sim_run(P, mask, opt, W, &f->T, &valid, &oom, f->gms.data(), f->gidle.data(), f->peak.data(),
-                 f->didle.data(), nullptr))
+                 f->didle.data(), f->lidle.empty() ? nullptr : f->lidle.data()))
         return false;
     f->oom = oom || !valid;
     if (!valid) {
         std::fill(f->gms.begin(), f->gms.end(), 0.0);
         std::fill(f->gidle.begin(), f->gidle.end(), 0.0);
         std::fill(f->didle.begin(), f->didle.end(), 0.0);
+        std::fill(f->lidle.begin(), f->lidle.end(), 0.0);
         return true;
     }
     for (int g = 0; g < P->K; ++g) f->gidle[g] = f->T > 0 ? std::min(f->gidle[g] / f->T, 1.0) : 0.0;
@@ -245,6 +247,7 @@ extern "C" tag_status tag_search_problem_create(const tag_search_problem_desc *d
     P->oo_dst.assign(d->oo_dst, d->oo_dst + d->e_oo);
     P->dd_a.assign(d->dd_a, d->dd_a + d->e_dd);
     P->dd_b.assign(d->dd_b, d->dd_b + d->e_dd);
+    P->dd_gbs.assign(d->dd_gbs, d->dd_gbs + d->e_dd);
     P->od_op.assign(d->od_op, d->od_op + d->e_od);
     P->od_dev.assign(d->od_dev, d->od_dev + d->e_od);
     for (int64_t e = 0; e < d->e_od; ++e)
@@ -362,6 +365,8 @@ extern "C" tag_status tag_search_upload(const tag_search_problem *p, void *stati
         dst[4 * j + 3] = (float)std::log10(p->dev_intra[j]);
     }
     for (size_t e = 0; e < p->od_op.size(); ++e) { odo[e] = p->od_op[e]; odd[e] = p->od_dev[e]; }
+    float *lbw = reinterpret_cast<float *>(h.data() + sl.dd_lbw);
+    for (size_t e = 0; e < p->dd_a.size(); ++e) lbw[e] = (float)(std::log10(p->dd_gbs[e]) - 1.0);
     hipStream_t st = static_cast<hipStream_t>(hip_stream);
     TAG_HIP_CHECK(hipMemcpyAsync(static_dev, h.data(), sl.total, hipMemcpyHostToDevice, st));
     TAG_HIP_CHECK(hipStreamSynchronize(st));
@@ -418,6 +423,8 @@ extern "C" tag_status tag_search_pack(const tag_search_problem *p, int32_t B, co
                 df[2 * j] = (float)f.memf[j];
                 df[2 * j + 1] = (float)f.didle[j];
             }
+            float *lf = reinterpret_cast<float *>(rec + L.lfeat);
+            for (size_t e = 0; e < f.lidle.size(); ++e) lf[e] = (float)f.lidle[e];
         }
         sim_scratch_free(W);
     };

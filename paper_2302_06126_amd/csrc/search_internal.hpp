@@ -23,6 +23,7 @@ struct tag_search_problem {
     std::vector<double> op_params;           // per op (the simulator works per op)
     std::vector<int32_t> oo_src, oo_dst;     // tensors in input order
     std::vector<int32_t> dd_a, dd_b;         // device links in input order
+    std::vector<double> dd_gbs;              // their bandwidths, GB/s
     std::vector<uint64_t> slice_mask;
     std::vector<int32_t> slice_opt;
     double T_base = 0.0;                     // baseline iteration time
@@ -56,15 +57,16 @@ constexpr int kPackThreads = 16;
 struct Feedback {
     double T = 0.0;
     bool oom = false;
-    std::vector<double> gms, gidle, memf, didle, peak;
+    std::vector<double> gms, gidle, memf, didle, peak, lidle;
 };
 bool strategy_feedback(const tag_search_problem *P, const uint64_t *mask, const int32_t *opt, SimScratch *W,
                        Feedback *f);
 
 // Static device part: group_of, op_type [N] int32; lflops, lbytes [N] float;
-// device rows [M][4] float; od_op, od_dev [E_od] int32.
+// device rows [M][4] float; od_op, od_dev [E_od] int32; link rows
+// log10(GB/s) - 1 [E_dd] float.
 struct StaticLayout {
-    size_t group_of, op_type, lflops, lbytes, dev, od_op, od_dev, total;
+    size_t group_of, op_type, lflops, lbytes, dev, od_op, od_dev, dd_lbw, total;
 };
 inline StaticLayout static_layout(const tag_search_problem *p) {
     StaticLayout s;
@@ -77,6 +79,7 @@ inline StaticLayout static_layout(const tag_search_problem *p) {
     s.dev = take(16 * (size_t)p->M);
     s.od_op = take(4 * p->od_op.size());
     s.od_dev = take(4 * p->od_op.size());
+    s.dd_lbw = take(4 * p->dd_a.size());
     s.total = std::max<size_t>(o, 16);
     return s;
 }
@@ -84,9 +87,10 @@ inline StaticLayout static_layout(const tag_search_problem *p) {
 // One packed state record: int32 next group (-1: complete), int32 pad;
 // uint64 mask[K]; int32 option[K]; int32 decided[K]; float gfeat[K][2]
 // (log10 makespan ms, idle fraction of decided groups); float dfeat[M][2]
-// (peak-memory fraction, idle fraction).
+// (peak-memory fraction, idle fraction); float lfeat[E_dd] (link idle
+// share: the simulator's, 0 under the analytic model).
 struct StateLayout {
-    size_t mask, option, decided, gfeat, dfeat, total;
+    size_t mask, option, decided, gfeat, dfeat, lfeat, total;
 };
 inline StateLayout state_layout(const tag_search_problem *p) {
     StateLayout s;
@@ -96,7 +100,8 @@ inline StateLayout state_layout(const tag_search_problem *p) {
     s.decided = s.option + 4 * K;
     s.gfeat = s.decided + 4 * K;
     s.dfeat = s.gfeat + 8 * K;
-    s.total = align_up(s.dfeat + 8 * M, 16);
+    s.lfeat = s.dfeat + 8 * M;
+    s.total = align_up(s.lfeat + 4 * p->dd_a.size(), 16);
     return s;
 }
 

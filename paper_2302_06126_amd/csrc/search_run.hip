@@ -11,7 +11,7 @@ namespace {
 
 struct RunLayout {
     // device
-    size_t stat, states, qop, qrep, qgraph, x_op, x_dev, x_od, fwd_ws, E_op, E_dev, dec_ws, argmax, best, prior;
+    size_t stat, states, qop, qrep, qgraph, x_op, x_dev, x_od, x_dd, fwd_ws, E_op, E_dev, dec_ws, argmax, best, prior;
     size_t fwd_bytes, dec_bytes, dev_total;
     // host (pinned): two stages of [states | qop] and of [prior]
     size_t h_stage, h_prior, host_total;
@@ -37,6 +37,7 @@ tag_status run_layout(const tag_search_problem *p, const tag_graph *g, const tag
     L->x_op = put(4 * (size_t)B * N * p->f_op);
     L->x_dev = put(4 * (size_t)B * M * 8);
     L->x_od = put((size_t)B * E);
+    L->x_dd = put(p->model ? 8 * (size_t)B * p->dd_a.size() : 0);   // per-leaf link rows (simulator)
     L->fwd_ws = put(L->fwd_bytes);
     L->E_op = put(4 * (size_t)B * N * F);
     L->E_dev = put(4 * (size_t)B * M * F);
@@ -114,10 +115,12 @@ extern "C" tag_status tag_search_run(const tag_search_run_args *a, void *hip_str
     feats.x_op = reinterpret_cast<const float *>(W + L.x_op);
     feats.x_dev = reinterpret_cast<const float *>(W + L.x_dev);
     feats.x_oo = a->x_oo;
-    feats.x_dd = a->x_dd;
+    // the simulator's link idle shares make the link rows per leaf
+    const bool own_dd = p->model != 0 && !p->dd_a.empty();
+    feats.x_dd = own_dd ? reinterpret_cast<const float *>(W + L.x_dd) : a->x_dd;
     feats.x_od = reinterpret_cast<const uint8_t *>(W + L.x_od);
     feats.stride_oo = 0;
-    feats.stride_dd = 0;
+    feats.stride_dd = own_dd ? 2 * (int64_t)p->dd_a.size() : 0;
     feats.stride_od = (int64_t)p->od_op.size();
 
     hipEvent_t done[2];
@@ -153,6 +156,11 @@ extern "C" tag_status tag_search_run(const tag_search_run_args *a, void *hip_str
                                             reinterpret_cast<float *>(W + L.x_dev),
                                             reinterpret_cast<uint8_t *>(W + L.x_od), hip_stream);
         if (s2 != TAG_OK) return s2;
+        if (own_dd) {
+            s2 = tag_search_link_features(p, B, W + L.stat, W + L.states, reinterpret_cast<float *>(W + L.x_dd),
+                                          hip_stream);
+            if (s2 != TAG_OK) return s2;
+        }
         s2 = tag_gnn_forward(a->graph, a->dims, a->weights, &feats, W + L.fwd_ws, L.fwd_bytes,
                              reinterpret_cast<float *>(W + L.E_op), reinterpret_cast<float *>(W + L.E_dev), hip_stream);
         if (s2 != TAG_OK) return s2;

@@ -207,7 +207,12 @@ class SearchService:
             if t.e_dd else np.zeros((0, 2), np.float32)
         self.x_oo = torch.from_numpy(np.ascontiguousarray(x_oo)).to(dev)
         self.x_dd = torch.from_numpy(np.ascontiguousarray(x_dd)).to(dev)
-        self.feats = make_features(self.x_op, self.x_dev, self.x_oo, self.x_dd, self.x_od)   # x_oo, x_dd shared
+        # under the simulator model every leaf has its own link rows (idle shares)
+        self.own_dd = problem.model == "simulator" and t.e_dd > 0
+        if self.own_dd:
+            self.x_dd_leaf = torch.empty((B, t.e_dd, 2), dtype=torch.float32, device=dev)
+        self.feats = make_features(self.x_op, self.x_dev, self.x_oo, self.x_dd_leaf if self.own_dd else self.x_dd,
+                                   self.x_od)
         st, self.fwd_ws_bytes = tag_gnn_workspace(self.graph.handle, model.dims, B)
         check(st, "tag_gnn_workspace")
         self.fwd_ws = torch.empty(self.fwd_ws_bytes, dtype=torch.uint8, device=dev)
@@ -247,6 +252,9 @@ class SearchService:
         check(lib.tag_search_features(self.problem.h, B, self.static.data_ptr(), self.states_d.data_ptr(),
                                       self.x_op.data_ptr(), self.x_dev.data_ptr(), self.x_od.data_ptr(), sh),
               "tag_search_features")
+        if self.own_dd:
+            check(lib.tag_search_link_features(self.problem.h, B, self.static.data_ptr(), self.states_d.data_ptr(),
+                                               self.x_dd_leaf.data_ptr(), sh), "tag_search_link_features")
         check(tag_gnn_forward(self.graph.handle, self.model.dims, self.model.weights, self.feats,
                               self.fwd_ws.data_ptr(), self.fwd_ws_bytes, self.E_op.data_ptr(),
                               self.E_dev.data_ptr(), sh), "tag_gnn_forward")

@@ -50,8 +50,13 @@ def test_features_kernel_matches_reference(torch, name, f_op, model):
     PS.check(PS._abi.load().tag_search_features(prob.h, B, static.data_ptr(), states.data_ptr(), x_op.data_ptr(),
                                                 x_dev.data_ptr(), x_od.data_ptr(), 0), "features")
     torch.cuda.synchronize()
-    g_op, g_dev, g_od = x_op.cpu().numpy(), x_dev.cpu().numpy(), x_od.cpu().numpy()
+    x_dd = torch.full((B, max(t.e_dd, 1), 2), np.nan, dtype=torch.float32, device=dev)
+    PS.check(PS._abi.load().tag_search_link_features(prob.h, B, static.data_ptr(), states.data_ptr(),
+                                                     x_dd.data_ptr(), 0), "link features")
+    torch.cuda.synchronize()
+    g_op, g_dev, g_od, g_dd = x_op.cpu().numpy(), x_dev.cpu().numpy(), x_od.cpu().numpy(), x_dd.cpu().numpy()
     for b in range(B):
+        assert np.array_equal(g_dd[b][:t.e_dd], OS.link_features(P, path[b, :depth[b]].tolist())), b
         x, xd, xod, _ = OS.features(P, path[b, :depth[b]].tolist(), f_op=f_op)
         exact = list(range(32)) + list(range(34, 40))          # one-hots and flags
         assert np.array_equal(g_op[b][:, exact], x[:, exact]), b
@@ -61,25 +66,26 @@ def test_features_kernel_matches_reference(torch, name, f_op, model):
     prob.close()
 
 
-@pytest.mark.parametrize("name,B,rounds", [("tiny", 8, 6), ("cnn", 16, 4)])
-def test_search_rounds_match_reference_tree(torch, name, B, rounds):
+@pytest.mark.parametrize("name,B,rounds,model", [("tiny", 8, 6, "analytic"), ("cnn", 16, 4, "analytic"),
+                                                  ("cnn", 16, 3, "simulator")])
+def test_search_rounds_match_reference_tree(torch, name, B, rounds, model):
     """The service's rounds, replayed through the reference tree with the
     priors the GPU produced and the reference rewards, select the same
     leaves and end with the same statistics; round 0's priors (the root
     expansion) match the reference GNN's."""
     import paper_2302_06126_amd as P0
     import paper_2302_06126_amd.search as PS
-    _say(f"[search] rounds {name} B={B}")
+    _say(f"[search] rounds {name} B={B} {model}")
     wl = synth.WORKLOADS[name]
     sp = synth.make_search_problem(name)
-    P = OS.Problem(sp)
+    P = OS.Problem(sp, model=model)
     w = synth.make_weights(wl.f, wl.heads, wl.layers, wl.f_op, wl.f)
-    model = P0.Model(w, f=wl.f, heads=wl.heads, layers=wl.layers, f_op=wl.f_op, dtype=wl.dtype)
-    prob = PS.SearchProblem(sp, f_op=wl.f_op)
-    svc = PS.SearchService(prob, sp, model, B)
+    gnn = P0.Model(w, f=wl.f, heads=wl.heads, layers=wl.layers, f_op=wl.f_op, dtype=wl.dtype)
+    prob = PS.SearchProblem(sp, f_op=wl.f_op, model=model)
+    svc = PS.SearchService(prob, sp, gnn, B)
     lib = PS.Mcts(P.K, P.S, 1.5, 0.0)
     ref = OS.Tree(P.K, P.S, 1.5, 0.0)
-    T_base = OS.evaluate(P, OS.full_strategy(P, []))["T"]
+    T_base = OS.feedback(P, OS.full_strategy(P, []))["T"]
     first = None
     for rnd in range(rounds):
         leaf, depth, path = lib.select(B)
@@ -102,7 +108,9 @@ def test_search_rounds_match_reference_tree(torch, name, B, rounds):
     x, xd, xod, rep = OS.features(P, p0, f_op=wl.f_op)
     t = sp.topo
     x_oo = (np.log10(t.op_bytes[t.oo_src]) - 6.0).astype(np.float32)
-    x_dd = np.stack([np.log10(t.dd_bw) - 1.0, np.zeros(t.e_dd)], axis=1).astype(np.float32)
+    x_dd = OS.link_features(P, p0)   # under the analytic model the idle column is 0
+    if model == "analytic":
+        assert np.array_equal(x_dd, np.stack([np.log10(t.dd_bw) - 1.0, np.zeros(t.e_dd)], axis=1).astype(np.float32))
     E_op, E_dev = oracle.forward(t, x, xd, x_oo, x_dd, xod, w, f=wl.f, heads=wl.heads, layers=wl.layers)
     od = oracle.decide(E_op, E_dev, sp.masks, sp.options, np.array([rep], np.int32), w, f=wl.f,
                        dec_hidden=wl.f, n_dev=t.n_dev, want_prior=True)

@@ -272,16 +272,18 @@ def test_library_rejects_bad_search_arguments(L):
     prob.close()
 
 
-def _records(prob, buf, B, K, M):
-    """Decode packed state records: (gfeat [B][K][2], dfeat [B][M][2])."""
+def _records(prob, buf, B, K, M, E_dd=0):
+    """Decode packed state records: (gfeat [B][K][2], dfeat [B][M][2], lfeat [B][E_dd])."""
     _, rb = prob.device_bytes()
     g0 = 8 + 8 * K + 4 * K + 4 * K
-    out_g, out_d = [], []
+    l0 = g0 + 8 * K + 8 * M
+    out_g, out_d, out_l = [], [], []
     for b in range(B):
         rec = buf[b * rb:(b + 1) * rb]
         out_g.append(np.frombuffer(rec[g0:g0 + 8 * K].tobytes(), np.float32).reshape(K, 2))
-        out_d.append(np.frombuffer(rec[g0 + 8 * K:g0 + 8 * K + 8 * M].tobytes(), np.float32).reshape(M, 2))
-    return out_g, out_d
+        out_d.append(np.frombuffer(rec[g0 + 8 * K:l0].tobytes(), np.float32).reshape(M, 2))
+        out_l.append(np.frombuffer(rec[l0:l0 + 4 * E_dd].tobytes(), np.float32))
+    return out_g, out_d, out_l
 
 
 @pytest.mark.parametrize("name", ["tiny", "cnn"])
@@ -306,7 +308,7 @@ def test_library_simulator_model_matches_reference(L, name):
     _, rb = prob.device_bytes()
     buf = np.zeros(B * rb, np.uint8)
     rewards, _ = prob.pack(depth, path, buf.ctypes.data)
-    gf, df = _records(prob, buf, B, P.K, P.M)
+    gf, df, lf = _records(prob, buf, B, P.K, P.M, sp.topo.e_dd)
     for b in range(B):
         p = path[b, :depth[b]].tolist()
         assert rewards[b] == pytest.approx(OS.reward(P, p, T_base), rel=1e-12)
@@ -317,6 +319,8 @@ def test_library_simulator_model_matches_reference(L, name):
             assert gf[b][g, 1] == np.float32(fb["gidle"][g])
         assert np.array_equal(df[b][:, 0], np.array(fb["memf"], np.float32))
         assert np.array_equal(df[b][:, 1], np.array(fb["didle"], np.float32))
+        assert np.array_equal(lf[b], np.array(fb["lidle"], np.float32))
+        assert np.array_equal(OS.link_features(P, p)[:, 1], lf[b])
     # the two models agree on the baseline's iteration time only by construction of the workloads,
     # not in general; both give a positive, finite time
     assert 0 < T_base < math.inf
