@@ -26,11 +26,13 @@
 // then the node encoders (ReLU mask, dA = dpre^T x, dc = column sums) and
 // the folded edge encoders (U = W^e A_r, c' = W^e c_r + b):
 //   dW^e = dU A_r^T + dc' c_r^T,  db = dc',  dA_r = sum_l W^e^T dU,  dc_r = sum_l W^e^T dc'.
-// Per-entry scalars live in slots keyed by edge id, so the source-side pass
-// finds the scalars of the entries a row feeds through the transposed
-// bucket: op-device links through the opposite bucket, undirected links
-// (op-op, device-device) through the row's own bucket with the direction bit
-// (destination id > source id).
+// Per-entry scalars live in slots the source-side pass can find through the
+// transposed bucket: undirected links (op-op, device-device) are keyed by
+// edge id with the direction bit (destination id > source id) and found
+// through the row's own bucket; op-device links (both directions) are keyed
+// by the entry's position in the op<-device bucket, which the
+// device<-op bucket reaches through a position map built at the start of the
+// step.
 //
 // Every reduction runs in a fixed order (per-block partials summed by one
 // thread per output), so the step is bitwise repeatable.
@@ -211,6 +213,8 @@ struct BwdBucket {
     int64_t n_slots;
     int32_t chunks;                   // kChunkA-entry chunks per row (max degree)
     float *Z; int zsel;               // [R*n_dst][2][K] per-destination dz sums
+    int spos;                         // slot = the entry's position in this bucket
+    const int32_t *smap;              // else, if set: slot = smap[position]
 };
 
 constexpr int kChunkA = 32;     // entries per score item
@@ -242,6 +246,12 @@ __device__ __forceinline__ float hsum(float v) {
 
 __device__ __forceinline__ int64_t slot_of(int twin, int32_t id, int32_t dst, int32_t src) {
     return twin ? 2 * (int64_t)id + (dst > src ? 1 : 0) : (int64_t)id;
+}
+
+// slot of the entry at position e of a bucket walk
+__device__ __forceinline__ int64_t entry_slot(int spos, const int32_t *smap, int32_t e, int twin, int32_t id,
+                                              int32_t dst, int32_t src) {
+    return spos ? (int64_t)e : (smap ? (int64_t)smap[e] : slot_of(twin, id, dst, src));
 }
 
 // scores: one wavefront per (replica, destination row, chunk of kChunkA
@@ -300,7 +310,8 @@ __global__ void __launch_bounds__(256) bwd_scores(BwdLayer P, BwdBucket B) {
             pd = hsum<LPH>(pd);
             const float s = leaky(pa + q, P.slope);
             if (e0 + i < end && (lane & (LPH - 1)) == 0) {
-                const int64_t idx = (sbase + slot_of(B.twin, id[i], u, vv[i])) * K + lane / LPH;
+                const int64_t slot = entry_slot(B.spos, B.smap, e0 + i, B.twin, id[i], u, vv[i]);
+                const int64_t idx = (sbase + slot) * K + lane / LPH;
                 B.SA[idx] = s;
                 B.SD[idx] = pd;
             }
@@ -335,7 +346,9 @@ __global__ void __launch_bounds__(256) bwd_softmax(BwdLayer P, BwdBucket B, floa
         for (int32_t e0 = beg; e0 < end; e0 += EPS) {
             const int32_t e = e0 + ei;
             if (e < end) {
-                const int64_t idx = (sbase + slot_of(B.twin, B.eid[e], u, B.col[e])) * K + k;
+                const int64_t slot = B.spos ? (int64_t)e
+                                            : (B.smap ? (int64_t)B.smap[e] : slot_of(B.twin, B.eid[e], u, B.col[e]));
+                const int64_t idx = (sbase + slot) * K + k;
                 const float s = B.SA[idx], da = B.SD[idx];
                 if (s > mx) {
                     const float sc = __expf(mx - s);
@@ -364,7 +377,9 @@ __global__ void __launch_bounds__(256) bwd_softmax(BwdLayer P, BwdBucket B, floa
         for (int32_t e0 = beg; e0 < end; e0 += EPS) {
             const int32_t e = e0 + ei;
             if (e < end) {
-                const int64_t idx = (sbase + slot_of(B.twin, B.eid[e], u, B.col[e])) * K + k;
+                const int64_t slot = B.spos ? (int64_t)e
+                                            : (B.smap ? (int64_t)B.smap[e] : slot_of(B.twin, B.eid[e], u, B.col[e]));
+                const int64_t idx = (sbase + slot) * K + k;
                 const float s = B.SA[idx], da = B.SD[idx];
                 const float al = __expf(s - mx) * inv;
                 const float dz = al * (da - cc) * (s > 0.f ? 1.f : P.slope);
@@ -402,6 +417,8 @@ struct BwdSrc {
     float *dY; int dyoff;             // [R*n_self][2F]
     float *PB;                        // [R*n_self][chunks][F] chunk partials (chunks > 1)
     int32_t chunks;
+    int spos;                         // slot = the entry's position in this bucket
+    const int32_t *smap;              // else, if set: slot = smap[position]
 };
 
 // messages: persistent wavefronts over (replica, source row, chunk of
@@ -449,7 +466,8 @@ __global__ void __launch_bounds__(256) bwd_messages(BwdLayer P, BwdSrc S, float 
             for (int i = 0; i < EB; ++i) {
                 load_ch<CPL, false>(S.dOn, ((int64_t)rep * S.n_nbr + uu[i]) * F + c0, dou[i]);
                 edge_x(P, S.xkind, rep, id[i], x0[i], x1[i]);
-                const int64_t idx = (sbase + slot_of(S.twin, id[i], uu[i], v)) * K + h;
+                const int64_t slot = entry_slot(S.spos, S.smap, min(e0 + i, end - 1), S.twin, id[i], uu[i], v);
+                const int64_t idx = (sbase + slot) * K + h;
                 al[i] = S.SA[idx];
                 dz[i] = S.SD[idx];
             }
@@ -504,6 +522,350 @@ __global__ void bwd_combine(BwdLayer P, BwdSrc S, int K) {
         float s = 0.f;
         for (int32_t ch = 0; ch < nch; ++ch) s += S.PB[(rv * S.chunks + ch) * F + c];
         S.dY[rv * 2 * F + S.dyoff + c] = fmaf(S.Z[(rv * 2 + S.zsel) * K + c / D], P.att_dst[r * F + c], s);
+    }
+}
+
+// ------------------------------------------------------- op-device tiles
+// Op-device links carry only the placement bit, so a device row's message
+// has two forms (bit 0 / 1).  One block per (replica, tile of consecutive
+// ops of one topology) stages the topology's device message rows, gradient
+// rows and attention terms in LDS and walks the tile's ops: op rows are
+// read once, and both directions of every op-device link are handled from
+// the op's side (the long device rows are never walked).
+struct OdTile {
+    const int32_t *tiles;          // [n_tiles][3]: first op (global), op count, topology
+    const int32_t *dev_off;        // [G+1]
+    const int32_t *rp, *col, *eid; // op<-device bucket (rows: ops)
+    int64_t n_op, n_dev, n_slots;
+    const float *Y_op, *Y_dev;     // saved Y rows, od half at +F
+    const float *dO_op, *dO_dev;   // gradient rows of the layer outputs
+    float gamma;
+    float *SA1, *SD1, *SA2, *SD2;  // slots of op<-device and device<-op entries
+    const float *Zop, *Zdev;       // [rows][2][K]; od at 1
+    float *dY_op, *dY_dev;         // od halves: dY_op + F, dY_dev + 0
+    float *PD;                     // [R][n_tiles][max_dev][F] device partials
+    int32_t max_dev, n_tiles;
+    const int32_t *tile_off;       // [G+1]
+    float *part;                   // [4][nb][F] parameter partials (da, dU0, dU1, dc')
+};
+
+// LDS row stride of the staged device rows (+4 floats: the four entry
+// groups of a wavefront read different rows at the same channels)
+template <int F>
+constexpr int od_stride() { return F + 4; }
+
+// Block set-up of the tile kernels: the tile's row pointers, one byte per
+// tile entry (local device index | placement bit << 7, read coalesced from
+// the entry range of the tile), and the device rows of the tile's topology:
+// messages for both bits, gamma dO rows and (TERMS) attention logit terms
+// and destination terms.
+template <int F, int K, bool ELU, bool TERMS>
+__device__ void od_stage(const BwdLayer &P, const OdTile &T, int32_t rep, int32_t u0, int32_t n, int32_t d0,
+                         int32_t nd, float *md, float *dod, float *pd, float *qdd, int32_t *rps, uint8_t *ent) {
+    constexpr int D = F / K, FS = od_stride<F>();
+    constexpr int RU = 8, EU = 4;   // loads issued together per thread (rows, entries)
+    const float *a = P.att_src + F, *ad = P.att_dst + F, *cp = P.cp + F;
+    const int tid = threadIdx.x, nt = blockDim.x;
+    for (int i = tid; i <= n; i += nt) rps[i] = T.rp[u0 + i];
+    const int32_t e0 = T.rp[u0], ne = T.rp[u0 + n] - e0;
+    const uint8_t *xb = P.x_od + (int64_t)rep * P.s_od;
+    for (int i0 = tid; i0 < ne; i0 += EU * nt) {
+        int32_t cl[EU], id[EU];
+#pragma unroll
+        for (int j = 0; j < EU; ++j) {
+            const int i = min(i0 + j * nt, ne - 1);
+            cl[j] = T.col[e0 + i];
+            id[j] = T.eid[e0 + i];
+        }
+        uint8_t xv[EU];
+#pragma unroll
+        for (int j = 0; j < EU; ++j) xv[j] = xb[id[j]];
+#pragma unroll
+        for (int j = 0; j < EU; ++j)
+            if (i0 + j * nt < ne) ent[i0 + j * nt] = (uint8_t)((cl[j] - d0) | (xv[j] ? 0x80 : 0));
+    }
+    const int total = nd * F;
+    for (int i0 = tid; i0 < total; i0 += RU * nt) {
+        float y[RU], g[RU], u[RU];
+#pragma unroll
+        for (int j = 0; j < RU; ++j) {
+            const int i = min(i0 + j * nt, total - 1);
+            const int v = i / F, c = i % F;
+            const int64_t row = (int64_t)rep * T.n_dev + d0 + v;
+            y[j] = T.Y_dev[row * 2 * F + F + c];
+            g[j] = T.dO_dev[row * F + c];
+            u[j] = P.U[((int64_t)F + c) * 2 + 0];
+        }
+#pragma unroll
+        for (int j = 0; j < RU; ++j) {
+            const int i = i0 + j * nt;
+            if (i < total) {
+                const int v = i / F, c = i % F;
+                md[(v * 2 + 0) * FS + c] = msg_act<ELU>(y[j]);
+                md[(v * 2 + 1) * FS + c] = msg_act<ELU>(y[j] + u[j]);
+                dod[v * FS + c] = T.gamma * g[j];
+            }
+        }
+    }
+    if constexpr (TERMS) {
+        __syncthreads();
+        for (int i = tid; i < nd * 3 * K; i += nt) {
+            const int v = i / (3 * K), r = i % (3 * K), x = r / K, k = r % K;
+            float t = 0.f;
+            if (x < 2) {
+                for (int c = k * D; c < (k + 1) * D; ++c) t = fmaf(a[c], md[(v * 2 + x) * FS + c], t);
+                pd[(v * 2 + x) * K + k] = t;
+            } else {
+                const float *y = T.Y_dev + ((int64_t)rep * T.n_dev + d0 + v) * 2 * F + F;
+                for (int c = k * D; c < (k + 1) * D; ++c) t = fmaf(ad[c], y[c] - cp[c], t);
+                qdd[v * K + k] = t;
+            }
+        }
+    }
+    __syncthreads();
+}
+
+// Lane layout of the tile kernels: a wavefront takes four entries of an op
+// at a time, 16 lanes per entry, f/16 consecutive channels per lane; a
+// head spans 16/K lanes (K <= 16).  Each wavefront walks ops u0 + wv,
+// u0 + wv + 4, ... and reads the rows of its next op while it works on the
+// current one.  Slots of op-device entries are keyed by their position in
+// the op<-device bucket.
+template <int F, int K, bool ELU>
+__global__ void __launch_bounds__(256) bwd_od_scores(BwdLayer P, OdTile T) {
+    constexpr int CPE = F / 16, D = F / K, HL = D / CPE, FS = od_stride<F>();
+    static_assert(K <= 16, "the op-device tile path needs heads of at least f/16 channels");
+    extern __shared__ float sh[];
+    __shared__ int32_t rps[kOpTile + 1];
+    const int32_t t = blockIdx.x, rep = blockIdx.y;
+    const int32_t u0 = T.tiles[3 * t], n = T.tiles[3 * t + 1], g = T.tiles[3 * t + 2];
+    const int32_t d0 = T.dev_off[g], nd = T.dev_off[g + 1] - d0;
+    float *md = sh, *dod = md + 2 * T.max_dev * FS, *pd = dod + T.max_dev * FS, *qdd = pd + 2 * T.max_dev * K;
+    uint8_t *ent = reinterpret_cast<uint8_t *>(qdd + T.max_dev * K);
+    od_stage<F, K, ELU, true>(P, T, rep, u0, n, d0, nd, md, dod, pd, qdd, rps, ent);
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int grp = lane >> 4, jl = lane & 15;
+    const int c0 = jl * CPE, h = c0 / D;
+    float a[CPE], u0c[CPE];
+    for (int c = 0; c < CPE; ++c) { a[c] = P.att_src[F + c0 + c]; u0c[c] = P.U[((int64_t)F + c0 + c) * 2 + 0]; }
+    const int64_t sbase = (int64_t)rep * T.n_slots;
+    const int32_t ebase = rps[0];
+    float nyo[CPE], ndO[CPE];
+    auto fetch = [&](int32_t ui) {
+        const int64_t row = (int64_t)rep * T.n_op + u0 + ui;
+        load_ch<CPE, false>(T.Y_op, row * 2 * F + F + c0, nyo);
+        load_ch<CPE, false>(T.dO_op, row * F + c0, ndO);
+    };
+    if (wv < n) fetch(wv);
+    for (int32_t ui = wv; ui < n; ui += 4) {
+        float yo[CPE], dO[CPE], m0[CPE], m1[CPE];
+        for (int c = 0; c < CPE; ++c) { yo[c] = nyo[c]; dO[c] = ndO[c]; }
+        if (ui + 4 < n) fetch(ui + 4);
+        float p0 = 0.f, p1 = 0.f, q = 0.f;
+        for (int c = 0; c < CPE; ++c) {
+            dO[c] *= T.gamma;
+            m0[c] = msg_act<ELU>(yo[c]);
+            m1[c] = msg_act<ELU>(yo[c] + u0c[c]);
+            p0 = fmaf(a[c], m0[c], p0);
+            p1 = fmaf(a[c], m1[c], p1);
+            q = fmaf(P.att_dst[F + c0 + c], yo[c] - P.cp[F + c0 + c], q);
+        }
+        p0 = row_sum<HL>(p0); p1 = row_sum<HL>(p1); q = row_sum<HL>(q);
+        const int32_t beg = rps[ui], end = rps[ui + 1];
+        for (int32_t e0 = beg; e0 < end; e0 += 4) {
+            const int32_t e = e0 + grp;
+            const bool ok = e < end;
+            const int eb = ent[(ok ? e : end - 1) - ebase];
+            const int v = eb & 0x7f, x = eb >> 7;
+            const float *mv = md + (v * 2 + x) * FS + c0, *dv = dod + v * FS + c0;
+            float d1 = 0.f, d2 = 0.f;
+            for (int c = 0; c < CPE; ++c) {
+                d1 = fmaf(dO[c], mv[c], d1);
+                d2 = fmaf(dv[c], x ? m1[c] : m0[c], d2);
+            }
+            d1 = row_sum<HL>(d1);
+            d2 = row_sum<HL>(d2);
+            if (ok && (jl % HL) == 0) {
+                const int64_t idx = (sbase + e) * K + h;
+                T.SA1[idx] = leaky(pd[(v * 2 + x) * K + h] + q, P.slope);   // op <- device
+                T.SD1[idx] = d1;
+                T.SA2[idx] = leaky((x ? p1 : p0) + qdd[v * K + h], P.slope);   // device <- op
+                T.SD2[idx] = d2;
+            }
+        }
+    }
+}
+
+// derivative of sigma from its output: ReLU [m > 0]; ELU 1 or e^z = m + 1
+template <bool ELU>
+__device__ __forceinline__ float dact(float m) { return m > 0.f ? 1.f : (ELU ? m + 1.f : 0.f); }
+
+// The (alpha, dz) scalars of an op's entries come in chunks of 64 / K
+// entries, lane i holding entry i / K, head i % K of the chunk (one
+// coalesced read per array); the first chunk of the next op is read ahead.
+template <int F, int K, bool ELU>
+__global__ void __launch_bounds__(256) bwd_od_messages(BwdLayer P, OdTile T) {
+    constexpr int CPE = F / 16, FS = od_stride<F>(), EPC = 64 / K;
+    constexpr bool AHEAD = CPE <= 8;   // read the next op's rows ahead (register budget)
+    static_assert(K <= 16, "the op-device tile path needs heads of at least f/16 channels");
+    extern __shared__ float sh[];
+    __shared__ float red[4][F];
+    __shared__ int32_t rps[kOpTile + 1];
+    const int32_t t = blockIdx.x, rep = blockIdx.y;
+    const int32_t u0 = T.tiles[3 * t], n = T.tiles[3 * t + 1], g = T.tiles[3 * t + 2];
+    const int32_t d0 = T.dev_off[g], nd = T.dev_off[g + 1] - d0;
+    float *md = sh, *dod = md + 2 * T.max_dev * FS, *acc = dod + T.max_dev * FS;   // acc [4][max_dev][FS]
+    uint8_t *ent = reinterpret_cast<uint8_t *>(acc + 4 * T.max_dev * FS);
+    for (int i = threadIdx.x; i < 4 * T.max_dev * FS; i += blockDim.x) acc[i] = 0.f;
+    od_stage<F, K, ELU, false>(P, T, rep, u0, n, d0, nd, md, dod, nullptr, nullptr, rps, ent);
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int grp = lane >> 4, jl = lane & 15;
+    const int c0 = jl * CPE, h = c0 / (F / K);
+    float a[CPE], ad[CPE], u0c[CPE], ga[CPE], gu0[CPE], gcp[CPE];
+    for (int c = 0; c < CPE; ++c) {
+        a[c] = P.att_src[F + c0 + c];
+        ad[c] = P.att_dst[F + c0 + c];
+        u0c[c] = P.U[((int64_t)F + c0 + c) * 2 + 0];
+        ga[c] = gu0[c] = gcp[c] = 0.f;
+    }
+    float *accw = acc + (size_t)wv * T.max_dev * FS;
+    const int64_t sbase = (int64_t)rep * T.n_slots * K;
+    const int32_t ebase = rps[0];
+    auto scalars = [&](int32_t cs, int32_t end, float (&m)[4]) {
+        if (cs + lane / K < end) {
+            const int64_t i = sbase + (int64_t)cs * K + lane;
+            m[0] = T.SA1[i]; m[1] = T.SD1[i]; m[2] = T.SA2[i]; m[3] = T.SD2[i];
+        } else {
+            m[0] = m[1] = m[2] = m[3] = 0.f;
+        }
+    };
+    float nyo[CPE], ndO[CPE], nm[4];
+    auto fetch = [&](int32_t ui) {
+        if constexpr (AHEAD) {
+            const int64_t row = (int64_t)rep * T.n_op + u0 + ui;
+            load_ch<CPE, false>(T.Y_op, row * 2 * F + F + c0, nyo);
+            load_ch<CPE, false>(T.dO_op, row * F + c0, ndO);
+        }
+        scalars(rps[ui], rps[ui + 1], nm);
+    };
+    if (wv < n) fetch(wv);
+    for (int32_t ui = wv; ui < n; ui += 4) {
+        const int64_t row = (int64_t)rep * T.n_op + u0 + ui;
+        float yo[CPE], dO[CPE], m0[CPE], m1[CPE], dys[CPE], sc[4];
+        if constexpr (AHEAD) {
+            for (int c = 0; c < CPE; ++c) { yo[c] = nyo[c]; dO[c] = ndO[c]; }
+        } else {
+            load_ch<CPE, false>(T.Y_op, row * 2 * F + F + c0, yo);
+            load_ch<CPE, false>(T.dO_op, row * F + c0, dO);
+        }
+        for (int i = 0; i < 4; ++i) sc[i] = nm[i];
+        const int32_t beg = rps[ui], end = rps[ui + 1];
+        if (ui + 4 < n) fetch(ui + 4);
+        for (int c = 0; c < CPE; ++c) {
+            dO[c] *= T.gamma;
+            m0[c] = msg_act<ELU>(yo[c]);
+            m1[c] = msg_act<ELU>(yo[c] + u0c[c]);
+            dys[c] = 0.f;
+        }
+        for (int32_t cs = beg; cs < end; cs += EPC) {
+            if (cs != beg) scalars(cs, end, sc);   // rows longer than one chunk
+            const int32_t ce = min(end, cs + EPC);
+            for (int32_t e0 = cs; e0 < ce; e0 += 4) {
+                const int32_t e = e0 + grp;
+                const int src = (e - cs) * K + h;   // < 64: e - cs < EPC
+                const float al1 = __shfl(sc[0], src, 64), dz1 = __shfl(sc[1], src, 64);   // op u <- device v
+                const float al2 = __shfl(sc[2], src, 64), dz2 = __shfl(sc[3], src, 64);   // device v <- op u
+                if (e < ce) {
+                    const int eb = ent[e - ebase];
+                    const int v = eb & 0x7f, x = eb >> 7;
+                    const float *mv = md + (v * 2 + x) * FS + c0, *dv = dod + v * FS + c0;
+                    float *av = accw + v * FS + c0;
+                    for (int c = 0; c < CPE; ++c) {
+                        const float mo = x ? m1[c] : m0[c];
+                        const float dpo = dact<ELU>(mo) * fmaf(al2, dv[c], dz2 * a[c]);
+                        dys[c] += dpo;
+                        ga[c] = fmaf(dz2, mo, ga[c]);
+                        const float dpd = dact<ELU>(mv[c]) * fmaf(al1, dO[c], dz1 * a[c]);
+                        av[c] += dpd;
+                        ga[c] = fmaf(dz1, mv[c], ga[c]);
+                        const float both = dpo + dpd;
+                        if (x) gu0[c] += both;
+                        gcp[c] += both;
+                    }
+                }
+            }
+        }
+        // the four entry groups' sums, in order
+        for (int c = 0; c < CPE; ++c) {
+            dys[c] += __shfl_xor(dys[c], 16, 64);
+            dys[c] += __shfl_xor(dys[c], 32, 64);
+        }
+        if (grp == 0) {
+            const float zo = T.Zop[(row * 2 + 1) * K + h];
+            float *o = T.dY_op + row * 2 * F + F + c0;
+            for (int c = 0; c < CPE; ++c) o[c] = fmaf(zo, ad[c], dys[c]);
+        }
+    }
+    for (int c = 0; c < CPE; ++c) {
+        ga[c] += __shfl_xor(ga[c], 16, 64);  ga[c] += __shfl_xor(ga[c], 32, 64);
+        gu0[c] += __shfl_xor(gu0[c], 16, 64); gu0[c] += __shfl_xor(gu0[c], 32, 64);
+        gcp[c] += __shfl_xor(gcp[c], 16, 64); gcp[c] += __shfl_xor(gcp[c], 32, 64);
+    }
+    __syncthreads();
+    // this tile's device partials: the four wavefronts' sums in order
+    float *pdst = T.PD + (((int64_t)rep * T.n_tiles + t) * T.max_dev) * F;
+    for (int i = threadIdx.x; i < nd * F; i += blockDim.x) {
+        const size_t o = (size_t)(i / F) * FS + i % F, st = (size_t)T.max_dev * FS;
+        pdst[i] = (acc[o] + acc[st + o]) + (acc[2 * st + o] + acc[3 * st + o]);
+    }
+    // parameter partials of the block
+    const int64_t nb = (int64_t)gridDim.x * gridDim.y, b = (int64_t)rep * gridDim.x + t;
+    float *q[3] = {ga, gu0, gcp};
+    const int slot_of_q[3] = {0, 1, 3};
+    for (int qq = 0; qq < 3; ++qq) {
+        if (grp == 0)
+            for (int c = 0; c < CPE; ++c) red[wv][c0 + c] = q[qq][c];
+        __syncthreads();
+        for (int c = threadIdx.x; c < F; c += 256)
+            T.part[((int64_t)slot_of_q[qq] * nb + b) * F + c] = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
+        __syncthreads();
+    }
+    for (int c = threadIdx.x; c < F; c += 256) T.part[((int64_t)2 * nb + b) * F + c] = 0.f;   // no dU1 for od
+}
+
+// device od rows: the tiles' partials of the row's topology in tile order + Z adst
+__global__ void bwd_od_devices(BwdLayer P, OdTile T, const int32_t *dev_topo, int K) {
+    const int F = P.F, D = F / K;
+    const int64_t total = (int64_t)P.R * T.n_dev * F;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = i / F;
+        const int c = (int)(i % F);
+        const int32_t rep = (int32_t)(row / T.n_dev), d = (int32_t)(row % T.n_dev);
+        const int32_t g = dev_topo[d], v = d - T.dev_off[g];
+        float s = 0.f;
+        for (int32_t t = T.tile_off[g]; t < T.tile_off[g + 1]; ++t)
+            s += T.PD[(((int64_t)rep * T.n_tiles + t) * T.max_dev + v) * F + c];
+        T.dY_dev[row * 2 * F + c] = fmaf(T.Zdev[(row * 2 + 1) * K + c / D], P.att_dst[F + c], s);
+    }
+}
+
+// slot keys of the op-device links: pos_of[eid] = position in the op<-device
+// bucket, then m21[q] = pos_of[eid of position q of the device<-op bucket]
+__global__ void od_positions(const int32_t *eid, int64_t n, int32_t *pos_of) {
+    for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n; p += (int64_t)gridDim.x * blockDim.x)
+        pos_of[eid[p]] = (int32_t)p;
+}
+__global__ void od_map(const int32_t *eid, int64_t n, const int32_t *pos_of, int32_t *m21) {
+    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < n; q += (int64_t)gridDim.x * blockDim.x)
+        m21[q] = pos_of[eid[q]];
+}
+
+// topology of every device row
+__global__ void dev_topology(const int32_t *dev_off, int32_t G, int64_t n_dev, int32_t *out) {
+    for (int64_t d = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; d < n_dev; d += (int64_t)gridDim.x * blockDim.x) {
+        int32_t g = 0;
+        while (g + 1 < G && dev_off[g + 1] <= d) ++g;
+        out[d] = g;
     }
 }
 
@@ -968,6 +1330,9 @@ struct TrainLayout {
     int32_t nb_a[4], nb_m[4];
     float *dU, *dcp;
     float *P0, *P1;
+    float *PD, *part_od;     // op-device tile path: device partials, parameter partials
+    int32_t *dev_topo;
+    int32_t *pos_of, *m21;   // op-device links: edge id -> op<-device position; device<-op position -> same
     // decoder
     float *t, *u, *v, *ds, *loss_q, *db2q, *dvq, *dT, *dopt_part, *dw2_part, *Eq, *dEq;
     int32_t *qrow, *qcnt, *qoff, *qlist;
@@ -977,6 +1342,22 @@ int32_t chunks_of(int32_t max_degree, int per) { return std::max<int32_t>(1, (ma
 
 int64_t n_slots(const tag_graph *g, int b) {
     return b == 0 ? 2 * g->e_oo : (b == 3 ? 2 * g->e_dd : g->e_od);
+}
+
+// the op-device tile path needs the topology's device rows in LDS
+// dynamic LDS bytes of the tile kernels: float rows, then one byte per tile entry
+size_t od_scores_lds(int F, int K, int max_dev) {
+    return sizeof(float) * ((size_t)3 * max_dev * (F + 4) + (size_t)3 * max_dev * K) + (size_t)kOpTile * max_dev;
+}
+size_t od_messages_lds(int F, int max_dev) {
+    return sizeof(float) * (size_t)7 * max_dev * (F + 4) + (size_t)kOpTile * max_dev;
+}
+
+// (heads of at least f/16 channels: one head inside a 16-lane entry group)
+bool od_tiles_fit(const tag_graph *g, int F, int K) {
+    // dynamic rows + the static reduction rows and row pointers of the messages kernel
+    return g->n_tiles > 0 && g->max_dev <= 64 && K <= 16 &&
+           od_messages_lds(F, g->max_dev) + sizeof(float) * 4 * F + sizeof(int32_t) * (kOpTile + 1) <= 64 * 1024;
 }
 
 int32_t persist_blocks(int64_t items) {
@@ -1042,6 +1423,17 @@ size_t carve_train(const tag_graph *g, const tag_model_dims *d, int32_t R, int32
         L->part_a[b] = c.take<float>((size_t)L->nb_a[b] * F);
         L->part_m[b] = c.take<float>((size_t)4 * L->nb_m[b] * F);
     }
+    if (od_tiles_fit(g, (int)F, (int)K)) {
+        const int64_t nb = (int64_t)R * g->n_tiles;
+        L->PD = c.take<float>((size_t)nb * g->max_dev * F);
+        L->part_od = c.take<float>((size_t)4 * nb * F);
+        L->dev_topo = c.take<int32_t>((size_t)std::max<int64_t>(g->n_dev, 1));
+    } else {
+        L->PD = L->part_od = nullptr;
+        L->dev_topo = nullptr;
+    }
+    L->pos_of = c.take<int32_t>((size_t)std::max<int64_t>(g->e_od, 1));
+    L->m21 = c.take<int32_t>((size_t)std::max<int64_t>(g->e_od, 1));
     L->dU = c.take<float>((size_t)d->layers * 3 * F * 2);
     L->dcp = c.take<float>((size_t)d->layers * 3 * F);
     const int64_t sp = split_floats(g, d, R, Q);
@@ -1067,11 +1459,21 @@ size_t carve_train(const tag_graph *g, const tag_model_dims *d, int32_t R, int32
     return c.used;
 }
 
+// LDS floats of the op-device tile kernels
+
 template <int F, int K, bool ELU>
-void launch_layer_bwd(const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], const ParamReduce &pr, hipStream_t st) {
+void launch_layer_bwd(const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], const ParamReduce &pr, const OdTile *od,
+                      const int32_t *dev_topo, hipStream_t st) {
+    const dim3 tgrid(od ? (unsigned)od->n_tiles : 1u, (unsigned)P.R);
+    if (od) {
+        prof_begin(TAG_STAGE_BWD_SCORES, st);
+        if constexpr (K <= 16)
+            bwd_od_scores<F, K, ELU><<<tgrid, 256, od_scores_lds(F, K, od->max_dev), st>>>(P, *od);
+        prof_end(TAG_STAGE_BWD_SCORES, st);
+    }
     for (int b = 0; b < 4; ++b) {
         const int64_t waves = (int64_t)P.R * B[b].n_dst * B[b].chunks;
-        if (waves <= 0) continue;
+        if (waves <= 0 || (od && (b == 1 || b == 2))) continue;
         prof_begin(TAG_STAGE_BWD_SCORES, st);
         bwd_scores<F, K, ELU><<<(unsigned)((waves + 3) / 4), 256, 0, st>>>(P, B[b]);
         prof_end(TAG_STAGE_BWD_SCORES, st);
@@ -1081,7 +1483,15 @@ void launch_layer_bwd(const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], cons
         bwd_softmax<F, K><<<pr.nb_a[b], 256, 0, st>>>(P, B[b], const_cast<float *>(pr.pa[b]));
         prof_end(TAG_STAGE_BWD_SOFTMAX, st);
     }
+    if (od) {
+        prof_begin(TAG_STAGE_BWD_MESSAGES, st);
+        if constexpr (K <= 16)
+            bwd_od_messages<F, K, ELU><<<tgrid, 256, od_messages_lds(F, od->max_dev), st>>>(P, *od);
+        prof_end(TAG_STAGE_BWD_MESSAGES, st);
+        bwd_od_devices<<<grid_for((int64_t)P.R * od->n_dev * F), 256, 0, st>>>(P, *od, dev_topo, K);
+    }
     for (int s = 0; s < 4; ++s) {
+        if (od && (s == 1 || s == 2)) continue;
         prof_begin(TAG_STAGE_BWD_MESSAGES, st);
         bwd_messages<F, K, ELU><<<pr.nb_m[s], 256, 0, st>>>(P, S[s], const_cast<float *>(pr.pm[s]));
         prof_end(TAG_STAGE_BWD_MESSAGES, st);
@@ -1092,29 +1502,30 @@ void launch_layer_bwd(const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], cons
 
 template <int F, bool ELU>
 bool dispatch_layer_bwd_f(int K, const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], const ParamReduce &pr,
-                          hipStream_t st) {
+                          const OdTile *od, const int32_t *dt, hipStream_t st) {
     switch (K) {
-        case 1: launch_layer_bwd<F, 1, ELU>(P, B, S, pr, st); return true;
-        case 2: launch_layer_bwd<F, 2, ELU>(P, B, S, pr, st); return true;
-        case 4: launch_layer_bwd<F, 4, ELU>(P, B, S, pr, st); return true;
-        case 8: launch_layer_bwd<F, 8, ELU>(P, B, S, pr, st); return true;
-        case 16: launch_layer_bwd<F, 16, ELU>(P, B, S, pr, st); return true;
-        case 32: launch_layer_bwd<F, 32, ELU>(P, B, S, pr, st); return true;
-        case 64: launch_layer_bwd<F, 64, ELU>(P, B, S, pr, st); return true;
+        case 1: launch_layer_bwd<F, 1, ELU>(P, B, S, pr, od, dt, st); return true;
+        case 2: launch_layer_bwd<F, 2, ELU>(P, B, S, pr, od, dt, st); return true;
+        case 4: launch_layer_bwd<F, 4, ELU>(P, B, S, pr, od, dt, st); return true;
+        case 8: launch_layer_bwd<F, 8, ELU>(P, B, S, pr, od, dt, st); return true;
+        case 16: launch_layer_bwd<F, 16, ELU>(P, B, S, pr, od, dt, st); return true;
+        case 32: launch_layer_bwd<F, 32, ELU>(P, B, S, pr, od, dt, st); return true;
+        case 64: launch_layer_bwd<F, 64, ELU>(P, B, S, pr, od, dt, st); return true;
     }
     return false;
 }
 
 bool dispatch_layer_bwd(int F, int K, bool elu, const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4],
-                        const ParamReduce &pr, hipStream_t st) {
-    if (F == 64) return elu ? dispatch_layer_bwd_f<64, true>(K, P, B, S, pr, st)
-                            : dispatch_layer_bwd_f<64, false>(K, P, B, S, pr, st);
-    if (F == 128) return elu ? dispatch_layer_bwd_f<128, true>(K, P, B, S, pr, st)
-                             : dispatch_layer_bwd_f<128, false>(K, P, B, S, pr, st);
-    if (F == 256) return elu ? dispatch_layer_bwd_f<256, true>(K, P, B, S, pr, st)
-                             : dispatch_layer_bwd_f<256, false>(K, P, B, S, pr, st);
+                        const ParamReduce &pr, const OdTile *od, const int32_t *dt, hipStream_t st) {
+    if (F == 64) return elu ? dispatch_layer_bwd_f<64, true>(K, P, B, S, pr, od, dt, st)
+                            : dispatch_layer_bwd_f<64, false>(K, P, B, S, pr, od, dt, st);
+    if (F == 128) return elu ? dispatch_layer_bwd_f<128, true>(K, P, B, S, pr, od, dt, st)
+                             : dispatch_layer_bwd_f<128, false>(K, P, B, S, pr, od, dt, st);
+    if (F == 256) return elu ? dispatch_layer_bwd_f<256, true>(K, P, B, S, pr, od, dt, st)
+                             : dispatch_layer_bwd_f<256, false>(K, P, B, S, pr, od, dt, st);
     return false;
 }
+
 
 tag_status check_train(const tag_graph *g, const tag_model_dims *dims, int32_t R, int32_t S, int32_t Q) {
     if (!g || !dims) TAG_FAIL(TAG_EINVAL, "graph and dims must be non-NULL");
@@ -1225,6 +1636,11 @@ extern "C" tag_status tag_train_step(const tag_graph *g, const tag_model_dims *d
     prof_end(TAG_STAGE_BWD_DECODER, stream);
 
     // layers, last to first
+    if (L.dev_topo) dev_topology<<<grid_for(g->n_dev), 256, 0, stream>>>(g->dev_off_d, g->G, g->n_dev, L.dev_topo);
+    if (g->e_od > 0) {
+        od_positions<<<grid_for(g->e_od), 256, 0, stream>>>(g->eid[1], g->e_od, L.pos_of);
+        od_map<<<grid_for(g->e_od), 256, 0, stream>>>(g->eid[2], g->e_od, L.pos_of, L.m21);
+    }
     BwdLayer P{};
     P.R = R; P.F = F;
     P.x_oo = x->x_oo; P.s_oo = x->stride_oo;
@@ -1258,17 +1674,34 @@ extern "C" tag_status tag_train_step(const tag_graph *g, const tag_model_dims *d
                        n_slots(g, 1), 0, 1, 1, L.Zdev, 1, L.dY_dev, 0, L.PB, chunks_of(g->max_degree[2], kChunkB)};
         Sx[3] = BwdSrc{g->rowptr[3], g->col[3], g->eid[3], g->n_dev, g->n_dev, Yd, 0, L.G_dev, gs, L.SA[3], L.SD[3],
                        n_slots(g, 3), 1, 2, 2, L.Zdev, 0, L.dY_dev, F, L.PB, chunks_of(g->max_degree[3], kChunkB)};
+        // op-device slots: positions of the op<-device bucket
+        B[1].spos = 1; B[2].smap = L.m21;
+        Sx[1].spos = 1; Sx[2].smap = L.m21;
         ParamReduce pr{};
         for (int b = 0; b < 4; ++b) {
             pr.pa[b] = L.part_a[b]; pr.nb_a[b] = L.nb_a[b];
             pr.pm[b] = L.part_m[b]; pr.nb_m[b] = L.nb_m[b];
         }
         pr.F = F;
+        OdTile od{};
+        const bool use_od = L.PD != nullptr;
+        if (use_od) {
+            od.tiles = g->tiles_d; od.dev_off = g->dev_off_d;
+            od.rp = g->rowptr[1]; od.col = g->col[1]; od.eid = g->eid[1];
+            od.n_op = g->n_op; od.n_dev = g->n_dev; od.n_slots = n_slots(g, 1);
+            od.Y_op = Yo; od.Y_dev = Yd; od.dO_op = L.G_op; od.dO_dev = L.G_dev; od.gamma = gc;
+            od.SA1 = L.SA[1]; od.SD1 = L.SD[1]; od.SA2 = L.SA[2]; od.SD2 = L.SD[2];
+            od.Zop = L.Zop; od.Zdev = L.Zdev; od.dY_op = L.dY_op; od.dY_dev = L.dY_dev;
+            od.PD = L.PD; od.max_dev = std::max(g->max_dev, 1); od.n_tiles = g->n_tiles;
+            od.tile_off = g->tile_off_d; od.part = L.part_od;
+            pr.pm[1] = L.part_od; pr.nb_m[1] = R * g->n_tiles;   // both op-device source passes
+            pr.nb_m[2] = 0;
+        }
         pr.g_att_src = gr->att_src + (size_t)l * 3 * F;
         pr.g_att_dst = gr->att_dst + (size_t)l * 3 * F;
         pr.dU = L.dU + (size_t)l * 3 * F * 2;
         pr.dcp = L.dcp + (size_t)l * 3 * F;
-        if (!dispatch_layer_bwd(F, K, dims->sigma == 1, P, B, Sx, pr, stream))
+        if (!dispatch_layer_bwd(F, K, dims->sigma == 1, P, B, Sx, pr, use_od ? &od : nullptr, L.dev_topo, stream))
             TAG_FAIL(TAG_ESHAPE, "unsupported f / heads");
         const float *Wl = w->layer_w + (size_t)l * 3 * F * 2 * F;
         float *gW = gr->layer_w + (size_t)l * 3 * F * 2 * F;
