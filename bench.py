@@ -38,19 +38,36 @@ KERNEL_BASES = {"transform": ("gemm_f32", "gemm_bf16"), "agg_op_op": ("agg_op",)
                 "dev_prep": ("prep_rows",)}
 
 
+# sources each stage's kernels are built from (their own files, the shared
+# headers and the forward launch code that configures them), relative to the
+# repository root; the traffic summary keeps a hash of each file
+_CSRC = "paper_2302_06126_amd/csrc/"
+TRAFFIC_COMMON = (_CSRC + "tag_internal.hpp", _CSRC + "fwd_internal.hpp", _CSRC + "forward.hip",
+                  "include/tag.h", "include/tag_profile.h")
+_AGG = (_CSRC + "agg_mfma.hip", _CSRC + "agg_common.hpp")
+KERNEL_SOURCES = {"transform": (_CSRC + "transform.hip", _CSRC + "transform.hpp"), "agg_op_op": _AGG,
+                  "agg_op_dev": _AGG, "agg_dev_op": _AGG, "agg_dev_merge": _AGG, "dev_prep": _AGG}
+
+
+def source_hashes(paths) -> dict:
+    import hashlib
+    return {p: hashlib.sha256(open(os.path.join(ROOT, p), "rb").read()).hexdigest() for p in paths}
+
+
 def measured_traffic(workload: str, stage: str):
     """HBM bytes per launch of the stage's kernel from the committed counter
     summary (FETCH_SIZE and WRITE_SIZE, copy-calibrated), or None when there
-    is none for this workload or the kernel sources changed since."""
-    import glob
-    import hashlib
+    is none for this workload or the kernel's sources changed since."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
     if not os.path.exists(path) or stage not in KERNEL_BASES:
         return None
     rec = json.load(open(path))
-    src = b"".join(open(f, "rb").read()
-                   for f in sorted(glob.glob(os.path.join(ROOT, "paper_2302_06126_amd", "csrc", "*"))))
-    if hashlib.sha256(src).hexdigest() != rec.get("source_sha256"):
+    recorded = rec.get("source_sha256")
+    if not isinstance(recorded, dict):
+        return None
+    files = TRAFFIC_COMMON + KERNEL_SOURCES[stage]
+    now = source_hashes(files)
+    if any(recorded.get(f) != h for f, h in now.items()):
         return None
     for k, v in rec["kernels"].items():
         if k.split("<")[0] in KERNEL_BASES[stage] and v.get("hbm_bytes_mean"):
@@ -350,9 +367,12 @@ def sim_bench(args) -> int:
     return 0
 
 
-TRAIN_KERNELS = {"bwd_decoder": "decoder loss + backward kernels", "bwd_scores": "bwd_scores",
-                 "bwd_softmax": "bwd_softmax", "bwd_messages": "bwd_messages", "bwd_dh": "gemm_f32 (dH)",
+TRAIN_KERNELS = {"bwd_decoder": "decoder loss + backward kernels", "bwd_scores": "bwd_scores / bwd_od_scores",
+                 "bwd_softmax": "bwd_softmax", "bwd_messages": "bwd_messages / bwd_od_messages",
+                 "bwd_dh": "gemm_f32 (dH)",
                  "bwd_dw": "gemm_f32 (split-K dW)"}
+# most launches per layer (the op-device tile path takes both op-device
+# passes of scores and messages in one launch)
 TRAIN_LAUNCHES = {"bwd_decoder": 1, "bwd_scores": 4, "bwd_softmax": 4, "bwd_messages": 4, "bwd_dh": 2, "bwd_dw": 2}
 
 
@@ -451,8 +471,9 @@ def train_bench(args) -> int:
     _abi.check(st, "tag_profile_end")
     loss = float(tr.loss.cpu()[0])
     flops, byts = train_work(stage, wl, topo, R)
-    flops /= TRAIN_LAUNCHES[stage]
-    byts /= TRAIN_LAUNCHES[stage]
+    per_layer = max(n_launch, 1) / (args.steps * wl.layers)   # launches of the stage per layer, as measured
+    flops /= per_layer
+    byts /= per_layer
     avg_s = kern_ms / 1e3 / max(n_launch, 1)
     if stage in ("bwd_dh", "bwd_dw"):
         ach = flops / avg_s / 1e12
