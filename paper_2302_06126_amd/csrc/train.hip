@@ -156,15 +156,47 @@ void launch_gemm(Gemm G, bool a_kc, bool b_kc, int64_t splits, hipStream_t st) {
 }
 
 // out[m ldo + n] (+)= sum_z P[z ps + m ldp + n], z in order
-__global__ void sum_splits(const float *P, int64_t ps, int64_t ldp, int32_t nz, int64_t M, int64_t N, float *out,
-                           int64_t ldo, int accumulate) {
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < M * N; i += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t m = i / N, n = i % N;
-        float s = 0.f;
-        for (int32_t z = 0; z < nz; ++z) s += P[z * ps + m * ldp + n];
-        float *o = out + m * ldo + n;
-        *o = accumulate ? *o + s : s;
+// out[m][n] (+)= sum over the nz split partials P[z][m][n] in a fixed order:
+// a block takes 256 / GS consecutive outputs and splits the partials into GS
+// contiguous groups (one per thread of an output, eight loads in flight); the
+// group sums are added in group order.  GS = 16 for launches with few outputs.
+template <int GS>
+__global__ void __launch_bounds__(256) sum_splits(const float *P, int64_t ps, int64_t ldp, int32_t nz, int64_t M,
+                                                  int64_t N, float *out, int64_t ldo, int accumulate) {
+    constexpr int OUT = 256 / GS;
+    __shared__ float red[GS][OUT];
+    const int o = threadIdx.x % OUT, q = threadIdx.x / OUT;
+    const int64_t i = (int64_t)blockIdx.x * OUT + o;
+    const bool ok = i < M * N;
+    const int64_t m = ok ? i / N : 0, n = ok ? i % N : 0;
+    const int32_t per = (nz + GS - 1) / GS, z0 = min(nz, q * per), z1 = min(nz, z0 + per);
+    float s = 0.f;
+    if (ok) {
+        const float *p = P + m * ldp + n;
+#pragma unroll 8
+        for (int32_t z = z0; z < z1; ++z) s += p[(int64_t)z * ps];
     }
+    red[q][o] = s;
+    __syncthreads();
+    if (q == 0 && ok) {
+        float t = 0.f;
+#pragma unroll
+        for (int g = 0; g < GS; ++g) t += red[g][o];
+        float *op = out + m * ldo + n;
+        *op = accumulate ? *op + t : t;
+    }
+}
+
+// launches with at most kFewOutputs outputs use 16 split groups per output
+constexpr int64_t kFewOutputs = 8192;
+void launch_sum_splits(const float *P, int64_t ps, int64_t ldp, int32_t nz, int64_t M, int64_t N, float *out,
+                       int64_t ldo, int accumulate, hipStream_t st) {
+    const int64_t outputs = M * N;
+    if (outputs <= 0) return;
+    if (outputs <= kFewOutputs)
+        sum_splits<16><<<(unsigned)((outputs + 15) / 16), 256, 0, st>>>(P, ps, ldp, nz, M, N, out, ldo, accumulate);
+    else
+        sum_splits<4><<<(unsigned)((outputs + 63) / 64), 256, 0, st>>>(P, ps, ldp, nz, M, N, out, ldo, accumulate);
 }
 
 inline unsigned grid_for(int64_t n, int per = 256) {
@@ -185,8 +217,8 @@ void weight_grad(const float *A, int64_t lda, const float *B, int64_t ldb, int64
     prof_begin(stage, st);
     launch_gemm(g, false, false, splits, st);
     prof_end(stage, st);
-    sum_splits<<<grid_for(M * nb), 256, 0, st>>>(P, M * N, N, (int32_t)splits, M, nb, out, ldo, accumulate);
-    if (ones) sum_splits<<<grid_for(M), 256, 0, st>>>(P + nb, M * N, N, (int32_t)splits, M, 1, bias_out, 1, accumulate);
+    launch_sum_splits(P, M * N, N, (int32_t)splits, M, nb, out, ldo, accumulate, st);
+    if (ones) launch_sum_splits(P + nb, M * N, N, (int32_t)splits, M, 1, bias_out, 1, accumulate, st);
 }
 
 // ------------------------------------------------------------- layer backward
@@ -220,6 +252,7 @@ struct BwdBucket {
 constexpr int kChunkA = 32;     // entries per score item
 constexpr int kChunkB = 128;    // entries per message item
 constexpr int kPersist = 2048;  // blocks of the passes that sum parameter gradients
+constexpr int kLongRow = 256;   // buckets with rows this long (max degree) take the entry-per-lane softmax
 
 __device__ __forceinline__ void edge_x(const BwdLayer &P, int xkind, int32_t rep, int32_t id, float &x0, float &x1) {
     if (xkind == 0) {
@@ -319,10 +352,121 @@ __global__ void __launch_bounds__(256) bwd_scores(BwdLayer P, BwdBucket B) {
     }
 }
 
+// online softmax statistics: fold logit s with weight d into (max, sum, weighted sum)
+__device__ __forceinline__ void softmax_fold(float s, float d, float &mx, float &den, float &num) {
+    if (s > mx) {
+        const float sc = __expf(mx - s);
+        den = fmaf(den, sc, 1.f);
+        num = fmaf(num, sc, d);
+        mx = s;
+    } else {
+        const float p = __expf(s - mx);
+        den += p;
+        num = fmaf(p, d, num);
+    }
+}
+
+// merge another lane's (max, sum, weighted sum) into this lane's
+__device__ __forceinline__ void softmax_merge(float m2, float d2, float n2, float &mx, float &den, float &num) {
+    const float M = fmaxf(mx, m2);
+    if (M == -INFINITY) return;
+    const float s1 = mx == -INFINITY ? 0.f : __expf(mx - M), s2 = m2 == -INFINITY ? 0.f : __expf(m2 - M);
+    den = den * s1 + d2 * s2;
+    num = num * s1 + n2 * s2;
+    mx = M;
+}
+
+// Softmax backward of one long row (rows of hundreds of entries): lanes over
+// entries, each lane all K heads of its entry, two 64-entry rounds of loads
+// in flight; returns the row's Z per head in every lane.
+template <int K>
+__device__ void softmax_row_long(const BwdLayer &P, const BwdBucket &B, int32_t u, int32_t beg, int32_t end,
+                                 int64_t sbase, int lane, float (&Z)[K]) {
+    constexpr int U = 2;
+    auto slot_at = [&](int32_t e) -> int64_t {
+        return B.spos ? (int64_t)e : (B.smap ? (int64_t)B.smap[e] : slot_of(B.twin, B.eid[e], u, B.col[e]));
+    };
+    float mx[K], den[K], num[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) { mx[k] = -INFINITY; den[k] = num[k] = 0.f; }
+    for (int32_t e0 = beg; e0 < end; e0 += 64 * U) {
+        int64_t sl[U];
+        bool ok[U];
+#pragma unroll
+        for (int j = 0; j < U; ++j) {
+            const int32_t e = e0 + 64 * j + lane;
+            ok[j] = e < end;
+            sl[j] = ok[j] ? slot_at(e) : 0;
+        }
+        float sv[U][K], dv[U][K];
+#pragma unroll
+        for (int j = 0; j < U; ++j)
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                sv[j][k] = ok[j] ? B.SA[(sbase + sl[j]) * K + k] : 0.f;
+                dv[j][k] = ok[j] ? B.SD[(sbase + sl[j]) * K + k] : 0.f;
+            }
+#pragma unroll
+        for (int j = 0; j < U; ++j)
+            if (ok[j])
+#pragma unroll
+                for (int k = 0; k < K; ++k) softmax_fold(sv[j][k], dv[j][k], mx[k], den[k], num[k]);
+    }
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1)
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const float m2 = __shfl_xor(mx[k], o, 64), d2 = __shfl_xor(den[k], o, 64), n2 = __shfl_xor(num[k], o, 64);
+            softmax_merge(m2, d2, n2, mx[k], den[k], num[k]);
+        }
+    float inv[K], cc[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        inv[k] = den[k] > 0.f ? 1.f / den[k] : 0.f;
+        cc[k] = num[k] * inv[k];
+        Z[k] = 0.f;
+    }
+    for (int32_t e0 = beg; e0 < end; e0 += 64 * U) {
+        int64_t sl[U];
+        bool ok[U];
+#pragma unroll
+        for (int j = 0; j < U; ++j) {
+            const int32_t e = e0 + 64 * j + lane;
+            ok[j] = e < end;
+            sl[j] = ok[j] ? slot_at(e) : 0;
+        }
+        float sv[U][K], dv[U][K];
+#pragma unroll
+        for (int j = 0; j < U; ++j)
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                sv[j][k] = ok[j] ? B.SA[(sbase + sl[j]) * K + k] : 0.f;
+                dv[j][k] = ok[j] ? B.SD[(sbase + sl[j]) * K + k] : 0.f;
+            }
+#pragma unroll
+        for (int j = 0; j < U; ++j)
+            if (ok[j])
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    const float s = sv[j][k];
+                    const float al = __expf(s - mx[k]) * inv[k];
+                    const float dz = al * (dv[j][k] - cc[k]) * (s > 0.f ? 1.f : P.slope);
+                    B.SA[(sbase + sl[j]) * K + k] = al;
+                    B.SD[(sbase + sl[j]) * K + k] = dz;
+                    Z[k] += dz;
+                }
+    }
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1)
+#pragma unroll
+        for (int k = 0; k < K; ++k) Z[k] += __shfl_xor(Z[k], o, 64);
+}
+
 // softmax backward: one wavefront per (replica, destination row), lanes
-// over (entry, head) pairs; turns (s, dalpha) into (alpha, dz) in place,
-// writes Z_u and sums d adst = Z_u (Y_u - c') per block
-template <int F, int K>
+// over (entry, head) pairs (LONG: lanes over entries, see softmax_row_long);
+// turns (s, dalpha) into (alpha, dz) in place, writes Z_u and sums
+// d adst = Z_u (Y_u - c') per block
+template <int F, int K, bool LONG>
 __global__ void __launch_bounds__(256) bwd_softmax(BwdLayer P, BwdBucket B, float *part_ad) {
     constexpr int CPL = F / 64, EPS = 64 / K, D = F / K;
     __shared__ float red[4][F];
@@ -342,55 +486,52 @@ __global__ void __launch_bounds__(256) bwd_softmax(BwdLayer P, BwdBucket B, floa
         const int32_t rep = (int32_t)(ru / B.n_dst), u = (int32_t)(ru % B.n_dst);
         const int32_t beg = B.rp[u], end = B.rp[u + 1];
         const int64_t sbase = (int64_t)rep * B.n_slots;
-        float mx = -INFINITY, den = 0.f, num = 0.f;
-        for (int32_t e0 = beg; e0 < end; e0 += EPS) {
-            const int32_t e = e0 + ei;
-            if (e < end) {
-                const int64_t slot = B.spos ? (int64_t)e
-                                            : (B.smap ? (int64_t)B.smap[e] : slot_of(B.twin, B.eid[e], u, B.col[e]));
-                const int64_t idx = (sbase + slot) * K + k;
-                const float s = B.SA[idx], da = B.SD[idx];
-                if (s > mx) {
-                    const float sc = __expf(mx - s);
-                    den = fmaf(den, sc, 1.f);
-                    num = fmaf(num, sc, da);
-                    mx = s;
-                } else {
-                    const float p = __expf(s - mx);
-                    den += p;
-                    num = fmaf(p, da, num);
+        float zh;
+        if constexpr (LONG) {
+            float Zk[K];
+            softmax_row_long<K>(P, B, u, beg, end, sbase, lane, Zk);
+            zh = 0.f;
+#pragma unroll
+            for (int kk = 0; kk < K; ++kk) {
+                if (kk == c0 / D) zh = Zk[kk];
+                if (lane == kk) B.Z[(ru * 2 + B.zsel) * K + kk] = Zk[kk];
+            }
+        } else {
+            float mx = -INFINITY, den = 0.f, num = 0.f;
+            for (int32_t e0 = beg; e0 < end; e0 += EPS) {
+                const int32_t e = e0 + ei;
+                if (e < end) {
+                    const int64_t slot = B.spos ? (int64_t)e
+                                                : (B.smap ? (int64_t)B.smap[e] : slot_of(B.twin, B.eid[e], u, B.col[e]));
+                    const int64_t idx = (sbase + slot) * K + k;
+                    softmax_fold(B.SA[idx], B.SD[idx], mx, den, num);
                 }
             }
-        }
-        for (int o = K; o < 64; o <<= 1) {
-            const float m2 = __shfl_xor(mx, o, 64), d2 = __shfl_xor(den, o, 64), n2 = __shfl_xor(num, o, 64);
-            const float M = fmaxf(mx, m2);
-            if (M == -INFINITY) continue;
-            const float s1 = mx == -INFINITY ? 0.f : __expf(mx - M), s2 = m2 == -INFINITY ? 0.f : __expf(m2 - M);
-            den = den * s1 + d2 * s2;
-            num = num * s1 + n2 * s2;
-            mx = M;
-        }
-        const float inv = den > 0.f ? 1.f / den : 0.f;
-        const float cc = num * inv;
-        float zs = 0.f;
-        for (int32_t e0 = beg; e0 < end; e0 += EPS) {
-            const int32_t e = e0 + ei;
-            if (e < end) {
-                const int64_t slot = B.spos ? (int64_t)e
-                                            : (B.smap ? (int64_t)B.smap[e] : slot_of(B.twin, B.eid[e], u, B.col[e]));
-                const int64_t idx = (sbase + slot) * K + k;
-                const float s = B.SA[idx], da = B.SD[idx];
-                const float al = __expf(s - mx) * inv;
-                const float dz = al * (da - cc) * (s > 0.f ? 1.f : P.slope);
-                B.SA[idx] = al;
-                B.SD[idx] = dz;
-                zs += dz;
+            for (int o = K; o < 64; o <<= 1) {
+                const float m2 = __shfl_xor(mx, o, 64), d2 = __shfl_xor(den, o, 64), n2 = __shfl_xor(num, o, 64);
+                softmax_merge(m2, d2, n2, mx, den, num);
             }
+            const float inv = den > 0.f ? 1.f / den : 0.f;
+            const float cc = num * inv;
+            float zs = 0.f;
+            for (int32_t e0 = beg; e0 < end; e0 += EPS) {
+                const int32_t e = e0 + ei;
+                if (e < end) {
+                    const int64_t slot = B.spos ? (int64_t)e
+                                                : (B.smap ? (int64_t)B.smap[e] : slot_of(B.twin, B.eid[e], u, B.col[e]));
+                    const int64_t idx = (sbase + slot) * K + k;
+                    const float s = B.SA[idx], da = B.SD[idx];
+                    const float al = __expf(s - mx) * inv;
+                    const float dz = al * (da - cc) * (s > 0.f ? 1.f : P.slope);
+                    B.SA[idx] = al;
+                    B.SD[idx] = dz;
+                    zs += dz;
+                }
+            }
+            for (int o = K; o < 64; o <<= 1) zs += __shfl_xor(zs, o, 64);
+            if (ei == 0) B.Z[(ru * 2 + B.zsel) * K + k] = zs;
+            zh = __shfl(zs, c0 / D, 64);   // lane h < K holds head h
         }
-        for (int o = K; o < 64; o <<= 1) zs += __shfl_xor(zs, o, 64);
-        if (ei == 0) B.Z[(ru * 2 + B.zsel) * K + k] = zs;
-        const float zh = __shfl(zs, c0 / D, 64);   // lane h < K holds head h
         if (end > beg) {
             float yd[CPL];
             load_ch<CPL, false>(B.Ydst, ru * 2 * F + B.ydst_off + c0, yd);
@@ -898,6 +1039,7 @@ __global__ void __launch_bounds__(256) bwd_params(ParamReduce R) {
             int32_t nb;
             if (qty == 0) { base = R.pa[p]; nb = R.nb_a[p]; }
             else { base = R.pm[p] + (int64_t)(qty - 1) * R.nb_m[p] * F; nb = R.nb_m[p]; }
+#pragma unroll 8
             for (int32_t b = grp; b < nb; b += 16) s += base[(int64_t)b * F + c];
         }
     }
@@ -958,6 +1100,7 @@ __global__ void __launch_bounds__(256) fold_bwd_enc(FoldBwd a) {
     if (k < F) {
         for (int l = 0; l < a.L; ++l) {
             const int64_t lr = (int64_t)l * 3 + r;
+#pragma unroll 8
             for (int o = grp; o < F; o += 4) {
                 const float we = a.layer_w[(lr * F + o) * 2 * F + F + k];
                 s0 = fmaf(we, a.dU[(lr * F + o) * 2 + 0], s0);
@@ -1480,7 +1623,14 @@ void launch_layer_bwd(const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], cons
     }
     for (int b = 0; b < 4; ++b) {
         prof_begin(TAG_STAGE_BWD_SOFTMAX, st);
-        bwd_softmax<F, K><<<pr.nb_a[b], 256, 0, st>>>(P, B[b], const_cast<float *>(pr.pa[b]));
+        float *pa = const_cast<float *>(pr.pa[b]);
+        bool long_rows = false;
+        if constexpr (K <= 16) long_rows = B[b].chunks * kChunkA >= kLongRow;
+        if (long_rows) {
+            if constexpr (K <= 16) bwd_softmax<F, K, true><<<pr.nb_a[b], 256, 0, st>>>(P, B[b], pa);
+        } else {
+            bwd_softmax<F, K, false><<<pr.nb_a[b], 256, 0, st>>>(P, B[b], pa);
+        }
         prof_end(TAG_STAGE_BWD_SOFTMAX, st);
     }
     if (od) {
@@ -1716,11 +1866,9 @@ extern "C" tag_status tag_train_step(const tag_graph *g, const tag_model_dims *d
             launch_gemm(gd, false, false, splits, stream);
             prof_end(TAG_STAGE_BWD_DW, stream);
             float *g1 = gW + (size_t)F * 2 * F;
-            sum_splits<<<grid_for((int64_t)F * F), 256, 0, stream>>>(L.P1, 2 * F * F, F, (int32_t)splits, F, F, g1,
-                                                                    2 * F, 1);
-            sum_splits<<<grid_for((int64_t)F * F), 256, 0, stream>>>(L.P1 + (size_t)F * F, 2 * F * F, F,
-                                                                    (int32_t)splits, F, F, g1 + (size_t)F * 2 * F,
-                                                                    2 * F, 0);
+            launch_sum_splits(L.P1, 2 * F * F, F, (int32_t)splits, F, F, g1, 2 * F, 1, stream);
+            launch_sum_splits(L.P1 + (size_t)F * F, 2 * F * F, F, (int32_t)splits, F, F, g1 + (size_t)F * 2 * F, 2 * F,
+                              0, stream);
         }
         // dH = dY [W^h ; W^h'] (overwrites the layer-output gradients, no longer needed)
         prof_begin(TAG_STAGE_BWD_DH, stream);
