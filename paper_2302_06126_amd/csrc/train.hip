@@ -682,12 +682,18 @@ struct OdTile {
     const float *dO_op, *dO_dev;   // gradient rows of the layer outputs
     float gamma;
     float *SA1, *SD1, *SA2, *SD2;  // slots of op<-device and device<-op entries
-    const float *Zop, *Zdev;       // [rows][2][K]; od at 1
+    float *Zop, *Zdev;             // [rows][2][K]; od at 1 (written by the tile kernels)
     float *dY_op, *dY_dev;         // od halves: dY_op + F, dY_dev + 0
     float *PD;                     // [R][n_tiles][max_dev][F] device partials
     int32_t max_dev, n_tiles;
     const int32_t *tile_off;       // [G+1]
     float *part;                   // [4][nb][F] parameter partials (da, dU0, dU1, dc')
+    // softmax of both op-device directions inside the tile kernels
+    float *part_a1;                // [R*n_tiles][F] d adst sums over the tile's op rows
+    float *drec;                   // [R*n_tiles][max_dev][K][3] device<-op records (max, sum, weighted sum)
+    float *dstat;                  // [R*n_dev][K][3] merged device statistics (max, 1/sum, c)
+    float *zrec;                   // [R*n_tiles][max_dev][K] sums of dz over the tile's device<-op entries
+    float *part_a2;                // [ceil(R*n_dev/4)][F] d adst sums over device rows
 };
 
 // LDS row stride of the staged device rows (+4 floats: the four entry
@@ -774,21 +780,36 @@ __device__ void od_stage(const BwdLayer &P, const OdTile &T, int32_t rep, int32_
 // the op<-device bucket.
 template <int F, int K, bool ELU>
 __global__ void __launch_bounds__(256) bwd_od_scores(BwdLayer P, OdTile T) {
-    constexpr int CPE = F / 16, D = F / K, HL = D / CPE, FS = od_stride<F>();
+    constexpr int CPE = F / 16, D = F / K, HL = D / CPE, FS = od_stride<F>(), EPS = 64 / K;
     static_assert(K <= 16, "the op-device tile path needs heads of at least f/16 channels");
     extern __shared__ float sh[];
     __shared__ int32_t rps[kOpTile + 1];
+    __shared__ float red[4][F];
     const int32_t t = blockIdx.x, rep = blockIdx.y;
     const int32_t u0 = T.tiles[3 * t], n = T.tiles[3 * t + 1], g = T.tiles[3 * t + 2];
     const int32_t d0 = T.dev_off[g], nd = T.dev_off[g + 1] - d0;
-    float *md = sh, *dod = md + 2 * T.max_dev * FS, *pd = dod + T.max_dev * FS, *qdd = pd + 2 * T.max_dev * K;
-    uint8_t *ent = reinterpret_cast<uint8_t *>(qdd + T.max_dev * K);
+    const int MD = T.max_dev;
+    float *md = sh, *dod = md + 2 * MD * FS, *pd = dod + MD * FS, *qdd = pd + 2 * MD * K;
+    float *ew = qdd + MD * K;            // [4][MD][K][2] (s, dalpha) of the wavefront's current op
+    float *dst = ew + 8 * MD * K;        // [4][MD][K][3] device<-op softmax statistics per wavefront
+    uint8_t *ent = reinterpret_cast<uint8_t *>(dst + 12 * MD * K);
+    for (int i = threadIdx.x; i < 4 * MD * K; i += blockDim.x) {
+        dst[3 * i] = -INFINITY;
+        dst[3 * i + 1] = dst[3 * i + 2] = 0.f;
+    }
     od_stage<F, K, ELU, true>(P, T, rep, u0, n, d0, nd, md, dod, pd, qdd, rps, ent);
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int grp = lane >> 4, jl = lane & 15;
     const int c0 = jl * CPE, h = c0 / D;
-    float a[CPE], u0c[CPE];
-    for (int c = 0; c < CPE; ++c) { a[c] = P.att_src[F + c0 + c]; u0c[c] = P.U[((int64_t)F + c0 + c) * 2 + 0]; }
+    const int ej = lane / K, kq = lane % K;   // (entry, head) of the lane in the op-row softmax
+    float a[CPE], u0c[CPE], cpc[CPE], acc[CPE];
+    for (int c = 0; c < CPE; ++c) {
+        a[c] = P.att_src[F + c0 + c];
+        u0c[c] = P.U[((int64_t)F + c0 + c) * 2 + 0];
+        cpc[c] = P.cp[F + c0 + c];
+        acc[c] = 0.f;
+    }
+    float *eww = ew + (size_t)wv * MD * K * 2, *dsw = dst + (size_t)wv * MD * K * 3;
     const int64_t sbase = (int64_t)rep * T.n_slots;
     const int32_t ebase = rps[0];
     float nyo[CPE], ndO[CPE];
@@ -799,6 +820,7 @@ __global__ void __launch_bounds__(256) bwd_od_scores(BwdLayer P, OdTile T) {
     };
     if (wv < n) fetch(wv);
     for (int32_t ui = wv; ui < n; ui += 4) {
+        const int64_t row = (int64_t)rep * T.n_op + u0 + ui;
         float yo[CPE], dO[CPE], m0[CPE], m1[CPE];
         for (int c = 0; c < CPE; ++c) { yo[c] = nyo[c]; dO[c] = ndO[c]; }
         if (ui + 4 < n) fetch(ui + 4);
@@ -809,7 +831,7 @@ __global__ void __launch_bounds__(256) bwd_od_scores(BwdLayer P, OdTile T) {
             m1[c] = msg_act<ELU>(yo[c] + u0c[c]);
             p0 = fmaf(a[c], m0[c], p0);
             p1 = fmaf(a[c], m1[c], p1);
-            q = fmaf(P.att_dst[F + c0 + c], yo[c] - P.cp[F + c0 + c], q);
+            q = fmaf(P.att_dst[F + c0 + c], yo[c] - cpc[c], q);
         }
         p0 = row_sum<HL>(p0); p1 = row_sum<HL>(p1); q = row_sum<HL>(q);
         const int32_t beg = rps[ui], end = rps[ui + 1];
@@ -827,13 +849,86 @@ __global__ void __launch_bounds__(256) bwd_od_scores(BwdLayer P, OdTile T) {
             d1 = row_sum<HL>(d1);
             d2 = row_sum<HL>(d2);
             if (ok && (jl % HL) == 0) {
+                const float s1 = leaky(pd[(v * 2 + x) * K + h] + q, P.slope);           // op <- device
+                const float s2 = leaky((x ? p1 : p0) + qdd[v * K + h], P.slope);   // device <- op
+                float *w = eww + ((e - beg) * K + h) * 2;
+                w[0] = s1;
+                w[1] = d1;
                 const int64_t idx = (sbase + e) * K + h;
-                T.SA1[idx] = leaky(pd[(v * 2 + x) * K + h] + q, P.slope);   // op <- device
-                T.SD1[idx] = d1;
-                T.SA2[idx] = leaky((x ? p1 : p0) + qdd[v * K + h], P.slope);   // device <- op
+                T.SA2[idx] = s2;
                 T.SD2[idx] = d2;
+                float *st = dsw + (v * K + h) * 3;   // the four groups hold distinct devices
+                float mx = st[0], den = st[1], num = st[2];
+                softmax_fold(s2, d2, mx, den, num);
+                st[0] = mx; st[1] = den; st[2] = num;
             }
         }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        // softmax of the op's row (op <- device), lanes over (entry, head)
+        const int32_t deg = end - beg;
+        float mx = -INFINITY, den = 0.f, num = 0.f;
+        for (int32_t j = ej; j < deg; j += EPS) softmax_fold(eww[(j * K + kq) * 2], eww[(j * K + kq) * 2 + 1], mx, den, num);
+        for (int o = K; o < 64; o <<= 1) {
+            const float m2 = __shfl_xor(mx, o, 64), d2 = __shfl_xor(den, o, 64), n2 = __shfl_xor(num, o, 64);
+            softmax_merge(m2, d2, n2, mx, den, num);
+        }
+        const float inv = den > 0.f ? 1.f / den : 0.f, cc = num * inv;
+        float zs = 0.f;
+        for (int32_t j = ej; j < deg; j += EPS) {
+            const float sv = eww[(j * K + kq) * 2], dv = eww[(j * K + kq) * 2 + 1];
+            const float al = __expf(sv - mx) * inv;
+            const float dz = al * (dv - cc) * (sv > 0.f ? 1.f : P.slope);
+            const int64_t idx = (sbase + beg + j) * K + kq;
+            T.SA1[idx] = al;
+            T.SD1[idx] = dz;
+            zs += dz;
+        }
+        for (int o = K; o < 64; o <<= 1) zs += __shfl_xor(zs, o, 64);
+        if (ej == 0) T.Zop[(row * 2 + 1) * K + kq] = zs;
+        const float zh = __shfl(zs, h, 64);   // lane h < K holds head h
+        if (grp == 0)
+            for (int c = 0; c < CPE; ++c) acc[c] = fmaf(zh, yo[c] - cpc[c], acc[c]);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+    if (grp == 0)
+        for (int c = 0; c < CPE; ++c) red[wv][c0 + c] = acc[c];
+    __syncthreads();
+    // the tile's sums of d adst (op rows) and device<-op records, wavefronts in order
+    const int64_t tb = (int64_t)rep * T.n_tiles + t;
+    for (int c = threadIdx.x; c < F; c += 256) T.part_a1[tb * F + c] = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
+    for (int i = threadIdx.x; i < nd * K; i += blockDim.x) {
+        float mx = dst[3 * i], den = dst[3 * i + 1], num = dst[3 * i + 2];
+        for (int w = 1; w < 4; ++w) {
+            const float *o = dst + ((size_t)w * MD * K + i) * 3;
+            softmax_merge(o[0], o[1], o[2], mx, den, num);
+        }
+        float *r = T.drec + ((tb * MD) * K + i) * 3;
+        r[0] = mx; r[1] = den; r[2] = num;
+    }
+}
+
+// device<-op softmax statistics: per (candidate, device, head) the tiles'
+// records of the device's topology merged in tile order
+__global__ void bwd_od_dev_stats(BwdLayer P, OdTile T, const int32_t *dev_topo, int K) {
+    const int64_t total = (int64_t)P.R * T.n_dev * K;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = i / K;
+        const int h = (int)(i % K);
+        const int32_t rep = (int32_t)(row / T.n_dev), d = (int32_t)(row % T.n_dev);
+        const int32_t g = dev_topo[d], v = d - T.dev_off[g];
+        float mx = -INFINITY, den = 0.f, num = 0.f;
+        for (int32_t t = T.tile_off[g]; t < T.tile_off[g + 1]; ++t) {
+            const float *r = T.drec + ((((int64_t)rep * T.n_tiles + t) * T.max_dev + v) * K + h) * 3;
+            softmax_merge(r[0], r[1], r[2], mx, den, num);
+        }
+        const float inv = den > 0.f ? 1.f / den : 0.f;
+        T.dstat[i * 3 + 0] = mx;
+        T.dstat[i * 3 + 1] = inv;
+        T.dstat[i * 3 + 2] = num * inv;
     }
 }
 
@@ -855,9 +950,17 @@ __global__ void __launch_bounds__(256) bwd_od_messages(BwdLayer P, OdTile T) {
     const int32_t t = blockIdx.x, rep = blockIdx.y;
     const int32_t u0 = T.tiles[3 * t], n = T.tiles[3 * t + 1], g = T.tiles[3 * t + 2];
     const int32_t d0 = T.dev_off[g], nd = T.dev_off[g + 1] - d0;
-    float *md = sh, *dod = md + 2 * T.max_dev * FS, *acc = dod + T.max_dev * FS;   // acc [4][max_dev][FS]
-    uint8_t *ent = reinterpret_cast<uint8_t *>(acc + 4 * T.max_dev * FS);
-    for (int i = threadIdx.x; i < 4 * T.max_dev * FS; i += blockDim.x) acc[i] = 0.f;
+    const int MD = T.max_dev;
+    float *md = sh, *dod = md + 2 * MD * FS, *acc = dod + MD * FS;   // acc [4][MD][FS]
+    float *dsm = acc + 4 * MD * FS;     // [MD][K][3] device<-op statistics (max, 1/sum, c)
+    float *zacc = dsm + 3 * MD * K;     // [4][MD][K] sums of dz over device<-op entries per wavefront
+    uint8_t *ent = reinterpret_cast<uint8_t *>(zacc + 4 * MD * K);
+    for (int i = threadIdx.x; i < 4 * MD * FS; i += blockDim.x) acc[i] = 0.f;
+    for (int i = threadIdx.x; i < 4 * MD * K; i += blockDim.x) zacc[i] = 0.f;
+    {
+        const float *src = T.dstat + ((int64_t)rep * T.n_dev + d0) * K * 3;
+        for (int i = threadIdx.x; i < nd * K * 3; i += blockDim.x) dsm[i] = src[i];
+    }
     od_stage<F, K, ELU, false>(P, T, rep, u0, n, d0, nd, md, dod, nullptr, nullptr, rps, ent);
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int grp = lane >> 4, jl = lane & 15;
@@ -869,7 +972,7 @@ __global__ void __launch_bounds__(256) bwd_od_messages(BwdLayer P, OdTile T) {
         u0c[c] = P.U[((int64_t)F + c0 + c) * 2 + 0];
         ga[c] = gu0[c] = gcp[c] = 0.f;
     }
-    float *accw = acc + (size_t)wv * T.max_dev * FS;
+    float *accw = acc + (size_t)wv * MD * FS, *zw = zacc + (size_t)wv * MD * K;
     const int64_t sbase = (int64_t)rep * T.n_slots * K;
     const int32_t ebase = rps[0];
     auto scalars = [&](int32_t cs, int32_t end, float (&m)[4]) {
@@ -878,6 +981,22 @@ __global__ void __launch_bounds__(256) bwd_od_messages(BwdLayer P, OdTile T) {
             m[0] = T.SA1[i]; m[1] = T.SD1[i]; m[2] = T.SA2[i]; m[3] = T.SD2[i];
         } else {
             m[0] = m[1] = m[2] = m[3] = 0.f;
+        }
+    };
+    // device<-op entries: (s, dalpha) -> (alpha, dz) with the device's merged
+    // statistics, and the dz sums per (device, head); the lanes of a chunk
+    // hold distinct (device, head) pairs
+    auto to_alpha = [&](int32_t cs, int32_t end, float (&m)[4]) {
+        const int32_t e = cs + lane / K;
+        if (e < end) {
+            const int v = ent[e - ebase] & 0x7f, k = lane % K;
+            const float *st = dsm + (v * K + k) * 3;
+            const float sv = m[2];
+            const float al = __expf(sv - st[0]) * st[1];
+            const float dz = al * (m[3] - st[2]) * (sv > 0.f ? 1.f : P.slope);
+            m[2] = al;
+            m[3] = dz;
+            zw[v * K + k] += dz;
         }
     };
     float nyo[CPE], ndO[CPE], nm[4];
@@ -902,6 +1021,7 @@ __global__ void __launch_bounds__(256) bwd_od_messages(BwdLayer P, OdTile T) {
         for (int i = 0; i < 4; ++i) sc[i] = nm[i];
         const int32_t beg = rps[ui], end = rps[ui + 1];
         if (ui + 4 < n) fetch(ui + 4);
+        if (beg < end) to_alpha(beg, end, sc);
         for (int c = 0; c < CPE; ++c) {
             dO[c] *= T.gamma;
             m0[c] = msg_act<ELU>(yo[c]);
@@ -909,7 +1029,10 @@ __global__ void __launch_bounds__(256) bwd_od_messages(BwdLayer P, OdTile T) {
             dys[c] = 0.f;
         }
         for (int32_t cs = beg; cs < end; cs += EPC) {
-            if (cs != beg) scalars(cs, end, sc);   // rows longer than one chunk
+            if (cs != beg) {   // rows longer than one chunk
+                scalars(cs, end, sc);
+                to_alpha(cs, end, sc);
+            }
             const int32_t ce = min(end, cs + EPC);
             for (int32_t e0 = cs; e0 < ce; e0 += 4) {
                 const int32_t e = e0 + grp;
@@ -953,11 +1076,16 @@ __global__ void __launch_bounds__(256) bwd_od_messages(BwdLayer P, OdTile T) {
         gcp[c] += __shfl_xor(gcp[c], 16, 64); gcp[c] += __shfl_xor(gcp[c], 32, 64);
     }
     __syncthreads();
-    // this tile's device partials: the four wavefronts' sums in order
-    float *pdst = T.PD + (((int64_t)rep * T.n_tiles + t) * T.max_dev) * F;
+    // this tile's device partials and dz sums: the four wavefronts' sums in order
+    float *pdst = T.PD + (((int64_t)rep * T.n_tiles + t) * MD) * F;
     for (int i = threadIdx.x; i < nd * F; i += blockDim.x) {
-        const size_t o = (size_t)(i / F) * FS + i % F, st = (size_t)T.max_dev * FS;
+        const size_t o = (size_t)(i / F) * FS + i % F, st = (size_t)MD * FS;
         pdst[i] = (acc[o] + acc[st + o]) + (acc[2 * st + o] + acc[3 * st + o]);
+    }
+    float *zdst = T.zrec + (((int64_t)rep * T.n_tiles + t) * MD) * K;
+    for (int i = threadIdx.x; i < nd * K; i += blockDim.x) {
+        const size_t st = (size_t)MD * K;
+        zdst[i] = (zacc[i] + zacc[st + i]) + (zacc[2 * st + i] + zacc[3 * st + i]);
     }
     // parameter partials of the block
     const int64_t nb = (int64_t)gridDim.x * gridDim.y, b = (int64_t)rep * gridDim.x + t;
@@ -974,20 +1102,39 @@ __global__ void __launch_bounds__(256) bwd_od_messages(BwdLayer P, OdTile T) {
     for (int c = threadIdx.x; c < F; c += 256) T.part[((int64_t)2 * nb + b) * F + c] = 0.f;   // no dU1 for od
 }
 
-// device od rows: the tiles' partials of the row's topology in tile order + Z adst
-__global__ void bwd_od_devices(BwdLayer P, OdTile T, const int32_t *dev_topo, int K) {
-    const int F = P.F, D = F / K;
-    const int64_t total = (int64_t)P.R * T.n_dev * F;
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t row = i / F;
-        const int c = (int)(i % F);
+// device od rows, one wavefront per row: Z = the tiles' dz sums in tile
+// order, dY = the tiles' partials in tile order + Z adst, and per-block sums
+// of d adst = Z (Y - c') over the block's four rows
+template <int F, int K>
+__global__ void __launch_bounds__(256) bwd_od_devices(BwdLayer P, OdTile T, const int32_t *dev_topo) {
+    constexpr int CPL = F / 64, D = F / K;
+    __shared__ float red[4][F];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int64_t row = (int64_t)blockIdx.x * 4 + wv;
+    const int c0 = lane * CPL;
+    float acc[CPL];
+    for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
+    if (row < (int64_t)P.R * T.n_dev) {
         const int32_t rep = (int32_t)(row / T.n_dev), d = (int32_t)(row % T.n_dev);
         const int32_t g = dev_topo[d], v = d - T.dev_off[g];
-        float s = 0.f;
-        for (int32_t t = T.tile_off[g]; t < T.tile_off[g + 1]; ++t)
-            s += T.PD[(((int64_t)rep * T.n_tiles + t) * T.max_dev + v) * F + c];
-        T.dY_dev[row * 2 * F + c] = fmaf(T.Zdev[(row * 2 + 1) * K + c / D], P.att_dst[F + c], s);
+        const int32_t t0 = T.tile_off[g], t1 = T.tile_off[g + 1];
+        const int64_t tb = (int64_t)rep * T.n_tiles;
+        float z = 0.f;
+        if (lane < K)
+            for (int32_t t = t0; t < t1; ++t) z += T.zrec[((tb + t) * T.max_dev + v) * K + lane];
+        if (lane < K) T.Zdev[(row * 2 + 1) * K + lane] = z;
+        const float zh = __shfl(z, c0 / D, 64);
+        for (int c = 0; c < CPL; ++c) {
+            float s = 0.f;
+            for (int32_t t = t0; t < t1; ++t) s += T.PD[((tb + t) * T.max_dev + v) * F + c0 + c];
+            T.dY_dev[row * 2 * F + c0 + c] = fmaf(zh, P.att_dst[F + c0 + c], s);
+            acc[c] = zh * (T.Y_dev[row * 2 * F + F + c0 + c] - P.cp[F + c0 + c]);
+        }
     }
+    for (int c = 0; c < CPL; ++c) red[wv][c0 + c] = acc[c];
+    __syncthreads();
+    for (int c = threadIdx.x; c < F; c += 256)
+        T.part_a2[(int64_t)blockIdx.x * F + c] = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
 }
 
 // slot keys of the op-device links: pos_of[eid] = position in the op<-device
@@ -1474,6 +1621,8 @@ struct TrainLayout {
     float *dU, *dcp;
     float *P0, *P1;
     float *PD, *part_od;     // op-device tile path: device partials, parameter partials
+    float *part_a1, *drec, *dstat, *zrec, *part_a2;   // ... and its softmax records and d adst sums
+    int32_t nb_dev4;         // blocks of bwd_od_devices (four device rows each)
     int32_t *dev_topo;
     int32_t *pos_of, *m21;   // op-device links: edge id -> op<-device position; device<-op position -> same
     // decoder
@@ -1490,17 +1639,18 @@ int64_t n_slots(const tag_graph *g, int b) {
 // the op-device tile path needs the topology's device rows in LDS
 // dynamic LDS bytes of the tile kernels: float rows, then one byte per tile entry
 size_t od_scores_lds(int F, int K, int max_dev) {
-    return sizeof(float) * ((size_t)3 * max_dev * (F + 4) + (size_t)3 * max_dev * K) + (size_t)kOpTile * max_dev;
+    return sizeof(float) * ((size_t)3 * max_dev * (F + 4) + (size_t)23 * max_dev * K) + (size_t)kOpTile * max_dev;
 }
-size_t od_messages_lds(int F, int max_dev) {
-    return sizeof(float) * (size_t)7 * max_dev * (F + 4) + (size_t)kOpTile * max_dev;
+size_t od_messages_lds(int F, int K, int max_dev) {
+    return sizeof(float) * ((size_t)7 * max_dev * (F + 4) + (size_t)7 * max_dev * K) + (size_t)kOpTile * max_dev;
 }
 
 // (heads of at least f/16 channels: one head inside a 16-lane entry group)
 bool od_tiles_fit(const tag_graph *g, int F, int K) {
     // dynamic rows + the static reduction rows and row pointers of the messages kernel
-    return g->n_tiles > 0 && g->max_dev <= 64 && K <= 16 &&
-           od_messages_lds(F, g->max_dev) + sizeof(float) * 4 * F + sizeof(int32_t) * (kOpTile + 1) <= 64 * 1024;
+    const size_t stat = sizeof(float) * 4 * F + sizeof(int32_t) * (kOpTile + 1);   // reduction rows, row pointers
+    return g->n_tiles > 0 && g->max_dev <= 64 && K <= 16 && od_messages_lds(F, K, g->max_dev) + stat <= 64 * 1024 &&
+           od_scores_lds(F, K, g->max_dev) + stat <= 64 * 1024;
 }
 
 int32_t persist_blocks(int64_t items) {
@@ -1570,9 +1720,17 @@ size_t carve_train(const tag_graph *g, const tag_model_dims *d, int32_t R, int32
         const int64_t nb = (int64_t)R * g->n_tiles;
         L->PD = c.take<float>((size_t)nb * g->max_dev * F);
         L->part_od = c.take<float>((size_t)4 * nb * F);
+        L->part_a1 = c.take<float>((size_t)nb * F);
+        L->drec = c.take<float>((size_t)nb * g->max_dev * K * 3);
+        L->dstat = c.take<float>((size_t)std::max<int64_t>(rd, 1) * K * 3);
+        L->zrec = c.take<float>((size_t)nb * g->max_dev * K);
+        L->nb_dev4 = (int32_t)std::max<int64_t>(1, (rd + 3) / 4);
+        L->part_a2 = c.take<float>((size_t)L->nb_dev4 * F);
         L->dev_topo = c.take<int32_t>((size_t)std::max<int64_t>(g->n_dev, 1));
     } else {
         L->PD = L->part_od = nullptr;
+        L->part_a1 = L->drec = L->dstat = L->zrec = L->part_a2 = nullptr;
+        L->nb_dev4 = 0;
         L->dev_topo = nullptr;
     }
     L->pos_of = c.take<int32_t>((size_t)std::max<int64_t>(g->e_od, 1));
@@ -1622,6 +1780,7 @@ void launch_layer_bwd(const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], cons
         prof_end(TAG_STAGE_BWD_SCORES, st);
     }
     for (int b = 0; b < 4; ++b) {
+        if (od && (b == 1 || b == 2)) continue;   // inside the tile kernels
         prof_begin(TAG_STAGE_BWD_SOFTMAX, st);
         float *pa = const_cast<float *>(pr.pa[b]);
         bool long_rows = false;
@@ -1634,11 +1793,14 @@ void launch_layer_bwd(const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], cons
         prof_end(TAG_STAGE_BWD_SOFTMAX, st);
     }
     if (od) {
+        prof_begin(TAG_STAGE_BWD_SOFTMAX, st);
+        bwd_od_dev_stats<<<grid_for((int64_t)P.R * od->n_dev * K), 256, 0, st>>>(P, *od, dev_topo, K);
+        prof_end(TAG_STAGE_BWD_SOFTMAX, st);
         prof_begin(TAG_STAGE_BWD_MESSAGES, st);
         if constexpr (K <= 16)
-            bwd_od_messages<F, K, ELU><<<tgrid, 256, od_messages_lds(F, od->max_dev), st>>>(P, *od);
+            bwd_od_messages<F, K, ELU><<<tgrid, 256, od_messages_lds(F, K, od->max_dev), st>>>(P, *od);
         prof_end(TAG_STAGE_BWD_MESSAGES, st);
-        bwd_od_devices<<<grid_for((int64_t)P.R * od->n_dev * F), 256, 0, st>>>(P, *od, dev_topo, K);
+        bwd_od_devices<F, K><<<(unsigned)(((int64_t)P.R * od->n_dev + 3) / 4), 256, 0, st>>>(P, *od, dev_topo);
     }
     for (int s = 0; s < 4; ++s) {
         if (od && (s == 1 || s == 2)) continue;
@@ -1844,8 +2006,11 @@ extern "C" tag_status tag_train_step(const tag_graph *g, const tag_model_dims *d
             od.Zop = L.Zop; od.Zdev = L.Zdev; od.dY_op = L.dY_op; od.dY_dev = L.dY_dev;
             od.PD = L.PD; od.max_dev = std::max(g->max_dev, 1); od.n_tiles = g->n_tiles;
             od.tile_off = g->tile_off_d; od.part = L.part_od;
+            od.part_a1 = L.part_a1; od.drec = L.drec; od.dstat = L.dstat; od.zrec = L.zrec; od.part_a2 = L.part_a2;
             pr.pm[1] = L.part_od; pr.nb_m[1] = R * g->n_tiles;   // both op-device source passes
             pr.nb_m[2] = 0;
+            pr.pa[1] = L.part_a1; pr.nb_a[1] = R * g->n_tiles;   // both op-device softmaxes
+            pr.pa[2] = L.part_a2; pr.nb_a[2] = L.nb_dev4;
         }
         pr.g_att_src = gr->att_src + (size_t)l * 3 * F;
         pr.g_att_dst = gr->att_dst + (size_t)l * 3 * F;
