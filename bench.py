@@ -75,6 +75,46 @@ def measured_traffic(workload: str, stage: str):
     return None
 
 
+def stage_rooflines(name, wl, topo, R, info, n_slices, n_query, stage_ms) -> tuple:
+    """Per single-kernel stage, from the one profiled step per stage (HIP
+    events on the launch stream, outside the timed region): the mean launch
+    time, the algorithmic bytes (and flops) per launch over it as a fraction
+    of the HBM (and MFMA) peak, and the counter bytes from the committed
+    traffic summary over it when that summary matches the sources.  Also the
+    aggregation stages together: their algorithmic and counter bytes per step
+    over their time per step."""
+    out, agg_t, agg_b, agg_c = {}, 0.0, 0.0, 0.0
+    counter_ok = True
+    for stage, ms in stage_ms.items():
+        if stage in ONCE_PER_STEP or ms <= 0.0:
+            continue
+        avg_s = ms / 1e3 / wl.layers
+        flops, byts = algorithmic_work(stage, wl, topo, R, info, n_slices, n_query)
+        rec = {"avg_launch_ms": round(avg_s * 1e3, 4), "algorithmic_gbs": round(byts / avg_s / 1e9, 1),
+               "algorithmic_hbm_frac": round(byts / avg_s / 1e9 / PEAK_HBM_GBS, 4)}
+        if stage == "transform":
+            rec["mfma_frac"] = round(flops / avg_s / 1e12 / PEAK_TFLOPS[wl.dtype], 4)
+        tr = measured_traffic(name, stage)
+        if tr is not None:
+            rec["counter_gbs"] = round(tr / avg_s / 1e9, 1)
+            rec["counter_hbm_frac"] = round(tr / avg_s / 1e9 / PEAK_HBM_GBS, 4)
+        out[stage] = rec
+        if stage.startswith("agg_") or stage == "dev_prep":
+            agg_t += ms / 1e3
+            agg_b += byts * wl.layers
+            if tr is None:
+                counter_ok = False
+            else:
+                agg_c += tr * wl.layers
+    agg = None
+    if agg_t > 0.0:
+        agg = {"ms_per_step": round(agg_t * 1e3, 4), "algorithmic_gbs": round(agg_b / agg_t / 1e9, 1),
+               "algorithmic_hbm_frac": round(agg_b / agg_t / 1e9 / PEAK_HBM_GBS, 4),
+               "counter_gbs": round(agg_c / agg_t / 1e9, 1) if counter_ok else None,
+               "counter_hbm_frac": round(agg_c / agg_t / 1e9 / PEAK_HBM_GBS, 4) if counter_ok else None}
+    return out, agg
+
+
 def algorithmic_work(stage: str, wl, topo, R: int, info, n_slices: int, n_query: int) -> tuple:
     """(flops, bytes) one launch of `stage` must do at minimum: every unique
     row it reads or writes counted once, graph structure shared by the
@@ -685,6 +725,7 @@ def main() -> int:
     roof.update({"traffic": measured_traffic(name, stage), "kernel": KERNEL_NAMES[stage], "stage": stage,
                  "avg_launch_ms": round(avg_s * 1e3, 4), "launches": n_launch,
                  "algorithmic_bytes_per_launch": byts, "algorithmic_flops_per_launch": flops})
+    stage_roofs, agg = stage_rooflines(name, wl, topo, R, info, len(masks), Q, stage_ms)
     out = {
         "metric": METRIC, "value": round(graphs_s, 2), "unit": "graphs/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
@@ -697,6 +738,8 @@ def main() -> int:
         "edge_layer_updates_per_s": round(T * wl.layers * R * args.steps / el, 1),
         "stage_ms_one_step": {k: round(v, 4) for k, v in stage_ms.items()},
         "roofline": roof,
+        "stage_rooflines": stage_roofs,
+        "aggregation_hbm": agg,
     }
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
