@@ -406,7 +406,7 @@ __global__ void __launch_bounds__(256) dec_full(FullArgs FA) {
 // start (H <= 128): the device part of the pre-activation lives in the
 // lane's registers, and since all lanes sit at the same offset inside
 // their runs, every step toggles the same device j = ctz(step) in all
-// lanes; the t row of j, the option bases and w2 are wave-uniform reads.
+// lanes; the t row of j, the option bases and w2 are wave-uniform LDS reads.
 constexpr int kFullRun = 16;
 
 struct FullTpm {
@@ -434,8 +434,18 @@ __global__ void __launch_bounds__(256) dec_full_tpm(FullTpm T) {
     const int64_t total = (int64_t)1 << nd;
     const int run = total < kFullRun ? (int)total : kFullRun;
     const int64_t g0 = ((int64_t)c * 256 + threadIdx.x) * run;
-    const float *trow = A.t + ((int64_t)r * A.n_dev + d0) * H;
-    const float *bq = T.base + (int64_t)q * 4 * HP;
+    // the query's option bases, w2 and the topology's t rows (zero past H), read
+    // as LDS broadcasts in the inner loops
+    __shared__ float sbq[4 * HP], sw2[HP], strow[16 * HP];
+    for (int i = threadIdx.x; i < 4 * HP; i += 256) sbq[i] = T.base[(int64_t)q * 4 * HP + i];
+    for (int i = threadIdx.x; i < HP; i += 256) sw2[i] = T.w2p[i];
+    for (int i = threadIdx.x; i < nd * HP; i += 256) {
+        const int j = i / HP, h = i % HP;
+        strow[i] = h < H ? A.t[((int64_t)r * A.n_dev + d0 + j) * H + h] : 0.f;
+    }
+    __syncthreads();
+    const float *trow = strow;
+    const float *bq = sbq;
     float m = -INFINITY, z = 0.f;
     int32_t im = INT32_MAX;
     if (g0 < total) {
@@ -447,7 +457,7 @@ __global__ void __launch_bounds__(256) dec_full_tpm(FullTpm T) {
             if (!((mask >> j) & 1u)) continue;
 #pragma unroll
             for (int h = 0; h < HP; ++h)
-                if (h < H) ds[h] += trow[(int64_t)j * H + h];
+                ds[h] += trow[j * HP + h];
         }
         for (int st = 0; st < run; ++st) {
             if (st > 0) {
@@ -456,7 +466,7 @@ __global__ void __launch_bounds__(256) dec_full_tpm(FullTpm T) {
                 const float sg = ((mask >> j) & 1u) ? 1.f : -1.f;
 #pragma unroll
                 for (int h = 0; h < HP; ++h)
-                    if (h < H) ds[h] = fmaf(sg, trow[(int64_t)j * H + h], ds[h]);
+                    ds[h] = fmaf(sg, trow[j * HP + h], ds[h]);
             }
             if (mask == 0) continue;
             float s[4];
@@ -464,7 +474,7 @@ __global__ void __launch_bounds__(256) dec_full_tpm(FullTpm T) {
             for (int o = 0; o < 4; ++o) {
                 float acc = 0.f;
 #pragma unroll
-                for (int h = 0; h < HP; ++h) acc = fmaf(T.w2p[h], fmaxf(ds[h] + bq[o * HP + h], 0.f), acc);
+                for (int h = 0; h < HP; ++h) acc = fmaf(sw2[h], fmaxf(ds[h] + bq[o * HP + h], 0.f), acc);
                 s[o] = A.b2[0] + acc;
             }
             const int32_t a0 = (int32_t)(4 * (mask - 1));
