@@ -352,6 +352,73 @@ __global__ void __launch_bounds__(256) bwd_scores(BwdLayer P, BwdBucket B) {
     }
 }
 
+// scores of short rows (buckets whose rows fit one kChunkA chunk): four
+// rows per wavefront, 16 lanes per row with F/16 channels per lane (heads of
+// at least F/16 channels); the same values as bwd_scores
+template <int F, int K, bool ELU>
+__global__ void __launch_bounds__(256) bwd_scores_short(BwdLayer P, BwdBucket B) {
+    constexpr int CPE = F / 16, LPH = 16 / K, EB = 4;
+    static_assert(K <= 16, "16-lane rows need heads of at least f/16 channels");
+    const int lane = threadIdx.x & 63, grp = lane >> 4, jl = lane & 15;
+    const int64_t ru = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * 4 + grp;
+    const int64_t rows = (int64_t)P.R * B.n_dst;
+    const bool have = ru < rows;
+    const int32_t rep = have ? (int32_t)(ru / B.n_dst) : 0, u = have ? (int32_t)(ru % B.n_dst) : 0;
+    const int32_t beg = have ? B.rp[u] : 0, n = have ? B.rp[u + 1] - beg : 0;
+    const int c0 = jl * CPE, h = c0 / (F / K);
+    const int r = B.rel;
+    float a[CPE], u0[CPE], u1[CPE], yd[CPE], dO[CPE];
+    load_ch<CPE, false>(B.Ydst, (have ? ru : 0) * 2 * F + B.ydst_off + c0, yd);
+    load_ch<CPE, false>(B.dO, (have ? ru : 0) * F + c0, dO);
+    float q = 0.f;
+    for (int c = 0; c < CPE; ++c) {
+        a[c] = P.att_src[r * F + c0 + c];
+        u0[c] = P.U[((int64_t)r * F + c0 + c) * 2 + 0];
+        u1[c] = P.U[((int64_t)r * F + c0 + c) * 2 + 1];
+        q = fmaf(P.att_dst[r * F + c0 + c], yd[c] - P.cp[r * F + c0 + c], q);
+        dO[c] *= B.gamma;
+    }
+    q = row_sum<LPH>(q);
+    int32_t nmax = n;   // the wavefront's longest row
+    nmax = max(nmax, __shfl_xor(nmax, 16, 64));
+    nmax = max(nmax, __shfl_xor(nmax, 32, 64));
+    const int64_t sbase = (int64_t)rep * B.n_slots;
+    for (int32_t i0 = 0; i0 < nmax; i0 += EB) {
+        float ys[EB][CPE], x0[EB], x1[EB];
+        int32_t vv[EB], id[EB];
+#pragma unroll
+        for (int i = 0; i < EB; ++i) {
+            const int32_t e = i0 + i < n ? beg + i0 + i : 0;   // rows past their end read entry 0
+            vv[i] = B.col[e];
+            id[i] = B.eid[e];
+        }
+#pragma unroll
+        for (int i = 0; i < EB; ++i) {
+            load_ch<CPE, false>(B.Ysrc, ((int64_t)rep * B.n_src + vv[i]) * 2 * F + B.ysrc_off + c0, ys[i]);
+            edge_x(P, B.xkind, rep, id[i], x0[i], x1[i]);
+        }
+#pragma unroll
+        for (int i = 0; i < EB; ++i) {
+            float pa = 0.f, pd = 0.f;
+            for (int c = 0; c < CPE; ++c) {
+                const float m = msg_act<ELU>(ys[i][c] + fmaf(u0[c], x0[i], u1[c] * x1[i]));
+                pa = fmaf(a[c], m, pa);
+                pd = fmaf(dO[c], m, pd);
+            }
+            pa = row_sum<LPH>(pa);
+            pd = row_sum<LPH>(pd);
+            const float sv = leaky(pa + q, P.slope);
+            if (i0 + i < n && (jl % LPH) == 0) {
+                const int32_t e = beg + i0 + i;
+                const int64_t slot = entry_slot(B.spos, B.smap, e, B.twin, id[i], u, vv[i]);
+                const int64_t idx = (sbase + slot) * K + h;
+                B.SA[idx] = sv;
+                B.SD[idx] = pd;
+            }
+        }
+    }
+}
+
 // online softmax statistics: fold logit s with weight d into (max, sum, weighted sum)
 __device__ __forceinline__ void softmax_fold(float s, float d, float &mx, float &den, float &num) {
     if (s > mx) {
@@ -1776,7 +1843,14 @@ void launch_layer_bwd(const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], cons
         const int64_t waves = (int64_t)P.R * B[b].n_dst * B[b].chunks;
         if (waves <= 0 || (od && (b == 1 || b == 2))) continue;
         prof_begin(TAG_STAGE_BWD_SCORES, st);
-        bwd_scores<F, K, ELU><<<(unsigned)((waves + 3) / 4), 256, 0, st>>>(P, B[b]);
+        bool short_rows = false;
+        if constexpr (K <= 16) short_rows = B[b].chunks == 1;
+        if (short_rows) {
+            if constexpr (K <= 16)
+                bwd_scores_short<F, K, ELU><<<(unsigned)((waves + 15) / 16), 256, 0, st>>>(P, B[b]);
+        } else {
+            bwd_scores<F, K, ELU><<<(unsigned)((waves + 3) / 4), 256, 0, st>>>(P, B[b]);
+        }
         prof_end(TAG_STAGE_BWD_SCORES, st);
     }
     for (int b = 0; b < 4; ++b) {
