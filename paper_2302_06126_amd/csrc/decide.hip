@@ -460,6 +460,9 @@ __global__ void __launch_bounds__(256) dec_full_tpm(FullTpm T) {
                 ds[h] += trow[j * HP + h];
         }
         for (int st = 0; st < run; ++st) {
+            // read the LDS constants afresh for every mask: held in registers across
+            // the loop they would take 640 of them (one wavefront per SIMD, spills)
+            asm volatile("" ::: "memory");
             if (st > 0) {
                 const int j = __builtin_ctz((unsigned)st);   // same in every lane
                 mask ^= 1u << j;

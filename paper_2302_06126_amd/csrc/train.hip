@@ -715,6 +715,102 @@ __global__ void __launch_bounds__(256) bwd_messages(BwdLayer P, BwdSrc S, float 
     }
 }
 
+// messages of short source rows (single-chunk buckets): persistent
+// wavefronts over quads of source rows, 16 lanes per row with F/16 channels
+// per lane (heads of at least F/16 channels), four entries in flight (two
+// at F = 256); the
+// same values and block sums as bwd_messages
+template <int F, int K, bool ELU>
+__global__ void __launch_bounds__(256) bwd_messages_short(BwdLayer P, BwdSrc S, float *part) {
+    constexpr int CPE = F / 16, D = F / K, EB = F >= 256 ? 2 : 4;   // entries in flight (register budget)
+    static_assert(K <= 16, "16-lane rows need heads of at least f/16 channels");
+    __shared__ float red[4][F];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, grp = lane >> 4, jl = lane & 15;
+    const int c0 = jl * CPE, h = c0 / D;
+    const int r = S.rel;
+    float a[CPE], ad[CPE], u0[CPE], u1[CPE];
+    float ga[CPE], gu0[CPE], gu1[CPE], gcp[CPE];
+    for (int c = 0; c < CPE; ++c) {
+        a[c] = P.att_src[r * F + c0 + c];
+        ad[c] = P.att_dst[r * F + c0 + c];
+        u0[c] = P.U[((int64_t)r * F + c0 + c) * 2 + 0];
+        u1[c] = P.U[((int64_t)r * F + c0 + c) * 2 + 1];
+        ga[c] = gu0[c] = gu1[c] = gcp[c] = 0.f;
+    }
+    const int64_t rows = (int64_t)P.R * S.n_self;
+    const int64_t nw = (int64_t)gridDim.x * 4;
+    for (int64_t qd = (int64_t)blockIdx.x * 4 + wv; qd * 4 < rows; qd += nw) {
+        const int64_t rv = qd * 4 + grp;
+        const bool have = rv < rows;
+        const int32_t rep = have ? (int32_t)(rv / S.n_self) : 0, v = have ? (int32_t)(rv % S.n_self) : 0;
+        const int32_t beg = have ? S.rp[v] : 0, n = have ? S.rp[v + 1] - beg : 0;
+        int32_t nmax = n;   // the wavefront's longest row
+        nmax = max(nmax, __shfl_xor(nmax, 16, 64));
+        nmax = max(nmax, __shfl_xor(nmax, 32, 64));
+        float ys[CPE], dys[CPE];
+        load_ch<CPE, false>(S.Yself, (have ? rv : 0) * 2 * F + S.yoff + c0, ys);
+        for (int c = 0; c < CPE; ++c) dys[c] = 0.f;
+        const int64_t sbase = (int64_t)rep * S.n_slots;
+        for (int32_t i0 = 0; i0 < nmax; i0 += EB) {
+            float dou[EB][CPE], x0[EB], x1[EB], al[EB], dz[EB];
+            int32_t uu[EB], id[EB];
+#pragma unroll
+            for (int i = 0; i < EB; ++i) {
+                const int32_t e = i0 + i < n ? beg + i0 + i : 0;   // rows past their end read entry 0
+                uu[i] = S.col[e];
+                id[i] = S.eid[e];
+            }
+#pragma unroll
+            for (int i = 0; i < EB; ++i) {
+                const int32_t e = i0 + i < n ? beg + i0 + i : 0;
+                load_ch<CPE, false>(S.dOn, ((int64_t)rep * S.n_nbr + uu[i]) * F + c0, dou[i]);
+                edge_x(P, S.xkind, rep, id[i], x0[i], x1[i]);
+                const int64_t slot = entry_slot(S.spos, S.smap, e, S.twin, id[i], uu[i], v);
+                const int64_t idx = (sbase + slot) * K + h;
+                al[i] = S.SA[idx];
+                dz[i] = S.SD[idx];
+            }
+#pragma unroll
+            for (int i = 0; i < EB; ++i) {
+                if (i0 + i >= n) continue;
+                for (int c = 0; c < CPE; ++c) {
+                    const float pre = ys[c] + fmaf(u0[c], x0[i], u1[c] * x1[i]);
+                    const float m = msg_act<ELU>(pre);
+                    const float dm = fmaf(al[i] * S.gamma, dou[i][c], dz[i] * a[c]);
+                    const float dp = pre > 0.f ? dm : (ELU ? dm * (m + 1.f) : 0.f);
+                    dys[c] += dp;
+                    ga[c] = fmaf(dz[i], m, ga[c]);
+                    gu0[c] = fmaf(dp, x0[i], gu0[c]);
+                    gu1[c] = fmaf(dp, x1[i], gu1[c]);
+                    gcp[c] += dp;
+                }
+            }
+        }
+        if (have) {
+            const float zv = S.Z[(rv * 2 + S.zsel) * K + h];
+            float *o = S.dY + rv * 2 * F + S.dyoff + c0;
+            for (int c = 0; c < CPE; ++c) o[c] = fmaf(zv, ad[c], dys[c]);
+        }
+    }
+    // the four row groups' sums, then the wavefronts' in order
+    auto flush = [&](int t, float (&qv)[CPE]) {
+        for (int c = 0; c < CPE; ++c) {
+            qv[c] += __shfl_xor(qv[c], 16, 64);
+            qv[c] += __shfl_xor(qv[c], 32, 64);
+        }
+        if (grp == 0)
+            for (int c = 0; c < CPE; ++c) red[wv][c0 + c] = qv[c];
+        __syncthreads();
+        for (int c = threadIdx.x; c < F; c += 256)
+            part[((int64_t)t * gridDim.x + blockIdx.x) * F + c] = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
+        __syncthreads();
+    };
+    flush(0, ga);
+    flush(1, gu0);
+    flush(2, gu1);
+    flush(3, gcp);
+}
+
 // dY rows of sources with several chunks: the row's chunk partials summed
 // in order, plus Z adst (heads of D = F / K channels)
 __global__ void bwd_combine(BwdLayer P, BwdSrc S, int K) {
@@ -1879,7 +1975,14 @@ void launch_layer_bwd(const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], cons
     for (int s = 0; s < 4; ++s) {
         if (od && (s == 1 || s == 2)) continue;
         prof_begin(TAG_STAGE_BWD_MESSAGES, st);
-        bwd_messages<F, K, ELU><<<pr.nb_m[s], 256, 0, st>>>(P, S[s], const_cast<float *>(pr.pm[s]));
+        bool short_rows = false;
+        if constexpr (K <= 16) short_rows = S[s].chunks == 1;
+        if (short_rows) {
+            if constexpr (K <= 16)
+                bwd_messages_short<F, K, ELU><<<pr.nb_m[s], 256, 0, st>>>(P, S[s], const_cast<float *>(pr.pm[s]));
+        } else {
+            bwd_messages<F, K, ELU><<<pr.nb_m[s], 256, 0, st>>>(P, S[s], const_cast<float *>(pr.pm[s]));
+        }
         prof_end(TAG_STAGE_BWD_MESSAGES, st);
         if (S[s].chunks > 1) bwd_combine<<<grid_for((int64_t)P.R * S[s].n_self * F), 256, 0, st>>>(P, S[s], K);
     }
