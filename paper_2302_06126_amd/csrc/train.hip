@@ -611,6 +611,85 @@ __global__ void __launch_bounds__(256) bwd_softmax(BwdLayer P, BwdBucket B, floa
         part_ad[(int64_t)blockIdx.x * F + c] = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
 }
 
+// softmax backward of short rows (single-chunk buckets): persistent
+// wavefronts over quads of destination rows, 16 lanes per row over (entry,
+// head) pairs for the statistics and over F/16 channels for d adst; the same
+// values as bwd_softmax
+template <int F, int K>
+__global__ void __launch_bounds__(256) bwd_softmax_short(BwdLayer P, BwdBucket B, float *part_ad) {
+    constexpr int CPE = F / 16, EPS = 16 / K, D = F / K;
+    static_assert(K <= 16, "16-lane rows need heads of at least f/16 channels");
+    __shared__ float red[4][F];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, grp = lane >> 4, jl = lane & 15;
+    const int ei = jl / K, k = jl % K;
+    const int c0 = jl * CPE;
+    const int r = B.rel;
+    float acc[CPE], cp[CPE];
+    for (int c = 0; c < CPE; ++c) {
+        acc[c] = 0.f;
+        cp[c] = P.cp[r * F + c0 + c];
+    }
+    const int64_t rows = (int64_t)P.R * B.n_dst;
+    const int64_t nw = (int64_t)gridDim.x * 4;
+    for (int64_t qd = (int64_t)blockIdx.x * 4 + wv; qd * 4 < rows; qd += nw) {
+        const int64_t ru = qd * 4 + grp;
+        const bool have = ru < rows;
+        const int32_t rep = have ? (int32_t)(ru / B.n_dst) : 0, u = have ? (int32_t)(ru % B.n_dst) : 0;
+        const int32_t beg = have ? B.rp[u] : 0, end = have ? B.rp[u + 1] : 0;
+        int32_t nmax = end - beg;   // the wavefront's longest row
+        nmax = max(nmax, __shfl_xor(nmax, 16, 64));
+        nmax = max(nmax, __shfl_xor(nmax, 32, 64));
+        const int64_t sbase = (int64_t)rep * B.n_slots;
+        auto slot_at = [&](int32_t e) -> int64_t {
+            return B.spos ? (int64_t)e : (B.smap ? (int64_t)B.smap[e] : slot_of(B.twin, B.eid[e], u, B.col[e]));
+        };
+        float mx = -INFINITY, den = 0.f, num = 0.f;
+        for (int32_t j0 = 0; j0 < nmax; j0 += EPS) {
+            const int32_t e = beg + j0 + ei;
+            if (e < end) {
+                const int64_t idx = (sbase + slot_at(e)) * K + k;
+                softmax_fold(B.SA[idx], B.SD[idx], mx, den, num);
+            }
+        }
+        for (int o = K; o < 16; o <<= 1) {
+            const float m2 = __shfl_xor(mx, o, 64), d2 = __shfl_xor(den, o, 64), n2 = __shfl_xor(num, o, 64);
+            softmax_merge(m2, d2, n2, mx, den, num);
+        }
+        const float inv = den > 0.f ? 1.f / den : 0.f, cc = num * inv;
+        float zs = 0.f;
+        for (int32_t j0 = 0; j0 < nmax; j0 += EPS) {
+            const int32_t e = beg + j0 + ei;
+            if (e < end) {
+                const int64_t idx = (sbase + slot_at(e)) * K + k;
+                const float sv = B.SA[idx], da = B.SD[idx];
+                const float al = __expf(sv - mx) * inv;
+                const float dz = al * (da - cc) * (sv > 0.f ? 1.f : P.slope);
+                B.SA[idx] = al;
+                B.SD[idx] = dz;
+                zs += dz;
+            }
+        }
+        for (int o = K; o < 16; o <<= 1) zs += __shfl_xor(zs, o, 64);
+        if (have && ei == 0) B.Z[(ru * 2 + B.zsel) * K + k] = zs;
+        const float zh = __shfl(zs, grp * 16 + c0 / D, 64);   // lane h of the group holds head h
+        if (have && end > beg) {
+            float yd[CPE];
+            load_ch<CPE, false>(B.Ydst, ru * 2 * F + B.ydst_off + c0, yd);
+            for (int c = 0; c < CPE; ++c) acc[c] = fmaf(zh, yd[c] - cp[c], acc[c]);
+        }
+    }
+    // the four row groups' sums, then the wavefronts' in order
+    for (int c = 0; c < CPE; ++c) {
+        acc[c] += __shfl_xor(acc[c], 16, 64);
+        acc[c] += __shfl_xor(acc[c], 32, 64);
+    }
+    if (grp == 0)
+        for (int c = 0; c < CPE; ++c) red[wv][c0 + c] = acc[c];
+    __syncthreads();
+    for (int c = threadIdx.x; c < F; c += 256)
+        part_ad[(int64_t)blockIdx.x * F + c] = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
+}
+
 // Rows of one node type as sources: the entries they feed, listed by the
 // bucket in which the row is the destination of the same relation.
 struct BwdSrc {
@@ -1953,10 +2032,15 @@ void launch_layer_bwd(const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], cons
         if (od && (b == 1 || b == 2)) continue;   // inside the tile kernels
         prof_begin(TAG_STAGE_BWD_SOFTMAX, st);
         float *pa = const_cast<float *>(pr.pa[b]);
-        bool long_rows = false;
-        if constexpr (K <= 16) long_rows = B[b].chunks * kChunkA >= kLongRow;
+        bool long_rows = false, short_rows = false;
+        if constexpr (K <= 16) {
+            long_rows = B[b].chunks * kChunkA >= kLongRow;
+            short_rows = B[b].chunks == 1;
+        }
         if (long_rows) {
             if constexpr (K <= 16) bwd_softmax<F, K, true><<<pr.nb_a[b], 256, 0, st>>>(P, B[b], pa);
+        } else if (short_rows) {
+            if constexpr (K <= 16) bwd_softmax_short<F, K><<<pr.nb_a[b], 256, 0, st>>>(P, B[b], pa);
         } else {
             bwd_softmax<F, K, false><<<pr.nb_a[b], 256, 0, st>>>(P, B[b], pa);
         }
