@@ -1181,24 +1181,39 @@ __device__ __forceinline__ float dact(float m) { return m > 0.f ? 1.f : (ELU ? m
 // The (alpha, dz) scalars of an op's entries come in chunks of 64 / K
 // entries, lane i holding entry i / K, head i % K of the chunk (one
 // coalesced read per array); the first chunk of the next op is read ahead.
+// Op side per entry (the wavefront's op is the source of device<-op links):
+// dY of the op row and the op's parts of d a, dU0 and dc'.  Device side
+// (op<-device links, the devices are the sources): each entry's alpha goes
+// into a dense per-head matrix aw[h][device][op] (the placement bit in the
+// sign bit; alpha >= 0) and its dz into per-bit sums; after the tile's ops,
+// sum_u alpha_uv gamma dO_u[c] for each placement bit is a (devices x 64 ops)
+// by (64 ops x channels) product on the matrix cores, and sigma' of the
+// device's message, the a Z terms and the device parts of d a, dU0 and dc'
+// are applied once per (device, channel).
+constexpr int kAS = 68;   // row stride of aw: the 16 x 4 operand reads fall on distinct banks
+
 template <int F, int K, bool ELU>
 __global__ void __launch_bounds__(256) bwd_od_messages(BwdLayer P, OdTile T) {
-    constexpr int CPE = F / 16, FS = od_stride<F>(), EPC = 64 / K;
+    constexpr int CPE = F / 16, FS = od_stride<F>(), EPC = 64 / K, D = F / K;
     constexpr bool AHEAD = CPE <= 8;   // read the next op's rows ahead (register budget)
-    static_assert(K <= 16, "the op-device tile path needs heads of at least f/16 channels");
+    static_assert(K <= 16 && D >= 16, "the op-device tile path needs heads of at least 16 channels");
     extern __shared__ float sh[];
     __shared__ float red[4][F];
+    __shared__ float dpart[3][F];      // device side of d a, dU0, dc' per channel
     __shared__ int32_t rps[kOpTile + 1];
     const int32_t t = blockIdx.x, rep = blockIdx.y;
     const int32_t u0 = T.tiles[3 * t], n = T.tiles[3 * t + 1], g = T.tiles[3 * t + 2];
     const int32_t d0 = T.dev_off[g], nd = T.dev_off[g + 1] - d0;
-    const int MD = T.max_dev;
-    float *md = sh, *dod = md + 2 * MD * FS, *acc = dod + MD * FS;   // acc [4][MD][FS]
-    float *dsm = acc + 4 * MD * FS;     // [MD][K][3] device<-op statistics (max, 1/sum, c)
+    const int MD = T.max_dev, MDP = (MD + 15) & ~15;
+    float *md = sh, *dod = md + 2 * MD * FS;
+    float *aw = dod + MD * FS;          // [K][MDP][kAS] alpha of op<-device entries, sign bit = placement bit
+    float *dsm = aw + K * MDP * kAS;    // [MD][K][3] device<-op statistics (max, 1/sum, c)
     float *zacc = dsm + 3 * MD * K;     // [4][MD][K] sums of dz over device<-op entries per wavefront
-    uint8_t *ent = reinterpret_cast<uint8_t *>(zacc + 4 * MD * K);
-    for (int i = threadIdx.x; i < 4 * MD * FS; i += blockDim.x) acc[i] = 0.f;
+    float *z1 = zacc + 4 * MD * K;      // [4][2][K][MDP] sums of dz over op<-device entries per wavefront and bit
+    uint8_t *ent = reinterpret_cast<uint8_t *>(z1 + 8 * K * MDP);
+    for (int i = threadIdx.x; i < K * MDP * kAS; i += blockDim.x) aw[i] = 0.f;
     for (int i = threadIdx.x; i < 4 * MD * K; i += blockDim.x) zacc[i] = 0.f;
+    for (int i = threadIdx.x; i < 8 * K * MDP; i += blockDim.x) z1[i] = 0.f;
     {
         const float *src = T.dstat + ((int64_t)rep * T.n_dev + d0) * K * 3;
         for (int i = threadIdx.x; i < nd * K * 3; i += blockDim.x) dsm[i] = src[i];
@@ -1206,7 +1221,7 @@ __global__ void __launch_bounds__(256) bwd_od_messages(BwdLayer P, OdTile T) {
     od_stage<F, K, ELU, false>(P, T, rep, u0, n, d0, nd, md, dod, nullptr, nullptr, rps, ent);
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int grp = lane >> 4, jl = lane & 15;
-    const int c0 = jl * CPE, h = c0 / (F / K);
+    const int c0 = jl * CPE, h = c0 / D;
     float a[CPE], ad[CPE], u0c[CPE], ga[CPE], gu0[CPE], gcp[CPE];
     for (int c = 0; c < CPE; ++c) {
         a[c] = P.att_src[F + c0 + c];
@@ -1214,7 +1229,7 @@ __global__ void __launch_bounds__(256) bwd_od_messages(BwdLayer P, OdTile T) {
         u0c[c] = P.U[((int64_t)F + c0 + c) * 2 + 0];
         ga[c] = gu0[c] = gcp[c] = 0.f;
     }
-    float *accw = acc + (size_t)wv * MD * FS, *zw = zacc + (size_t)wv * MD * K;
+    float *zw = zacc + (size_t)wv * MD * K, *z1w = z1 + (size_t)wv * 2 * K * MDP;
     const int64_t sbase = (int64_t)rep * T.n_slots * K;
     const int32_t ebase = rps[0];
     auto scalars = [&](int32_t cs, int32_t end, float (&m)[4]) {
@@ -1225,13 +1240,17 @@ __global__ void __launch_bounds__(256) bwd_od_messages(BwdLayer P, OdTile T) {
             m[0] = m[1] = m[2] = m[3] = 0.f;
         }
     };
-    // device<-op entries: (s, dalpha) -> (alpha, dz) with the device's merged
-    // statistics, and the dz sums per (device, head); the lanes of a chunk
-    // hold distinct (device, head) pairs
-    auto to_alpha = [&](int32_t cs, int32_t end, float (&m)[4]) {
+    // per entry and head (the lanes of a chunk hold distinct (device, head)
+    // pairs): op<-device alpha into aw and dz into the per-bit sums;
+    // device<-op (s, dalpha) -> (alpha, dz) with the device's merged
+    // statistics, and the dz sums per (device, head)
+    auto to_alpha = [&](int32_t cs, int32_t end, int32_t ui, float (&m)[4]) {
         const int32_t e = cs + lane / K;
         if (e < end) {
-            const int v = ent[e - ebase] & 0x7f, k = lane % K;
+            const int eb = ent[e - ebase];
+            const int v = eb & 0x7f, x = eb >> 7, k = lane % K;
+            aw[(k * MDP + v) * kAS + ui] = __int_as_float(__float_as_int(m[0]) | (x << 31));
+            z1w[(x * K + k) * MDP + v] += m[1];
             const float *st = dsm + (v * K + k) * 3;
             const float sv = m[2];
             const float al = __expf(sv - st[0]) * st[1];
@@ -1246,26 +1265,23 @@ __global__ void __launch_bounds__(256) bwd_od_messages(BwdLayer P, OdTile T) {
         if constexpr (AHEAD) {
             const int64_t row = (int64_t)rep * T.n_op + u0 + ui;
             load_ch<CPE, false>(T.Y_op, row * 2 * F + F + c0, nyo);
-            load_ch<CPE, false>(T.dO_op, row * F + c0, ndO);
         }
         scalars(rps[ui], rps[ui + 1], nm);
     };
     if (wv < n) fetch(wv);
     for (int32_t ui = wv; ui < n; ui += 4) {
         const int64_t row = (int64_t)rep * T.n_op + u0 + ui;
-        float yo[CPE], dO[CPE], m0[CPE], m1[CPE], dys[CPE], sc[4];
+        float yo[CPE], m0[CPE], m1[CPE], dys[CPE], sc[4];
         if constexpr (AHEAD) {
-            for (int c = 0; c < CPE; ++c) { yo[c] = nyo[c]; dO[c] = ndO[c]; }
+            for (int c = 0; c < CPE; ++c) yo[c] = nyo[c];
         } else {
             load_ch<CPE, false>(T.Y_op, row * 2 * F + F + c0, yo);
-            load_ch<CPE, false>(T.dO_op, row * F + c0, dO);
         }
         for (int i = 0; i < 4; ++i) sc[i] = nm[i];
         const int32_t beg = rps[ui], end = rps[ui + 1];
         if (ui + 4 < n) fetch(ui + 4);
-        if (beg < end) to_alpha(beg, end, sc);
+        if (beg < end) to_alpha(beg, end, ui, sc);
         for (int c = 0; c < CPE; ++c) {
-            dO[c] *= T.gamma;
             m0[c] = msg_act<ELU>(yo[c]);
             m1[c] = msg_act<ELU>(yo[c] + u0c[c]);
             dys[c] = 0.f;
@@ -1273,30 +1289,24 @@ __global__ void __launch_bounds__(256) bwd_od_messages(BwdLayer P, OdTile T) {
         for (int32_t cs = beg; cs < end; cs += EPC) {
             if (cs != beg) {   // rows longer than one chunk
                 scalars(cs, end, sc);
-                to_alpha(cs, end, sc);
+                to_alpha(cs, end, ui, sc);
             }
             const int32_t ce = min(end, cs + EPC);
             for (int32_t e0 = cs; e0 < ce; e0 += 4) {
                 const int32_t e = e0 + grp;
                 const int src = (e - cs) * K + h;   // < 64: e - cs < EPC
-                const float al1 = __shfl(sc[0], src, 64), dz1 = __shfl(sc[1], src, 64);   // op u <- device v
                 const float al2 = __shfl(sc[2], src, 64), dz2 = __shfl(sc[3], src, 64);   // device v <- op u
                 if (e < ce) {
                     const int eb = ent[e - ebase];
                     const int v = eb & 0x7f, x = eb >> 7;
-                    const float *mv = md + (v * 2 + x) * FS + c0, *dv = dod + v * FS + c0;
-                    float *av = accw + v * FS + c0;
+                    const float *dv = dod + v * FS + c0;
                     for (int c = 0; c < CPE; ++c) {
                         const float mo = x ? m1[c] : m0[c];
                         const float dpo = dact<ELU>(mo) * fmaf(al2, dv[c], dz2 * a[c]);
                         dys[c] += dpo;
                         ga[c] = fmaf(dz2, mo, ga[c]);
-                        const float dpd = dact<ELU>(mv[c]) * fmaf(al1, dO[c], dz1 * a[c]);
-                        av[c] += dpd;
-                        ga[c] = fmaf(dz1, mv[c], ga[c]);
-                        const float both = dpo + dpd;
-                        if (x) gu0[c] += both;
-                        gcp[c] += both;
+                        if (x) gu0[c] += dpo;
+                        gcp[c] += dpo;
                     }
                 }
             }
@@ -1318,29 +1328,76 @@ __global__ void __launch_bounds__(256) bwd_od_messages(BwdLayer P, OdTile T) {
         gcp[c] += __shfl_xor(gcp[c], 16, 64); gcp[c] += __shfl_xor(gcp[c], 32, 64);
     }
     __syncthreads();
-    // this tile's device partials and dz sums: the four wavefronts' sums in order
+    // device side on the matrix cores: wavefront w takes the 16-channel column
+    // blocks w, w + 4, ...; lane l supplies aw[h][rb + l % 16][ks + l / 16]
+    // (A, by bit) and gamma dO[ks + l / 16][column] (B); result register r of
+    // lane l is device rb + 4 (l / 16) + r, channel cb 16 + l % 16
     float *pdst = T.PD + (((int64_t)rep * T.n_tiles + t) * MD) * F;
-    for (int i = threadIdx.x; i < nd * F; i += blockDim.x) {
-        const size_t o = (size_t)(i / F) * FS + i % F, st = (size_t)MD * FS;
-        pdst[i] = (acc[o] + acc[st + o]) + (acc[2 * st + o] + acc[3 * st + o]);
+    for (int cb = wv; cb < F / 16; cb += 4) {
+        const int cl = cb * 16 + (lane & 15), hc = cl / D;
+        const float ac = P.att_src[F + cl];
+        float sga = 0.f, sgu = 0.f, sgc = 0.f;
+        float bo[kOpTile / 4];   // this lane's B operands, one per k step
+#pragma unroll
+        for (int ks = 0; ks < kOpTile / 4; ++ks) {
+            const int uk = 4 * ks + (lane >> 4);
+            bo[ks] = uk < n ? T.gamma * T.dO_op[((int64_t)rep * T.n_op + u0 + uk) * F + cl] : 0.f;
+        }
+        for (int rb = 0; rb < MDP; rb += 16) {
+            f4 t0 = f4{0.f, 0.f, 0.f, 0.f}, t1 = f4{0.f, 0.f, 0.f, 0.f};
+            const float *arow = aw + (hc * MDP + rb + (lane & 15)) * kAS + (lane >> 4);
+#pragma unroll
+            for (int ks = 0; ks < kOpTile / 4; ++ks) {
+                const float w = arow[4 * ks];
+                const bool bit = __float_as_int(w) < 0;
+                const float wa = fabsf(w);
+                t0 = __builtin_amdgcn_mfma_f32_16x16x4f32(bit ? 0.f : wa, bo[ks], t0, 0, 0, 0);
+                t1 = __builtin_amdgcn_mfma_f32_16x16x4f32(bit ? wa : 0.f, bo[ks], t1, 0, 0, 0);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int v = rb + 4 * (lane >> 4) + r;
+                if (v < nd) {
+                    float zb0 = 0.f, zb1 = 0.f;   // the wavefronts' dz sums in order
+                    for (int w = 0; w < 4; ++w) {
+                        zb0 += z1[((w * 2 + 0) * K + hc) * MDP + v];
+                        zb1 += z1[((w * 2 + 1) * K + hc) * MDP + v];
+                    }
+                    const float mb0 = md[(v * 2 + 0) * FS + cl], mb1 = md[(v * 2 + 1) * FS + cl];
+                    const float p0 = dact<ELU>(mb0) * fmaf(ac, zb0, t0[r]);
+                    const float p1 = dact<ELU>(mb1) * fmaf(ac, zb1, t1[r]);
+                    pdst[(int64_t)v * F + cl] = p0 + p1;
+                    sga = fmaf(mb0, zb0, fmaf(mb1, zb1, sga));
+                    sgu += p1;
+                    sgc += p0 + p1;
+                }
+            }
+        }
+        // the column's sums over the four lane groups (device rows)
+        sga += __shfl_xor(sga, 16, 64); sga += __shfl_xor(sga, 32, 64);
+        sgu += __shfl_xor(sgu, 16, 64); sgu += __shfl_xor(sgu, 32, 64);
+        sgc += __shfl_xor(sgc, 16, 64); sgc += __shfl_xor(sgc, 32, 64);
+        if (lane < 16) { dpart[0][cl] = sga; dpart[1][cl] = sgu; dpart[2][cl] = sgc; }
     }
+    // this tile's dz sums of device<-op entries: the four wavefronts' sums in order
     float *zdst = T.zrec + (((int64_t)rep * T.n_tiles + t) * MD) * K;
     for (int i = threadIdx.x; i < nd * K; i += blockDim.x) {
         const size_t st = (size_t)MD * K;
         zdst[i] = (zacc[i] + zacc[st + i]) + (zacc[2 * st + i] + zacc[3 * st + i]);
     }
-    // parameter partials of the block
+    // parameter partials of the block: the wavefronts' op-side sums in order, then the device side
     const int64_t nb = (int64_t)gridDim.x * gridDim.y, b = (int64_t)rep * gridDim.x + t;
-    float *q[3] = {ga, gu0, gcp};
-    const int slot_of_q[3] = {0, 1, 3};
-    for (int qq = 0; qq < 3; ++qq) {
+    auto flush = [&](int qq, int slot, const float (&qv)[CPE]) {
         if (grp == 0)
-            for (int c = 0; c < CPE; ++c) red[wv][c0 + c] = q[qq][c];
+            for (int c = 0; c < CPE; ++c) red[wv][c0 + c] = qv[c];
         __syncthreads();
         for (int c = threadIdx.x; c < F; c += 256)
-            T.part[((int64_t)slot_of_q[qq] * nb + b) * F + c] = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
+            T.part[((int64_t)slot * nb + b) * F + c] = ((red[0][c] + red[1][c]) + (red[2][c] + red[3][c])) + dpart[qq][c];
         __syncthreads();
-    }
+    };
+    flush(0, 0, ga);
+    flush(1, 1, gu0);
+    flush(2, 3, gcp);
     for (int c = threadIdx.x; c < F; c += 256) T.part[((int64_t)2 * nb + b) * F + c] = 0.f;   // no dU1 for od
 }
 
@@ -1884,14 +1941,18 @@ size_t od_scores_lds(int F, int K, int max_dev) {
     return sizeof(float) * ((size_t)3 * max_dev * (F + 4) + (size_t)23 * max_dev * K) + (size_t)kOpTile * max_dev;
 }
 size_t od_messages_lds(int F, int K, int max_dev) {
-    return sizeof(float) * ((size_t)7 * max_dev * (F + 4) + (size_t)7 * max_dev * K) + (size_t)kOpTile * max_dev;
+    const size_t mdp = (size_t)(max_dev + 15) / 16 * 16;
+    return sizeof(float) * ((size_t)3 * max_dev * (F + 4) + (size_t)K * mdp * kAS + (size_t)7 * max_dev * K +
+                            (size_t)8 * K * mdp) + (size_t)kOpTile * max_dev;
 }
 
-// (heads of at least f/16 channels: one head inside a 16-lane entry group)
+// (heads of at least 16 channels and at least f/16: one head inside a 16-lane
+// entry group and inside a 16-channel column block of the device-side products)
 bool od_tiles_fit(const tag_graph *g, int F, int K) {
     // dynamic rows + the static reduction rows and row pointers of the messages kernel
-    const size_t stat = sizeof(float) * 4 * F + sizeof(int32_t) * (kOpTile + 1);   // reduction rows, row pointers
-    return g->n_tiles > 0 && g->max_dev <= 64 && K <= 16 && od_messages_lds(F, K, g->max_dev) + stat <= 64 * 1024 &&
+    const size_t stat = sizeof(float) * 7 * F + sizeof(int32_t) * (kOpTile + 1);   // reduction rows, row pointers
+    return g->n_tiles > 0 && g->max_dev <= 64 && K <= 16 && F / K >= 16 &&
+           od_messages_lds(F, K, g->max_dev) + stat <= 64 * 1024 &&
            od_scores_lds(F, K, g->max_dev) + stat <= 64 * 1024;
 }
 
@@ -2010,7 +2071,7 @@ void launch_layer_bwd(const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], cons
     const dim3 tgrid(od ? (unsigned)od->n_tiles : 1u, (unsigned)P.R);
     if (od) {
         prof_begin(TAG_STAGE_BWD_SCORES, st);
-        if constexpr (K <= 16)
+        if constexpr (K <= 16 && F / K >= 16)
             bwd_od_scores<F, K, ELU><<<tgrid, 256, od_scores_lds(F, K, od->max_dev), st>>>(P, *od);
         prof_end(TAG_STAGE_BWD_SCORES, st);
     }
@@ -2051,7 +2112,7 @@ void launch_layer_bwd(const BwdLayer &P, BwdBucket (&B)[4], BwdSrc (&S)[4], cons
         bwd_od_dev_stats<<<grid_for((int64_t)P.R * od->n_dev * K), 256, 0, st>>>(P, *od, dev_topo, K);
         prof_end(TAG_STAGE_BWD_SOFTMAX, st);
         prof_begin(TAG_STAGE_BWD_MESSAGES, st);
-        if constexpr (K <= 16)
+        if constexpr (K <= 16 && F / K >= 16)
             bwd_od_messages<F, K, ELU><<<tgrid, 256, od_messages_lds(F, K, od->max_dev), st>>>(P, *od);
         prof_end(TAG_STAGE_BWD_MESSAGES, st);
         bwd_od_devices<F, K><<<(unsigned)(((int64_t)P.R * od->n_dev + 3) / 4), 256, 0, st>>>(P, *od, dev_topo);
