@@ -1020,124 +1020,159 @@ __device__ void od_stage(const BwdLayer &P, const OdTile &T, int32_t rep, int32_
 // u0 + wv + 4, ... and reads the rows of its next op while it works on the
 // current one.  Slots of op-device entries are keyed by their position in
 // the op<-device bucket.
+// max over aligned groups of 16 lanes (DPP inside a 16-lane row)
+__device__ __forceinline__ float row_max16(float v) {
+    auto dpp = [](float x, auto ctrl) {
+        return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), decltype(ctrl)::value, 0xf, 0xf, true));
+    };
+    v = fmaxf(v, dpp(v, std::integral_constant<int, 0xB1>{}));    // quad_perm [1,0,3,2]
+    v = fmaxf(v, dpp(v, std::integral_constant<int, 0x4E>{}));    // quad_perm [2,3,0,1]
+    v = fmaxf(v, dpp(v, std::integral_constant<int, 0x141>{}));   // row_half_mirror
+    v = fmaxf(v, dpp(v, std::integral_constant<int, 0x140>{}));   // row_mirror
+    return v;
+}
+
+// Scores on the matrix cores (topologies of at most 16 devices): wavefront w
+// takes the tile's ops 16 w .. 16 w + 15; per head and placement bit b the
+// logit gradients dO_u . m_b(v) (op <- device) and dO_v . m_b(u) (device <-
+// op) are fp32 MFMA 16x16x4 products over the head's channels, lane l
+// supplying op 16 w + l % 16 (A) and device l % 16 (B) at channel slice
+// l / 16.  Result register r of lane l is op 16 w + 4 (l / 16) + r, device
+// l % 16: an op row's entries lie in the 16 lanes of one lane group, so its
+// softmax (op <- device) reduces over those lanes; the device<-op records
+// fold per lane over its four ops, then over lane groups and wavefronts in order.
 template <int F, int K, bool ELU>
 __global__ void __launch_bounds__(256) bwd_od_scores(BwdLayer P, OdTile T) {
-    constexpr int CPE = F / 16, D = F / K, HL = D / CPE, FS = od_stride<F>(), EPS = 64 / K;
-    static_assert(K <= 16, "the op-device tile path needs heads of at least f/16 channels");
+    constexpr int D = F / K, FS = od_stride<F>(), CPL = F / 64;
+    static_assert(K <= 16 && D >= 16, "the op-device tile path needs heads of at least 16 channels");
     extern __shared__ float sh[];
     __shared__ int32_t rps[kOpTile + 1];
+    __shared__ uint64_t pres[kOpTile], bits[kOpTile];
+    __shared__ float zop[kOpTile][K];   // Z of the tile's op rows (op <- device)
     __shared__ float red[4][F];
     const int32_t t = blockIdx.x, rep = blockIdx.y;
     const int32_t u0 = T.tiles[3 * t], n = T.tiles[3 * t + 1], g = T.tiles[3 * t + 2];
     const int32_t d0 = T.dev_off[g], nd = T.dev_off[g + 1] - d0;
     const int MD = T.max_dev;
     float *md = sh, *dod = md + 2 * MD * FS, *pd = dod + MD * FS, *qdd = pd + 2 * MD * K;
-    float *ew = qdd + MD * K;            // [4][MD][K][2] (s, dalpha) of the wavefront's current op
-    float *dst = ew + 8 * MD * K;        // [4][MD][K][3] device<-op softmax statistics per wavefront
-    uint8_t *ent = reinterpret_cast<uint8_t *>(dst + 12 * MD * K);
-    for (int i = threadIdx.x; i < 4 * MD * K; i += blockDim.x) {
+    float *dst = qdd + MD * K;           // [4][16][K][3] device<-op records per wavefront
+    uint8_t *ent = reinterpret_cast<uint8_t *>(dst + 4 * 16 * K * 3);
+    for (int i = threadIdx.x; i < 4 * 16 * K; i += blockDim.x) {
         dst[3 * i] = -INFINITY;
         dst[3 * i + 1] = dst[3 * i + 2] = 0.f;
     }
     od_stage<F, K, ELU, true>(P, T, rep, u0, n, d0, nd, md, dod, pd, qdd, rps, ent);
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const int grp = lane >> 4, jl = lane & 15;
-    const int c0 = jl * CPE, h = c0 / D;
-    const int ej = lane / K, kq = lane % K;   // (entry, head) of the lane in the op-row softmax
-    float a[CPE], u0c[CPE], cpc[CPE], acc[CPE];
-    for (int c = 0; c < CPE; ++c) {
-        a[c] = P.att_src[F + c0 + c];
-        u0c[c] = P.U[((int64_t)F + c0 + c) * 2 + 0];
-        cpc[c] = P.cp[F + c0 + c];
-        acc[c] = 0.f;
-    }
-    float *eww = ew + (size_t)wv * MD * K * 2, *dsw = dst + (size_t)wv * MD * K * 3;
-    const int64_t sbase = (int64_t)rep * T.n_slots;
-    const int32_t ebase = rps[0];
-    float nyo[CPE], ndO[CPE];
-    auto fetch = [&](int32_t ui) {
-        const int64_t row = (int64_t)rep * T.n_op + u0 + ui;
-        load_ch<CPE, false>(T.Y_op, row * 2 * F + F + c0, nyo);
-        load_ch<CPE, false>(T.dO_op, row * F + c0, ndO);
-    };
-    if (wv < n) fetch(wv);
-    for (int32_t ui = wv; ui < n; ui += 4) {
-        const int64_t row = (int64_t)rep * T.n_op + u0 + ui;
-        float yo[CPE], dO[CPE], m0[CPE], m1[CPE];
-        for (int c = 0; c < CPE; ++c) { yo[c] = nyo[c]; dO[c] = ndO[c]; }
-        if (ui + 4 < n) fetch(ui + 4);
-        float p0 = 0.f, p1 = 0.f, q = 0.f;
-        for (int c = 0; c < CPE; ++c) {
-            dO[c] *= T.gamma;
-            m0[c] = msg_act<ELU>(yo[c]);
-            m1[c] = msg_act<ELU>(yo[c] + u0c[c]);
-            p0 = fmaf(a[c], m0[c], p0);
-            p1 = fmaf(a[c], m1[c], p1);
-            q = fmaf(P.att_dst[F + c0 + c], yo[c] - cpc[c], q);
-        }
-        p0 = row_sum<HL>(p0); p1 = row_sum<HL>(p1); q = row_sum<HL>(q);
-        const int32_t beg = rps[ui], end = rps[ui + 1];
-        for (int32_t e0 = beg; e0 < end; e0 += 4) {
-            const int32_t e = e0 + grp;
-            const bool ok = e < end;
-            const int eb = ent[(ok ? e : end - 1) - ebase];
-            const int v = eb & 0x7f, x = eb >> 7;
-            const float *mv = md + (v * 2 + x) * FS + c0, *dv = dod + v * FS + c0;
-            float d1 = 0.f, d2 = 0.f;
-            for (int c = 0; c < CPE; ++c) {
-                d1 = fmaf(dO[c], mv[c], d1);
-                d2 = fmaf(dv[c], x ? m1[c] : m0[c], d2);
+    // link and placement-bit masks of the tile's ops over the topology's devices
+    if (threadIdx.x < kOpTile) {
+        uint64_t pr = 0ull, bt = 0ull;
+        if ((int)threadIdx.x < n)
+            for (int32_t e = rps[threadIdx.x]; e < rps[threadIdx.x + 1]; ++e) {
+                const int eb = ent[e - rps[0]];
+                pr |= 1ull << (eb & 0x7f);
+                if (eb >> 7) bt |= 1ull << (eb & 0x7f);
             }
-            d1 = row_sum<HL>(d1);
-            d2 = row_sum<HL>(d2);
-            if (ok && (jl % HL) == 0) {
-                const float s1 = leaky(pd[(v * 2 + x) * K + h] + q, P.slope);           // op <- device
-                const float s2 = leaky((x ? p1 : p0) + qdd[v * K + h], P.slope);   // device <- op
-                float *w = eww + ((e - beg) * K + h) * 2;
-                w[0] = s1;
-                w[1] = d1;
+        pres[threadIdx.x] = pr;
+        bits[threadIdx.x] = bt;
+    }
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, lr = lane & 15, lg = lane >> 4;
+    const int ua = 16 * wv + lr;                       // op this lane supplies (A rows)
+    const bool aok = ua < n;
+    const int64_t rowa = (int64_t)rep * T.n_op + u0 + (aok ? ua : 0);
+    const float *ya = T.Y_op + rowa * 2 * F + F, *da = T.dO_op + rowa * F;
+    const bool vok = lr < nd;                          // device of this lane's column (B, results)
+    const int64_t sbase = (int64_t)rep * T.n_slots;
+    for (int h = 0; h < K; ++h) {
+        f4 d1[2] = {f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}};
+        f4 d2[2] = {f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}};
+        float qp = 0.f, p0p = 0.f, p1p = 0.f;          // this lane's parts of the op's head terms
+#pragma unroll
+        for (int ks = 0; ks < D / 4; ++ks) {
+            const int c = h * D + 4 * ks + lg;
+            const float y = aok ? ya[c] : 0.f;
+            const float gd = aok ? T.gamma * da[c] : 0.f;
+            const float m0 = aok ? msg_act<ELU>(y) : 0.f;
+            const float m1 = aok ? msg_act<ELU>(y + P.U[((int64_t)F + c) * 2 + 0]) : 0.f;
+            const float as = P.att_src[F + c];
+            qp = fmaf(P.att_dst[F + c], y - P.cp[F + c], qp);
+            p0p = fmaf(as, m0, p0p);
+            p1p = fmaf(as, m1, p1p);
+            const float bm0 = vok ? md[(lr * 2 + 0) * FS + c] : 0.f, bm1 = vok ? md[(lr * 2 + 1) * FS + c] : 0.f;
+            const float bd = vok ? dod[lr * FS + c] : 0.f;
+            d1[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(gd, bm0, d1[0], 0, 0, 0);
+            d1[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(gd, bm1, d1[1], 0, 0, 0);
+            d2[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(m0, bd, d2[0], 0, 0, 0);
+            d2[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(m1, bd, d2[1], 0, 0, 0);
+        }
+        // the op's head terms: sums over the four channel slices (lane groups)
+        qp += __shfl_xor(qp, 16, 64); qp += __shfl_xor(qp, 32, 64);
+        p0p += __shfl_xor(p0p, 16, 64); p0p += __shfl_xor(p0p, 32, 64);
+        p1p += __shfl_xor(p1p, 16, 64); p1p += __shfl_xor(p1p, 32, 64);
+        float dmx = -INFINITY, dden = 0.f, dnum = 0.f;   // device<-op record of this lane's device
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int u = 16 * wv + 4 * lg + r;          // the op of result register r
+            const int src = 4 * lg + r;                  // a lane supplying op u
+            const float qu = __shfl(qp, src, 64), p0u = __shfl(p0p, src, 64), p1u = __shfl(p1p, src, 64);
+            const uint64_t pr = u < n ? pres[u] : 0ull, bt = u < n ? bits[u] : 0ull;
+            const bool ok = vok && ((pr >> lr) & 1ull);
+            const int x = (int)((bt >> lr) & 1ull);
+            const float dd1 = x ? d1[1][r] : d1[0][r], dd2 = x ? d2[1][r] : d2[0][r];
+            const float s1 = ok ? leaky(pd[(lr * 2 + x) * K + h] + qu, P.slope) : -INFINITY;   // op <- device
+            const float s2 = leaky((x ? p1u : p0u) + (vok ? qdd[lr * K + h] : 0.f), P.slope);   // device <- op
+            const int32_t e = ok ? rps[u] + __popcll(pr & ((1ull << lr) - 1ull)) : 0;
+            if (ok) {
                 const int64_t idx = (sbase + e) * K + h;
                 T.SA2[idx] = s2;
-                T.SD2[idx] = d2;
-                float *st = dsw + (v * K + h) * 3;   // the four groups hold distinct devices
-                float mx = st[0], den = st[1], num = st[2];
-                softmax_fold(s2, d2, mx, den, num);
-                st[0] = mx; st[1] = den; st[2] = num;
+                T.SD2[idx] = dd2;
+                softmax_fold(s2, dd2, dmx, dden, dnum);
+            }
+            // softmax of op u's row over its devices (the lane group)
+            const float mx = row_max16(s1);
+            const float ex = ok ? __expf(s1 - mx) : 0.f;
+            const float den = row_sum<16>(ex), num = row_sum<16>(ex * dd1);
+            const float inv = den > 0.f ? 1.f / den : 0.f, cc = num * inv;
+            const float al = ex * inv;
+            const float dz = ok ? al * (dd1 - cc) * (s1 > 0.f ? 1.f : P.slope) : 0.f;
+            if (ok) {
+                const int64_t idx = (sbase + e) * K + h;
+                T.SA1[idx] = al;
+                T.SD1[idx] = dz;
+            }
+            const float zs = row_sum<16>(dz);
+            if (lr == 0 && u < n) {
+                zop[u][h] = zs;
+                T.Zop[(((int64_t)rep * T.n_op + u0 + u) * 2 + 1) * K + h] = zs;
             }
         }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        // softmax of the op's row (op <- device), lanes over (entry, head)
-        const int32_t deg = end - beg;
-        float mx = -INFINITY, den = 0.f, num = 0.f;
-        for (int32_t j = ej; j < deg; j += EPS) softmax_fold(eww[(j * K + kq) * 2], eww[(j * K + kq) * 2 + 1], mx, den, num);
-        for (int o = K; o < 64; o <<= 1) {
-            const float m2 = __shfl_xor(mx, o, 64), d2 = __shfl_xor(den, o, 64), n2 = __shfl_xor(num, o, 64);
-            softmax_merge(m2, d2, n2, mx, den, num);
+        // this wavefront's record of device lr: its lane groups in order
+        for (int o = 16; o < 64; o <<= 1) {
+            const float m2 = __shfl_xor(dmx, o, 64), d2v = __shfl_xor(dden, o, 64), n2 = __shfl_xor(dnum, o, 64);
+            softmax_merge(m2, d2v, n2, dmx, dden, dnum);
         }
-        const float inv = den > 0.f ? 1.f / den : 0.f, cc = num * inv;
-        float zs = 0.f;
-        for (int32_t j = ej; j < deg; j += EPS) {
-            const float sv = eww[(j * K + kq) * 2], dv = eww[(j * K + kq) * 2 + 1];
-            const float al = __expf(sv - mx) * inv;
-            const float dz = al * (dv - cc) * (sv > 0.f ? 1.f : P.slope);
-            const int64_t idx = (sbase + beg + j) * K + kq;
-            T.SA1[idx] = al;
-            T.SD1[idx] = dz;
-            zs += dz;
+        if (lg == 0) {
+            float *st = dst + ((wv * 16 + lr) * K + h) * 3;
+            st[0] = dmx; st[1] = dden; st[2] = dnum;
         }
-        for (int o = K; o < 64; o <<= 1) zs += __shfl_xor(zs, o, 64);
-        if (ej == 0) T.Zop[(row * 2 + 1) * K + kq] = zs;
-        const float zh = __shfl(zs, h, 64);   // lane h < K holds head h
-        if (grp == 0)
-            for (int c = 0; c < CPE; ++c) acc[c] = fmaf(zh, yo[c] - cpc[c], acc[c]);
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
-    if (grp == 0)
-        for (int c = 0; c < CPE; ++c) red[wv][c0 + c] = acc[c];
+    // d adst of the op rows: sum over the wavefront's ops of Z_u (Y_u - c'), lanes over channels
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    {
+        float acc[CPL];
+        for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
+        const int cc0 = lane * CPL, hh = cc0 / D;
+        for (int uu = 0; uu < 16; ++uu) {
+            const int u = 16 * wv + uu;
+            if (u >= n) break;
+            float y[CPL];
+            load_ch<CPL, false>(T.Y_op, ((int64_t)rep * T.n_op + u0 + u) * 2 * F + F + cc0, y);
+            const float z = zop[u][hh];
+            for (int c = 0; c < CPL; ++c) acc[c] = fmaf(z, y[c] - P.cp[F + cc0 + c], acc[c]);
+        }
+        for (int c = 0; c < CPL; ++c) red[wv][cc0 + c] = acc[c];
+    }
     __syncthreads();
     // the tile's sums of d adst (op rows) and device<-op records, wavefronts in order
     const int64_t tb = (int64_t)rep * T.n_tiles + t;
@@ -1145,7 +1180,7 @@ __global__ void __launch_bounds__(256) bwd_od_scores(BwdLayer P, OdTile T) {
     for (int i = threadIdx.x; i < nd * K; i += blockDim.x) {
         float mx = dst[3 * i], den = dst[3 * i + 1], num = dst[3 * i + 2];
         for (int w = 1; w < 4; ++w) {
-            const float *o = dst + ((size_t)w * MD * K + i) * 3;
+            const float *o = dst + ((size_t)w * 16 * K + i) * 3;
             softmax_merge(o[0], o[1], o[2], mx, den, num);
         }
         float *r = T.drec + ((tb * MD) * K + i) * 3;
@@ -1938,7 +1973,8 @@ int64_t n_slots(const tag_graph *g, int b) {
 // the op-device tile path needs the topology's device rows in LDS
 // dynamic LDS bytes of the tile kernels: float rows, then one byte per tile entry
 size_t od_scores_lds(int F, int K, int max_dev) {
-    return sizeof(float) * ((size_t)3 * max_dev * (F + 4) + (size_t)23 * max_dev * K) + (size_t)kOpTile * max_dev;
+    return sizeof(float) * ((size_t)3 * max_dev * (F + 4) + (size_t)3 * max_dev * K + (size_t)4 * 16 * K * 3) +
+           (size_t)kOpTile * max_dev;
 }
 size_t od_messages_lds(int F, int K, int max_dev) {
     const size_t mdp = (size_t)(max_dev + 15) / 16 * 16;
@@ -1951,7 +1987,7 @@ size_t od_messages_lds(int F, int K, int max_dev) {
 bool od_tiles_fit(const tag_graph *g, int F, int K) {
     // dynamic rows + the static reduction rows and row pointers of the messages kernel
     const size_t stat = sizeof(float) * 7 * F + sizeof(int32_t) * (kOpTile + 1);   // reduction rows, row pointers
-    return g->n_tiles > 0 && g->max_dev <= 64 && K <= 16 && F / K >= 16 &&
+    return g->n_tiles > 0 && g->max_dev <= 16 && K <= 16 && F / K >= 16 &&
            od_messages_lds(F, K, g->max_dev) + stat <= 64 * 1024 &&
            od_scores_lds(F, K, g->max_dev) + stat <= 64 * 1024;
 }
