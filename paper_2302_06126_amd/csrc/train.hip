@@ -1044,12 +1044,14 @@ __device__ __forceinline__ float row_max16(float v) {
 template <int F, int K, bool ELU>
 __global__ void __launch_bounds__(256) bwd_od_scores(BwdLayer P, OdTile T) {
     constexpr int D = F / K, FS = od_stride<F>(), CPL = F / 64;
+    constexpr int HG = K >= 2 ? 2 : 1;   // heads per pass over the channels (register budget)
     static_assert(K <= 16 && D >= 16, "the op-device tile path needs heads of at least 16 channels");
     extern __shared__ float sh[];
     __shared__ int32_t rps[kOpTile + 1];
     __shared__ uint64_t pres[kOpTile], bits[kOpTile];
     __shared__ float zop[kOpTile][K];   // Z of the tile's op rows (op <- device)
     __shared__ float red[4][F];
+    __shared__ float cst[4][F];         // U (bit column), a, a~, c' of the relation
     const int32_t t = blockIdx.x, rep = blockIdx.y;
     const int32_t u0 = T.tiles[3 * t], n = T.tiles[3 * t + 1], g = T.tiles[3 * t + 2];
     const int32_t d0 = T.dev_off[g], nd = T.dev_off[g + 1] - d0;
@@ -1060,6 +1062,12 @@ __global__ void __launch_bounds__(256) bwd_od_scores(BwdLayer P, OdTile T) {
     for (int i = threadIdx.x; i < 4 * 16 * K; i += blockDim.x) {
         dst[3 * i] = -INFINITY;
         dst[3 * i + 1] = dst[3 * i + 2] = 0.f;
+    }
+    for (int i = threadIdx.x; i < F; i += blockDim.x) {
+        cst[0][i] = P.U[((int64_t)F + i) * 2 + 0];
+        cst[1][i] = P.att_src[F + i];
+        cst[2][i] = P.att_dst[F + i];
+        cst[3][i] = P.cp[F + i];
     }
     od_stage<F, K, ELU, true>(P, T, rep, u0, n, d0, nd, md, dod, pd, qdd, rps, ent);
     // link and placement-bit masks of the tile's ops over the topology's devices
@@ -1082,29 +1090,39 @@ __global__ void __launch_bounds__(256) bwd_od_scores(BwdLayer P, OdTile T) {
     const float *ya = T.Y_op + rowa * 2 * F + F, *da = T.dO_op + rowa * F;
     const bool vok = lr < nd;                          // device of this lane's column (B, results)
     const int64_t sbase = (int64_t)rep * T.n_slots;
-    for (int h = 0; h < K; ++h) {
-        f4 d1[2] = {f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}};
-        f4 d2[2] = {f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}};
-        float qp = 0.f, p0p = 0.f, p1p = 0.f;          // this lane's parts of the op's head terms
+    for (int hg = 0; hg < K; hg += HG) {
+        f4 d1[HG][2], d2[HG][2];
+        float qv[HG], p0v[HG], p1v[HG];                // this lane's parts of the op's head terms
 #pragma unroll
-        for (int ks = 0; ks < D / 4; ++ks) {
-            const int c = h * D + 4 * ks + lg;
+        for (int j = 0; j < HG; ++j) {
+            d1[j][0] = d1[j][1] = d2[j][0] = d2[j][1] = f4{0.f, 0.f, 0.f, 0.f};
+            qv[j] = p0v[j] = p1v[j] = 0.f;
+        }
+        // one pass over the channels of heads hg .. hg + HG - 1
+#pragma unroll
+        for (int kk = 0; kk < HG * D / 4; ++kk) {
+            const int j = kk / (D / 4);
+            const int c = hg * D + 4 * kk + lg;
             const float y = aok ? ya[c] : 0.f;
             const float gd = aok ? T.gamma * da[c] : 0.f;
             const float m0 = aok ? msg_act<ELU>(y) : 0.f;
-            const float m1 = aok ? msg_act<ELU>(y + P.U[((int64_t)F + c) * 2 + 0]) : 0.f;
-            const float as = P.att_src[F + c];
-            qp = fmaf(P.att_dst[F + c], y - P.cp[F + c], qp);
-            p0p = fmaf(as, m0, p0p);
-            p1p = fmaf(as, m1, p1p);
+            const float m1 = aok ? msg_act<ELU>(y + cst[0][c]) : 0.f;
+            const float as = cst[1][c];
+            qv[j] = fmaf(cst[2][c], y - cst[3][c], qv[j]);
+            p0v[j] = fmaf(as, m0, p0v[j]);
+            p1v[j] = fmaf(as, m1, p1v[j]);
             const float bm0 = vok ? md[(lr * 2 + 0) * FS + c] : 0.f, bm1 = vok ? md[(lr * 2 + 1) * FS + c] : 0.f;
             const float bd = vok ? dod[lr * FS + c] : 0.f;
-            d1[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(gd, bm0, d1[0], 0, 0, 0);
-            d1[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(gd, bm1, d1[1], 0, 0, 0);
-            d2[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(m0, bd, d2[0], 0, 0, 0);
-            d2[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(m1, bd, d2[1], 0, 0, 0);
+            d1[j][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(gd, bm0, d1[j][0], 0, 0, 0);
+            d1[j][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(gd, bm1, d1[j][1], 0, 0, 0);
+            d2[j][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(m0, bd, d2[j][0], 0, 0, 0);
+            d2[j][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(m1, bd, d2[j][1], 0, 0, 0);
         }
+#pragma unroll
+        for (int j = 0; j < HG; ++j) {
+        const int h = hg + j;
         // the op's head terms: sums over the four channel slices (lane groups)
+        float qp = qv[j], p0p = p0v[j], p1p = p1v[j];
         qp += __shfl_xor(qp, 16, 64); qp += __shfl_xor(qp, 32, 64);
         p0p += __shfl_xor(p0p, 16, 64); p0p += __shfl_xor(p0p, 32, 64);
         p1p += __shfl_xor(p1p, 16, 64); p1p += __shfl_xor(p1p, 32, 64);
@@ -1117,7 +1135,7 @@ __global__ void __launch_bounds__(256) bwd_od_scores(BwdLayer P, OdTile T) {
             const uint64_t pr = u < n ? pres[u] : 0ull, bt = u < n ? bits[u] : 0ull;
             const bool ok = vok && ((pr >> lr) & 1ull);
             const int x = (int)((bt >> lr) & 1ull);
-            const float dd1 = x ? d1[1][r] : d1[0][r], dd2 = x ? d2[1][r] : d2[0][r];
+            const float dd1 = x ? d1[j][1][r] : d1[j][0][r], dd2 = x ? d2[j][1][r] : d2[j][0][r];
             const float s1 = ok ? leaky(pd[(lr * 2 + x) * K + h] + qu, P.slope) : -INFINITY;   // op <- device
             const float s2 = leaky((x ? p1u : p0u) + (vok ? qdd[lr * K + h] : 0.f), P.slope);   // device <- op
             const int32_t e = ok ? rps[u] + __popcll(pr & ((1ull << lr) - 1ull)) : 0;
@@ -1154,6 +1172,7 @@ __global__ void __launch_bounds__(256) bwd_od_scores(BwdLayer P, OdTile T) {
             float *st = dst + ((wv * 16 + lr) * K + h) * 3;
             st[0] = dmx; st[1] = dden; st[2] = dnum;
         }
+        }
     }
     // d adst of the op rows: sum over the wavefront's ops of Z_u (Y_u - c'), lanes over channels
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -1169,7 +1188,7 @@ __global__ void __launch_bounds__(256) bwd_od_scores(BwdLayer P, OdTile T) {
             float y[CPL];
             load_ch<CPL, false>(T.Y_op, ((int64_t)rep * T.n_op + u0 + u) * 2 * F + F + cc0, y);
             const float z = zop[u][hh];
-            for (int c = 0; c < CPL; ++c) acc[c] = fmaf(z, y[c] - P.cp[F + cc0 + c], acc[c]);
+            for (int c = 0; c < CPL; ++c) acc[c] = fmaf(z, y[c] - cst[3][cc0 + c], acc[c]);
         }
         for (int c = 0; c < CPL; ++c) red[wv][cc0 + c] = acc[c];
     }
