@@ -1591,17 +1591,20 @@ __global__ void fold_bwd_we(FoldBwd a) {
 // Block (relation, 64 k); thread (k, o group of 4) sums its o over the
 // layers, then the groups are added in order.
 __global__ void __launch_bounds__(256) fold_bwd_enc(FoldBwd a) {
-    __shared__ float red[3][4][64];
+    // block (relation r, 16 encoder outputs k); thread (k, output group of 16):
+    // sums its outputs o of every layer, then the 16 groups are added in order
+    __shared__ float red[3][16][17];
     const int F = a.F;
-    const int kb = (F + 63) / 64;
-    const int r = blockIdx.x / kb, k = (blockIdx.x % kb) * 64 + (threadIdx.x & 63), grp = threadIdx.x >> 6;
+    const int kb = (F + 15) / 16;
+    const int r = blockIdx.x / kb, kk = threadIdx.x & 15, grp = threadIdx.x >> 4;
+    const int k = (blockIdx.x % kb) * 16 + kk;
     const int d = r == 2 ? 2 : 1;
     float s0 = 0.f, s1 = 0.f, sc = 0.f;
     if (k < F) {
         for (int l = 0; l < a.L; ++l) {
             const int64_t lr = (int64_t)l * 3 + r;
-#pragma unroll 8
-            for (int o = grp; o < F; o += 4) {
+#pragma unroll 4
+            for (int o = grp; o < F; o += 16) {
                 const float we = a.layer_w[(lr * F + o) * 2 * F + F + k];
                 s0 = fmaf(we, a.dU[(lr * F + o) * 2 + 0], s0);
                 s1 = fmaf(we, a.dU[(lr * F + o) * 2 + 1], s1);
@@ -1609,14 +1612,13 @@ __global__ void __launch_bounds__(256) fold_bwd_enc(FoldBwd a) {
             }
         }
     }
-    const int kk = threadIdx.x & 63;
     red[0][grp][kk] = s0;
     red[1][grp][kk] = s1;
     red[2][grp][kk] = sc;
     __syncthreads();
     if (grp != 0 || k >= F) return;
     float t0 = 0.f, t1 = 0.f, tc = 0.f;
-    for (int g = 0; g < 4; ++g) { t0 += red[0][g][kk]; t1 += red[1][g][kk]; tc += red[2][g][kk]; }
+    for (int gq = 0; gq < 16; ++gq) { t0 += red[0][gq][kk]; t1 += red[1][gq][kk]; tc += red[2][gq][kk]; }
     a.g_A[r][(int64_t)k * d + 0] = t0;
     if (d == 2) a.g_A[r][(int64_t)k * d + 1] = t1;
     a.g_c[r][k] = tc;
@@ -2435,7 +2437,7 @@ extern "C" tag_status tag_train_step(const tag_graph *g, const tag_model_dims *d
                {gr->enc_edge_w[0], gr->enc_edge_w[1], gr->enc_edge_w[2]},
                {gr->enc_edge_b[0], gr->enc_edge_b[1], gr->enc_edge_b[2]}, F, NL};
     fold_bwd_we<<<grid_for((int64_t)NL * 3 * F * F), 256, 0, stream>>>(fb);
-    fold_bwd_enc<<<3 * ((F + 63) / 64), 256, 0, stream>>>(fb);
+    fold_bwd_enc<<<3 * ((F + 15) / 16), 256, 0, stream>>>(fb);
 
     if (lr > 0.f) {
         SgdList sl{};
