@@ -585,7 +585,7 @@ def main() -> int:
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        sys.exit("bench.py measures one GPU only: this build has no multi-GPU path "
+        sys.exit("bench.py measures one GPU only: the library has no multi-GPU path "
                  "(candidates would shard across GPUs with no per-layer exchange); run with --gpus 1")
 
     if args.mode == "search":
