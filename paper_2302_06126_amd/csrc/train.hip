@@ -2007,10 +2007,13 @@ size_t od_messages_lds(int F, int K, int max_dev) {
 // entry group and inside a 16-channel column block of the device-side products)
 bool od_tiles_fit(const tag_graph *g, int F, int K) {
     // dynamic rows + the static reduction rows and row pointers of the messages kernel
-    const size_t stat = sizeof(float) * 7 * F + sizeof(int32_t) * (kOpTile + 1);   // reduction rows, row pointers
+    // static LDS of the two kernels: row pointers, reduction and constant rows, op masks and Z
+    const size_t rp = sizeof(int32_t) * (kOpTile + 1);
+    const size_t stat_m = sizeof(float) * 7 * F + rp;
+    const size_t stat_s = sizeof(float) * (8 * F + (size_t)kOpTile * K) + 2 * sizeof(uint64_t) * kOpTile + rp;
     return g->n_tiles > 0 && g->max_dev <= 16 && K <= 16 && F / K >= 16 &&
-           od_messages_lds(F, K, g->max_dev) + stat <= 64 * 1024 &&
-           od_scores_lds(F, K, g->max_dev) + stat <= 64 * 1024;
+           od_messages_lds(F, K, g->max_dev) + stat_m <= 64 * 1024 &&
+           od_scores_lds(F, K, g->max_dev) + stat_s <= 64 * 1024;
 }
 
 int32_t persist_blocks(int64_t items) {
