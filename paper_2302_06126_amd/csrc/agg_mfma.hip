@@ -22,33 +22,46 @@ namespace tag {
 namespace {
 
 // omask[r][u] = (present, bits) over the local devices of u's topology.
-// One block per (op tile, candidate): the tile's op<-dev entries are one
-// contiguous CSR range, read coalesced and OR-ed into LDS masks.
+// One block per (op tile, kMaskCands candidates): the tile's op<-dev CSR range
+// is read once for the group; four lanes per op row walk its entries and OR
+// device bits in registers, and the four partial masks meet by shuffles.
+constexpr int kMaskCands = 4;
+static_assert(kMaskCands == 4 && kOpTile * 4 == 256, "one lane per quarter row and per stored candidate");
+
 __global__ void __launch_bounds__(256) pack_op_masks(AggArgs A) {
-    __shared__ int32_t rp[kOpTile + 1];
-    __shared__ unsigned long long pres[kOpTile], bits[kOpTile];
-    const int32_t t = blockIdx.x, r = blockIdx.y;
+    typedef unsigned long long u64;
+    const int32_t t = blockIdx.x, r0 = blockIdx.y * kMaskCands;
     const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1], g = A.tiles[3 * t + 2];
     const int32_t d0 = A.dev_off[g];
-    for (int i = threadIdx.x; i <= nu; i += blockDim.x) rp[i] = A.rp[1][u0 + i];
-    for (int i = threadIdx.x; i < kOpTile; i += blockDim.x) { pres[i] = 0ull; bits[i] = 0ull; }
-    __syncthreads();
-    const uint8_t *xb = A.x_od + (int64_t)r * A.s_od;
-    for (int32_t e = rp[0] + threadIdx.x; e < rp[nu]; e += blockDim.x) {
-        int lo = 0, hi = nu;   // last local row with rp[row] <= e
-        while (hi - lo > 1) {
-            const int mid = (lo + hi) >> 1;
-            if (rp[mid] <= e) lo = mid; else hi = mid;
+    const int i = threadIdx.x >> 2, q = threadIdx.x & 3;   // op row of the tile, quarter
+    u64 pres = 0ull, bits[kMaskCands];
+#pragma unroll
+    for (int k = 0; k < kMaskCands; ++k) bits[k] = 0ull;
+    if (i < nu) {
+        const int32_t e1 = A.rp[1][u0 + i + 1];
+        for (int32_t e = A.rp[1][u0 + i] + q; e < e1; e += 4) {
+            const u64 m = 1ull << (A.col[1][e] - d0);
+            const int64_t id = A.eid[1][e];
+            pres |= m;
+#pragma unroll
+            for (int k = 0; k < kMaskCands; ++k)
+                if (r0 + k < A.R && A.x_od[(int64_t)(r0 + k) * A.s_od + id]) bits[k] |= m;
         }
-        const unsigned long long m = 1ull << (A.col[1][e] - d0);
-        atomicOr(&pres[lo], m);
-        if (xb[A.eid[1][e]]) atomicOr(&bits[lo], m);
     }
-    __syncthreads();
-    for (int i = threadIdx.x; i < nu; i += blockDim.x) {
-        const int64_t mi = 2 * ((int64_t)r * A.n_op + u0 + i);
-        A.omask[mi] = pres[i];
-        A.omask[mi + 1] = bits[i];
+    // lanes 4i .. 4i + 3 of one wavefront hold the quarters of row i
+#pragma unroll
+    for (int o = 1; o < 4; o <<= 1) {
+        pres |= __shfl_xor(pres, o);
+#pragma unroll
+        for (int k = 0; k < kMaskCands; ++k) bits[k] |= __shfl_xor(bits[k], o);
+    }
+    if (i < nu && r0 + q < A.R) {   // lane q stores candidate r0 + q
+        u64 b = bits[0];
+#pragma unroll
+        for (int k = 1; k < kMaskCands; ++k) b = q == k ? bits[k] : b;
+        const int64_t mi = 2 * ((int64_t)(r0 + q) * A.n_op + u0 + i);
+        A.omask[mi] = pres;
+        A.omask[mi + 1] = b;
     }
 }
 
@@ -782,7 +795,7 @@ bool dispatch_mfma_heads(int K, const AggArgs &A, hipStream_t st) {
 bool mfma_path_supported(int F, int K) { return K >= 1 && F / K >= 16 && K <= 16; }
 
 void launch_pack_masks(const AggArgs &A, hipStream_t st) {
-    pack_op_masks<<<dim3((unsigned)A.n_tiles, (unsigned)A.R), 256, 0, st>>>(A);
+    pack_op_masks<<<dim3((unsigned)A.n_tiles, (unsigned)((A.R + kMaskCands - 1) / kMaskCands)), 256, 0, st>>>(A);
 }
 
 bool launch_agg_mfma(int F, int K, bool bf, const AggArgs &A, hipStream_t st) {
