@@ -185,6 +185,9 @@ __global__ void __launch_bounds__(kThreads) scan_buckets(Buckets B) {
             v[k] = (i0 + k < n) ? B.cnt[b][i0 + k] : 0;
             s += v[k];
         }
+        // the counters restart at zero for the placement pass
+        for (int k = 0; k < kScanItems; ++k)
+            if (i0 + k < n) B.cnt[b][i0 + k] = 0;
         int32_t tot;
         int32_t ex = block_exclusive_scan(s, &tot, sh) + carry;
         for (int k = 0; k < kScanItems; ++k) {
@@ -635,11 +638,11 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
     fill_i32<<<grid_for(tl.cnt_ints + FLAG_COUNT), kThreads, 0, stream>>>(tl.cnt_all, tl.cnt_ints + FLAG_COUNT, 0);
     if (ea.blk_off[3] > 0) edges_pass<0><<<(unsigned)ea.blk_off[3], kThreads, 0, stream>>>(ea);
     if (std::max(s.rows[0], s.rows[2]) + 1 <= kSmallScan) {
-        scan_buckets<<<4, kThreads, 0, stream>>>(B);
+        scan_buckets<<<4, kThreads, 0, stream>>>(B);   // also zeroes the counters
     } else {
         for (int b = 0; b < 4; ++b) enqueue_scan(tl.cnt[b], s.rows[b], cl.rowptr[b], tl.tile_sums, stream);
+        fill_i32<<<grid_for(tl.cnt_ints), kThreads, 0, stream>>>(tl.cnt_all, tl.cnt_ints, 0);
     }
-    fill_i32<<<grid_for(tl.cnt_ints), kThreads, 0, stream>>>(tl.cnt_all, tl.cnt_ints, 0);
     if (ea.blk_off[3] > 0) edges_pass<1><<<(unsigned)ea.blk_off[3], kThreads, 0, stream>>>(ea);
     if (nnz_all > 0) {
         const int64_t r1 = s.rows[0], r2 = r1 + s.rows[1], r3 = r2 + s.rows[2], rtot = r3 + s.rows[3];
