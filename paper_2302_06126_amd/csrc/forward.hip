@@ -189,9 +189,10 @@ __global__ void __launch_bounds__(256) agg_dev_final(AggArgs A) {
     const int head = lane / LPH;
     float out[CPL];
     for (int c = 0; c < CPL; ++c) out[c] = 0.f;
-    {   // B2 merge in record order (records with a zero sum hold no links);
-        // records are read four at a time so their loads overlap
-        constexpr int RB = 4;
+    {   // B2 merge in record order (records with a zero sum hold no links),
+        // one online pass: records are read sixteen at a time so their loads
+        // overlap, and the running sums are rescaled to each batch's maximum
+        constexpr int RB = 16;
         const int32_t deg = A.rp[2][j + 1] - A.rp[2][j];
         int32_t nch = (deg + kChunk - 1) / kChunk;
         if (A.rec_mode) {
@@ -205,15 +206,7 @@ __global__ void __launch_bounds__(256) agg_dev_final(AggArgs A) {
         if (deg > 0 && nch > 0) {
             constexpr int REC = F + 2 * K;
             const float *p0 = A.part + ((int64_t)rep * A.n_dev + j) * A.maxc * REC;
-            float M = -INFINITY;
-            for (int32_t c = 0; c < nch; c += RB) {
-                float mv[RB];
-#pragma unroll
-                for (int i = 0; i < RB; ++i) mv[i] = c + i < nch ? p0[(int64_t)(c + i) * REC + head] : -INFINITY;
-#pragma unroll
-                for (int i = 0; i < RB; ++i) M = fmaxf(M, mv[i]);
-            }
-            float den = 0.f, acc[CPL];
+            float M = -INFINITY, den = 0.f, acc[CPL];
             for (int cc = 0; cc < CPL; ++cc) acc[cc] = 0.f;
             for (int32_t c = 0; c < nch; c += RB) {
                 float mv[RB], dv[RB], av[RB][CPL];
@@ -230,19 +223,27 @@ __global__ void __launch_bounds__(256) agg_dev_final(AggArgs A) {
                         for (int cc = 0; cc < CPL; ++cc) av[i][cc] = 0.f;
                     }
                 }
+                float Mb = M;
+#pragma unroll
+                for (int i = 0; i < RB; ++i) Mb = fmaxf(Mb, mv[i]);
+                // records without links (maximum -inf) weigh nothing
+                const float r = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(M - Mb);
+                den *= r;
+                for (int cc = 0; cc < CPL; ++cc) acc[cc] *= r;
 #pragma unroll
                 for (int i = 0; i < RB; ++i) {
-                    const float sc = c + i < nch ? __builtin_amdgcn_exp2f(mv[i] - M) : 0.f;
+                    const float sc = mv[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mv[i] - Mb);
                     den = fmaf(dv[i], sc, den);
                     for (int cc = 0; cc < CPL; ++cc) acc[cc] = fmaf(av[i][cc], sc, acc[cc]);
                 }
+                M = Mb;
             }
             float inv = A.g_cross / den;
             for (int cc = 0; cc < CPL; ++cc) out[cc] = acc[cc] * inv;
         }
     }
     {   // B3: dev <- dev, relation dd, EB entries per step
-        constexpr int EB = 4;
+        constexpr int EB = 16;
         RelConst<CPL> k; k.load(A, 2, F, c0);
         float yd[CPL]; load_ch<CPL, BF>(A.Y_dev, ((int64_t)rep * A.n_dev + j) * 2 * F + c0, yd);
         float q = 0.f;
