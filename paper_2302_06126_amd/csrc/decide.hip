@@ -112,13 +112,15 @@ __device__ __forceinline__ float slice_score(const DecArgs &A, const float *urg,
     return A.b2[0] + s;
 }
 
-// one block per query: scores, softmax prior, argmax, decoded decision
+// one block per query: scores, softmax prior, argmax, decoded decision.
+// Consecutive queries (usually one candidate's, reading the same u) run on
+// one XCD, so each candidate's u is fetched into one L2 rather than all eight.
 __global__ void __launch_bounds__(kScoreThreads) dec_score(DecArgs A) {
     extern __shared__ float sh[];   // v[Hx] | w2[H]
     __shared__ float red_m[kScoreThreads];
     __shared__ int32_t red_i[kScoreThreads];
     __shared__ float red_z[kScoreThreads];
-    const int32_t q = blockIdx.x;
+    const int32_t q = (int32_t)xcd_swizzle(blockIdx.x, gridDim.x);
     int32_t r, g, op;
     const bool ok = query_valid(A, q, &r, &g, &op);
     if (!ok) {
