@@ -240,12 +240,12 @@ __global__ void scan_add(int32_t *out, int64_t n, const int32_t *tile_sums) {
 // entries, and its rank is counted against the others through lane
 // shuffles.  Only the rp[rows] entries of a bucket were scattered (links
 // rejected during the count pass never were).
-__global__ void __launch_bounds__(256) rank_rows(Buckets B, int64_t r1, int64_t r2, int64_t r3, int64_t rtot,
-                                                 int32_t *flags) {
+__device__ void rank_rows(const Buckets &B, int64_t r1, int64_t r2, int64_t r3, int64_t rtot, int32_t *flags,
+                          int64_t blk) {
     __shared__ int32_t bmax[4];
     if (threadIdx.x < 4) bmax[threadIdx.x] = 0;
     __syncthreads();
-    const int64_t w = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
+    const int64_t w = blk * (blockDim.x / 64) + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (w < rtot) {
         const int b = w < r1 ? 0 : (w < r2 ? 1 : (w < r3 ? 2 : 3));
@@ -283,16 +283,16 @@ __global__ void __launch_bounds__(256) rank_rows(Buckets B, int64_t r1, int64_t 
 // by source id (sources are unique in a valid row; a repeated source is
 // caught by the atomic OR).  Ranges beyond the LDS bitmap (rmax source ids,
 // at most kBitmapRange) fall back to the per-entry rank inside the block.
-__global__ void __launch_bounds__(256) rank_long_rows(Buckets B, const int32_t *op_off, const int32_t *dev_off,
-                                                      int32_t G, int32_t rmax, int32_t *flags) {
+__device__ void rank_long_rows(const Buckets &B, const int32_t *op_off, const int32_t *dev_off, int32_t G,
+                               int32_t rmax, int32_t *flags, int64_t blk) {
     extern __shared__ int32_t dyn[];   // bm [rmax/32] | wpre [rmax/32] | eid_of [rmax]
     __shared__ int32_t scan[256];
     const int nwmax = (rmax + 31) / 32;
     uint32_t *bm = reinterpret_cast<uint32_t *>(dyn);
     int32_t *wpre = dyn + nwmax;
     int32_t *eid_of = dyn + 2 * nwmax;
-    const int b = blockIdx.x < B.rows[0] ? 0 : 2;
-    const int32_t r = b == 0 ? (int32_t)blockIdx.x : (int32_t)(blockIdx.x - B.rows[0]);
+    const int b = blk < B.rows[0] ? 0 : 2;
+    const int32_t r = b == 0 ? (int32_t)blk : (int32_t)(blk - B.rows[0]);
     const int32_t *rp = B.rp[b];
     const int32_t *tcol = B.tcol[b], *teid = B.teid[b];
     int32_t *col = B.col[b], *eid = B.eid[b];
@@ -359,6 +359,15 @@ __global__ void __launch_bounds__(256) rank_long_rows(Buckets B, const int32_t *
             ++pos;
         }
     }
+}
+
+// Both ranks in one launch: blocks [0, n_short) take four short rows each,
+// the rest one B0 or B2 row each (long rows only).
+__global__ void __launch_bounds__(256) rank_all(Buckets B, int64_t r1, int64_t r2, int64_t r3, int64_t rtot,
+                                                int64_t n_short, const int32_t *op_off, const int32_t *dev_off,
+                                                int32_t G, int32_t rmax, int32_t *flags) {
+    if ((int64_t)blockIdx.x < n_short) rank_rows(B, r1, r2, r3, rtot, flags, blockIdx.x);
+    else rank_long_rows(B, op_off, dev_off, G, rmax, flags, (int64_t)blockIdx.x - n_short);
 }
 
 inline unsigned grid_for(int64_t n, int64_t cap = 65536) {
@@ -646,18 +655,16 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
     if (ea.blk_off[3] > 0) edges_pass<1><<<(unsigned)ea.blk_off[3], kThreads, 0, stream>>>(ea);
     if (nnz_all > 0) {
         const int64_t r1 = s.rows[0], r2 = r1 + s.rows[1], r3 = r2 + s.rows[2], rtot = r3 + s.rows[3];
-        rank_rows<<<(unsigned)((rtot + kThreads / 64 - 1) / (kThreads / 64)), kThreads, 0, stream>>>(
-            B, r1, r2, r3, rtot, tl.flags);
-    }
-    // op<-op and dev<-op rows can be long; valid op<-dev and dev<-dev rows have at most 64 entries
-    if (s.nnz[0] + s.nnz[2] > 0) {
+        const int64_t n_short = (rtot + kThreads / 64 - 1) / (kThreads / 64);
+        // op<-op and dev<-op rows can be long; valid op<-dev and dev<-dev rows have at most 64 entries
+        const int64_t n_long = s.nnz[0] + s.nnz[2] > 0 ? s.rows[0] + s.rows[2] : 0;
         // bitmap sized for the largest topology (sources of both buckets are ops)
         int32_t rmax = 1;
         for (int32_t gi = 0; gi < s.G; ++gi) rmax = std::max(rmax, desc->n_op[gi]);
         rmax = std::min(rmax, kBitmapRange);
         const size_t lds = sizeof(int32_t) * (2 * (size_t)((rmax + 31) / 32) + (size_t)rmax);
-        rank_long_rows<<<(unsigned)(s.rows[0] + s.rows[2]), kThreads, lds, stream>>>(B, cl.op_off, cl.dev_off, s.G,
-                                                                                      rmax, tl.flags);
+        rank_all<<<(unsigned)(n_short + n_long), kThreads, lds, stream>>>(B, r1, r2, r3, rtot, n_short, cl.op_off,
+                                                                           cl.dev_off, s.G, rmax, tl.flags);
     }
     prof_end(TAG_STAGE_GRAPH_BUILD, stream);
     {
