@@ -154,6 +154,20 @@ def test_forward_random_graphs(f, heads, layers, dtype):
     say(f"  worst row-rel err {err:.2e}")
 
 
+@pytest.mark.parametrize("f,heads,dtype", [(128, 4, "f32"), (256, 4, "bf16")])
+def test_forward_many_rows_ragged_tail(f, heads, dtype):
+    # 17 x 1001 = 17017 op rows: the node encoder takes its 64-row tiles
+    # (265 full tiles and a 57-row tail; f = 256 spans two 128-column blocks,
+    # bf16 output takes the packed 16-byte stores); first and last candidates
+    topo = synth.random_topology(11 + f, 1001, 9, 1500, od_per_op=None, dd_density=0.6)
+    R = 17
+    c = Case(topo, R, f, heads, 1, dtype=dtype, seed=5)
+    say(f"forward many rows f={f} K={heads} {dtype}: {R * topo.n_op} op rows")
+    _, _, E_op, E_dev = c.gpu_forward()
+    err = c.check(E_op, E_dev, [0, R - 1])
+    say(f"  worst row-rel err {err:.2e}")
+
+
 def test_forward_long_rows_and_sparse_placements():
     # device rows of ~1000 entries (several 256-entry chunks), 3 devices per op
     topo = synth.random_topology(5, 1500, 5, 2000, od_per_op=3, dd_density=0.5)
