@@ -40,7 +40,7 @@ struct DecArgs {
 // One block per (candidate graph rg, chunk of kSliceH hidden units): the
 // chunk of the graph's device rows t and the option columns sit in LDS; each
 // thread walks the set bits of its slices' masks in ascending device order.
-constexpr int kSliceH = 32;
+constexpr int kSliceH = 8;
 __global__ void __launch_bounds__(256) dec_slice(DecArgs A) {
     __shared__ float tl[64][kSliceH + 1];
     __shared__ float po[4][kSliceH];
