@@ -41,6 +41,29 @@ def _stream(stream=None) -> int:
     return int(s.cuda_stream)
 
 
+class _OnStream:
+    """Orders a one-shot call on `stream` against torch's current stream: the
+    given stream first waits for the current one (which allocated and filled
+    the temporaries), and on exit the current stream waits for the given one,
+    so results read and temporaries freed on the current stream come after
+    the library's kernels."""
+
+    def __init__(self, stream):
+        self.stream = stream
+
+    def __enter__(self):
+        torch = _torch()
+        self.cur = torch.cuda.current_stream()
+        if self.stream is not None and self.stream != self.cur:
+            self.stream.wait_stream(self.cur)
+        return self
+
+    def __exit__(self, *exc):
+        if self.stream is not None and self.stream != self.cur:
+            self.cur.wait_stream(self.stream)
+        return False
+
+
 # ------------------------------------------------------------ C-ABI names --
 
 def tag_last_error() -> str:
@@ -145,7 +168,8 @@ class Graph:
         check(st, "tag_graph_plan")
         self.csr = torch.empty(cb, dtype=torch.uint8, device=self.device)
         tmp = torch.empty(tb, dtype=torch.uint8, device=self.device)
-        st, h = tag_graph_build(d, _ptr(self.csr), cb, _ptr(tmp), tb, _stream(stream))
+        with _OnStream(stream):
+            st, h = tag_graph_build(d, _ptr(self.csr), cb, _ptr(tmp), tb, _stream(stream))
         check(st, "tag_graph_build")
         del tmp
         self.handle = h
@@ -255,7 +279,8 @@ class Forward:
 def forward(graph: Graph, model: Model, x_op, x_dev, x_oo, x_dd, x_od, stream=None):
     fw = Forward(graph, model, int(x_op.shape[0]))
     keep = (x_op, x_dev, x_oo, x_dd, x_od)
-    E_op, E_dev = fw(make_features(*keep), stream)
+    with _OnStream(stream):
+        E_op, E_dev = fw(make_features(*keep), stream)
     return E_op, E_dev
 
 
@@ -306,7 +331,8 @@ class Decide:
 def decide(graph: Graph, model: Model, E_op, E_dev, masks, options, q_rep, q_graph, q_op, want_prior=True,
            stream=None) -> dict:
     d = Decide(graph, model, int(E_op.shape[0]), masks, options, q_rep, q_graph, q_op, want_prior)
-    d(E_op, E_dev, stream)
+    with _OnStream(stream):
+        d(E_op, E_dev, stream)
     return d.results()
 
 
@@ -329,10 +355,12 @@ def decide_full(graph: Graph, model: Model, E_op, E_dev, q_rep, q_graph, q_op, w
     best = torch.empty(max(Q, 1), dtype=torch.float32, device=dev)
     prior = torch.empty((max(Q, 1), S_full), dtype=torch.float32, device=dev) if want_prior else None
     decision = torch.empty((max(Q, 1), C.sizeof(tag_decision)), dtype=torch.uint8, device=dev)
-    check(lib.tag_gnn_decide_full(graph.handle, C.byref(model.dims), C.byref(model.weights), R, _ptr(E_op),
-                                  _ptr(E_dev), Q, _ptr(q[0]), _ptr(q[1]), _ptr(q[2]), _ptr(argmax), _ptr(best),
-                                  _ptr(prior), _ptr(decision), _ptr(ws), b.value, _stream(stream)),
-          "tag_gnn_decide_full")
+    with _OnStream(stream):
+        check(lib.tag_gnn_decide_full(graph.handle, C.byref(model.dims), C.byref(model.weights), R, _ptr(E_op),
+                                      _ptr(E_dev), Q, _ptr(q[0]), _ptr(q[1]), _ptr(q[2]), _ptr(argmax),
+                                      _ptr(best), _ptr(prior), _ptr(decision), _ptr(ws), b.value,
+                                      _stream(stream)),
+              "tag_gnn_decide_full")
     raw = decision[:Q].cpu().numpy()
     rec = np.frombuffer(raw.tobytes(), dtype=np.dtype([("mask", "<u8"), ("option", "<i4"), ("replicas", "<i4"),
                                                       ("sync", "<i4"), ("sfb", "<i4")]))

@@ -1,6 +1,8 @@
 """GPU-side helpers for the parity tests: upload seeded inputs, call the
 library through its binding, and compare with the oracle candidate by
 candidate.  (Imported only by tests marked gpu.)"""
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 import oracle
@@ -73,11 +75,18 @@ class Case:
         return oracle.forward(self.topo, self.x_op[r], self.x_dev[r], self.x_oo[r], self.x_dd[r], self.x_od[r],
                               self.w, f=self.f, heads=self.heads, layers=self.layers, bf16=self.dtype == "bf16")
 
-    def check(self, E_op, E_dev, reps):
+    def oracle_many(self, reps):
+        """Oracle outputs of several candidates, computed in parallel threads
+        (each call is single-threaded C that releases the interpreter lock)."""
+        with ThreadPoolExecutor(max_workers=max(1, min(len(reps), 8))) as ex:
+            return dict(zip(reps, ex.map(self.oracle_forward, reps)))
+
+    def check(self, E_op, E_dev, reps, refs=None):
         tol = BF16_TOL if self.dtype == "bf16" else FP32_TOL
+        refs = refs if refs is not None else self.oracle_many(list(reps))
         worst = 0.0
         for r in reps:
-            R_op, R_dev = self.oracle_forward(r)
+            R_op, R_dev = refs[r]
             got = np.vstack([E_op[r].cpu().numpy(), E_dev[r].cpu().numpy()])
             err = row_rel_err(got, np.vstack([R_op, R_dev]))
             worst = max(worst, err)
@@ -88,7 +97,38 @@ class Case:
 
 def decide_gap_ok(prior_row, best, delta_rel):
     """True when the oracle's top-two score gap exceeds delta (a unique winner)."""
+    return top_gap(prior_row) > delta_rel * max(1.0, abs(best))
+
+
+def top_gap(prior_row):
+    """The oracle's gap between its best and second-best score (from the
+    priors: log p_a - log p_b = s_a - s_b)."""
     s = np.sort(np.log(np.maximum(prior_row, 1e-300)))[::-1]
-    if len(s) < 2:
-        return True
-    return (s[0] - s[1]) > delta_rel * max(1.0, abs(best))
+    return np.inf if len(s) < 2 else float(s[0] - s[1])
+
+
+def score_error_bound(w, f, H, E_op, E_dev, masks, query_op, n_dev, emb_err):
+    """Per query, a bound on how far any slice's decoder score can move when
+    every embedding row x moves by at most emb_err * ||x||_inf (the measured
+    row-relative error of the forward pass).  The decoder input is
+    [sum_j mask_j E_dev[j] ; E_op[i] ; onehot], the first layer is linear and
+    ReLU is 1-Lipschitz, so
+      |d score| <= sum_h |w2_h| (sum_{c<f} |W1_hc| D_a + sum_c |W1_h,f+c| ||E_op[i]||) emb_err
+    with D_a = sum_{j in mask a} ||E_dev[j]||_inf (H = 0: |w2| in place of
+    the sum over h); row norms are floored as in the error measure (1e-6 of
+    the largest).  Two scores move by at most twice the largest bound."""
+    w1 = np.abs(np.asarray(w["dec_w1"], np.float64))
+    w2 = np.abs(np.asarray(w["dec_w2"], np.float64))
+    if H > 0:
+        alpha = float(w2 @ w1[:, :f].sum(axis=1))
+        beta = float(w2 @ w1[:, f:2 * f].sum(axis=1))
+    else:
+        alpha, beta = float(w2[:f].sum()), float(w2[f:2 * f].sum())
+    dev_n = np.abs(np.asarray(E_dev, np.float64)).max(axis=1)
+    all_op = np.abs(np.asarray(E_op, np.float64)).max(axis=1)
+    floor = 1e-6 * max(float(dev_n.max(initial=0.0)), float(all_op.max(initial=0.0)))
+    dev_n = np.maximum(dev_n, floor)
+    bits = ((np.asarray(masks, np.uint64)[:, None] >> np.arange(n_dev, dtype=np.uint64)) & np.uint64(1)).astype(bool)
+    d_max = float((bits * dev_n[None, :]).sum(axis=1).max())
+    op_n = np.maximum(all_op[np.asarray(query_op)], floor)
+    return emb_err * (alpha * d_max + beta * op_n)

@@ -39,12 +39,13 @@ def random_features(topo, f_op, seed, nonneg=False):
 
 def row_rel_err(got, ref):
     """max over rows of ||got - ref||_inf / max(||ref||_inf, floor), with the
-    floor at 1e-3 of the largest row norm (rows that are all zero in the
-    reference are compared on that absolute scale)."""
+    floor at 1e-6 of the largest row norm: rows that are all zero (or nearly
+    so) in the reference are compared on that absolute scale, every other row
+    on its own norm."""
     got = np.asarray(got, np.float64).reshape(ref.shape[0], -1)
     ref = np.asarray(ref, np.float64).reshape(ref.shape[0], -1)
     if ref.size == 0:
         return 0.0
     nrm = np.abs(ref).max(axis=1)
-    floor = max(1e-3 * float(nrm.max()), 1e-30)
+    floor = max(1e-6 * float(nrm.max()), 1e-30)
     return float((np.abs(got - ref).max(axis=1) / np.maximum(nrm, floor)).max())

@@ -426,6 +426,43 @@ def test_bf16_variant_rounds_transforms(orc):
     np.testing.assert_allclose(E1, E2, rtol=0, atol=1e-15)
 
 
+def test_bf16_rounding_points_hand_worked(orc):
+    """The bf16 variant rounds exactly three quantities of the relation
+    transform (Section 4.2.1 layer equation, W^h acting on h_v): the input
+    row h, the weights W^h and the product W^h h; the edge term W^e e + b,
+    the message and the output stay unrounded.  Worked by hand with
+    u = 2^-10 (bf16 keeps 8 significant bits, so its spacing on [1, 2) is 8u
+    and on [2, 4) is 16u):
+
+      h   = (1 + 5u, 5u)          -> bf16 (1 + 8u, 5u)
+      W^h = [[1, 1], [1 + 5u, 1]] -> bf16 [[1, 1], [1 + 8u, 1]]
+      Y_0 = (1 + 8u) + 5u = 1 + 13u                 -> bf16 1 + 16u
+      Y_1 = (1 + 8u)(1 + 8u) + 5u = 1 + 21u + 64u^2 -> bf16 1 + 24u
+      te  = W^e e + b = (1 + u, 1 + u)   (W^e = 0, b = 1 + u: not a bf16 value)
+
+    Op 1 has the single op neighbour 0, so alpha = 1 and its output is the
+    message m = ReLU(Y + te) = (2 + 17u, 2 + 25u).  Dropping any one rounding
+    or adding one gives a different number:
+      no rounding of h: Y = (1 + 8u, 1 + 16u) after rounding the sums;
+      no rounding of W: Y_1 = (1 + 5u)(1 + 8u) + 5u -> 1 + 16u;
+      no rounding of Y: Y = (1 + 13u, 1 + 21u + 64u^2);
+      rounding te or m: 2 + 16u or 2 + 24u in place of 2 + 17u, 2 + 25u."""
+    u = 2.0 ** -10
+    topo = mk_topo(2, 1, oo=[(0, 1)], od=[])
+    w = zero_weights(2, 1, 2)
+    w["enc_op_w"][:] = np.eye(2)
+    w["layer_w"][0, 0, :, :2] = [[1.0, 1.0], [1.0 + 5 * u, 1.0]]
+    w["layer_b"][0, 0, :] = 1.0 + u
+    x_op = np.array([[1 + 5 * u, 5 * u], [0.0, 0.0]], np.float32)
+    args = (x_op, np.zeros((1, 8), np.float32), np.zeros(1, np.float32), np.zeros((0, 2), np.float32),
+            np.zeros(0, np.uint8), w)
+    E, _ = orc.forward(topo, *args, f=2, heads=1, layers=1, bf16=True)
+    assert E[1].tolist() == [2 + 17 * u, 2 + 25 * u]
+    # the fp32 variant takes the unrounded values: Y = (1 + 10u, (1 + 5u)^2 + 5u)
+    F, _ = orc.forward(topo, *args, f=2, heads=1, layers=1)
+    assert F[1].tolist() == [2 + 11 * u, 2 + 16 * u + 25 * u * u]
+
+
 # ----------------------------------------------------------- decoder -------
 
 def _full_table(m):
