@@ -16,7 +16,9 @@
  * Conventions shared by every call:
  *  - The library never allocates device memory.  All buffers are caller
  *    owned; `tag_graph_plan`, `tag_gnn_workspace` and
- *    `tag_gnn_decide_workspace` give their sizes.  Pointers documented as
+ *    `tag_gnn_decide_workspace` give their sizes.  (The one exception is
+ *    the static scratch array of `tag_gnn_decide_noalloc`, part of the
+ *    library's code object.)  Pointers documented as
  *    DEVICE must be device (or managed) memory, 256-byte alignment is
  *    recommended and 16-byte alignment is required.
  *  - `hip_stream` is a hipStream_t passed as void* (NULL = legacy stream).
@@ -269,6 +271,30 @@ tag_status tag_gnn_decide(const tag_graph *g, const tag_model_dims *dims, const 
                           const int32_t *query_graph, const int32_t *query_op,
                           int32_t *argmax, float *best_score, float *prior, tag_decision *decision,
                           void *workspace, size_t ws_bytes, void *hip_stream);
+
+/*
+ * Allocation-free variant of tag_gnn_decide, for callers that cannot
+ * allocate device memory or pass a workspace: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc.  Same arguments,
+ * results and errors as tag_gnn_decide, without workspace/ws_bytes: the
+ * scratch is a static device array inside the library of
+ * tag_gnn_decide_noalloc_max_bytes() bytes (64 MiB), one copy per GPU,
+ * held until the process ends; its address is looked up once per device
+ * (on the device current at the first call).  A problem whose workspace
+ * (tag_gnn_decide_workspace) exceeds that size is rejected with
+ * TAG_ENOSPACE before anything is enqueued.  Every call on one GPU shares
+ * that GPU's scratch: calls that overlap in time on one GPU (different
+ * streams or host threads without ordering) race and must be serialised by
+ * the caller.  Nothing in the scratch needs to start at zero: every value a
+ * call reads was written earlier in the same call.  Asynchronous.
+ */
+size_t tag_gnn_decide_noalloc_max_bytes(void);
+tag_status tag_gnn_decide_noalloc(const tag_graph *g, const tag_model_dims *dims, const tag_weights *w,
+                                  int32_t n_replicas, const float *E_op, const float *E_dev,
+                                  const tag_slices *slices, int32_t n_query, const int32_t *query_rep,
+                                  const int32_t *query_graph, const int32_t *query_op,
+                                  int32_t *argmax, float *best_score, float *prior, tag_decision *decision,
+                                  void *hip_stream);
 
 /*
  * Full-enumeration variant of tag_gnn_decide (topologies of at most 16

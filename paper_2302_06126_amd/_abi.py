@@ -21,7 +21,8 @@ STATUS_NAMES = {0: "TAG_OK", -1: "TAG_EINVAL", -2: "TAG_ERANGE", -3: "TAG_EDUP",
 EXPORTS = ("tag_graph_plan", "tag_graph_build", "tag_graph_get_info", "tag_graph_export",
            "tag_graph_destroy", "tag_gnn_workspace", "tag_gnn_forward", "tag_gnn_decide_workspace",
            "tag_gnn_decide", "tag_last_error", "tag_version", "tag_profile_begin", "tag_profile_end",
-           "tag_gnn_decide_full_workspace", "tag_gnn_decide_full")
+           "tag_gnn_decide_full_workspace", "tag_gnn_decide_full", "tag_gnn_decide_noalloc_max_bytes",
+           "tag_gnn_decide_noalloc")
 # include/tag_search.h
 SEARCH_EXPORTS = ("tag_search_problem_create", "tag_search_problem_destroy", "tag_search_order",
                   "tag_search_evaluate", "tag_mcts_create", "tag_mcts_destroy", "tag_mcts_select",
@@ -196,6 +197,11 @@ def load() -> C.CDLL:
                                         vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]
     lib.tag_gnn_decide_full_workspace.restype = S
     lib.tag_gnn_decide_full.restype = S
+    lib.tag_gnn_decide_noalloc_max_bytes.argtypes = []
+    lib.tag_gnn_decide_noalloc_max_bytes.restype = C.c_size_t
+    lib.tag_gnn_decide_noalloc.argtypes = [vp, C.POINTER(tag_model_dims), C.POINTER(tag_weights), S, vp, vp,
+                                           C.POINTER(tag_slices), S, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.tag_gnn_decide_noalloc.restype = S
     for name in SEARCH_EXPORTS:
         if name not in ("tag_search_problem_destroy", "tag_mcts_destroy"):
             getattr(lib, name).restype = S

@@ -12,6 +12,8 @@
 // gives the priors; the argmax (lowest index among equal maxima) is decoded
 // into placement, replica count, sync scheme and the compression (SFB) flag.
 #include <algorithm>
+#include <mutex>
+#include <string>
 
 #include "tag_internal.hpp"
 
@@ -238,13 +240,16 @@ extern "C" tag_status tag_gnn_decide_workspace(const tag_graph *g, const tag_mod
     return TAG_OK;
 }
 
-extern "C" tag_status tag_gnn_decide(const tag_graph *g, const tag_model_dims *dims, const tag_weights *w,
-                                     int32_t n_replicas, const float *E_op, const float *E_dev,
-                                     const tag_slices *slices, int32_t n_query, const int32_t *query_rep,
-                                     const int32_t *query_graph, const int32_t *query_op, int32_t *argmax,
-                                     float *best_score, float *prior, tag_decision *decision, void *workspace,
-                                     size_t ws_bytes, void *hip_stream) {
-    clear_error();
+namespace tag {
+namespace {
+
+// The body of tag_gnn_decide over a workspace of ws_bytes at `workspace`
+// (the caller's buffer, or the library's static scratch).
+tag_status decide_run(const tag_graph *g, const tag_model_dims *dims, const tag_weights *w, int32_t n_replicas,
+                      const float *E_op, const float *E_dev, const tag_slices *slices, int32_t n_query,
+                      const int32_t *query_rep, const int32_t *query_graph, const int32_t *query_op,
+                      int32_t *argmax, float *best_score, float *prior, tag_decision *decision, void *workspace,
+                      size_t ws_bytes, void *hip_stream, const char *ws_what) {
     if (!g || !dims || !w || !E_op || !E_dev || !slices) TAG_FAIL(TAG_EINVAL, "NULL argument");
     if (dims->f != 64 && dims->f != 128 && dims->f != 256) TAG_FAIL(TAG_ESHAPE, "f must be 64, 128 or 256");
     if (dims->dec_hidden < 0 || dims->dec_hidden > 1024) TAG_FAIL(TAG_ESHAPE, "dec_hidden must be in [0, 1024]");
@@ -259,8 +264,10 @@ extern "C" tag_status tag_gnn_decide(const tag_graph *g, const tag_model_dims *d
     if (!workspace) TAG_FAIL(TAG_EINVAL, "workspace must be non-NULL");
     const int32_t H = dims->dec_hidden, Hx = std::max(H, 1);
     DecLayout L;
-    if (carve_dec(g, Hx, n_replicas, slices->n_slices, n_query, nullptr, &L) > ws_bytes)
-        TAG_FAIL(TAG_ENOSPACE, "decide workspace too small (see tag_gnn_decide_workspace)");
+    const size_t need = carve_dec(g, Hx, n_replicas, slices->n_slices, n_query, nullptr, &L);
+    if (need > ws_bytes)
+        TAG_FAIL(TAG_ENOSPACE, std::string(ws_what) + ": needs " + std::to_string(need) + " bytes, has " +
+                                   std::to_string(ws_bytes));
     carve_dec(g, Hx, n_replicas, slices->n_slices, n_query, workspace, &L);
     hipStream_t stream = static_cast<hipStream_t>(hip_stream);
     DecArgs A{};
@@ -285,6 +292,65 @@ extern "C" tag_status tag_gnn_decide(const tag_graph *g, const tag_model_dims *d
     dec_score<<<(unsigned)A.Q, kScoreThreads, sizeof(float) * (Hx + H), stream>>>(A);
     prof_end(TAG_STAGE_DECIDE, stream);
     return launch_status("tag_gnn_decide");
+}
+
+// Static scratch of the allocation-free entry point: one copy per GPU the
+// library runs on, held until the process ends.  Host code never passes the
+// symbol itself to a kernel (on the host it only names the variable); it
+// passes the device address hipGetSymbolAddress returns for the current
+// device, looked up once per device.
+constexpr size_t kDecideScratchBytes = size_t(64) << 20;
+__device__ __align__(256) unsigned char scratch[kDecideScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+tag_status scratch_for_current_device(void **out) {
+    int dev = -1;
+    TAG_HIP_CHECK(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) TAG_FAIL(TAG_EINVAL, "device index out of range for the static scratch");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        TAG_HIP_CHECK(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p) TAG_FAIL(TAG_EHIP, "hipGetSymbolAddress returned NULL for the static scratch");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return TAG_OK;
+}
+
+}  // namespace
+}  // namespace tag
+
+extern "C" tag_status tag_gnn_decide(const tag_graph *g, const tag_model_dims *dims, const tag_weights *w,
+                                     int32_t n_replicas, const float *E_op, const float *E_dev,
+                                     const tag_slices *slices, int32_t n_query, const int32_t *query_rep,
+                                     const int32_t *query_graph, const int32_t *query_op, int32_t *argmax,
+                                     float *best_score, float *prior, tag_decision *decision, void *workspace,
+                                     size_t ws_bytes, void *hip_stream) {
+    clear_error();
+    return decide_run(g, dims, w, n_replicas, E_op, E_dev, slices, n_query, query_rep, query_graph, query_op,
+                      argmax, best_score, prior, decision, workspace, ws_bytes, hip_stream,
+                      "decide workspace too small (see tag_gnn_decide_workspace)");
+}
+
+extern "C" size_t tag_gnn_decide_noalloc_max_bytes(void) { return kDecideScratchBytes; }
+
+extern "C" tag_status tag_gnn_decide_noalloc(const tag_graph *g, const tag_model_dims *dims, const tag_weights *w,
+                                             int32_t n_replicas, const float *E_op, const float *E_dev,
+                                             const tag_slices *slices, int32_t n_query, const int32_t *query_rep,
+                                             const int32_t *query_graph, const int32_t *query_op,
+                                             int32_t *argmax, float *best_score, float *prior,
+                                             tag_decision *decision, void *hip_stream) {
+    clear_error();
+    void *ws = nullptr;
+    const tag_status st = scratch_for_current_device(&ws);
+    if (st != TAG_OK) return st;
+    return decide_run(g, dims, w, n_replicas, E_op, E_dev, slices, n_query, query_rep, query_graph, query_op,
+                      argmax, best_score, prior, decision, ws, kDecideScratchBytes, hip_stream,
+                      "problem exceeds the static decide scratch (tag_gnn_decide_noalloc_max_bytes)");
 }
 
 // ------------------------------------------------------------ full enumeration

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def _declared():
     import glob
     src = "".join(open(h).read() for h in sorted(glob.glob(os.path.join(ROOT, "include", "*.h"))))
-    return sorted(set(re.findall(r"^\s*(?:tag_status|void|const char \*)\s*\*?\s*(tag_\w+)\s*\(", src, re.M)))
+    return sorted(set(re.findall(r"^\s*(?:tag_status|void|size_t|const char \*)\s*\*?\s*(tag_\w+)\s*\(", src, re.M)))
 
 
 @pytest.fixture(scope="module")
