@@ -3,11 +3,13 @@
 CSR and decoded decisions: bit-exact.  Embeddings: max over nodes of
 ||gpu - oracle||_inf / ||oracle||_inf <= 1e-4 (fp32) or 2e-2 (bf16 relation
 transforms).  Argmax on the forward pass's own embeddings: exact wherever the
-oracle's top-two gap exceeds a band delta = twice the score error bound that
-the measured embedding error implies (tests/_gpu.py, score_error_bound) plus
-1e-5 * max(1, |top score|) for the decoder's own fp32 rounding; inside the
-band any slice within delta of the top is accepted (and counted; fp32
-workloads must have at most 1% of queries inside it).
+oracle's top-two gap exceeds a band delta; inside the band any slice within
+delta of the top is accepted (and counted).  fp32: delta = 1e-5 * max(1,
+|top score|), the band of the identical-embedding decide tests (measured
+embedding errors are ~5e-7 relative), and at most 1% of the queries (at
+least one) may fall inside it.  bf16: delta = twice the worst-case score
+change that the measured embedding error allows through the decoder
+(tests/_gpu.py, score_error_bound) plus that fp32 band.
 """
 import numpy as np
 import pytest
@@ -273,7 +275,8 @@ def test_workload_full_batch(name):
         qsel = qr[sel] == r
         qops = batch.query_op[sel][qsel]
         od = oracle.decide(R_op, R_dev, masks, opts, qops, w, f=wl.f, dec_hidden=wl.f, n_dev=topo.n_dev)
-        bound = score_error_bound(w, wl.f, wl.f, R_op, R_dev, masks, qops, topo.n_dev, err)
+        bound = score_error_bound(w, wl.f, wl.f, R_op, R_dev, masks, qops, topo.n_dev, err) \
+            if wl.dtype == "bf16" else np.zeros(len(qops))
         ga = res["argmax"][qsel]
         for q in range(len(ga)):
             delta = 2.0 * bound[q] + 1e-5 * max(1.0, abs(od["best"][q]))
