@@ -199,13 +199,22 @@ struct Online {
     }
 };
 
+// Stored relation rows Y: the fp32 variant stores W^h h + c' (c' of the
+// column's relation), the bf16 variant stores bf16(W^h h) -- only the
+// transform's product is rounded, and c' is added in fp32 where a message is
+// formed.  stored_dst gives W^h h (attention destination terms).
+template <bool BF>
+__device__ __forceinline__ float stored_dst(float stored, float cp) { return BF ? stored : stored - cp; }
+
 // message + score of one entry; returns the log2-domain score
-template <int CPL, int LPH, bool ELU = false>
+template <int CPL, int LPH, bool ELU = false, bool BF = false>
 __device__ __forceinline__ float entry_score(const float (&y)[CPL], float x0, float x1, const RelConst<CPL> &k,
                                              float qd, float slope, float (&m)[CPL]) {
     float part = 0.f;
     for (int c = 0; c < CPL; ++c) {
-        float z = y[c] + fmaf(k.u0[c], x0, k.u1[c] * x1);   // y = Y + c' as stored
+        // fp32 rows hold Y + c'; bf16 rows hold Y, and the edge term U x + c' is added whole
+        const float z = BF ? y[c] + fmaf(k.u0[c], x0, fmaf(k.u1[c], x1, k.cp[c]))
+                           : y[c] + fmaf(k.u0[c], x0, k.u1[c] * x1);
         m[c] = msg_act<ELU>(z);
         part = fmaf(k.a[c], m[c], part);
     }

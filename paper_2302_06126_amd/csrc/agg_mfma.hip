@@ -67,7 +67,7 @@ __global__ void __launch_bounds__(256) pack_op_masks(AggArgs A) {
 
 // Attention terms of node rows when the transform epilogue cannot form them
 // (heads wider than 64 channels): per row, S = (p0, p1, q_od, q_same) and, for
-// device rows, the message table T (bit 0 / 1).  One wavefront per row.
+// device rows, the fp32 message table T (bit 0 / 1).  One wavefront per row.
 template <int F, int K, bool BF, bool ELU = false>
 __global__ void __launch_bounds__(256) prep_rows(AggArgs A, int dev_side) {
     constexpr int CPL = F / 64, LPH = 64 / K;
@@ -85,20 +85,16 @@ __global__ void __launch_bounds__(256) prep_rows(AggArgs A, int dev_side) {
     load_ch<CPL, BF>(Y, i * 2 * F + c0, ys);
     float p0 = 0.f, p1 = 0.f, qo = 0.f, qs = 0.f;
     for (int c = 0; c < CPL; ++c) {
-        const float yc = yo[c];   // stored rows hold Y + c'
+        const float yc = BF ? yo[c] + od.cp[c] : yo[c];   // Y + c' (fp32 rows store it, bf16 rows store Y)
         const float t0 = msg_act<ELU>(yc), t1 = msg_act<ELU>(yc + od.u0[c]);
         if (dev_side) {
-            if (BF) {
-                reinterpret_cast<unsigned *>(A.T)[i * F + c0 + c] = pack_bf2(t0, t1);
-            } else {
-                A.T[(i * 2 + 0) * F + c0 + c] = t0;
-                A.T[(i * 2 + 1) * F + c0 + c] = t1;
-            }
+            A.T[(i * 2 + 0) * F + c0 + c] = t0;
+            A.T[(i * 2 + 1) * F + c0 + c] = t1;
         }
         p0 = fmaf(od.a[c], t0, p0);
         p1 = fmaf(od.a[c], t1, p1);
-        qo = fmaf(od.ad[c], yo[c] - od.cp[c], qo);
-        qs = fmaf(same.ad[c], ys[c] - same.cp[c], qs);
+        qo = fmaf(od.ad[c], stored_dst<BF>(yo[c], od.cp[c]), qo);
+        qs = fmaf(same.ad[c], stored_dst<BF>(ys[c], same.cp[c]), qs);
     }
     p0 = head_sum<LPH>(p0); p1 = head_sum<LPH>(p1);
     qo = head_sum<LPH>(qo); qs = head_sum<LPH>(qs);
@@ -136,7 +132,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     __shared__ float pb[kOpTile][2][K];
     __shared__ int mxk[64][K];
     __shared__ float qd[64][K], mrun[64][K];
-    __shared__ float US[F];
+    __shared__ float US[F], CS[F];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int32_t r = blockIdx.y;
@@ -151,6 +147,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
 
     for (int i = tid; i < F; i += 256) {
         US[i] = A.U[(size_t)(F + i) * 2];
+        CS[i] = A.cp[F + i];
     }
     for (int i = tid; i < 64 * K; i += 256) {
         const int j = i / K, h = i % K;
@@ -187,11 +184,12 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     const int h0 = cbase / D;
     const int NRB = (Mg + 15) / 16;
     const int b = (lane >> 4) & 1;
-    float Uv[NCB];
+    float Uv[NCB], Cv[NCB];
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
         const int col = cbase + cb * 16 + (lane & 15);
         Uv[cb] = US[col];
+        Cv[cb] = CS[col];
     }
     f4 acc[4][NCB];
     float zl[4][HPW], q2[4][HPW], m2[4][HPW];
@@ -244,70 +242,17 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
                 }
             }
         }
-        if constexpr (BF) {
-            // bf16 16x16x32 products: k = 2u + b over the tile's 64 ops; lane l
-            // supplies k = 8(l/16) .. 8(l/16)+7 of a 32-wide step, i.e. ops
-            // ub .. ub+3 with both bits
-#pragma unroll 1
-            for (int ks = 0; ks < kOpTile / 16; ++ks) {
-                const int ub = 16 * ks + 4 * (lane >> 4);
-                bf8 bop[NCB];
-#pragma unroll
-                for (int cb = 0; cb < NCB; ++cb) {
-                    const int c = cbase + cb * 16 + (lane & 15);
-                    unsigned w[4];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const float yc = bf2f(Ys[(ub + q) * YS + c]);
-                        w[q] = pack_bf2(fmaxf(yc, 0.f), fmaxf(yc + Uv[cb], 0.f));
-                    }
-                    bop[cb] = as_bf8(w[0], w[1], w[2], w[3]);
-                }
-                uint64_t prq[4], btq[4];
-                float p0q[4][HPW], p1q[4][HPW];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    prq[q] = pres[ub + q];
-                    btq[q] = bits[ub + q];
-#pragma unroll
-                    for (int hh = 0; hh < HPW; ++hh) {
-                        p0q[q][hh] = pb[ub + q][0][h0 + hh];
-                        p1q[q][hh] = pb[ub + q][1][h0 + hh];
-                    }
-                }
-#pragma unroll
-                for (int rb = 0; rb < 4; ++rb) {
-                    if (rb < NRB) {
-                        const int j = rb * 16 + (lane & 15);
-#pragma unroll
-                        for (int hh = 0; hh < HPW; ++hh) {
-                            unsigned w[4];
-#pragma unroll
-                            for (int q = 0; q < 4; ++q) {
-                                const bool on = (prq[q] >> j) & 1ull;
-                                const bool bit = (btq[q] >> j) & 1ull;
-                                const float x = (bit ? p1q[q][hh] : p0q[q][hh]) + q2[rb][hh];
-                                const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
-                                zl[rb][hh] += af;
-                                w[q] = pack_bf2(bit ? 0.f : af, bit ? af : 0.f);
-                            }
-                            const bf8 aop = as_bf8(w[0], w[1], w[2], w[3]);
-#pragma unroll
-                            for (int c2 = 0; c2 < CPH; ++c2)
-                                acc[rb][hh * CPH + c2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                                    aop, bop[hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
-                        }
-                    }
-                }
-            }
-        } else
+        // fp32 16x16x4 products: k = 4 (op, bit) pairs per step, two ops per
+        // step; lane l supplies op 2s + l / 32 with bit (l / 16) % 2
         for (int s = 0; s < kOpTile / 2; ++s) {
             const int ul = 2 * s + (lane >> 5);
             const uint64_t pr = pres[ul], bt = b ? bits[ul] : ~bits[ul];   // bt bit j: link bit equals b
             float bv[NCB];
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) {
-                const float yc = static_cast<float>(Ys[ul * YS + cbase + cb * 16 + (lane & 15)]);
+                const int col = cbase + cb * 16 + (lane & 15);
+                // Y + c': fp32 rows store it, bf16 rows store Y
+                const float yc = BF ? bf2f(Ys[ul * YS + col]) + Cv[cb] : static_cast<float>(Ys[ul * YS + col]);
                 bv[cb] = msg_act<ELU>(b ? yc + Uv[cb] : yc);
             }
             float pu[HPW];
@@ -498,11 +443,12 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
         for (int i = 0; i < 4; ++i)
             if (gr0 + i < nu)
                 for (int c = 0; c < CPL; ++c) Ot[(gr0 + i) * OS + c0 + c] = 0.f;   // rows without entries stay zero
-        float a[CPL], u0c[CPL];
+        float a[CPL], u0c[CPL], cpc[CPL];
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
             a[c] = A.att_src[c0 + c] * kLog2e;
             u0c[c] = A.U[(size_t)(c0 + c) * 2];
+            cpc[c] = BF ? A.cp[c0 + c] : 0.f;
         }
         const float gs = A.g_same;
         int ri = -1;                  // row being accumulated (-1: none yet)
@@ -547,7 +493,10 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
                     float part = 0.f;
 #pragma unroll
                     for (int c = 0; c < CPL; ++c) {
-                        m[c] = msg_act<ELU>(fmaf(u0c[c], xs[s], slot[s].get(c)));
+                        // fp32 rows hold Y + c'; bf16 rows hold Y and get the edge term U x + c' whole
+                        const float z = BF ? slot[s].get(c) + fmaf(u0c[c], xs[s], cpc[c])
+                                           : fmaf(u0c[c], xs[s], slot[s].get(c));
+                        m[c] = msg_act<ELU>(z);
                         part = fmaf(a[c], m[c], part);
                     }
                     const int rl = (e >= rb_[1]) + (e >= rb_[2]) + (e >= rb_[3]);   // row of e in the group
@@ -596,132 +545,64 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
 #pragma unroll
         for (int hh = 0; hh < HPW; ++hh) zl[rb][hh] = 0.f;
     }
-    if constexpr (BF) {
-        // bf16 16x16x32 products: k = 2j + b over the tile's devices; lane l
-        // supplies devices jb .. jb+3 (both bits) of a 32-wide step
-        const unsigned *Tp = reinterpret_cast<const unsigned *>(A.T) + ((int64_t)r * A.n_dev + d0) * F;
-        bf8 bops[4][NCB];
+    // fp32 16x16x4 products: k = 4 (device, bit) pairs per step, two
+    // devices per step; the table loads of SB steps are issued together
+    const float *Tb = A.T + ((int64_t)r * A.n_dev + d0) * 2 * F;
+    const int steps = (Mg + 1) / 2;
+    const int b = (lane >> 4) & 1;
+    float bv[SB][NCB];
+    auto load_batch = [&](int s0) {
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            const int jb = 16 * ks + 4 * (lane >> 4);
+        for (int k = 0; k < SB; ++k) {
+            const int j = 2 * (s0 + k) + (lane >> 5);
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) {
-                const int c = cbase + cb * 16 + (lane & 15);
-                unsigned w[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) w[q] = jb + q < Mg ? Tp[(int64_t)(jb + q) * F + c] : 0u;
-                bops[ks][cb] = as_bf8(w[0], w[1], w[2], w[3]);
-            }
+            for (int cb = 0; cb < NCB; ++cb)
+                bv[k][cb] = j < Mg ? Tb[((int64_t)j * 2 + b) * F + cbase + cb * 16 + (lane & 15)] : 0.f;
         }
-        __syncthreads();
-        uint64_t prs[4], bts[4];
-        float q2[4][HPW], m2[4][HPW];
+    };
+    load_batch(0);
+    __syncthreads();
+    // per-lane constants of the lane's op rows u = rb*16 + l%16
+    uint64_t prs[4], bts[4];
+    float q2[4][HPW], m2[4][HPW];
 #pragma unroll
-        for (int rb = 0; rb < 4; ++rb) {
-            const int u = rb * 16 + (lane & 15);
-            prs[rb] = pres[u];
-            bts[rb] = bits[u];
+    for (int rb = 0; rb < 4; ++rb) {
+        const int u = rb * 16 + (lane & 15);
+        prs[rb] = pres[u];
+        bts[rb] = bits[u];
 #pragma unroll
-            for (int hh = 0; hh < HPW; ++hh) {
-                q2[rb][hh] = qo[u][h0 + hh];
-                m2[rb][hh] = mxS[u][h0 + hh];
-            }
+        for (int hh = 0; hh < HPW; ++hh) {
+            q2[rb][hh] = qo[u][h0 + hh];
+            m2[rb][hh] = mxS[u][h0 + hh];
         }
-        const int ksteps = (Mg + 15) / 16;
+    }
+    for (int s0 = 0; s0 < steps; s0 += SB) {
+        float bc[SB][NCB];
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            if (ks >= ksteps) break;
-            const int jb = 16 * ks + 4 * (lane >> 4);
-            float p0q[4][HPW], p1q[4][HPW];
+        for (int k = 0; k < SB; ++k)
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
+            for (int cb = 0; cb < NCB; ++cb) bc[k][cb] = bv[k][cb];
+        if (s0 + SB < steps) load_batch(s0 + SB);
 #pragma unroll
-                for (int hh = 0; hh < HPW; ++hh) {
-                    p0q[q][hh] = P[jb + q][0][h0 + hh];
-                    p1q[q][hh] = P[jb + q][1][h0 + hh];
-                }
+        for (int k = 0; k < SB; ++k) {
+            const int j = 2 * (s0 + k) + (lane >> 5);
+            if (2 * (s0 + k) >= Mg) break;
+            const bool jok = j < Mg;
+            float pj[HPW];
+#pragma unroll
+            for (int hh = 0; hh < HPW; ++hh) pj[hh] = P[j][b][h0 + hh];
 #pragma unroll
             for (int rb = 0; rb < 4; ++rb) {
+                const bool on = jok && ((prs[rb] >> j) & 1ull) && ((int)((bts[rb] >> j) & 1ull) == b);
 #pragma unroll
                 for (int hh = 0; hh < HPW; ++hh) {
-                    unsigned w[4];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const bool on = (prs[rb] >> (jb + q)) & 1ull;    // never set for jb + q >= Mg
-                        const bool bit = (bts[rb] >> (jb + q)) & 1ull;
-                        const float x = (bit ? p1q[q][hh] : p0q[q][hh]) + q2[rb][hh];
-                        const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
-                        zl[rb][hh] += af;
-                        w[q] = pack_bf2(bit ? 0.f : af, bit ? af : 0.f);
-                    }
-                    const bf8 aop = as_bf8(w[0], w[1], w[2], w[3]);
+                    const float x = pj[hh] + q2[rb][hh];
+                    const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
+                    zl[rb][hh] += af;
 #pragma unroll
                     for (int c2 = 0; c2 < CPH; ++c2)
-                        acc[rb][hh * CPH + c2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                            aop, bops[ks][hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
-                }
-            }
-        }
-    } else {
-        // fp32 16x16x4 products: k = 4 (device, bit) pairs per step, two
-        // devices per step; the table loads of SB steps are issued together
-        const float *Tb = A.T + ((int64_t)r * A.n_dev + d0) * 2 * F;
-        const int steps = (Mg + 1) / 2;
-        const int b = (lane >> 4) & 1;
-        float bv[SB][NCB];
-        auto load_batch = [&](int s0) {
-#pragma unroll
-            for (int k = 0; k < SB; ++k) {
-                const int j = 2 * (s0 + k) + (lane >> 5);
-#pragma unroll
-                for (int cb = 0; cb < NCB; ++cb)
-                    bv[k][cb] = j < Mg ? Tb[((int64_t)j * 2 + b) * F + cbase + cb * 16 + (lane & 15)] : 0.f;
-            }
-        };
-        load_batch(0);
-        __syncthreads();
-        // per-lane constants of the lane's op rows u = rb*16 + l%16
-        uint64_t prs[4], bts[4];
-        float q2[4][HPW], m2[4][HPW];
-#pragma unroll
-        for (int rb = 0; rb < 4; ++rb) {
-            const int u = rb * 16 + (lane & 15);
-            prs[rb] = pres[u];
-            bts[rb] = bits[u];
-#pragma unroll
-            for (int hh = 0; hh < HPW; ++hh) {
-                q2[rb][hh] = qo[u][h0 + hh];
-                m2[rb][hh] = mxS[u][h0 + hh];
-            }
-        }
-        for (int s0 = 0; s0 < steps; s0 += SB) {
-            float bc[SB][NCB];
-#pragma unroll
-            for (int k = 0; k < SB; ++k)
-#pragma unroll
-                for (int cb = 0; cb < NCB; ++cb) bc[k][cb] = bv[k][cb];
-            if (s0 + SB < steps) load_batch(s0 + SB);
-#pragma unroll
-            for (int k = 0; k < SB; ++k) {
-                const int j = 2 * (s0 + k) + (lane >> 5);
-                if (2 * (s0 + k) >= Mg) break;
-                const bool jok = j < Mg;
-                float pj[HPW];
-#pragma unroll
-                for (int hh = 0; hh < HPW; ++hh) pj[hh] = P[j][b][h0 + hh];
-#pragma unroll
-                for (int rb = 0; rb < 4; ++rb) {
-                    const bool on = jok && ((prs[rb] >> j) & 1ull) && ((int)((bts[rb] >> j) & 1ull) == b);
-#pragma unroll
-                    for (int hh = 0; hh < HPW; ++hh) {
-                        const float x = pj[hh] + q2[rb][hh];
-                        const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
-                        zl[rb][hh] += af;
-#pragma unroll
-                        for (int c2 = 0; c2 < CPH; ++c2)
-                            acc[rb][hh * CPH + c2] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                                af, bc[k][hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
-                    }
+                        acc[rb][hh * CPH + c2] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                            af, bc[k][hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
                 }
             }
         }

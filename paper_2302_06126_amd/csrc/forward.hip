@@ -92,7 +92,7 @@ __global__ void __launch_bounds__(256) agg_op(AggArgs A) {
         RelConst<CPL> k; k.load(A, 0, F, c0);
         float yd[CPL]; load_ch<CPL, BF>(A.Y_op, yrow_u + c0, yd);
         float q = 0.f;
-        for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], yd[c] - k.cp[c], q);   // stored rows hold Y + c'
+        for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], stored_dst<BF>(yd[c], k.cp[c]), q);
         q = head_sum<LPH>(q);
         Online<CPL> o; o.init();
         const int32_t beg = A.rp[0][u], end = A.rp[0][u + 1];
@@ -102,7 +102,7 @@ __global__ void __launch_bounds__(256) agg_op(AggArgs A) {
             const float x0 = xo[A.eid[0][e]];
             float y[CPL]; load_ch<CPL, BF>(A.Y_op, ((int64_t)rep * A.n_op + v) * 2 * F + c0, y);
             float m[CPL];
-            float s2 = entry_score<CPL, LPH, ELU>(y, x0, 0.f, k, q, A.slope, m);
+            float s2 = entry_score<CPL, LPH, ELU, BF>(y, x0, 0.f, k, q, A.slope, m);
             o.push(s2, m);
         }
         if (end > beg) {
@@ -114,7 +114,7 @@ __global__ void __launch_bounds__(256) agg_op(AggArgs A) {
         RelConst<CPL> k; k.load(A, 1, F, c0);
         float yd[CPL]; load_ch<CPL, BF>(A.Y_op, yrow_u + F + c0, yd);
         float q = 0.f;
-        for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], yd[c] - k.cp[c], q);   // stored rows hold Y + c'
+        for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], stored_dst<BF>(yd[c], k.cp[c]), q);
         q = head_sum<LPH>(q);
         Online<CPL> o; o.init();
         const int32_t beg = A.rp[1][u], end = A.rp[1][u + 1];
@@ -124,7 +124,7 @@ __global__ void __launch_bounds__(256) agg_op(AggArgs A) {
             const float x0 = xb[A.eid[1][e]] ? 1.f : 0.f;
             float y[CPL]; load_ch<CPL, BF>(A.Y_dev, ((int64_t)rep * A.n_dev + j) * 2 * F + F + c0, y);
             float m[CPL];
-            float s2 = entry_score<CPL, LPH, ELU>(y, x0, 0.f, k, q, A.slope, m);
+            float s2 = entry_score<CPL, LPH, ELU, BF>(y, x0, 0.f, k, q, A.slope, m);
             o.push(s2, m);
         }
         if (end > beg) {
@@ -157,7 +157,7 @@ __global__ void __launch_bounds__(256) agg_dev_part(AggArgs A) {
     RelConst<CPL> k; k.load(A, 1, F, c0);
     float yd[CPL]; load_ch<CPL, BF>(A.Y_dev, ((int64_t)rep * A.n_dev + j) * 2 * F + F + c0, yd);
     float q = 0.f;
-    for (int cc = 0; cc < CPL; ++cc) q = fmaf(k.ad[cc], yd[cc] - k.cp[cc], q);   // stored rows hold Y + c'
+    for (int cc = 0; cc < CPL; ++cc) q = fmaf(k.ad[cc], stored_dst<BF>(yd[cc], k.cp[cc]), q);
     q = head_sum<LPH>(q);
     Online<CPL> o; o.init();
     const uint8_t *xb = A.x_od + (int64_t)rep * A.s_od;
@@ -166,7 +166,7 @@ __global__ void __launch_bounds__(256) agg_dev_part(AggArgs A) {
         const float x0 = xb[A.eid[2][e]] ? 1.f : 0.f;
         float y[CPL]; load_ch<CPL, BF>(A.Y_op, ((int64_t)rep * A.n_op + u) * 2 * F + F + c0, y);
         float m[CPL];
-        float s2 = entry_score<CPL, LPH, ELU>(y, x0, 0.f, k, q, A.slope, m);
+        float s2 = entry_score<CPL, LPH, ELU, BF>(y, x0, 0.f, k, q, A.slope, m);
         o.push(s2, m);
     }
     // partial record: [mx per head][den per head][acc F]
@@ -247,7 +247,7 @@ __global__ void __launch_bounds__(256) agg_dev_final(AggArgs A) {
         RelConst<CPL> k; k.load(A, 2, F, c0);
         float yd[CPL]; load_ch<CPL, BF>(A.Y_dev, ((int64_t)rep * A.n_dev + j) * 2 * F + c0, yd);
         float q = 0.f;
-        for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], yd[c] - k.cp[c], q);   // stored rows hold Y + c'
+        for (int c = 0; c < CPL; ++c) q = fmaf(k.ad[c], stored_dst<BF>(yd[c], k.cp[c]), q);
         q = head_sum<LPH>(q);
         Online<CPL> o; o.init();
         const int32_t beg = A.rp[3][j], end = A.rp[3][j + 1];
@@ -269,7 +269,7 @@ __global__ void __launch_bounds__(256) agg_dev_final(AggArgs A) {
             }
             float s2[EB], m[EB][CPL];
 #pragma unroll
-            for (int i = 0; i < EB; ++i) s2[i] = entry_score<CPL, LPH, ELU>(y[i], x0[i], x1[i], k, q, A.slope, m[i]);
+            for (int i = 0; i < EB; ++i) s2[i] = entry_score<CPL, LPH, ELU, BF>(y[i], x0[i], x1[i], k, q, A.slope, m[i]);
             o.template push_n<EB>(s2, m, n);
         }
         if (end > beg) {

@@ -1,7 +1,9 @@
 // Relation transforms (Section 4.2.1 layer equation, the W^h h part):
 //   op rows:     Y = H [W^h_oo ; W^h_od]^T     device rows: Y = H [W^h_dd ; W^h_od]^T
-// stored with the folded bias c' of each relation added (Y + c' starts every
-// message ReLU(Y + c' + U x)); the attention destination terms use Y itself.
+// The fp32 kernel stores Y with the folded bias c' of each relation added
+// (Y + c' starts every message ReLU(Y + c' + U x)); the bf16 kernel stores
+// bf16(Y) alone, the rounded product of the bf16 variant, and the message
+// kernels add c' in fp32.  The attention destination terms use Y itself.
 // One launch covers both row sets of a layer.  128 x 128 block tiles, four
 // wavefronts of 64 x 64, k-chunks staged through LDS with the next chunk's
 // global loads in flight while the current one feeds the matrix cores.  The
@@ -62,8 +64,8 @@ __device__ __forceinline__ float xpose_sum4(const float (&v)[4], int lane) {
 // Epilogue of the bf16 kernel, whose products are taken as Y = H W^T: result
 // register v of block (i, j) in lane l holds row 16 i + 4 (l / 16) + v and
 // column 16 j + l % 16 of the wavefront's 64 x 64 tile (one bf16 column per
-// lane and block, two-byte stores).  The terms use the bf16-rounded values
-// that are stored.
+// lane and block, two-byte stores).  The stored row is bf16(W^h h) without
+// c'; the terms and the fp32 message table use that rounded value plus c'.
 template <int JPH, bool BF>
 __device__ void store_tile_rows(const GemmArgs &G, const Tile &t, int wm, int wn, int lane, const f4 (&acc)[4][4]) {
     constexpr int HW = JPH > 0 ? 4 / JPH : 1;      // heads per wavefront
@@ -92,16 +94,13 @@ __device__ void store_tile_rows(const GemmArgs &G, const Tile &t, int wm, int wn
             c1[j] = 0.f; c2[j] = P.ad_same[t.sd][c]; c4[j] = 0.f;
         }
     }
-    // yv: W^h h (bf16-rounded in BF) for the destination terms; ys: the stored
-    // row Y + c' (messages and their logits start from it)
+    // yv: W^h h (bf16-rounded in BF, the stored value) for the destination
+    // terms; ys: Y + c' in fp32, where messages and their logits start
     auto yv = [&](int i, int j, int v) {
         const float y = acc[i][j][v];
         return BF ? bf2f(f2bf(y)) : y;
     };
-    auto ys = [&](int i, int j, int v) {
-        const float y = acc[i][j][v] + c3[j];
-        return BF ? bf2f(f2bf(y)) : y;
-    };
+    auto ys = [&](int i, int j, int v) { return yv(i, j, v) + c3[j]; };
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -110,9 +109,9 @@ __device__ void store_tile_rows(const GemmArgs &G, const Tile &t, int wm, int wn
             if (m >= rows) continue;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const float y = acc[i][j][v] + c3[j];
-                if (BF) static_cast<uint16_t *>(Yp)[m * ldy + col0 + j * 16 + k] = f2bf(y);
-                else static_cast<float *>(Yp)[m * ldy + col0 + j * 16 + k] = y;
+                // bf16 rows store the rounded product alone; fp32 rows store Y + c'
+                if (BF) static_cast<uint16_t *>(Yp)[m * ldy + col0 + j * 16 + k] = f2bf(acc[i][j][v]);
+                else static_cast<float *>(Yp)[m * ldy + col0 + j * 16 + k] = acc[i][j][v] + c3[j];
             }
         }
         if constexpr (JPH == 0) continue;
@@ -126,12 +125,8 @@ __device__ void store_tile_rows(const GemmArgs &G, const Tile &t, int wm, int wn
                 for (int j = 0; j < 4; ++j) {
                     const float yc = ys(i, j, v);
                     const float t0 = fmaxf(yc, 0.f), t1 = fmaxf(yc + c4[j], 0.f);
-                    if (BF) {   // packed (bit 0, bit 1) bf16 pairs
-                        reinterpret_cast<unsigned *>(P.T)[rv * F + cw + j * 16 + k] = pack_bf2(t0, t1);
-                    } else {
-                        P.T[(rv * 2 + 0) * F + cw + j * 16 + k] = t0;
-                        P.T[(rv * 2 + 1) * F + cw + j * 16 + k] = t1;
-                    }
+                    P.T[(rv * 2 + 0) * F + cw + j * 16 + k] = t0;
+                    P.T[(rv * 2 + 1) * F + cw + j * 16 + k] = t1;
                 }
             }
         }

@@ -14,16 +14,18 @@ struct GemmSide {
     int ldb;
     void *Y;             // [rows][2F]
 };
-// Y is stored as W^h h + c' (c' of the column's relation: same-type half or
-// od half).  Optional epilogue: per-(row, head) attention terms of the layer, taken from
-// the output rows while they are still in registers (heads of 16, 32 or 64
-// channels, so one head lies inside one wavefront's 64 columns):
+// fp32: Y is stored as W^h h + c' (c' of the column's relation: same-type
+// half or od half); bf16: Y is stored as bf16(W^h h), the only rounded
+// quantity besides the operands, and consumers add c' in fp32.
+// Optional epilogue: per-(row, head) attention terms of the layer, taken
+// from the output rows while they are still in registers (heads of 16, 32
+// or 64 channels, so one head lies inside one wavefront's 64 columns):
 //   S[row][0][h] = a_od . sigma(Y_od + c'_od)         logit of message bit 0
 //   S[row][1][h] = a_od . sigma(Y_od + c'_od + U_od)  logit of message bit 1
 // (with Y the unbiased W^h h)
 //   S[row][2][h] = a~_od . Y_od                       destination term, od
 //   S[row][3][h] = a~_same . Y_same                   destination term, oo / dd
-// and, for device rows, the two message rows T[row][b] = sigma(Y_od + c'_od + b U_od)
+// and, for device rows, the two fp32 message rows T[row][b] = sigma(Y_od + c'_od + b U_od)
 // (sigma: ReLU, or ELU for the variant).
 struct GemmPrep {
     int jph;             // 16-column blocks per head (1, 2, 4); 0: no attention terms
