@@ -130,7 +130,8 @@ def algorithmic_work(stage: str, wl, topo, R: int, info, n_slices: int, n_query:
     tpg = 1 if tiles <= 16 else -(-tiles // 16)    # op tiles per device<-op block
     groups = -(-tiles // tpg)
     rec = R * M * groups * (F + 2 * K) * 4         # device<-op partial records
-    tbytes = R * M * F * 8                         # fp32 device message table (bit 0 / 1)
+    # device message table (bit 0 / 1): fp32, or its three bf16 split parts
+    tbytes = R * M * F * (12 if wl.dtype == "bf16" else 8)
     if stage == "transform":
         # H in, W in, Y out, plus the attention terms (4K per row) and the
         # device message table that the epilogue writes

@@ -18,6 +18,22 @@ __device__ __forceinline__ bf8 as_bf8(unsigned w0, unsigned w1, unsigned w2, uns
     return __builtin_bit_cast(bf8, u4v{w0, w1, w2, w3});
 }
 
+// acc += A B for fp32 operands given as exact three-way bf16 splits
+// (split3): the eight part products a_i b_j with i + j <= 3 on 16x16x32 bf16
+// MFMAs, smallest first.  Each part product is exact in fp32 and the one
+// dropped term a_2 b_2 is below 2^-32 |a b|, so the result is the fp32
+// contraction of A and B up to fp32 accumulation.
+__device__ __forceinline__ f4 mfma_split3(const bf8 (&a)[3], const bf8 (&b)[3], f4 acc) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[2], b[1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[1], b[2], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[2], b[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[1], b[1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[0], b[2], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[1], b[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[0], b[1], acc, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[0], b[0], acc, 0, 0, 0);
+}
+
 // -------------------------------------------------------------- aggregation
 struct AggArgs {
     int32_t R;
@@ -41,8 +57,9 @@ struct AggArgs {
     const int32_t *tiles, *tile_off, *op_off, *dev_off;
     uint64_t *omask;                  // [R*n_op][2]: present / placement-bit masks over local devices
     float *Sdev;                      // [R*n_dev][4][K]: p0, p1, q_od, q_dd of device rows
-    float *T;                         // [R*n_dev][2][F]: device messages for bit 0 / 1 (fp32 path);
-                                      // bf16 path: [R*n_dev][F] packed (bit 0, bit 1) bf16 pairs
+    float *T;                         // fp32 variant: [R*n_dev][2][F] device messages for bit 0 / 1;
+                                      // bf16 variant: [3][R*n_dev][F] the exact three-way bf16 splits
+                                      // (split3) of the same fp32 messages, packed (bit 0, bit 1)
     float *Sop;                       // [R*n_op][4][K]: p0, p1, q_od, q_oo of op rows
     int32_t prep_done;                // Sop, Sdev and T already written by the transform
     int32_t rec_mode;                 // 0: records per 256-entry chunk, 1: per tile group

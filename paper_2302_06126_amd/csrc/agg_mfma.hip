@@ -67,7 +67,8 @@ __global__ void __launch_bounds__(256) pack_op_masks(AggArgs A) {
 
 // Attention terms of node rows when the transform epilogue cannot form them
 // (heads wider than 64 channels): per row, S = (p0, p1, q_od, q_same) and, for
-// device rows, the fp32 message table T (bit 0 / 1).  One wavefront per row.
+// device rows, the message table T (bit 0 / 1; fp32, or its exact bf16
+// splits in the bf16 variant).  One wavefront per row.
 template <int F, int K, bool BF, bool ELU = false>
 __global__ void __launch_bounds__(256) prep_rows(AggArgs A, int dev_side) {
     constexpr int CPL = F / 64, LPH = 64 / K;
@@ -88,8 +89,15 @@ __global__ void __launch_bounds__(256) prep_rows(AggArgs A, int dev_side) {
         const float yc = BF ? yo[c] + od.cp[c] : yo[c];   // Y + c' (fp32 rows store it, bf16 rows store Y)
         const float t0 = msg_act<ELU>(yc), t1 = msg_act<ELU>(yc + od.u0[c]);
         if (dev_side) {
-            A.T[(i * 2 + 0) * F + c0 + c] = t0;
-            A.T[(i * 2 + 1) * F + c0 + c] = t1;
+            if (BF) {   // exact three-way bf16 splits, (bit 0, bit 1) pairs
+                unsigned sp[3];
+                split3(t0, t1, sp);
+                unsigned *Tu = reinterpret_cast<unsigned *>(A.T);
+                for (int q = 0; q < 3; ++q) Tu[q * rows * F + i * F + c0 + c] = sp[q];
+            } else {
+                A.T[(i * 2 + 0) * F + c0 + c] = t0;
+                A.T[(i * 2 + 1) * F + c0 + c] = t1;
+            }
         }
         p0 = fmaf(od.a[c], t0, p0);
         p1 = fmaf(od.a[c], t1, p1);
@@ -242,6 +250,72 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
                 }
             }
         }
+        if constexpr (BF) {
+            // 16x16x32 bf16 products over the exact three-way splits of the
+            // fp32 attention weights and messages (mfma_split3): k = 2u + b
+            // over the tile's 64 ops; lane l supplies k = 8(l/16) .. 8(l/16)+7
+            // of a 32-wide step, i.e. ops ub .. ub+3 with both bits
+#pragma unroll 1
+            for (int ks = 0; ks < kOpTile / 16; ++ks) {
+                const int ub = 16 * ks + 4 * (lane >> 4);
+                bf8 bop[NCB][3];
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb) {
+                    const int col = cbase + cb * 16 + (lane & 15);
+                    unsigned w[3][4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const float yc = bf2f(Ys[(ub + q) * YS + col]) + Cv[cb];   // Y + c'
+                        unsigned sp[3];
+                        split3(fmaxf(yc, 0.f), fmaxf(yc + Uv[cb], 0.f), sp);
+#pragma unroll
+                        for (int z = 0; z < 3; ++z) w[z][q] = sp[z];
+                    }
+#pragma unroll
+                    for (int z = 0; z < 3; ++z) bop[cb][z] = as_bf8(w[z][0], w[z][1], w[z][2], w[z][3]);
+                }
+                uint64_t prq[4], btq[4];
+                float p0q[4][HPW], p1q[4][HPW];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    prq[q] = pres[ub + q];
+                    btq[q] = bits[ub + q];
+#pragma unroll
+                    for (int hh = 0; hh < HPW; ++hh) {
+                        p0q[q][hh] = pb[ub + q][0][h0 + hh];
+                        p1q[q][hh] = pb[ub + q][1][h0 + hh];
+                    }
+                }
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) {
+                    if (rb < NRB) {
+                        const int j = rb * 16 + (lane & 15);
+#pragma unroll
+                        for (int hh = 0; hh < HPW; ++hh) {
+                            unsigned w[3][4];
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) {
+                                const bool on = (prq[q] >> j) & 1ull;
+                                const bool bit = (btq[q] >> j) & 1ull;
+                                const float x = (bit ? p1q[q][hh] : p0q[q][hh]) + q2[rb][hh];
+                                const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
+                                zl[rb][hh] += af;
+                                unsigned sp[3];
+                                split3(bit ? 0.f : af, bit ? af : 0.f, sp);
+#pragma unroll
+                                for (int z = 0; z < 3; ++z) w[z][q] = sp[z];
+                            }
+                            const bf8 aop[3] = {as_bf8(w[0][0], w[0][1], w[0][2], w[0][3]),
+                                                as_bf8(w[1][0], w[1][1], w[1][2], w[1][3]),
+                                                as_bf8(w[2][0], w[2][1], w[2][2], w[2][3])};
+#pragma unroll
+                            for (int c2 = 0; c2 < CPH; ++c2)
+                                acc[rb][hh * CPH + c2] = mfma_split3(aop, bop[hh * CPH + c2], acc[rb][hh * CPH + c2]);
+                        }
+                    }
+                }
+            }
+        } else
         // fp32 16x16x4 products: k = 4 (op, bit) pairs per step, two ops per
         // step; lane l supplies op 2s + l / 32 with bit (l / 16) % 2
         for (int s = 0; s < kOpTile / 2; ++s) {
@@ -545,64 +619,144 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
 #pragma unroll
         for (int hh = 0; hh < HPW; ++hh) zl[rb][hh] = 0.f;
     }
-    // fp32 16x16x4 products: k = 4 (device, bit) pairs per step, two
-    // devices per step; the table loads of SB steps are issued together
-    const float *Tb = A.T + ((int64_t)r * A.n_dev + d0) * 2 * F;
-    const int steps = (Mg + 1) / 2;
-    const int b = (lane >> 4) & 1;
-    float bv[SB][NCB];
-    auto load_batch = [&](int s0) {
+    if constexpr (BF) {
+        // 16x16x32 bf16 products over the exact three-way splits of the fp32
+        // attention weights and message table (mfma_split3): k = 2j + b over
+        // the tile's devices; lane l supplies devices jb .. jb+3 (both bits)
+        // of a 32-wide step.  The next step's table parts load while the
+        // current step runs.
+        const unsigned *Tp = reinterpret_cast<const unsigned *>(A.T) + ((int64_t)r * A.n_dev + d0) * F;
+        const int64_t tpart = (int64_t)A.R * A.n_dev * F;   // stride between the three parts
+        const int ksteps = (Mg + 15) / 16;
+        bf8 bops[2][NCB][3];
+        auto load_b = [&](int ks, bf8 (&bo)[NCB][3]) {
+            const int jb = 16 * ks + 4 * (lane >> 4);
 #pragma unroll
-        for (int k = 0; k < SB; ++k) {
-            const int j = 2 * (s0 + k) + (lane >> 5);
+            for (int cb = 0; cb < NCB; ++cb) {
+                const int c = cbase + cb * 16 + (lane & 15);
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb)
-                bv[k][cb] = j < Mg ? Tb[((int64_t)j * 2 + b) * F + cbase + cb * 16 + (lane & 15)] : 0.f;
+                for (int z = 0; z < 3; ++z) {
+                    unsigned w[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) w[q] = jb + q < Mg ? Tp[z * tpart + (int64_t)(jb + q) * F + c] : 0u;
+                    bo[cb][z] = as_bf8(w[0], w[1], w[2], w[3]);
+                }
+            }
+        };
+        load_b(0, bops[0]);
+        __syncthreads();
+        uint64_t prs[4], bts[4];
+        float q2[4][HPW], m2[4][HPW];
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb) {
+            const int u = rb * 16 + (lane & 15);
+            prs[rb] = pres[u];
+            bts[rb] = bits[u];
+#pragma unroll
+            for (int hh = 0; hh < HPW; ++hh) {
+                q2[rb][hh] = qo[u][h0 + hh];
+                m2[rb][hh] = mxS[u][h0 + hh];
+            }
         }
-    };
-    load_batch(0);
-    __syncthreads();
-    // per-lane constants of the lane's op rows u = rb*16 + l%16
-    uint64_t prs[4], bts[4];
-    float q2[4][HPW], m2[4][HPW];
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb) {
-        const int u = rb * 16 + (lane & 15);
-        prs[rb] = pres[u];
-        bts[rb] = bits[u];
+        for (int ks = 0; ks < 4; ++ks) {
+            if (ks >= ksteps) break;
+            if (ks + 1 < ksteps) load_b(ks + 1, bops[(ks + 1) & 1]);
+            const int jb = 16 * ks + 4 * (lane >> 4);
+            float p0q[4][HPW], p1q[4][HPW];
 #pragma unroll
-        for (int hh = 0; hh < HPW; ++hh) {
-            q2[rb][hh] = qo[u][h0 + hh];
-            m2[rb][hh] = mxS[u][h0 + hh];
-        }
-    }
-    for (int s0 = 0; s0 < steps; s0 += SB) {
-        float bc[SB][NCB];
-#pragma unroll
-        for (int k = 0; k < SB; ++k)
-#pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) bc[k][cb] = bv[k][cb];
-        if (s0 + SB < steps) load_batch(s0 + SB);
-#pragma unroll
-        for (int k = 0; k < SB; ++k) {
-            const int j = 2 * (s0 + k) + (lane >> 5);
-            if (2 * (s0 + k) >= Mg) break;
-            const bool jok = j < Mg;
-            float pj[HPW];
-#pragma unroll
-            for (int hh = 0; hh < HPW; ++hh) pj[hh] = P[j][b][h0 + hh];
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb) {
-                const bool on = jok && ((prs[rb] >> j) & 1ull) && ((int)((bts[rb] >> j) & 1ull) == b);
+            for (int q = 0; q < 4; ++q)
 #pragma unroll
                 for (int hh = 0; hh < HPW; ++hh) {
-                    const float x = pj[hh] + q2[rb][hh];
-                    const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
-                    zl[rb][hh] += af;
+                    p0q[q][hh] = P[jb + q][0][h0 + hh];
+                    p1q[q][hh] = P[jb + q][1][h0 + hh];
+                }
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) {
+#pragma unroll
+                for (int hh = 0; hh < HPW; ++hh) {
+                    unsigned w[3][4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const bool on = (prs[rb] >> (jb + q)) & 1ull;    // never set for jb + q >= Mg
+                        const bool bit = (bts[rb] >> (jb + q)) & 1ull;
+                        const float x = (bit ? p1q[q][hh] : p0q[q][hh]) + q2[rb][hh];
+                        const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
+                        zl[rb][hh] += af;
+                        unsigned sp[3];
+                        split3(bit ? 0.f : af, bit ? af : 0.f, sp);
+#pragma unroll
+                        for (int z = 0; z < 3; ++z) w[z][q] = sp[z];
+                    }
+                    const bf8 aop[3] = {as_bf8(w[0][0], w[0][1], w[0][2], w[0][3]),
+                                        as_bf8(w[1][0], w[1][1], w[1][2], w[1][3]),
+                                        as_bf8(w[2][0], w[2][1], w[2][2], w[2][3])};
 #pragma unroll
                     for (int c2 = 0; c2 < CPH; ++c2)
-                        acc[rb][hh * CPH + c2] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                            af, bc[k][hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
+                        acc[rb][hh * CPH + c2] = mfma_split3(aop, bops[ks & 1][hh * CPH + c2], acc[rb][hh * CPH + c2]);
+                }
+            }
+        }
+    } else {
+        // fp32 16x16x4 products: k = 4 (device, bit) pairs per step, two
+        // devices per step; the table loads of SB steps are issued together
+        const float *Tb = A.T + ((int64_t)r * A.n_dev + d0) * 2 * F;
+        const int steps = (Mg + 1) / 2;
+        const int b = (lane >> 4) & 1;
+        float bv[SB][NCB];
+        auto load_batch = [&](int s0) {
+    #pragma unroll
+            for (int k = 0; k < SB; ++k) {
+                const int j = 2 * (s0 + k) + (lane >> 5);
+    #pragma unroll
+                for (int cb = 0; cb < NCB; ++cb)
+                    bv[k][cb] = j < Mg ? Tb[((int64_t)j * 2 + b) * F + cbase + cb * 16 + (lane & 15)] : 0.f;
+            }
+        };
+        load_batch(0);
+        __syncthreads();
+        // per-lane constants of the lane's op rows u = rb*16 + l%16
+        uint64_t prs[4], bts[4];
+        float q2[4][HPW], m2[4][HPW];
+    #pragma unroll
+        for (int rb = 0; rb < 4; ++rb) {
+            const int u = rb * 16 + (lane & 15);
+            prs[rb] = pres[u];
+            bts[rb] = bits[u];
+    #pragma unroll
+            for (int hh = 0; hh < HPW; ++hh) {
+                q2[rb][hh] = qo[u][h0 + hh];
+                m2[rb][hh] = mxS[u][h0 + hh];
+            }
+        }
+        for (int s0 = 0; s0 < steps; s0 += SB) {
+            float bc[SB][NCB];
+    #pragma unroll
+            for (int k = 0; k < SB; ++k)
+    #pragma unroll
+                for (int cb = 0; cb < NCB; ++cb) bc[k][cb] = bv[k][cb];
+            if (s0 + SB < steps) load_batch(s0 + SB);
+    #pragma unroll
+            for (int k = 0; k < SB; ++k) {
+                const int j = 2 * (s0 + k) + (lane >> 5);
+                if (2 * (s0 + k) >= Mg) break;
+                const bool jok = j < Mg;
+                float pj[HPW];
+    #pragma unroll
+                for (int hh = 0; hh < HPW; ++hh) pj[hh] = P[j][b][h0 + hh];
+    #pragma unroll
+                for (int rb = 0; rb < 4; ++rb) {
+                    const bool on = jok && ((prs[rb] >> j) & 1ull) && ((int)((bts[rb] >> j) & 1ull) == b);
+    #pragma unroll
+                    for (int hh = 0; hh < HPW; ++hh) {
+                        const float x = pj[hh] + q2[rb][hh];
+                        const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
+                        zl[rb][hh] += af;
+    #pragma unroll
+                        for (int c2 = 0; c2 < CPH; ++c2)
+                            acc[rb][hh * CPH + c2] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                af, bc[k][hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
+                    }
                 }
             }
         }

@@ -142,6 +142,21 @@ __device__ __forceinline__ unsigned pack_bf2(float lo, float hi) {
 __device__ __forceinline__ uint16_t f2bf(float x) { return static_cast<uint16_t>(pack_bf2(x, 0.f) & 0xffffu); }
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
 
+// Exact three-way bf16 split of two fp32 values, packed pairwise (lo in the
+// low halves): x = part0 + part1 + part2, each part a bf16 value.  Each step
+// rounds to nearest even and the residual it leaves is exact in fp32; the
+// last residual has at most 8 significant bits, so part2 holds it exactly
+// (values far below 2^-100 may lose their smallest parts as denormals).
+// Products of two parts are exact in fp32.
+__device__ __forceinline__ void split3(float lo, float hi, unsigned (&p)[3]) {
+    p[0] = pack_bf2(lo, hi);
+    float rl = lo - __uint_as_float(p[0] << 16), rh = hi - __uint_as_float(p[0] & 0xffff0000u);
+    p[1] = pack_bf2(rl, rh);
+    rl -= __uint_as_float(p[1] << 16);
+    rh -= __uint_as_float(p[1] & 0xffff0000u);
+    p[2] = pack_bf2(rl, rh);
+}
+
 // XCD-aware block order: the hardware deals consecutive workgroups to the
 // 8 XCDs round-robin; remap so that logically consecutive blocks share an
 // XCD (and its L2).  Bijective on [0, n).

@@ -65,7 +65,9 @@ __device__ __forceinline__ float xpose_sum4(const float (&v)[4], int lane) {
 // register v of block (i, j) in lane l holds row 16 i + 4 (l / 16) + v and
 // column 16 j + l % 16 of the wavefront's 64 x 64 tile (one bf16 column per
 // lane and block, two-byte stores).  The stored row is bf16(W^h h) without
-// c'; the terms and the fp32 message table use that rounded value plus c'.
+// c'; the terms and the message table use that rounded value plus c' in
+// fp32, and the table holds the exact three-way bf16 splits of the fp32
+// messages (the operands of the op <- device contraction).
 template <int JPH, bool BF>
 __device__ void store_tile_rows(const GemmArgs &G, const Tile &t, int wm, int wn, int lane, const f4 (&acc)[4][4]) {
     constexpr int HW = JPH > 0 ? 4 / JPH : 1;      // heads per wavefront
@@ -125,8 +127,16 @@ __device__ void store_tile_rows(const GemmArgs &G, const Tile &t, int wm, int wn
                 for (int j = 0; j < 4; ++j) {
                     const float yc = ys(i, j, v);
                     const float t0 = fmaxf(yc, 0.f), t1 = fmaxf(yc + c4[j], 0.f);
-                    P.T[(rv * 2 + 0) * F + cw + j * 16 + k] = t0;
-                    P.T[(rv * 2 + 1) * F + cw + j * 16 + k] = t1;
+                    if (BF) {   // exact three-way bf16 splits of the fp32 messages, (bit 0, bit 1) pairs
+                        unsigned sp[3];
+                        split3(t0, t1, sp);
+                        unsigned *Tu = reinterpret_cast<unsigned *>(P.T);
+#pragma unroll
+                        for (int q = 0; q < 3; ++q) Tu[q * rows * F + rv * F + cw + j * 16 + k] = sp[q];
+                    } else {
+                        P.T[(rv * 2 + 0) * F + cw + j * 16 + k] = t0;
+                        P.T[(rv * 2 + 1) * F + cw + j * 16 + k] = t1;
+                    }
                 }
             }
         }

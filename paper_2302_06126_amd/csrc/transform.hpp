@@ -36,7 +36,8 @@ struct GemmPrep {
     const float *u_od;                   // U_od[c] at u_od[2c]
     const float *ad_same[2];             // [F]: oo (side 0), dd (side 1)
     float *S[2];                         // [rows][4][K]
-    float *T;                            // device rows: [rows][2][F]
+    float *T;                            // device rows: fp32 [rows][2][F]; bf16 variant: [3][rows][F]
+                                         // packed (bit 0, bit 1) pairs of the split3 parts
 };
 struct GemmArgs {
     GemmSide side[2];
