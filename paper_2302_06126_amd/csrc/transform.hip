@@ -15,7 +15,7 @@
 // result register v of lane l holds row 4 (l / 16) + v, column l % 16.  The
 // fp32 kernel feeds the weights as the first operand and the hidden rows as
 // the second, so its result blocks are tiles of Y^T (see store_tile); the bf16
-// kernel takes Y = H W^T directly (store_tile_rows).
+// kernel takes Y = H W^T directly (store_tile_bf16).
 #include "tag_internal.hpp"
 #include "transform.hpp"
 
@@ -27,6 +27,7 @@ typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 typedef u4v u4;
 
 constexpr int BM = 128, BN = 128;
+constexpr int kBkBf16 = 32;   // k-chunk of the bf16 kernel (a multiple of 32)
 
 struct Tile {
     int sd;
@@ -63,83 +64,88 @@ __device__ __forceinline__ float xpose_sum4(const float (&v)[4], int lane) {
 
 // Epilogue of the bf16 kernel, whose products are taken as Y = H W^T: result
 // register v of block (i, j) in lane l holds row 16 i + 4 (l / 16) + v and
-// column 16 j + l % 16 of the wavefront's 64 x 64 tile (one bf16 column per
-// lane and block, two-byte stores).  The stored row is bf16(W^h h) without
-// c'; the terms and the message table use that rounded value plus c' in
-// fp32, and the table holds the exact three-way bf16 splits of the fp32
-// messages (the operands of the op <- device contraction).
-template <int JPH, bool BF>
-__device__ void store_tile_rows(const GemmArgs &G, const Tile &t, int wm, int wn, int lane, const f4 (&acc)[4][4]) {
+// column 16 j + l % 16 of the wavefront's 64 x 64 tile.  The stored row is
+// bf16(W^h h) without c'; the attention terms and the device message table
+// use that rounded value plus c' in fp32, and the table holds the exact
+// three-way bf16 splits of the fp32 messages (the operands of the op <-
+// device contraction).  The k loop's LDS buffers are reused: the block's
+// per-column constants are staged first (so no global load follows a store),
+// the rounded 128 x 128 tile is written to LDS, and whole rows leave in
+// 16-byte stores.
+constexpr int kTileStride = BN + 8;   // bf16 elements per LDS tile row (272 bytes)
+
+template <int JPH>
+__device__ void store_tile_bf16(const GemmArgs &G, const Tile &t, int wm, int wn, int lane, const f4 (&acc)[4][4],
+                                uint16_t *sm) {
     constexpr int HW = JPH > 0 ? 4 / JPH : 1;      // heads per wavefront
     const GemmPrep &P = G.prep;
     const int64_t rows = t.sd ? G.side[1].rows : G.side[0].rows;
     const int F = G.F, K = P.K, D = 16 * (JPH > 0 ? JPH : 1);
     const int64_t ldy = 2 * F;
-    void *Yp = t.sd ? G.side[1].Y : G.side[0].Y;
+    uint16_t *Yp = static_cast<uint16_t *>(t.sd ? G.side[1].Y : G.side[0].Y);
+    uint16_t *tile = sm;                                            // [BM][kTileStride]
+    float *cst = reinterpret_cast<float *>(sm + BM * kTileStride);  // [4][BN]: c', a, a~, U
+    const int tid = threadIdx.x;
+    if (tid < BN) {   // constants of block column n0 + tid (same-type half: a = U = 0)
+        const int n = t.n0 + tid;
+        const bool od = n >= F;
+        const int c = od ? n - F : n;
+        cst[tid] = od ? P.cp_od[c] : P.cp_same[t.sd][c];
+        cst[BN + tid] = (JPH > 0 && od) ? P.a_od[c] : 0.f;
+        cst[2 * BN + tid] = JPH > 0 ? (od ? P.ad_od[c] : P.ad_same[t.sd][c]) : 0.f;
+        cst[3 * BN + tid] = (JPH > 0 && od) ? P.u_od[2 * c] : 0.f;
+    }
+    __syncthreads();
     const int col0 = t.n0 + wn * 64;
     const bool od = col0 >= F;
     const int cw = od ? col0 - F : col0;           // first channel of the relation
     const int k = lane & 15;
-    const int64_t rbase = t.m0 + wm * 64 + 4 * (lane >> 4);
+    const int rt0 = wm * 64 + 4 * (lane >> 4);     // this lane's first row in the block tile
+    const int64_t rbase = t.m0 + rt0;
     const bool writer = (k & 3) == 0;
+    const bool dev_od = od && t.sd == 1;
     float *S = P.S[t.sd];
-    float c1[4], c2[4], c3[4], c4[4];   // od: a, a~, c', U;  same-type: a~ and c'
+    float c3[4], c1[4], c2[4], c4[4];   // c', a, a~, U of the lane's four columns
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-        const int c = cw + j * 16 + k;
-        c3[j] = od ? P.cp_od[c] : P.cp_same[t.sd][c];
-        if (JPH == 0) {
-            c1[j] = c2[j] = c4[j] = 0.f;
-        } else if (od) {
-            c1[j] = P.a_od[c]; c2[j] = P.ad_od[c]; c4[j] = P.u_od[2 * c];
-        } else {
-            c1[j] = 0.f; c2[j] = P.ad_same[t.sd][c]; c4[j] = 0.f;
-        }
+        const int cl = wn * 64 + j * 16 + k;
+        c3[j] = cst[cl]; c1[j] = cst[BN + cl]; c2[j] = cst[2 * BN + cl]; c4[j] = cst[3 * BN + cl];
     }
-    // yv: W^h h (bf16-rounded in BF, the stored value) for the destination
-    // terms; ys: Y + c' in fp32, where messages and their logits start
-    auto yv = [&](int i, int j, int v) {
-        const float y = acc[i][j][v];
-        return BF ? bf2f(f2bf(y)) : y;
-    };
-    auto ys = [&](int i, int j, int v) { return yv(i, j, v) + c3[j]; };
+    unsigned *Tu = reinterpret_cast<unsigned *>(P.T);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
+        float yv[4][4];   // [j][v]: the rounded product W^h h as stored
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int64_t m = rbase + i * 16 + v;
-            if (m >= rows) continue;
+        for (int j = 0; j < 4; ++j) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                // bf16 rows store the rounded product alone; fp32 rows store Y + c'
-                if (BF) static_cast<uint16_t *>(Yp)[m * ldy + col0 + j * 16 + k] = f2bf(acc[i][j][v]);
-                else static_cast<float *>(Yp)[m * ldy + col0 + j * 16 + k] = acc[i][j][v] + c3[j];
+            for (int v = 0; v < 4; v += 2) {
+                const unsigned pr = pack_bf2(acc[i][j][v], acc[i][j][v + 1]);
+                yv[j][v] = __uint_as_float(pr << 16);
+                yv[j][v + 1] = __uint_as_float(pr & 0xffff0000u);
+                const int cl = wn * 64 + j * 16 + k;
+                tile[(rt0 + i * 16 + v) * kTileStride + cl] = static_cast<uint16_t>(pr & 0xffffu);
+                tile[(rt0 + i * 16 + v + 1) * kTileStride + cl] = static_cast<uint16_t>(pr >> 16);
             }
         }
-        if constexpr (JPH == 0) continue;
-        const int64_t row = rbase + i * 16 + (k >> 2);   // row of this lane's totals
-        if (od && t.sd == 1) {
+        // device message rows, bit 0 / 1, as exact bf16 splits (the table exists
+        // only with the attention-term epilogue, JPH > 0)
+        if (JPH > 0 && dev_od) {
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const int64_t rv = rbase + i * 16 + v;
                 if (rv >= rows) continue;
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    const float yc = ys(i, j, v);
-                    const float t0 = fmaxf(yc, 0.f), t1 = fmaxf(yc + c4[j], 0.f);
-                    if (BF) {   // exact three-way bf16 splits of the fp32 messages, (bit 0, bit 1) pairs
-                        unsigned sp[3];
-                        split3(t0, t1, sp);
-                        unsigned *Tu = reinterpret_cast<unsigned *>(P.T);
+                    const float ys = yv[j][v] + c3[j];
+                    unsigned sp[3];
+                    split3(fmaxf(ys, 0.f), fmaxf(ys + c4[j], 0.f), sp);
 #pragma unroll
-                        for (int q = 0; q < 3; ++q) Tu[q * rows * F + rv * F + cw + j * 16 + k] = sp[q];
-                    } else {
-                        P.T[(rv * 2 + 0) * F + cw + j * 16 + k] = t0;
-                        P.T[(rv * 2 + 1) * F + cw + j * 16 + k] = t1;
-                    }
+                    for (int q = 0; q < 3; ++q) Tu[q * rows * F + rv * F + cw + j * 16 + k] = sp[q];
                 }
             }
         }
+        if constexpr (JPH == 0) continue;
+        const int64_t row = rbase + i * 16 + (k >> 2);   // row of this lane's totals
 #pragma unroll
         for (int hw = 0; hw < HW; ++hw) {
             const int h = cw / D + hw;
@@ -151,10 +157,10 @@ __device__ void store_tile_rows(const GemmArgs &G, const Tile &t, int wm, int wn
 #pragma unroll
                     for (int jj = 0; jj < JPH; ++jj) {
                         const int j = hw * JPH + jj;
-                        const float yc = ys(i, j, v);
-                        p0[v] = fmaf(c1[j], fmaxf(yc, 0.f), p0[v]);
-                        p1[v] = fmaf(c1[j], fmaxf(yc + c4[j], 0.f), p1[v]);
-                        q[v] = fmaf(c2[j], yv(i, j, v), q[v]);
+                        const float ys = yv[j][v] + c3[j];
+                        p0[v] = fmaf(c1[j], fmaxf(ys, 0.f), p0[v]);
+                        p1[v] = fmaf(c1[j], fmaxf(ys + c4[j], 0.f), p1[v]);
+                        q[v] = fmaf(c2[j], yv[j][v], q[v]);
                     }
                 }
                 const float s0 = xpose_sum4(p0, lane), s1 = xpose_sum4(p1, lane), s2 = xpose_sum4(q, lane);
@@ -169,13 +175,24 @@ __device__ void store_tile_rows(const GemmArgs &G, const Tile &t, int wm, int wn
                 for (int v = 0; v < 4; ++v) {
                     q[v] = 0.f;
 #pragma unroll
-                    for (int jj = 0; jj < JPH; ++jj) q[v] = fmaf(c2[hw * JPH + jj], yv(i, hw * JPH + jj, v), q[v]);
+                    for (int jj = 0; jj < JPH; ++jj) q[v] = fmaf(c2[hw * JPH + jj], yv[hw * JPH + jj][v], q[v]);
                 }
                 const float s2 = xpose_sum4(q, lane);
                 if (writer && row < rows) S[row * 4 * K + 3 * K + h] = s2;
             }
         }
-        __builtin_amdgcn_sched_barrier(0);   // keep one row block's values live at a time
+    }
+    __syncthreads();
+    // whole rows of the block's 128 columns: 16 threads per row, 16 bytes each
+#pragma unroll
+    for (int it = 0; it < BM * BN / 8 / 256; ++it) {
+        const int idx = it * 256 + tid;
+        const int rr = idx >> 4, ch = idx & 15;
+        const int64_t m = t.m0 + rr;
+        if (m < rows) {
+            const u4 v = *reinterpret_cast<const u4 *>(&tile[rr * kTileStride + ch * 8]);
+            *reinterpret_cast<u4 *>(Yp + m * ldy + t.n0 + ch * 8) = v;
+        }
     }
 }
 
@@ -358,9 +375,14 @@ __global__ void __launch_bounds__(256) gemm_f32(GemmArgs G) {
 
 template <int JPH>
 __global__ void __launch_bounds__(256) gemm_bf16(GemmArgs G) {
-    constexpr int BK = 32, LS = BK + 8;    // row-major LDS rows of 40 bf16 (80 B)
-    __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LS];
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * LS];
+    constexpr int BK = kBkBf16, LS = BK + 8;   // row-major LDS rows of BK + 8 bf16
+    // k-chunk buffers As[2][BM * LS], Bs[2][BN * LS]; the epilogue reuses the
+    // space for the output tile and the column constants
+    constexpr int SM = 2 * BM * LS + 2 * BN * LS;
+    static_assert(BM * kTileStride * 2 + 4 * BN * 4 <= SM * 2, "epilogue tile must fit the k-chunk buffers");
+    __shared__ __attribute__((aligned(16))) uint16_t sm[SM];
+    uint16_t (*As)[BM * LS] = reinterpret_cast<uint16_t (*)[BM * LS]>(sm);
+    uint16_t (*Bs)[BN * LS] = reinterpret_cast<uint16_t (*)[BN * LS]>(sm + 2 * BM * LS);
     const Tile t = tile_of(G);
     const GemmSide S = t.sd ? G.side[1] : G.side[0];
     const uint16_t *__restrict__ H = static_cast<const uint16_t *>(S.H);
@@ -368,24 +390,25 @@ __global__ void __launch_bounds__(256) gemm_bf16(GemmArgs G) {
     const int F = G.F;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    const int lr = tid >> 1, lk = (tid & 1) * 16;
+    constexpr int NQ = BK / 16;            // 16-byte loads per thread and operand (two threads per row)
+    const int lr = tid >> 1, lk = (tid & 1) * (BK / 2);
     const int64_t gm = t.m0 + lr;
     const bool aok = gm < S.rows;
     const uint16_t *arow = H + (aok ? gm : 0) * F;
     const int gn = t.n0 + lr;
     const uint16_t *brow = gn < F ? static_cast<const uint16_t *>(S.B0) + (size_t)gn * S.ldb
                                   : static_cast<const uint16_t *>(S.B1) + (size_t)(gn - F) * S.ldb;
-    u4 ra[2], rb[2];
+    u4 ra[NQ], rb[NQ];
     auto gload = [&](int k0) {
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
+        for (int q = 0; q < NQ; ++q) {
             ra[q] = aok ? *reinterpret_cast<const u4 *>(arow + k0 + lk + 8 * q) : u4{0u, 0u, 0u, 0u};
             rb[q] = *reinterpret_cast<const u4 *>(brow + k0 + lk + 8 * q);
         }
     };
     auto sstore = [&](int buf) {
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
+        for (int q = 0; q < NQ; ++q) {
             *reinterpret_cast<u4 *>(&As[buf][lr * LS + lk + 8 * q]) = ra[q];
             *reinterpret_cast<u4 *>(&Bs[buf][lr * LS + lk + 8 * q]) = rb[q];
         }
@@ -421,7 +444,7 @@ __global__ void __launch_bounds__(256) gemm_bf16(GemmArgs G) {
         if (kc + 1 < nk) sstore(buf ^ 1);
         __syncthreads();
     }
-    store_tile_rows<JPH, true>(G, t, wm, wn, lane, acc);
+    store_tile_bf16<JPH>(G, t, wm, wn, lane, acc, sm);
 }
 
 }  // namespace
