@@ -35,7 +35,8 @@ class _Dims(C.Structure):
     _fields_ = [("f", C.c_int32), ("heads", C.c_int32), ("layers", C.c_int32),
                 ("f_op", C.c_int32), ("f_dev", C.c_int32), ("dec_hidden", C.c_int32),
                 ("bf16", C.c_int32), ("gamma_same", C.c_double),
-                ("gamma_cross", C.c_double), ("leaky_slope", C.c_double), ("sigma", C.c_int32)]
+                ("gamma_cross", C.c_double), ("leaky_slope", C.c_double), ("sigma", C.c_int32),
+                ("relations", C.c_int32), ("edge_act", C.c_int32), ("head_mode", C.c_int32)]
 
 
 _FP = C.POINTER(C.c_float)
@@ -100,9 +101,10 @@ def csr(n_op: int, n_dev: int, oo_src, oo_dst, dd_a, dd_b, od_op, od_dev
     return OK, [(rp, c[:n], e[:n]) for (rp, c, e), (_, n) in zip(outs, shapes)]
 
 
-def _dims(f, heads, layers, f_op, f_dev, dec_hidden, bf16, gamma_same, gamma_cross, slope, sigma=0):
+def _dims(f, heads, layers, f_op, f_dev, dec_hidden, bf16, gamma_same, gamma_cross, slope, sigma=0,
+          relations=3, edge_act=0, head_mode=0):
     return _Dims(f, heads, layers, f_op, f_dev, dec_hidden, 1 if bf16 else 0,
-                 gamma_same, gamma_cross, slope, sigma)
+                 gamma_same, gamma_cross, slope, sigma, relations, edge_act, head_mode)
 
 
 def _weights(w: Dict[str, np.ndarray]):
@@ -123,18 +125,27 @@ def _weights(w: Dict[str, np.ndarray]):
 def forward(topo, x_op, x_dev, x_oo, x_dd, x_od, w: Dict[str, np.ndarray], *,
             f: int, heads: int, layers: int, bf16: bool = False,
             gamma_same: float = 1.0, gamma_cross: float = 0.1, leaky_slope: float = 0.2,
-            want_alpha: bool = False, sigma: str = "relu"):
+            want_alpha: bool = False, sigma: str = "relu", relations: int = 3,
+            edge_act: str = "affine", heads_mode: str = "concat"):
     """E_op [N, f], E_dev [M, f] (float64) for one candidate graph; with
     want_alpha also the layer-0 attention weights [T, heads] in bucket order
-    B0, B1, B2, B3 (each bucket in CSR order)."""
+    B0, B1, B2, B3 (each bucket in CSR order; three relations only).
+    relations: 3 undirected link types or 5 directed relations (weights
+    [L][5][...]); edge_act: "affine" or "relu" edge encoders; heads_mode:
+    "concat" (K heads of f/K channels) or "avg" (K full-width heads averaged,
+    att_src / att_dst [L][R][K][f])."""
     x_op, x_dev = _f32(x_op), _f32(x_dev)
     x_oo, x_dd = _f32(x_oo).reshape(-1), _f32(x_dd).reshape(-1)
     x_od = np.ascontiguousarray(np.asarray(x_od, dtype=np.uint8)).reshape(-1)
     n, m = topo.n_op, topo.n_dev
-    if sigma not in ("relu", "elu"):
-        raise ValueError(sigma)
+    if sigma not in ("relu", "elu") or relations not in (3, 5) or edge_act not in ("affine", "relu") \
+            or heads_mode not in ("concat", "avg"):
+        raise ValueError((sigma, relations, edge_act, heads_mode))
+    if relations == 5:
+        want_alpha = False
     dims = _dims(f, heads, layers, x_op.shape[1] if x_op.ndim == 2 else 0, 8,
-                 0, bf16, gamma_same, gamma_cross, leaky_slope, 1 if sigma == "elu" else 0)
+                 0, bf16, gamma_same, gamma_cross, leaky_slope, 1 if sigma == "elu" else 0,
+                 relations, 1 if edge_act == "relu" else 0, 1 if heads_mode == "avg" else 0)
     ws, keep = _weights(w)
     E_op = np.zeros((n, f), np.float64)
     E_dev = np.zeros((m, f), np.float64)

@@ -33,7 +33,13 @@
 typedef struct {
     int32_t f, heads, layers, f_op, f_dev, dec_hidden, bf16;
     double gamma_same, gamma_cross, leaky_slope;
-    int32_t sigma;   /* message non-linearity: 0 ReLU, 1 ELU (alpha = 1) */
+    int32_t sigma;      /* message non-linearity: 0 ReLU, 1 ELU (alpha = 1) */
+    int32_t relations;  /* 3: undirected link types (op-op, op-device, device-device);
+                           5: directed (op<-op along the tensor, op<-op against it,
+                           op<-device, device<-op, device<-device) */
+    int32_t edge_act;   /* edge encoders: 0 affine, 1 affine + ReLU */
+    int32_t head_mode;  /* 0: K concatenated heads of f/K channels; 1: K heads over all
+                           f channels with their own attention vectors, averaged */
 } tago_dims;
 
 typedef struct {
@@ -171,10 +177,23 @@ int tago_csr(int32_t n_op, int32_t n_dev,
 /* No self loop, residual or normalisation.  An empty bucket adds zero.      */
 /* bf16 variant: h and W^h are rounded to bf16 before the W^h product and    */
 /* the product W^h h is rounded to bf16 after it; all else stays double.     */
+/*                                                                           */
+/* Readings where the paper leaves a choice (defaults first):                */
+/*  - link types: three undirected relations (op-op, op-device, device-      */
+/*    device; both ends of a link share W), or five directed ones (op<-op    */
+/*    along the tensor, op<-op against it, op<-device, device<-op,           */
+/*    device<-device), each with its own W, b, a, adst;                      */
+/*  - edge encoders: affine, or affine followed by ReLU;                     */
+/*  - heads: K concatenated heads of f/K channels, or K heads over all f     */
+/*    channels (attention vectors a, adst of length f per head) averaged.    */
 /* ------------------------------------------------------------------------ */
 static double leaky(double x, double slope) { return x > 0.0 ? x : slope * x; }
 
-/* one destination row of one bucket: adds gamma * agg into out[f] */
+/* one destination row of one bucket: adds gamma * agg into out[f].
+ * Concatenated heads (head_mode 0): head k scores and aggregates channels
+ * [k f/K, (k+1) f/K) with a_src, a_dst of length f.  Averaged full-width
+ * heads (head_mode 1): head k scores all f channels with its own vectors
+ * a_src + k f, a_dst + k f, and the K aggregates are averaged. */
 static void aggregate_row(const tago_dims *d, int32_t beg, int32_t end,
                           const int32_t *col, const int32_t *eid,
                           const double *ysrc,       /* [n_src][f]  W^h h_v  */
@@ -185,7 +204,8 @@ static void aggregate_row(const tago_dims *d, int32_t beg, int32_t end,
                           double gamma, double *out, double *scratch_m, double *scratch_s,
                           double *alpha_out)
 {
-    const int f = d->f, K = d->heads, dh = f / K;
+    const int f = d->f, K = d->heads, avg = d->head_mode == 1, dh = avg ? f : f / K;
+    const double g = avg ? gamma / K : gamma;
     const int32_t n = end - beg;
     if (n == 0) return;
     for (int32_t e = 0; e < n; ++e) {
@@ -199,12 +219,15 @@ static void aggregate_row(const tago_dims *d, int32_t beg, int32_t end,
         }
     }
     for (int k = 0; k < K; ++k) {
+        const int c0 = avg ? 0 : k * dh, c1 = c0 + dh;
+        const float *as = avg ? a_src + (size_t)k * f : a_src;
+        const float *ad = avg ? a_dst + (size_t)k * f : a_dst;
         double qd = 0.0;
-        for (int c = k * dh; c < (k + 1) * dh; ++c) qd += (double)a_dst[c] * ydst_u[c];
+        for (int c = c0; c < c1; ++c) qd += (double)ad[c] * ydst_u[c];
         double mx = -INFINITY;
         for (int32_t e = 0; e < n; ++e) {
             double s = 0.0;
-            for (int c = k * dh; c < (k + 1) * dh; ++c) s += (double)a_src[c] * scratch_m[(size_t)e * f + c];
+            for (int c = c0; c < c1; ++c) s += (double)as[c] * scratch_m[(size_t)e * f + c];
             s = leaky(s + qd, d->leaky_slope);
             scratch_s[e] = s;
             if (s > mx) mx = s;
@@ -214,8 +237,8 @@ static void aggregate_row(const tago_dims *d, int32_t beg, int32_t end,
         for (int32_t e = 0; e < n; ++e) {
             double al = exp(scratch_s[e] - mx) / z;
             if (alpha_out) alpha_out[(size_t)(beg + e) * K + k] = al;
-            for (int c = k * dh; c < (k + 1) * dh; ++c)
-                out[c] += gamma * al * scratch_m[(size_t)e * f + c];
+            for (int c = c0; c < c1; ++c)
+                out[c] += g * al * scratch_m[(size_t)e * f + c];
         }
     }
 }
@@ -270,6 +293,24 @@ static void encode(int f, int32_t n, int din, const float *A, const float *c,
         }
 }
 
+/* B0 split by direction for the directed reading: forward entries (row =
+ * consumer, src = producer) and backward entries (row = producer, src =
+ * consumer), each sorted by (source, edge id).  Links were validated by
+ * tago_csr. */
+static int directed_op_buckets(int32_t n_op, int32_t e_oo, const int32_t *oo_src, const int32_t *oo_dst,
+                               int32_t *rpf, int32_t *colf, int32_t *eidf,
+                               int32_t *rpb, int32_t *colb, int32_t *eidb)
+{
+    tago_entry *ent = (tago_entry *)malloc((size_t)(e_oo > 0 ? e_oo : 1) * sizeof(tago_entry));
+    if (!ent) return TAGO_ENOMEM;
+    for (int32_t i = 0; i < e_oo; ++i) ent[i] = (tago_entry){oo_dst[i], oo_src[i], i};
+    finish_bucket(ent, e_oo, n_op, rpf, colf, eidf);
+    for (int32_t i = 0; i < e_oo; ++i) ent[i] = (tago_entry){oo_src[i], oo_dst[i], i};
+    finish_bucket(ent, e_oo, n_op, rpb, colb, eidb);
+    free(ent);
+    return TAGO_OK;
+}
+
 int tago_forward(const tago_dims *d,
                  int32_t n_op, int32_t n_dev,
                  int32_t e_oo, const int32_t *oo_src, const int32_t *oo_dst,
@@ -279,10 +320,17 @@ int tago_forward(const tago_dims *d,
                  const float *x_dd, const uint8_t *x_od,
                  const tago_weights *w,
                  double *E_op, double *E_dev,
-                 double *alpha_layer0 /* optional: [T][K], buckets B0,B1,B2,B3 concatenated */)
+                 double *alpha_layer0 /* optional: [T][K], buckets B0,B1,B2,B3 concatenated
+                                         (three undirected relations only) */)
 {
-    if (!d || !w || d->f <= 0 || d->heads <= 0 || d->f % d->heads || d->layers < 0) return TAGO_ESHAPE;
-    const int f = d->f;
+    if (!d || !w || d->f <= 0 || d->heads <= 0 || d->layers < 0) return TAGO_ESHAPE;
+    if (d->relations != 3 && d->relations != 5) return TAGO_ESHAPE;
+    if (d->head_mode != 0 && d->head_mode != 1) return TAGO_ESHAPE;
+    if (d->edge_act != 0 && d->edge_act != 1) return TAGO_ESHAPE;
+    if (d->head_mode == 0 && d->f % d->heads) return TAGO_ESHAPE;
+    const int f = d->f, NR = d->relations;
+    const size_t asz = (size_t)(d->head_mode == 1 ? d->heads : 1) * f;   /* attention vector length */
+    if (NR == 5) alpha_layer0 = NULL;
     int st = TAGO_OK;
     const int64_t nn0 = 2 * (int64_t)e_oo, nn1 = e_od, nn3 = 2 * (int64_t)e_dd;
     int32_t *rp0 = malloc(sizeof(int32_t) * (n_op + 1)), *rp1 = malloc(sizeof(int32_t) * (n_op + 1));
@@ -291,33 +339,41 @@ int tago_forward(const tago_dims *d,
     int32_t *c1 = malloc(sizeof(int32_t) * (nn1 + 1)), *i1 = malloc(sizeof(int32_t) * (nn1 + 1));
     int32_t *c2 = malloc(sizeof(int32_t) * (nn1 + 1)), *i2 = malloc(sizeof(int32_t) * (nn1 + 1));
     int32_t *c3 = malloc(sizeof(int32_t) * (nn3 + 1)), *i3 = malloc(sizeof(int32_t) * (nn3 + 1));
-    const int32_t n_all = n_op + n_dev;
+    /* directed reading: op<-op split into forward (along the tensor) and backward */
+    int32_t *rpf = malloc(sizeof(int32_t) * (n_op + 1)), *rpb = malloc(sizeof(int32_t) * (n_op + 1));
+    int32_t *cf = malloc(sizeof(int32_t) * ((size_t)e_oo + 1)), *idf = malloc(sizeof(int32_t) * ((size_t)e_oo + 1));
+    int32_t *cb = malloc(sizeof(int32_t) * ((size_t)e_oo + 1)), *idb = malloc(sizeof(int32_t) * ((size_t)e_oo + 1));
     double *h_op = calloc((size_t)n_op * f + 1, sizeof(double));
     double *h_dev = calloc((size_t)n_dev * f + 1, sizeof(double));
     double *nh_op = calloc((size_t)n_op * f + 1, sizeof(double));
     double *nh_dev = calloc((size_t)n_dev * f + 1, sizeof(double));
-    double *y_op = calloc((size_t)n_op * f + 1, sizeof(double));
-    double *y_dev = calloc((size_t)n_dev * f + 1, sizeof(double));
+    double *ys_op = calloc((size_t)n_op * f + 1, sizeof(double));    /* W^h h of a relation's sources */
+    double *ys_dev = calloc((size_t)n_dev * f + 1, sizeof(double));
+    double *yd_op = calloc((size_t)n_op * f + 1, sizeof(double));    /* W^h h of its destinations */
+    double *yd_dev = calloc((size_t)n_dev * f + 1, sizeof(double));
     double *enc_oo = calloc((size_t)e_oo * f + 1, sizeof(double));
     double *enc_dd = calloc((size_t)e_dd * f + 1, sizeof(double));
     double *enc_od = calloc((size_t)2 * f, sizeof(double));
     double *te_oo = calloc((size_t)e_oo * f + 1, sizeof(double));
     double *te_dd = calloc((size_t)e_dd * f + 1, sizeof(double));
     double *te_od = calloc((size_t)2 * f, sizeof(double));
-    double *y2_op = calloc((size_t)n_op * f + 1, sizeof(double));   /* second relation on ops */
-    double *y2_dev = calloc((size_t)n_dev * f + 1, sizeof(double)); /* second relation on devices */
     int64_t maxdeg = 1;
     double *sm = NULL, *ss = NULL;
     float *xbit = malloc(sizeof(float) * 2);
     uint8_t *bit_of = malloc((size_t)nn1 + 1);
-    (void)n_all;
-    if (!rp0 || !rp1 || !rp2 || !rp3 || !c0 || !i0 || !c1 || !i1 || !c2 || !i2 || !c3 || !i3 || !h_op ||
-        !h_dev || !nh_op || !nh_dev || !y_op || !y_dev || !enc_oo || !enc_dd || !enc_od || !te_oo ||
-        !te_dd || !te_od || !y2_op || !y2_dev || !xbit || !bit_of) { st = TAGO_ENOMEM; goto done; }
+    if (!rp0 || !rp1 || !rp2 || !rp3 || !c0 || !i0 || !c1 || !i1 || !c2 || !i2 || !c3 || !i3 || !rpf ||
+        !rpb || !cf || !idf || !cb || !idb || !h_op || !h_dev || !nh_op || !nh_dev || !ys_op || !ys_dev ||
+        !yd_op || !yd_dev || !enc_oo || !enc_dd || !enc_od || !te_oo || !te_dd || !te_od || !xbit || !bit_of) {
+        st = TAGO_ENOMEM; goto done;
+    }
 
     st = tago_csr(n_op, n_dev, e_oo, oo_src, oo_dst, e_dd, dd_a, dd_b, e_od, od_op, od_dev,
                   rp0, c0, i0, rp1, c1, i1, rp2, c2, i2, rp3, c3, i3);
     if (st != TAGO_OK) goto done;
+    if (NR == 5) {
+        st = directed_op_buckets(n_op, e_oo, oo_src, oo_dst, rpf, cf, idf, rpb, cb, idb);
+        if (st != TAGO_OK) goto done;
+    }
     for (int32_t r = 0; r < n_op; ++r) {
         if (rp0[r + 1] - rp0[r] > maxdeg) maxdeg = rp0[r + 1] - rp0[r];
         if (rp1[r + 1] - rp1[r] > maxdeg) maxdeg = rp1[r + 1] - rp1[r];
@@ -331,56 +387,88 @@ int tago_forward(const tago_dims *d,
     if (!sm || !ss) { st = TAGO_ENOMEM; goto done; }
     for (int64_t i = 0; i < nn1; ++i) bit_of[i] = x_od[i] ? 1 : 0;
 
-    /* input encoders */
+    /* input encoders (edge encoders: affine, or affine + ReLU) */
     encode(f, n_op, d->f_op, w->enc_op_w, w->enc_op_b, x_op, h_op, 1);
     encode(f, n_dev, d->f_dev, w->enc_dev_w, w->enc_dev_b, x_dev, h_dev, 1);
-    encode(f, e_oo, 1, w->enc_edge_w[0], w->enc_edge_b[0], x_oo, enc_oo, 0);
-    encode(f, e_dd, 2, w->enc_edge_w[2], w->enc_edge_b[2], x_dd, enc_dd, 0);
+    encode(f, e_oo, 1, w->enc_edge_w[0], w->enc_edge_b[0], x_oo, enc_oo, d->edge_act);
+    encode(f, e_dd, 2, w->enc_edge_w[2], w->enc_edge_b[2], x_dd, enc_dd, d->edge_act);
     /* the op-device edge feature is a single placement bit: encode both values */
     xbit[0] = 0.0f; xbit[1] = 1.0f;
-    encode(f, 2, 1, w->enc_edge_w[1], w->enc_edge_b[1], xbit, enc_od, 0);
+    encode(f, 2, 1, w->enc_edge_w[1], w->enc_edge_b[1], xbit, enc_od, d->edge_act);
 
     for (int layer = 0; layer < d->layers; ++layer) {
-        const float *Woo = w->layer_w + ((size_t)layer * 3 + 0) * f * 2 * f;
-        const float *Wod = w->layer_w + ((size_t)layer * 3 + 1) * f * 2 * f;
-        const float *Wdd = w->layer_w + ((size_t)layer * 3 + 2) * f * 2 * f;
-        const float *boo = w->layer_b + ((size_t)layer * 3 + 0) * f;
-        const float *bod = w->layer_b + ((size_t)layer * 3 + 1) * f;
-        const float *bdd = w->layer_b + ((size_t)layer * 3 + 2) * f;
-        const float *as_oo = w->att_src + ((size_t)layer * 3 + 0) * f, *ad_oo = w->att_dst + ((size_t)layer * 3 + 0) * f;
-        const float *as_od = w->att_src + ((size_t)layer * 3 + 1) * f, *ad_od = w->att_dst + ((size_t)layer * 3 + 1) * f;
-        const float *as_dd = w->att_src + ((size_t)layer * 3 + 2) * f, *ad_dd = w->att_dst + ((size_t)layer * 3 + 2) * f;
+        const float *W[5], *bb[5], *as[5], *ad[5];
+        for (int r = 0; r < NR; ++r) {
+            W[r] = w->layer_w + ((size_t)layer * NR + r) * f * 2 * f;
+            bb[r] = w->layer_b + ((size_t)layer * NR + r) * f;
+            as[r] = w->att_src + ((size_t)layer * NR + r) * asz;
+            ad[r] = w->att_dst + ((size_t)layer * NR + r) * asz;
+        }
         double *alpha = (layer == 0) ? alpha_layer0 : NULL;
         const int64_t off1 = nn0, off2 = nn0 + nn1, off3 = nn0 + 2 * nn1;
-
         memset(nh_op, 0, sizeof(double) * (size_t)n_op * f);
         memset(nh_dev, 0, sizeof(double) * (size_t)n_dev * f);
-        apply_we(f, e_oo, Woo, boo, enc_oo, te_oo);
-        apply_we(f, e_dd, Wdd, bdd, enc_dd, te_dd);
-        apply_we(f, 2, Wod, bod, enc_od, te_od);
 
-        /* op <- op (tensor links) */
-        apply_wh(f, n_op, Woo, h_op, y_op, d->bf16);
-        for (int32_t u = 0; u < n_op; ++u)
-            aggregate_row(d, rp0[u], rp0[u + 1], c0, i0, y_op, y_op + (size_t)u * f, te_oo, NULL,
-                          as_oo, ad_oo, d->gamma_same, nh_op + (size_t)u * f, sm, ss, alpha);
-        /* placement links: W^h_od applies to both node types */
-        apply_wh(f, n_op, Wod, h_op, y2_op, d->bf16);
-        apply_wh(f, n_dev, Wod, h_dev, y2_dev, d->bf16);
-        for (int32_t u = 0; u < n_op; ++u)   /* op <- device */
-            aggregate_row(d, rp1[u], rp1[u + 1], c1, i1, y2_dev, y2_op + (size_t)u * f, te_od, bit_of,
-                          as_od, ad_od, d->gamma_cross, nh_op + (size_t)u * f, sm, ss,
-                          alpha ? alpha + (size_t)off1 * d->heads : NULL);
-        for (int32_t j = 0; j < n_dev; ++j)  /* device <- op */
-            aggregate_row(d, rp2[j], rp2[j + 1], c2, i2, y2_op, y2_dev + (size_t)j * f, te_od, bit_of,
-                          as_od, ad_od, d->gamma_cross, nh_dev + (size_t)j * f, sm, ss,
-                          alpha ? alpha + (size_t)off2 * d->heads : NULL);
-        /* device <- device (network links) */
-        apply_wh(f, n_dev, Wdd, h_dev, y_dev, d->bf16);
-        for (int32_t j = 0; j < n_dev; ++j)
-            aggregate_row(d, rp3[j], rp3[j + 1], c3, i3, y_dev, y_dev + (size_t)j * f, te_dd, NULL,
-                          as_dd, ad_dd, d->gamma_same, nh_dev + (size_t)j * f, sm, ss,
-                          alpha ? alpha + (size_t)off3 * d->heads : NULL);
+        if (NR == 3) {
+            /* op <- op (tensor links, both directions, one relation) */
+            apply_we(f, e_oo, W[0], bb[0], enc_oo, te_oo);
+            apply_wh(f, n_op, W[0], h_op, ys_op, d->bf16);
+            for (int32_t u = 0; u < n_op; ++u)
+                aggregate_row(d, rp0[u], rp0[u + 1], c0, i0, ys_op, ys_op + (size_t)u * f, te_oo, NULL,
+                              as[0], ad[0], d->gamma_same, nh_op + (size_t)u * f, sm, ss, alpha);
+            /* placement links: W^h_od applies to both node types */
+            apply_we(f, 2, W[1], bb[1], enc_od, te_od);
+            apply_wh(f, n_op, W[1], h_op, ys_op, d->bf16);
+            apply_wh(f, n_dev, W[1], h_dev, ys_dev, d->bf16);
+            for (int32_t u = 0; u < n_op; ++u)   /* op <- device */
+                aggregate_row(d, rp1[u], rp1[u + 1], c1, i1, ys_dev, ys_op + (size_t)u * f, te_od, bit_of,
+                              as[1], ad[1], d->gamma_cross, nh_op + (size_t)u * f, sm, ss,
+                              alpha ? alpha + (size_t)off1 * d->heads : NULL);
+            for (int32_t j = 0; j < n_dev; ++j)  /* device <- op */
+                aggregate_row(d, rp2[j], rp2[j + 1], c2, i2, ys_op, ys_dev + (size_t)j * f, te_od, bit_of,
+                              as[1], ad[1], d->gamma_cross, nh_dev + (size_t)j * f, sm, ss,
+                              alpha ? alpha + (size_t)off2 * d->heads : NULL);
+            /* device <- device (network links) */
+            apply_we(f, e_dd, W[2], bb[2], enc_dd, te_dd);
+            apply_wh(f, n_dev, W[2], h_dev, ys_dev, d->bf16);
+            for (int32_t j = 0; j < n_dev; ++j)
+                aggregate_row(d, rp3[j], rp3[j + 1], c3, i3, ys_dev, ys_dev + (size_t)j * f, te_dd, NULL,
+                              as[2], ad[2], d->gamma_same, nh_dev + (size_t)j * f, sm, ss,
+                              alpha ? alpha + (size_t)off3 * d->heads : NULL);
+        } else {
+            /* relation 0: op <- op along the tensor (row = consumer) */
+            apply_we(f, e_oo, W[0], bb[0], enc_oo, te_oo);
+            apply_wh(f, n_op, W[0], h_op, ys_op, d->bf16);
+            for (int32_t u = 0; u < n_op; ++u)
+                aggregate_row(d, rpf[u], rpf[u + 1], cf, idf, ys_op, ys_op + (size_t)u * f, te_oo, NULL,
+                              as[0], ad[0], d->gamma_same, nh_op + (size_t)u * f, sm, ss, NULL);
+            /* relation 1: op <- op against the tensor (row = producer) */
+            apply_we(f, e_oo, W[1], bb[1], enc_oo, te_oo);
+            apply_wh(f, n_op, W[1], h_op, ys_op, d->bf16);
+            for (int32_t u = 0; u < n_op; ++u)
+                aggregate_row(d, rpb[u], rpb[u + 1], cb, idb, ys_op, ys_op + (size_t)u * f, te_oo, NULL,
+                              as[1], ad[1], d->gamma_same, nh_op + (size_t)u * f, sm, ss, NULL);
+            /* relation 2: op <- device (W_2 on device sources and op destinations) */
+            apply_we(f, 2, W[2], bb[2], enc_od, te_od);
+            apply_wh(f, n_dev, W[2], h_dev, ys_dev, d->bf16);
+            apply_wh(f, n_op, W[2], h_op, yd_op, d->bf16);
+            for (int32_t u = 0; u < n_op; ++u)
+                aggregate_row(d, rp1[u], rp1[u + 1], c1, i1, ys_dev, yd_op + (size_t)u * f, te_od, bit_of,
+                              as[2], ad[2], d->gamma_cross, nh_op + (size_t)u * f, sm, ss, NULL);
+            /* relation 3: device <- op (W_3 on op sources and device destinations) */
+            apply_we(f, 2, W[3], bb[3], enc_od, te_od);
+            apply_wh(f, n_op, W[3], h_op, ys_op, d->bf16);
+            apply_wh(f, n_dev, W[3], h_dev, yd_dev, d->bf16);
+            for (int32_t j = 0; j < n_dev; ++j)
+                aggregate_row(d, rp2[j], rp2[j + 1], c2, i2, ys_op, yd_dev + (size_t)j * f, te_od, bit_of,
+                              as[3], ad[3], d->gamma_cross, nh_dev + (size_t)j * f, sm, ss, NULL);
+            /* relation 4: device <- device */
+            apply_we(f, e_dd, W[4], bb[4], enc_dd, te_dd);
+            apply_wh(f, n_dev, W[4], h_dev, ys_dev, d->bf16);
+            for (int32_t j = 0; j < n_dev; ++j)
+                aggregate_row(d, rp3[j], rp3[j + 1], c3, i3, ys_dev, ys_dev + (size_t)j * f, te_dd, NULL,
+                              as[4], ad[4], d->gamma_same, nh_dev + (size_t)j * f, sm, ss, NULL);
+        }
         memcpy(h_op, nh_op, sizeof(double) * (size_t)n_op * f);
         memcpy(h_dev, nh_dev, sizeof(double) * (size_t)n_dev * f);
     }
@@ -389,9 +477,10 @@ int tago_forward(const tago_dims *d,
 
 done:
     free(rp0); free(rp1); free(rp2); free(rp3); free(c0); free(i0); free(c1); free(i1);
-    free(c2); free(i2); free(c3); free(i3); free(h_op); free(h_dev); free(nh_op); free(nh_dev);
-    free(y_op); free(y_dev); free(enc_oo); free(enc_dd); free(enc_od); free(te_oo); free(te_dd);
-    free(te_od); free(y2_op); free(y2_dev); free(sm); free(ss); free(xbit); free(bit_of);
+    free(c2); free(i2); free(c3); free(i3); free(rpf); free(rpb); free(cf); free(idf); free(cb); free(idb);
+    free(h_op); free(h_dev); free(nh_op); free(nh_dev);
+    free(ys_op); free(ys_dev); free(yd_op); free(yd_dev); free(enc_oo); free(enc_dd); free(enc_od); free(te_oo);
+    free(te_dd); free(te_od); free(sm); free(ss); free(xbit); free(bit_of);
     return st;
 }
 

@@ -461,15 +461,20 @@ def _glorot(rng, rows, cols):
 
 
 def make_weights(f: int, heads: int, layers: int, f_op: int, dec_hidden: int,
-                 bias_scale: float = 0.1, seed_extra: int = 0) -> Dict[str, np.ndarray]:
+                 bias_scale: float = 0.1, seed_extra: int = 0, relations: int = 3,
+                 heads_mode: str = "concat") -> Dict[str, np.ndarray]:
     """All parameters, float32, in the library's documented layouts:
     enc_op_w [f, f_op], enc_op_b [f], enc_dev_w [f, 8], enc_dev_b [f],
     enc_edge_w{r} [f, d_r], enc_edge_b{r} [f],
-    layer_w [L, 3, f, 2f] (= [W^h | W^e] per relation), layer_b [L, 3, f],
-    att_src [L, 3, f], att_dst [L, 3, f],
+    layer_w [L, R, f, 2f] (= [W^h | W^e] per relation), layer_b [L, R, f],
+    att_src [L, R, f], att_dst [L, R, f] (heads_mode "avg": [L, R, K, f]),
     dec_w1 [H, 2f+4], dec_b1 [H], dec_w2 [H], dec_b2 [1] (H = dec_hidden > 0)
-    or dec_w2 [2f+4], dec_b2 [1] (linear decoder, H = 0)."""
-    d = f // heads
+    or dec_w2 [2f+4], dec_b2 [1] (linear decoder, H = 0).  R = relations
+    (3 undirected link types, or 5 directed relations); the first three
+    relations draw the same numbers whatever R is."""
+    avg = heads_mode == "avg"
+    d = f if avg else f // heads
+    R = relations
     w: Dict[str, np.ndarray] = {}
     r0 = rng_for(WEIGHT_STREAM, 100, seed_extra)
     w["enc_op_w"] = _glorot(r0, f, f_op)
@@ -479,18 +484,19 @@ def make_weights(f: int, heads: int, layers: int, f_op: int, dec_hidden: int,
     for r, dr in enumerate(EDGE_DIMS):
         w[f"enc_edge_w{r}"] = _glorot(r0, f, dr)
         w[f"enc_edge_b{r}"] = (r0.uniform(-1, 1, f) * bias_scale).astype(np.float32)
-    lw = np.zeros((layers, 3, f, 2 * f), np.float32)
-    lb = np.zeros((layers, 3, f), np.float32)
-    asrc = np.zeros((layers, 3, f), np.float32)
-    adst = np.zeros((layers, 3, f), np.float32)
+    lw = np.zeros((layers, R, f, 2 * f), np.float32)
+    lb = np.zeros((layers, R, f), np.float32)
+    ashape = (layers, R, heads, f) if avg else (layers, R, f)
+    asrc = np.zeros(ashape, np.float32)
+    adst = np.zeros(ashape, np.float32)
     for layer in range(layers):
-        for r in range(3):
+        for r in range(R):
             rg = rng_for(WEIGHT_STREAM, layer, r, seed_extra)
             lw[layer, r] = _glorot(rg, f, 2 * f)
             lb[layer, r] = rg.uniform(-1, 1, f) * bias_scale
             lim = math.sqrt(6.0 / (d + 1))
-            asrc[layer, r] = rg.uniform(-lim, lim, f)
-            adst[layer, r] = rg.uniform(-lim, lim, f)
+            asrc[layer, r] = rg.uniform(-lim, lim, ashape[2:])
+            adst[layer, r] = rg.uniform(-lim, lim, ashape[2:])
     w["layer_w"], w["layer_b"], w["att_src"], w["att_dst"] = lw, lb, asrc, adst
     rd = rng_for(WEIGHT_STREAM, 200, seed_extra)
     din = 2 * f + 4

@@ -272,11 +272,17 @@ def test_identical_messages_ignore_attention(orc):
     np.testing.assert_allclose(np.vstack([E_op, E_dev]), want, rtol=0, atol=1e-15)
 
 
-def _dense_forward(topo, x_op, x_dev, x_oo, x_dd, x_od, w, f, heads, layers, slope=0.2):
+def _dense_forward(topo, x_op, x_dev, x_oo, x_dd, x_od, w, f, heads, layers, slope=0.2, relations=3,
+                   edge_act="affine", heads_mode="concat"):
     """Independent dense formulation: masked (dst x src x f) message tensors,
-    -inf-masked softmax over the source axis, einsum aggregation."""
+    -inf-masked softmax over the source axis, einsum aggregation.  Variants:
+    5 directed relations (op<-op along / against the tensor as separate
+    relations with their own parameters and softmax, op<-device and
+    device<-op separate), ReLU after the edge encoders, K full-width heads
+    averaged."""
     n, m = topo.n_op, topo.n_dev
-    d = f // heads
+    avg = heads_mode == "avg"
+    d = f if avg else f // heads
     relu = lambda t: np.maximum(t, 0)
     W = w["layer_w"].astype(np.float64)
     h_op = relu(x_op.astype(np.float64) @ w["enc_op_w"].T.astype(np.float64) + w["enc_op_b"])
@@ -287,11 +293,15 @@ def _dense_forward(topo, x_op, x_dev, x_oo, x_dd, x_od, w, f, heads, layers, slo
         c = w[f"enc_edge_b{r}"].astype(np.float64)
         T = np.full((nd, ns, f), np.nan)
         for (dst, src), x in zip(pairs, feats):
-            T[dst, src] = A @ np.atleast_1d(np.asarray(x, np.float64)) + c
+            e = A @ np.atleast_1d(np.asarray(x, np.float64)) + c
+            T[dst, src] = relu(e) if edge_act == "relu" else e
         return T
-    oo_pairs = list(zip(topo.oo_dst, topo.oo_src)) + list(zip(topo.oo_src, topo.oo_dst))
-    oo_feat = list(x_oo) + list(x_oo)
-    E0 = etensor(n, n, oo_pairs, oo_feat, 0)
+    fwd = list(zip(topo.oo_dst, topo.oo_src))     # consumer <- producer
+    bwd = list(zip(topo.oo_src, topo.oo_dst))     # producer <- consumer
+    if relations == 3:
+        E0 = [etensor(n, n, fwd + bwd, list(x_oo) + list(x_oo), 0)]
+    else:
+        E0 = [etensor(n, n, fwd, list(x_oo), 0), etensor(n, n, bwd, list(x_oo), 0)]
     E1 = etensor(n, m, list(zip(topo.od_op, topo.od_dev)), list(x_od.astype(np.float64)), 1)
     E2 = etensor(m, n, list(zip(topo.od_dev, topo.od_op)), list(x_od.astype(np.float64)), 1)
     dd_pairs = list(zip(topo.dd_a, topo.dd_b)) + list(zip(topo.dd_b, topo.dd_a))
@@ -300,15 +310,16 @@ def _dense_forward(topo, x_op, x_dev, x_oo, x_dd, x_od, w, f, heads, layers, slo
     def bucket(hs, hd, E, l, r):
         Wh, We = W[l, r, :, :f], W[l, r, :, f:]
         b = w["layer_b"][l, r].astype(np.float64)
-        a = w["att_src"][l, r].astype(np.float64)
-        ad = w["att_dst"][l, r].astype(np.float64)
         mask = ~np.isnan(E[..., 0])
         Ys, Yd = hs @ Wh.T, hd @ Wh.T
         Z = Ys[None, :, :] + np.einsum("dsk,ck->dsc", np.nan_to_num(E), We) + b
         M = relu(Z)
         out = np.zeros((hd.shape[0], f))
         for k in range(heads):
-            sl = slice(k * d, (k + 1) * d)
+            sl = slice(0, f) if avg else slice(k * d, (k + 1) * d)
+            a = w["att_src"][l, r][k] if avg else w["att_src"][l, r]
+            ad = w["att_dst"][l, r][k] if avg else w["att_dst"][l, r]
+            a, ad = a.astype(np.float64), ad.astype(np.float64)
             s = np.einsum("dsc,c->ds", M[:, :, sl], a[sl]) + (Yd[:, sl] @ ad[sl])[:, None]
             s = np.where(s > 0, s, slope * s)
             s = np.where(mask, s, -np.inf)
@@ -317,12 +328,17 @@ def _dense_forward(topo, x_op, x_dev, x_oo, x_dd, x_od, w, f, heads, layers, slo
             p = np.where(mask, np.exp(s - mx), 0.0)
             z = p.sum(axis=1, keepdims=True)
             al = np.divide(p, z, out=np.zeros_like(p), where=z > 0)
-            out[:, sl] = np.einsum("ds,dsc->dc", al, M[:, :, sl])
+            out[:, sl] += np.einsum("ds,dsc->dc", al, M[:, :, sl]) / (heads if avg else 1)
         return out
 
     for l in range(layers):
-        n_op_new = bucket(h_op, h_op, E0, l, 0) + 0.1 * bucket(h_dev, h_op, E1, l, 1)
-        n_dev_new = 0.1 * bucket(h_op, h_dev, E2, l, 1) + bucket(h_dev, h_dev, E3, l, 2)
+        if relations == 3:
+            n_op_new = bucket(h_op, h_op, E0[0], l, 0) + 0.1 * bucket(h_dev, h_op, E1, l, 1)
+            n_dev_new = 0.1 * bucket(h_op, h_dev, E2, l, 1) + bucket(h_dev, h_dev, E3, l, 2)
+        else:
+            n_op_new = (bucket(h_op, h_op, E0[0], l, 0) + bucket(h_op, h_op, E0[1], l, 1)
+                        + 0.1 * bucket(h_dev, h_op, E1, l, 2))
+            n_dev_new = 0.1 * bucket(h_op, h_dev, E2, l, 3) + bucket(h_dev, h_dev, E3, l, 4)
         h_op, h_dev = n_op_new, n_dev_new
     return h_op, h_dev
 
@@ -338,6 +354,165 @@ def test_dense_recomputation(orc, seed, n, m, e, per, f, heads, layers):
     R_op, R_dev = _dense_forward(topo, *x, w, f, heads, layers)
     np.testing.assert_allclose(E_op, R_op, rtol=0, atol=1e-12)
     np.testing.assert_allclose(E_dev, R_dev, rtol=0, atol=1e-12)
+
+
+# ---------------------------------------- variants of the layer readings ---
+
+VARIANTS = [(5, "affine", "concat"), (3, "relu", "concat"), (3, "affine", "avg"), (5, "relu", "avg")]
+
+
+@pytest.mark.parametrize("relations,edge_act,heads_mode", VARIANTS)
+@pytest.mark.parametrize("seed,n,m,e,per,f,heads,layers", [
+    (0, 12, 3, 20, None, 8, 2, 2), (1, 20, 4, 35, 2, 16, 4, 3), (3, 24, 4, 60, 3, 32, 4, 2)])
+def test_variants_dense_recomputation(orc, relations, edge_act, heads_mode, seed, n, m, e, per, f, heads, layers):
+    """Each reading the paper leaves open (directed relations, ReLU edge
+    encoders, averaged full-width heads) against the independent dense
+    formulation."""
+    topo = synth.random_topology(170 + seed, n, m, e, od_per_op=per, dd_density=0.7)
+    w = synth.make_weights(f, heads, layers, 42, 0, bias_scale=0.3, seed_extra=seed, relations=relations,
+                           heads_mode=heads_mode)
+    x = random_features(topo, 42, 130 + seed)
+    kw = dict(relations=relations, edge_act=edge_act, heads_mode=heads_mode)
+    E_op, E_dev = orc.forward(topo, *x, w, f=f, heads=heads, layers=layers, **kw)
+    R_op, R_dev = _dense_forward(topo, *x, w, f, heads, layers, **kw)
+    np.testing.assert_allclose(E_op, R_op, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(E_dev, R_dev, rtol=0, atol=1e-12)
+    # the variant changes the result (it is not silently the default)
+    D_op, _ = orc.forward(topo, *x, synth.make_weights(f, heads, layers, 42, 0, bias_scale=0.3, seed_extra=seed),
+                          f=f, heads=heads, layers=layers)
+    assert np.abs(E_op - D_op).max() > 1e-6
+
+
+def test_directed_relations_reduce_on_a_bipartite_dag(orc):
+    """Two op layers (producers 0..4, consumers 5..11): every op row has
+    links in one direction only, so with the forward and backward relations
+    sharing the op-op parameters and op<-device / device<-op sharing the
+    placement parameters, the directed reading equals the undirected one."""
+    rng = np.random.default_rng(9)
+    pairs = sorted({(int(p), int(c)) for p, c in zip(rng.integers(0, 5, 30), rng.integers(5, 12, 30))})
+    topo = mk_topo(12, 3, oo=pairs, dd=[(0, 1), (1, 2)])
+    f, heads, layers = 16, 4, 2
+    w3 = synth.make_weights(f, heads, layers, 42, 0, bias_scale=0.3)
+    w5 = dict(w3)
+    for k in ("layer_w", "layer_b", "att_src", "att_dst"):
+        w5[k] = np.ascontiguousarray(w3[k][:, [0, 0, 1, 1, 2]])
+    x = random_features(topo, 42, 12)
+    A = orc.forward(topo, *x, w3, f=f, heads=heads, layers=layers)
+    B = orc.forward(topo, *x, w5, f=f, heads=heads, layers=layers, relations=5)
+    for a, b in zip(A, B):
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-13)
+    # a chain has both directions at its inner ops: there the readings differ
+    chain = mk_topo(12, 3, oo=[(i, i + 1) for i in range(11)], dd=[(0, 1), (1, 2)])
+    xc = random_features(chain, 42, 13)
+    C3 = orc.forward(chain, *xc, w3, f=f, heads=heads, layers=layers)[0]
+    C5 = orc.forward(chain, *xc, w5, f=f, heads=heads, layers=layers, relations=5)[0]
+    assert np.abs(C3 - C5).max() > 1e-6
+
+
+def test_directed_relation_transforms_are_applied_per_direction(orc):
+    """Uniform attention, W^e = 0, b = 0, W^h_r a distinct permutation per
+    relation: one layer gives H' = sum_r gamma_r P_r H Pi_r^T with P_r the
+    row-normalised adjacency of relation r (forward: consumer <- producer;
+    backward: producer <- consumer); catches swapped directions or
+    relations."""
+    f = 8
+    topo = synth.random_topology(31, 12, 3, 20, dd_density=1.0)
+    w = zero_weights(f, 1, f)
+    _identity_encoders(w, f)
+    w["layer_w"] = np.zeros((1, 5, f, 2 * f), np.float32)
+    for k in ("layer_b", "att_src", "att_dst"):
+        w[k] = np.zeros((1, 5, f), np.float32)
+    perms = [np.roll(np.eye(f), s, axis=0)[:, np.random.default_rng(s).permutation(f)] for s in range(1, 6)]
+    for r in range(5):
+        w["layer_w"][0, r, :, :f] = perms[r]
+    x_op, x_dev, x_oo, x_dd, x_od = random_features(topo, f, 7, nonneg=True)
+    E_op, E_dev = orc.forward(topo, x_op, x_dev, x_oo, x_dd, x_od, w, f=f, heads=4, layers=1, relations=5)
+    n, m = topo.n_op, topo.n_dev
+    Af, Ab = np.zeros((n, n)), np.zeros((n, n))
+    for p, c in zip(topo.oo_src, topo.oo_dst):
+        Af[c, p] = 1
+        Ab[p, c] = 1
+    Aod, Ado = np.zeros((n, m)), np.zeros((m, n))
+    for u, j in zip(topo.od_op, topo.od_dev):
+        Aod[u, j] = 1
+        Ado[j, u] = 1
+    Add = np.zeros((m, m))
+    for a, b in zip(topo.dd_a, topo.dd_b):
+        Add[a, b] = Add[b, a] = 1
+    Ho, Hd = x_op.astype(np.float64), x_dev.astype(np.float64)
+    want_op = (_rownorm(Af) @ Ho @ perms[0].T + _rownorm(Ab) @ Ho @ perms[1].T
+               + 0.1 * _rownorm(Aod) @ Hd @ perms[2].T)
+    want_dev = 0.1 * _rownorm(Ado) @ Ho @ perms[3].T + _rownorm(Add) @ Hd @ perms[4].T
+    np.testing.assert_allclose(E_op, want_op, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(E_dev, want_dev, rtol=0, atol=1e-12)
+
+
+def test_relu_edge_encoder_special_cases(orc):
+    """ReLU after the edge encoders: with encoder biases that keep every
+    pre-activation positive it is the identity (equals the affine reading);
+    with encoder rows A = -1, c = 0 and non-negative raw features every edge
+    vector is zero, so each message is ReLU(W^h h_v + b) alone."""
+    topo = synth.random_topology(44, 16, 4, 30, od_per_op=2, dd_density=0.8)
+    f, heads, layers = 16, 4, 2
+    w = synth.make_weights(f, heads, layers, 42, 0, bias_scale=0.3)
+    x = random_features(topo, 42, 8, nonneg=True)
+    wp = dict(w)
+    for r in range(3):
+        wp[f"enc_edge_b{r}"] = w[f"enc_edge_b{r}"] + 50.0
+    A = orc.forward(topo, *x, wp, f=f, heads=heads, layers=layers)
+    B = orc.forward(topo, *x, wp, f=f, heads=heads, layers=layers, edge_act="relu")
+    for a, b in zip(A, B):
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
+    wn = dict(w)
+    for r in range(3):
+        wn[f"enc_edge_w{r}"] = -np.ones_like(w[f"enc_edge_w{r}"])
+        wn[f"enc_edge_b{r}"] = np.zeros_like(w[f"enc_edge_b{r}"])
+    wz = dict(wn)
+    wz["layer_w"] = w["layer_w"].copy()
+    wz["layer_w"][:, :, :, f:] = 0.0      # no edge term at all
+    C = orc.forward(topo, *x, wn, f=f, heads=heads, layers=layers, edge_act="relu")
+    D = orc.forward(topo, *x, wz, f=f, heads=heads, layers=layers)
+    for a, b in zip(C, D):
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
+    E = orc.forward(topo, *x, wn, f=f, heads=heads, layers=layers)   # affine: the negative edge vectors count
+    assert np.abs(E[0] - C[0]).max() > 1e-6
+
+
+def test_averaged_heads_special_cases(orc):
+    """K full-width heads averaged: one head is one concatenated head of f
+    channels; K identical heads equal one head; with zero attention vectors
+    every head is uniform and the layer is the gamma-weighted mean
+    aggregation of the messages."""
+    topo = synth.random_topology(52, 14, 3, 26, od_per_op=2, dd_density=0.7)
+    f, layers = 16, 2
+    w1 = synth.make_weights(f, 1, layers, 42, 0, bias_scale=0.3)
+    x = random_features(topo, 42, 5)
+    A = orc.forward(topo, *x, w1, f=f, heads=1, layers=layers)
+    wa = dict(w1)
+    wa["att_src"] = w1["att_src"][:, :, None, :].copy()
+    wa["att_dst"] = w1["att_dst"][:, :, None, :].copy()
+    B = orc.forward(topo, *x, wa, f=f, heads=1, layers=layers, heads_mode="avg")
+    for a, b in zip(A, B):
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-14)
+    wk = dict(w1)
+    wk["att_src"] = np.repeat(w1["att_src"][:, :, None, :], 4, axis=2)
+    wk["att_dst"] = np.repeat(w1["att_dst"][:, :, None, :], 4, axis=2)
+    C = orc.forward(topo, *x, wk, f=f, heads=4, layers=layers, heads_mode="avg")
+    for a, b in zip(A, C):
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-13)
+    # uniform attention in every head: mean aggregation of ReLU(W^h h + W^e e + b)
+    f8 = 8
+    wu = zero_weights(f8, 1, f8)
+    _identity_encoders(wu, f8)
+    wu["layer_w"][0, :, :, :f8] = np.eye(f8)
+    wu["att_src"] = np.zeros((1, 3, 4, f8), np.float32)
+    wu["att_dst"] = np.zeros((1, 3, 4, f8), np.float32)
+    xu = random_features(topo, f8, 6, nonneg=True)
+    E_op, E_dev = orc.forward(topo, *xu, wu, f=f8, heads=4, layers=1, heads_mode="avg")
+    Aj = _adjacency(topo)
+    Pm = _rownorm(Aj[0]) + 0.1 * _rownorm(Aj[1]) + _rownorm(Aj[2])
+    H = Pm @ np.vstack([xu[0], xu[1]]).astype(np.float64)
+    np.testing.assert_allclose(np.vstack([E_op, E_dev]), H, rtol=0, atol=1e-12)
 
 
 def test_relabelling_equivariance(orc):
