@@ -158,6 +158,20 @@ typedef struct tag_model_dims {
     float gamma_same, gamma_cross, leaky_slope;
     int32_t sigma;   /* message non-linearity: 0 ReLU (default), 1 ELU with   */
                      /* alpha = 1 (a variant; needs dtype TAG_F32)           */
+    /* Readings of Section 4.2.1 that the paper leaves open.  0 = default.  */
+    /* The three variants run on a generic fp32 path (dtype TAG_F32, ReLU   */
+    /* messages, no training step).                                         */
+    int32_t relations;  /* 0 or 3: three undirected link types (R = 3).     */
+                        /* 5: directed relations (R = 5) in this order:     */
+                        /* op<-op along the tensor (row = consumer), op<-op */
+                        /* against it (row = producer), op<-device,         */
+                        /* device<-op, device<-device; each has its own W,  */
+                        /* b, a, adst and softmax; gamma as for its types.  */
+    int32_t edge_act;   /* 0: affine edge encoders e = A x + c;             */
+                        /* 1: e = ReLU(A x + c)                             */
+    int32_t head_mode;  /* 0: K concatenated heads of f/K channels;         */
+                        /* 1: K heads over all f channels, each with its    */
+                        /* own attention vectors, averaged (K <= 8)         */
 } tag_model_dims;
 
 /*
@@ -167,12 +181,15 @@ typedef struct tag_model_dims {
  *   enc_edge_w[r] [f][d_r], enc_edge_b[r] [f]  edge encoder of relation r,
  *                                           e = A x + c (no activation);
  *                                           d = 1 (oo), 1 (od), 2 (dd)
- *   layer_w [L][3][f][2f]                   W_{l,r} = [W^h | W^e] acting on
+ *   layer_w [L][R][f][2f]                   W_{l,r} = [W^h | W^e] acting on
  *                                           the concatenation [h_v ; e_uv]
- *   layer_b [L][3][f]                       b_{l,r}
- *   att_src [L][3][f]                       message attention vector a_{l,r}
- *   att_dst [L][3][f]                       destination attention vector,
- *                                           applied to W^h_{l,r} h_u
+ *                                           (R = 3, or 5 with relations = 5)
+ *   layer_b [L][R][f]                       b_{l,r}
+ *   att_src [L][R][f]                       message attention vector a_{l,r}
+ *                                           ([L][R][K][f] with head_mode = 1)
+ *   att_dst [L][R][f]                       destination attention vector,
+ *                                           applied to W^h_{l,r} h_u (same
+ *                                           shape as att_src)
  *   dec_w1 [H][2f+4], dec_b1 [H], dec_w2 [H], dec_b2 [1]   decoder (H > 0)
  *   dec_w2 [2f+4], dec_b2 [1]               decoder (H = 0; w1, b1 unused)
  * Decoder input order: [sum_j P_ij E_dev[j] ; E_op[i] ; onehot(option)].

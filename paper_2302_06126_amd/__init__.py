@@ -213,15 +213,19 @@ class Model:
     def __init__(self, weights: Dict[str, np.ndarray], *, f: int, heads: int, layers: int, f_op: int,
                  f_dev: int = 8, dec_hidden: Optional[int] = None, dtype: str = "f32",
                  gamma_same: float = 1.0, gamma_cross: float = 0.1, leaky_slope: float = 0.2,
-                 device: str = "cuda", sigma: str = "relu"):
+                 device: str = "cuda", sigma: str = "relu", relations: int = 3, edge_act: str = "affine",
+                 heads_mode: str = "concat"):
         torch = _torch()
         if dec_hidden is None:
             dec_hidden = int(weights["dec_w1"].shape[0])
         if sigma not in ("relu", "elu"):
             raise ValueError("sigma must be 'relu' or 'elu'")
+        if relations not in (3, 5) or edge_act not in ("affine", "relu") or heads_mode not in ("concat", "avg"):
+            raise ValueError("relations must be 3 or 5, edge_act 'affine' or 'relu', heads_mode 'concat' or 'avg'")
         self.dims = tag_model_dims(f, heads, layers, f_op, f_dev, dec_hidden,
                                    TAG_BF16 if dtype == "bf16" else TAG_F32,
-                                   gamma_same, gamma_cross, leaky_slope, 1 if sigma == "elu" else 0)
+                                   gamma_same, gamma_cross, leaky_slope, 1 if sigma == "elu" else 0,
+                                   relations, 1 if edge_act == "relu" else 0, 1 if heads_mode == "avg" else 0)
         self.t = {k: torch.from_numpy(np.ascontiguousarray(v, np.float32).reshape(-1).copy()).to(device)
                   for k, v in weights.items()}
         # non-empty placeholders keep every pointer valid

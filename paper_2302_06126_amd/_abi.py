@@ -63,7 +63,8 @@ class tag_model_dims(C.Structure):
     _fields_ = [("f", C.c_int32), ("heads", C.c_int32), ("layers", C.c_int32), ("f_op", C.c_int32),
                 ("f_dev", C.c_int32), ("dec_hidden", C.c_int32), ("dtype", C.c_int32),
                 ("gamma_same", C.c_float), ("gamma_cross", C.c_float), ("leaky_slope", C.c_float),
-                ("sigma", C.c_int32)]
+                ("sigma", C.c_int32), ("relations", C.c_int32), ("edge_act", C.c_int32),
+                ("head_mode", C.c_int32)]
 
 
 class tag_weights(C.Structure):

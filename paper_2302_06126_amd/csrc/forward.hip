@@ -357,7 +357,7 @@ tag_status check_dims(const tag_model_dims *d) {
         TAG_FAIL(TAG_EINVAL, "leaky_slope must be in [0, 1]");
     if (d->sigma != 0 && d->sigma != 1) TAG_FAIL(TAG_EINVAL, "sigma must be 0 (ReLU) or 1 (ELU)");
     if (d->sigma == 1 && d->dtype != TAG_F32) TAG_FAIL(TAG_ESHAPE, "the ELU variant needs the fp32 variant");
-    return TAG_OK;
+    return check_variant(d);
 }
 
 size_t carve_fwd(const tag_graph *g, const tag_model_dims *d, int32_t R, void *base, FwdLayout *L) {
@@ -401,6 +401,10 @@ extern "C" tag_status tag_gnn_workspace(const tag_graph *g, const tag_model_dims
     tag_status st = check_dims(dims);
     if (st != TAG_OK) return st;
     if (n_replicas < 1) TAG_FAIL(TAG_EINVAL, "n_replicas must be >= 1");
+    if (is_variant(dims)) {
+        *bytes = variant_workspace(g, dims, n_replicas);
+        return TAG_OK;
+    }
     FwdLayout L;
     *bytes = carve_fwd(g, dims, n_replicas, nullptr, &L);
     return TAG_OK;
@@ -480,6 +484,10 @@ tag_status forward_run(const tag_graph *g, const tag_model_dims *dims, const tag
          reinterpret_cast<uintptr_t>(E_dev) | reinterpret_cast<uintptr_t>(w->layer_w) |
          reinterpret_cast<uintptr_t>(workspace)) & 15)
         TAG_FAIL(TAG_EINVAL, "x_op, E_op, E_dev, layer_w and workspace must be 16-byte aligned");
+    if (is_variant(dims)) {
+        if (save) TAG_FAIL(TAG_ESHAPE, "saved activations need the default readings");
+        return forward_variant(g, dims, w, x, workspace, ws_bytes, E_op, E_dev, stream);
+    }
     FwdLayout L;
     if (carve_fwd(g, dims, R, nullptr, &L) > ws_bytes) TAG_FAIL(TAG_ENOSPACE, "workspace too small (see tag_gnn_workspace)");
     carve_fwd(g, dims, R, workspace, &L);

@@ -19,6 +19,15 @@ struct FwdLayout {
 };
 
 tag_status check_dims(const tag_model_dims *d);
+
+// The readings of variants.hip (five directed relations, ReLU edge
+// encoders, averaged full-width heads): generic fp32 forward path.
+bool is_variant(const tag_model_dims *d);
+tag_status check_variant(const tag_model_dims *d);
+size_t variant_workspace(const tag_graph *g, const tag_model_dims *d, int32_t R);
+tag_status forward_variant(const tag_graph *g, const tag_model_dims *dims, const tag_weights *w,
+                           const tag_features *x, void *workspace, size_t ws_bytes, float *E_op, float *E_dev,
+                           hipStream_t stream);
 size_t carve_fwd(const tag_graph *g, const tag_model_dims *d, int32_t R, void *base, FwdLayout *L);
 
 // Where a forward pass keeps every layer's activations (fp32): the input

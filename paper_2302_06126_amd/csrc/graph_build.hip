@@ -88,6 +88,7 @@ struct EdgeArgs {
     int32_t n_dev;             // total device rows (LDS counter range)
     Buckets B;
     int32_t *flags;
+    int32_t *oo_head;          // [E_oo] consumer (global op id) of each tensor link
 };
 
 // MODE 0: count degrees; MODE 1: scatter entries.  One thread per link.
@@ -148,6 +149,7 @@ __global__ void __launch_bounds__(kThreads) edges_pass(EdgeArgs A) {
         }
     }
     if (MODE == 1 && ok) {
+        if (r == 0) A.oo_head[i] = gb;   // the direction of each op<-op entry follows from it
         const int32_t p = A.B.rp[bk0][row0] + slot0;
         A.B.tcol[bk0][p] = col0; A.B.teid[bk0][p] = (int32_t)i; A.B.rowof[bk0][p] = row0;
         const int32_t q = A.B.rp[bk1][row1] + slot1;
@@ -441,6 +443,7 @@ int64_t count_groups(const tag_graph_desc *d) {
 // tiles [n_tiles][3] | groups [n_groups][2]
 struct CsrLayout {
     int32_t *rowptr[4], *col[4], *eid[4];
+    int32_t *oo_head;
     int32_t *meta;
     int32_t *op_off, *dev_off, *tile_off, *group_off, *tiles, *groups;
     size_t meta_ints;
@@ -462,6 +465,7 @@ size_t carve_csr(const Sizes &s, int64_t n_tiles, int64_t n_groups, void *base, 
         L->col[b] = c.take<int32_t>(std::max<int64_t>(s.nnz[b], 1));
         L->eid[b] = c.take<int32_t>(std::max<int64_t>(s.nnz[b], 1));
     }
+    L->oo_head = c.take<int32_t>(std::max<int64_t>(s.e_oo, 1));
     const size_t nt = (size_t)std::max<int64_t>(n_tiles, 1);
     L->meta_ints = 4 * (size_t)(s.G + 1) + 3 * nt + 2 * (size_t)std::max<int64_t>(n_groups, 1);
     L->meta = c.take<int32_t>(L->meta_ints);
@@ -630,6 +634,7 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
     ea.n_dev = (int32_t)std::min<int64_t>(s.n_dev, kPrivRows);
     ea.B = B;
     ea.flags = tl.flags;
+    ea.oo_head = cl.oo_head;
     const int64_t *oo_off = tl.links, *dd_off = tl.links + (s.G + 1), *od_off = tl.links + 2 * (s.G + 1);
     // op->op: (row = consumer, col = producer) and the reverse, both into B0
     ea.rel[0] = Rel{desc->oo_src, desc->oo_dst, oo_off, cl.op_off, cl.op_off, s.e_oo, 1, 0, 0, 0, 0};
@@ -682,6 +687,7 @@ extern "C" tag_status tag_graph_build(const tag_graph_desc *desc, void *csr_buf,
         g->eid[b] = cl.eid[b];
         g->max_degree[b] = flags[FLAG_MAXDEG + b];
     }
+    g->oo_head = cl.oo_head;
     g->op_off_d = cl.op_off;
     g->dev_off_d = cl.dev_off;
     g->tiles_d = cl.tiles;

@@ -67,6 +67,7 @@ struct tag_graph {
     const int32_t *rowptr[4] = {nullptr, nullptr, nullptr, nullptr};
     const int32_t *col[4] = {nullptr, nullptr, nullptr, nullptr};
     const int32_t *eid[4] = {nullptr, nullptr, nullptr, nullptr};
+    const int32_t *oo_head = nullptr;    // [E_oo] global id of each tensor link's consumer
     const int32_t *op_off_d = nullptr;   // [G+1]
     const int32_t *dev_off_d = nullptr;  // [G+1]
     // op tiles: runs of at most kOpTile consecutive ops of one topology

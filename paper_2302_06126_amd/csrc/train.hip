@@ -2226,6 +2226,8 @@ tag_status check_train(const tag_graph *g, const tag_model_dims *dims, int32_t R
     tag_status st = check_dims(dims);
     if (st != TAG_OK) return st;
     if (dims->dtype != TAG_F32) TAG_FAIL(TAG_ESHAPE, "training supports the fp32 variant only");
+    if (is_variant(dims)) TAG_FAIL(TAG_ESHAPE, "training supports the default readings (3 relations, affine "
+                                               "edge encoders, concatenated heads) only");
     if (dims->dec_hidden < 1) TAG_FAIL(TAG_ESHAPE, "training needs the MLP decoder (dec_hidden >= 1)");
     if (R < 1 || S < 1 || Q < 1) TAG_FAIL(TAG_EINVAL, "need n_replicas, n_slices and n_query >= 1");
     if (S > 4096) TAG_FAIL(TAG_ESHAPE, "training supports at most 4096 slices");
