@@ -11,7 +11,9 @@ import ctypes as C
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libtag.so")
+# TAG_LIBRARY selects another build of the same sources (the CPU sanitizer
+# builds of paper_2302_06126_amd/sanitize.py); the default is the in-tree library
+LIB_PATH = os.environ.get("TAG_LIBRARY") or os.path.join(_HERE, "libtag.so")
 
 TAG_OK, TAG_EINVAL, TAG_ERANGE, TAG_EDUP, TAG_ESHAPE, TAG_ENOSPACE, TAG_EHIP = 0, -1, -2, -3, -4, -5, -6
 TAG_F32, TAG_BF16 = 0, 1
