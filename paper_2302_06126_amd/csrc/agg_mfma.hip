@@ -419,7 +419,12 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
     __shared__ float Ex[ECAP];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int32_t t = blockIdx.x, r = blockIdx.y;
+    // XCD-aware order: the hardware deals blocks to the XCDs round-robin; the
+    // swizzle gives each XCD a contiguous run of (candidate, tile) pairs, so a
+    // candidate's consecutive tiles -- whose op<-op sources overlap -- and its
+    // device message table share one L2
+    const uint32_t lb = xcd_swizzle(blockIdx.y * gridDim.x + blockIdx.x, gridDim.x * gridDim.y);
+    const int32_t t = (int32_t)(lb % gridDim.x), r = (int32_t)(lb / gridDim.x);
     const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1], g = A.tiles[3 * t + 2];
     const int32_t d0 = A.dev_off[g], Mg = A.dev_off[g + 1] - d0;
     const float *xo = A.x_oo + (int64_t)r * A.s_oo;
