@@ -411,7 +411,7 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
     constexpr int OS = F + 4;                // LDS tile row stride
     constexpr int ECAP = F >= 256 ? 512 : 192;   // op<-op entries staged in LDS per chunk (192 keeps
                                                  // four blocks per CU at f = 128)
-    __shared__ float Ot[kOpTile * OS];
+    __shared__ __attribute__((aligned(16))) float Ot[kOpTile * OS];
     __shared__ uint64_t pres[kOpTile], bits[kOpTile];
     __shared__ float qo[kOpTile][K], mxS[kOpTile][K];
     __shared__ float P[64][2][K];
@@ -779,21 +779,37 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const float zv = __shfl(z, 4 * (lane >> 4) + v, 64);
-                scale[hh][v] = zv > 0.f ? A.g_cross / zv : 0.f;
+                scale[hh][v] = zv > 0.f ? A.g_cross * __builtin_amdgcn_rcpf(zv) : 0.f;
             }
         }
+        // the op<-device part is added into the LDS tile in place (each
+        // (row, column) belongs to one lane)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
             const int u = rb * 16 + 4 * (lane >> 4) + v;
-            if (u >= nu) continue;
-            const int64_t row = (int64_t)r * A.n_op + u0 + u;
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) {
                 const int col = cbase + cb * 16 + (lane & 15);
-                const float val = fmaf(scale[cb / CPH][v], acc[rb][cb][v], Ot[u * OS + col]);
-                if (A.out_f32) static_cast<float *>(A.H_op)[row * F + col] = val;
-                else static_cast<uint16_t *>(A.H_op)[row * F + col] = f2bf(val);
+                Ot[u * OS + col] = fmaf(scale[cb / CPH][v], acc[rb][cb][v], Ot[u * OS + col]);
             }
+        }
+    }
+    __syncthreads();
+    // whole rows leave in 16-byte stores: 4 floats (last layer) or 8 bf16
+    if (A.out_f32) {
+        float *out = static_cast<float *>(A.H_op) + ((int64_t)r * A.n_op + u0) * F;
+        for (int idx = tid; idx < nu * (F / 4); idx += 256) {
+            const int u = idx / (F / 4), c = (idx % (F / 4)) * 4;
+            *reinterpret_cast<float4 *>(out + (int64_t)u * F + c) = *reinterpret_cast<const float4 *>(&Ot[u * OS + c]);
+        }
+    } else {
+        uint16_t *out = static_cast<uint16_t *>(A.H_op) + ((int64_t)r * A.n_op + u0) * F;
+        for (int idx = tid; idx < nu * (F / 8); idx += 256) {
+            const int u = idx / (F / 8), c = (idx % (F / 8)) * 8;
+            const float4 a = *reinterpret_cast<const float4 *>(&Ot[u * OS + c]);
+            const float4 b = *reinterpret_cast<const float4 *>(&Ot[u * OS + c + 4]);
+            *reinterpret_cast<u4v *>(out + (int64_t)u * F + c) =
+                u4v{pack_bf2(a.x, a.y), pack_bf2(a.z, a.w), pack_bf2(b.x, b.y), pack_bf2(b.z, b.w)};
         }
     }
 }
