@@ -19,13 +19,13 @@ __device__ __forceinline__ bf8 as_bf8(unsigned w0, unsigned w1, unsigned w2, uns
 }
 
 // acc += A B for fp32 operands given as exact three-way bf16 splits
-// (split3): the eight part products a_i b_j with i + j <= 3 on 16x16x32 bf16
-// MFMAs, smallest first.  Each part product is exact in fp32 and the one
-// dropped term a_2 b_2 is below 2^-32 |a b|, so the result is the fp32
-// contraction of A and B up to fp32 accumulation.
+// (split3, round-to-nearest-even parts: |a_1| <= 2^-8 |a|, |a_2| <= 2^-16 |a|):
+// the six part products a_i b_j with i + j <= 2 on 16x16x32 bf16 MFMAs,
+// smallest first.  Each part product is exact in fp32; the dropped terms
+// a_1 b_2, a_2 b_1 and a_2 b_2 add up to at most (2^-23 + 2^-32) |a b|, the
+// size of one fp32 rounding of the product, so the result is an fp32
+// contraction of A and B up to fp32 rounding.
 __device__ __forceinline__ f4 mfma_split3(const bf8 (&a)[3], const bf8 (&b)[3], f4 acc) {
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[2], b[1], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[1], b[2], acc, 0, 0, 0);
     acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[2], b[0], acc, 0, 0, 0);
     acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[1], b[1], acc, 0, 0, 0);
     acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[0], b[2], acc, 0, 0, 0);
