@@ -34,6 +34,29 @@ __device__ __forceinline__ f4 mfma_split3(const bf8 (&a)[3], const bf8 (&b)[3], 
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[0], b[0], acc, 0, 0, 0);
 }
 
+// Sparse 16x16x64 bf16 products (v_smfmac_f32_16x16x64_bf16).  A is 16 x 64
+// with at most two nonzeros in every four consecutive k, given as its eight
+// nonzero values per lane plus 2-bit positions; B is dense 64 x 16.  Lane
+// layout, lane l, g = l / 16: A row l % 16, value v at k = 16g + 4(v/2) + i_v
+// with i_v = bits 2v+1..2v of the index operand; B column l % 16, element t
+// at k = 8g + t (t < 8) or 32 + 8g + t - 8 (t >= 8); the result as for the
+// dense 16x16 products (row 4g + i in register i).
+typedef __bf16 bf16x16 __attribute__((ext_vector_type(16)));
+typedef unsigned u8v __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ bf16x16 as_bf16x16(const unsigned (&w)[8]) {
+    return __builtin_bit_cast(bf16x16, u8v{w[0], w[1], w[2], w[3], w[4], w[5], w[6], w[7]});
+}
+// mfma_split3 on the sparse products: the same six part products, with the
+// index operand shared by the three parts of A
+__device__ __forceinline__ f4 smfmac_split3(const bf8 (&a)[3], const bf16x16 (&b)[3], int idx, f4 acc) {
+    acc = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[2], b[0], acc, idx, 0, 0);
+    acc = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[1], b[1], acc, idx, 0, 0);
+    acc = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[0], b[2], acc, idx, 0, 0);
+    acc = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[1], b[0], acc, idx, 0, 0);
+    acc = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[0], b[1], acc, idx, 0, 0);
+    return __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[0], b[0], acc, idx, 0, 0);
+}
+
 // -------------------------------------------------------------- aggregation
 struct AggArgs {
     int32_t R;

@@ -397,7 +397,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
 //    registers) with the device message table.
 // Both parts are combined and each op row is written once.
 template <int F, int K, bool BF, bool ELU = false>
-__global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
+__global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile(AggArgs A) {
     constexpr int D = F / K;
     constexpr int WC = F / 4;
     constexpr int NCB = WC / 16;
@@ -625,30 +625,36 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
         for (int hh = 0; hh < HPW; ++hh) zl[rb][hh] = 0.f;
     }
     if constexpr (BF) {
-        // 16x16x32 bf16 products over the exact three-way splits of the fp32
-        // attention weights and message table (mfma_split3): k = 2j + b over
-        // the tile's devices; lane l supplies devices jb .. jb+3 (both bits)
-        // of a 32-wide step.  The next step's table parts load while the
-        // current step runs.
+        // sparse 16x16x64 bf16 products (smfmac_split3) over the exact
+        // three-way splits of the fp32 attention weights and message table:
+        // k = 2j + b over 32 devices per step.  An (op, device) link carries
+        // one bit, so each device's pair of k holds at most one nonzero
+        // weight: the 2:4 structure the sparse products take.  Lane group
+        // g = l / 16 gives the weights of devices 8g .. 8g+7 of a step (value v
+        // at position 2 (v % 2) + bit of its device pair's four k) and the
+        // table entries of devices 4g .. 4g+3 and 16+4g .. 16+4g+3 (both bits).
+        // Per step, the weights of one head for the four row blocks are formed
+        // first; the table parts then stream one 16-column block at a time,
+        // the next block's loads in flight while the current one is used.
         const unsigned *Tp = reinterpret_cast<const unsigned *>(A.T) + ((int64_t)r * A.n_dev + d0) * F;
         const int64_t tpart = (int64_t)A.R * A.n_dev * F;   // stride between the three parts
-        const int ksteps = (Mg + 15) / 16;
-        bf8 bops[2][NCB][3];
-        auto load_b = [&](int ks, bf8 (&bo)[NCB][3]) {
-            const int jb = 16 * ks + 4 * (lane >> 4);
+        const int ksteps = (Mg + 31) / 32;
+        auto load_b = [&](int ks, int cb, bf16x16 (&bo)[3]) {
+            const int jb = 32 * ks + 4 * (lane >> 4);
+            const int c = cbase + cb * 16 + (lane & 15);
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) {
-                const int c = cbase + cb * 16 + (lane & 15);
+            for (int z = 0; z < 3; ++z) {
+                unsigned w[8];
 #pragma unroll
-                for (int z = 0; z < 3; ++z) {
-                    unsigned w[4];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) w[q] = jb + q < Mg ? Tp[z * tpart + (int64_t)(jb + q) * F + c] : 0u;
-                    bo[cb][z] = as_bf8(w[0], w[1], w[2], w[3]);
+                for (int q = 0; q < 8; ++q) {
+                    const int j = jb + (q < 4 ? q : 12 + q);
+                    w[q] = j < Mg ? Tp[z * tpart + (int64_t)j * F + c] : 0u;
                 }
+                bo[z] = as_bf16x16(w);
             }
         };
-        load_b(0, bops[0]);
+        bf16x16 bops[2][3];
+        load_b(0, 0, bops[0]);
         __syncthreads();
         uint64_t prs[4], bts[4];
         float q2[4][HPW], m2[4][HPW];
@@ -663,42 +669,63 @@ __global__ void __launch_bounds__(256) agg_op_tile(AggArgs A) {
                 m2[rb][hh] = mxS[u][h0 + hh];
             }
         }
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            if (ks >= ksteps) break;
-            if (ks + 1 < ksteps) load_b(ks + 1, bops[(ks + 1) & 1]);
-            const int jb = 16 * ks + 4 * (lane >> 4);
-            float p0q[4][HPW], p1q[4][HPW];
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-#pragma unroll
-                for (int hh = 0; hh < HPW; ++hh) {
-                    p0q[q][hh] = P[jb + q][0][h0 + hh];
-                    p1q[q][hh] = P[jb + q][1][h0 + hh];
-                }
+#pragma unroll 1
+        for (int ks = 0; ks < ksteps; ++ks) {   // ksteps <= 2: a tile group holds at most 64 devices
+            const int jb = 32 * ks + 8 * (lane >> 4);
+            unsigned on8[4], bit8[4];
+            int idx[4];
 #pragma unroll
             for (int rb = 0; rb < 4; ++rb) {
+                // the lane's eight presence and bit flags (never set for jb + q >= Mg)
+                on8[rb] = (unsigned)(prs[rb] >> jb) & 0xffu;
+                bit8[rb] = (unsigned)(bts[rb] >> jb) & 0xffu;
+                // position of value q: 2 (q % 2) + bit, in bits 2q+1..2q
+                unsigned sb = (bit8[rb] | (bit8[rb] << 4)) & 0x0f0fu;
+                sb = (sb | (sb << 2)) & 0x3333u;
+                sb = (sb | (sb << 1)) & 0x5555u;
+                idx[rb] = (int)(0x8888u | sb);
+            }
 #pragma unroll
-                for (int hh = 0; hh < HPW; ++hh) {
+            for (int hh = 0; hh < HPW; ++hh) {
+                float p0q[8], p1q[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    p0q[q] = P[jb + q][0][h0 + hh];
+                    p1q[q] = P[jb + q][1][h0 + hh];
+                }
+                bf8 aop[4][3];
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) {
                     unsigned w[3][4];
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const bool on = (prs[rb] >> (jb + q)) & 1ull;    // never set for jb + q >= Mg
-                        const bool bit = (bts[rb] >> (jb + q)) & 1ull;
-                        const float x = (bit ? p1q[q][hh] : p0q[q][hh]) + q2[rb][hh];
-                        const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
-                        zl[rb][hh] += af;
+                    for (int pr = 0; pr < 4; ++pr) {
+                        float af2[2];
+#pragma unroll
+                        for (int e = 0; e < 2; ++e) {
+                            const int q = 2 * pr + e;
+                            const bool on = (on8[rb] >> q) & 1u;
+                            const bool bit = (bit8[rb] >> q) & 1u;
+                            const float x = (bit ? p1q[q] : p0q[q]) + q2[rb][hh];
+                            af2[e] = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
+                            zl[rb][hh] += af2[e];
+                        }
                         unsigned sp[3];
-                        split3(bit ? 0.f : af, bit ? af : 0.f, sp);
+                        split3(af2[0], af2[1], sp);
 #pragma unroll
-                        for (int z = 0; z < 3; ++z) w[z][q] = sp[z];
+                        for (int z = 0; z < 3; ++z) w[z][pr] = sp[z];
                     }
-                    const bf8 aop[3] = {as_bf8(w[0][0], w[0][1], w[0][2], w[0][3]),
-                                        as_bf8(w[1][0], w[1][1], w[1][2], w[1][3]),
-                                        as_bf8(w[2][0], w[2][1], w[2][2], w[2][3])};
 #pragma unroll
-                    for (int c2 = 0; c2 < CPH; ++c2)
-                        acc[rb][hh * CPH + c2] = mfma_split3(aop, bops[ks & 1][hh * CPH + c2], acc[rb][hh * CPH + c2]);
+                    for (int z = 0; z < 3; ++z) aop[rb][z] = as_bf8(w[z][0], w[z][1], w[z][2], w[z][3]);
+                }
+#pragma unroll
+                for (int c2 = 0; c2 < CPH; ++c2) {
+                    const int cb = hh * CPH + c2;
+                    // the next (step, column block) pair's table parts
+                    if (cb + 1 < NCB) load_b(ks, cb + 1, bops[(cb + 1) & 1]);
+                    else if (ks + 1 < ksteps) load_b(ks + 1, 0, bops[0]);
+#pragma unroll
+                    for (int rb = 0; rb < 4; ++rb)
+                        acc[rb][cb] = smfmac_split3(aop[rb], bops[cb & 1], idx[rb], acc[rb][cb]);
                 }
             }
         }
