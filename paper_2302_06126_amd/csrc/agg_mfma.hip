@@ -251,67 +251,80 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
             }
         }
         if constexpr (BF) {
-            // 16x16x32 bf16 products over the exact three-way splits of the
-            // fp32 attention weights and messages (mfma_split3): k = 2u + b
-            // over the tile's 64 ops; lane l supplies k = 8(l/16) .. 8(l/16)+7
-            // of a 32-wide step, i.e. ops ub .. ub+3 with both bits
+            // sparse 16x16x64 bf16 products (smfmac_split3) over the exact
+            // three-way splits of the fp32 attention weights and messages:
+            // k = 2u + b over 32 ops per step.  A link carries one bit, so a
+            // device row has at most one nonzero weight in each op's pair of
+            // k (the 2:4 structure).  Lane group g = l / 16 gives the weights
+            // of ops 8g .. 8g+7 of a step (value v at position 2 (v % 2) +
+            // bit of its op pair's four k) and the messages of ops 4g .. 4g+3
+            // and 16+4g .. 16+4g+3 (both bits).
 #pragma unroll 1
-            for (int ks = 0; ks < kOpTile / 16; ++ks) {
-                const int ub = 16 * ks + 4 * (lane >> 4);
-                bf8 bop[NCB][3];
+            for (int ks = 0; ks < kOpTile / 32; ++ks) {
+                const int ua = 32 * ks + 8 * (lane >> 4);
+                const int ubm = 32 * ks + 4 * (lane >> 4);
+                uint64_t prq[8], btq[8];
 #pragma unroll
-                for (int cb = 0; cb < NCB; ++cb) {
-                    const int col = cbase + cb * 16 + (lane & 15);
-                    unsigned w[3][4];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const float yc = bf2f(Ys[(ub + q) * YS + col]) + Cv[cb];   // Y + c'
-                        unsigned sp[3];
-                        split3(fmaxf(yc, 0.f), fmaxf(yc + Uv[cb], 0.f), sp);
-#pragma unroll
-                        for (int z = 0; z < 3; ++z) w[z][q] = sp[z];
-                    }
-#pragma unroll
-                    for (int z = 0; z < 3; ++z) bop[cb][z] = as_bf8(w[z][0], w[z][1], w[z][2], w[z][3]);
-                }
-                uint64_t prq[4], btq[4];
-                float p0q[4][HPW], p1q[4][HPW];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    prq[q] = pres[ub + q];
-                    btq[q] = bits[ub + q];
-#pragma unroll
-                    for (int hh = 0; hh < HPW; ++hh) {
-                        p0q[q][hh] = pb[ub + q][0][h0 + hh];
-                        p1q[q][hh] = pb[ub + q][1][h0 + hh];
-                    }
+                for (int q = 0; q < 8; ++q) {
+                    prq[q] = pres[ua + q];
+                    btq[q] = bits[ua + q];
                 }
 #pragma unroll
-                for (int rb = 0; rb < 4; ++rb) {
-                    if (rb < NRB) {
-                        const int j = rb * 16 + (lane & 15);
+                for (int hh = 0; hh < HPW; ++hh) {
+                    float p0q[8], p1q[8];
 #pragma unroll
-                        for (int hh = 0; hh < HPW; ++hh) {
-                            unsigned w[3][4];
+                    for (int q = 0; q < 8; ++q) {
+                        p0q[q] = pb[ua + q][0][h0 + hh];
+                        p1q[q] = pb[ua + q][1][h0 + hh];
+                    }
+                    bf8 aop[4][3];
+                    int idx[4];
 #pragma unroll
-                            for (int q = 0; q < 4; ++q) {
-                                const bool on = (prq[q] >> j) & 1ull;
-                                const bool bit = (btq[q] >> j) & 1ull;
-                                const float x = (bit ? p1q[q][hh] : p0q[q][hh]) + q2[rb][hh];
-                                const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
-                                zl[rb][hh] += af;
+                    for (int rb = 0; rb < 4; ++rb) {
+                        if (rb < NRB) {
+                            const int j = rb * 16 + (lane & 15);
+                            unsigned w[3][4], sb = 0u;
+#pragma unroll
+                            for (int pr = 0; pr < 4; ++pr) {
+                                float af2[2];
+#pragma unroll
+                                for (int e = 0; e < 2; ++e) {
+                                    const int q = 2 * pr + e;
+                                    const bool on = (prq[q] >> j) & 1ull;
+                                    const unsigned bit = (unsigned)(btq[q] >> j) & 1u;
+                                    const float x = (bit ? p1q[q] : p0q[q]) + q2[rb][hh];
+                                    af2[e] = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
+                                    zl[rb][hh] += af2[e];
+                                    sb |= bit << (2 * q);
+                                }
                                 unsigned sp[3];
-                                split3(bit ? 0.f : af, bit ? af : 0.f, sp);
+                                split3(af2[0], af2[1], sp);
 #pragma unroll
-                                for (int z = 0; z < 3; ++z) w[z][q] = sp[z];
+                                for (int z = 0; z < 3; ++z) w[z][pr] = sp[z];
                             }
-                            const bf8 aop[3] = {as_bf8(w[0][0], w[0][1], w[0][2], w[0][3]),
-                                                as_bf8(w[1][0], w[1][1], w[1][2], w[1][3]),
-                                                as_bf8(w[2][0], w[2][1], w[2][2], w[2][3])};
 #pragma unroll
-                            for (int c2 = 0; c2 < CPH; ++c2)
-                                acc[rb][hh * CPH + c2] = mfma_split3(aop, bop[hh * CPH + c2], acc[rb][hh * CPH + c2]);
+                            for (int z = 0; z < 3; ++z) aop[rb][z] = as_bf8(w[z][0], w[z][1], w[z][2], w[z][3]);
+                            idx[rb] = (int)(0x8888u | sb);
                         }
+                    }
+#pragma unroll
+                    for (int c2 = 0; c2 < CPH; ++c2) {
+                        const int cb = hh * CPH + c2;
+                        const int col = cbase + cb * 16 + (lane & 15);
+                        unsigned w[3][8];
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) {
+                            const int u = ubm + (q < 4 ? q : 12 + q);
+                            const float yc = bf2f(Ys[u * YS + col]) + Cv[cb];   // Y + c'
+                            unsigned sp[3];
+                            split3(fmaxf(yc, 0.f), fmaxf(yc + Uv[cb], 0.f), sp);
+#pragma unroll
+                            for (int z = 0; z < 3; ++z) w[z][q] = sp[z];
+                        }
+                        const bf16x16 bo[3] = {as_bf16x16(w[0]), as_bf16x16(w[1]), as_bf16x16(w[2])};
+#pragma unroll
+                        for (int rb = 0; rb < 4; ++rb)
+                            if (rb < NRB) acc[rb][cb] = smfmac_split3(aop[rb], bo, idx[rb], acc[rb][cb]);
                     }
                 }
             }
