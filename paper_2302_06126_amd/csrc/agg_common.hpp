@@ -91,7 +91,7 @@ struct AggArgs {
 };
 
 // MFMA path (agg_mfma.hip)
-bool mfma_path_supported(int F, int K);
+bool mfma_path_supported(int F, int K, int64_t n_op, int esz);
 void launch_pack_masks(const AggArgs &A, hipStream_t st);
 bool launch_agg_mfma(int F, int K, bool bf, const AggArgs &A, hipStream_t st);
 
@@ -146,6 +146,22 @@ struct RowRaw {
             for (int i = 0; i < CPL / 4; ++i) { const uint2 q = p[i]; w[2 * i] = q.x; w[2 * i + 1] = q.y; }
         } else {
             const uint4 *p = reinterpret_cast<const uint4 *>(static_cast<const float *>(base) + off);
+#pragma unroll
+            for (int i = 0; i < CPL / 4; ++i) {
+                const uint4 q = p[i];
+                w[4 * i] = q.x; w[4 * i + 1] = q.y; w[4 * i + 2] = q.z; w[4 * i + 3] = q.w;
+            }
+        }
+    }
+    // the same from a wave-uniform base and a 32-bit byte offset
+    __device__ __forceinline__ void load32(const void *base, uint32_t byte_off) {
+        const char *b = static_cast<const char *>(base) + byte_off;
+        if constexpr (BF) {
+            const uint2 *p = reinterpret_cast<const uint2 *>(b);
+#pragma unroll
+            for (int i = 0; i < CPL / 4; ++i) { const uint2 q = p[i]; w[2 * i] = q.x; w[2 * i + 1] = q.y; }
+        } else {
+            const uint4 *p = reinterpret_cast<const uint4 *>(b);
 #pragma unroll
             for (int i = 0; i < CPL / 4; ++i) {
                 const uint4 q = p[i];

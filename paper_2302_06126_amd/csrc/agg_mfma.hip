@@ -428,8 +428,9 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
     __shared__ uint64_t pres[kOpTile], bits[kOpTile];
     __shared__ float qo[kOpTile][K], mxS[kOpTile][K];
     __shared__ float P[64][2][K];
-    __shared__ int32_t Erp[kOpTile + 1], Ecol[ECAP];
-    __shared__ float Ex[ECAP];
+    __shared__ int32_t Erp[kOpTile + 1];
+    __shared__ int2 Ecx[ECAP];             // staged entries: (source op, edge feature bits)
+    __shared__ uint8_t Erw[ECAP];          // tile row of each staged entry
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     // XCD-aware order: the hardware deals blocks to the XCDs round-robin; the
@@ -453,11 +454,12 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
     const int32_t ne = min(ntot, ECAP);
     {
         constexpr int NQ = (kOpTile * K + 255) / 256, NP = (64 * 2 * K + 255) / 256, NE = (ECAP + 255) / 256;
-        int32_t rp0 = 0;
+        int32_t rp0 = 0, rp1 = 0;
         uint64_t om0 = 0, om1 = 0;
         float q2v[NQ], pv[NP], exv[NE];
         int32_t ecv[NE], eiv[NE];
         if (tid <= nu) rp0 = A.rp[0][u0 + tid] - eb;
+        if (tid < nu) rp1 = A.rp[0][u0 + tid + 1] - eb;
         if (tid < nu) {
             const int64_t mi = 2 * ((int64_t)r * A.n_op + u0 + tid);
             om0 = A.omask[mi];
@@ -497,8 +499,10 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
 #pragma unroll
         for (int k = 0; k < NE; ++k) {
             const int i = tid + 256 * k;
-            if (i < ne) { Ecol[i] = ecv[k]; Ex[i] = exv[k]; }
+            if (i < ne) Ecx[i] = int2{ecv[k], __float_as_int(exv[k])};
         }
+        if (tid < nu)
+            for (int32_t i = rp0; i < min(rp1, ECAP); ++i) Erw[i] = (uint8_t)tid;
     }
     __syncthreads();
     // op <- device softmax maxima (LeakyReLU of the largest pre-activation)
@@ -521,12 +525,12 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
         const int li = lane & 15;
         const int c0 = li * CPL;
         const int hd = c0 / D;                          // this lane's head
-        const int64_t ybase = (int64_t)r * A.n_op * 2 * F + c0;
+        // the candidate's relation transforms (a wave-uniform base; a row's
+        // offset from it fits 32 bits, which the host checks)
+        const void *Yc = static_cast<const char *>(A.Y_op) + (size_t)r * A.n_op * 2 * F * (BF ? 2 : 4);
         const int gr0 = wave * 16 + (lane >> 4) * 4;   // the group's first tile row
-        int32_t rb_[5];               // the group's row boundaries (rows >= nu are empty)
-#pragma unroll
-        for (int i = 0; i < 5; ++i) rb_[i] = Erp[min(gr0 + i, nu)];
-        const int32_t ebeg = rb_[0], eend = rb_[4];
+        // the group's entries (rows >= nu are empty)
+        const int32_t ebeg = Erp[min(gr0, nu)], eend = Erp[min(gr0 + 4, nu)];
         float qv[4];                  // op<-op destination terms of the group's rows (exp2 domain)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -557,70 +561,83 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
                 __syncthreads();
                 const int32_t n = min(ntot - cb0, ECAP);
                 for (int i = tid; i < n; i += 256) {
-                    Ecol[i] = A.col[0][eb + cb0 + i];
-                    Ex[i] = xo[A.eid[0][eb + cb0 + i]];
+                    Ecx[i] = int2{A.col[0][eb + cb0 + i], __float_as_int(xo[A.eid[0][eb + cb0 + i]])};
                 }
+                if (tid < nu)
+                    for (int32_t i = max(Erp[tid], cb0); i < min(Erp[tid + 1], cb0 + n); ++i)
+                        Erw[i - cb0] = (uint8_t)tid;
                 __syncthreads();
             }
-            const int32_t lo = max(ebeg, cb0), hi = min(eend, cb0 + ECAP);
-            RowRaw<CPL, BF> slot[EB];
-            float xs[EB];
-            // slot s <- entry le (past hi: the tile's first row, never
-            // consumed, so every refill is the same unconditional load)
-            auto fetch = [&](int s, int32_t le) {
-                const int32_t lc = max(min(le, hi - 1) - cb0, 0);
-                const bool ok = le < hi;
-                const int32_t v = ok ? Ecol[lc] : u0;
-                xs[s] = ok ? Ex[lc] : 0.f;
-                slot[s].load(A.Y_op, ybase + (int64_t)v * 2 * F);
+            // the group's entries of this chunk, in chunk-local indices
+            const int32_t lo = max(ebeg, cb0) - cb0, hi = min(eend, cb0 + ECAP) - cb0;
+            const int32_t hm = max(hi - 1, 0);
+            // two halves of EB / 2 row slots: while one half is consumed the
+            // other half's rows are in flight; a half is refilled as a whole
+            // right after it has been consumed (past hi a slot is refilled
+            // with the tile's first row, never consumed)
+            constexpr int HB = EB / 2;
+            RowRaw<CPL, BF> sa[HB], sb[HB];
+            float xa[HB], xb[HB];
+            int la[HB], lb2[HB];
+            auto fetch = [&](RowRaw<CPL, BF> &sl, float &xv, int &rl, int32_t le) {
+                const int32_t lc = min(le, hm);
+                const int2 cx = Ecx[lc];
+                rl = (int)Erw[lc] - gr0;              // meaningful only for le < hi
+                xv = __int_as_float(cx.y);
+                const int32_t v = le < hi ? cx.x : u0;
+                sl.load32(Yc, ((uint32_t)v * (2 * F) + c0) * (BF ? 2u : 4u));
+            };
+            auto consume = [&](const RowRaw<CPL, BF> &sl, float xv, int rl, int32_t e) {
+                float m[CPL];
+                float part = 0.f;
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) {
+                    // fp32 rows hold Y + c'; bf16 rows hold Y and get the edge term U x + c' whole
+                    const float z = BF ? sl.get(c) + fmaf(u0c[c], xv, cpc[c]) : fmaf(u0c[c], xv, sl.get(c));
+                    m[c] = msg_act<ELU>(z);
+                    part = fmaf(a[c], m[c], part);
+                }
+                const float qa = (rl & 1) ? qv[1] : qv[0], qb = (rl & 1) ? qv[3] : qv[2];
+                const float sv = row_sum<LPH>(part) + ((rl & 2) ? qb : qa);
+                const float s2 = fmaxf(sv, slope * sv);
+                if (e < hi) {
+                    const int rowe = gr0 + rl;
+                    if (rowe != ri) {   // first entry of row rowe: finish row ri
+                        if (ri >= 0) finish();
+                        ri = rowe;
+                        mref = s2;
+                        den = 0.f;
+#pragma unroll
+                        for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
+                    }
+                    float d = s2 - mref;
+                    if (d > 64.f) {   // keep the weights finite: move the reference up
+                        const float sc = __builtin_amdgcn_exp2f(-d);
+                        den *= sc;
+#pragma unroll
+                        for (int c = 0; c < CPL; ++c) acc[c] *= sc;
+                        mref = s2;
+                        d = 0.f;
+                    }
+                    const float p = __builtin_amdgcn_exp2f(d);
+                    den += p;
+#pragma unroll
+                    for (int c = 0; c < CPL; ++c) acc[c] = fmaf(p, m[c], acc[c]);
+                }
             };
 #pragma unroll
-            for (int s = 0; s < EB; ++s) fetch(s, lo + s);
+            for (int s = 0; s < HB; ++s) fetch(sa[s], xa[s], la[s], lo + s);
+#pragma unroll
+            for (int s = 0; s < HB; ++s) fetch(sb[s], xb[s], lb2[s], lo + HB + s);
             for (int32_t base = lo; base < hi; base += EB) {
 #pragma unroll
-                for (int s = 0; s < EB; ++s) {
-                    const int32_t e = base + s;
-                    const bool act = e < hi;
-                    float m[CPL];
-                    float part = 0.f;
+                for (int s = 0; s < HB; ++s) consume(sa[s], xa[s], la[s], base + s);
 #pragma unroll
-                    for (int c = 0; c < CPL; ++c) {
-                        // fp32 rows hold Y + c'; bf16 rows hold Y and get the edge term U x + c' whole
-                        const float z = BF ? slot[s].get(c) + fmaf(u0c[c], xs[s], cpc[c])
-                                           : fmaf(u0c[c], xs[s], slot[s].get(c));
-                        m[c] = msg_act<ELU>(z);
-                        part = fmaf(a[c], m[c], part);
-                    }
-                    const int rl = (e >= rb_[1]) + (e >= rb_[2]) + (e >= rb_[3]);   // row of e in the group
-                    const int rowe = gr0 + rl;
-                    fetch(s, e + EB);
-                    const float q = rl == 0 ? qv[0] : (rl == 1 ? qv[1] : (rl == 2 ? qv[2] : qv[3]));
-                    const float sv = row_sum<LPH>(part) + q;
-                    const float s2 = fmaxf(sv, slope * sv);
-                    if (act) {
-                        if (rowe != ri) {   // first entry of row rowe: finish row ri
-                            if (ri >= 0) finish();
-                            ri = rowe;
-                            mref = s2;
-                            den = 0.f;
+                for (int s = 0; s < HB; ++s) fetch(sa[s], xa[s], la[s], base + EB + s);
 #pragma unroll
-                            for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
-                        }
-                        float d = s2 - mref;
-                        if (d > 64.f) {   // keep the weights finite: move the reference up
-                            const float sc = __builtin_amdgcn_exp2f(-d);
-                            den *= sc;
+                for (int s = 0; s < HB; ++s) consume(sb[s], xb[s], lb2[s], base + HB + s);
 #pragma unroll
-                            for (int c = 0; c < CPL; ++c) acc[c] *= sc;
-                            mref = s2;
-                            d = 0.f;
-                        }
-                        const float p = __builtin_amdgcn_exp2f(d);
-                        den += p;
-#pragma unroll
-                        for (int c = 0; c < CPL; ++c) acc[c] = fmaf(p, m[c], acc[c]);
-                    }
-                }
+                for (int s = 0; s < HB; ++s) fetch(sb[s], xb[s], lb2[s], base + EB + HB + s);
             }
         }
         if (ri >= 0) finish();
@@ -888,14 +905,18 @@ bool dispatch_mfma_heads(int K, const AggArgs &A, hipStream_t st) {
 
 }  // namespace
 
-bool mfma_path_supported(int F, int K) { return K >= 1 && F / K >= 16 && K <= 16; }
+// heads of at least 16 channels, at most 16 heads, and a candidate's relation
+// transforms within 32-bit byte offsets of its base (the op<-op gathers)
+bool mfma_path_supported(int F, int K, int64_t n_op, int esz) {
+    return K >= 1 && F / K >= 16 && K <= 16 && n_op * 2 * F * esz < (int64_t(1) << 32);
+}
 
 void launch_pack_masks(const AggArgs &A, hipStream_t st) {
     pack_op_masks<<<dim3((unsigned)A.n_tiles, (unsigned)((A.R + kMaskCands - 1) / kMaskCands)), 256, 0, st>>>(A);
 }
 
 bool launch_agg_mfma(int F, int K, bool bf, const AggArgs &A, hipStream_t st) {
-    if (!mfma_path_supported(F, K)) return false;
+    if (!mfma_path_supported(F, K, A.n_op, bf ? 2 : 4)) return false;
     if (A.elu) {   // the ELU variant runs in fp32
         if (bf) return false;
         if (F == 64) return dispatch_mfma_heads<64, false, true>(K, A, st);
