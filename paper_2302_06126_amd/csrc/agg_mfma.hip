@@ -427,6 +427,10 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
     __shared__ __attribute__((aligned(16))) float Ot[kOpTile * OS];
     __shared__ uint64_t pres[kOpTile], bits[kOpTile];
     __shared__ float qo[kOpTile][K], mxS[kOpTile][K];
+    // op<-op per-channel constants (a log2 e, U_0, c') staged once per block
+    // where the LDS budget allows (f = 256); smaller f loads them per lane
+    constexpr bool kCS = F >= 256;
+    __shared__ __attribute__((aligned(16))) float CA[kCS ? 3 : 1][kCS ? F : 4];
     __shared__ float P[64][2][K];
     __shared__ int32_t Erp[kOpTile + 1];
     __shared__ int2 Ecx[ECAP];             // staged entries: (source op, edge feature bits)
@@ -446,6 +450,23 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
     const float slope = A.slope;
     const int cbase = wave * WC;
     const int h0 = cbase / D;
+
+    // op<-op terms of this lane: its channels c0 .. c0+CPL-1 of the group's
+    // four rows (loaded with the prologue so their latency overlaps it)
+    const int c0 = (lane & 15) * CPL;
+    const int gr0 = wave * 16 + (lane >> 4) * 4;   // the group's first tile row
+    float qv3[4];                                  // op<-op destination terms of the group's rows
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        qv3[i] = gr0 + i < nu ? Sop[(int64_t)(u0 + gr0 + i) * 4 * K + 3 * K + c0 / D] : 0.f;
+    float a[CPL], u0c[CPL], cpc[CPL];
+    static_assert(!kCS || F == 256, "one staged constant per thread");
+    float ca3[3];
+    if constexpr (kCS) {
+        ca3[0] = A.att_src[tid] * kLog2e;
+        ca3[1] = A.U[(size_t)tid * 2];
+        ca3[2] = BF ? A.cp[tid] : 0.f;
+    }
 
     // ---- prologue: every global load is issued before the first LDS store
     // (the logits go to the exp2 domain: LeakyReLU commutes with log2(e) > 0)
@@ -503,6 +524,10 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
         }
         if (tid < nu)
             for (int32_t i = rp0; i < min(rp1, ECAP); ++i) Erw[i] = (uint8_t)tid;
+        if constexpr (kCS) {
+#pragma unroll
+            for (int z = 0; z < 3; ++z) CA[z][tid] = ca3[z];
+        }
     }
     __syncthreads();
     // op <- device softmax maxima (LeakyReLU of the largest pre-activation)
@@ -511,10 +536,15 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
         uint64_t pr = pres[u];
         const uint64_t bt = bits[u];
         float mx = -INFINITY;
-        while (pr) {
-            const int j = __builtin_ctzll(pr);
-            pr &= pr - 1;
-            mx = fmaxf(mx, P[j][(bt >> j) & 1ull][h]);
+        while (pr) {   // four linked devices per round, their LDS reads issued together
+            float v[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int j = pr ? __builtin_ctzll(pr) : 0;
+                v[q] = pr ? P[j][(bt >> j) & 1ull][h] : -INFINITY;
+                pr &= pr - 1;
+            }
+            mx = fmaxf(mx, fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
         }
         const float x = mx + qo[u][h];
         mxS[u][h] = mx == -INFINITY ? -INFINITY : fmaxf(x, slope * x);
@@ -522,30 +552,37 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
 
     // ---- op <- op into the LDS tile (gamma_same applied)
     {
-        const int li = lane & 15;
-        const int c0 = li * CPL;
         const int hd = c0 / D;                          // this lane's head
         // the candidate's relation transforms (a wave-uniform base; a row's
         // offset from it fits 32 bits, which the host checks)
         const void *Yc = static_cast<const char *>(A.Y_op) + (size_t)r * A.n_op * 2 * F * (BF ? 2 : 4);
-        const int gr0 = wave * 16 + (lane >> 4) * 4;   // the group's first tile row
+        if constexpr (kCS) {
+#pragma unroll
+            for (int c = 0; c < CPL; c += 4) {
+                const float4 x = *reinterpret_cast<const float4 *>(&CA[0][c0 + c]);
+                const float4 y = *reinterpret_cast<const float4 *>(&CA[1][c0 + c]);
+                const float4 z = *reinterpret_cast<const float4 *>(&CA[2][c0 + c]);
+                a[c] = x.x; a[c + 1] = x.y; a[c + 2] = x.z; a[c + 3] = x.w;
+                u0c[c] = y.x; u0c[c + 1] = y.y; u0c[c + 2] = y.z; u0c[c + 3] = y.w;
+                cpc[c] = z.x; cpc[c + 1] = z.y; cpc[c + 2] = z.z; cpc[c + 3] = z.w;
+            }
+        } else {
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) {
+                a[c] = A.att_src[c0 + c] * kLog2e;
+                u0c[c] = A.U[(size_t)(c0 + c) * 2];
+                cpc[c] = BF ? A.cp[c0 + c] : 0.f;
+            }
+        }
         // the group's entries (rows >= nu are empty)
         const int32_t ebeg = Erp[min(gr0, nu)], eend = Erp[min(gr0 + 4, nu)];
         float qv[4];                  // op<-op destination terms of the group's rows (exp2 domain)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            qv[i] = gr0 + i < nu ? Sop[(int64_t)(u0 + gr0 + i) * 4 * K + 3 * K + hd] * kLog2e : 0.f;
+        for (int i = 0; i < 4; ++i) qv[i] = qv3[i] * kLog2e;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
             if (gr0 + i < nu)
                 for (int c = 0; c < CPL; ++c) Ot[(gr0 + i) * OS + c0 + c] = 0.f;   // rows without entries stay zero
-        float a[CPL], u0c[CPL], cpc[CPL];
-#pragma unroll
-        for (int c = 0; c < CPL; ++c) {
-            a[c] = A.att_src[c0 + c] * kLog2e;
-            u0c[c] = A.U[(size_t)(c0 + c) * 2];
-            cpc[c] = BF ? A.cp[c0 + c] : 0.f;
-        }
         const float gs = A.g_same;
         int ri = -1;                  // row being accumulated (-1: none yet)
         float mref = 0.f, den = 0.f, acc[CPL];
