@@ -34,6 +34,15 @@ __device__ __forceinline__ f4 mfma_split3(const bf8 (&a)[3], const bf8 (&b)[3], 
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[0], b[0], acc, 0, 0, 0);
 }
 
+// 16 bytes from global memory straight into LDS (global_load_lds_dwordx4):
+// lane l of the wavefront writes lds + 16 l, lds being wave-uniform; counted
+// by vmcnt like any global load.  The builtin exists in the device pass only.
+__device__ __forceinline__ void load_lds16(const void *src, void *lds) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
+#endif
+}
+
 // Sparse 16x16x64 bf16 products (v_smfmac_f32_16x16x64_bf16).  A is 16 x 64
 // with at most two nonzeros in every four consecutive k, given as its eight
 // nonzero values per lane plus 2-bit positions; B is dense 64 x 16.  Lane

@@ -133,11 +133,15 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     constexpr int NCB = WC / 16;                   // 16-column blocks per wavefront
     constexpr int HPW = WC >= D ? WC / D : 1;      // heads per wavefront
     constexpr int CPH = NCB / HPW;                 // column blocks per head inside a wavefront
-    constexpr int YS = BF ? F + 8 : F + 4;         // padded LDS row (bf16 rows stay 16-byte aligned)
+    // bf16: op tiles double-buffered and filled by direct global -> LDS
+    // loads, rows unpadded with their 16-byte chunks XOR-swizzled (see
+    // ys_off); fp32: one tile, rows padded
+    constexpr int NB = BF ? 2 : 1;
+    constexpr int YS = BF ? F : F + 4;
     typedef typename std::conditional<BF, uint16_t, float>::type YT;
-    __shared__ __attribute__((aligned(16))) YT Ys[kOpTile * YS];
-    __shared__ uint64_t pres[kOpTile], bits[kOpTile];
-    __shared__ float pb[kOpTile][2][K];
+    __shared__ __attribute__((aligned(16))) YT Ys[NB][kOpTile * YS];
+    __shared__ __attribute__((aligned(16))) uint64_t MK[NB][kOpTile][2];   // (present, bit) masks per op
+    __shared__ float pb[NB][kOpTile][2][K];
     __shared__ int mxk[64][K];
     __shared__ float qd[64][K], mrun[64][K];
     __shared__ float US[F], CS[F];
@@ -209,162 +213,198 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
         for (int hh = 0; hh < HPW; ++hh) zl[rb][hh] = 0.f;
     }
 
-    for (int32_t t = t0; t < t1; ++t) {
-        const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1];
-        for (int i = tid; i < kOpTile; i += 256) {
-            const bool ok = i < nu;
-            pres[i] = ok ? om[2 * (int64_t)(u0 + i)] : 0ull;
-            bits[i] = ok ? om[2 * (int64_t)(u0 + i) + 1] : 0ull;
+    __syncthreads();   // the maxima are in place
+    // per-lane constants of the lane's device rows j = rb*16 + l%16
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+        const int j = rb * 16 + (lane & 15);
+#pragma unroll
+        for (int hh = 0; hh < HPW; ++hh) {
+            q2[rb][hh] = qd[j][h0 + hh];
+            m2[rb][hh] = j < Mg ? mrun[j][h0 + hh] : 0.f;
         }
-        for (int i = tid; i < kOpTile * 2 * K; i += 256) {
-            const int u = i / (2 * K), bh = i % (2 * K);
-            pb[u][bh / K][bh % K] = u < nu ? Sop[(int64_t)(u0 + u) * 4 * K + bh] * kLog2e : 0.f;
-        }
-        if constexpr (BF) {
-            for (int i = tid; i < kOpTile * (F / 8); i += 256) {
-                const int u = i / (F / 8), c = (i % (F / 8)) * 8;
-                u4v v = u4v{0u, 0u, 0u, 0u};
-                if (u < nu)
-                    v = *reinterpret_cast<const u4v *>(static_cast<const uint16_t *>(A.Y_op) +
-                                                       ((int64_t)r * A.n_op + u0 + u) * 2 * F + F + c);
-                *reinterpret_cast<u4v *>(&Ys[u * YS + c]) = v;
+    }
+    constexpr int NPB = (kOpTile * 2 * K + 255) / 256;
+    if constexpr (BF) {
+        // element (op u, column col) of a bf16 tile: 16-byte chunk col / 8 of
+        // row u, XORed with 2 ((u / 4) % 4) so that the four lane groups of a
+        // message read (rows 4 apart) fall on different banks
+        auto ys_off = [](int u, int col) { return u * F + ((((col >> 3) ^ (2 * ((u >> 2) & 3))) << 3) | (col & 7)); };
+        // tile t into buffer bf: the op rows' second halves and the masks by
+        // direct loads into LDS (rows past the tile repeat op u0: their
+        // weights are zero), the attention terms into registers
+        float pbv[NPB];
+        auto stage = [&](int32_t t, int bf) {
+            const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1];
+            const uint16_t *Yr = static_cast<const uint16_t *>(A.Y_op) + ((int64_t)r * A.n_op + u0) * 2 * F + F;
+            constexpr int NI = kOpTile * F / 8 / 256;   // 16-byte chunks per thread
+#pragma unroll
+            for (int i = 0; i < NI; ++i) {
+                const int P = (wave * NI + i) * 64 + lane;   // physical chunk; the wave fills 1 KB
+                const int u = P / (F / 8), k = (P % (F / 8)) ^ (2 * ((u >> 2) & 3));
+                load_lds16(Yr + (int64_t)(u < nu ? u : 0) * 2 * F + 8 * k, &Ys[bf][(wave * NI + i) * 64 * 8]);
             }
-        } else {
+            if (wave == 0)
+                load_lds16(om + 2 * (int64_t)(u0 + (lane < nu ? lane : 0)), &MK[bf][0][0]);
+#pragma unroll
+            for (int k = 0; k < NPB; ++k) {
+                const int i = tid + 256 * k, u = i / (2 * K), bh = i % (2 * K);
+                pbv[k] = (i < kOpTile * 2 * K && u < nu) ? Sop[(int64_t)(u0 + u) * 4 * K + bh] : 0.f;
+            }
+        };
+        auto put_pb = [&](int bf) {
+#pragma unroll
+            for (int k = 0; k < NPB; ++k) {
+                const int i = tid + 256 * k, u = i / (2 * K), bh = i % (2 * K);
+                if (i < kOpTile * 2 * K) pb[bf][u][bh / K][bh % K] = pbv[k] * kLog2e;
+            }
+        };
+        stage(t0, 0);
+        put_pb(0);
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        for (int32_t t = t0; t < t1; ++t) {
+            const int buf = (t - t0) & 1;
+            const int32_t nu = A.tiles[3 * t + 1];
+            if (t + 1 < t1) stage(t + 1, buf ^ 1);   // lands while this tile is aggregated
+                // sparse 16x16x64 bf16 products (smfmac_split3) over the exact
+                // three-way splits of the fp32 attention weights and messages:
+                // k = 2u + b over 32 ops per step.  A link carries one bit, so a
+                // device row has at most one nonzero weight in each op's pair of
+                // k (the 2:4 structure).  Lane group g = l / 16 gives the weights
+                // of ops 8g .. 8g+7 of a step (value v at position 2 (v % 2) +
+                // bit of its op pair's four k) and the messages of ops 4g .. 4g+3
+                // and 16+4g .. 16+4g+3 (both bits).
+#pragma unroll 1
+                for (int ks = 0; ks < kOpTile / 32; ++ks) {
+                    const int ua = 32 * ks + 8 * (lane >> 4);
+                    const int ubm = 32 * ks + 4 * (lane >> 4);
+                    uint64_t prq[8], btq[8];
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) {
+                        const bool live = ua + q < nu;   // rows past the tile hold another op's masks
+                        prq[q] = live ? MK[buf][ua + q][0] : 0ull;
+                        btq[q] = live ? MK[buf][ua + q][1] : 0ull;
+                    }
+#pragma unroll
+                    for (int hh = 0; hh < HPW; ++hh) {
+                        float p0q[8], p1q[8];
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) {
+                            p0q[q] = pb[buf][ua + q][0][h0 + hh];
+                            p1q[q] = pb[buf][ua + q][1][h0 + hh];
+                        }
+                        bf8 aop[4][3];
+                        int idx[4];
+#pragma unroll
+                        for (int rb = 0; rb < 4; ++rb) {
+                            if (rb < NRB) {
+                                const int j = rb * 16 + (lane & 15);
+                                unsigned w[3][4], sb = 0u;
+#pragma unroll
+                                for (int pr = 0; pr < 4; ++pr) {
+                                    float af2[2];
+#pragma unroll
+                                    for (int e = 0; e < 2; ++e) {
+                                        const int q = 2 * pr + e;
+                                        const bool on = (prq[q] >> j) & 1ull;
+                                        const unsigned bit = (unsigned)(btq[q] >> j) & 1u;
+                                        const float x = (bit ? p1q[q] : p0q[q]) + q2[rb][hh];
+                                        af2[e] = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
+                                        zl[rb][hh] += af2[e];
+                                        sb |= bit << (2 * q);
+                                    }
+                                    unsigned sp[3];
+                                    split3(af2[0], af2[1], sp);
+#pragma unroll
+                                    for (int z = 0; z < 3; ++z) w[z][pr] = sp[z];
+                                }
+#pragma unroll
+                                for (int z = 0; z < 3; ++z) aop[rb][z] = as_bf8(w[z][0], w[z][1], w[z][2], w[z][3]);
+                                idx[rb] = (int)(0x8888u | sb);
+                            }
+                        }
+#pragma unroll
+                        for (int c2 = 0; c2 < CPH; ++c2) {
+                            const int cb = hh * CPH + c2;
+                            const int col = cbase + cb * 16 + (lane & 15);
+                            unsigned w[3][8];
+#pragma unroll
+                            for (int q = 0; q < 8; ++q) {
+                                const int u = ubm + (q < 4 ? q : 12 + q);
+                                const float yc = bf2f(Ys[buf][ys_off(u, col)]) + Cv[cb];   // Y + c'
+                                unsigned sp[3];
+                                split3(fmaxf(yc, 0.f), fmaxf(yc + Uv[cb], 0.f), sp);
+#pragma unroll
+                                for (int z = 0; z < 3; ++z) w[z][q] = sp[z];
+                            }
+                            const bf16x16 bo[3] = {as_bf16x16(w[0]), as_bf16x16(w[1]), as_bf16x16(w[2])};
+#pragma unroll
+                            for (int rb = 0; rb < 4; ++rb)
+                                if (rb < NRB) acc[rb][cb] = smfmac_split3(aop[rb], bo, idx[rb], acc[rb][cb]);
+                        }
+                    }
+                }
+            if (t + 1 < t1) put_pb(buf ^ 1);
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();   // the next tile is in place; this one is free again
+        }
+    } else {
+        for (int32_t t = t0; t < t1; ++t) {
+            const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1];
+            for (int i = tid; i < kOpTile; i += 256) {
+                const bool ok = i < nu;
+                MK[0][i][0] = ok ? om[2 * (int64_t)(u0 + i)] : 0ull;
+                MK[0][i][1] = ok ? om[2 * (int64_t)(u0 + i) + 1] : 0ull;
+            }
+            for (int i = tid; i < kOpTile * 2 * K; i += 256) {
+                const int u = i / (2 * K), bh = i % (2 * K);
+                pb[0][u][bh / K][bh % K] = u < nu ? Sop[(int64_t)(u0 + u) * 4 * K + bh] * kLog2e : 0.f;
+            }
             for (int i = tid; i < kOpTile * (F / 4); i += 256) {
                 const int u = i / (F / 4), c = (i % (F / 4)) * 4;
                 float v[4] = {0.f, 0.f, 0.f, 0.f};
                 if (u < nu) load_ch<4, false>(A.Y_op, ((int64_t)r * A.n_op + u0 + u) * 2 * F + F + c, v);
-                for (int q = 0; q < 4; ++q) Ys[u * YS + c + q] = v[q];
+                for (int q = 0; q < 4; ++q) Ys[0][u * YS + c + q] = v[q];
             }
-        }
-        __syncthreads();
-        if (t == t0) {
-            // per-lane constants of the lane's device rows j = rb*16 + l%16
+            __syncthreads();
+            // fp32 16x16x4 products: k = 4 (op, bit) pairs per step, two ops per
+            // step; lane l supplies op 2s + l / 32 with bit (l / 16) % 2
+            for (int s = 0; s < kOpTile / 2; ++s) {
+                const int ul = 2 * s + (lane >> 5);
+                const uint64_t pr = MK[0][ul][0], bt = b ? MK[0][ul][1] : ~MK[0][ul][1];   // bt bit j: link bit equals b
+                float bv[NCB];
 #pragma unroll
-            for (int rb = 0; rb < 4; ++rb) {
-                const int j = rb * 16 + (lane & 15);
-#pragma unroll
-                for (int hh = 0; hh < HPW; ++hh) {
-                    q2[rb][hh] = qd[j][h0 + hh];
-                    m2[rb][hh] = j < Mg ? mrun[j][h0 + hh] : 0.f;
+                for (int cb = 0; cb < NCB; ++cb) {
+                    const int col = cbase + cb * 16 + (lane & 15);
+                    // fp32 rows store Y + c'
+                    const float yc = static_cast<float>(Ys[0][ul * YS + col]);
+                    bv[cb] = msg_act<ELU>(b ? yc + Uv[cb] : yc);
                 }
-            }
-        }
-        if constexpr (BF) {
-            // sparse 16x16x64 bf16 products (smfmac_split3) over the exact
-            // three-way splits of the fp32 attention weights and messages:
-            // k = 2u + b over 32 ops per step.  A link carries one bit, so a
-            // device row has at most one nonzero weight in each op's pair of
-            // k (the 2:4 structure).  Lane group g = l / 16 gives the weights
-            // of ops 8g .. 8g+7 of a step (value v at position 2 (v % 2) +
-            // bit of its op pair's four k) and the messages of ops 4g .. 4g+3
-            // and 16+4g .. 16+4g+3 (both bits).
-#pragma unroll 1
-            for (int ks = 0; ks < kOpTile / 32; ++ks) {
-                const int ua = 32 * ks + 8 * (lane >> 4);
-                const int ubm = 32 * ks + 4 * (lane >> 4);
-                uint64_t prq[8], btq[8];
+                float pu[HPW];
 #pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    prq[q] = pres[ua + q];
-                    btq[q] = bits[ua + q];
-                }
+                for (int hh = 0; hh < HPW; ++hh) pu[hh] = pb[0][ul][b][h0 + hh];
+                const uint64_t sel = pr & bt;
 #pragma unroll
-                for (int hh = 0; hh < HPW; ++hh) {
-                    float p0q[8], p1q[8];
+                for (int rb = 0; rb < 4; ++rb) {
+                    if (rb < NRB) {
+                        const int j = rb * 16 + (lane & 15);
+                        const bool on = (sel >> j) & 1ull;   // j < Mg holds for every set bit
 #pragma unroll
-                    for (int q = 0; q < 8; ++q) {
-                        p0q[q] = pb[ua + q][0][h0 + hh];
-                        p1q[q] = pb[ua + q][1][h0 + hh];
-                    }
-                    bf8 aop[4][3];
-                    int idx[4];
+                        for (int hh = 0; hh < HPW; ++hh) {
+                            const float x = pu[hh] + q2[rb][hh];
+                            const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
+                            zl[rb][hh] += af;
 #pragma unroll
-                    for (int rb = 0; rb < 4; ++rb) {
-                        if (rb < NRB) {
-                            const int j = rb * 16 + (lane & 15);
-                            unsigned w[3][4], sb = 0u;
-#pragma unroll
-                            for (int pr = 0; pr < 4; ++pr) {
-                                float af2[2];
-#pragma unroll
-                                for (int e = 0; e < 2; ++e) {
-                                    const int q = 2 * pr + e;
-                                    const bool on = (prq[q] >> j) & 1ull;
-                                    const unsigned bit = (unsigned)(btq[q] >> j) & 1u;
-                                    const float x = (bit ? p1q[q] : p0q[q]) + q2[rb][hh];
-                                    af2[e] = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
-                                    zl[rb][hh] += af2[e];
-                                    sb |= bit << (2 * q);
-                                }
-                                unsigned sp[3];
-                                split3(af2[0], af2[1], sp);
-#pragma unroll
-                                for (int z = 0; z < 3; ++z) w[z][pr] = sp[z];
-                            }
-#pragma unroll
-                            for (int z = 0; z < 3; ++z) aop[rb][z] = as_bf8(w[z][0], w[z][1], w[z][2], w[z][3]);
-                            idx[rb] = (int)(0x8888u | sb);
+                            for (int c2 = 0; c2 < CPH; ++c2)
+                                acc[rb][hh * CPH + c2] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                    af, bv[hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
                         }
                     }
-#pragma unroll
-                    for (int c2 = 0; c2 < CPH; ++c2) {
-                        const int cb = hh * CPH + c2;
-                        const int col = cbase + cb * 16 + (lane & 15);
-                        unsigned w[3][8];
-#pragma unroll
-                        for (int q = 0; q < 8; ++q) {
-                            const int u = ubm + (q < 4 ? q : 12 + q);
-                            const float yc = bf2f(Ys[u * YS + col]) + Cv[cb];   // Y + c'
-                            unsigned sp[3];
-                            split3(fmaxf(yc, 0.f), fmaxf(yc + Uv[cb], 0.f), sp);
-#pragma unroll
-                            for (int z = 0; z < 3; ++z) w[z][q] = sp[z];
-                        }
-                        const bf16x16 bo[3] = {as_bf16x16(w[0]), as_bf16x16(w[1]), as_bf16x16(w[2])};
-#pragma unroll
-                        for (int rb = 0; rb < 4; ++rb)
-                            if (rb < NRB) acc[rb][cb] = smfmac_split3(aop[rb], bo, idx[rb], acc[rb][cb]);
-                    }
                 }
             }
-        } else
-        // fp32 16x16x4 products: k = 4 (op, bit) pairs per step, two ops per
-        // step; lane l supplies op 2s + l / 32 with bit (l / 16) % 2
-        for (int s = 0; s < kOpTile / 2; ++s) {
-            const int ul = 2 * s + (lane >> 5);
-            const uint64_t pr = pres[ul], bt = b ? bits[ul] : ~bits[ul];   // bt bit j: link bit equals b
-            float bv[NCB];
-#pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) {
-                const int col = cbase + cb * 16 + (lane & 15);
-                // Y + c': fp32 rows store it, bf16 rows store Y
-                const float yc = BF ? bf2f(Ys[ul * YS + col]) + Cv[cb] : static_cast<float>(Ys[ul * YS + col]);
-                bv[cb] = msg_act<ELU>(b ? yc + Uv[cb] : yc);
-            }
-            float pu[HPW];
-#pragma unroll
-            for (int hh = 0; hh < HPW; ++hh) pu[hh] = pb[ul][b][h0 + hh];
-            const uint64_t sel = pr & bt;
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb) {
-                if (rb < NRB) {
-                    const int j = rb * 16 + (lane & 15);
-                    const bool on = (sel >> j) & 1ull;   // j < Mg holds for every set bit
-#pragma unroll
-                    for (int hh = 0; hh < HPW; ++hh) {
-                        const float x = pu[hh] + q2[rb][hh];
-                        const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
-                        zl[rb][hh] += af;
-#pragma unroll
-                        for (int c2 = 0; c2 < CPH; ++c2)
-                            acc[rb][hh * CPH + c2] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                                af, bv[hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
-                    }
-                }
-            }
+            __syncthreads();   // the next tile overwrites the LDS tile and masks
         }
-        __syncthreads();   // the next tile overwrites the LDS tile and masks
     }
 
     const int REC = F + 2 * K;
