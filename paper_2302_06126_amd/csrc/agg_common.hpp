@@ -34,12 +34,16 @@ __device__ __forceinline__ f4 mfma_split3(const bf8 (&a)[3], const bf8 (&b)[3], 
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[0], b[0], acc, 0, 0, 0);
 }
 
-// 16 bytes from global memory straight into LDS (global_load_lds_dwordx4):
-// lane l of the wavefront writes lds + 16 l, lds being wave-uniform; counted
-// by vmcnt like any global load.  The builtin exists in the device pass only.
-__device__ __forceinline__ void load_lds16(const void *src, void *lds) {
+// SZ bytes per lane from global memory straight into LDS (global_load_lds,
+// dword or dwordx4): lane l of the wavefront writes lds + SZ l, lds being
+// wave-uniform; counted by vmcnt like any global load.  The builtin exists in
+// the device pass only.
+template <int SZ = 16>
+__device__ __forceinline__ void load_lds(const void *src, void *lds) {
+    static_assert(SZ == 4 || SZ == 16, "4- or 16-byte lanes");
 #if defined(__HIP_DEVICE_COMPILE__)
-    __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
+    if constexpr (SZ == 16) __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
+    else __builtin_amdgcn_global_load_lds(src, lds, 4, 0, 0);
 #endif
 }
 

@@ -139,9 +139,11 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     constexpr int NB = BF ? 2 : 1;
     constexpr int YS = BF ? F : F + 4;
     typedef typename std::conditional<BF, uint16_t, float>::type YT;
-    __shared__ __attribute__((aligned(16))) YT Ys[NB][kOpTile * YS];
-    __shared__ __attribute__((aligned(16))) uint64_t MK[NB][kOpTile][2];   // (present, bit) masks per op
-    __shared__ float pb[NB][kOpTile][2][K];
+    // (two separate arrays per buffer, so that the compiler sees that the
+    // loads into one buffer do not alias the reads of the other)
+    __shared__ __attribute__((aligned(16))) YT Ys0[kOpTile * YS], Ys1[NB > 1 ? kOpTile * YS : 8];
+    __shared__ __attribute__((aligned(16))) uint64_t MK0[kOpTile][2], MK1[NB > 1 ? kOpTile : 1][2];   // (present, bit) per op
+    __shared__ float pb0[kOpTile][2][K], pb1[NB > 1 ? kOpTile : 1][2][K];
     __shared__ int mxk[64][K];
     __shared__ float qd[64][K], mrun[64][K];
     __shared__ float US[F], CS[F];
@@ -224,49 +226,42 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
             m2[rb][hh] = j < Mg ? mrun[j][h0 + hh] : 0.f;
         }
     }
-    constexpr int NPB = (kOpTile * 2 * K + 255) / 256;
     if constexpr (BF) {
         // element (op u, column col) of a bf16 tile: 16-byte chunk col / 8 of
         // row u, XORed with 2 ((u / 4) % 4) so that the four lane groups of a
         // message read (rows 4 apart) fall on different banks
         auto ys_off = [](int u, int col) { return u * F + ((((col >> 3) ^ (2 * ((u >> 2) & 3))) << 3) | (col & 7)); };
-        // tile t into buffer bf: the op rows' second halves and the masks by
-        // direct loads into LDS (rows past the tile repeat op u0: their
-        // weights are zero), the attention terms into registers
-        float pbv[NPB];
-        auto stage = [&](int32_t t, int bf) {
+        // tile t into the given buffers, all by direct loads into LDS: the op
+        // rows' second halves, the masks and the raw attention terms (rows
+        // past the tile repeat op u0: their weights are zero)
+        auto stage = [&](int32_t t, auto &ys, auto &mk, auto &pbn) {
             const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1];
             const uint16_t *Yr = static_cast<const uint16_t *>(A.Y_op) + ((int64_t)r * A.n_op + u0) * 2 * F + F;
             constexpr int NI = kOpTile * F / 8 / 256;   // 16-byte chunks per thread
+            const int wv = __builtin_amdgcn_readfirstlane(wave);   // (wave-uniform LDS addresses)
 #pragma unroll
             for (int i = 0; i < NI; ++i) {
-                const int P = (wave * NI + i) * 64 + lane;   // physical chunk; the wave fills 1 KB
+                const int P = (wv * NI + i) * 64 + lane;   // physical chunk; the wave fills 1 KB
                 const int u = P / (F / 8), k = (P % (F / 8)) ^ (2 * ((u >> 2) & 3));
-                load_lds16(Yr + (int64_t)(u < nu ? u : 0) * 2 * F + 8 * k, &Ys[bf][(wave * NI + i) * 64 * 8]);
+                load_lds<16>(Yr + (int64_t)(u < nu ? u : 0) * 2 * F + 8 * k, &ys[(wv * NI + i) * 64 * 8]);
             }
-            if (wave == 0)
-                load_lds16(om + 2 * (int64_t)(u0 + (lane < nu ? lane : 0)), &MK[bf][0][0]);
+            if (wv == 0)
+                load_lds<16>(om + 2 * (int64_t)(u0 + (lane < nu ? lane : 0)), &mk[0][0]);
+            // an op's 2K attention terms (8K bytes) in PC-byte lanes
+            constexpr int PC = 8 * K >= 16 ? 16 : 4, PCO = 8 * K / PC, PNI = kOpTile * PCO / 64;
 #pragma unroll
-            for (int k = 0; k < NPB; ++k) {
-                const int i = tid + 256 * k, u = i / (2 * K), bh = i % (2 * K);
-                pbv[k] = (i < kOpTile * 2 * K && u < nu) ? Sop[(int64_t)(u0 + u) * 4 * K + bh] : 0.f;
+            for (int j = 0; j < (PNI + 3) / 4; ++j) {
+                const int i = wv + 4 * j;
+                if (i >= PNI) break;
+                const int P = i * 64 + lane, u = P / PCO;
+                load_lds<PC>(Sop + (int64_t)(u0 + (u < nu ? u : 0)) * 4 * K + (P % PCO) * (PC / 4),
+                             &pbn[0][0][0] + i * 64 * (PC / 4));
             }
         };
-        auto put_pb = [&](int bf) {
-#pragma unroll
-            for (int k = 0; k < NPB; ++k) {
-                const int i = tid + 256 * k, u = i / (2 * K), bh = i % (2 * K);
-                if (i < kOpTile * 2 * K) pb[bf][u][bh / K][bh % K] = pbv[k] * kLog2e;
-            }
-        };
-        stage(t0, 0);
-        put_pb(0);
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        for (int32_t t = t0; t < t1; ++t) {
-            const int buf = (t - t0) & 1;
+        // tile t from the current buffers while tile t + 1 lands in the others
+        auto run = [&](int32_t t, auto &ysc, auto &mkc, auto &pbc, auto &ysn, auto &mkn, auto &pbn) {
             const int32_t nu = A.tiles[3 * t + 1];
-            if (t + 1 < t1) stage(t + 1, buf ^ 1);   // lands while this tile is aggregated
+            if (t + 1 < t1) stage(t + 1, ysn, mkn, pbn);
                 // sparse 16x16x64 bf16 products (smfmac_split3) over the exact
                 // three-way splits of the fp32 attention weights and messages:
                 // k = 2u + b over 32 ops per step.  A link carries one bit, so a
@@ -283,16 +278,16 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
 #pragma unroll
                     for (int q = 0; q < 8; ++q) {
                         const bool live = ua + q < nu;   // rows past the tile hold another op's masks
-                        prq[q] = live ? MK[buf][ua + q][0] : 0ull;
-                        btq[q] = live ? MK[buf][ua + q][1] : 0ull;
+                        prq[q] = live ? mkc[ua + q][0] : 0ull;
+                        btq[q] = live ? mkc[ua + q][1] : 0ull;
                     }
 #pragma unroll
                     for (int hh = 0; hh < HPW; ++hh) {
                         float p0q[8], p1q[8];
 #pragma unroll
                         for (int q = 0; q < 8; ++q) {
-                            p0q[q] = pb[buf][ua + q][0][h0 + hh];
-                            p1q[q] = pb[buf][ua + q][1][h0 + hh];
+                            p0q[q] = pbc[ua + q][0][h0 + hh];
+                            p1q[q] = pbc[ua + q][1][h0 + hh];
                         }
                         bf8 aop[4][3];
                         int idx[4];
@@ -309,7 +304,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
                                         const int q = 2 * pr + e;
                                         const bool on = (prq[q] >> j) & 1ull;
                                         const unsigned bit = (unsigned)(btq[q] >> j) & 1u;
-                                        const float x = (bit ? p1q[q] : p0q[q]) + q2[rb][hh];
+                                        const float x = fmaf(bit ? p1q[q] : p0q[q], kLog2e, q2[rb][hh]);   // raw terms
                                         af2[e] = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
                                         zl[rb][hh] += af2[e];
                                         sb |= bit << (2 * q);
@@ -332,7 +327,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
 #pragma unroll
                             for (int q = 0; q < 8; ++q) {
                                 const int u = ubm + (q < 4 ? q : 12 + q);
-                                const float yc = bf2f(Ys[buf][ys_off(u, col)]) + Cv[cb];   // Y + c'
+                                const float yc = bf2f(ysc[ys_off(u, col)]) + Cv[cb];   // Y + c'
                                 unsigned sp[3];
                                 split3(fmaxf(yc, 0.f), fmaxf(yc + Uv[cb], 0.f), sp);
 #pragma unroll
@@ -345,45 +340,51 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
                         }
                     }
                 }
-            if (t + 1 < t1) put_pb(buf ^ 1);
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();   // the next tile is in place; this one is free again
+        };
+        stage(t0, Ys0, MK0, pb0);
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        for (int32_t t = t0; t < t1; t += 2) {
+            run(t, Ys0, MK0, pb0, Ys1, MK1, pb1);
+            if (t + 1 < t1) run(t + 1, Ys1, MK1, pb1, Ys0, MK0, pb0);
         }
     } else {
         for (int32_t t = t0; t < t1; ++t) {
             const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1];
             for (int i = tid; i < kOpTile; i += 256) {
                 const bool ok = i < nu;
-                MK[0][i][0] = ok ? om[2 * (int64_t)(u0 + i)] : 0ull;
-                MK[0][i][1] = ok ? om[2 * (int64_t)(u0 + i) + 1] : 0ull;
+                MK0[i][0] = ok ? om[2 * (int64_t)(u0 + i)] : 0ull;
+                MK0[i][1] = ok ? om[2 * (int64_t)(u0 + i) + 1] : 0ull;
             }
             for (int i = tid; i < kOpTile * 2 * K; i += 256) {
                 const int u = i / (2 * K), bh = i % (2 * K);
-                pb[0][u][bh / K][bh % K] = u < nu ? Sop[(int64_t)(u0 + u) * 4 * K + bh] * kLog2e : 0.f;
+                pb0[u][bh / K][bh % K] = u < nu ? Sop[(int64_t)(u0 + u) * 4 * K + bh] * kLog2e : 0.f;
             }
             for (int i = tid; i < kOpTile * (F / 4); i += 256) {
                 const int u = i / (F / 4), c = (i % (F / 4)) * 4;
                 float v[4] = {0.f, 0.f, 0.f, 0.f};
                 if (u < nu) load_ch<4, false>(A.Y_op, ((int64_t)r * A.n_op + u0 + u) * 2 * F + F + c, v);
-                for (int q = 0; q < 4; ++q) Ys[0][u * YS + c + q] = v[q];
+                for (int q = 0; q < 4; ++q) Ys0[u * YS + c + q] = v[q];
             }
             __syncthreads();
             // fp32 16x16x4 products: k = 4 (op, bit) pairs per step, two ops per
             // step; lane l supplies op 2s + l / 32 with bit (l / 16) % 2
             for (int s = 0; s < kOpTile / 2; ++s) {
                 const int ul = 2 * s + (lane >> 5);
-                const uint64_t pr = MK[0][ul][0], bt = b ? MK[0][ul][1] : ~MK[0][ul][1];   // bt bit j: link bit equals b
+                const uint64_t pr = MK0[ul][0], bt = b ? MK0[ul][1] : ~MK0[ul][1];   // bt bit j: link bit equals b
                 float bv[NCB];
 #pragma unroll
                 for (int cb = 0; cb < NCB; ++cb) {
                     const int col = cbase + cb * 16 + (lane & 15);
                     // fp32 rows store Y + c'
-                    const float yc = static_cast<float>(Ys[0][ul * YS + col]);
+                    const float yc = static_cast<float>(Ys0[ul * YS + col]);
                     bv[cb] = msg_act<ELU>(b ? yc + Uv[cb] : yc);
                 }
                 float pu[HPW];
 #pragma unroll
-                for (int hh = 0; hh < HPW; ++hh) pu[hh] = pb[0][ul][b][h0 + hh];
+                for (int hh = 0; hh < HPW; ++hh) pu[hh] = pb0[ul][b][h0 + hh];
                 const uint64_t sel = pr & bt;
 #pragma unroll
                 for (int rb = 0; rb < 4; ++rb) {
