@@ -375,42 +375,54 @@ __global__ void __launch_bounds__(256) gemm_f32(GemmArgs G) {
 
 template <int JPH>
 __global__ void __launch_bounds__(256) gemm_bf16(GemmArgs G) {
-    constexpr int BK = kBkBf16, LS = BK + 8;   // row-major LDS rows of BK + 8 bf16
-    // k-chunk buffers As[2][BM * LS], Bs[2][BN * LS]; the epilogue reuses the
-    // space for the output tile and the column constants
-    constexpr int SM = 2 * BM * LS + 2 * BN * LS;
+    constexpr int BK = kBkBf16;
+    static_assert(BK == 32, "four 16-byte chunks per LDS row");
+    // k-chunk buffers As[2][BM * BK], Bs[2][BN * BK]: unpadded rows whose four
+    // 16-byte chunks are XOR-swizzled (chunk c of row r at c ^ sw(r)) so that
+    // neither the loader's stores (4 threads per row) nor the operand reads
+    // (16 rows, one chunk) meet a bank twice; the epilogue reuses the space
+    // for the output tile and the column constants
+    constexpr int SM = 2 * BM * (BK + 8) + 2 * BN * (BK + 8);
     static_assert(BM * kTileStride * 2 + 4 * BN * 4 <= SM * 2, "epilogue tile must fit the k-chunk buffers");
     __shared__ __attribute__((aligned(16))) uint16_t sm[SM];
-    uint16_t (*As)[BM * LS] = reinterpret_cast<uint16_t (*)[BM * LS]>(sm);
-    uint16_t (*Bs)[BN * LS] = reinterpret_cast<uint16_t (*)[BN * LS]>(sm + 2 * BM * LS);
+    uint16_t (*As)[BM * BK] = reinterpret_cast<uint16_t (*)[BM * BK]>(sm);
+    uint16_t (*Bs)[BN * BK] = reinterpret_cast<uint16_t (*)[BN * BK]>(sm + 2 * BM * BK);
+    auto sw = [](int r) { return ((r >> 1) ^ (r >> 2)) & 3; };
     const Tile t = tile_of(G);
     const GemmSide S = t.sd ? G.side[1] : G.side[0];
     const uint16_t *__restrict__ H = static_cast<const uint16_t *>(S.H);
-    uint16_t *__restrict__ Y = static_cast<uint16_t *>(S.Y);
     const int F = G.F;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    constexpr int NQ = BK / 16;            // 16-byte loads per thread and operand (two threads per row)
-    const int lr = tid >> 1, lk = (tid & 1) * (BK / 2);
-    const int64_t gm = t.m0 + lr;
-    const bool aok = gm < S.rows;
-    const uint16_t *arow = H + (aok ? gm : 0) * F;
-    const int gn = t.n0 + lr;
-    const uint16_t *brow = gn < F ? static_cast<const uint16_t *>(S.B0) + (size_t)gn * S.ldb
-                                  : static_cast<const uint16_t *>(S.B1) + (size_t)(gn - F) * S.ldb;
-    u4 ra[NQ], rb[NQ];
+    // loader: thread -> rows tid/4 and tid/4 + 64, 16-byte chunk tid % 4
+    const int lc = tid & 3;
+    const uint16_t *arow[2], *brow[2];
+    bool aok[2];
+    int loff[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const int lr = (tid >> 2) + 64 * q;
+        const int64_t gm = t.m0 + lr;
+        aok[q] = gm < S.rows;
+        arow[q] = H + (aok[q] ? gm : 0) * F + 8 * lc;
+        const int gn = t.n0 + lr;
+        brow[q] = (gn < F ? static_cast<const uint16_t *>(S.B0) + (size_t)gn * S.ldb
+                          : static_cast<const uint16_t *>(S.B1) + (size_t)(gn - F) * S.ldb) + 8 * lc;
+        loff[q] = lr * BK + 8 * (lc ^ sw(lr));
+    }
+    u4 ra[2], rb[2];
     auto gload = [&](int k0) {
 #pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            ra[q] = aok ? *reinterpret_cast<const u4 *>(arow + k0 + lk + 8 * q) : u4{0u, 0u, 0u, 0u};
-            rb[q] = *reinterpret_cast<const u4 *>(brow + k0 + lk + 8 * q);
+        for (int q = 0; q < 2; ++q) {
+            ra[q] = aok[q] ? *reinterpret_cast<const u4 *>(arow[q] + k0) : u4{0u, 0u, 0u, 0u};
+            rb[q] = *reinterpret_cast<const u4 *>(brow[q] + k0);
         }
     };
     auto sstore = [&](int buf) {
 #pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            *reinterpret_cast<u4 *>(&As[buf][lr * LS + lk + 8 * q]) = ra[q];
-            *reinterpret_cast<u4 *>(&Bs[buf][lr * LS + lk + 8 * q]) = rb[q];
+        for (int q = 0; q < 2; ++q) {
+            *reinterpret_cast<u4 *>(&As[buf][loff[q]]) = ra[q];
+            *reinterpret_cast<u4 *>(&Bs[buf][loff[q]]) = rb[q];
         }
     };
     f4 acc[4][4];
@@ -422,25 +434,27 @@ __global__ void __launch_bounds__(256) gemm_bf16(GemmArgs G) {
     sstore(0);
     __syncthreads();
     const int nk = F / BK;
+    const int kc4 = lane >> 4;   // this lane's chunk of a 32-wide step
+    int aoff[4], boff[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int ra_ = wm * 64 + i * 16 + (lane & 15), rb_ = wn * 64 + i * 16 + (lane & 15);
+        aoff[i] = ra_ * BK + 8 * (kc4 ^ sw(ra_));
+        boff[i] = rb_ * BK + 8 * (kc4 ^ sw(rb_));
+    }
     for (int kc = 0; kc < nk; ++kc) {
         const int buf = kc & 1;
         if (kc + 1 < nk) gload((kc + 1) * BK);
+        bf8 a[4], b[4];
 #pragma unroll
-        for (int kk = 0; kk < BK; kk += 32) {
-            const int koff = kk + 8 * (lane >> 4);
-            bf8 a[4], b[4];
+        for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const bf8 *>(&As[buf][aoff[i]]);
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                a[i] = *reinterpret_cast<const bf8 *>(&As[buf][(wm * 64 + i * 16 + (lane & 15)) * LS + koff]);
+        for (int j = 0; j < 4; ++j) b[j] = *reinterpret_cast<const bf8 *>(&Bs[buf][boff[j]]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                b[j] = *reinterpret_cast<const bf8 *>(&Bs[buf][(wn * 64 + j * 16 + (lane & 15)) * LS + koff]);
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-        }
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
         if (kc + 1 < nk) sstore(buf ^ 1);
         __syncthreads();
     }
