@@ -101,11 +101,17 @@ struct AggArgs {
     int32_t rec_mode;                 // 0: records per 256-entry chunk, 1: per tile group
     int32_t n_groups;
     const int32_t *groups, *group_off;   // tile groups of the device<-op blocks
+    // written once per forward pass by prep_tiles_x: per op tile (first op,
+    // op count, topology, first op<-op CSR entry, op<-op entries, first
+    // device, device count, 0), and the op<-op edge features in CSR order
+    int32_t *tile_ext;                // [n_tiles][8]
+    float *xcsr; int64_t s_xcsr;      // [xrep][nnz of B0], xrep = 1 (shared features) or R
 };
 
 // MFMA path (agg_mfma.hip)
 bool mfma_path_supported(int F, int K, int64_t n_op, int esz);
 void launch_pack_masks(const AggArgs &A, hipStream_t st);
+void launch_prep_tiles_x(const AggArgs &A, int64_t nnz0, hipStream_t st);
 bool launch_agg_mfma(int F, int K, bool bf, const AggArgs &A, hipStream_t st);
 
 // CPL consecutive channels starting at element `off` (fp32 or bf16 storage);

@@ -69,6 +69,26 @@ __global__ void __launch_bounds__(256) pack_op_masks(AggArgs A) {
 // (heads wider than 64 channels): per row, S = (p0, p1, q_od, q_same) and, for
 // device rows, the message table T (bit 0 / 1; fp32, or its exact bf16
 // splits in the bf16 variant).  One wavefront per row.
+// Once per forward pass: the op tiles' descriptors (so an op-destination block
+// finds its CSR range and device group in one load round) and the op<-op
+// edge features in CSR order (so it loads them without the edge-id gather).
+__global__ void __launch_bounds__(256) prep_tiles_x(AggArgs A, int64_t nnz0, int32_t xrep) {
+    const int64_t n = (int64_t)A.n_tiles + (int64_t)xrep * nnz0;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+        if (i < A.n_tiles) {
+            const int32_t t = (int32_t)i;
+            const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1], g = A.tiles[3 * t + 2];
+            const int32_t eb = A.rp[0][u0], d0 = A.dev_off[g];
+            int32_t *o = A.tile_ext + 8 * (int64_t)t;
+            o[0] = u0; o[1] = nu; o[2] = g; o[3] = eb; o[4] = A.rp[0][u0 + nu] - eb;
+            o[5] = d0; o[6] = A.dev_off[g + 1] - d0; o[7] = 0;
+        } else {
+            const int64_t j = i - A.n_tiles, r = j / nnz0, e = j % nnz0;
+            A.xcsr[j] = A.x_oo[r * A.s_oo + A.eid[0][e]];
+        }
+    }
+}
+
 template <int F, int K, bool BF, bool ELU = false>
 __global__ void __launch_bounds__(256) prep_rows(AggArgs A, int dev_side) {
     constexpr int CPL = F / 64, LPH = 64 / K;
@@ -484,9 +504,11 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
     // device message table share one L2
     const uint32_t lb = xcd_swizzle(blockIdx.y * gridDim.x + blockIdx.x, gridDim.x * gridDim.y);
     const int32_t t = (int32_t)(lb % gridDim.x), r = (int32_t)(lb / gridDim.x);
-    const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1], g = A.tiles[3 * t + 2];
-    const int32_t d0 = A.dev_off[g], Mg = A.dev_off[g + 1] - d0;
-    const float *xo = A.x_oo + (int64_t)r * A.s_oo;
+    const int4 te0 = *reinterpret_cast<const int4 *>(A.tile_ext + 8 * (int64_t)t);
+    const int4 te1 = *reinterpret_cast<const int4 *>(A.tile_ext + 8 * (int64_t)t + 4);
+    const int32_t u0 = te0.x, nu = te0.y;
+    const int32_t d0 = te1.y, Mg = te1.z;
+    const float *xc = A.xcsr + (int64_t)r * A.s_xcsr;   // op<-op edge features in CSR order
     const float *Sop = A.Sop + (int64_t)r * A.n_op * 4 * K;
     const float slope = A.slope;
     const int cbase = wave * WC;
@@ -511,15 +533,15 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
 
     // ---- prologue: every global load is issued before the first LDS store
     // (the logits go to the exp2 domain: LeakyReLU commutes with log2(e) > 0)
-    const int32_t eb = A.rp[0][u0];
-    const int32_t ntot = A.rp[0][u0 + nu] - eb;    // the tile's op<-op entries: one CSR range
+    const int32_t eb = te0.w;
+    const int32_t ntot = te1.x;                    // the tile's op<-op entries: one CSR range
     const int32_t ne = min(ntot, ECAP);
     {
         constexpr int NQ = (kOpTile * K + 255) / 256, NP = (64 * 2 * K + 255) / 256, NE = (ECAP + 255) / 256;
         int32_t rp0 = 0, rp1 = 0;
         uint64_t om0 = 0, om1 = 0;
         float q2v[NQ], pv[NP], exv[NE];
-        int32_t ecv[NE], eiv[NE];
+        int32_t ecv[NE];
         if (tid <= nu) rp0 = A.rp[0][u0 + tid] - eb;
         if (tid < nu) rp1 = A.rp[0][u0 + tid + 1] - eb;
         if (tid < nu) {
@@ -542,10 +564,8 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
         for (int k = 0; k < NE; ++k) {
             const int i = tid + 256 * k;
             ecv[k] = i < ne ? A.col[0][eb + i] : 0;
-            eiv[k] = i < ne ? A.eid[0][eb + i] : 0;
+            exv[k] = i < ne ? xc[eb + i] : 0.f;
         }
-#pragma unroll
-        for (int k = 0; k < NE; ++k) exv[k] = (tid + 256 * k) < ne ? xo[eiv[k]] : 0.f;
         if (tid <= nu) Erp[tid] = rp0;
         if (tid < kOpTile) { pres[tid] = om0; bits[tid] = om1; }
 #pragma unroll
@@ -639,7 +659,7 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
                 __syncthreads();
                 const int32_t n = min(ntot - cb0, ECAP);
                 for (int i = tid; i < n; i += 256) {
-                    Ecx[i] = int2{A.col[0][eb + cb0 + i], __float_as_int(xo[A.eid[0][eb + cb0 + i]])};
+                    Ecx[i] = int2{A.col[0][eb + cb0 + i], __float_as_int(xc[eb + cb0 + i])};
                 }
                 if (tid < nu)
                     for (int32_t i = max(Erp[tid], cb0); i < min(Erp[tid + 1], cb0 + n); ++i)
@@ -987,6 +1007,14 @@ bool dispatch_mfma_heads(int K, const AggArgs &A, hipStream_t st) {
 // transforms within 32-bit byte offsets of its base (the op<-op gathers)
 bool mfma_path_supported(int F, int K, int64_t n_op, int esz) {
     return K >= 1 && F / K >= 16 && K <= 16 && n_op * 2 * F * esz < (int64_t(1) << 32);
+}
+
+void launch_prep_tiles_x(const AggArgs &A, int64_t nnz0, hipStream_t st) {
+    const int32_t xrep = A.s_xcsr ? A.R : 1;
+    const int64_t n = (int64_t)A.n_tiles + (int64_t)xrep * nnz0;
+    if (n == 0) return;
+    const unsigned blocks = (unsigned)std::min<int64_t>((n + 255) / 256, 4096);
+    prep_tiles_x<<<blocks, 256, 0, st>>>(A, nnz0, xrep);
 }
 
 void launch_pack_masks(const AggArgs &A, hipStream_t st) {

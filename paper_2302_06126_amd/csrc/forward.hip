@@ -383,9 +383,13 @@ size_t carve_fwd(const tag_graph *g, const tag_model_dims *d, int32_t R, void *b
         // fp32 message table [R n_dev][2][F], or its three bf16 split parts [3][R n_dev][F]
         L->T = c.take<float>((size_t)R * g->n_dev * (d->dtype == TAG_BF16 ? 3 : 2) * F);
         L->Sop = c.take<float>((size_t)R * g->n_op * 4 * d->heads);
+        L->tile_ext = c.take<int32_t>((size_t)std::max<int32_t>(g->n_tiles, 1) * 8);
+        L->xcsr = c.take<float>((size_t)R * std::max<int64_t>(g->nnz[0], 1));
     } else {
         L->omask = nullptr;
         L->Sdev = L->T = L->Sop = nullptr;
+        L->tile_ext = nullptr;
+        L->xcsr = nullptr;
     }
     return c.used;
 }
@@ -532,7 +536,13 @@ tag_status forward_run(const tag_graph *g, const tag_model_dims *dims, const tag
     A.n_groups = g->n_groups; A.groups = g->groups_d; A.group_off = g->group_off_d;
     A.omask = L.omask; A.Sdev = L.Sdev; A.T = L.T; A.Sop = L.Sop;
     A.rec_mode = L.mfma ? 1 : 0;
-    if (L.mfma) launch_pack_masks(A, stream);
+    A.tile_ext = L.tile_ext;
+    A.xcsr = L.xcsr;
+    A.s_xcsr = x->stride_oo ? g->nnz[0] : 0;
+    if (L.mfma) {
+        launch_pack_masks(A, stream);
+        launch_prep_tiles_x(A, g->nnz[0], stream);
+    }
 
     // the transform epilogue forms the attention terms when a head fits one
     // wavefront's 64 columns

@@ -16,6 +16,8 @@ struct FwdLayout {
     bool mfma;
     uint64_t *omask;
     float *Sdev, *T, *Sop;
+    int32_t *tile_ext;             // per op tile descriptors (see AggArgs)
+    float *xcsr;                   // op<-op edge features in CSR order
 };
 
 tag_status check_dims(const tag_model_dims *d);
