@@ -101,6 +101,10 @@ def stage_rooflines(name, wl, topo, R, info, n_slices, n_query, stage_ms) -> tup
                "algorithmic_hbm_frac": round(byts / avg_s / 1e9 / PEAK_HBM_GBS, 4)}
         if stage == "transform":
             rec["mfma_frac"] = round(flops / avg_s / 1e12 / PEAK_TFLOPS[wl.dtype], 4)
+        elif stage.startswith("agg_") and flops > 0.0:
+            # message formation, scores and aggregates on the vector ALUs
+            rec["valu_tflops"] = round(flops / avg_s / 1e12, 3)
+            rec["valu_frac"] = round(flops / avg_s / 1e12 / PEAK_VALU_F32_TFLOPS, 4)
         tr = measured_traffic(name, stage)
         if tr is not None:
             rec["counter_gbs"] = round(tr / avg_s / 1e9, 1)
@@ -772,6 +776,12 @@ def main() -> int:
     if stage == "transform" and flops / byts >= peak_fl * 1e12 / (PEAK_HBM_GBS * 1e9):
         roof = {"bound": "mfma", "achieved": round(fl_tf, 3), "peak": peak_fl, "unit": "TFLOP/s",
                 "frac": round(fl_tf / peak_fl, 4)}
+    elif stage.startswith("agg_") and fl_tf / PEAK_VALU_F32_TFLOPS > bw_gbs / PEAK_HBM_GBS:
+        # the aggregation's vector arithmetic is the nearer roof: bound by the
+        # fp32 VALU (non-packed) rate
+        roof = {"bound": "alu", "achieved": round(fl_tf, 3), "peak": round(PEAK_VALU_F32_TFLOPS, 2),
+                "unit": "TFLOP/s", "frac": round(fl_tf / PEAK_VALU_F32_TFLOPS, 4),
+                "hbm_gbs": round(bw_gbs, 1), "hbm_frac": round(bw_gbs / PEAK_HBM_GBS, 4)}
     else:
         roof = {"bound": "hbm", "achieved": round(bw_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(bw_gbs / PEAK_HBM_GBS, 4)}
