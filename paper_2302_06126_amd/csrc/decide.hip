@@ -114,41 +114,11 @@ __device__ __forceinline__ float slice_score(const DecArgs &A, const float *urg,
     return A.b2[0] + s;
 }
 
-// one block per query: scores, softmax prior, argmax, decoded decision.
-// Consecutive queries (usually one candidate's, reading the same u) run on
-// one XCD, so each candidate's u is fetched into one L2 rather than all eight.
-__global__ void __launch_bounds__(kScoreThreads) dec_score(DecArgs A) {
-    extern __shared__ float sh[];   // v[Hx] | w2[H]
-    __shared__ float red_m[kScoreThreads];
-    __shared__ int32_t red_i[kScoreThreads];
-    __shared__ float red_z[kScoreThreads];
-    const int32_t q = (int32_t)xcd_swizzle(blockIdx.x, gridDim.x);
-    int32_t r, g, op;
-    const bool ok = query_valid(A, q, &r, &g, &op);
-    if (!ok) {
-        if (threadIdx.x == 0) {
-            A.argmax[q] = -1;
-            A.best[q] = __builtin_nanf("");
-            if (A.dec) A.dec[q] = tag_decision{0, 0, 0, 0, 0};
-        }
-        if (A.prior)
-            for (int32_t a = threadIdx.x; a < A.S; a += blockDim.x) A.prior[(int64_t)q * A.S + a] = 0.f;
-        return;
-    }
-    float *vq = sh, *w2s = sh + A.Hx;
-    for (int h = threadIdx.x; h < A.Hx; h += blockDim.x) vq[h] = A.v[(int64_t)q * A.Hx + h];
-    for (int h = threadIdx.x; h < A.H; h += blockDim.x) w2s[h] = A.w2[h];
-    __syncthreads();
-    const float *urg = A.u + ((int64_t)r * A.G + g) * A.Hx * A.S;
-    // pass 1: max (lowest index on ties) and the running sum of exponentials
-    float m = -INFINITY, z = 0.f;
-    int32_t im = INT32_MAX;
-    for (int32_t a = threadIdx.x; a < A.S; a += blockDim.x) {
-        float s = slice_score(A, urg, vq, w2s, a);
-        if (A.prior) A.prior[(int64_t)q * A.S + a] = s;
-        if (s > m) { z = z * __expf(m - s) + 1.f; m = s; im = a; }
-        else z += __expf(s - m);
-    }
+// Max (lowest index on ties) and sum of exponentials over the block's
+// per-thread partials, then the prior, argmax and decoded decision of query
+// q whose raw scores are already in A.prior (when it is given).
+__device__ void finish_query(const DecArgs &A, int32_t q, int32_t g, float m, int32_t im, float z,
+                             float *red_m, int32_t *red_i, float *red_z) {
     red_m[threadIdx.x] = m; red_i[threadIdx.x] = im; red_z[threadIdx.x] = z;
     __syncthreads();
     for (int off = kScoreThreads / 2; off > 0; off >>= 1) {
@@ -165,6 +135,7 @@ __global__ void __launch_bounds__(kScoreThreads) dec_score(DecArgs A) {
     }
     const float M = red_m[0], Z = red_z[0];
     const int32_t best = red_i[0];
+    __syncthreads();   // the reduction arrays are reused by the next query
     if (A.prior) {
         const float inv = 1.f / Z;
         for (int32_t a = threadIdx.x; a < A.S; a += blockDim.x) {
@@ -189,6 +160,112 @@ __global__ void __launch_bounds__(kScoreThreads) dec_score(DecArgs A) {
             const int pc = __popcll(msk);
             A.dec[q] = tag_decision{msk, o, o == 3 ? 1 : pc, o == 0 ? 0 : (o == 1 ? 1 : 2), o == 2 ? 1 : 0};
         }
+    }
+}
+
+__device__ void invalid_query(const DecArgs &A, int32_t q) {
+    if (threadIdx.x == 0) {
+        A.argmax[q] = -1;
+        A.best[q] = __builtin_nanf("");
+        if (A.dec) A.dec[q] = tag_decision{0, 0, 0, 0, 0};
+    }
+    if (A.prior)
+        for (int32_t a = threadIdx.x; a < A.S; a += blockDim.x) A.prior[(int64_t)q * A.S + a] = 0.f;
+}
+
+// QB consecutive queries per block: scores, softmax prior, argmax, decoded
+// decision.  When the block's queries are all valid and read one
+// candidate's slice terms u (consecutive queries usually do), every u value
+// is loaded once for all QB of them; otherwise the queries are taken one by
+// one.  Consecutive blocks run on one XCD, so a candidate's u is fetched into
+// one L2 rather than all eight.
+template <int QB>
+__global__ void __launch_bounds__(kScoreThreads) dec_score(DecArgs A) {
+    extern __shared__ float sh[];   // v[QB][Hx] | w2[H]
+    __shared__ float red_m[kScoreThreads];
+    __shared__ int32_t red_i[kScoreThreads];
+    __shared__ float red_z[kScoreThreads];
+    const int32_t q0 = (int32_t)xcd_swizzle(blockIdx.x, gridDim.x) * QB;
+    const int32_t nq = min(QB, A.Q - q0);
+    float *w2s = sh + QB * A.Hx;
+    for (int h = threadIdx.x; h < A.H; h += blockDim.x) w2s[h] = A.w2[h];
+    int32_t rq[QB], gq[QB];
+    bool shared = nq == QB;
+#pragma unroll
+    for (int i = 0; i < QB; ++i) {
+        int32_t op;
+        const bool ok = i < nq && query_valid(A, q0 + i, &rq[i], &gq[i], &op);
+        shared = shared && ok && rq[i] == rq[0] && gq[i] == gq[0];
+    }
+    if (shared && QB > 1) {
+        for (int i = 0; i < QB; ++i)
+            for (int h = threadIdx.x; h < A.Hx; h += blockDim.x) sh[i * A.Hx + h] = A.v[(int64_t)(q0 + i) * A.Hx + h];
+        __syncthreads();
+        const float *urg = A.u + ((int64_t)rq[0] * A.G + gq[0]) * A.Hx * A.S;
+        float m[QB], z[QB];
+        int32_t im[QB];
+#pragma unroll
+        for (int i = 0; i < QB; ++i) { m[i] = -INFINITY; z[i] = 0.f; im[i] = INT32_MAX; }
+        for (int32_t a = threadIdx.x; a < A.S; a += blockDim.x) {
+            float sc[QB];
+            if (A.H == 0) {
+#pragma unroll
+                for (int i = 0; i < QB; ++i) sc[i] = A.b2[0] + urg[a] + sh[i * A.Hx];
+            } else {
+                // independent loads in batches of 16 hidden units, summed in order
+#pragma unroll
+                for (int i = 0; i < QB; ++i) sc[i] = 0.f;
+                int h = 0;
+                for (; h + 16 <= A.H; h += 16) {
+                    float uu[16];
+#pragma unroll
+                    for (int k = 0; k < 16; ++k) uu[k] = urg[(int64_t)(h + k) * A.S + a];
+#pragma unroll
+                    for (int k = 0; k < 16; ++k)
+#pragma unroll
+                        for (int i = 0; i < QB; ++i)
+                            sc[i] = fmaf(w2s[h + k], fmaxf(uu[k] + sh[i * A.Hx + h + k], 0.f), sc[i]);
+                }
+                for (; h < A.H; ++h) {
+                    const float uu = urg[(int64_t)h * A.S + a];
+#pragma unroll
+                    for (int i = 0; i < QB; ++i) sc[i] = fmaf(w2s[h], fmaxf(uu + sh[i * A.Hx + h], 0.f), sc[i]);
+                }
+#pragma unroll
+                for (int i = 0; i < QB; ++i) sc[i] += A.b2[0];
+            }
+#pragma unroll
+            for (int i = 0; i < QB; ++i) {
+                if (A.prior) A.prior[(int64_t)(q0 + i) * A.S + a] = sc[i];
+                if (sc[i] > m[i]) { z[i] = z[i] * __expf(m[i] - sc[i]) + 1.f; m[i] = sc[i]; im[i] = a; }
+                else z[i] += __expf(sc[i] - m[i]);
+            }
+        }
+        for (int i = 0; i < QB; ++i) finish_query(A, q0 + i, gq[0], m[i], im[i], z[i], red_m, red_i, red_z);
+        return;
+    }
+    for (int i = 0; i < nq; ++i) {
+        const int32_t q = q0 + i;
+        int32_t r, g, op;
+        if (!query_valid(A, q, &r, &g, &op)) {
+            invalid_query(A, q);
+            continue;
+        }
+        float *vq = sh;
+        __syncthreads();   // the previous query's reads of v are done
+        for (int h = threadIdx.x; h < A.Hx; h += blockDim.x) vq[h] = A.v[(int64_t)q * A.Hx + h];
+        __syncthreads();
+        const float *urg = A.u + ((int64_t)r * A.G + g) * A.Hx * A.S;
+        // max (lowest index on ties) and the running sum of exponentials
+        float m = -INFINITY, z = 0.f;
+        int32_t im = INT32_MAX;
+        for (int32_t a = threadIdx.x; a < A.S; a += blockDim.x) {
+            float s = slice_score(A, urg, vq, w2s, a);
+            if (A.prior) A.prior[(int64_t)q * A.S + a] = s;
+            if (s > m) { z = z * __expf(m - s) + 1.f; m = s; im = a; }
+            else z += __expf(s - m);
+        }
+        finish_query(A, q, g, m, im, z, red_m, red_i, red_z);
     }
 }
 
@@ -289,7 +366,11 @@ tag_status decide_run(const tag_graph *g, const tag_model_dims *dims, const tag_
     dec_query_rows<<<grid_for(A.Q), 256, 0, stream>>>(A, L.qrow);
     launch_small_gemm(SmallGemm{E_op, A.F, A.Q, L.qrow, A.F, A.P + A.F, din, Hx, nullptr, 0, A.v, Hx, 0}, stream);
     dec_slice<<<(unsigned)((int64_t)A.R * A.G * ((Hx + kSliceH - 1) / kSliceH)), 256, 0, stream>>>(A);
-    dec_score<<<(unsigned)A.Q, kScoreThreads, sizeof(float) * (Hx + H), stream>>>(A);
+    // four queries per block once there are enough blocks to fill the GPU
+    if (A.Q >= 8192)
+        dec_score<4><<<(unsigned)((A.Q + 3) / 4), kScoreThreads, sizeof(float) * (4 * Hx + H), stream>>>(A);
+    else
+        dec_score<1><<<(unsigned)A.Q, kScoreThreads, sizeof(float) * (Hx + H), stream>>>(A);
     prof_end(TAG_STAGE_DECIDE, stream);
     return launch_status("tag_gnn_decide");
 }

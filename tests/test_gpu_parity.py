@@ -336,6 +336,39 @@ def test_decide_on_identical_embeddings(m_dev, f, H, S, full):
         assert abs(res["prior"][q].sum() - 1.0) < 1e-5
 
 
+def test_decide_many_queries_four_per_block():
+    """8,203 queries (enough for four queries per block): queries sorted by
+    candidate, so most blocks share one candidate's slice terms; blocks that
+    straddle a candidate, hold an invalid query, or are the ragged last one
+    take the queries one by one.  Sampled queries against the oracle."""
+    topo, R, E_op, E_dev, w, masks, opts = _decide_case(16, 128, 128, 256, 11, False)
+    g = P.Graph([topo])
+    m = P.Model(w, f=128, heads=4, layers=1, f_op=42, dec_hidden=128)
+    rng = np.random.default_rng(5)
+    Q = 8203
+    qr = np.sort(rng.integers(0, R, Q)).astype(np.int32)
+    qo = rng.integers(0, topo.n_op, Q).astype(np.int32)
+    bad = rng.choice(Q, 9, replace=False)
+    qo[bad[:5]] = topo.n_op + 3          # op out of range
+    qr[bad[5:]] = -1                     # candidate out of range
+    res = P.decide(g, m, dev_tensor(E_op), dev_tensor(E_dev), masks, opts, qr, np.zeros(Q, np.int32), qo)
+    assert np.all(res["argmax"][bad] == -1) and np.all(np.isnan(res["best"][bad]))
+    edges = np.flatnonzero(np.diff(qr)) + 1          # first queries of a new candidate
+    sample = np.unique(np.concatenate([edges - 1, edges, [0, Q - 1, Q - 2, Q - 4],
+                                       rng.choice(Q, 200, replace=False)]))
+    sample = [int(q) for q in sample if q not in set(bad.tolist())]
+    for q in sample:
+        od = oracle.decide(E_op[qr[q]].astype(np.float64), E_dev[qr[q]].astype(np.float64), masks, opts,
+                           qo[q:q + 1], w, f=128, dec_hidden=128, n_dev=16)
+        if decide_gap_ok(od["prior"][0], od["best"][0], 1e-5):
+            assert res["argmax"][q] == od["argmax"][0], q
+            for k in ("mask", "option", "replicas", "sync", "sfb"):
+                assert res[k][q] == od[k][0], (q, k)
+        np.testing.assert_allclose(res["best"][q], od["best"][0], rtol=1e-5, atol=1e-5)
+        np.testing.assert_allclose(res["prior"][q], od["prior"][0], rtol=1e-4, atol=1e-7)
+    say(f"four-per-block decide: {len(sample)} sampled queries match")
+
+
 def test_decide_invalid_queries_and_high_mask_bits():
     topo, R, E_op, E_dev, w, masks, opts = _decide_case(6, 64, 64, 40, 1)
     g = P.Graph([topo])
