@@ -4,17 +4,18 @@
 // (Y + c' starts every message ReLU(Y + c' + U x)); the bf16 kernel stores
 // bf16(Y) alone, the rounded product of the bf16 variant, and the message
 // kernels add c' in fp32.  The attention destination terms use Y itself.
-// One launch covers both row sets of a layer.  128 x 128 block tiles, four
-// wavefronts of 64 x 64, k-chunks staged through LDS with the next chunk's
-// global loads in flight while the current one feeds the matrix cores.  The
-// 1-D block order is XCD-swizzled so the column tiles of one row tile (which
-// re-read the same rows of H) land on the same XCD and share its L2.
+// One launch covers both row sets of a layer, in 128 x 128 block tiles whose
+// k-chunks pass through LDS with the next chunk's global loads in flight
+// while the current one feeds the matrix cores.  The 1-D block order is
+// XCD-swizzled so the column tiles of one row tile (which re-read the same
+// rows of H) land on the same XCD and share its L2.
 //
-// MFMA 16x16 operand layout: lane l supplies row/column l % 16 of A/B and
-// k-slice l / 16 (4 k per slice for fp32 16x16x4, 8 for bf16 16x16x32);
-// result register v of lane l holds row 4 (l / 16) + v, column l % 16.  The
-// fp32 kernel feeds the weights as the first operand and the hidden rows as
-// the second, so its result blocks are tiles of Y^T (see store_tile); the bf16
+// Both kernels run on 16x16x32 bf16 MFMAs; the fp32 kernel contracts exact
+// three-way bf16 splits of its fp32 operands.  Operand layout: lane l
+// supplies row/column l % 16 of A/B and the 8-wide k-slice l / 16; result
+// register v of lane l holds row 4 (l / 16) + v, column l % 16.  The fp32
+// kernel feeds the weights as the first operand and the hidden rows as the
+// second, so its result blocks are tiles of Y^T (see store_rows); the bf16
 // kernel takes Y = H W^T directly (store_tile_bf16).
 #include "tag_internal.hpp"
 #include "transform.hpp"
@@ -196,60 +197,53 @@ __device__ void store_tile_bf16(const GemmArgs &G, const Tile &t, int wm, int wn
     }
 }
 
-// Epilogue of the fp32 kernel.  The products are taken as Y^T = W H^T (operands swapped), so
-// result register v of block (j, i) in lane l holds output row 16 i + l % 16
-// and output column 16 j + 4 (l / 16) + v of the wavefront's 64 x 64 tile:
-// each lane owns four consecutive columns of one row per block, written with
-// one vector store, and a head's attention sums reduce inside the lane and
-// then over the four lanes l % 16 + {0, 16, 32, 48}.
+// Epilogue of the fp32 kernel.  The products are taken as Y^T = W H^T
+// (weights as the first MFMA operand), so result register v of block (j, i)
+// in lane l holds output row 16 i + l % 16 and output column 16 j + 4 (l / 16)
+// + v of a 64-column slab: each lane owns four consecutive columns of one row
+// per block, written with one vector store, and a head's attention sums
+// reduce inside the lane and then over the four lanes l % 16 + {0, 16, 32, 48}.
 //
-// The per-column constants of the wavefront's 64 columns are staged in LDS
-// (`cst`, 256 floats per wavefront, free once the k loop is done) before any
-// store is issued: on this GPU a wait for an outstanding load also waits for
-// earlier stores, so no global load may follow the first store.
-template <int JPH, bool ELU = false>
-__device__ void store_tile(const GemmArgs &G, const Tile &t, int wm, int wn, int lane, const f4 (&acc)[4][4],
-                           float *cst) {
+// The per-column constants are read from LDS (`cst[kind * CS + column]`,
+// kinds c', a, a~, U; CS columns per kind), staged before any store is
+// issued: on this GPU a wait for an outstanding load also waits for earlier
+// stores, so no global load may follow the first store.
+//
+// One call covers NI row blocks of 16 (rows rbase + 16 i, rbase carrying the
+// lane's l % 16) and the 64 columns col0 .. col0 + 63, which lie in one
+// relation half (F is a multiple of 64), from accumulator blocks
+// acc[J0 .. J0 + 3][0 .. NI - 1].
+template <int JPH, bool ELU, int NI, int CS, int J0, int NJ>
+__device__ void store_rows(const GemmArgs &G, const Tile &t, int64_t rbase, int col0, int lane,
+                           const f4 (&acc)[NJ][NI], const float *cst) {
+    static_assert(J0 + 4 <= NJ, "four column blocks");
     const GemmPrep &P = G.prep;
     const int64_t rows = t.sd ? G.side[1].rows : G.side[0].rows;
     const int F = G.F, K = P.K, D = 16 * (JPH > 0 ? JPH : 1);
     const int64_t ldy = 2 * F;
     void *Yp = t.sd ? G.side[1].Y : G.side[0].Y;
-    const int col0 = t.n0 + wn * 64;
     const bool od = col0 >= F;
     const int cw = od ? col0 - F : col0;           // first channel of the relation
     const int g = lane >> 4;
-    const int64_t rbase = t.m0 + wm * 64 + (lane & 15);
-    const float *cp = od ? P.cp_od : P.cp_same[t.sd];
     const bool dev_od = od && t.sd == 1;           // device rows also get the message table
     float *S = P.S[t.sd];
-    {   // cst[kind][64]: c'; od: a, a~, U; same-type: a~ (lane l holds column l)
-        const int cl = cw + lane;
-        const float v3 = cp[cl];
-        float v1 = 0.f, v2 = 0.f, v4 = 0.f;
-        if (JPH > 0) {
-            if (od) { v1 = P.a_od[cl]; v2 = P.ad_od[cl]; v4 = P.u_od[2 * cl]; }
-            else v2 = P.ad_same[t.sd][cl];
-        }
-        cst[lane] = v3; cst[64 + lane] = v1; cst[128 + lane] = v2; cst[192 + lane] = v4;
-    }
     // row blocks outer, column blocks inner: the four stores of a row block
-    // complete whole 128-byte row segments back to back
+    // complete whole 256-byte row segments back to back
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < NI; ++i) {
         const int64_t m = rbase + 16 * i;
         const bool mok = m < rows;
         float p0 = 0.f, p1 = 0.f, q = 0.f;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int c = cw + 16 * j + 4 * g;         // the lane's first channel in this block
-            const int cc = 16 * j + 4 * g;             // ... within the wavefront's columns
+            const int cc = 16 * j + 4 * g;             // ... within the slab's columns
             float c3[4], c1[4], c2[4], c4[4];           // c'; od: a, a~, U; same-type: a~
             {
                 const float4 x3 = *reinterpret_cast<const float4 *>(cst + cc);
-                const float4 x1 = *reinterpret_cast<const float4 *>(cst + 64 + cc);
-                const float4 x2 = *reinterpret_cast<const float4 *>(cst + 128 + cc);
-                const float4 x4 = *reinterpret_cast<const float4 *>(cst + 192 + cc);
+                const float4 x1 = *reinterpret_cast<const float4 *>(cst + CS + cc);
+                const float4 x2 = *reinterpret_cast<const float4 *>(cst + 2 * CS + cc);
+                const float4 x4 = *reinterpret_cast<const float4 *>(cst + 3 * CS + cc);
                 c3[0] = x3.x; c3[1] = x3.y; c3[2] = x3.z; c3[3] = x3.w;
                 c1[0] = x1.x; c1[1] = x1.y; c1[2] = x1.z; c1[3] = x1.w;
                 c2[0] = x2.x; c2[1] = x2.y; c2[2] = x2.z; c2[3] = x2.w;
@@ -258,7 +252,7 @@ __device__ void store_tile(const GemmArgs &G, const Tile &t, int wm, int wn, int
             if (mok) {
                 float ys[4], yv[4];
 #pragma unroll
-                for (int v = 0; v < 4; ++v) { ys[v] = acc[j][i][v] + c3[v]; yv[v] = acc[j][i][v]; }
+                for (int v = 0; v < 4; ++v) { ys[v] = acc[J0 + j][i][v] + c3[v]; yv[v] = acc[J0 + j][i][v]; }
                 *reinterpret_cast<float4 *>(static_cast<float *>(Yp) + m * ldy + col0 + cc) =
                     make_float4(ys[0], ys[1], ys[2], ys[3]);
                 if constexpr (JPH > 0) {
@@ -304,73 +298,167 @@ __device__ void store_tile(const GemmArgs &G, const Tile &t, int wm, int wn, int
     }
 }
 
+// The four per-column constants of output column n (c'; od: a, a~, U;
+// same-type: a~; zero where a kind does not apply)
+template <int JPH>
+__device__ __forceinline__ void column_consts(const GemmArgs &G, int sd, int n, float (&v)[4]) {
+    const GemmPrep &P = G.prep;
+    const bool od = n >= G.F;
+    const int c = od ? n - G.F : n;
+    v[0] = od ? P.cp_od[c] : P.cp_same[sd][c];
+    v[1] = v[2] = v[3] = 0.f;
+    if (JPH > 0) {
+        if (od) { v[1] = P.a_od[c]; v[2] = P.ad_od[c]; v[3] = P.u_od[2 * c]; }
+        else v[2] = P.ad_same[sd][c];
+    }
+}
+
+// fp32 relation transform on the bf16 matrix cores: both operands are split
+// exactly into three bf16 parts (split3) as they are loaded, and each 16 x 16
+// output block takes the six part products a_i b_j with i + j <= 2 on 16x16x32
+// bf16 MFMAs with fp32 accumulation.  Every part product is exact in fp32;
+// the three dropped ones add up to at most (2^-23 + 2^-32) |a b|, one fp32
+// rounding of the product, so the result is the fp32 contraction up to fp32
+// rounding.  At the matrix cores' rates (bf16 16 times fp32) the six
+// 16x16x32 products of a 16 x 16 x 32 contraction take 3/8 of the time of
+// its eight 16x16x4 fp32 products.
+//
+// 128 x 128 block tiles, four wavefronts of 32 rows x 128 columns, so each
+// hidden row is loaded and split by one wavefront only: lanes read their H
+// operands straight from global memory into registers (row l % 16 of a row
+// block, k-slice 8 (l / 16) of the 32-wide step) and split them there.  The
+// weights of the block's 128 columns pass through LDS as split planes, one
+// 32-wide k-step at a time, double-buffered, rows unpadded with XOR-swizzled
+// 16-byte chunks (as in gemm_bf16).  The next step's global loads are in
+// flight while the current step's 96 products per wavefront run.
 template <int JPH, bool ELU = false>
-__global__ void __launch_bounds__(256) gemm_f32(GemmArgs G) {
-    constexpr int BK = 16, LS = BM + 16;   // k-major LDS rows, stride = 16 (mod 64) banks
-    __shared__ float As[2][BK * LS];
-    __shared__ float Bs[2][BK * LS];
+__global__ void __launch_bounds__(256) gemm_f32s(GemmArgs G) {
+    constexpr int BK = 32;
+    __shared__ __attribute__((aligned(16))) uint16_t Ws[2][3][BN * BK];
+    __shared__ __attribute__((aligned(16))) float cst[4 * BN];   // column constants, 4 kinds x 128
+    auto sw = [](int r) { return ((r >> 1) ^ (r >> 2)) & 3; };
     const Tile t = tile_of(G);
     const GemmSide S = t.sd ? G.side[1] : G.side[0];
     const float *__restrict__ H = static_cast<const float *>(S.H);
-    float *__restrict__ Y = static_cast<float *>(S.Y);
     const int F = G.F;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-    // loader: thread -> (row lr, 8 consecutive k at lk)
-    const int lr = tid >> 1, lk = (tid & 1) * 8;
-    const int64_t gm = t.m0 + lr;
-    const bool aok = gm < S.rows;
-    const float *arow = H + (aok ? gm : 0) * F;
-    const int gn = t.n0 + lr;
-    const float *brow = gn < F ? static_cast<const float *>(S.B0) + (size_t)gn * S.ldb
-                               : static_cast<const float *>(S.B1) + (size_t)(gn - F) * S.ldb;
-    float4 ra[2], rb[2];
+    if (tid < BN) {
+        float v[4];
+        column_consts<JPH>(G, t.sd, t.n0 + tid, v);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) cst[q * BN + tid] = v[q];
+    }
+    // weight loader: thread -> rows tid/4 and tid/4 + 64 of the block's
+    // columns, 8-wide k-chunk tid % 4 of the step
+    const int lc = tid & 3;
+    const float *brow[2];
+    int loff[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const int lr = (tid >> 2) + 64 * q;
+        const int gn = t.n0 + lr;
+        brow[q] = (gn < F ? static_cast<const float *>(S.B0) + (size_t)gn * S.ldb
+                          : static_cast<const float *>(S.B1) + (size_t)(gn - F) * S.ldb) + 8 * lc;
+        loff[q] = lr * BK + 8 * (lc ^ sw(lr));
+    }
+    // hidden-row operands: row blocks i = 0, 1 of the wavefront's 32 rows
+    const int64_t rbase = t.m0 + wave * 32 + (lane & 15);
+    const float *hrow[2];
+    bool hok[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        hok[i] = rbase + 16 * i < S.rows;
+        hrow[i] = H + (hok[i] ? rbase + 16 * i : 0) * F + 8 * (lane >> 4);
+    }
+    int boff[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int r = j * 16 + (lane & 15);
+        boff[j] = r * BK + 8 * ((lane >> 4) ^ sw(r));
+    }
+    float4 rb[2][2], rh[2][2];
     auto gload = [&](int k0) {
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
-            ra[q] = aok ? *reinterpret_cast<const float4 *>(arow + k0 + lk + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
-            rb[q] = *reinterpret_cast<const float4 *>(brow + k0 + lk + 4 * q);
+            rb[q][0] = *reinterpret_cast<const float4 *>(brow[q] + k0);
+            rb[q][1] = *reinterpret_cast<const float4 *>(brow[q] + k0 + 4);
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {   // rows past the end read row 0 (zeroed when split)
+            rh[i][0] = *reinterpret_cast<const float4 *>(hrow[i] + k0);
+            rh[i][1] = *reinterpret_cast<const float4 *>(hrow[i] + k0 + 4);
         }
     };
-    auto sstore = [&](int buf) {
+    // eight fp32 values -> their three bf16 planes, 16 bytes each
+    auto split8 = [](const float4 (&x)[2], u4 (&o)[3]) {
+        unsigned p[4][3];
+        split3(x[0].x, x[0].y, p[0]);
+        split3(x[0].z, x[0].w, p[1]);
+        split3(x[1].x, x[1].y, p[2]);
+        split3(x[1].z, x[1].w, p[3]);
+#pragma unroll
+        for (int z = 0; z < 3; ++z) o[z] = u4{p[0][z], p[1][z], p[2][z], p[3][z]};
+    };
+    auto wstore = [&](int buf) {
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
-            const int k = lk + 4 * q;
-            As[buf][(k + 0) * LS + lr] = ra[q].x; As[buf][(k + 1) * LS + lr] = ra[q].y;
-            As[buf][(k + 2) * LS + lr] = ra[q].z; As[buf][(k + 3) * LS + lr] = ra[q].w;
-            Bs[buf][(k + 0) * LS + lr] = rb[q].x; Bs[buf][(k + 1) * LS + lr] = rb[q].y;
-            Bs[buf][(k + 2) * LS + lr] = rb[q].z; Bs[buf][(k + 3) * LS + lr] = rb[q].w;
+            u4 o[3];
+            split8(rb[q], o);
+#pragma unroll
+            for (int z = 0; z < 3; ++z) *reinterpret_cast<u4 *>(&Ws[buf][z][loff[q]]) = o[z];
         }
     };
-    f4 acc[4][4];
+    bf8 ah[2][3];
+    auto hsplit = [&]() {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 2; ++i) {
+            u4 o[3];
+            split8(rh[i], o);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+            for (int z = 0; z < 3; ++z) ah[i][z] = __builtin_bit_cast(bf8, hok[i] ? o[z] : u4{0u, 0u, 0u, 0u});
+        }
+    };
+    f4 acc[8][2];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) acc[j][i] = f4{0.f, 0.f, 0.f, 0.f};
     gload(0);
-    sstore(0);
+    wstore(0);
+    hsplit();
     __syncthreads();
     const int nk = F / BK;
     for (int kc = 0; kc < nk; ++kc) {
         const int buf = kc & 1;
         if (kc + 1 < nk) gload((kc + 1) * BK);
+        // two column blocks at a time: 24 products over four accumulators,
+        // part products outer so that no two consecutive ones share one
 #pragma unroll
-        for (int kk = 0; kk < BK; kk += 4) {
-            const int krow = (kk + (lane >> 4)) * LS;
-            float a[4], b[4];
+        for (int jp = 0; jp < 4; ++jp) {
+            bf8 bw[2][3];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) a[i] = As[buf][krow + wm * 64 + i * 16 + (lane & 15)];
+            for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) b[j] = Bs[buf][krow + wn * 64 + j * 16 + (lane & 15)];
+                for (int z = 0; z < 3; ++z)
+                    bw[jj][z] = *reinterpret_cast<const bf8 *>(&Ws[buf][z][boff[2 * jp + jj]]);
+            constexpr int PW[6] = {2, 1, 0, 1, 0, 0}, PH[6] = {0, 1, 2, 0, 1, 0};   // smallest first
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int pp = 0; pp < 6; ++pp)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[j], a[i], acc[j][i], 0, 0, 0);
+                for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+                    for (int i = 0; i < 2; ++i)
+                        acc[2 * jp + jj][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            bw[jj][PW[pp]], ah[i][PH[pp]], acc[2 * jp + jj][i], 0, 0, 0);
         }
-        if (kc + 1 < nk) sstore(buf ^ 1);
+        if (kc + 1 < nk) {
+            wstore(buf ^ 1);
+            hsplit();
+        }
         __syncthreads();
     }
-    store_tile<JPH, ELU>(G, t, wm, wn, lane, acc, &As[0][wave * 256]);
+    store_rows<JPH, ELU, 2, BN, 0>(G, t, rbase, t.n0, lane, acc, cst);
+    store_rows<JPH, ELU, 2, BN, 4>(G, t, rbase, t.n0 + 64, lane, acc, cst + 64);
 }
 
 template <int JPH>
@@ -468,8 +556,8 @@ int64_t transform_row_tiles(int64_t rows) { return (rows + BM - 1) / BM; }
 template <int JPH>
 void launch_gemm(const GemmArgs &G, bool bf, unsigned blocks, hipStream_t st) {
     if (bf) gemm_bf16<JPH><<<blocks, 256, 0, st>>>(G);
-    else if (G.prep.elu) gemm_f32<JPH, true><<<blocks, 256, 0, st>>>(G);
-    else gemm_f32<JPH><<<blocks, 256, 0, st>>>(G);
+    else if (G.prep.elu) gemm_f32s<JPH, true><<<blocks, 256, 0, st>>>(G);
+    else gemm_f32s<JPH><<<blocks, 256, 0, st>>>(G);
 }
 
 void launch_transform(const GemmArgs &G, bool bf, hipStream_t st) {
