@@ -212,10 +212,14 @@ __device__ void store_tile_bf16(const GemmArgs &G, const Tile &t, int wm, int wn
 // One call covers NI row blocks of 16 (rows rbase + 16 i, rbase carrying the
 // lane's l % 16) and the 64 columns col0 .. col0 + 63, which lie in one
 // relation half (F is a multiple of 64), from accumulator blocks
-// acc[J0 .. J0 + 3][0 .. NI - 1].
+// acc[J0 .. J0 + 3][0 .. NI - 1].  The Y rows go through the wavefront's
+// LDS slice `stage` (16 NI rows of kStageStride floats) and leave as whole
+// 256-byte row segments, four rows per store instruction (stored from the
+// accumulator layout, each instruction would cover half of sixteen lines).
+constexpr int kStageStride = 64 + 4;
 template <int JPH, bool ELU, int NI, int CS, int J0, int NJ>
 __device__ void store_rows(const GemmArgs &G, const Tile &t, int64_t rbase, int col0, int lane,
-                           const f4 (&acc)[NJ][NI], const float *cst) {
+                           const f4 (&acc)[NJ][NI], const float *cst, float *stage) {
     static_assert(J0 + 4 <= NJ, "four column blocks");
     const GemmPrep &P = G.prep;
     const int64_t rows = t.sd ? G.side[1].rows : G.side[0].rows;
@@ -249,12 +253,17 @@ __device__ void store_rows(const GemmArgs &G, const Tile &t, int64_t rbase, int 
                 c2[0] = x2.x; c2[1] = x2.y; c2[2] = x2.z; c2[3] = x2.w;
                 c4[0] = x4.x; c4[1] = x4.y; c4[2] = x4.z; c4[3] = x4.w;
             }
+            {
+                float ys[4];
+#pragma unroll
+                for (int v = 0; v < 4; ++v) ys[v] = acc[J0 + j][i][v] + c3[v];
+                *reinterpret_cast<float4 *>(stage + (16 * i + (lane & 15)) * kStageStride + cc) =
+                    make_float4(ys[0], ys[1], ys[2], ys[3]);
+            }
             if (mok) {
                 float ys[4], yv[4];
 #pragma unroll
                 for (int v = 0; v < 4; ++v) { ys[v] = acc[J0 + j][i][v] + c3[v]; yv[v] = acc[J0 + j][i][v]; }
-                *reinterpret_cast<float4 *>(static_cast<float *>(Yp) + m * ldy + col0 + cc) =
-                    make_float4(ys[0], ys[1], ys[2], ys[3]);
                 if constexpr (JPH > 0) {
                     if (od) {
                         float t0[4], t1[4];
@@ -295,6 +304,16 @@ __device__ void store_rows(const GemmArgs &G, const Tile &t, int64_t rbase, int 
                 }
             }
         }
+    }
+    // the staged rows, four per instruction (a wavefront's own LDS slice:
+    // its writes above are ordered before these reads)
+    const int64_t r0 = rbase - (lane & 15);
+#pragma unroll
+    for (int it = 0; it < 4 * NI; ++it) {
+        const int rr = 4 * it + (lane >> 4);
+        const float4 v = *reinterpret_cast<const float4 *>(stage + rr * kStageStride + 4 * (lane & 15));
+        if (r0 + rr < rows)
+            *reinterpret_cast<float4 *>(static_cast<float *>(Yp) + (r0 + rr) * ldy + col0 + 4 * (lane & 15)) = v;
     }
 }
 
@@ -457,8 +476,12 @@ __global__ void __launch_bounds__(256) gemm_f32s(GemmArgs G) {
         }
         __syncthreads();
     }
-    store_rows<JPH, ELU, 2, BN, 0>(G, t, rbase, t.n0, lane, acc, cst);
-    store_rows<JPH, ELU, 2, BN, 4>(G, t, rbase, t.n0 + 64, lane, acc, cst + 64);
+    // the k-step buffers are free (the loop ends with a barrier): one row
+    // stage per wavefront
+    float *stage = reinterpret_cast<float *>(&Ws[0][0][0]) + wave * 32 * kStageStride;
+    static_assert(4 * 32 * kStageStride * 4 <= sizeof(Ws), "row stages must fit the k-step buffers");
+    store_rows<JPH, ELU, 2, BN, 0>(G, t, rbase, t.n0, lane, acc, cst, stage);
+    store_rows<JPH, ELU, 2, BN, 4>(G, t, rbase, t.n0 + 64, lane, acc, cst + 64, stage);
 }
 
 template <int JPH>
