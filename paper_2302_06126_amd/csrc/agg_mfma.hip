@@ -153,11 +153,14 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     constexpr int NCB = WC / 16;                   // 16-column blocks per wavefront
     constexpr int HPW = WC >= D ? WC / D : 1;      // heads per wavefront
     constexpr int CPH = NCB / HPW;                 // column blocks per head inside a wavefront
-    // bf16: op tiles double-buffered and filled by direct global -> LDS
-    // loads, rows unpadded with their 16-byte chunks XOR-swizzled (see
-    // ys_off); fp32: one tile, rows padded
-    constexpr int NB = BF ? 2 : 1;
-    constexpr int YS = BF ? F : F + 4;
+    // SP (bf16, and fp32 at F <= 128): op tiles double-buffered and filled
+    // by direct global -> LDS loads, rows unpadded with their 16-byte chunks
+    // XOR-swizzled (see ys_off), sparse products over exact splits; fp32 at
+    // F = 256 (whose two fp32 tiles would take 128 KiB of LDS): one tile,
+    // rows padded, fp32 16x16x4 products
+    constexpr bool SP = BF || F <= 128;
+    constexpr int NB = SP ? 2 : 1;
+    constexpr int YS = SP ? F : F + 4;
     typedef typename std::conditional<BF, uint16_t, float>::type YT;
     // (two separate arrays per buffer, so that the compiler sees that the
     // loads into one buffer do not alias the reads of the other)
@@ -179,6 +182,42 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     const uint64_t *om = A.omask + (int64_t)r * A.n_op * 2;
     const float slope = A.slope;
 
+    // element (op u, column col) of a tile: 16-byte chunk col / EPC of
+    // row u (EPC elements per chunk), XORed with ((u / 4) % 4) times the
+    // chunks that sixteen lanes read, so that the four lane groups of a
+    // message read (rows 4 apart) fall on different banks
+    constexpr int EPC = 16 / sizeof(YT), GSW = 16 / EPC;
+    auto ys_off = [](int u, int col) {
+        return u * F + ((((col / EPC) ^ (GSW * ((u >> 2) & 3))) * EPC) | (col % EPC));
+    };
+    // tile t into the given buffers, all by direct loads into LDS: the op
+    // rows' second halves, the masks and the raw attention terms (rows
+    // past the tile repeat op u0: their weights are zero)
+    auto stage = [&](int32_t t, auto &ys, auto &mk, auto &pbn) {   // (SP only)
+        const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1];
+        const YT *Yr = static_cast<const YT *>(A.Y_op) + ((int64_t)r * A.n_op + u0) * 2 * F + F;
+        constexpr int NI = kOpTile * F / EPC / 256;   // 16-byte chunks per thread
+        const int wv = __builtin_amdgcn_readfirstlane(wave);   // (wave-uniform LDS addresses)
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int P = (wv * NI + i) * 64 + lane;   // physical chunk; the wave fills 1 KB
+            const int u = P / (F / EPC), k = (P % (F / EPC)) ^ (GSW * ((u >> 2) & 3));
+            load_lds<16>(Yr + (int64_t)(u < nu ? u : 0) * 2 * F + EPC * k, &ys[(wv * NI + i) * 64 * EPC]);
+        }
+        if (wv == 0)
+            load_lds<16>(om + 2 * (int64_t)(u0 + (lane < nu ? lane : 0)), &mk[0][0]);
+        // an op's 2K attention terms (8K bytes) in PC-byte lanes
+        constexpr int PC = 8 * K >= 16 ? 16 : 4, PCO = 8 * K / PC, PNI = kOpTile * PCO / 64;
+#pragma unroll
+        for (int j = 0; j < (PNI + 3) / 4; ++j) {
+            const int i = wv + 4 * j;
+            if (i >= PNI) break;
+            const int P = i * 64 + lane, u = P / PCO;
+            load_lds<PC>(Sop + (int64_t)(u0 + (u < nu ? u : 0)) * 4 * K + (P % PCO) * (PC / 4),
+                         &pbn[0][0][0] + i * 64 * (PC / 4));
+        }
+    };
+    if constexpr (SP) stage(t0, Ys0, MK0, pb0);   // the first tile lands while the maxima are taken
     for (int i = tid; i < F; i += 256) {
         US[i] = A.U[(size_t)(F + i) * 2];
         CS[i] = A.cp[F + i];
@@ -189,18 +228,36 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
         mxk[j][h] = INT_MIN;
     }
     __syncthreads();
-    for (int32_t t = t0; t < t1; ++t) {
-        const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1];
-        for (int i = tid; i < nu * K; i += 256) {
-            const int64_t u = u0 + i / K;
-            const int h = i % K;
-            uint64_t pr = om[2 * u];
-            const uint64_t bt = om[2 * u + 1];
-            const int k0 = fkey(Sop[u * 4 * K + h]), k1 = fkey(Sop[u * 4 * K + K + h]);
-            while (pr) {
-                const int j = __builtin_ctzll(pr);
-                pr &= pr - 1;
-                atomicMax(&mxk[j][h], ((bt >> j) & 1ull) ? k1 : k0);
+    {
+        // (op, head) items of the block's tiles, which cover the contiguous
+        // ops ub .. ue - 1; MB items per thread have their loads in flight
+        // together before their LDS maxima are taken
+        const int32_t ub = A.tiles[3 * t0], ue = A.tiles[3 * (t1 - 1)] + A.tiles[3 * (t1 - 1) + 1];
+        const int32_t n_items = (ue - ub) * K;
+        constexpr int MB = 4;
+        for (int32_t base = tid; base < n_items; base += 256 * MB) {
+            uint64_t prv[MB], btv[MB];
+            float s0v[MB], s1v[MB];
+#pragma unroll
+            for (int q = 0; q < MB; ++q) {
+                const int32_t i = base + 256 * q;
+                const int64_t u = ub + (i < n_items ? i : 0) / K;
+                const int h = i % K;
+                prv[q] = i < n_items ? om[2 * u] : 0ull;
+                btv[q] = om[2 * u + 1];
+                s0v[q] = Sop[u * 4 * K + h];
+                s1v[q] = Sop[u * 4 * K + K + h];
+            }
+#pragma unroll
+            for (int q = 0; q < MB; ++q) {
+                const int h = (base + 256 * q) % K;
+                const int k0 = fkey(s0v[q]), k1 = fkey(s1v[q]);
+                uint64_t pr = prv[q];
+                while (pr) {
+                    const int j = __builtin_ctzll(pr);
+                    pr &= pr - 1;
+                    atomicMax(&mxk[j][h], ((btv[q] >> j) & 1ull) ? k1 : k0);
+                }
             }
         }
     }
@@ -246,38 +303,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
             m2[rb][hh] = j < Mg ? mrun[j][h0 + hh] : 0.f;
         }
     }
-    if constexpr (BF) {
-        // element (op u, column col) of a bf16 tile: 16-byte chunk col / 8 of
-        // row u, XORed with 2 ((u / 4) % 4) so that the four lane groups of a
-        // message read (rows 4 apart) fall on different banks
-        auto ys_off = [](int u, int col) { return u * F + ((((col >> 3) ^ (2 * ((u >> 2) & 3))) << 3) | (col & 7)); };
-        // tile t into the given buffers, all by direct loads into LDS: the op
-        // rows' second halves, the masks and the raw attention terms (rows
-        // past the tile repeat op u0: their weights are zero)
-        auto stage = [&](int32_t t, auto &ys, auto &mk, auto &pbn) {
-            const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1];
-            const uint16_t *Yr = static_cast<const uint16_t *>(A.Y_op) + ((int64_t)r * A.n_op + u0) * 2 * F + F;
-            constexpr int NI = kOpTile * F / 8 / 256;   // 16-byte chunks per thread
-            const int wv = __builtin_amdgcn_readfirstlane(wave);   // (wave-uniform LDS addresses)
-#pragma unroll
-            for (int i = 0; i < NI; ++i) {
-                const int P = (wv * NI + i) * 64 + lane;   // physical chunk; the wave fills 1 KB
-                const int u = P / (F / 8), k = (P % (F / 8)) ^ (2 * ((u >> 2) & 3));
-                load_lds<16>(Yr + (int64_t)(u < nu ? u : 0) * 2 * F + 8 * k, &ys[(wv * NI + i) * 64 * 8]);
-            }
-            if (wv == 0)
-                load_lds<16>(om + 2 * (int64_t)(u0 + (lane < nu ? lane : 0)), &mk[0][0]);
-            // an op's 2K attention terms (8K bytes) in PC-byte lanes
-            constexpr int PC = 8 * K >= 16 ? 16 : 4, PCO = 8 * K / PC, PNI = kOpTile * PCO / 64;
-#pragma unroll
-            for (int j = 0; j < (PNI + 3) / 4; ++j) {
-                const int i = wv + 4 * j;
-                if (i >= PNI) break;
-                const int P = i * 64 + lane, u = P / PCO;
-                load_lds<PC>(Sop + (int64_t)(u0 + (u < nu ? u : 0)) * 4 * K + (P % PCO) * (PC / 4),
-                             &pbn[0][0][0] + i * 64 * (PC / 4));
-            }
-        };
+    if constexpr (SP) {
         // tile t from the current buffers while tile t + 1 lands in the others
         auto run = [&](int32_t t, auto &ysc, auto &mkc, auto &pbc, auto &ysn, auto &mkn, auto &pbn) {
             const int32_t nu = A.tiles[3 * t + 1];
@@ -347,9 +373,11 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
 #pragma unroll
                             for (int q = 0; q < 8; ++q) {
                                 const int u = ubm + (q < 4 ? q : 12 + q);
-                                const float yc = bf2f(ysc[ys_off(u, col)]) + Cv[cb];   // Y + c'
+                                float yc;   // Y + c' (bf16 rows hold Y, fp32 rows Y + c')
+                                if constexpr (BF) yc = bf2f(ysc[ys_off(u, col)]) + Cv[cb];
+                                else yc = ysc[ys_off(u, col)];
                                 unsigned sp[3];
-                                split3(fmaxf(yc, 0.f), fmaxf(yc + Uv[cb], 0.f), sp);
+                                split3(msg_act<ELU>(yc), msg_act<ELU>(yc + Uv[cb]), sp);
 #pragma unroll
                                 for (int z = 0; z < 3; ++z) w[z][q] = sp[z];
                             }
@@ -363,8 +391,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();   // the next tile is in place; this one is free again
         };
-        stage(t0, Ys0, MK0, pb0);
-        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_s_waitcnt(0);   // the first tile (staged before the maxima)
         __syncthreads();
         for (int32_t t = t0; t < t1; t += 2) {
             run(t, Ys0, MK0, pb0, Ys1, MK1, pb1);
