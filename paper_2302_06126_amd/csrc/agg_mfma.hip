@@ -153,20 +153,15 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     constexpr int NCB = WC / 16;                   // 16-column blocks per wavefront
     constexpr int HPW = WC >= D ? WC / D : 1;      // heads per wavefront
     constexpr int CPH = NCB / HPW;                 // column blocks per head inside a wavefront
-    // SP (bf16, and fp32 at F <= 128): op tiles double-buffered and filled
-    // by direct global -> LDS loads, rows unpadded with their 16-byte chunks
-    // XOR-swizzled (see ys_off), sparse products over exact splits; fp32 at
-    // F = 256 (whose two fp32 tiles would take 128 KiB of LDS): one tile,
-    // rows padded, fp32 16x16x4 products
-    constexpr bool SP = BF || F <= 128;
-    constexpr int NB = SP ? 2 : 1;
-    constexpr int YS = SP ? F : F + 4;
+    // op tiles double-buffered and filled by direct global -> LDS loads,
+    // rows unpadded with their 16-byte chunks XOR-swizzled (see ys_off);
+    // fp32 rows at F = 256 take 2 x 64 KiB (one block per CU)
     typedef typename std::conditional<BF, uint16_t, float>::type YT;
     // (two separate arrays per buffer, so that the compiler sees that the
     // loads into one buffer do not alias the reads of the other)
-    __shared__ __attribute__((aligned(16))) YT Ys0[kOpTile * YS], Ys1[NB > 1 ? kOpTile * YS : 8];
-    __shared__ __attribute__((aligned(16))) uint64_t MK0[kOpTile][2], MK1[NB > 1 ? kOpTile : 1][2];   // (present, bit) per op
-    __shared__ float pb0[kOpTile][2][K], pb1[NB > 1 ? kOpTile : 1][2][K];
+    __shared__ __attribute__((aligned(16))) YT Ys0[kOpTile * F], Ys1[kOpTile * F];
+    __shared__ __attribute__((aligned(16))) uint64_t MK0[kOpTile][2], MK1[kOpTile][2];   // (present, bit) per op
+    __shared__ float pb0[kOpTile][2][K], pb1[kOpTile][2][K];
     __shared__ int mxk[64][K];
     __shared__ float qd[64][K], mrun[64][K];
     __shared__ float US[F], CS[F];
@@ -193,7 +188,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     // tile t into the given buffers, all by direct loads into LDS: the op
     // rows' second halves, the masks and the raw attention terms (rows
     // past the tile repeat op u0: their weights are zero)
-    auto stage = [&](int32_t t, auto &ys, auto &mk, auto &pbn) {   // (SP only)
+    auto stage = [&](int32_t t, auto &ys, auto &mk, auto &pbn) {
         const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1];
         const YT *Yr = static_cast<const YT *>(A.Y_op) + ((int64_t)r * A.n_op + u0) * 2 * F + F;
         constexpr int NI = kOpTile * F / EPC / 256;   // 16-byte chunks per thread
@@ -217,7 +212,7 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
                          &pbn[0][0][0] + i * 64 * (PC / 4));
         }
     };
-    if constexpr (SP) stage(t0, Ys0, MK0, pb0);   // the first tile lands while the maxima are taken
+    stage(t0, Ys0, MK0, pb0);   // the first tile lands while the maxima are taken
     for (int i = tid; i < F; i += 256) {
         US[i] = A.U[(size_t)(F + i) * 2];
         CS[i] = A.cp[F + i];
@@ -274,7 +269,6 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
     const int cbase = wave * WC;
     const int h0 = cbase / D;
     const int NRB = (Mg + 15) / 16;
-    const int b = (lane >> 4) & 1;
     float Uv[NCB], Cv[NCB];
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
@@ -303,156 +297,98 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
             m2[rb][hh] = j < Mg ? mrun[j][h0 + hh] : 0.f;
         }
     }
-    if constexpr (SP) {
-        // tile t from the current buffers while tile t + 1 lands in the others
-        auto run = [&](int32_t t, auto &ysc, auto &mkc, auto &pbc, auto &ysn, auto &mkn, auto &pbn) {
-            const int32_t nu = A.tiles[3 * t + 1];
-            if (t + 1 < t1) stage(t + 1, ysn, mkn, pbn);
-                // sparse 16x16x64 bf16 products (smfmac_split3) over the exact
-                // three-way splits of the fp32 attention weights and messages:
-                // k = 2u + b over 32 ops per step.  A link carries one bit, so a
-                // device row has at most one nonzero weight in each op's pair of
-                // k (the 2:4 structure).  Lane group g = l / 16 gives the weights
-                // of ops 8g .. 8g+7 of a step (value v at position 2 (v % 2) +
-                // bit of its op pair's four k) and the messages of ops 4g .. 4g+3
-                // and 16+4g .. 16+4g+3 (both bits).
+    // tile t from the current buffers while tile t + 1 lands in the others
+    auto run = [&](int32_t t, auto &ysc, auto &mkc, auto &pbc, auto &ysn, auto &mkn, auto &pbn) {
+        const int32_t nu = A.tiles[3 * t + 1];
+        if (t + 1 < t1) stage(t + 1, ysn, mkn, pbn);
+            // sparse 16x16x64 bf16 products (smfmac_split3) over the exact
+            // three-way splits of the fp32 attention weights and messages:
+            // k = 2u + b over 32 ops per step.  A link carries one bit, so a
+            // device row has at most one nonzero weight in each op's pair of
+            // k (the 2:4 structure).  Lane group g = l / 16 gives the weights
+            // of ops 8g .. 8g+7 of a step (value v at position 2 (v % 2) +
+            // bit of its op pair's four k) and the messages of ops 4g .. 4g+3
+            // and 16+4g .. 16+4g+3 (both bits).
 #pragma unroll 1
-                for (int ks = 0; ks < kOpTile / 32; ++ks) {
-                    const int ua = 32 * ks + 8 * (lane >> 4);
-                    const int ubm = 32 * ks + 4 * (lane >> 4);
-                    uint64_t prq[8], btq[8];
+            for (int ks = 0; ks < kOpTile / 32; ++ks) {
+                const int ua = 32 * ks + 8 * (lane >> 4);
+                const int ubm = 32 * ks + 4 * (lane >> 4);
+                uint64_t prq[8], btq[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const bool live = ua + q < nu;   // rows past the tile hold another op's masks
+                    prq[q] = live ? mkc[ua + q][0] : 0ull;
+                    btq[q] = live ? mkc[ua + q][1] : 0ull;
+                }
+#pragma unroll
+                for (int hh = 0; hh < HPW; ++hh) {
+                    float p0q[8], p1q[8];
 #pragma unroll
                     for (int q = 0; q < 8; ++q) {
-                        const bool live = ua + q < nu;   // rows past the tile hold another op's masks
-                        prq[q] = live ? mkc[ua + q][0] : 0ull;
-                        btq[q] = live ? mkc[ua + q][1] : 0ull;
+                        p0q[q] = pbc[ua + q][0][h0 + hh];
+                        p1q[q] = pbc[ua + q][1][h0 + hh];
+                    }
+                    bf8 aop[4][3];
+                    int idx[4];
+#pragma unroll
+                    for (int rb = 0; rb < 4; ++rb) {
+                        if (rb < NRB) {
+                            const int j = rb * 16 + (lane & 15);
+                            unsigned w[3][4], sb = 0u;
+#pragma unroll
+                            for (int pr = 0; pr < 4; ++pr) {
+                                float af2[2];
+#pragma unroll
+                                for (int e = 0; e < 2; ++e) {
+                                    const int q = 2 * pr + e;
+                                    const bool on = (prq[q] >> j) & 1ull;
+                                    const unsigned bit = (unsigned)(btq[q] >> j) & 1u;
+                                    const float x = fmaf(bit ? p1q[q] : p0q[q], kLog2e, q2[rb][hh]);   // raw terms
+                                    af2[e] = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
+                                    zl[rb][hh] += af2[e];
+                                    sb |= bit << (2 * q);
+                                }
+                                unsigned sp[3];
+                                split3(af2[0], af2[1], sp);
+#pragma unroll
+                                for (int z = 0; z < 3; ++z) w[z][pr] = sp[z];
+                            }
+#pragma unroll
+                            for (int z = 0; z < 3; ++z) aop[rb][z] = as_bf8(w[z][0], w[z][1], w[z][2], w[z][3]);
+                            idx[rb] = (int)(0x8888u | sb);
+                        }
                     }
 #pragma unroll
-                    for (int hh = 0; hh < HPW; ++hh) {
-                        float p0q[8], p1q[8];
+                    for (int c2 = 0; c2 < CPH; ++c2) {
+                        const int cb = hh * CPH + c2;
+                        const int col = cbase + cb * 16 + (lane & 15);
+                        unsigned w[3][8];
 #pragma unroll
                         for (int q = 0; q < 8; ++q) {
-                            p0q[q] = pbc[ua + q][0][h0 + hh];
-                            p1q[q] = pbc[ua + q][1][h0 + hh];
+                            const int u = ubm + (q < 4 ? q : 12 + q);
+                            float yc;   // Y + c' (bf16 rows hold Y, fp32 rows Y + c')
+                            if constexpr (BF) yc = bf2f(ysc[ys_off(u, col)]) + Cv[cb];
+                            else yc = ysc[ys_off(u, col)];
+                            unsigned sp[3];
+                            split3(msg_act<ELU>(yc), msg_act<ELU>(yc + Uv[cb]), sp);
+#pragma unroll
+                            for (int z = 0; z < 3; ++z) w[z][q] = sp[z];
                         }
-                        bf8 aop[4][3];
-                        int idx[4];
+                        const bf16x16 bo[3] = {as_bf16x16(w[0]), as_bf16x16(w[1]), as_bf16x16(w[2])};
 #pragma unroll
-                        for (int rb = 0; rb < 4; ++rb) {
-                            if (rb < NRB) {
-                                const int j = rb * 16 + (lane & 15);
-                                unsigned w[3][4], sb = 0u;
-#pragma unroll
-                                for (int pr = 0; pr < 4; ++pr) {
-                                    float af2[2];
-#pragma unroll
-                                    for (int e = 0; e < 2; ++e) {
-                                        const int q = 2 * pr + e;
-                                        const bool on = (prq[q] >> j) & 1ull;
-                                        const unsigned bit = (unsigned)(btq[q] >> j) & 1u;
-                                        const float x = fmaf(bit ? p1q[q] : p0q[q], kLog2e, q2[rb][hh]);   // raw terms
-                                        af2[e] = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
-                                        zl[rb][hh] += af2[e];
-                                        sb |= bit << (2 * q);
-                                    }
-                                    unsigned sp[3];
-                                    split3(af2[0], af2[1], sp);
-#pragma unroll
-                                    for (int z = 0; z < 3; ++z) w[z][pr] = sp[z];
-                                }
-#pragma unroll
-                                for (int z = 0; z < 3; ++z) aop[rb][z] = as_bf8(w[z][0], w[z][1], w[z][2], w[z][3]);
-                                idx[rb] = (int)(0x8888u | sb);
-                            }
-                        }
-#pragma unroll
-                        for (int c2 = 0; c2 < CPH; ++c2) {
-                            const int cb = hh * CPH + c2;
-                            const int col = cbase + cb * 16 + (lane & 15);
-                            unsigned w[3][8];
-#pragma unroll
-                            for (int q = 0; q < 8; ++q) {
-                                const int u = ubm + (q < 4 ? q : 12 + q);
-                                float yc;   // Y + c' (bf16 rows hold Y, fp32 rows Y + c')
-                                if constexpr (BF) yc = bf2f(ysc[ys_off(u, col)]) + Cv[cb];
-                                else yc = ysc[ys_off(u, col)];
-                                unsigned sp[3];
-                                split3(msg_act<ELU>(yc), msg_act<ELU>(yc + Uv[cb]), sp);
-#pragma unroll
-                                for (int z = 0; z < 3; ++z) w[z][q] = sp[z];
-                            }
-                            const bf16x16 bo[3] = {as_bf16x16(w[0]), as_bf16x16(w[1]), as_bf16x16(w[2])};
-#pragma unroll
-                            for (int rb = 0; rb < 4; ++rb)
-                                if (rb < NRB) acc[rb][cb] = smfmac_split3(aop[rb], bo, idx[rb], acc[rb][cb]);
-                        }
-                    }
-                }
-            __builtin_amdgcn_s_waitcnt(0);
-            __syncthreads();   // the next tile is in place; this one is free again
-        };
-        __builtin_amdgcn_s_waitcnt(0);   // the first tile (staged before the maxima)
-        __syncthreads();
-        for (int32_t t = t0; t < t1; t += 2) {
-            run(t, Ys0, MK0, pb0, Ys1, MK1, pb1);
-            if (t + 1 < t1) run(t + 1, Ys1, MK1, pb1, Ys0, MK0, pb0);
-        }
-    } else {
-        for (int32_t t = t0; t < t1; ++t) {
-            const int32_t u0 = A.tiles[3 * t], nu = A.tiles[3 * t + 1];
-            for (int i = tid; i < kOpTile; i += 256) {
-                const bool ok = i < nu;
-                MK0[i][0] = ok ? om[2 * (int64_t)(u0 + i)] : 0ull;
-                MK0[i][1] = ok ? om[2 * (int64_t)(u0 + i) + 1] : 0ull;
-            }
-            for (int i = tid; i < kOpTile * 2 * K; i += 256) {
-                const int u = i / (2 * K), bh = i % (2 * K);
-                pb0[u][bh / K][bh % K] = u < nu ? Sop[(int64_t)(u0 + u) * 4 * K + bh] * kLog2e : 0.f;
-            }
-            for (int i = tid; i < kOpTile * (F / 4); i += 256) {
-                const int u = i / (F / 4), c = (i % (F / 4)) * 4;
-                float v[4] = {0.f, 0.f, 0.f, 0.f};
-                if (u < nu) load_ch<4, false>(A.Y_op, ((int64_t)r * A.n_op + u0 + u) * 2 * F + F + c, v);
-                for (int q = 0; q < 4; ++q) Ys0[u * YS + c + q] = v[q];
-            }
-            __syncthreads();
-            // fp32 16x16x4 products: k = 4 (op, bit) pairs per step, two ops per
-            // step; lane l supplies op 2s + l / 32 with bit (l / 16) % 2
-            for (int s = 0; s < kOpTile / 2; ++s) {
-                const int ul = 2 * s + (lane >> 5);
-                const uint64_t pr = MK0[ul][0], bt = b ? MK0[ul][1] : ~MK0[ul][1];   // bt bit j: link bit equals b
-                float bv[NCB];
-#pragma unroll
-                for (int cb = 0; cb < NCB; ++cb) {
-                    const int col = cbase + cb * 16 + (lane & 15);
-                    // fp32 rows store Y + c'
-                    const float yc = static_cast<float>(Ys0[ul * YS + col]);
-                    bv[cb] = msg_act<ELU>(b ? yc + Uv[cb] : yc);
-                }
-                float pu[HPW];
-#pragma unroll
-                for (int hh = 0; hh < HPW; ++hh) pu[hh] = pb0[ul][b][h0 + hh];
-                const uint64_t sel = pr & bt;
-#pragma unroll
-                for (int rb = 0; rb < 4; ++rb) {
-                    if (rb < NRB) {
-                        const int j = rb * 16 + (lane & 15);
-                        const bool on = (sel >> j) & 1ull;   // j < Mg holds for every set bit
-#pragma unroll
-                        for (int hh = 0; hh < HPW; ++hh) {
-                            const float x = pu[hh] + q2[rb][hh];
-                            const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
-                            zl[rb][hh] += af;
-#pragma unroll
-                            for (int c2 = 0; c2 < CPH; ++c2)
-                                acc[rb][hh * CPH + c2] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                                    af, bv[hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
-                        }
+                        for (int rb = 0; rb < 4; ++rb)
+                            if (rb < NRB) acc[rb][cb] = smfmac_split3(aop[rb], bo, idx[rb], acc[rb][cb]);
                     }
                 }
             }
-            __syncthreads();   // the next tile overwrites the LDS tile and masks
-        }
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();   // the next tile is in place; this one is free again
+    };
+    __builtin_amdgcn_s_waitcnt(0);   // the first tile (staged before the maxima)
+    __syncthreads();
+    for (int32_t t = t0; t < t1; t += 2) {
+        run(t, Ys0, MK0, pb0, Ys1, MK1, pb1);
+        if (t + 1 < t1) run(t + 1, Ys1, MK1, pb1, Ys0, MK0, pb0);
     }
 
     const int REC = F + 2 * K;
