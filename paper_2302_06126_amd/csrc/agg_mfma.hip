@@ -109,7 +109,7 @@ __global__ void __launch_bounds__(256) prep_rows(AggArgs A, int dev_side) {
         const float yc = BF ? yo[c] + od.cp[c] : yo[c];   // Y + c' (fp32 rows store it, bf16 rows store Y)
         const float t0 = msg_act<ELU>(yc), t1 = msg_act<ELU>(yc + od.u0[c]);
         if (dev_side) {
-            if (BF) {   // exact three-way bf16 splits, (bit 0, bit 1) pairs
+            if constexpr (BF || F >= 256) {   // exact three-way bf16 splits, (bit 0, bit 1) pairs
                 unsigned sp[3];
                 split3(t0, t1, sp);
                 unsigned *Tu = reinterpret_cast<unsigned *>(A.T);
@@ -444,7 +444,6 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
     constexpr int LPH = 16 / K;              // op<-op lanes per head (K <= 16 on this path)
     // neighbour rows in flight per 16-lane group (a slot holds CPL or CPL/2 words)
     constexpr int EB = BF ? (F >= 256 && K >= 8 ? 4 : 8) : (F >= 256 ? 2 : 4);
-    constexpr int SB = 4;                    // fp32 op<-dev: device steps per batch of table loads
     constexpr int OS = F + 4;                // LDS tile row stride
     constexpr int ECAP = F >= 256 ? 512 : 192;   // op<-op entries staged in LDS per chunk (192 keeps
                                                  // four blocks per CU at f = 128)
@@ -704,134 +703,191 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
         if (ri >= 0) finish();
     }
 
-    // ---- op <- device on the matrix cores; the message-table operands are
-    // loaded before the barrier so their latency overlaps the slowest group
-    f4 acc[4][NCB];
-    float zl[4][HPW];
-#pragma unroll
-    for (int rb = 0; rb < 4; ++rb) {
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) acc[rb][cb] = f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int hh = 0; hh < HPW; ++hh) zl[rb][hh] = 0.f;
-    }
-    if constexpr (BF) {
-        // sparse 16x16x64 bf16 products (smfmac_split3) over the exact
-        // three-way splits of the fp32 attention weights and message table:
-        // k = 2j + b over 32 devices per step.  An (op, device) link carries
-        // one bit, so each device's pair of k holds at most one nonzero
-        // weight: the 2:4 structure the sparse products take.  Lane group
-        // g = l / 16 gives the weights of devices 8g .. 8g+7 of a step (value v
-        // at position 2 (v % 2) + bit of its device pair's four k) and the
-        // table entries of devices 4g .. 4g+3 and 16+4g .. 16+4g+3 (both bits).
-        // Per step, the weights of one head for the four row blocks are formed
-        // first; the table parts then stream one 16-column block at a time,
-        // the next block's loads in flight while the current one is used.
-        const unsigned *Tp = reinterpret_cast<const unsigned *>(A.T) + ((int64_t)r * A.n_dev + d0) * F;
-        const int64_t tpart = (int64_t)A.R * A.n_dev * F;   // stride between the three parts
-        const int ksteps = (Mg + 31) / 32;
+    // ---- op <- device on the matrix cores.  bf16, and fp32 at F = 256:
+    // sparse 16x16x64 bf16 products (smfmac_split3) over the exact three-way
+    // splits of the fp32 attention weights and message table: k = 2j + b
+    // over 32 devices per step.  An
+    // (op, device) link carries one bit, so each device's pair of k holds at
+    // most one nonzero weight: the 2:4 structure the sparse products take.
+    // Lane group g = l / 16 gives the weights of devices 8g .. 8g+7 of a step
+    // (value v at position 2 (v % 2) + bit of its device pair's four k) and
+    // the table entries of devices 4g .. 4g+3 and 16+4g .. 16+4g+3 (both
+    // bits).  The tile's four row blocks go in two halves of two (halving the
+    // registers that hold weights and accumulators); per step the weights of
+    // one head are formed first, then the table parts stream one 16-column
+    // block at a time, the next block's loads in flight while the current one
+    // is used.  The first table loads are issued before the barrier, so their
+    // latency overlaps the slowest op<-op group.
+    constexpr bool kSparseDev = BF || F >= 256;   // (fp32 at F <= 128: see below)
+    if constexpr (kSparseDev) {
+        // table words by 32-bit byte offsets from the table's (wave-uniform)
+        // start; the host checks that the table fits 4 GiB.  Devices past the
+        // group read its last device (their weights are zero).
+        const char *Tb = reinterpret_cast<const char *>(A.T);
+        const uint32_t tpart = (uint32_t)A.R * (uint32_t)A.n_dev * F * 4u;   // bytes between the three parts
+        const uint32_t trow = ((uint32_t)r * (uint32_t)A.n_dev + (uint32_t)d0) * F * 4u + (cbase + (lane & 15)) * 4u;
+        const int ksteps = (Mg + 31) / 32;   // <= 2: a tile group holds at most 64 devices
         auto load_b = [&](int ks, int cb, bf16x16 (&bo)[3]) {
             const int jb = 32 * ks + 4 * (lane >> 4);
-            const int c = cbase + cb * 16 + (lane & 15);
 #pragma unroll
             for (int z = 0; z < 3; ++z) {
                 unsigned w[8];
 #pragma unroll
                 for (int q = 0; q < 8; ++q) {
-                    const int j = jb + (q < 4 ? q : 12 + q);
-                    w[q] = j < Mg ? Tp[z * tpart + (int64_t)j * F + c] : 0u;
+                    const int j = min(jb + (q < 4 ? q : 12 + q), Mg - 1);
+                    w[q] = *reinterpret_cast<const unsigned *>(Tb + (trow + z * tpart + (uint32_t)(j * F + cb * 16) * 4u));
                 }
                 bo[z] = as_bf16x16(w);
             }
         };
         bf16x16 bops[2][3];
-        load_b(0, 0, bops[0]);
+        if (ksteps > 0) load_b(0, 0, bops[0]);
         __syncthreads();
-        uint64_t prs[4], bts[4];
-        float q2[4][HPW], m2[4][HPW];
-#pragma unroll
-        for (int rb = 0; rb < 4; ++rb) {
-            const int u = rb * 16 + (lane & 15);
-            prs[rb] = pres[u];
-            bts[rb] = bits[u];
-#pragma unroll
-            for (int hh = 0; hh < HPW; ++hh) {
-                q2[rb][hh] = qo[u][h0 + hh];
-                m2[rb][hh] = mxS[u][h0 + hh];
-            }
-        }
 #pragma unroll 1
-        for (int ks = 0; ks < ksteps; ++ks) {   // ksteps <= 2: a tile group holds at most 64 devices
-            const int jb = 32 * ks + 8 * (lane >> 4);
-            unsigned on8[4], bit8[4];
-            int idx[4];
+        for (int half = 0; half < 2; ++half) {
+            f4 acc[2][NCB];
+            float zl[2][HPW], q2[2][HPW], m2[2][HPW];
+            uint64_t prs[2], bts[2];
 #pragma unroll
-            for (int rb = 0; rb < 4; ++rb) {
-                // the lane's eight presence and bit flags (never set for jb + q >= Mg)
-                on8[rb] = (unsigned)(prs[rb] >> jb) & 0xffu;
-                bit8[rb] = (unsigned)(bts[rb] >> jb) & 0xffu;
-                // position of value q: 2 (q % 2) + bit, in bits 2q+1..2q
-                unsigned sb = (bit8[rb] | (bit8[rb] << 4)) & 0x0f0fu;
-                sb = (sb | (sb << 2)) & 0x3333u;
-                sb = (sb | (sb << 1)) & 0x5555u;
-                idx[rb] = (int)(0x8888u | sb);
-            }
+            for (int b2 = 0; b2 < 2; ++b2) {
+                const int u = (2 * half + b2) * 16 + (lane & 15);
+                prs[b2] = pres[u];
+                bts[b2] = bits[u];
 #pragma unroll
-            for (int hh = 0; hh < HPW; ++hh) {
-                float p0q[8], p1q[8];
-#pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    p0q[q] = P[jb + q][0][h0 + hh];
-                    p1q[q] = P[jb + q][1][h0 + hh];
+                for (int hh = 0; hh < HPW; ++hh) {
+                    q2[b2][hh] = qo[u][h0 + hh];
+                    m2[b2][hh] = mxS[u][h0 + hh];
+                    zl[b2][hh] = 0.f;
                 }
-                bf8 aop[4][3];
 #pragma unroll
-                for (int rb = 0; rb < 4; ++rb) {
-                    unsigned w[3][4];
+                for (int cb = 0; cb < NCB; ++cb) acc[b2][cb] = f4{0.f, 0.f, 0.f, 0.f};
+            }
+#pragma unroll 1
+            for (int ks = 0; ks < ksteps; ++ks) {
+                const int jb = 32 * ks + 8 * (lane >> 4);
+                unsigned on8[2], bit8[2];
+                int idx[2];
 #pragma unroll
-                    for (int pr = 0; pr < 4; ++pr) {
-                        float af2[2];
+                for (int b2 = 0; b2 < 2; ++b2) {
+                    // the lane's eight presence and bit flags (never set for jb + q >= Mg)
+                    on8[b2] = (unsigned)(prs[b2] >> jb) & 0xffu;
+                    bit8[b2] = (unsigned)(bts[b2] >> jb) & 0xffu;
+                    // position of value q: 2 (q % 2) + bit, in bits 2q+1..2q
+                    unsigned sb = (bit8[b2] | (bit8[b2] << 4)) & 0x0f0fu;
+                    sb = (sb | (sb << 2)) & 0x3333u;
+                    sb = (sb | (sb << 1)) & 0x5555u;
+                    idx[b2] = (int)(0x8888u | sb);
+                }
 #pragma unroll
-                        for (int e = 0; e < 2; ++e) {
-                            const int q = 2 * pr + e;
-                            const bool on = (on8[rb] >> q) & 1u;
-                            const bool bit = (bit8[rb] >> q) & 1u;
-                            const float x = (bit ? p1q[q] : p0q[q]) + q2[rb][hh];
-                            af2[e] = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
-                            zl[rb][hh] += af2[e];
+                for (int hh = 0; hh < HPW; ++hh) {
+                    float p0q[8], p1q[8];
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) {
+                        p0q[q] = P[jb + q][0][h0 + hh];
+                        p1q[q] = P[jb + q][1][h0 + hh];
+                    }
+                    bf8 aop[2][3];
+#pragma unroll
+                    for (int b2 = 0; b2 < 2; ++b2) {
+                        unsigned w[3][4];
+#pragma unroll
+                        for (int pr = 0; pr < 4; ++pr) {
+                            float af2[2];
+#pragma unroll
+                            for (int e = 0; e < 2; ++e) {
+                                const int q = 2 * pr + e;
+                                const bool on = (on8[b2] >> q) & 1u;
+                                const bool bit = (bit8[b2] >> q) & 1u;
+                                const float x = (bit ? p1q[q] : p0q[q]) + q2[b2][hh];
+                                af2[e] = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[b2][hh]) : 0.f;
+                                zl[b2][hh] += af2[e];
+                            }
+                            unsigned sp[3];
+                            split3(af2[0], af2[1], sp);
+#pragma unroll
+                            for (int z = 0; z < 3; ++z) w[z][pr] = sp[z];
                         }
-                        unsigned sp[3];
-                        split3(af2[0], af2[1], sp);
 #pragma unroll
-                        for (int z = 0; z < 3; ++z) w[z][pr] = sp[z];
+                        for (int z = 0; z < 3; ++z) aop[b2][z] = as_bf8(w[z][0], w[z][1], w[z][2], w[z][3]);
                     }
 #pragma unroll
-                    for (int z = 0; z < 3; ++z) aop[rb][z] = as_bf8(w[z][0], w[z][1], w[z][2], w[z][3]);
+                    for (int c2 = 0; c2 < CPH; ++c2) {
+                        const int cb = hh * CPH + c2;
+                        // the next (step, column block) pair's table parts
+                        // (after the first half's last pair: the first pair
+                        // again), into the buffer this pair does not use; with
+                        // one column block (NCB = 1) every pair uses bops[0], so
+                        // the next step's parts are loaded after its products
+                        auto prefetch = [&]() {
+                            if (cb + 1 < NCB) load_b(ks, cb + 1, bops[(cb + 1) & 1]);
+                            else if (ks + 1 < ksteps) load_b(ks + 1, 0, bops[0]);
+                            else if (half == 0) load_b(0, 0, bops[0]);
+                        };
+                        constexpr bool kAlt = NCB % 2 == 0;   // consecutive pairs alternate buffers
+                        if (kAlt || cb + 1 < NCB) prefetch();
+#pragma unroll
+                        for (int b2 = 0; b2 < 2; ++b2)
+                            acc[b2][cb] = smfmac_split3(aop[b2], bops[cb & 1], idx[b2], acc[b2][cb]);
+                        if (!kAlt && cb + 1 == NCB) prefetch();
+                    }
+                }
+            }
+            // softmax sums of op row rb*16 + l%16 are spread over lanes l,
+            // l+16, l+32, l+48; the output row of register v in lane l is
+            // rb*16 + 4(l/16) + v; the op<-device part is added into the LDS
+            // tile in place (each (row, column) belongs to one lane)
+#pragma unroll
+            for (int b2 = 0; b2 < 2; ++b2) {
+                const int rb = 2 * half + b2;
+                float scale[HPW][4];
+#pragma unroll
+                for (int hh = 0; hh < HPW; ++hh) {
+                    float z = zl[b2][hh];
+                    z += __shfl_xor(z, 16, 64);
+                    z += __shfl_xor(z, 32, 64);
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const float zv = __shfl(z, 4 * (lane >> 4) + v, 64);
+                        scale[hh][v] = zv > 0.f ? A.g_cross * __builtin_amdgcn_rcpf(zv) : 0.f;
+                    }
                 }
 #pragma unroll
-                for (int c2 = 0; c2 < CPH; ++c2) {
-                    const int cb = hh * CPH + c2;
-                    // the next (step, column block) pair's table parts
-                    if (cb + 1 < NCB) load_b(ks, cb + 1, bops[(cb + 1) & 1]);
-                    else if (ks + 1 < ksteps) load_b(ks + 1, 0, bops[0]);
+                for (int v = 0; v < 4; ++v) {
+                    const int u = rb * 16 + 4 * (lane >> 4) + v;
 #pragma unroll
-                    for (int rb = 0; rb < 4; ++rb)
-                        acc[rb][cb] = smfmac_split3(aop[rb], bops[cb & 1], idx[rb], acc[rb][cb]);
+                    for (int cb = 0; cb < NCB; ++cb) {
+                        const int col = cbase + cb * 16 + (lane & 15);
+                        Ot[u * OS + col] = fmaf(scale[cb / CPH][v], acc[b2][cb][v], Ot[u * OS + col]);
+                    }
                 }
             }
         }
     } else {
-        // fp32 16x16x4 products: k = 4 (device, bit) pairs per step, two
-        // devices per step; the table loads of SB steps are issued together
+        // fp32 at F <= 128: fp32 16x16x4 products over the fp32 message table
+        // [rows][2][F], k = 4 (device, bit) pairs per step, two devices per
+        // step (half of each step's k is zero, but the narrower register
+        // footprint keeps four blocks per CU, which measured faster here than
+        // the sparse products at two); the table loads of SB steps are issued
+        // together
+        constexpr int SB = 4;
+        f4 acc[4][NCB];
+        float zl[4][HPW];
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb) {
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) acc[rb][cb] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int hh = 0; hh < HPW; ++hh) zl[rb][hh] = 0.f;
+        }
         const float *Tb = A.T + ((int64_t)r * A.n_dev + d0) * 2 * F;
         const int steps = (Mg + 1) / 2;
         const int b = (lane >> 4) & 1;
         float bv[SB][NCB];
         auto load_batch = [&](int s0) {
-    #pragma unroll
+#pragma unroll
             for (int k = 0; k < SB; ++k) {
                 const int j = 2 * (s0 + k) + (lane >> 5);
-    #pragma unroll
+#pragma unroll
                 for (int cb = 0; cb < NCB; ++cb)
                     bv[k][cb] = j < Mg ? Tb[((int64_t)j * 2 + b) * F + cbase + cb * 16 + (lane & 15)] : 0.f;
             }
@@ -841,12 +897,12 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
         // per-lane constants of the lane's op rows u = rb*16 + l%16
         uint64_t prs[4], bts[4];
         float q2[4][HPW], m2[4][HPW];
-    #pragma unroll
+#pragma unroll
         for (int rb = 0; rb < 4; ++rb) {
             const int u = rb * 16 + (lane & 15);
             prs[rb] = pres[u];
             bts[rb] = bits[u];
-    #pragma unroll
+#pragma unroll
             for (int hh = 0; hh < HPW; ++hh) {
                 q2[rb][hh] = qo[u][h0 + hh];
                 m2[rb][hh] = mxS[u][h0 + hh];
@@ -854,28 +910,28 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
         }
         for (int s0 = 0; s0 < steps; s0 += SB) {
             float bc[SB][NCB];
-    #pragma unroll
+#pragma unroll
             for (int k = 0; k < SB; ++k)
-    #pragma unroll
+#pragma unroll
                 for (int cb = 0; cb < NCB; ++cb) bc[k][cb] = bv[k][cb];
             if (s0 + SB < steps) load_batch(s0 + SB);
-    #pragma unroll
+#pragma unroll
             for (int k = 0; k < SB; ++k) {
                 const int j = 2 * (s0 + k) + (lane >> 5);
                 if (2 * (s0 + k) >= Mg) break;
                 const bool jok = j < Mg;
                 float pj[HPW];
-    #pragma unroll
+#pragma unroll
                 for (int hh = 0; hh < HPW; ++hh) pj[hh] = P[j][b][h0 + hh];
-    #pragma unroll
+#pragma unroll
                 for (int rb = 0; rb < 4; ++rb) {
                     const bool on = jok && ((prs[rb] >> j) & 1ull) && ((int)((bts[rb] >> j) & 1ull) == b);
-    #pragma unroll
+#pragma unroll
                     for (int hh = 0; hh < HPW; ++hh) {
                         const float x = pj[hh] + q2[rb][hh];
                         const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
                         zl[rb][hh] += af;
-    #pragma unroll
+#pragma unroll
                         for (int c2 = 0; c2 < CPH; ++c2)
                             acc[rb][hh * CPH + c2] = __builtin_amdgcn_mfma_f32_16x16x4f32(
                                 af, bc[k][hh * CPH + c2], acc[rb][hh * CPH + c2], 0, 0, 0);
@@ -883,32 +939,32 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
                 }
             }
         }
-    }
-    // softmax sums of op row rb*16 + l%16 are spread over lanes l, l+16,
-    // l+32, l+48; the output row of register v in lane l is rb*16 + 4(l/16) + v
+        // softmax sums of op row rb*16 + l%16 are spread over lanes l, l+16,
+        // l+32, l+48; the output row of register v in lane l is rb*16 + 4(l/16) + v
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb) {
-        float scale[HPW][4];
+        for (int rb = 0; rb < 4; ++rb) {
+            float scale[HPW][4];
 #pragma unroll
-        for (int hh = 0; hh < HPW; ++hh) {
-            float z = zl[rb][hh];
-            z += __shfl_xor(z, 16, 64);
-            z += __shfl_xor(z, 32, 64);
+            for (int hh = 0; hh < HPW; ++hh) {
+                float z = zl[rb][hh];
+                z += __shfl_xor(z, 16, 64);
+                z += __shfl_xor(z, 32, 64);
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const float zv = __shfl(z, 4 * (lane >> 4) + v, 64);
+                    scale[hh][v] = zv > 0.f ? A.g_cross * __builtin_amdgcn_rcpf(zv) : 0.f;
+                }
+            }
+            // the op<-device part is added into the LDS tile in place (each
+            // (row, column) belongs to one lane)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const float zv = __shfl(z, 4 * (lane >> 4) + v, 64);
-                scale[hh][v] = zv > 0.f ? A.g_cross * __builtin_amdgcn_rcpf(zv) : 0.f;
-            }
-        }
-        // the op<-device part is added into the LDS tile in place (each
-        // (row, column) belongs to one lane)
+                const int u = rb * 16 + 4 * (lane >> 4) + v;
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int u = rb * 16 + 4 * (lane >> 4) + v;
-#pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) {
-                const int col = cbase + cb * 16 + (lane & 15);
-                Ot[u * OS + col] = fmaf(scale[cb / CPH][v], acc[rb][cb][v], Ot[u * OS + col]);
+                for (int cb = 0; cb < NCB; ++cb) {
+                    const int col = cbase + cb * 16 + (lane & 15);
+                    Ot[u * OS + col] = fmaf(scale[cb / CPH][v], acc[rb][cb][v], Ot[u * OS + col]);
+                }
             }
         }
     }
@@ -986,6 +1042,9 @@ void launch_pack_masks(const AggArgs &A, hipStream_t st) {
 
 bool launch_agg_mfma(int F, int K, bool bf, const AggArgs &A, hipStream_t st) {
     if (!mfma_path_supported(F, K, A.n_op, bf ? 2 : 4)) return false;
+    // the device message table (three parts of R n_dev F words) is addressed
+    // by 32-bit byte offsets
+    if ((int64_t)A.R * A.n_dev * F * 12 >= (int64_t(1) << 32)) return false;
     if (A.elu) {   // the ELU variant runs in fp32
         if (bf) return false;
         if (F == 64) return dispatch_mfma_heads<64, false, true>(K, A, st);

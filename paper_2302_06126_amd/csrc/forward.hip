@@ -381,7 +381,7 @@ size_t carve_fwd(const tag_graph *g, const tag_model_dims *d, int32_t R, void *b
         L->omask = c.take<uint64_t>((size_t)R * g->n_op * 2);
         L->Sdev = c.take<float>((size_t)R * g->n_dev * 4 * d->heads);
         // fp32 message table [R n_dev][2][F], or its three bf16 split parts [3][R n_dev][F]
-        L->T = c.take<float>((size_t)R * g->n_dev * (d->dtype == TAG_BF16 ? 3 : 2) * F);
+        L->T = c.take<float>((size_t)R * g->n_dev * 3 * F);
         L->Sop = c.take<float>((size_t)R * g->n_op * 4 * d->heads);
         L->tile_ext = c.take<int32_t>((size_t)std::max<int32_t>(g->n_tiles, 1) * 8);
         L->xcsr = c.take<float>((size_t)R * std::max<int64_t>(g->nnz[0], 1));

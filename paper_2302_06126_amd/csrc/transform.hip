@@ -217,7 +217,7 @@ __device__ void store_tile_bf16(const GemmArgs &G, const Tile &t, int wm, int wn
 // 256-byte row segments, four rows per store instruction (stored from the
 // accumulator layout, each instruction would cover half of sixteen lines).
 constexpr int kStageStride = 64 + 4;
-template <int JPH, bool ELU, int NI, int CS, int J0, int NJ>
+template <int JPH, bool ELU, int NI, int CS, int J0, int NJ, bool TSP>
 __device__ void store_rows(const GemmArgs &G, const Tile &t, int64_t rbase, int col0, int lane,
                            const f4 (&acc)[NJ][NI], const float *cst, float *stage) {
     static_assert(J0 + 4 <= NJ, "four column blocks");
@@ -275,7 +275,16 @@ __device__ void store_rows(const GemmArgs &G, const Tile &t, int64_t rbase, int 
                             p1 = fmaf(c1[v], t1[v], p1);
                             q = fmaf(c2[v], yv[v], q);
                         }
-                        if (dev_od) {   // message rows of bit 0 / 1
+                        if (TSP && dev_od) {   // message rows of bit 0 / 1 as exact splits, (bit 0, bit 1) pairs
+                            unsigned sp[4][3];
+#pragma unroll
+                            for (int v = 0; v < 4; ++v) split3(t0[v], t1[v], sp[v]);
+                            unsigned *Tu = reinterpret_cast<unsigned *>(P.T);
+#pragma unroll
+                            for (int z = 0; z < 3; ++z)
+                                *reinterpret_cast<u4 *>(Tu + z * rows * F + m * F + c) =
+                                    u4{sp[0][z], sp[1][z], sp[2][z], sp[3][z]};
+                        } else if (!TSP && dev_od) {   // fp32 message rows of bit 0 / 1
                             *reinterpret_cast<float4 *>(P.T + (m * 2 + 0) * F + c) = make_float4(t0[0], t0[1], t0[2], t0[3]);
                             *reinterpret_cast<float4 *>(P.T + (m * 2 + 1) * F + c) = make_float4(t1[0], t1[1], t1[2], t1[3]);
                         }
@@ -350,7 +359,7 @@ __device__ __forceinline__ void column_consts(const GemmArgs &G, int sd, int n, 
 // 32-wide k-step at a time, double-buffered, rows unpadded with XOR-swizzled
 // 16-byte chunks (as in gemm_bf16).  The next step's global loads are in
 // flight while the current step's 96 products per wavefront run.
-template <int JPH, bool ELU = false>
+template <int JPH, bool ELU, bool TSP>
 __global__ void __launch_bounds__(256) gemm_f32s(GemmArgs G) {
     constexpr int BK = 32;
     __shared__ __attribute__((aligned(16))) uint16_t Ws[2][3][BN * BK];
@@ -480,8 +489,8 @@ __global__ void __launch_bounds__(256) gemm_f32s(GemmArgs G) {
     // stage per wavefront
     float *stage = reinterpret_cast<float *>(&Ws[0][0][0]) + wave * 32 * kStageStride;
     static_assert(4 * 32 * kStageStride * 4 <= sizeof(Ws), "row stages must fit the k-step buffers");
-    store_rows<JPH, ELU, 2, BN, 0>(G, t, rbase, t.n0, lane, acc, cst, stage);
-    store_rows<JPH, ELU, 2, BN, 4>(G, t, rbase, t.n0 + 64, lane, acc, cst + 64, stage);
+    store_rows<JPH, ELU, 2, BN, 0, 8, TSP>(G, t, rbase, t.n0, lane, acc, cst, stage);
+    store_rows<JPH, ELU, 2, BN, 4, 8, TSP>(G, t, rbase, t.n0 + 64, lane, acc, cst + 64, stage);
 }
 
 template <int JPH>
@@ -578,9 +587,15 @@ int64_t transform_row_tiles(int64_t rows) { return (rows + BM - 1) / BM; }
 
 template <int JPH>
 void launch_gemm(const GemmArgs &G, bool bf, unsigned blocks, hipStream_t st) {
+    // the device message table: split planes at F = 256, fp32 rows below
     if (bf) gemm_bf16<JPH><<<blocks, 256, 0, st>>>(G);
-    else if (G.prep.elu) gemm_f32s<JPH, true><<<blocks, 256, 0, st>>>(G);
-    else gemm_f32s<JPH><<<blocks, 256, 0, st>>>(G);
+    else if (G.F >= 256) {
+        if (G.prep.elu) gemm_f32s<JPH, true, true><<<blocks, 256, 0, st>>>(G);
+        else gemm_f32s<JPH, false, true><<<blocks, 256, 0, st>>>(G);
+    } else {
+        if (G.prep.elu) gemm_f32s<JPH, true, false><<<blocks, 256, 0, st>>>(G);
+        else gemm_f32s<JPH, false, false><<<blocks, 256, 0, st>>>(G);
+    }
 }
 
 void launch_transform(const GemmArgs &G, bool bf, hipStream_t st) {

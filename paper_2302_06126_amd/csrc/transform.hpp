@@ -25,8 +25,9 @@ struct GemmSide {
 // (with Y the unbiased W^h h)
 //   S[row][2][h] = a~_od . Y_od                       destination term, od
 //   S[row][3][h] = a~_same . Y_same                   destination term, oo / dd
-// and, for device rows, the two fp32 message rows T[row][b] = sigma(Y_od + c'_od + b U_od)
-// (sigma: ReLU, or ELU for the variant).
+// and, for device rows, the two message rows T[row][b] = sigma(Y_od + c'_od + b U_od)
+// (sigma: ReLU, or ELU for the variant): as exact three-way bf16 splits in
+// the bf16 variant and at F = 256, as fp32 rows otherwise.
 struct GemmPrep {
     int jph;             // 16-column blocks per head (1, 2, 4); 0: no attention terms
     int K;
@@ -36,8 +37,8 @@ struct GemmPrep {
     const float *u_od;                   // U_od[c] at u_od[2c]
     const float *ad_same[2];             // [F]: oo (side 0), dd (side 1)
     float *S[2];                         // [rows][4][K]
-    float *T;                            // device rows: fp32 [rows][2][F]; bf16 variant: [3][rows][F]
-                                         // packed (bit 0, bit 1) pairs of the split3 parts
+    float *T;                            // device rows: [3][rows][F] packed (bit 0, bit 1) pairs
+                                         // of the split3 parts (bf16, or F = 256), else fp32 [rows][2][F]
 };
 struct GemmArgs {
     GemmSide side[2];

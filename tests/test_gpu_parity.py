@@ -205,6 +205,18 @@ def test_forward_edge_cases(n, m, oo, dd, od):
     c.check(E_op, E_dev, range(2))
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_forward_two_device_steps_one_column_block(dtype):
+    # f = 64: each wavefront of the op<-device contraction covers a single
+    # 16-column block, and 64 linked devices take two 32-device steps, so
+    # every (step, block) pair uses the same table buffer
+    topo = mk_topo(70, 64, [(i, i + 1) for i in range(69)], [(0, 63), (5, 6)], None)
+    c = Case(topo, 3, 64, 4, 2, dtype=dtype, seed=71)
+    say(f"forward two device steps, one column block, {dtype}")
+    _, _, E_op, E_dev = c.gpu_forward()
+    c.check(E_op, E_dev, range(3))
+
+
 def test_forward_deterministic_and_batch_invariant():
     topo = synth.random_topology(9, 400, 16, 700, od_per_op=6)
     c = Case(topo, 4, 128, 4, 3, seed=9)
