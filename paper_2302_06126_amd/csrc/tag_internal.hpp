@@ -86,7 +86,7 @@ struct tag_graph {
 
 namespace tag {
 constexpr int kOpTile = 64;
-constexpr int kMaxDevRecords = 16;   // device<-op partial records per device row
+constexpr int kMaxDevRecords = 8;    // device<-op partial records per device row
 
 // tiles per group for a topology of nt op tiles
 inline int32_t tiles_per_group(int64_t nt) {
