@@ -50,6 +50,22 @@ def test_elu_forward_matches_oracle(f, heads, layers):
     say(f"  worst row-relative error {worst:.2e}")
 
 
+def test_elu_forward_many_devices_wide_rows():
+    # 40 devices at f = 256: the op<-device contraction on sparse split
+    # products over the ELU message table, two 32-device steps (the second ragged)
+    say("[elu] forward f=256, 40 devices")
+    topo = synth.random_topology(440, 120, 40, 250, od_per_op=None, dd_density=0.3)
+    c = Case(topo, 2, 256, 4, 2, seed=40)
+    E_op, E_dev = _elu_forward(c)
+    for r in range(c.R):
+        R_op, R_dev = oracle.forward(c.topo, c.x_op[r], c.x_dev[r], c.x_oo[r], c.x_dd[r], c.x_od[r], c.w, f=256,
+                                     heads=4, layers=2, sigma="elu")
+        got = np.vstack([E_op[r], E_dev[r]])
+        assert np.all(np.isfinite(got))
+        err = row_rel_err(got, np.vstack([R_op, R_dev]))
+        assert err <= FP32_TOL, (r, err)
+
+
 def test_elu_saturated_messages_give_minus_gamma_sums():
     say("[elu] saturated messages")
     topo = synth.random_topology(410, 90, 5, 150, od_per_op=3, dd_density=0.6)

@@ -217,6 +217,20 @@ def test_forward_two_device_steps_one_column_block(dtype):
     c.check(E_op, E_dev, range(3))
 
 
+@pytest.mark.parametrize("f,dtype,m,od", [(256, "f32", 40, None), (256, "f32", 64, 6), (128, "bf16", 40, None),
+                                          (256, "bf16", 48, 5)])
+def test_forward_device_groups_past_32(f, dtype, m, od):
+    # more than 32 devices per topology: the op<-device contraction takes two
+    # 32-device steps (the second ragged for 40 and 48), with the device
+    # message table as split planes (bf16, and fp32 at f = 256)
+    topo = synth.random_topology(f + m, 150, m, 300, od_per_op=od, dd_density=0.3)
+    c = Case(topo, 2, f, 4, 2, dtype=dtype, seed=m)
+    say(f"forward {m} devices f={f} {dtype} od_per_op={od}")
+    _, _, E_op, E_dev = c.gpu_forward()
+    err = c.check(E_op, E_dev, range(2))
+    say(f"  worst row-rel err {err:.2e}")
+
+
 def test_forward_deterministic_and_batch_invariant():
     topo = synth.random_topology(9, 400, 16, 700, od_per_op=6)
     c = Case(topo, 4, 128, 4, 3, seed=9)
