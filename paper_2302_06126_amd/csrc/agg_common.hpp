@@ -109,7 +109,11 @@ struct AggArgs {
 };
 
 // MFMA path (agg_mfma.hip)
-bool mfma_path_supported(int F, int K, int64_t n_op, int esz);
+// whether the tile path takes a layer: heads of 16 to F channels (K <= 16),
+// and the per-candidate transform rows (n_op 2F elements of esz bytes) and
+// the device message table (three parts of R n_dev F words) addressed by
+// 32-bit byte offsets
+bool mfma_path_supported(int F, int K, int64_t n_op, int64_t R, int64_t n_dev, int esz);
 void launch_pack_masks(const AggArgs &A, hipStream_t st);
 void launch_prep_tiles_x(const AggArgs &A, int64_t nnz0, hipStream_t st);
 bool launch_agg_mfma(int F, int K, bool bf, const AggArgs &A, hipStream_t st);

@@ -8,9 +8,14 @@
 // 64-op tile of one topology:
 //   device <- op:  acc[j][c] = sum_{u, b} alpha_k(j, u, b) m_b[u][c]   (M x 128) x (128 x f)
 //   op <- device:  acc[u][c] = sum_{j, b} alpha_k(u, j, b) m_b[j][c]   (64 x 2M) x (2M x f)
-// with alpha = 0 unless (u, j) is a placement link whose bit is b.  They run
-// as fp32 MFMA 16x16x4 products; the attention weights are formed in
-// registers as the A operand.  device <- op tiles write (max, sum, partial)
+// with alpha = 0 unless (u, j) is a placement link whose bit is b, so each
+// (row, source) pair of k = 2 source + b holds at most one nonzero weight:
+// the 2:4 structure of the sparse 16x16x64 bf16 products, which take both
+// operands as exact three-way bf16 splits (six part products, an fp32
+// contraction up to fp32 rounding).  fp32 op <- device at F <= 128 runs on
+// fp32 16x16x4 products instead (fewer registers, four blocks per CU).  The
+// attention weights are formed in registers as the A operand.  device <- op
+// tiles write (max, sum, partial)
 // records that a merge pass combines in tile order; op <- device rows are
 // complete inside one tile and are normalised directly; the same kernel
 // gathers the tile's op <- op rows and writes each op row once.
@@ -1024,8 +1029,9 @@ bool dispatch_mfma_heads(int K, const AggArgs &A, hipStream_t st) {
 
 // heads of at least 16 channels, at most 16 heads, and a candidate's relation
 // transforms within 32-bit byte offsets of its base (the op<-op gathers)
-bool mfma_path_supported(int F, int K, int64_t n_op, int esz) {
-    return K >= 1 && F / K >= 16 && K <= 16 && n_op * 2 * F * esz < (int64_t(1) << 32);
+bool mfma_path_supported(int F, int K, int64_t n_op, int64_t R, int64_t n_dev, int esz) {
+    return K >= 1 && F / K >= 16 && K <= 16 && n_op * 2 * F * esz < (int64_t(1) << 32) &&
+           R * n_dev * F * 12 < (int64_t(1) << 32);
 }
 
 void launch_prep_tiles_x(const AggArgs &A, int64_t nnz0, hipStream_t st) {
@@ -1041,10 +1047,7 @@ void launch_pack_masks(const AggArgs &A, hipStream_t st) {
 }
 
 bool launch_agg_mfma(int F, int K, bool bf, const AggArgs &A, hipStream_t st) {
-    if (!mfma_path_supported(F, K, A.n_op, bf ? 2 : 4)) return false;
-    // the device message table (three parts of R n_dev F words) is addressed
-    // by 32-bit byte offsets
-    if ((int64_t)A.R * A.n_dev * F * 12 >= (int64_t(1) << 32)) return false;
+    if (!mfma_path_supported(F, K, A.n_op, A.R, A.n_dev, bf ? 2 : 4)) return false;
     if (A.elu) {   // the ELU variant runs in fp32
         if (bf) return false;
         if (F == 64) return dispatch_mfma_heads<64, false, true>(K, A, st);

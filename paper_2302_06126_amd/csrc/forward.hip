@@ -307,7 +307,7 @@ void launch_dev_final(const AggArgs &A, hipStream_t st) {
 template <int F, int K, bool BF, bool ELU = false>
 void launch_layer(bool mfma, const AggArgs &A, hipStream_t st) {
     if (!mfma) launch_agg<F, K, BF, ELU>(A, st);
-    else launch_agg_mfma(F, K, BF, A, st);
+    else launch_agg_mfma(F, K, BF, A, st);   // takes every layer the layout was planned for
     launch_dev_final<F, K, BF, ELU>(A, st);
 }
 
@@ -373,7 +373,7 @@ size_t carve_fwd(const tag_graph *g, const tag_model_dims *d, int32_t R, void *b
     }
     L->Y_op = c.take<char>((size_t)R * g->n_op * 2 * F * es);
     L->Y_dev = c.take<char>((size_t)R * g->n_dev * 2 * F * es);
-    L->mfma = mfma_path_supported(F, d->heads, g->n_op, (int)es);
+    L->mfma = mfma_path_supported(F, d->heads, g->n_op, R, g->n_dev, (int)es);
     L->maxc = L->mfma ? std::max<int32_t>(1, g->max_groups)
                       : std::max<int32_t>(1, (g->max_degree[2] + kChunk - 1) / kChunk);
     L->part = c.take<float>((size_t)R * g->n_dev * L->maxc * (F + 2 * d->heads));

@@ -201,7 +201,7 @@ __device__ void store_tile_bf16(const GemmArgs &G, const Tile &t, int wm, int wn
 // (weights as the first MFMA operand), so result register v of block (j, i)
 // in lane l holds output row 16 i + l % 16 and output column 16 j + 4 (l / 16)
 // + v of a 64-column slab: each lane owns four consecutive columns of one row
-// per block, written with one vector store, and a head's attention sums
+// per block, staged with one 16-byte LDS write, and a head's attention sums
 // reduce inside the lane and then over the four lanes l % 16 + {0, 16, 32, 48}.
 //
 // The per-column constants are read from LDS (`cst[kind * CS + column]`,
@@ -231,8 +231,7 @@ __device__ void store_rows(const GemmArgs &G, const Tile &t, int64_t rbase, int 
     const int g = lane >> 4;
     const bool dev_od = od && t.sd == 1;           // device rows also get the message table
     float *S = P.S[t.sd];
-    // row blocks outer, column blocks inner: the four stores of a row block
-    // complete whole 256-byte row segments back to back
+    // row blocks outer, column blocks inner
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
         const int64_t m = rbase + 16 * i;
