@@ -36,6 +36,7 @@ struct Tile {
     int n0;
 };
 
+template <int TM = BM>
 __device__ __forceinline__ Tile tile_of(const GemmArgs &G) {
     const uint32_t lb = xcd_swizzle(blockIdx.x, gridDim.x);
     const int ct = 2 * G.F / BN;
@@ -43,7 +44,7 @@ __device__ __forceinline__ Tile tile_of(const GemmArgs &G) {
     Tile t;
     t.n0 = (int)(lb % ct) * BN;
     t.sd = rt < G.tiles0 ? 0 : 1;
-    t.m0 = (rt - (t.sd ? G.tiles0 : 0)) * BM;
+    t.m0 = (rt - (t.sd ? G.tiles0 : 0)) * TM;
     return t;
 }
 
@@ -75,17 +76,18 @@ __device__ __forceinline__ float xpose_sum4(const float (&v)[4], int lane) {
 // 16-byte stores.
 constexpr int kTileStride = BN + 8;   // bf16 elements per LDS tile row (272 bytes)
 
-template <int JPH>
+template <int JPH, int MB>
 __device__ void store_tile_bf16(const GemmArgs &G, const Tile &t, int wm, int wn, int lane, const f4 (&acc)[4][4],
                                 uint16_t *sm) {
+    constexpr int NT = 2 * MB;                     // threads per block
     constexpr int HW = JPH > 0 ? 4 / JPH : 1;      // heads per wavefront
     const GemmPrep &P = G.prep;
     const int64_t rows = t.sd ? G.side[1].rows : G.side[0].rows;
     const int F = G.F, K = P.K, D = 16 * (JPH > 0 ? JPH : 1);
     const int64_t ldy = 2 * F;
     uint16_t *Yp = static_cast<uint16_t *>(t.sd ? G.side[1].Y : G.side[0].Y);
-    uint16_t *tile = sm;                                            // [BM][kTileStride]
-    float *cst = reinterpret_cast<float *>(sm + BM * kTileStride);  // [4][BN]: c', a, a~, U
+    uint16_t *tile = sm;                                            // [MB][kTileStride]
+    float *cst = reinterpret_cast<float *>(sm + MB * kTileStride);  // [4][BN]: c', a, a~, U
     const int tid = threadIdx.x;
     if (tid < BN) {   // constants of block column n0 + tid (same-type half: a = U = 0)
         const int n = t.n0 + tid;
@@ -186,8 +188,8 @@ __device__ void store_tile_bf16(const GemmArgs &G, const Tile &t, int wm, int wn
     __syncthreads();
     // whole rows of the block's 128 columns: 16 threads per row, 16 bytes each
 #pragma unroll
-    for (int it = 0; it < BM * BN / 8 / 256; ++it) {
-        const int idx = it * 256 + tid;
+    for (int it = 0; it < MB * BN / 8 / NT; ++it) {
+        const int idx = it * NT + tid;
         const int rr = idx >> 4, ch = idx & 15;
         const int64_t m = t.m0 + rr;
         if (m < rows) {
@@ -492,57 +494,66 @@ __global__ void __launch_bounds__(256) gemm_f32s(GemmArgs G) {
     store_rows<JPH, ELU, 2, BN, 4, 8, TSP>(G, t, rbase, t.n0 + 64, lane, acc, cst + 64, stage);
 }
 
-template <int JPH>
-__global__ void __launch_bounds__(256) gemm_bf16(GemmArgs G) {
-    constexpr int BK = kBkBf16;
+template <int JPH, int MB>
+__global__ void __launch_bounds__(2 * MB) gemm_bf16(GemmArgs G) {
+    // MB x 128 block tiles, MB / 32 wavefronts of 64 x 64 (two per column
+    // half): a taller block reads each k-chunk of the weights for more rows
+    constexpr int BK = kBkBf16, NT = 2 * MB;
     static_assert(BK == 32, "four 16-byte chunks per LDS row");
-    // k-chunk buffers As[2][BM * BK], Bs[2][BN * BK]: unpadded rows whose four
+    static_assert(MB == 128 || MB == 256, "two or four row wavefronts");
+    // k-chunk buffers As[2][MB * BK], Bs[2][BN * BK]: unpadded rows whose four
     // 16-byte chunks are XOR-swizzled (chunk c of row r at c ^ sw(r)) so that
     // neither the loader's stores (4 threads per row) nor the operand reads
     // (16 rows, one chunk) meet a bank twice; the epilogue reuses the space
     // for the output tile and the column constants
-    constexpr int SM = 2 * BM * (BK + 8) + 2 * BN * (BK + 8);
-    static_assert(BM * kTileStride * 2 + 4 * BN * 4 <= SM * 2, "epilogue tile must fit the k-chunk buffers");
+    constexpr int SMK = 2 * MB * BK + 2 * BN * BK, SME = (MB * kTileStride * 2 + 4 * BN * 4) / 2;
+    constexpr int SM = SMK > SME ? SMK : SME;
     __shared__ __attribute__((aligned(16))) uint16_t sm[SM];
-    uint16_t (*As)[BM * BK] = reinterpret_cast<uint16_t (*)[BM * BK]>(sm);
-    uint16_t (*Bs)[BN * BK] = reinterpret_cast<uint16_t (*)[BN * BK]>(sm + 2 * BM * BK);
+    uint16_t (*As)[MB * BK] = reinterpret_cast<uint16_t (*)[MB * BK]>(sm);
+    uint16_t (*Bs)[BN * BK] = reinterpret_cast<uint16_t (*)[BN * BK]>(sm + 2 * MB * BK);
     auto sw = [](int r) { return ((r >> 1) ^ (r >> 2)) & 3; };
-    const Tile t = tile_of(G);
+    const Tile t = tile_of<MB>(G);
     const GemmSide S = t.sd ? G.side[1] : G.side[0];
     const uint16_t *__restrict__ H = static_cast<const uint16_t *>(S.H);
     const int F = G.F;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    // loader: thread -> rows tid/4 and tid/4 + 64, 16-byte chunk tid % 4
+    // loader: 16-byte chunk tid % 4 of rows tid/4 + (NT/4) q; the A tile's MB
+    // rows take two per thread, the B tile's 128 rows 512 / NT
+    constexpr int QB = 4 * BN / NT;
     const int lc = tid & 3;
-    const uint16_t *arow[2], *brow[2];
+    const uint16_t *arow[2], *brow[QB];
     bool aok[2];
-    int loff[2];
+    int loffa[2], loffb[QB];
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-        const int lr = (tid >> 2) + 64 * q;
+        const int lr = (tid >> 2) + (NT / 4) * q;
         const int64_t gm = t.m0 + lr;
         aok[q] = gm < S.rows;
         arow[q] = H + (aok[q] ? gm : 0) * F + 8 * lc;
+        loffa[q] = lr * BK + 8 * (lc ^ sw(lr));
+    }
+#pragma unroll
+    for (int q = 0; q < QB; ++q) {
+        const int lr = (tid >> 2) + (NT / 4) * q;
         const int gn = t.n0 + lr;
         brow[q] = (gn < F ? static_cast<const uint16_t *>(S.B0) + (size_t)gn * S.ldb
                           : static_cast<const uint16_t *>(S.B1) + (size_t)(gn - F) * S.ldb) + 8 * lc;
-        loff[q] = lr * BK + 8 * (lc ^ sw(lr));
+        loffb[q] = lr * BK + 8 * (lc ^ sw(lr));
     }
-    u4 ra[2], rb[2];
+    u4 ra[2], rb[QB];
     auto gload = [&](int k0) {
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
+        for (int q = 0; q < 2; ++q)
             ra[q] = aok[q] ? *reinterpret_cast<const u4 *>(arow[q] + k0) : u4{0u, 0u, 0u, 0u};
-            rb[q] = *reinterpret_cast<const u4 *>(brow[q] + k0);
-        }
+#pragma unroll
+        for (int q = 0; q < QB; ++q) rb[q] = *reinterpret_cast<const u4 *>(brow[q] + k0);
     };
     auto sstore = [&](int buf) {
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
-            *reinterpret_cast<u4 *>(&As[buf][loff[q]]) = ra[q];
-            *reinterpret_cast<u4 *>(&Bs[buf][loff[q]]) = rb[q];
-        }
+        for (int q = 0; q < 2; ++q) *reinterpret_cast<u4 *>(&As[buf][loffa[q]]) = ra[q];
+#pragma unroll
+        for (int q = 0; q < QB; ++q) *reinterpret_cast<u4 *>(&Bs[buf][loffb[q]]) = rb[q];
     };
     f4 acc[4][4];
 #pragma unroll
@@ -577,17 +588,19 @@ __global__ void __launch_bounds__(256) gemm_bf16(GemmArgs G) {
         if (kc + 1 < nk) sstore(buf ^ 1);
         __syncthreads();
     }
-    store_tile_bf16<JPH>(G, t, wm, wn, lane, acc, sm);
+    store_tile_bf16<JPH, MB>(G, t, wm, wn, lane, acc, sm);
 }
 
 }  // namespace
 
 int64_t transform_row_tiles(int64_t rows) { return (rows + BM - 1) / BM; }
 
+constexpr int kBf16Rows = 128;   // rows per bf16 block tile (256 measured no faster)
+
 template <int JPH>
 void launch_gemm(const GemmArgs &G, bool bf, unsigned blocks, hipStream_t st) {
     // the device message table: split planes at F = 256, fp32 rows below
-    if (bf) gemm_bf16<JPH><<<blocks, 256, 0, st>>>(G);
+    if (bf) gemm_bf16<JPH, kBf16Rows><<<blocks, 2 * kBf16Rows, 0, st>>>(G);
     else if (G.F >= 256) {
         if (G.prep.elu) gemm_f32s<JPH, true, true><<<blocks, 256, 0, st>>>(G);
         else gemm_f32s<JPH, false, true><<<blocks, 256, 0, st>>>(G);
@@ -597,8 +610,11 @@ void launch_gemm(const GemmArgs &G, bool bf, unsigned blocks, hipStream_t st) {
     }
 }
 
-void launch_transform(const GemmArgs &G, bool bf, hipStream_t st) {
-    const int64_t tiles1 = transform_row_tiles(G.side[1].rows);
+void launch_transform(const GemmArgs &G0, bool bf, hipStream_t st) {
+    GemmArgs G = G0;
+    const int64_t bm = bf ? kBf16Rows : BM;   // rows per block tile
+    G.tiles0 = (G.side[0].rows + bm - 1) / bm;
+    const int64_t tiles1 = (G.side[1].rows + bm - 1) / bm;
     const unsigned blocks = (unsigned)((G.tiles0 + tiles1) * (2 * G.F / BN));
     switch (G.prep.jph) {
         case 1: launch_gemm<1>(G, bf, blocks, st); break;
