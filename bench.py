@@ -140,11 +140,12 @@ def algorithmic_work(stage: str, wl, topo, R: int, info, n_slices: int, n_query:
     N, M, F, K = topo.n_op, topo.n_dev, wl.f, wl.heads
     s = 2 if wl.dtype == "bf16" else 4            # storage of W^h h and hidden rows
     tiles = (N + 63) // 64
-    tpg = 1 if tiles <= 16 else -(-tiles // 16)    # op tiles per device<-op block
+    tpg = 1 if tiles <= 8 else -(-tiles // 8)      # op tiles per device<-op block (at most 8 groups)
     groups = -(-tiles // tpg)
     rec = R * M * groups * (F + 2 * K) * 4         # device<-op partial records
-    # device message table (bit 0 / 1): fp32, or its three bf16 split parts
-    tbytes = R * M * F * (12 if wl.dtype == "bf16" else 8)
+    # device message table (bit 0 / 1): its three bf16 split parts (bf16, and
+    # fp32 at f = 256), else fp32 rows
+    tbytes = R * M * F * (12 if (wl.dtype == "bf16" or F >= 256) else 8)
     if stage == "transform":
         # H in, W in, Y out, plus the attention terms (4K per row) and the
         # device message table that the epilogue writes
@@ -175,6 +176,31 @@ def algorithmic_work(stage: str, wl, topo, R: int, info, n_slices: int, n_query:
               + n_query * n_slices * H * 4 + n_query * n_slices * 4)
         return float(2 * n_query * n_slices * H), float(by)
     return 0.0, 0.0
+
+
+def nearest_roof(stage: str, dtype: str, flops: float, byts: float, avg_s: float) -> dict:
+    """The roofline entry of a stage's kernel: the transform against its
+    matrix-core peak (fp32: the bf16 peak over six part products) when its
+    flop/byte ratio is above that peak's ridge, else against HBM; an
+    aggregation stage against the non-packed fp32 VALU rate when its vector
+    flops are the larger fraction of their peak, with the HBM figures beside;
+    everything else against HBM."""
+    fl_tf = flops / avg_s / 1e12
+    bw_gbs = byts / avg_s / 1e9
+    peak_fl = TRANSFORM_PEAK[dtype] if stage == "transform" else None
+    if stage == "transform" and flops / byts >= peak_fl * 1e12 / (PEAK_HBM_GBS * 1e9):
+        roof = {"bound": "mfma", "achieved": round(fl_tf, 3), "peak": round(peak_fl, 2), "unit": "TFLOP/s",
+                "frac": round(fl_tf / peak_fl, 4)}
+        if dtype == "f32":
+            roof["peak_basis"] = "bf16 dense MFMA peak / 6 part products (fp32 contraction of exact bf16 splits)"
+    elif stage.startswith("agg_") and fl_tf / PEAK_VALU_F32_TFLOPS > bw_gbs / PEAK_HBM_GBS:
+        roof = {"bound": "alu", "achieved": round(fl_tf, 3), "peak": round(PEAK_VALU_F32_TFLOPS, 2),
+                "unit": "TFLOP/s", "frac": round(fl_tf / PEAK_VALU_F32_TFLOPS, 4),
+                "hbm_gbs": round(bw_gbs, 1), "hbm_frac": round(bw_gbs / PEAK_HBM_GBS, 4)}
+    else:
+        roof = {"bound": "hbm", "achieved": round(bw_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(bw_gbs / PEAK_HBM_GBS, 4)}
+    return roof
 
 
 def cpu_model() -> str:
@@ -776,23 +802,7 @@ def main() -> int:
     T = topo.entries()
     flops, byts = algorithmic_work(stage, wl, topo, R, info, len(masks), Q)
     avg_s = kern_ms / 1e3 / max(n_launch, 1)
-    fl_tf = flops / avg_s / 1e12
-    bw_gbs = byts / avg_s / 1e9
-    peak_fl = TRANSFORM_PEAK[wl.dtype] if stage == "transform" else None
-    if stage == "transform" and flops / byts >= peak_fl * 1e12 / (PEAK_HBM_GBS * 1e9):
-        roof = {"bound": "mfma", "achieved": round(fl_tf, 3), "peak": round(peak_fl, 2), "unit": "TFLOP/s",
-                "frac": round(fl_tf / peak_fl, 4)}
-        if wl.dtype == "f32":
-            roof["peak_basis"] = "bf16 dense MFMA peak / 6 part products (fp32 contraction of exact bf16 splits)"
-    elif stage.startswith("agg_") and fl_tf / PEAK_VALU_F32_TFLOPS > bw_gbs / PEAK_HBM_GBS:
-        # the aggregation's vector arithmetic is the nearer roof: bound by the
-        # fp32 VALU (non-packed) rate
-        roof = {"bound": "alu", "achieved": round(fl_tf, 3), "peak": round(PEAK_VALU_F32_TFLOPS, 2),
-                "unit": "TFLOP/s", "frac": round(fl_tf / PEAK_VALU_F32_TFLOPS, 4),
-                "hbm_gbs": round(bw_gbs, 1), "hbm_frac": round(bw_gbs / PEAK_HBM_GBS, 4)}
-    else:
-        roof = {"bound": "hbm", "achieved": round(bw_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(bw_gbs / PEAK_HBM_GBS, 4)}
+    roof = nearest_roof(stage, wl.dtype, flops, byts, avg_s)
     roof.update({"traffic": measured_traffic(name, stage), "kernel": KERNEL_NAMES[stage], "stage": stage,
                  "avg_launch_ms": round(avg_s * 1e3, 4), "launches": n_launch,
                  "algorithmic_bytes_per_launch": byts, "algorithmic_flops_per_launch": flops})
