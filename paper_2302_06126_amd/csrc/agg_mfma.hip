@@ -349,7 +349,9 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
                                     const bool on = (prq[q] >> j) & 1ull;
                                     const unsigned bit = (unsigned)(btq[q] >> j) & 1u;
                                     const float x = fmaf(bit ? p1q[q] : p0q[q], kLog2e, q2[rb][hh]);   // raw terms
-                                    af2[e] = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
+                                    // (no link: exp2(-inf) = 0, without a branch)
+                                    const float y = fmaxf(x, slope * x) - m2[rb][hh];
+                                    af2[e] = __builtin_amdgcn_exp2f(on ? y : -INFINITY);
                                     zl[rb][hh] += af2[e];
                                     sb |= bit << (2 * q);
                                 }
@@ -732,16 +734,19 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
         const uint32_t tpart = (uint32_t)A.R * (uint32_t)A.n_dev * F * 4u;   // bytes between the three parts
         const uint32_t trow = ((uint32_t)r * (uint32_t)A.n_dev + (uint32_t)d0) * F * 4u + (cbase + (lane & 15)) * 4u;
         const int ksteps = (Mg + 31) / 32;   // <= 2: a tile group holds at most 64 devices
+        // (the part and column block go into a wave-uniform base, so that a
+        // load needs only the lane's row offset)
         auto load_b = [&](int ks, int cb, bf16x16 (&bo)[3]) {
             const int jb = 32 * ks + 4 * (lane >> 4);
+            uint32_t off[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) off[q] = trow + (uint32_t)(min(jb + (q < 4 ? q : 12 + q), Mg - 1) * F) * 4u;
 #pragma unroll
             for (int z = 0; z < 3; ++z) {
+                const char *bz = Tb + (size_t)z * tpart + cb * 64;
                 unsigned w[8];
 #pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    const int j = min(jb + (q < 4 ? q : 12 + q), Mg - 1);
-                    w[q] = *reinterpret_cast<const unsigned *>(Tb + (trow + z * tpart + (uint32_t)(j * F + cb * 16) * 4u));
-                }
+                for (int q = 0; q < 8; ++q) w[q] = *reinterpret_cast<const unsigned *>(bz + off[q]);
                 bo[z] = as_bf16x16(w);
             }
         };
@@ -804,7 +809,8 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
                                 const bool on = (on8[b2] >> q) & 1u;
                                 const bool bit = (bit8[b2] >> q) & 1u;
                                 const float x = (bit ? p1q[q] : p0q[q]) + q2[b2][hh];
-                                af2[e] = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[b2][hh]) : 0.f;
+                                const float y = fmaxf(x, slope * x) - m2[b2][hh];
+                                af2[e] = __builtin_amdgcn_exp2f(on ? y : -INFINITY);   // (no link: 0)
                                 zl[b2][hh] += af2[e];
                             }
                             unsigned sp[3];
@@ -934,7 +940,8 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
 #pragma unroll
                     for (int hh = 0; hh < HPW; ++hh) {
                         const float x = pj[hh] + q2[rb][hh];
-                        const float af = on ? __builtin_amdgcn_exp2f(fmaxf(x, slope * x) - m2[rb][hh]) : 0.f;
+                        const float y = fmaxf(x, slope * x) - m2[rb][hh];
+                        const float af = __builtin_amdgcn_exp2f(on ? y : -INFINITY);   // (no link: 0)
                         zl[rb][hh] += af;
 #pragma unroll
                         for (int c2 = 0; c2 < CPH; ++c2)

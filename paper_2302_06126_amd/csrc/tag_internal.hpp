@@ -127,7 +127,9 @@ __device__ __forceinline__ float leaky(float x, float slope) { return x > 0.f ? 
 template <bool ELU>
 __device__ __forceinline__ float msg_act(float z) {
     if constexpr (ELU) return z > 0.f ? z : __expf(z) - 1.f;
-    else return fmaxf(z, 0.f);
+    // max(z, 0) as one integer max of the bits (a set sign bit gives +0), so
+    // that no quieting of z is needed first
+    else return __int_as_float(max(__float_as_int(z), 0));
 }
 
 typedef unsigned u4v __attribute__((ext_vector_type(4)));
