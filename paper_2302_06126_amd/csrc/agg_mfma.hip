@@ -457,6 +457,11 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
     __shared__ __attribute__((aligned(16))) float Ot[kOpTile * OS];
     __shared__ uint64_t pres[kOpTile], bits[kOpTile];
     __shared__ float qo[kOpTile][K], mxS[kOpTile][K];
+    // op<-op destination terms: staged per tile row where the LDS budget
+    // allows (f = 256); smaller f keeps the group's four rows in registers
+    // (four blocks per CU at f = 128 leave no room for the array)
+    constexpr bool kQL = F >= 256;
+    __shared__ float qoo[kQL ? kOpTile : 1][kQL ? K : 1];
     // op<-op per-channel constants (a log2 e, U_0, c') staged once per block
     // where the LDS budget allows (f = 256); smaller f loads them per lane
     constexpr bool kCS = F >= 256;
@@ -483,14 +488,15 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
     const int cbase = wave * WC;
     const int h0 = cbase / D;
 
-    // op<-op terms of this lane: its channels c0 .. c0+CPL-1 of the group's
-    // four rows (loaded with the prologue so their latency overlaps it)
+    // this lane's op<-op channels c0 .. c0+CPL-1 of the group's four rows
     const int c0 = (lane & 15) * CPL;
     const int gr0 = wave * 16 + (lane >> 4) * 4;   // the group's first tile row
-    float qv3[4];                                  // op<-op destination terms of the group's rows
+    float qv[4];                                   // (kQL false) the group's op<-op destination terms
+    if constexpr (!kQL) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-        qv3[i] = gr0 + i < nu ? Sop[(int64_t)(u0 + gr0 + i) * 4 * K + 3 * K + c0 / D] : 0.f;
+        for (int i = 0; i < 4; ++i)
+            qv[i] = gr0 + i < nu ? Sop[(int64_t)(u0 + gr0 + i) * 4 * K + 3 * K + c0 / D] : 0.f;
+    }
     float a[CPL], u0c[CPL], cpc[CPL];
     static_assert(!kCS || F == 256, "one staged constant per thread");
     float ca3[3];
@@ -509,7 +515,7 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
         constexpr int NQ = (kOpTile * K + 255) / 256, NP = (64 * 2 * K + 255) / 256, NE = (ECAP + 255) / 256;
         int32_t rp0 = 0, rp1 = 0;
         uint64_t om0 = 0, om1 = 0;
-        float q2v[NQ], pv[NP], exv[NE];
+        float q2v[NQ], q3v[NQ], pv[NP], exv[NE];
         int32_t ecv[NE];
         if (tid <= nu) rp0 = A.rp[0][u0 + tid] - eb;
         if (tid < nu) rp1 = A.rp[0][u0 + tid + 1] - eb;
@@ -522,7 +528,8 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
         for (int k = 0; k < NQ; ++k) {
             const int i = tid + 256 * k, u = i / K, h = i % K;
             const bool ok = i < kOpTile * K && u < nu;
-            q2v[k] = ok ? Sop[(int64_t)(u0 + u) * 4 * K + 2 * K + h] : 0.f;
+            q2v[k] = ok ? Sop[(int64_t)(u0 + u) * 4 * K + 2 * K + h] : 0.f;   // op <- device
+            q3v[k] = kQL && ok ? Sop[(int64_t)(u0 + u) * 4 * K + 3 * K + h] : 0.f;   // op <- op
         }
 #pragma unroll
         for (int k = 0; k < NP; ++k) {
@@ -540,7 +547,10 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
 #pragma unroll
         for (int k = 0; k < NQ; ++k) {
             const int i = tid + 256 * k;
-            if (i < kOpTile * K) qo[i / K][i % K] = q2v[k] * kLog2e;
+            if (i < kOpTile * K) {
+                qo[i / K][i % K] = q2v[k] * kLog2e;
+                if constexpr (kQL) qoo[i / K][i % K] = q3v[k] * kLog2e;
+            }
         }
 #pragma unroll
         for (int k = 0; k < NP; ++k) {
@@ -606,9 +616,10 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
         }
         // the group's entries (rows >= nu are empty)
         const int32_t ebeg = Erp[min(gr0, nu)], eend = Erp[min(gr0 + 4, nu)];
-        float qv[4];                  // op<-op destination terms of the group's rows (exp2 domain)
+        if constexpr (!kQL) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) qv[i] = qv3[i] * kLog2e;
+            for (int i = 0; i < 4; ++i) qv[i] *= kLog2e;
+        }
 #pragma unroll
         for (int i = 0; i < 4; ++i)
             if (gr0 + i < nu)
@@ -649,7 +660,7 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
             auto fetch = [&](RowRaw<CPL, BF> &sl, float &xv, int &rl, int32_t le) {
                 const int32_t lc = min(le, hm);
                 const int2 cx = Ecx[lc];
-                rl = (int)Erw[lc] - gr0;              // meaningful only for le < hi
+                rl = (int)Erw[lc];                    // past hi: the row of the group's last entry
                 xv = __int_as_float(cx.y);
                 const int32_t v = le < hi ? cx.x : u0;
                 sl.load32(Yc, ((uint32_t)v * (2 * F) + c0) * (BF ? 2u : 4u));
@@ -664,33 +675,38 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
                     m[c] = msg_act<ELU>(z);
                     part = fmaf(a[c], m[c], part);
                 }
-                const float qa = (rl & 1) ? qv[1] : qv[0], qb = (rl & 1) ? qv[3] : qv[2];
-                const float sv = row_sum<LPH>(part) + ((rl & 2) ? qb : qa);
-                const float s2 = fmaxf(sv, slope * sv);
-                if (e < hi) {
-                    const int rowe = gr0 + rl;
-                    if (rowe != ri) {   // first entry of row rowe: finish row ri
-                        if (ri >= 0) finish();
-                        ri = rowe;
-                        mref = s2;
-                        den = 0.f;
-#pragma unroll
-                        for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
-                    }
-                    float d = s2 - mref;
-                    if (d > 64.f) {   // keep the weights finite: move the reference up
-                        const float sc = __builtin_amdgcn_exp2f(-d);
-                        den *= sc;
-#pragma unroll
-                        for (int c = 0; c < CPL; ++c) acc[c] *= sc;
-                        mref = s2;
-                        d = 0.f;
-                    }
-                    const float p = __builtin_amdgcn_exp2f(d);
-                    den += p;
-#pragma unroll
-                    for (int c = 0; c < CPL; ++c) acc[c] = fmaf(p, m[c], acc[c]);
+                float qd;   // the destination term of row rl
+                if constexpr (kQL) qd = qoo[rl][hd];
+                else {
+                    const int i = rl - gr0;
+                    const float qa = (i & 1) ? qv[1] : qv[0], qb = (i & 1) ? qv[3] : qv[2];
+                    qd = (i & 2) ? qb : qa;
                 }
+                const float sv = row_sum<LPH>(part) + qd;
+                // a slot past hi gets weight exp2(-inf) = 0 (its row is the one
+                // in progress, so it neither starts nor finishes a row)
+                const float s2 = fmaxf(sv, slope * sv) + (e < hi ? 0.f : -INFINITY);
+                if (rl != ri) {   // first entry of row rl: finish row ri
+                    if (ri >= 0) finish();
+                    ri = rl;
+                    mref = s2;
+                    den = 0.f;
+#pragma unroll
+                    for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
+                }
+                float d = s2 - mref;
+                if (d > 64.f) {   // keep the weights finite: move the reference up
+                    const float sc = __builtin_amdgcn_exp2f(-d);
+                    den *= sc;
+#pragma unroll
+                    for (int c = 0; c < CPL; ++c) acc[c] *= sc;
+                    mref = s2;
+                    d = 0.f;
+                }
+                const float p = __builtin_amdgcn_exp2f(d);
+                den += p;
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) acc[c] = fmaf(p, m[c], acc[c]);
             };
 #pragma unroll
             for (int s = 0; s < HB; ++s) fetch(sa[s], xa[s], la[s], lo + s);
