@@ -652,7 +652,8 @@ __global__ void __launch_bounds__(256, (F >= 256 && K >= 8) ? 1 : 2) agg_op_tile
             // two halves of EB / 2 row slots: while one half is consumed the
             // other half's rows are in flight; a half is refilled as a whole
             // right after it has been consumed (past hi a slot is refilled
-            // with the tile's first row, never consumed)
+            // with the tile's first row under the group's last entry's tile
+            // row; the last loop round consumes such slots at weight 0)
             constexpr int HB = EB / 2;
             RowRaw<CPL, BF> sa[HB], sb[HB];
             float xa[HB], xb[HB];
