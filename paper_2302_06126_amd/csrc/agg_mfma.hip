@@ -346,8 +346,11 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
 #pragma unroll
                                 for (int e = 0; e < 2; ++e) {
                                     const int q = 2 * pr + e;
-                                    const bool on = (prq[q] >> j) & 1ull;
-                                    const unsigned bit = (unsigned)(btq[q] >> j) & 1u;
+                                    // (device j's flags sit in the low mask word for rb < 2)
+                                    const uint32_t pw = (uint32_t)(rb < 2 ? prq[q] : prq[q] >> 32);
+                                    const uint32_t bw = (uint32_t)(rb < 2 ? btq[q] : btq[q] >> 32);
+                                    const bool on = (pw >> (j & 31)) & 1u;
+                                    const unsigned bit = (bw >> (j & 31)) & 1u;
                                     const float x = fmaf(bit ? p1q[q] : p0q[q], kLog2e, q2[rb][hh]);   // raw terms
                                     // (no link: exp2(-inf) = 0, without a branch)
                                     const float y = fmaxf(x, slope * x) - m2[rb][hh];
