@@ -321,9 +321,11 @@ __global__ void __launch_bounds__(256) agg_b2(AggArgs A) {
                 uint64_t prq[8], btq[8];
 #pragma unroll
                 for (int q = 0; q < 8; ++q) {
-                    const bool live = ua + q < nu;   // rows past the tile hold another op's masks
-                    prq[q] = live ? mkc[ua + q][0] : 0ull;
-                    btq[q] = live ? mkc[ua + q][1] : 0ull;
+                    // rows past the tile hold another op's masks: their presence
+                    // is cleared (the loads stay unconditional: ua + q < 64)
+                    const uint64_t p = mkc[ua + q][0], b = mkc[ua + q][1];
+                    prq[q] = ua + q < nu ? p : 0ull;
+                    btq[q] = b;
                 }
 #pragma unroll
                 for (int hh = 0; hh < HPW; ++hh) {
